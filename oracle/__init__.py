@@ -1,0 +1,179 @@
+"""ORACLE -- test infrastructure only.
+
+Only the test suite, the smoke check and the benchmark's CPU-baseline leg may import this
+package.  The GPU library and its Python binding never import, link or call it, and it shares
+no code with them.  It wraps ``liborc.so`` (built from ``alp_oracle.c`` by :func:`build`) with
+ctypes and adds a slow pure-Python statement of the same definitions for tiny cases
+(:mod:`oracle.pyref`).
+
+Functions take a batch dictionary as produced by :mod:`workloads` and an instance number.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liborc.so")
+U64_NONE = (1 << 64) - 1
+
+
+def build() -> str:
+    """Compile ``liborc.so`` with gcc (always rebuilds)."""
+    src = os.path.join(_HERE, "alp_oracle.c")
+    tmp = LIB_PATH + ".tmp"
+    subprocess.run(["gcc", "-std=c11", "-O2", "-Wall", "-Wextra", "-shared", "-fPIC", src, "-o", tmp],
+                   check=True)
+    os.replace(tmp, LIB_PATH)
+    return LIB_PATH
+
+
+class _Inst(C.Structure):
+    _fields_ = [("M", C.c_uint32), ("n_tp", C.c_uint32), ("n_fq", C.c_uint32), ("D", C.c_uint32),
+                ("K", C.c_uint32), ("Q", C.c_uint32),
+                ("tp", C.c_void_p), ("fq", C.c_void_p), ("W", C.c_void_p), ("n", C.c_void_p),
+                ("p", C.c_void_p), ("allowed", C.c_void_p), ("rate", C.c_void_p),
+                ("lat", C.c_void_p), ("H", C.c_uint64)]
+
+
+class _Term(C.Structure):
+    _fields_ = [("ok", C.c_uint32), ("thr_ok", C.c_uint32), ("c", C.c_uint64), ("u", C.c_uint64),
+                ("tau", C.c_uint64)]
+
+
+class _Eval(C.Structure):
+    _fields_ = [("flags", C.c_uint32), ("L", C.c_uint64), ("T", C.c_uint64), ("U", C.c_uint64)]
+
+
+class _Argmin(C.Structure):
+    _fields_ = [("best_x", C.c_uint64), ("best_L", C.c_uint64), ("n_feasible", C.c_uint64),
+                ("sum_L", C.c_uint64)]
+
+
+EVAL_DTYPE = np.dtype([("flags", np.uint32), ("L", np.uint64), ("T", np.uint64), ("U", np.uint64)],
+                      align=True)
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            build()
+        L = C.CDLL(LIB_PATH)
+        P = C.POINTER
+        L.orc_num_options.argtypes = [P(_Inst)]
+        L.orc_num_options.restype = C.c_uint32
+        L.orc_option_term.argtypes = [P(_Inst), C.c_uint32, C.c_uint32, C.c_uint32, P(_Term)]
+        L.orc_eval.argtypes = [P(_Inst), C.c_uint32, C.c_uint32, C.c_uint64, P(_Eval)]
+        L.orc_eval_many.argtypes = [P(_Inst), C.c_uint32, C.c_uint32, C.c_void_p, C.c_uint64,
+                                    C.c_void_p]
+        L.orc_argmin.argtypes = [P(_Inst), C.c_uint32, C.c_uint32, C.c_uint64, C.c_uint64,
+                                 C.c_void_p, P(_Argmin)]
+        L.orc_tmax_brute.argtypes = [P(_Inst), C.c_uint32, C.c_uint64, C.c_uint64,
+                                     P(C.c_uint64)]
+        L.orc_tmax_threshold.argtypes = [P(_Inst), C.c_uint32, C.c_void_p, P(C.c_uint64)]
+        for f in (L.orc_option_term, L.orc_eval, L.orc_eval_many, L.orc_argmin, L.orc_tmax_brute,
+                  L.orc_tmax_threshold):
+            f.restype = C.c_int
+        _lib = L
+    return _lib
+
+
+class Instance:
+    """Keeps the numpy arrays of one instance alive and exposes them as an ``orc_instance``."""
+
+    def __init__(self, batch: dict, i: int = 0):
+        sp = batch["space"]
+        self.arrays = {
+            "tp": np.ascontiguousarray(sp["tp"], dtype=np.uint32),
+            "fq": np.ascontiguousarray(sp["fq"], dtype=np.uint32),
+            "W": np.ascontiguousarray(batch["W"][i], dtype=np.uint64),
+            "n": np.ascontiguousarray(batch["n"][i], dtype=np.uint32),
+            "p": np.ascontiguousarray(batch["p"][i], dtype=np.uint32),
+            "allowed": np.ascontiguousarray(batch["allowed"][i], dtype=np.uint8),
+            "rate": np.ascontiguousarray(batch["rate"][i], dtype=np.uint32),
+            "lat": np.ascontiguousarray(batch["lat"][i], dtype=np.uint32),
+        }
+        a = self.arrays
+        self.M, self.K = int(sp["M"]), int(sp["K"])
+        self.O = len(a["tp"]) * len(a["fq"]) * int(sp["D"])
+        self.N = self.O ** self.M
+        self.G = int(batch["G"][i])
+        self.u_ppm = int(batch["u_ppm"][i])
+        self.c = _Inst(self.M, len(a["tp"]), len(a["fq"]), int(sp["D"]), self.K, int(sp["Q"]),
+                       *(a[k].ctypes.data for k in ("tp", "fq", "W", "n", "p", "allowed", "rate",
+                                                     "lat")),
+                       int(batch["H"]))
+        self._scratch = (_Term * (self.M * self.O))()
+
+
+def option_term(inst: Instance, m: int, o: int, lam: int) -> dict:
+    t = _Term()
+    if lib().orc_option_term(C.byref(inst.c), m, o, lam, C.byref(t)) != 0:
+        raise ValueError("option out of range")
+    return {"ok": int(t.ok), "thr_ok": int(t.thr_ok), "c": int(t.c), "u": int(t.u),
+            "tau": int(t.tau)}
+
+
+def option_terms(inst: Instance, lam: int) -> list:
+    """[m][o] -> term dictionaries."""
+    return [[option_term(inst, m, o, lam) for o in range(inst.O)] for m in range(inst.M)]
+
+
+def evaluate(inst: Instance, G: int, lam: int, x: int) -> dict:
+    e = _Eval()
+    if lib().orc_eval(C.byref(inst.c), G, lam, x, C.byref(e)) != 0:
+        raise ValueError("candidate index out of range")
+    return {"flags": int(e.flags), "L": int(e.L), "T": int(e.T), "U": int(e.U)}
+
+
+def evaluate_many(inst: Instance, G: int, lam: int, xs: np.ndarray) -> np.ndarray:
+    xs = np.ascontiguousarray(xs, dtype=np.uint64)
+    out = np.zeros(len(xs), dtype=EVAL_DTYPE)
+    assert EVAL_DTYPE.itemsize == C.sizeof(_Eval)
+    if lib().orc_eval_many(C.byref(inst.c), G, lam, xs.ctypes.data, len(xs), out.ctypes.data) != 0:
+        raise ValueError("candidate index out of range")
+    return out
+
+
+def argmin(inst: Instance, G: int, lam: int, lo: int = 0, hi: int | None = None) -> dict:
+    hi = inst.N if hi is None else hi
+    if not (0 <= lo <= hi <= inst.N):
+        raise ValueError("range outside the candidate space")
+    r = _Argmin()
+    if lib().orc_argmin(C.byref(inst.c), G, lam, lo, hi, inst._scratch, C.byref(r)) != 0:
+        raise ValueError("bad instance")
+    return {"x": None if r.best_x == U64_NONE else int(r.best_x),
+            "L": None if r.best_x == U64_NONE else int(r.best_L),
+            "n_feasible": int(r.n_feasible), "sum_L": int(r.sum_L)}
+
+
+def tmax_brute(inst: Instance, G: int, lo: int = 0, hi: int | None = None) -> int:
+    hi = inst.N if hi is None else hi
+    out = C.c_uint64()
+    if lib().orc_tmax_brute(C.byref(inst.c), G, lo, hi, C.byref(out)) != 0:
+        raise ValueError("bad range")
+    return int(out.value)
+
+
+def tmax(inst: Instance, G: int) -> int:
+    """Largest T_w reachable within budget G (threshold method)."""
+    out = C.c_uint64()
+    lib().orc_tmax_threshold(C.byref(inst.c), G, inst._scratch, C.byref(out))
+    return int(out.value)
+
+
+def merge_argmin(parts: list) -> dict:
+    """Merges argmin results of disjoint index slices (lexicographic (L, x) minimum)."""
+    best = {"x": None, "L": None, "n_feasible": 0, "sum_L": 0}
+    for r in parts:
+        best["n_feasible"] += r["n_feasible"]
+        best["sum_L"] = (best["sum_L"] + r["sum_L"]) % (1 << 64)
+        if r["x"] is not None and (best["x"] is None or (r["L"], r["x"]) < (best["L"], best["x"])):
+            best["x"], best["L"] = r["x"], r["L"]
+    return best

@@ -1,0 +1,269 @@
+/*
+ * alp_oracle.c -- ORACLE.  Test infrastructure only: the test suite, the smoke check and the
+ * CPU-baseline leg of the benchmark load this library; the GPU library never includes, links
+ * or calls anything here, and nothing here is shared with it.
+ *
+ * A plain, slow, single-threaded statement of the Aggregate LLM Pipeline (ALP) allocation
+ * search of "Scepsy" (arXiv 2604.15186):
+ *   - per LLM m and per-LLM option (tp, GPU share q, replicas d), the workflow-level latency
+ *     contribution L_m(lambda * n_m / d) * n_m / p_m of Eq. 1 (Section 4, step 4 and step 5,
+ *     replicas divide the per-replica arrival rate) and the workflow-normalised maximum
+ *     throughput d * T_m / n_m of Eq. 2 (throughput scales linearly with replicas, Section 4,
+ *     step 3);
+ *   - per candidate allocation (one option per LLM), L_w = sum of the contributions (Eq. 1),
+ *     T_w = minimum of the normalised throughputs (Eq. 2), and the feasibility conditions:
+ *     every LLM's option deployable and its weights fit in its GPU share (Section 5, step 1,
+ *     minimum fractions that hold the parameters), the target rate is sustained (T_w >= lambda,
+ *     Section 3 "lowest latency within a target workflow-level arrival rate"), and the GPU
+ *     budget is respected;
+ *   - the search result: the feasible candidate of lowest L_w, ties broken by lowest index.
+ *
+ * Fixed-point readings (the paper computes in reals):
+ *   rates in milli-requests/s, latencies in microseconds, n_m and p_m in milli-units;
+ *   the per-replica LLM rate is rounded up, the interpolated latency, the latency contribution
+ *   and the normalised throughput are rounded down; between profiled points latency is linear
+ *   in the rate, below the first point it is flat, above the last (saturation) point the option
+ *   cannot sustain the load.  GPU shares are counted in units of 1/Q GPU; the budget is
+ *   sum(tp * q * d) <= Q * G.  The memory fit is W_m * Q <= tp * q * H (weights sharded over tp
+ *   must fit the share q/Q of H bytes).
+ *
+ * Candidate numbering: option o = (i * |FQ| + j) * D + (d - 1) for tp = tp[i], q = fq[j]
+ * (replicas vary fastest); candidate x = sum_m o_m * O^(M-1-m) (LLM 0 most significant).
+ *
+ * Arithmetic is 64-bit unsigned throughout; inputs are assumed to satisfy the documented ranges
+ * (values below 2^31, weights and HBM size below 2^48), which keep every product below 2^63.
+ */
+#include <stdint.h>
+#include <stddef.h>
+
+#define ORC_U64_NONE UINT64_MAX
+
+typedef struct {
+    uint32_t M;                 /* LLMs in the workflow */
+    uint32_t n_tp;              /* number of tensor-parallel degrees */
+    uint32_t n_fq;              /* number of GPU-share choices */
+    uint32_t D;                 /* replica counts 1..D */
+    uint32_t K;                 /* profile points per (tp, share) */
+    uint32_t Q;                 /* share units per GPU */
+    const uint32_t *tp;         /* [n_tp] */
+    const uint32_t *fq;         /* [n_fq] share in units of 1/Q */
+    const uint64_t *W;          /* [M] weight bytes */
+    const uint32_t *n;          /* [M] invocations per workflow request (milli) */
+    const uint32_t *p;          /* [M] request-level parallelism (milli) */
+    const uint8_t *allowed;     /* [M][n_tp][n_fq] */
+    const uint32_t *rate;       /* [M][n_tp][n_fq][K] milli-req/s, strictly ascending in k */
+    const uint32_t *lat;        /* [M][n_tp][n_fq][K] microseconds */
+    uint64_t H;                 /* HBM bytes per GPU */
+} orc_instance;
+
+typedef struct {
+    uint32_t ok;        /* deployable and weights fit the share */
+    uint32_t thr_ok;    /* the per-replica load does not exceed saturation */
+    uint64_t c;         /* latency contribution, microseconds (valid iff thr_ok) */
+    uint64_t u;         /* GPU share units used: tp * q * d */
+    uint64_t tau;       /* workflow-normalised max throughput, milli-req/s */
+} orc_term;
+
+typedef struct {
+    uint32_t flags;     /* bit0: every option ok; bit1: every option thr_ok; bit2: budget ok */
+    uint64_t L;         /* L_w, defined iff bit0 and bit1, else ORC_U64_NONE */
+    uint64_t T;         /* T_w, defined iff bit0, else 0 */
+    uint64_t U;         /* sum of share units */
+} orc_eval_out;
+
+typedef struct {
+    uint64_t best_x;        /* ORC_U64_NONE if no feasible candidate in the range */
+    uint64_t best_L;
+    uint64_t n_feasible;
+    uint64_t sum_L;         /* sum of L_w over feasible candidates, modulo 2^64 */
+} orc_argmin_out;
+
+uint32_t orc_num_options(const orc_instance *s) { return s->n_tp * s->n_fq * s->D; }
+
+/* Linear interpolation of one profiled latency curve at per-replica rate r (milli-req/s).
+ * Called only when r <= rate[K-1].  Below the first point the curve is flat. */
+static uint64_t orc_latency_at(const uint32_t *rate, const uint32_t *lat, uint32_t K, uint64_t r)
+{
+    if (r <= rate[0])
+        return lat[0];
+    for (uint32_t k = 1; k < K; ++k) {
+        if (r <= rate[k]) {
+            uint64_t r0 = rate[k - 1], r1 = rate[k];
+            uint64_t num = (uint64_t)lat[k - 1] * (r1 - r) + (uint64_t)lat[k] * (r - r0);
+            return num / (r1 - r0);
+        }
+    }
+    return lat[K - 1]; /* not reached when r <= rate[K-1] */
+}
+
+/* Per-LLM, per-option ALP terms at workflow rate lambda (Eq. 1 and Eq. 2 terms; Section 4,
+ * step 5, the load of one of d replicas is lambda * n_m / d; Section 5 step 1, memory bound). */
+int orc_option_term(const orc_instance *s, uint32_t m, uint32_t o, uint32_t lambda, orc_term *out)
+{
+    if (m >= s->M || o >= orc_num_options(s))
+        return -1;
+    uint32_t d = o % s->D + 1;
+    uint32_t ij = o / s->D;
+    uint32_t j = ij % s->n_fq;
+    uint32_t i = ij / s->n_fq;
+    uint64_t tp = s->tp[i], q = s->fq[j];
+    size_t tab = ((size_t)m * s->n_tp + i) * s->n_fq + j;
+    const uint32_t *rate = s->rate + tab * s->K;
+    const uint32_t *lat = s->lat + tab * s->K;
+    uint64_t n = s->n[m], p = s->p[m];
+
+    out->ok = s->allowed[tab] && (s->W[m] * (uint64_t)s->Q <= tp * q * s->H);
+    uint64_t T = rate[s->K - 1];                                   /* saturation throughput */
+    uint64_t tau = 1000ull * d * T / n;                            /* d * T_m / n_m (Eq. 2) */
+    out->tau = tau > 0xFFFFFFFFull ? 0xFFFFFFFFull : tau;
+    uint64_t r = ((uint64_t)lambda * n + 1000ull * d - 1) / (1000ull * d); /* ceil(lambda n / d) */
+    out->thr_ok = (r <= T);
+    out->c = 0;
+    if (out->thr_ok) {
+        uint64_t ell = orc_latency_at(rate, lat, s->K, r);        /* L_m at the replica's load */
+        out->c = ell * n / p;                                      /* times n_m / p_m (Eq. 1) */
+    }
+    out->u = tp * q * d;
+    return 0;
+}
+
+/* Evaluates one candidate from the raw tables (no precomputation). */
+int orc_eval(const orc_instance *s, uint32_t G, uint32_t lambda, uint64_t x, orc_eval_out *out)
+{
+    uint32_t O = orc_num_options(s);
+    uint32_t digit[16];
+    if (s->M == 0 || s->M > 16)
+        return -1;
+    for (uint32_t k = 0; k < s->M; ++k) {                         /* LLM M-1 is the last digit */
+        uint32_t m = s->M - 1 - k;
+        digit[m] = (uint32_t)(x % O);
+        x /= O;
+    }
+    if (x != 0)
+        return -1;                                                 /* index out of range */
+    int all_ok = 1, all_thr = 1;
+    uint64_t L = 0, T = ORC_U64_NONE, U = 0;
+    for (uint32_t m = 0; m < s->M; ++m) {
+        orc_term t;
+        orc_option_term(s, m, digit[m], lambda, &t);
+        all_ok &= (int)t.ok;
+        all_thr &= (int)t.thr_ok;
+        L += t.c;
+        if (t.tau < T)
+            T = t.tau;
+        U += t.u;
+    }
+    int budget_ok = U <= (uint64_t)s->Q * G;
+    out->flags = (uint32_t)all_ok | ((uint32_t)all_thr << 1) | ((uint32_t)budget_ok << 2);
+    out->L = (all_ok && all_thr) ? L : ORC_U64_NONE;
+    out->T = all_ok ? T : 0;
+    out->U = U;
+    return 0;
+}
+
+int orc_eval_many(const orc_instance *s, uint32_t G, uint32_t lambda, const uint64_t *x,
+                  uint64_t count, orc_eval_out *out)
+{
+    for (uint64_t i = 0; i < count; ++i)
+        if (orc_eval(s, G, lambda, x[i], &out[i]) != 0)
+            return -1;
+    return 0;
+}
+
+/* Exhaustive argmin over candidates [lo, hi): the feasible candidate of lowest L_w, lowest
+ * index among ties (scanning in increasing index order, only a strictly lower L_w replaces the
+ * current best).  The per-option terms do not depend on the candidate, so they are computed
+ * once per (m, o) and looked up; every candidate is then combined by Eq. 1, Eq. 2 and the
+ * budget exactly as orc_eval does. */
+int orc_argmin(const orc_instance *s, uint32_t G, uint32_t lambda, uint64_t lo, uint64_t hi,
+               orc_term *scratch /* [M * O] */, orc_argmin_out *out)
+{
+    uint32_t O = orc_num_options(s);
+    if (s->M == 0 || s->M > 16)
+        return -1;
+    for (uint32_t m = 0; m < s->M; ++m)
+        for (uint32_t o = 0; o < O; ++o)
+            orc_option_term(s, m, o, lambda, &scratch[(size_t)m * O + o]);
+    uint64_t capacity = (uint64_t)s->Q * G;
+    out->best_x = ORC_U64_NONE;
+    out->best_L = ORC_U64_NONE;
+    out->n_feasible = 0;
+    out->sum_L = 0;
+    for (uint64_t x = lo; x < hi; ++x) {
+        uint64_t rest = x, L = 0, U = 0;
+        int feasible = 1;
+        for (uint32_t k = 0; k < s->M; ++k) {
+            uint32_t m = s->M - 1 - k;
+            const orc_term *t = &scratch[(size_t)m * O + rest % O];
+            rest /= O;
+            feasible &= (int)(t->ok && t->thr_ok);
+            L += t->c;
+            U += t->u;
+        }
+        if (!feasible || U > capacity)
+            continue;
+        out->n_feasible += 1;
+        out->sum_L += L;
+        if (L < out->best_L) {
+            out->best_L = L;
+            out->best_x = x;
+        }
+    }
+    return 0;
+}
+
+/* Largest workflow throughput any candidate reaches within the budget, ignoring the target:
+ * max over candidates with every option ok and sum(u) <= Q*G of T_w (Eq. 2); 0 if none.
+ * Brute force over [lo, hi). */
+int orc_tmax_brute(const orc_instance *s, uint32_t G, uint64_t lo, uint64_t hi, uint64_t *out)
+{
+    uint64_t best = 0;
+    for (uint64_t x = lo; x < hi; ++x) {
+        orc_eval_out e;
+        if (orc_eval(s, G, 0, x, &e) != 0)
+            return -1;
+        if ((e.flags & 1u) && (e.flags & 4u) && e.T > best)
+            best = e.T;
+    }
+    *out = best;
+    return 0;
+}
+
+/* The same maximum by thresholds: T_w(x) >= t holds iff every LLM's option has normalised
+ * throughput >= t, so t is reachable within the budget iff the cheapest such options of all
+ * LLMs together fit in Q*G.  Reachability only shrinks as t grows, and the maximum is one of
+ * the options' own throughputs; try each. */
+int orc_tmax_threshold(const orc_instance *s, uint32_t G, orc_term *scratch /* [M * O] */,
+                       uint64_t *out)
+{
+    uint32_t O = orc_num_options(s);
+    for (uint32_t m = 0; m < s->M; ++m)
+        for (uint32_t o = 0; o < O; ++o)
+            orc_option_term(s, m, o, 0, &scratch[(size_t)m * O + o]);
+    uint64_t capacity = (uint64_t)s->Q * G, best = 0;
+    for (size_t a = 0; a < (size_t)s->M * O; ++a) {
+        if (!scratch[a].ok)
+            continue;
+        uint64_t t = scratch[a].tau;
+        if (t <= best)
+            continue;
+        uint64_t need = 0;
+        int reachable = 1;
+        for (uint32_t m = 0; m < s->M && reachable; ++m) {
+            uint64_t cheapest = ORC_U64_NONE;
+            for (uint32_t o = 0; o < O; ++o) {
+                const orc_term *e = &scratch[(size_t)m * O + o];
+                if (e->ok && e->tau >= t && e->u < cheapest)
+                    cheapest = e->u;
+            }
+            if (cheapest == ORC_U64_NONE)
+                reachable = 0;
+            else
+                need += cheapest;
+        }
+        if (reachable && need <= capacity)
+            best = t;
+    }
+    *out = best;
+    return 0;
+}
