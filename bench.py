@@ -1,0 +1,168 @@
+"""Benchmark of the ALP allocation search on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload cfg3] [--no-cpu-baseline]
+
+One step = one complete search (alp_search: per-option terms, exhaustive scan of every
+candidate, final reduction and result decode, result copied to the host) over the synthetic
+workload.  The default workload is the 5-LLM space with G = 64 GPUs and 128 options per LLM
+(2^35 = 34,359,738,368 candidates per step).  Inputs are resident in HBM before timing starts.
+Prints one JSON line.
+
+``value`` = candidates evaluated per second.  ``roofline`` relates the scan kernel (the dominant
+kernel) to the integer VALU peak of the chip: 2 int32 lane operations per candidate (the budget
+comparison and the objective minimum update), 256 CUs x 64 lanes x 2.4 GHz = 39.32 Tlane-op/s;
+the kernel duration is measured with HIP events on the stream the library launches on.
+``cpu_baseline`` times the CPU oracle, single-threaded, on a bounded slice of the same space.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from workloads import CONFIGS, make_batch, target_from_tmax  # noqa: E402
+
+PEAK_LANE_OPS = 256 * 64 * 2.4e9        # int32 VALU lane-ops/s of MI355X
+OPS_PER_CANDIDATE = 2                   # budget compare + objective min
+WORKLOADS = {"cfg2": 2, "cfg3": 3, "cfg4": 4, "cfg1": 1}
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "scan_traffic.json")
+
+
+def _traffic(kernel_digest: str, workload: str):
+    """HBM bytes per scan launch from the committed rocprofv3 counter summary, if it was taken
+    on the current kernel source and this workload."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    entry = t.get(workload)
+    if not entry or entry.get("kernel_source_sha256") != kernel_digest:
+        return None
+    return entry.get("bytes_per_launch")
+
+
+def _kernel_digest() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    with open(os.path.join(ROOT, "paper_2604_15186_amd", "csrc", "alp_kernels.hip"), "rb") as f:
+        h.update(f.read())
+    return h.hexdigest()
+
+
+def cpu_baseline(batch, G, lam, seconds: float):
+    """Single-threaded oracle argmin over the first indices of instance 0, sized to ~seconds."""
+    import oracle
+    inst = oracle.Instance(batch, 0)
+    n = 1 << 20
+    t0 = time.perf_counter()
+    oracle.argmin(inst, G, lam, 0, n)
+    dt = time.perf_counter() - t0
+    total = min(inst.N, max(n, int(n * seconds / max(dt, 1e-6))))
+    t0 = time.perf_counter()
+    oracle.argmin(inst, G, lam, 0, total)
+    dt = time.perf_counter() - t0
+    return {"value": total / dt, "unit": "candidates/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {total:,} candidate indices of the same instance, exhaustive "
+                      f"single-threaded C oracle ({dt:.1f} s)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="cfg3", choices=sorted(WORKLOADS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--variant", type=int, default=0)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the search runs on a single MI355X; "
+              "multi-GPU sharding is not built (run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2604_15186_amd import alp
+
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    cfg_id = WORKLOADS[args.workload]
+    cfg = CONFIGS[cfg_id]
+    insts = list(range(cfg.num_instances)) if cfg_id == 4 else [0]
+    batch = make_batch(cfg_id, insts)
+    ctx = alp.Context(batch)
+    ctx.set_launch(args.variant)
+    G = batch["G"]
+    tmax = ctx.max_throughput(G)
+    lam = np.asarray([target_from_tmax(int(batch["u_ppm"][i]), int(tmax[i]))
+                      for i in range(len(insts))], dtype=np.uint32)
+    per_step = ctx.num_candidates * len(insts)
+
+    def step():
+        if cfg_id == 4:
+            out = ctx.search_batch(G, lam)
+            return int(out["status"].max())
+        return int(ctx.search(0, int(G[0]), int(lam[0]))["status"])
+
+    for _ in range(args.warmup):
+        step()
+    ctx.set_timing(True)
+    scan_ms = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        status = step()
+        scan_ms.append(ctx.kernel_times()[1])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ctx.set_timing(False)
+    assert status in (0, 5)
+    terms_ms, _, final_ms, blocks = ctx.kernel_times()
+
+    value = per_step * args.steps / elapsed
+    avg_scan_s = float(np.mean(scan_ms)) / 1e3
+    achieved = per_step * OPS_PER_CANDIDATE / avg_scan_s
+    digest = _kernel_digest()
+    line = {
+        "metric": "ALP candidate allocations evaluated/sec on 1 GPU",
+        "value": value,
+        "unit": "candidates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": elapsed / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u32",
+        "data": "synthetic (seeded profile tables, see workloads/)",
+        "config": {"workload": f"{cfg.name}: {cfg.description}",
+                   "candidates_per_step": per_step, "instances": len(insts),
+                   "llms": cfg.num_llms, "gpu_budget": cfg.gpu_budget,
+                   "options_per_llm": len(cfg.tp_values) * len(cfg.frac_q) * cfg.max_replicas,
+                   "scan_blocks": blocks},
+        "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_LANE_OPS / 1e12,
+                     "unit": "TOP/s", "frac": achieved / PEAK_LANE_OPS,
+                     "traffic": _traffic(digest, args.workload),
+                     "kernel": "scan", "kernel_ms": avg_scan_s * 1e3,
+                     "ops_per_candidate": OPS_PER_CANDIDATE,
+                     "other_kernels_ms": {"option_terms": terms_ms, "final": final_ms}},
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(batch, int(G[0]), int(lam[0]), args.cpu_seconds)
+    ctx.close()
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,184 @@
+/*
+ * alp.h -- C ABI of the MI355X (gfx950) Aggregate LLM Pipeline allocation search.
+ *
+ * The search follows "Scepsy" (arXiv 2604.15186).  An agentic workflow is abstracted as a
+ * pipeline of its LLMs (Section 4).  For LLM m the inputs are its workflow statistics n_m
+ * (invocations per workflow request) and p_m (request-level parallelism) (Section 4, step 2),
+ * and its per-replica throughput--latency profile, one curve per tensor-parallel degree and GPU
+ * share (Section 4, step 3).  A candidate allocation picks, per LLM, a tensor-parallel degree
+ * tp, a GPU share q (in units of 1/Q GPU) and a replica count d (the three search dimensions
+ * of Section 1 and Section 5).  The predictor (Section 4, steps 4-5) gives
+ *   L_w = sum_m L_m(lambda * n_m / d_m) * n_m / p_m     (Eq. 1, the latency at each replica's load)
+ *   T_w = min_m d_m * T_m / n_m                         (Eq. 2, T_m the saturation throughput)
+ * and the search returns the allocation of lowest L_w that sustains the target workflow rate
+ * (T_w >= lambda), fits every LLM's weights into its GPU share (Section 5, step 1) and uses at
+ * most the GPU budget (Section 3, step 3: "lowest latency within a target workflow-level
+ * arrival rate").  Every candidate of the space is evaluated; ties go to the lowest index.
+ *
+ * Fixed point: rates in milli-requests/s, latencies in microseconds, n_m and p_m in thousandths.
+ * Per-replica rate r = ceil(lambda * n / (1000 d)); latency at r is lat[0] for r <= rate[0],
+ * linear between profile points (rounded down) and undefined above rate[K-1] (the option cannot
+ * sustain the load); contribution c = floor(latency * n / p); normalised throughput
+ * tau = floor(1000 d rate[K-1] / n); share units u = tp * q * d; memory fit W * Q <= tp * q * H.
+ *
+ * Numbering.  Option o of an LLM = (i * num_frac + j) * max_replicas + (d - 1) for
+ * tp = tp_values[i], q = frac_units[j] (replicas vary fastest).  Candidate
+ * x = sum_m o_m * O^(M-1-m) with O options per LLM (LLM 0 is the most significant digit).
+ *
+ * Conventions.  Every function returns an alp_status (int32_t).  No exception crosses the ABI.
+ * Host pointers unless stated.  Inputs are owned by the caller and deep-copied where kept.
+ * Out-parameters are written only on ALP_OK (and ALP_INFEASIBLE where stated).  A failed call
+ * leaves the context usable and unchanged.  A context is not thread-safe; distinct contexts are
+ * independent.  alp_last_error() describes the last failure of the calling thread.
+ */
+#ifndef ALP_H
+#define ALP_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    ALP_OK = 0,
+    ALP_EINVAL = 1,      /* malformed argument or table */
+    ALP_ERANGE = 2,      /* values would overflow the fixed-point objective or index space */
+    ALP_ENOMEM = 3,      /* device or host allocation failed */
+    ALP_EDEVICE = 4,     /* no usable device, or a HIP call failed */
+    ALP_INFEASIBLE = 5   /* no candidate meets target, memory fit and budget */
+} alp_status;
+
+#define ALP_MAX_LLMS 8
+#define ALP_MAX_TP 8
+#define ALP_MAX_FRAC 8
+#define ALP_MAX_REPLICAS 16
+#define ALP_MAX_POINTS 16
+#define ALP_MAX_OPTIONS 512      /* num_tp * num_frac * max_replicas */
+#define ALP_NO_INDEX UINT64_MAX
+
+/* Shape of the search space, shared by every instance of a context (Section 5: the scheduler
+ * enumerates GPU fractions, tensor-parallel degrees and replica counts per LLM).
+ *   num_llms      M, 1..8
+ *   tp_values     strictly ascending tensor-parallel degrees, 1..64 (Section 5, step 3 caps tp
+ *                 at the high-bandwidth interconnect degree; an MI355X node has 8)
+ *   frac_units    strictly ascending GPU shares in units of 1/units_per_gpu, 1..units_per_gpu
+ *   units_per_gpu Q, 1..16 (4 = quarters)
+ *   max_replicas  D, replica counts 1..D, D in 1..16
+ *   num_points    K profile points per (tp, share) curve, 1..16
+ * O = num_tp * num_frac * max_replicas must be <= ALP_MAX_OPTIONS and O^M < 2^63. */
+typedef struct {
+    uint32_t num_llms;
+    uint32_t num_tp;
+    uint32_t tp_values[ALP_MAX_TP];
+    uint32_t num_frac;
+    uint32_t frac_units[ALP_MAX_FRAC];
+    uint32_t units_per_gpu;
+    uint32_t max_replicas;
+    uint32_t num_points;
+} alp_space_t;
+
+/* Search result (48 bytes).  status is ALP_OK or ALP_INFEASIBLE; on INFEASIBLE index is
+ * ALP_NO_INDEX and the other fields are 0.  latency_us = L_w (Eq. 1), throughput_milli = T_w
+ * (Eq. 2), gpu_units = sum of tp * q * d; per LLM the chosen tp, share (units of 1/Q) and
+ * replica count, entries beyond num_llms 0. */
+typedef struct {
+    uint64_t index;
+    uint32_t latency_us;
+    uint32_t throughput_milli;
+    uint32_t gpu_units;
+    uint32_t status;
+    uint8_t tp[ALP_MAX_LLMS];
+    uint8_t frac_units[ALP_MAX_LLMS];
+    uint8_t replicas[ALP_MAX_LLMS];
+} alp_result_t;
+
+/* Evaluation of one candidate (16 bytes).
+ *   flags bit0: every LLM's option is deployable and its weights fit (Section 5, step 1)
+ *         bit1: every LLM sustains its per-replica load (r <= rate[K-1]; same as T_w >= lambda)
+ *         bit2: sum of share units <= Q * gpu_budget
+ *   latency_us       L_w (Eq. 1) if bit0 and bit1, else UINT32_MAX
+ *   throughput_milli T_w (Eq. 2) if bit0, else 0
+ *   gpu_units        sum of tp * q * d */
+typedef struct {
+    uint32_t flags;
+    uint32_t latency_us;
+    uint32_t throughput_milli;
+    uint32_t gpu_units;
+} alp_eval_t;
+
+typedef struct alp_ctx alp_ctx;
+
+/* Loads and validates the profiles of num_instances workflow instances and copies them to the
+ * device (Section 4, steps 2-3 produce these tables).  Host arrays, row-major, B = num_instances:
+ *   weight_bytes  uint64 [B][M]               model weights in bytes, < 2^48
+ *   n_milli       uint32 [B][M]               n_m * 1000, 1 .. 2^31-1
+ *   p_milli       uint32 [B][M]               p_m * 1000, 1 .. 2^31-1
+ *   allowed       uint8  [B][M][num_tp][num_frac]     0/1: the (tp, share) pair may be deployed
+ *   rate_milli    uint32 [B][M][num_tp][num_frac][K]  per-replica rates, strictly ascending in
+ *                                                     k, < 2^31; the last is saturation
+ *   lat_us        uint32 [B][M][num_tp][num_frac][K]  latency at that rate, < 2^31 (the caller
+ *                                                     picks mean or a percentile, Section 4 step 5)
+ * hbm_bytes_per_gpu H, 1 .. 2^48-1.  device: HIP device ordinal.  hip_stream: hipStream_t all
+ * work of the context is ordered on (NULL: the device's null stream); it must outlive the ctx.
+ * Errors: EINVAL (shape, ranges, ordering, NULL pointer), ERANGE (some instance's largest
+ * possible L_w over deployable options reaches 2^32-1), EDEVICE, ENOMEM.  On success *out
+ * owns device memory until alp_free. */
+int32_t alp_load_profiles(alp_ctx **out, const alp_space_t *space, uint32_t num_instances,
+                          const uint64_t *weight_bytes, const uint32_t *n_milli,
+                          const uint32_t *p_milli, const uint8_t *allowed,
+                          const uint32_t *rate_milli, const uint32_t *lat_us,
+                          uint64_t hbm_bytes_per_gpu, int32_t device, void *hip_stream);
+
+/* Exhaustive constrained argmin for one instance at GPU budget gpu_budget (whole GPUs) and
+ * target workflow rate target_milli.  Synchronous on the context stream.  Returns ALP_OK with
+ * the result, or ALP_INFEASIBLE with out->status = ALP_INFEASIBLE.  EINVAL: bad instance. */
+int32_t alp_search(alp_ctx *ctx, uint32_t instance, uint32_t gpu_budget, uint32_t target_milli,
+                   alp_result_t *out);
+
+/* count independent searches in one launch sequence (the multi-workflow level of Section 5 runs
+ * one search per workflow).  instances may be NULL (0..count-1).  out[i].status is ALP_OK or
+ * ALP_INFEASIBLE per query; the call returns ALP_OK unless an argument or device error occurs.
+ * count = 0 is a no-op. */
+int32_t alp_search_batch(alp_ctx *ctx, uint32_t count, const uint32_t *instances,
+                         const uint32_t *gpu_budget, const uint32_t *target_milli,
+                         alp_result_t *out);
+
+/* Largest workflow throughput T_w (Eq. 2) any candidate with deployable, fitting options
+ * reaches within the budget, ignoring the target; 0 if none fits.  A target above it is
+ * infeasible, a target at or below it is feasible.  instances may be NULL. */
+int32_t alp_max_throughput(alp_ctx *ctx, uint32_t count, const uint32_t *instances,
+                           const uint32_t *gpu_budget, uint32_t *out_tmax);
+
+/* Evaluates count given candidate indices (each < O^M, else EINVAL) of one instance. */
+int32_t alp_eval_candidates(alp_ctx *ctx, uint32_t instance, uint32_t gpu_budget,
+                            uint32_t target_milli, const uint64_t *indices, uint64_t count,
+                            alp_eval_t *out);
+
+/* Launch choices, for tests and tuning.  variant: 0 automatic, 1 lane-per-last-option kernel,
+ * 2 thread-per-candidate kernel.  blocks_per_item and threads_per_block (a multiple of 64, at
+ * most 1024): 0 = automatic.  Results do not depend on these choices. */
+int32_t alp_set_launch(alp_ctx *ctx, uint32_t variant, uint32_t blocks_per_item,
+                       uint32_t threads_per_block);
+
+/* Enables (1) or disables (0) HIP-event timing of the searches' kernels on the context stream.
+ * alp_kernel_times writes, for the last search or batch, the milliseconds of the option-term
+ * kernel, the candidate scan kernel and the final reduction kernel, and the scan kernel's
+ * grid size in blocks (ms[0..2], *scan_blocks). */
+int32_t alp_set_timing(alp_ctx *ctx, int32_t enable);
+int32_t alp_kernel_times(alp_ctx *ctx, float ms[3], uint32_t *scan_blocks);
+
+/* Candidates per instance, O^M. */
+int32_t alp_num_candidates(const alp_ctx *ctx, uint64_t *out);
+
+/* Releases the context (NULL is a no-op). */
+void alp_free(alp_ctx *ctx);
+
+const char *alp_status_str(int32_t status);
+const char *alp_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ALP_H */

@@ -1,0 +1,690 @@
+// C ABI of the ALP allocation search: validation, device memory, launch geometry and timing.
+// The arithmetic of the search runs in the kernels of alp_kernels.hip; this file only checks
+// arguments, moves the tables and query values to the device and the results back.
+#include <hip/hip_runtime.h>
+
+#include <stdarg.h>
+#include <stdint.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <new>
+#include <vector>
+
+#include "alp.h"
+#include "alp_internal.h"
+
+using alp::kCapacityMax;
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+int32_t fail(int32_t status, const char *fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+    va_end(ap);
+    return status;
+}
+
+int32_t hip_fail(hipError_t e, const char *what)
+{
+    if (e == hipErrorOutOfMemory || e == hipErrorMemoryAllocation)
+        return fail(ALP_ENOMEM, "%s: %s", what, hipGetErrorString(e));
+    return fail(ALP_EDEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Device buffer that only grows.
+struct DevBuf {
+    void *ptr = nullptr;
+    size_t cap = 0;
+    hipError_t ensure(size_t bytes)
+    {
+        if (bytes <= cap)
+            return hipSuccess;
+        if (ptr) {
+            hipError_t e = hipFree(ptr);
+            ptr = nullptr;
+            cap = 0;
+            if (e != hipSuccess)
+                return e;
+        }
+        hipError_t e = hipMalloc(&ptr, bytes);
+        if (e == hipSuccess)
+            cap = bytes;
+        else
+            ptr = nullptr;
+        return e;
+    }
+    void release()
+    {
+        if (ptr)
+            (void)hipFree(ptr);
+        ptr = nullptr;
+        cap = 0;
+    }
+};
+
+// Restores the caller's current device on scope exit.
+struct DeviceGuard {
+    int prev = -1;
+    hipError_t status = hipSuccess;
+    explicit DeviceGuard(int dev)
+    {
+        status = hipGetDevice(&prev);
+        if (status == hipSuccess && prev != dev)
+            status = hipSetDevice(dev);
+    }
+    ~DeviceGuard()
+    {
+        if (prev >= 0)
+            (void)hipSetDevice(prev);
+    }
+};
+
+}  // namespace
+
+struct alp_ctx {
+    int device = 0;
+    hipStream_t stream = nullptr;
+    alp_space_t space{};
+    alp::SpaceDev sp{};
+    uint64_t N = 0;
+    uint32_t B = 0;
+    uint64_t H = 0;
+    int num_cus = 0;
+
+    DevBuf tables;                 // W | n | p | allowed | rate | lat
+    alp::TablesDev tdev{};
+
+    DevBuf q_inst, q_cap, q_lambda, rec, ext, winners, results, idx, evals, tmax;
+    alp_result_t *host_results = nullptr;   // pinned staging
+    size_t host_results_cap = 0;
+
+    uint32_t variant = 0, bpi_override = 0, tpb_override = 0;
+    int timing = 0;
+    hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
+    float last_ms[3] = {0, 0, 0};
+    uint32_t last_blocks = 0;
+};
+
+namespace {
+
+uint64_t ceil_div(uint64_t a, uint64_t b) { return (a + b - 1) / b; }
+
+int32_t validate_space(const alp_space_t *s, uint32_t *O_out, uint64_t *N_out)
+{
+    if (!s)
+        return fail(ALP_EINVAL, "space is NULL");
+    if (s->num_llms < 1 || s->num_llms > ALP_MAX_LLMS)
+        return fail(ALP_EINVAL, "num_llms %u outside 1..%d", s->num_llms, ALP_MAX_LLMS);
+    if (s->num_tp < 1 || s->num_tp > ALP_MAX_TP)
+        return fail(ALP_EINVAL, "num_tp %u outside 1..%d", s->num_tp, ALP_MAX_TP);
+    if (s->num_frac < 1 || s->num_frac > ALP_MAX_FRAC)
+        return fail(ALP_EINVAL, "num_frac %u outside 1..%d", s->num_frac, ALP_MAX_FRAC);
+    if (s->units_per_gpu < 1 || s->units_per_gpu > 16)
+        return fail(ALP_EINVAL, "units_per_gpu %u outside 1..16", s->units_per_gpu);
+    if (s->max_replicas < 1 || s->max_replicas > ALP_MAX_REPLICAS)
+        return fail(ALP_EINVAL, "max_replicas %u outside 1..%d", s->max_replicas, ALP_MAX_REPLICAS);
+    if (s->num_points < 1 || s->num_points > ALP_MAX_POINTS)
+        return fail(ALP_EINVAL, "num_points %u outside 1..%d", s->num_points, ALP_MAX_POINTS);
+    for (uint32_t i = 0; i < s->num_tp; ++i) {
+        if (s->tp_values[i] < 1 || s->tp_values[i] > 64)
+            return fail(ALP_EINVAL, "tp_values[%u]=%u outside 1..64", i, s->tp_values[i]);
+        if (i && s->tp_values[i] <= s->tp_values[i - 1])
+            return fail(ALP_EINVAL, "tp_values not strictly ascending");
+    }
+    for (uint32_t j = 0; j < s->num_frac; ++j) {
+        if (s->frac_units[j] < 1 || s->frac_units[j] > s->units_per_gpu)
+            return fail(ALP_EINVAL, "frac_units[%u]=%u outside 1..%u", j, s->frac_units[j],
+                        s->units_per_gpu);
+        if (j && s->frac_units[j] <= s->frac_units[j - 1])
+            return fail(ALP_EINVAL, "frac_units not strictly ascending");
+    }
+    const uint32_t O = s->num_tp * s->num_frac * s->max_replicas;
+    if (O > ALP_MAX_OPTIONS)
+        return fail(ALP_EINVAL, "%u options per LLM exceed %d", O, ALP_MAX_OPTIONS);
+    uint64_t N = 1;
+    for (uint32_t m = 0; m < s->num_llms; ++m) {
+        if (N > (UINT64_C(1) << 63) / O)
+            return fail(ALP_ERANGE, "candidate space O^M reaches 2^63");
+        N *= O;
+    }
+    if (N >= (UINT64_C(1) << 63))
+        return fail(ALP_ERANGE, "candidate space O^M reaches 2^63");
+    *O_out = O;
+    *N_out = N;
+    return ALP_OK;
+}
+
+int32_t validate_tables(const alp_space_t *s, uint32_t B, const uint64_t *W, const uint32_t *n,
+                        const uint32_t *p, const uint8_t *allowed, const uint32_t *rate,
+                        const uint32_t *lat, uint64_t H)
+{
+    if (!W || !n || !p || !allowed || !rate || !lat)
+        return fail(ALP_EINVAL, "a table pointer is NULL");
+    if (H < 1 || H >= (UINT64_C(1) << 48))
+        return fail(ALP_EINVAL, "hbm_bytes_per_gpu outside 1..2^48-1");
+    const uint32_t M = s->num_llms, nt = s->num_tp, nf = s->num_frac, K = s->num_points;
+    for (uint32_t b = 0; b < B; ++b) {
+        uint64_t worst = 0;   // largest possible L_w over deployable, fitting options
+        for (uint32_t m = 0; m < M; ++m) {
+            const uint64_t lm = (uint64_t)b * M + m;
+            if (W[lm] >= (UINT64_C(1) << 48))
+                return fail(ALP_EINVAL, "instance %u llm %u: weight_bytes >= 2^48", b, m);
+            if (n[lm] < 1 || n[lm] >= (1u << 31) || p[lm] < 1 || p[lm] >= (1u << 31))
+                return fail(ALP_EINVAL, "instance %u llm %u: n_milli/p_milli outside 1..2^31-1", b, m);
+            uint64_t worst_m = 0;
+            for (uint32_t i = 0; i < nt; ++i) {
+                for (uint32_t j = 0; j < nf; ++j) {
+                    const uint64_t tab = (lm * nt + i) * nf + j;
+                    if (allowed[tab] > 1)
+                        return fail(ALP_EINVAL, "instance %u llm %u: allowed must be 0 or 1", b, m);
+                    const uint32_t *r = rate + tab * K, *l = lat + tab * K;
+                    uint32_t max_lat = 0;
+                    for (uint32_t k = 0; k < K; ++k) {
+                        if (r[k] >= (1u << 31) || l[k] >= (1u << 31))
+                            return fail(ALP_EINVAL, "instance %u llm %u: rate/latency >= 2^31", b, m);
+                        if (k && r[k] <= r[k - 1])
+                            return fail(ALP_EINVAL,
+                                        "instance %u llm %u tp#%u share#%u: rates not strictly ascending",
+                                        b, m, i, j);
+                        max_lat = l[k] > max_lat ? l[k] : max_lat;
+                    }
+                    const bool fits = W[lm] * s->units_per_gpu <=
+                                      (uint64_t)s->tp_values[i] * s->frac_units[j] * H;
+                    if (allowed[tab] && fits) {
+                        const uint64_t c = (uint64_t)max_lat * n[lm] / p[lm];
+                        worst_m = c > worst_m ? c : worst_m;
+                    }
+                }
+            }
+            worst += worst_m;
+            if (worst >= 0xFFFFFFFFull)
+                return fail(ALP_ERANGE,
+                            "instance %u: latency sum can reach %llu us, beyond the 32-bit objective",
+                            b, (unsigned long long)worst);
+        }
+    }
+    return ALP_OK;
+}
+
+uint32_t capacity_of(const alp_ctx *c, uint32_t gpu_budget)
+{
+    const uint64_t cap = (uint64_t)c->space.units_per_gpu * gpu_budget;
+    return cap > kCapacityMax ? kCapacityMax : (uint32_t)cap;
+}
+
+uint32_t slots_for(uint32_t O)
+{
+    return O <= 64 ? 1 : O <= 128 ? 2 : O <= 256 ? 4 : 8;
+}
+
+alp::ScanGeometry plan_scan(const alp_ctx *c, uint32_t count)
+{
+    alp::ScanGeometry g{};
+    const alp::SpaceDev &sp = c->sp;
+    g.variant = c->variant ? c->variant : 1;
+    g.threads = c->tpb_override ? c->tpb_override : 256;
+    g.slots = slots_for(sp.O);
+    const uint32_t wpb = g.threads / 64;
+    const uint64_t resident =
+        (uint64_t)(c->num_cus > 0 ? c->num_cus : 256) *
+        (uint64_t)alp::scan_blocks_per_cu(g.variant, g.slots, g.threads, sp);
+    const uint64_t want = count ? ceil_div(resident, count) : 1;
+    if (g.variant == 1) {
+        g.rows = 1;
+        for (uint32_t m = 2; m < sp.M; ++m)
+            g.rows *= sp.O;
+        uint64_t bpi = c->bpi_override ? c->bpi_override : want;
+        const uint64_t max_bpi = ceil_div(g.rows, wpb);
+        if (!c->bpi_override && bpi > max_bpi)
+            bpi = max_bpi;
+        if (bpi < 1)
+            bpi = 1;
+        g.rows_per_wave = ceil_div(g.rows, bpi * wpb);
+        if (!c->bpi_override)
+            bpi = ceil_div(g.rows, g.rows_per_wave * wpb);
+        g.blocks_per_item = (uint32_t)bpi;
+    } else {
+        uint64_t bpi = c->bpi_override ? c->bpi_override : want;
+        const uint64_t max_bpi = ceil_div(c->N, g.threads);
+        if (!c->bpi_override && bpi > max_bpi)
+            bpi = max_bpi;
+        if (bpi < 1)
+            bpi = 1;
+        g.per_thread = ceil_div(c->N, bpi * g.threads);
+        g.blocks_per_item = (uint32_t)bpi;
+    }
+    return g;
+}
+
+int32_t ensure_host_results(alp_ctx *c, size_t count)
+{
+    if (count <= c->host_results_cap)
+        return ALP_OK;
+    if (c->host_results)
+        (void)hipHostFree(c->host_results);
+    c->host_results = nullptr;
+    c->host_results_cap = 0;
+    hipError_t e = hipHostMalloc((void **)&c->host_results, count * sizeof(alp_result_t),
+                                 hipHostMallocDefault);
+    if (e != hipSuccess)
+        return hip_fail(e, "hipHostMalloc(results)");
+    c->host_results_cap = count;
+    return ALP_OK;
+}
+
+// Runs option terms -> scan -> final for `count` items described by q; results land in
+// c->host_results[0..count).
+int32_t run_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count)
+{
+    const alp::SpaceDev &sp = c->sp;
+    const alp::ScanGeometry g = plan_scan(c, count);
+    const uint64_t items_bytes = (uint64_t)count * sp.M * sp.O * sizeof(uint2);
+    const uint64_t nwin = (uint64_t)count * g.blocks_per_item;
+    if (nwin >= (UINT64_C(1) << 31))
+        return fail(ALP_ERANGE, "batch too large for one launch (%llu blocks)",
+                    (unsigned long long)nwin);
+    hipError_t e;
+    if ((e = c->rec.ensure(items_bytes)) != hipSuccess)
+        return hip_fail(e, "hipMalloc(rec)");
+    if ((e = c->ext.ensure(items_bytes)) != hipSuccess)
+        return hip_fail(e, "hipMalloc(ext)");
+    if ((e = c->winners.ensure(nwin * sizeof(alp::Winner))) != hipSuccess)
+        return hip_fail(e, "hipMalloc(winners)");
+    if ((e = c->results.ensure((uint64_t)count * sizeof(alp_result_t))) != hipSuccess)
+        return hip_fail(e, "hipMalloc(results)");
+    int32_t st = ensure_host_results(c, count);
+    if (st != ALP_OK)
+        return st;
+
+    uint2 *rec = (uint2 *)c->rec.ptr, *ext = (uint2 *)c->ext.ptr;
+    alp::Winner *win = (alp::Winner *)c->winners.ptr;
+    alp_result_t *res = (alp_result_t *)c->results.ptr;
+    if (c->timing && (e = hipEventRecord(c->ev[0], c->stream)) != hipSuccess)
+        return hip_fail(e, "hipEventRecord");
+    if ((e = alp::launch_option_terms(sp, c->tdev, q, count, rec, ext, c->stream)) != hipSuccess)
+        return hip_fail(e, "option_terms launch");
+    if (c->timing && (e = hipEventRecord(c->ev[1], c->stream)) != hipSuccess)
+        return hip_fail(e, "hipEventRecord");
+    if ((e = alp::launch_scan(sp, q, count, rec, g, win, c->stream)) != hipSuccess)
+        return hip_fail(e, "scan launch");
+    if (c->timing && (e = hipEventRecord(c->ev[2], c->stream)) != hipSuccess)
+        return hip_fail(e, "hipEventRecord");
+    if ((e = alp::launch_final(sp, count, g.blocks_per_item, win, ext, res, c->stream)) != hipSuccess)
+        return hip_fail(e, "final launch");
+    if (c->timing && (e = hipEventRecord(c->ev[3], c->stream)) != hipSuccess)
+        return hip_fail(e, "hipEventRecord");
+    if ((e = hipMemcpyAsync(c->host_results, res, (size_t)count * sizeof(alp_result_t),
+                            hipMemcpyDeviceToHost, c->stream)) != hipSuccess)
+        return hip_fail(e, "copy results");
+    if ((e = hipStreamSynchronize(c->stream)) != hipSuccess)
+        return hip_fail(e, "hipStreamSynchronize");
+    if (c->timing) {
+        for (int k = 0; k < 3; ++k)
+            if ((e = hipEventElapsedTime(&c->last_ms[k], c->ev[k], c->ev[k + 1])) != hipSuccess)
+                return hip_fail(e, "hipEventElapsedTime");
+    }
+    c->last_blocks = count * g.blocks_per_item;
+    return ALP_OK;
+}
+
+int32_t check_instance(const alp_ctx *c, uint32_t inst)
+{
+    if (inst >= c->B)
+        return fail(ALP_EINVAL, "instance %u out of range (%u loaded)", inst, c->B);
+    return ALP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t alp_load_profiles(alp_ctx **out, const alp_space_t *space, uint32_t num_instances,
+                          const uint64_t *weight_bytes, const uint32_t *n_milli,
+                          const uint32_t *p_milli, const uint8_t *allowed,
+                          const uint32_t *rate_milli, const uint32_t *lat_us,
+                          uint64_t hbm_bytes_per_gpu, int32_t device, void *hip_stream)
+{
+    if (!out)
+        return fail(ALP_EINVAL, "out is NULL");
+    uint32_t O = 0;
+    uint64_t N = 0;
+    int32_t st = validate_space(space, &O, &N);
+    if (st != ALP_OK)
+        return st;
+    if (num_instances < 1)
+        return fail(ALP_EINVAL, "num_instances must be >= 1");
+    st = validate_tables(space, num_instances, weight_bytes, n_milli, p_milli, allowed, rate_milli,
+                         lat_us, hbm_bytes_per_gpu);
+    if (st != ALP_OK)
+        return st;
+
+    int ndev = 0;
+    hipError_t e = hipGetDeviceCount(&ndev);
+    if (e != hipSuccess || ndev <= 0)
+        return fail(ALP_EDEVICE, "no HIP device available");
+    if (device < 0 || device >= ndev)
+        return fail(ALP_EDEVICE, "device %d out of range (%d devices)", device, ndev);
+    DeviceGuard guard(device);
+    if (guard.status != hipSuccess)
+        return hip_fail(guard.status, "hipSetDevice");
+
+    alp_ctx *c = new (std::nothrow) alp_ctx();
+    if (!c)
+        return fail(ALP_ENOMEM, "host allocation failed");
+    c->device = device;
+    c->stream = (hipStream_t)hip_stream;
+    c->space = *space;
+    c->N = N;
+    c->B = num_instances;
+    c->H = hbm_bytes_per_gpu;
+    alp::SpaceDev &sp = c->sp;
+    sp.M = space->num_llms;
+    sp.n_tp = space->num_tp;
+    sp.n_fq = space->num_frac;
+    sp.D = space->max_replicas;
+    sp.K = space->num_points;
+    sp.Q = space->units_per_gpu;
+    sp.O = O;
+    for (uint32_t i = 0; i < ALP_MAX_TP; ++i)
+        sp.tp[i] = i < sp.n_tp ? space->tp_values[i] : 0;
+    for (uint32_t j = 0; j < ALP_MAX_FRAC; ++j)
+        sp.fq[j] = j < sp.n_fq ? space->frac_units[j] : 0;
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, device) == hipSuccess)
+        c->num_cus = prop.multiProcessorCount;
+
+    const uint64_t BM = (uint64_t)num_instances * sp.M;
+    const uint64_t BMT = BM * sp.n_tp * sp.n_fq;
+    const uint64_t BMTK = BMT * sp.K;
+    auto align = [](uint64_t v) { return (v + 255) & ~UINT64_C(255); };
+    const uint64_t offW = 0, offn = align(offW + BM * 8), offp = align(offn + BM * 4),
+                   offA = align(offp + BM * 4), offR = align(offA + BMT),
+                   offL = align(offR + BMTK * 4), total = align(offL + BMTK * 4);
+    if ((e = c->tables.ensure(total)) != hipSuccess) {
+        st = hip_fail(e, "hipMalloc(tables)");
+        alp_free(c);
+        return st;
+    }
+    uint8_t *base = (uint8_t *)c->tables.ptr;
+    struct {
+        uint64_t off;
+        const void *src;
+        uint64_t bytes;
+    } parts[] = {{offW, weight_bytes, BM * 8}, {offn, n_milli, BM * 4}, {offp, p_milli, BM * 4},
+                 {offA, allowed, BMT}, {offR, rate_milli, BMTK * 4}, {offL, lat_us, BMTK * 4}};
+    for (auto &pp : parts) {
+        if ((e = hipMemcpyAsync(base + pp.off, pp.src, pp.bytes, hipMemcpyHostToDevice,
+                                c->stream)) != hipSuccess) {
+            st = hip_fail(e, "copy tables");
+            alp_free(c);
+            return st;
+        }
+    }
+    if ((e = hipStreamSynchronize(c->stream)) != hipSuccess) {
+        st = hip_fail(e, "hipStreamSynchronize");
+        alp_free(c);
+        return st;
+    }
+    c->tdev.W = (const uint64_t *)(base + offW);
+    c->tdev.n = (const uint32_t *)(base + offn);
+    c->tdev.p = (const uint32_t *)(base + offp);
+    c->tdev.allowed = (const uint8_t *)(base + offA);
+    c->tdev.rate = (const uint32_t *)(base + offR);
+    c->tdev.lat = (const uint32_t *)(base + offL);
+    c->tdev.H = hbm_bytes_per_gpu;
+    for (int k = 0; k < 4; ++k) {
+        if ((e = hipEventCreate(&c->ev[k])) != hipSuccess) {
+            st = hip_fail(e, "hipEventCreate");
+            alp_free(c);
+            return st;
+        }
+    }
+    *out = c;
+    return ALP_OK;
+}
+
+int32_t alp_search(alp_ctx *ctx, uint32_t instance, uint32_t gpu_budget, uint32_t target_milli,
+                   alp_result_t *out)
+{
+    if (!ctx || !out)
+        return fail(ALP_EINVAL, "ctx or out is NULL");
+    int32_t st = check_instance(ctx, instance);
+    if (st != ALP_OK)
+        return st;
+    DeviceGuard guard(ctx->device);
+    if (guard.status != hipSuccess)
+        return hip_fail(guard.status, "hipSetDevice");
+    alp::QueryDev q{};
+    q.inst1 = instance;
+    q.cap1 = capacity_of(ctx, gpu_budget);
+    q.lambda1 = target_milli;
+    if ((st = run_search(ctx, q, 1)) != ALP_OK)
+        return st;
+    *out = ctx->host_results[0];
+    return out->status == ALP_OK ? ALP_OK : ALP_INFEASIBLE;
+}
+
+int32_t alp_search_batch(alp_ctx *ctx, uint32_t count, const uint32_t *instances,
+                         const uint32_t *gpu_budget, const uint32_t *target_milli,
+                         alp_result_t *out)
+{
+    if (!ctx)
+        return fail(ALP_EINVAL, "ctx is NULL");
+    if (count == 0)
+        return ALP_OK;
+    if (!gpu_budget || !target_milli || !out)
+        return fail(ALP_EINVAL, "gpu_budget, target_milli or out is NULL");
+    std::vector<uint32_t> inst(count), cap(count);
+    for (uint32_t i = 0; i < count; ++i) {
+        inst[i] = instances ? instances[i] : i;
+        int32_t st = check_instance(ctx, inst[i]);
+        if (st != ALP_OK)
+            return st;
+        cap[i] = capacity_of(ctx, gpu_budget[i]);
+    }
+    DeviceGuard guard(ctx->device);
+    if (guard.status != hipSuccess)
+        return hip_fail(guard.status, "hipSetDevice");
+    hipError_t e;
+    const size_t bytes = (size_t)count * sizeof(uint32_t);
+    if ((e = ctx->q_inst.ensure(bytes)) != hipSuccess || (e = ctx->q_cap.ensure(bytes)) != hipSuccess ||
+        (e = ctx->q_lambda.ensure(bytes)) != hipSuccess)
+        return hip_fail(e, "hipMalloc(queries)");
+    if ((e = hipMemcpyAsync(ctx->q_inst.ptr, inst.data(), bytes, hipMemcpyHostToDevice, ctx->stream)) != hipSuccess ||
+        (e = hipMemcpyAsync(ctx->q_cap.ptr, cap.data(), bytes, hipMemcpyHostToDevice, ctx->stream)) != hipSuccess ||
+        (e = hipMemcpyAsync(ctx->q_lambda.ptr, target_milli, bytes, hipMemcpyHostToDevice, ctx->stream)) != hipSuccess)
+        return hip_fail(e, "copy queries");
+    alp::QueryDev q{};
+    q.inst = (const uint32_t *)ctx->q_inst.ptr;
+    q.capacity = (const uint32_t *)ctx->q_cap.ptr;
+    q.lambda = (const uint32_t *)ctx->q_lambda.ptr;
+    int32_t st = run_search(ctx, q, count);
+    if (st != ALP_OK)
+        return st;
+    memcpy(out, ctx->host_results, (size_t)count * sizeof(alp_result_t));
+    return ALP_OK;
+}
+
+int32_t alp_max_throughput(alp_ctx *ctx, uint32_t count, const uint32_t *instances,
+                           const uint32_t *gpu_budget, uint32_t *out_tmax)
+{
+    if (!ctx)
+        return fail(ALP_EINVAL, "ctx is NULL");
+    if (count == 0)
+        return ALP_OK;
+    if (!gpu_budget || !out_tmax)
+        return fail(ALP_EINVAL, "gpu_budget or out_tmax is NULL");
+    std::vector<uint32_t> inst(count), cap(count), zero(count, 0);
+    for (uint32_t i = 0; i < count; ++i) {
+        inst[i] = instances ? instances[i] : i;
+        int32_t st = check_instance(ctx, inst[i]);
+        if (st != ALP_OK)
+            return st;
+        cap[i] = capacity_of(ctx, gpu_budget[i]);
+    }
+    DeviceGuard guard(ctx->device);
+    if (guard.status != hipSuccess)
+        return hip_fail(guard.status, "hipSetDevice");
+    hipError_t e;
+    const size_t bytes = (size_t)count * sizeof(uint32_t);
+    const uint64_t items_bytes = (uint64_t)count * ctx->sp.M * ctx->sp.O * sizeof(uint2);
+    if ((e = ctx->q_inst.ensure(bytes)) != hipSuccess || (e = ctx->q_cap.ensure(bytes)) != hipSuccess ||
+        (e = ctx->q_lambda.ensure(bytes)) != hipSuccess || (e = ctx->tmax.ensure(bytes)) != hipSuccess ||
+        (e = ctx->rec.ensure(items_bytes)) != hipSuccess || (e = ctx->ext.ensure(items_bytes)) != hipSuccess)
+        return hip_fail(e, "hipMalloc(max_throughput)");
+    if ((e = hipMemcpyAsync(ctx->q_inst.ptr, inst.data(), bytes, hipMemcpyHostToDevice, ctx->stream)) != hipSuccess ||
+        (e = hipMemcpyAsync(ctx->q_cap.ptr, cap.data(), bytes, hipMemcpyHostToDevice, ctx->stream)) != hipSuccess ||
+        (e = hipMemcpyAsync(ctx->q_lambda.ptr, zero.data(), bytes, hipMemcpyHostToDevice, ctx->stream)) != hipSuccess)
+        return hip_fail(e, "copy queries");
+    alp::QueryDev q{};
+    q.inst = (const uint32_t *)ctx->q_inst.ptr;
+    q.capacity = (const uint32_t *)ctx->q_cap.ptr;
+    q.lambda = (const uint32_t *)ctx->q_lambda.ptr;
+    if ((e = alp::launch_option_terms(ctx->sp, ctx->tdev, q, count, (uint2 *)ctx->rec.ptr,
+                                      (uint2 *)ctx->ext.ptr, ctx->stream)) != hipSuccess)
+        return hip_fail(e, "option_terms launch");
+    if ((e = alp::launch_tmax(ctx->sp, q, count, (const uint2 *)ctx->ext.ptr,
+                              (uint32_t *)ctx->tmax.ptr, ctx->stream)) != hipSuccess)
+        return hip_fail(e, "tmax launch");
+    std::vector<uint32_t> host(count);
+    if ((e = hipMemcpyAsync(host.data(), ctx->tmax.ptr, bytes, hipMemcpyDeviceToHost, ctx->stream)) != hipSuccess)
+        return hip_fail(e, "copy results");
+    if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess)
+        return hip_fail(e, "hipStreamSynchronize");
+    memcpy(out_tmax, host.data(), bytes);
+    return ALP_OK;
+}
+
+int32_t alp_eval_candidates(alp_ctx *ctx, uint32_t instance, uint32_t gpu_budget,
+                            uint32_t target_milli, const uint64_t *indices, uint64_t count,
+                            alp_eval_t *out)
+{
+    if (!ctx)
+        return fail(ALP_EINVAL, "ctx is NULL");
+    int32_t st = check_instance(ctx, instance);
+    if (st != ALP_OK)
+        return st;
+    if (count == 0)
+        return ALP_OK;
+    if (!indices || !out)
+        return fail(ALP_EINVAL, "indices or out is NULL");
+    for (uint64_t i = 0; i < count; ++i)
+        if (indices[i] >= ctx->N)
+            return fail(ALP_EINVAL, "indices[%llu]=%llu outside the %llu candidates",
+                        (unsigned long long)i, (unsigned long long)indices[i],
+                        (unsigned long long)ctx->N);
+    DeviceGuard guard(ctx->device);
+    if (guard.status != hipSuccess)
+        return hip_fail(guard.status, "hipSetDevice");
+    hipError_t e;
+    const uint64_t item_bytes = (uint64_t)ctx->sp.M * ctx->sp.O * sizeof(uint2);
+    if ((e = ctx->rec.ensure(item_bytes)) != hipSuccess || (e = ctx->ext.ensure(item_bytes)) != hipSuccess ||
+        (e = ctx->idx.ensure(count * sizeof(uint64_t))) != hipSuccess ||
+        (e = ctx->evals.ensure(count * sizeof(alp_eval_t))) != hipSuccess)
+        return hip_fail(e, "hipMalloc(eval)");
+    alp::QueryDev q{};
+    q.inst1 = instance;
+    q.cap1 = capacity_of(ctx, gpu_budget);
+    q.lambda1 = target_milli;
+    if ((e = hipMemcpyAsync(ctx->idx.ptr, indices, count * sizeof(uint64_t), hipMemcpyHostToDevice,
+                            ctx->stream)) != hipSuccess)
+        return hip_fail(e, "copy indices");
+    if ((e = alp::launch_option_terms(ctx->sp, ctx->tdev, q, 1, (uint2 *)ctx->rec.ptr,
+                                      (uint2 *)ctx->ext.ptr, ctx->stream)) != hipSuccess)
+        return hip_fail(e, "option_terms launch");
+    if ((e = alp::launch_eval(ctx->sp, q.cap1, (const uint2 *)ctx->rec.ptr, (const uint2 *)ctx->ext.ptr,
+                              (const uint64_t *)ctx->idx.ptr, count, (alp_eval_t *)ctx->evals.ptr,
+                              ctx->stream)) != hipSuccess)
+        return hip_fail(e, "eval launch");
+    if ((e = hipMemcpyAsync(out, ctx->evals.ptr, count * sizeof(alp_eval_t), hipMemcpyDeviceToHost,
+                            ctx->stream)) != hipSuccess)
+        return hip_fail(e, "copy evaluations");
+    if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess)
+        return hip_fail(e, "hipStreamSynchronize");
+    return ALP_OK;
+}
+
+int32_t alp_set_launch(alp_ctx *ctx, uint32_t variant, uint32_t blocks_per_item,
+                       uint32_t threads_per_block)
+{
+    if (!ctx)
+        return fail(ALP_EINVAL, "ctx is NULL");
+    if (variant > 2)
+        return fail(ALP_EINVAL, "variant %u not in 0..2", variant);
+    if (threads_per_block && (threads_per_block % 64 || threads_per_block > 1024))
+        return fail(ALP_EINVAL, "threads_per_block must be a multiple of 64, at most 1024");
+    if (blocks_per_item > (1u << 24))
+        return fail(ALP_EINVAL, "blocks_per_item too large");
+    ctx->variant = variant;
+    ctx->bpi_override = blocks_per_item;
+    ctx->tpb_override = threads_per_block;
+    return ALP_OK;
+}
+
+int32_t alp_set_timing(alp_ctx *ctx, int32_t enable)
+{
+    if (!ctx)
+        return fail(ALP_EINVAL, "ctx is NULL");
+    ctx->timing = enable ? 1 : 0;
+    return ALP_OK;
+}
+
+int32_t alp_kernel_times(alp_ctx *ctx, float ms[3], uint32_t *scan_blocks)
+{
+    if (!ctx || !ms)
+        return fail(ALP_EINVAL, "ctx or ms is NULL");
+    for (int k = 0; k < 3; ++k)
+        ms[k] = ctx->last_ms[k];
+    if (scan_blocks)
+        *scan_blocks = ctx->last_blocks;
+    return ALP_OK;
+}
+
+int32_t alp_num_candidates(const alp_ctx *ctx, uint64_t *out)
+{
+    if (!ctx || !out)
+        return fail(ALP_EINVAL, "ctx or out is NULL");
+    *out = ctx->N;
+    return ALP_OK;
+}
+
+void alp_free(alp_ctx *ctx)
+{
+    if (!ctx)
+        return;
+    DeviceGuard guard(ctx->device);
+    if (ctx->stream)
+        (void)hipStreamSynchronize(ctx->stream);
+    for (int k = 0; k < 4; ++k)
+        if (ctx->ev[k])
+            (void)hipEventDestroy(ctx->ev[k]);
+    DevBuf *bufs[] = {&ctx->tables, &ctx->q_inst, &ctx->q_cap, &ctx->q_lambda, &ctx->rec,
+                      &ctx->ext, &ctx->winners, &ctx->results, &ctx->idx, &ctx->evals, &ctx->tmax};
+    for (DevBuf *b : bufs)
+        b->release();
+    if (ctx->host_results)
+        (void)hipHostFree(ctx->host_results);
+    delete ctx;
+}
+
+const char *alp_status_str(int32_t status)
+{
+    switch (status) {
+    case ALP_OK: return "ALP_OK";
+    case ALP_EINVAL: return "ALP_EINVAL";
+    case ALP_ERANGE: return "ALP_ERANGE";
+    case ALP_ENOMEM: return "ALP_ENOMEM";
+    case ALP_EDEVICE: return "ALP_EDEVICE";
+    case ALP_INFEASIBLE: return "ALP_INFEASIBLE";
+    default: return "ALP_UNKNOWN";
+    }
+}
+
+const char *alp_last_error(void) { return g_last_error; }
+
+}  // extern "C"

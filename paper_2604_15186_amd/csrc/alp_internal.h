@@ -1,0 +1,79 @@
+// Internal declarations shared by the ABI layer (alp_api.hip) and the gfx950 kernels
+// (alp_kernels.hip).  Not installed; the public interface is include/alp.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "alp.h"
+
+namespace alp {
+
+// Share-unit value stored for an option that cannot be used at the query's target (not
+// deployable, weights do not fit, or the replica load exceeds saturation).  Real share units
+// are at most 64 * 16 * 16 = 16384 per LLM and 131072 per candidate, budgets are clamped
+// below the sentinel, so any candidate containing such an option fails the budget test.
+constexpr uint32_t kSentinelUnits = 1u << 24;
+constexpr uint32_t kCapacityMax = kSentinelUnits - 1;
+constexpr uint32_t kNoLatency = 0xFFFFFFFFu;
+
+// Search-space shape passed by value to kernels.
+struct SpaceDev {
+    uint32_t M, n_tp, n_fq, D, K, Q, O;
+    uint32_t tp[ALP_MAX_TP];
+    uint32_t fq[ALP_MAX_FRAC];
+};
+
+// Device copies of the profile tables of all instances (layouts as in alp_load_profiles).
+struct TablesDev {
+    const uint64_t *W;
+    const uint32_t *n;
+    const uint32_t *p;
+    const uint8_t *allowed;
+    const uint32_t *rate;
+    const uint32_t *lat;
+    uint64_t H;
+};
+
+// Per-item query: device arrays for batches, or by-value scalars for a single query.
+struct QueryDev {
+    const uint32_t *inst;       // instance of item i, or nullptr -> inst1
+    const uint32_t *capacity;   // share-unit capacity Q*G of item i (clamped), or nullptr -> cap1
+    const uint32_t *lambda;     // target rate of item i, or nullptr -> lambda1
+    uint32_t inst1, cap1, lambda1;
+};
+
+// Per-block winner of a scan: lexicographic (L, x) minimum; L = kNoLatency if none.
+struct Winner {
+    uint32_t L;
+    uint32_t pad;
+    uint64_t x;
+};
+
+// Launch geometry of one scan.
+struct ScanGeometry {
+    uint32_t variant;          // 1: lane-per-last-option, 2: thread-per-candidate
+    uint32_t threads;          // per block
+    uint32_t blocks_per_item;
+    uint64_t rows;             // variant 1: rows of O prefixes per item
+    uint64_t rows_per_wave;    // variant 1
+    uint64_t per_thread;       // variant 2: candidates per thread
+    uint32_t slots;            // variant 1: options of the last LLM per lane (1, 2, 4, 8)
+};
+
+hipError_t launch_option_terms(const SpaceDev &sp, const TablesDev &tb, const QueryDev &q,
+                               uint32_t count, uint2 *rec, uint2 *ext, hipStream_t st);
+hipError_t launch_scan(const SpaceDev &sp, const QueryDev &q, uint32_t count, const uint2 *rec,
+                       const ScanGeometry &g, Winner *winners, hipStream_t st);
+hipError_t launch_final(const SpaceDev &sp, uint32_t count, uint32_t blocks_per_item,
+                        const Winner *winners, const uint2 *ext, alp_result_t *out,
+                        hipStream_t st);
+hipError_t launch_eval(const SpaceDev &sp, uint32_t capacity, const uint2 *rec, const uint2 *ext,
+                       const uint64_t *idx, uint64_t count, alp_eval_t *out, hipStream_t st);
+hipError_t launch_tmax(const SpaceDev &sp, const QueryDev &q, uint32_t count, const uint2 *ext,
+                       uint32_t *out, hipStream_t st);
+
+// Resident blocks per CU of the scan kernels at a given block size (occupancy query).
+int scan_blocks_per_cu(uint32_t variant, uint32_t slots, uint32_t threads, const SpaceDev &sp);
+
+}  // namespace alp

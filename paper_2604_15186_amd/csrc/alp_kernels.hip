@@ -1,0 +1,587 @@
+// gfx950 kernels of the ALP allocation search (Scepsy, arXiv 2604.15186, Sections 4-5).
+//
+// Pipeline of one search (or a batch of independent searches, one "item" each):
+//   1. option_terms_kernel: per (item, LLM m, option o) the Eq. 1 contribution c and the share
+//      units u (replaced by a sentinel when the option is unusable at the target), plus the
+//      Eq. 2 normalised throughput tau and validity flags for result decoding.
+//   2. scan_lane_kernel<S> (or scan_flat_kernel): every candidate x = (o_0 .. o_{M-1}) is
+//      evaluated -- L_w = sum c, feasible iff sum u <= Q*G -- and the lexicographic (L_w, x)
+//      minimum is reduced per wave, per block, and written as one 16-byte winner per block.
+//   3. final_kernel: minimum over an item's block winners; decodes the winning index and
+//      recomputes T_w (Eq. 2) and the share units from the per-option records.
+// Everything is integer; results are bit-identical for every launch geometry.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "alp_internal.h"
+
+namespace alp {
+
+namespace {
+
+constexpr uint32_t kMaxOuter = ALP_MAX_LLMS - 2;   // digits above the last two LLMs
+
+__device__ __forceinline__ bool lex_less(uint32_t aL, uint64_t ax, uint32_t bL, uint64_t bx)
+{
+    return aL < bL || (aL == bL && ax < bx);
+}
+
+// Wave-wide lexicographic minimum of (L, x); every lane ends with the result.
+__device__ __forceinline__ void wave_min(uint32_t &L, uint64_t &x)
+{
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        uint32_t oL = __shfl_xor(L, off, 64);
+        uint64_t ox = __shfl_xor((unsigned long long)x, off, 64);
+        if (lex_less(oL, ox, L, x)) {
+            L = oL;
+            x = ox;
+        }
+    }
+}
+
+// Block-wide minimum; thread 0 writes the block's winner.
+__device__ __forceinline__ void block_min_store(uint32_t L, uint64_t x, Winner *dst)
+{
+    __shared__ uint32_t sL[16];
+    __shared__ uint64_t sx[16];
+    wave_min(L, x);
+    const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    if (lane == 0) {
+        sL[wave] = L;
+        sx[wave] = x;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (uint32_t w = 1; w < nw; ++w)
+            if (lex_less(sL[w], sx[w], L, x)) {
+                L = sL[w];
+                x = sx[w];
+            }
+        Winner r;
+        r.L = L;
+        r.pad = 0;
+        r.x = x;
+        *dst = r;
+    }
+}
+
+// Workgroups are dispatched to the 8 XCDs round-robin; renumber them so that consecutive
+// logical blocks (the blocks of one item, which read the same few-KiB option table) share an
+// XCD and its L2.  A bijection on [0, nblocks).
+__device__ __forceinline__ uint32_t xcd_logical_block(uint32_t b, uint32_t nblocks)
+{
+    const uint32_t per = nblocks >> 3;
+    if (b >= (per << 3))
+        return b;
+    return (b & 7u) * per + (b >> 3);
+}
+
+__device__ __forceinline__ uint32_t query_value(const uint32_t *arr, uint32_t single, uint32_t i)
+{
+    return arr ? arr[i] : single;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------------------------
+// 1. Per-option terms.  One thread per (item, m, o).
+//    rec[item][m][o] = (c, usable ? u : sentinel), c = 0 when unusable
+//    ext[item][m][o] = (tau, u | ok << 16 | thr_ok << 17)
+__global__ void __launch_bounds__(256)
+option_terms_kernel(SpaceDev sp, TablesDev tb, QueryDev q, uint32_t count, uint2 *__restrict__ rec,
+                    uint2 *__restrict__ ext)
+{
+    const uint64_t per_item = (uint64_t)sp.M * sp.O;
+    const uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= per_item * count)
+        return;
+    const uint32_t item = (uint32_t)(t / per_item);
+    const uint32_t rem = (uint32_t)(t - (uint64_t)item * per_item);
+    const uint32_t m = rem / sp.O, o = rem - m * sp.O;
+    const uint32_t inst = query_value(q.inst, q.inst1, item);
+    const uint64_t lambda = query_value(q.lambda, q.lambda1, item);
+
+    const uint32_t d = o % sp.D + 1;
+    const uint32_t ij = o / sp.D;
+    const uint32_t j = ij % sp.n_fq, i = ij / sp.n_fq;
+    const uint64_t tp = sp.tp[i], fq = sp.fq[j];
+    const uint64_t lm = (uint64_t)inst * sp.M + m;
+    const uint64_t tab = (lm * sp.n_tp + i) * sp.n_fq + j;
+    const uint32_t *rate = tb.rate + tab * sp.K;
+    const uint32_t *lat = tb.lat + tab * sp.K;
+    const uint64_t n = tb.n[lm], p = tb.p[lm];
+
+    // Deployable and the weights, sharded over tp, fit the share fq/Q of one GPU's memory.
+    const bool ok = tb.allowed[tab] != 0 && tb.W[lm] * sp.Q <= tp * fq * tb.H;
+    // Eq. 2 term: d replicas of saturation throughput T, per workflow request.
+    const uint64_t T = rate[sp.K - 1];
+    uint64_t tau = 1000ull * d * T / n;
+    tau = tau > 0xFFFFFFFFull ? 0xFFFFFFFFull : tau;
+    // Each replica receives lambda * n / d (rounded up).
+    const uint64_t dd = 1000ull * d;
+    const uint64_t r = (lambda * n + dd - 1) / dd;
+    const bool thr = r <= T;
+    uint64_t c = 0;
+    if (thr) {
+        // Eq. 1 term: latency at the replica's load, scaled by n / p.
+        uint64_t ell = lat[0];
+        if (r > rate[0]) {
+            uint32_t k = 1;
+            while (r > rate[k])
+                ++k;
+            const uint64_t r0 = rate[k - 1], r1 = rate[k];
+            ell = ((uint64_t)lat[k - 1] * (r1 - r) + (uint64_t)lat[k] * (r - r0)) / (r1 - r0);
+        }
+        c = ell * n / p;
+    }
+    const uint32_t u = (uint32_t)(tp * fq * d);
+    const bool usable = ok && thr;
+    rec[t] = make_uint2(usable ? (uint32_t)c : 0u, usable ? u : kSentinelUnits);
+    ext[t] = make_uint2((uint32_t)tau, u | ((uint32_t)ok << 16) | ((uint32_t)thr << 17));
+}
+
+// ---------------------------------------------------------------------------------------------
+// 2a. Lane-per-last-option scan.
+//
+// A wave walks "rows": fixed digits o_0..o_{M-3} (their c and u sums are wave-uniform and live
+// in SGPRs) and every o_{M-2} in turn (one uniform 8-byte record per step, fetched with scalar
+// loads).  Lane l owns the last LLM's options l, l+64, ... (S of them, records held in VGPRs for
+// the whole kernel).  For a prefix with latency sum pc and remaining share units slack, the
+// lane's candidate is feasible iff u_last <= slack and has latency pc + c_last; because c_last
+// is constant per lane, "better than the lane's best so far" is pc < best_pc.  Per candidate:
+// two compares, one mask AND (scalar), two selects.  Within a row a lane scans prefixes in
+// increasing index order and only a strictly smaller pc replaces its best, so ties keep the
+// lowest index; rows and lanes are merged lexicographically on (L, x).
+template <int S>
+__global__ void __launch_bounds__(1024)
+scan_lane_kernel(const uint2 *__restrict__ rec, QueryDev q, uint32_t M, uint32_t O,
+                 uint64_t rows, uint64_t rows_per_wave, uint32_t blocks_per_item,
+                 uint32_t nblocks, Winner *__restrict__ winners)
+{
+    const uint32_t lb = xcd_logical_block(blockIdx.x, nblocks);
+    const uint32_t item = lb / blocks_per_item;
+    const uint32_t sub = lb - item * blocks_per_item;
+    const int32_t capacity = (int32_t)query_value(q.capacity, q.cap1, item);
+    const uint2 *R = rec + (uint64_t)item * M * O;
+    const uint32_t lane = threadIdx.x & 63;
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const uint32_t wpb = blockDim.x >> 6;
+
+    // The last LLM's options owned by this lane.
+    const uint2 *last = R + (uint64_t)(M - 1) * O;
+    uint32_t c_last[S];
+    int32_t u_last[S];
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+        const uint32_t o = lane + 64u * s;
+        if (o < O) {
+            const uint2 v = last[o];
+            c_last[s] = v.x;
+            u_last[s] = (int32_t)v.y;
+        } else {
+            c_last[s] = 0;
+            u_last[s] = 0x7FFFFFFF;          // never within any slack
+        }
+    }
+
+    // The LLM before the last one varies inside a row; with a single LLM there is no prefix:
+    // one row of one empty prefix (inner record (0, 0)).
+    const bool has_inner = M >= 2;
+    const uint2 *inner = R + (uint64_t)(has_inner ? M - 2 : 0) * O;
+    const uint32_t n_inner = has_inner ? O : 1;
+    const uint32_t n_outer = M >= 2 ? M - 2 : 0;
+
+    uint32_t bestL = kNoLatency;
+    uint64_t bestX = ~0ull;
+
+    const uint64_t gw = (uint64_t)sub * wpb + wave;
+    const uint64_t r_begin = gw * rows_per_wave;
+    const uint64_t r_end = r_begin + rows_per_wave < rows ? r_begin + rows_per_wave : rows;
+
+    if (r_begin < r_end) {
+        uint32_t digit[kMaxOuter];
+        {
+            uint64_t rr = r_begin;
+#pragma unroll
+            for (int k = (int)kMaxOuter - 1; k >= 0; --k) {
+                digit[k] = 0;
+                if ((uint32_t)k < n_outer) {
+                    digit[k] = (uint32_t)(rr % O);
+                    rr /= O;
+                }
+            }
+        }
+        for (uint64_t r = r_begin; r < r_end; ++r) {
+            uint32_t oc = 0;
+            int32_t ou = 0;
+#pragma unroll
+            for (uint32_t k = 0; k < kMaxOuter; ++k) {
+                if (k < n_outer) {
+                    const uint2 v = R[(uint64_t)k * O + digit[k]];
+                    oc += v.x;
+                    ou += (int32_t)v.y;
+                }
+            }
+            const int32_t base_slack = capacity - ou;
+
+            uint32_t best_pc[S], best_j[S];
+#pragma unroll
+            for (int s = 0; s < S; ++s) {
+                best_pc[s] = kNoLatency;
+                best_j[s] = 0;
+            }
+            auto step = [&](const uint2 v, const uint32_t jj) {
+                const uint32_t pc = oc + v.x;
+                const int32_t slack = base_slack - (int32_t)v.y;
+#pragma unroll
+                for (int s = 0; s < S; ++s) {
+                    const bool take = (u_last[s] <= slack) & (pc < best_pc[s]);
+                    best_pc[s] = take ? pc : best_pc[s];
+                    best_j[s] = take ? jj : best_j[s];
+                }
+            };
+            if (has_inner) {
+                uint32_t jb = 0;
+                for (; jb + 8 <= n_inner; jb += 8) {
+#pragma unroll
+                    for (uint32_t t = 0; t < 8; ++t)
+                        step(inner[jb + t], jb + t);
+                }
+                for (; jb < n_inner; ++jb)
+                    step(inner[jb], jb);
+            } else {
+                step(make_uint2(0u, 0u), 0u);
+            }
+
+            // Merge the row into the lane's running best.
+#pragma unroll
+            for (int s = 0; s < S; ++s) {
+                if (best_pc[s] != kNoLatency) {
+                    const uint32_t L = best_pc[s] + c_last[s];
+                    const uint64_t x = ((r * n_inner + best_j[s]) * (uint64_t)O) + lane + 64u * s;
+                    if (lex_less(L, x, bestL, bestX)) {
+                        bestL = L;
+                        bestX = x;
+                    }
+                }
+            }
+            // Next row: odometer on the outer digits (last outer digit fastest).
+            bool carry = true;
+#pragma unroll
+            for (int k = (int)kMaxOuter - 1; k >= 0; --k) {
+                if ((uint32_t)k < n_outer && carry) {
+                    ++digit[k];
+                    if (digit[k] == O)
+                        digit[k] = 0;
+                    else
+                        carry = false;
+                }
+            }
+        }
+    }
+    block_min_store(bestL, bestX, &winners[lb]);
+}
+
+// ---------------------------------------------------------------------------------------------
+// 2b. Thread-per-candidate scan (cross-check variant and fallback): each thread evaluates a
+// contiguous index range from the LDS-staged option table, decoding the start index once and
+// counting the digits up from there.
+__global__ void __launch_bounds__(1024)
+scan_flat_kernel(const uint2 *__restrict__ rec, QueryDev q, uint32_t M, uint32_t O, uint64_t N,
+                 uint64_t per_thread, uint32_t blocks_per_item, uint32_t nblocks,
+                 Winner *__restrict__ winners)
+{
+    extern __shared__ uint2 table[];
+    const uint32_t lb = xcd_logical_block(blockIdx.x, nblocks);
+    const uint32_t item = lb / blocks_per_item;
+    const uint32_t sub = lb - item * blocks_per_item;
+    const uint32_t capacity = query_value(q.capacity, q.cap1, item);
+    const uint2 *R = rec + (uint64_t)item * M * O;
+    for (uint32_t a = threadIdx.x; a < M * O; a += blockDim.x)
+        table[a] = R[a];
+    __syncthreads();
+
+    uint32_t bestL = kNoLatency;
+    uint64_t bestX = ~0ull;
+    const uint64_t t = (uint64_t)sub * blockDim.x + threadIdx.x;
+    const uint64_t x0 = t * per_thread;
+    const uint64_t x1 = x0 + per_thread < N ? x0 + per_thread : N;
+    if (x0 < x1) {
+        uint32_t digit[ALP_MAX_LLMS];
+        uint64_t rr = x0;
+#pragma unroll
+        for (int m = ALP_MAX_LLMS - 1; m >= 0; --m) {
+            digit[m] = 0;
+            if ((uint32_t)m < M) {
+                digit[m] = (uint32_t)(rr % O);
+                rr /= O;
+            }
+        }
+        for (uint64_t x = x0; x < x1; ++x) {
+            uint32_t L = 0, U = 0;
+#pragma unroll
+            for (uint32_t m = 0; m < ALP_MAX_LLMS; ++m) {
+                if (m < M) {
+                    const uint2 v = table[m * O + digit[m]];
+                    L += v.x;
+                    U += v.y;
+                }
+            }
+            if (U <= capacity && L < bestL) {
+                bestL = L;
+                bestX = x;
+            }
+            bool carry = true;
+#pragma unroll
+            for (int m = ALP_MAX_LLMS - 1; m >= 0; --m) {
+                if ((uint32_t)m < M && carry) {
+                    ++digit[m];
+                    if (digit[m] == O)
+                        digit[m] = 0;
+                    else
+                        carry = false;
+                }
+            }
+        }
+    }
+    block_min_store(bestL, bestX, &winners[lb]);
+}
+
+// ---------------------------------------------------------------------------------------------
+// 3. Final reduction and result decoding, one 64-thread block per item.
+__global__ void __launch_bounds__(64)
+final_kernel(SpaceDev sp, uint32_t blocks_per_item, const Winner *__restrict__ winners,
+             const uint2 *__restrict__ ext, alp_result_t *__restrict__ out)
+{
+    const uint32_t item = blockIdx.x;
+    uint32_t L = kNoLatency;
+    uint64_t x = ~0ull;
+    for (uint32_t k = threadIdx.x; k < blocks_per_item; k += 64) {
+        const Winner w = winners[(uint64_t)item * blocks_per_item + k];
+        if (lex_less(w.L, w.x, L, x)) {
+            L = w.L;
+            x = w.x;
+        }
+    }
+    wave_min(L, x);
+    if (threadIdx.x != 0)
+        return;
+    alp_result_t res;
+    uint8_t *raw = reinterpret_cast<uint8_t *>(&res);
+    for (uint32_t b = 0; b < sizeof(res); ++b)
+        raw[b] = 0;
+    if (L == kNoLatency) {
+        res.index = ALP_NO_INDEX;
+        res.status = ALP_INFEASIBLE;
+    } else {
+        res.index = x;
+        res.latency_us = L;
+        res.status = ALP_OK;
+        const uint2 *E = ext + (uint64_t)item * sp.M * sp.O;
+        uint64_t rr = x;
+        uint32_t T = 0xFFFFFFFFu, U = 0;
+        for (int m = (int)sp.M - 1; m >= 0; --m) {
+            const uint32_t o = (uint32_t)(rr % sp.O);
+            rr /= sp.O;
+            const uint2 e = E[(uint64_t)m * sp.O + o];
+            T = e.x < T ? e.x : T;                      // Eq. 2: minimum over LLMs
+            U += e.y & 0xFFFFu;
+            const uint32_t ij = o / sp.D;
+            res.tp[m] = (uint8_t)sp.tp[ij / sp.n_fq];
+            res.frac_units[m] = (uint8_t)sp.fq[ij % sp.n_fq];
+            res.replicas[m] = (uint8_t)(o % sp.D + 1);
+        }
+        res.throughput_milli = T;
+        res.gpu_units = U;
+    }
+    out[item] = res;
+}
+
+// ---------------------------------------------------------------------------------------------
+// Evaluation of listed candidates (one thread each).
+__global__ void __launch_bounds__(256)
+eval_kernel(SpaceDev sp, uint32_t capacity, const uint2 *__restrict__ rec,
+            const uint2 *__restrict__ ext, const uint64_t *__restrict__ idx, uint64_t count,
+            alp_eval_t *__restrict__ out)
+{
+    const uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= count)
+        return;
+    uint64_t rr = idx[t];
+    bool ok = true, thr = true;
+    uint32_t L = 0, T = 0xFFFFFFFFu, U = 0;
+    for (int m = (int)sp.M - 1; m >= 0; --m) {
+        const uint32_t o = (uint32_t)(rr % sp.O);
+        rr /= sp.O;
+        const uint64_t a = (uint64_t)m * sp.O + o;
+        const uint2 e = ext[a];
+        ok &= ((e.y >> 16) & 1u) != 0;
+        thr &= ((e.y >> 17) & 1u) != 0;
+        U += e.y & 0xFFFFu;
+        T = e.x < T ? e.x : T;
+        L += rec[a].x;
+    }
+    alp_eval_t r;
+    r.flags = (uint32_t)ok | ((uint32_t)thr << 1) | ((uint32_t)(U <= capacity) << 2);
+    r.latency_us = (ok && thr) ? L : kNoLatency;
+    r.throughput_milli = ok ? T : 0u;
+    r.gpu_units = U;
+    out[t] = r;
+}
+
+// ---------------------------------------------------------------------------------------------
+// Largest reachable T_w within the budget, one block per item.  T_w >= t is reachable iff the
+// cheapest options with tau >= t of all LLMs together fit; the maximum is one of the taus.
+__global__ void __launch_bounds__(256)
+tmax_kernel(SpaceDev sp, QueryDev q, const uint2 *__restrict__ ext, uint32_t *__restrict__ out)
+{
+    extern __shared__ uint2 e[];
+    __shared__ uint32_t red[256];
+    const uint32_t item = blockIdx.x;
+    const uint32_t MO = sp.M * sp.O;
+    const uint2 *E = ext + (uint64_t)item * MO;
+    for (uint32_t a = threadIdx.x; a < MO; a += blockDim.x)
+        e[a] = E[a];
+    __syncthreads();
+    const uint64_t capacity = (uint64_t)query_value(q.capacity, q.cap1, item);
+    uint32_t best = 0;
+    for (uint32_t a = threadIdx.x; a < MO; a += blockDim.x) {
+        if (!((e[a].y >> 16) & 1u))
+            continue;
+        const uint32_t t = e[a].x;
+        if (t <= best)
+            continue;
+        uint64_t need = 0;
+        bool reachable = true;
+        for (uint32_t m = 0; m < sp.M && reachable; ++m) {
+            uint32_t cheapest = 0xFFFFFFFFu;
+            for (uint32_t o = 0; o < sp.O; ++o) {
+                const uint2 v = e[m * sp.O + o];
+                const uint32_t u = v.y & 0xFFFFu;
+                if (((v.y >> 16) & 1u) && v.x >= t && u < cheapest)
+                    cheapest = u;
+            }
+            if (cheapest == 0xFFFFFFFFu)
+                reachable = false;
+            else
+                need += cheapest;
+        }
+        if (reachable && need <= capacity)
+            best = t;
+    }
+    red[threadIdx.x] = best;
+    __syncthreads();
+    for (uint32_t s = blockDim.x / 2; s > 0; s >>= 1) {
+        if (threadIdx.x < s)
+            red[threadIdx.x] = red[threadIdx.x] > red[threadIdx.x + s] ? red[threadIdx.x]
+                                                                        : red[threadIdx.x + s];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0)
+        out[item] = red[0];
+}
+
+// ---------------------------------------------------------------------------------------------
+// Launchers.
+
+hipError_t launch_option_terms(const SpaceDev &sp, const TablesDev &tb, const QueryDev &q,
+                               uint32_t count, uint2 *rec, uint2 *ext, hipStream_t st)
+{
+    const uint64_t total = (uint64_t)count * sp.M * sp.O;
+    if (total == 0)
+        return hipSuccess;
+    const uint32_t blocks = (uint32_t)((total + 255) / 256);
+    hipLaunchKernelGGL(option_terms_kernel, dim3(blocks), dim3(256), 0, st, sp, tb, q, count, rec,
+                       ext);
+    return hipGetLastError();
+}
+
+template <int S>
+static hipError_t launch_lane(const SpaceDev &sp, const QueryDev &q, uint32_t count,
+                              const uint2 *rec, const ScanGeometry &g, Winner *winners,
+                              hipStream_t st)
+{
+    const uint32_t nblocks = count * g.blocks_per_item;
+    hipLaunchKernelGGL(HIP_KERNEL_NAME(scan_lane_kernel<S>), dim3(nblocks), dim3(g.threads), 0, st,
+                       rec, q, sp.M, sp.O, g.rows, g.rows_per_wave, g.blocks_per_item, nblocks,
+                       winners);
+    return hipGetLastError();
+}
+
+hipError_t launch_scan(const SpaceDev &sp, const QueryDev &q, uint32_t count, const uint2 *rec,
+                       const ScanGeometry &g, Winner *winners, hipStream_t st)
+{
+    if (count == 0)
+        return hipSuccess;
+    if (g.variant == 2) {
+        uint64_t N = 1;
+        for (uint32_t m = 0; m < sp.M; ++m)
+            N *= sp.O;
+        const uint32_t nblocks = count * g.blocks_per_item;
+        const size_t lds = (size_t)sp.M * sp.O * sizeof(uint2);
+        hipLaunchKernelGGL(scan_flat_kernel, dim3(nblocks), dim3(g.threads), lds, st, rec, q, sp.M,
+                           sp.O, N, g.per_thread, g.blocks_per_item, nblocks, winners);
+        return hipGetLastError();
+    }
+    switch (g.slots) {
+    case 1: return launch_lane<1>(sp, q, count, rec, g, winners, st);
+    case 2: return launch_lane<2>(sp, q, count, rec, g, winners, st);
+    case 4: return launch_lane<4>(sp, q, count, rec, g, winners, st);
+    case 8: return launch_lane<8>(sp, q, count, rec, g, winners, st);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_final(const SpaceDev &sp, uint32_t count, uint32_t blocks_per_item,
+                        const Winner *winners, const uint2 *ext, alp_result_t *out,
+                        hipStream_t st)
+{
+    if (count == 0)
+        return hipSuccess;
+    hipLaunchKernelGGL(final_kernel, dim3(count), dim3(64), 0, st, sp, blocks_per_item, winners,
+                       ext, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_eval(const SpaceDev &sp, uint32_t capacity, const uint2 *rec, const uint2 *ext,
+                       const uint64_t *idx, uint64_t count, alp_eval_t *out, hipStream_t st)
+{
+    if (count == 0)
+        return hipSuccess;
+    const uint64_t blocks = (count + 255) / 256;
+    hipLaunchKernelGGL(eval_kernel, dim3((uint32_t)blocks), dim3(256), 0, st, sp, capacity, rec,
+                       ext, idx, count, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_tmax(const SpaceDev &sp, const QueryDev &q, uint32_t count, const uint2 *ext,
+                       uint32_t *out, hipStream_t st)
+{
+    if (count == 0)
+        return hipSuccess;
+    const size_t lds = (size_t)sp.M * sp.O * sizeof(uint2);
+    hipLaunchKernelGGL(tmax_kernel, dim3(count), dim3(256), lds, st, sp, q, ext, out);
+    return hipGetLastError();
+}
+
+int scan_blocks_per_cu(uint32_t variant, uint32_t slots, uint32_t threads, const SpaceDev &sp)
+{
+    int n = 0;
+    hipError_t e = hipErrorInvalidValue;
+    if (variant == 2) {
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_flat_kernel, (int)threads,
+                                                         (size_t)sp.M * sp.O * sizeof(uint2));
+    } else {
+        switch (slots) {
+        case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_lane_kernel<1>, (int)threads, 0); break;
+        case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_lane_kernel<2>, (int)threads, 0); break;
+        case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_lane_kernel<4>, (int)threads, 0); break;
+        case 8: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_lane_kernel<8>, (int)threads, 0); break;
+        default: break;
+        }
+    }
+    return (e == hipSuccess && n > 0) ? n : 1;
+}
+
+}  // namespace alp

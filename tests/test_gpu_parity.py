@@ -1,0 +1,245 @@
+"""Parity of the HIP search (through the C ABI) with the oracle.  Needs an MI355X.
+
+Integer results must be bit-identical: winning index, L_w, T_w, share units, per-LLM choices,
+per-candidate evaluations, maximum throughput.  Full-size configurations compare against the
+results ``golden/make_golden.py`` wrote with the oracle; small spaces compare against the oracle
+directly.  Launch geometry and kernel variant must not change any result.
+"""
+from __future__ import annotations
+
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from workloads import make_batch, make_custom, sample_indices, target_from_tmax
+
+from hand_cases import case_batch, load_cases
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+NONE32 = (1 << 32) - 1
+
+
+@pytest.fixture(scope="module")
+def alp():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2604_15186_amd import alp as binding
+    binding.lib()
+    return binding
+
+
+def golden(cfg):
+    with open(os.path.join(GOLDEN, f"cfg{cfg}_argmin.json")) as f:
+        return json.load(f)
+
+
+def _decode_expect(batch, i, x):
+    """Per-LLM (tp, share, replicas) of candidate x, from the space description alone."""
+    sp = batch["space"]
+    D, nfq, O, M = int(sp["D"]), len(sp["fq"]), \
+        len(sp["tp"]) * len(sp["fq"]) * int(sp["D"]), int(sp["M"])
+    digits = []
+    for _ in range(M):
+        digits.append(x % O)
+        x //= O
+    digits = digits[::-1]
+    tp = [int(sp["tp"][(o // D) // nfq]) for o in digits]
+    fq = [int(sp["fq"][(o // D) % nfq]) for o in digits]
+    d = [o % D + 1 for o in digits]
+    pad = [0] * (8 - M)
+    return tp + pad, fq + pad, d + pad
+
+
+def check_result(batch, i, res, x, L, T=None, U=None):
+    r = {k: int(res[k]) for k in ("index", "latency_us", "throughput_milli", "gpu_units", "status")}
+    if x is None:
+        assert r["status"] == 5 and r["index"] == (1 << 64) - 1, r
+        return
+    assert r["status"] == 0, r
+    assert (r["index"], r["latency_us"]) == (x, L), (r, x, L)
+    if T is not None:
+        assert (r["throughput_milli"], r["gpu_units"]) == (T, U), (r, T, U)
+    tp, fq, d = _decode_expect(batch, i, x)
+    assert [int(v) for v in res["tp"]] == tp
+    assert [int(v) for v in res["frac_units"]] == fq
+    assert [int(v) for v in res["replicas"]] == d
+
+
+def oracle_expect(batch, i, G, lam):
+    inst = oracle.Instance(batch, i)
+    a = oracle.argmin(inst, G, lam)
+    if a["x"] is None:
+        return None, None, None, None
+    ev = oracle.evaluate(inst, G, lam, a["x"])
+    return a["x"], a["L"], ev["T"], ev["U"]
+
+
+# --------------------------------------------------------------------------------------------
+CASES = load_cases()
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c["id"] for c in CASES])
+def test_hand_cases(alp, case):
+    b = case_batch(case)
+    with alp.Context(b) as ctx:
+        for variant in (1, 2):
+            ctx.set_launch(variant)
+            for q in case["queries"]:
+                res = ctx.search(0, q["G"], q["lambda"])
+                check_result(b, 0, res, q["x"], q.get("L"), q.get("T"), q.get("U"))
+        for t in case["tmax"]:
+            assert int(ctx.max_throughput([t["G"]])[0]) == t["T"]
+        for e in case["evals"]:
+            ev = ctx.eval_candidates(0, e["G"], e["lambda"], [e["x"]])[0]
+            want_L = NONE32 if e["L"] is None else e["L"]
+            assert (int(ev["flags"]), int(ev["latency_us"]), int(ev["throughput_milli"]),
+                    int(ev["gpu_units"])) == (e["flags"], want_L, e["T"], e["U"])
+
+
+def test_cfg0_all_instances_batch_and_single(alp):
+    """2-LLM workload, 1000 instances, full space: one batched call vs the oracle."""
+    b = make_batch(0, range(1000))
+    exp_tmax = np.asarray([oracle.tmax(oracle.Instance(b, i), int(b["G"][i])) for i in range(1000)])
+    lam = np.asarray([target_from_tmax(int(b["u_ppm"][i]), exp_tmax[i]) for i in range(1000)],
+                     dtype=np.uint32)
+    with alp.Context(b) as ctx:
+        assert np.array_equal(ctx.max_throughput(b["G"]), exp_tmax)
+        out = ctx.search_batch(b["G"], lam)
+        for i in range(1000):
+            x, L, T, U = oracle_expect(b, i, int(b["G"][i]), int(lam[i]))
+            check_result(b, i, out[i], x, L, T, U)
+        for i in (0, 1, 999):
+            check_result(b, i, ctx.search(i, int(b["G"][i]), int(lam[i])),
+                         *oracle_expect(b, i, int(b["G"][i]), int(lam[i])))
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_full_space_matches_golden(alp, cfg):
+    g = golden(cfg)
+    rows = g["results"]
+    b = make_batch(cfg, [r["inst"] for r in rows])
+    with alp.Context(b) as ctx:
+        tm = ctx.max_throughput([r["G"] for r in rows])
+        assert [int(v) for v in tm] == [r["tmax"] for r in rows]
+        for i, r in enumerate(rows):
+            res = ctx.search(i, r["G"], r["lambda"])
+            check_result(b, i, res, r["x"], r["L"], r["T"], r["U"])
+
+
+def test_cfg4_batch_matches_golden(alp):
+    """4,096 independent 3-LLM instances in one alp_search_batch call."""
+    g = golden(4)
+    rows = g["results"]
+    b = make_batch(4, [r["inst"] for r in rows])
+    with alp.Context(b) as ctx:
+        tm = ctx.max_throughput([r["G"] for r in rows])
+        assert [int(v) for v in tm] == [r["tmax"] for r in rows]
+        out = ctx.search_batch([r["G"] for r in rows], [r["lambda"] for r in rows])
+        bad = [i for i, r in enumerate(rows)
+               if (int(out[i]["index"]), int(out[i]["latency_us"]), int(out[i]["throughput_milli"]),
+                   int(out[i]["gpu_units"])) != (r["x"], r["L"], r["T"], r["U"])]
+        assert not bad, bad[:10]
+
+
+@pytest.mark.parametrize("cfg,count", [(2, 1_000_000), (3, 10_000_000)])
+def test_random_candidates_elementwise(alp, cfg, count):
+    """Sampled candidates of the full-size spaces, evaluated one by one by both sides."""
+    r = golden(cfg)["results"][0]
+    b = make_batch(cfg, [r["inst"]])
+    inst = oracle.Instance(b, 0)
+    xs = sample_indices(cfg, r["inst"], count, inst.N)
+    x = r["x"]
+    xs = np.concatenate([xs, np.asarray([x, x - 1, x + 1], dtype=np.uint64)])
+    want = oracle.evaluate_many(inst, r["G"], r["lambda"], xs)
+    with alp.Context(b) as ctx:
+        got = ctx.eval_candidates(0, r["G"], r["lambda"], xs)
+    want_L = np.where(want["L"] == (1 << 64) - 1, NONE32, want["L"]).astype(np.uint64)
+    assert np.array_equal(got["flags"], want["flags"])
+    assert np.array_equal(got["latency_us"].astype(np.uint64), want_L)
+    assert np.array_equal(got["throughput_milli"].astype(np.uint64), want["T"])
+    assert np.array_equal(got["gpu_units"].astype(np.uint64), want["U"])
+
+
+def test_launch_geometry_and_variant_do_not_change_results(alp):
+    g = golden(2)["results"][1]
+    b = make_batch(2, [g["inst"]])
+    with alp.Context(b) as ctx:
+        for variant, bpi, tpb in [(1, 0, 0), (1, 1, 64), (1, 7, 128), (1, 3000, 1024),
+                                  (2, 0, 0), (2, 5, 256), (0, 64, 512)]:
+            ctx.set_launch(variant, bpi, tpb)
+            res = ctx.search(0, g["G"], g["lambda"])
+            check_result(b, 0, res, g["x"], g["L"], g["T"], g["U"])
+        ctx.set_launch(0, 0, 0)
+        first = ctx.search(0, g["G"], g["lambda"])
+        for _ in range(3):
+            assert ctx.search(0, g["G"], g["lambda"]).tobytes() == first.tobytes()
+
+
+SHAPES = [
+    # seed, M, tp, fq, D, K, G, count   (O = |tp|*|fq|*D; 1..8 options per lane)
+    (31, 1, (1, 2, 4, 8), (1, 2, 3, 4), 8, 8, 16, 3),      # M = 1, O = 128
+    (32, 2, (1, 2), (2, 4), 3, 4, 6, 4),                   # O = 12 (ragged, one lane slot)
+    (33, 3, (1, 2, 4), (1, 2, 4), 7, 3, 12, 3),            # O = 63
+    (34, 3, (1, 2, 4, 8), (1, 2, 3, 4), 5, 1, 20, 2),      # O = 80, K = 1
+    (35, 2, (1, 2, 4, 8), (1, 2, 3, 4), 13, 8, 24, 2),     # O = 208 (four slots)
+    (36, 2, (1, 2, 4, 8, 16), (1, 2, 4, 8), 16, 6, 40, 2),  # O = 320 (eight slots), Q = 8
+    (37, 4, (1, 2), (4,), 4, 2, 8, 3),                      # O = 8, M = 4
+    (38, 6, (1, 2), (2, 4), 2, 2, 10, 1),                   # O = 8, M = 6 (three outer digits)
+]
+
+
+@pytest.mark.parametrize("spec", SHAPES, ids=[f"seed{s[0]}" for s in SHAPES])
+def test_ragged_and_degenerate_spaces(alp, spec):
+    seed, M, tps, fqs, D, K, G, count = spec
+    Q = 8 if max(fqs) > 4 else 4
+    b = make_custom(seed, M, tps, fqs, D, K, G, count=count, frac_den=Q, deny_prob=0.1,
+                    param_range=(0.5e9, 400e9))
+    with alp.Context(b) as ctx:
+        tms = ctx.max_throughput([G] * count)
+        for i in range(count):
+            inst = oracle.Instance(b, i)
+            assert int(tms[i]) == oracle.tmax(inst, G)
+            t = int(tms[i])
+            for lam in sorted({1, target_from_tmax(int(b["u_ppm"][i]), t), t, t + 1}):
+                for g in (0, G // 2, G):
+                    want = oracle_expect(b, i, g, lam)
+                    for variant in (1, 2):
+                        ctx.set_launch(variant)
+                        check_result(b, i, ctx.search(i, g, lam), *want)
+            ctx.set_launch(0)
+            xs = np.arange(min(inst.N, 50_000), dtype=np.uint64)
+            lam = target_from_tmax(int(b["u_ppm"][i]), t)
+            want = oracle.evaluate_many(inst, G, lam, xs)
+            got = ctx.eval_candidates(i, G, lam, xs)
+            assert np.array_equal(got["flags"], want["flags"])
+            assert np.array_equal(got["latency_us"].astype(np.uint64),
+                                  np.where(want["L"] == (1 << 64) - 1, NONE32, want["L"]))
+
+
+def test_batch_edge_cases(alp):
+    b = make_batch(1, range(3))
+    with alp.Context(b) as ctx:
+        assert len(ctx.search_batch([], [])) == 0
+        G = [16, 0, 16]
+        t = ctx.max_throughput(G)
+        assert int(t[1]) == 0
+        lam = [int(t[0]), 1, int(t[2]) + 1]
+        out = ctx.search_batch(G, lam, instances=[0, 1, 2])
+        assert int(out[0]["status"]) == 0
+        assert int(out[1]["status"]) == 5 and int(out[2]["status"]) == 5
+        inst = oracle.Instance(b, 0)
+        a = oracle.argmin(inst, 16, int(t[0]))
+        assert int(out[0]["index"]) == a["x"]
+        # repeated instance ids in one batch
+        out = ctx.search_batch([16, 16], [lam[0], lam[0]], instances=[0, 0])
+        assert out[0].tobytes() == out[1].tobytes()
+        with pytest.raises(alp.AlpError):
+            ctx.search(3, 16, 1)
+        with pytest.raises(alp.AlpError):
+            ctx.eval_candidates(0, 16, 1, [ctx.num_candidates])
