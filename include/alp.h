@@ -155,8 +155,8 @@ int32_t alp_eval_candidates(alp_ctx *ctx, uint32_t instance, uint32_t gpu_budget
                             uint32_t target_milli, const uint64_t *indices, uint64_t count,
                             alp_eval_t *out);
 
-/* Launch choices, for tests and tuning.  variant: 0 automatic, 1 lane-per-last-option kernel,
- * 2 thread-per-candidate kernel.  blocks_per_item and threads_per_block (a multiple of 64, at
+/* Launch choices, for tests and tuning.  variant: 0 automatic (= 1), 1 row-minimum scan
+ * (default), 2 thread-per-candidate scan, 3 exact-tracking lane scan.  blocks_per_item and threads_per_block (a multiple of 64, at
  * most 1024): 0 = automatic.  Results do not depend on these choices. */
 int32_t alp_set_launch(alp_ctx *ctx, uint32_t variant, uint32_t blocks_per_item,
                        uint32_t threads_per_block);

@@ -99,7 +99,7 @@ struct alp_ctx {
     DevBuf tables;                 // W | n | p | allowed | rate | lat
     alp::TablesDev tdev{};
 
-    DevBuf q_inst, q_cap, q_lambda, rec, ext, winners, results, idx, evals, tmax;
+    DevBuf q_inst, q_cap, q_lambda, rec, ext, inner, winners, results, idx, evals, tmax;
     alp_result_t *host_results = nullptr;   // pinned staging
     size_t host_results_cap = 0;
 
@@ -234,7 +234,7 @@ alp::ScanGeometry plan_scan(const alp_ctx *c, uint32_t count)
         (uint64_t)(c->num_cus > 0 ? c->num_cus : 256) *
         (uint64_t)alp::scan_blocks_per_cu(g.variant, g.slots, g.threads, sp);
     const uint64_t want = count ? ceil_div(resident, count) : 1;
-    if (g.variant == 1) {
+    if (g.variant != 2) {
         g.rows = 1;
         for (uint32_t m = 2; m < sp.M; ++m)
             g.rows *= sp.O;
@@ -293,6 +293,8 @@ int32_t run_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count)
         return hip_fail(e, "hipMalloc(rec)");
     if ((e = c->ext.ensure(items_bytes)) != hipSuccess)
         return hip_fail(e, "hipMalloc(ext)");
+    if ((e = c->inner.ensure((uint64_t)count * sp.O * sizeof(uint2))) != hipSuccess)
+        return hip_fail(e, "hipMalloc(inner)");
     if ((e = c->winners.ensure(nwin * sizeof(alp::Winner))) != hipSuccess)
         return hip_fail(e, "hipMalloc(winners)");
     if ((e = c->results.ensure((uint64_t)count * sizeof(alp_result_t))) != hipSuccess)
@@ -301,16 +303,16 @@ int32_t run_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count)
     if (st != ALP_OK)
         return st;
 
-    uint2 *rec = (uint2 *)c->rec.ptr, *ext = (uint2 *)c->ext.ptr;
+    uint2 *rec = (uint2 *)c->rec.ptr, *ext = (uint2 *)c->ext.ptr, *inner = (uint2 *)c->inner.ptr;
     alp::Winner *win = (alp::Winner *)c->winners.ptr;
     alp_result_t *res = (alp_result_t *)c->results.ptr;
     if (c->timing && (e = hipEventRecord(c->ev[0], c->stream)) != hipSuccess)
         return hip_fail(e, "hipEventRecord");
-    if ((e = alp::launch_option_terms(sp, c->tdev, q, count, rec, ext, c->stream)) != hipSuccess)
+    if ((e = alp::launch_option_terms(sp, c->tdev, q, count, rec, ext, inner, c->stream)) != hipSuccess)
         return hip_fail(e, "option_terms launch");
     if (c->timing && (e = hipEventRecord(c->ev[1], c->stream)) != hipSuccess)
         return hip_fail(e, "hipEventRecord");
-    if ((e = alp::launch_scan(sp, q, count, rec, g, win, c->stream)) != hipSuccess)
+    if ((e = alp::launch_scan(sp, q, count, rec, inner, g, win, c->stream)) != hipSuccess)
         return hip_fail(e, "scan launch");
     if (c->timing && (e = hipEventRecord(c->ev[2], c->stream)) != hipSuccess)
         return hip_fail(e, "hipEventRecord");
@@ -546,7 +548,7 @@ int32_t alp_max_throughput(alp_ctx *ctx, uint32_t count, const uint32_t *instanc
     q.capacity = (const uint32_t *)ctx->q_cap.ptr;
     q.lambda = (const uint32_t *)ctx->q_lambda.ptr;
     if ((e = alp::launch_option_terms(ctx->sp, ctx->tdev, q, count, (uint2 *)ctx->rec.ptr,
-                                      (uint2 *)ctx->ext.ptr, ctx->stream)) != hipSuccess)
+                                      (uint2 *)ctx->ext.ptr, nullptr, ctx->stream)) != hipSuccess)
         return hip_fail(e, "option_terms launch");
     if ((e = alp::launch_tmax(ctx->sp, q, count, (const uint2 *)ctx->ext.ptr,
                               (uint32_t *)ctx->tmax.ptr, ctx->stream)) != hipSuccess)
@@ -595,7 +597,7 @@ int32_t alp_eval_candidates(alp_ctx *ctx, uint32_t instance, uint32_t gpu_budget
                             ctx->stream)) != hipSuccess)
         return hip_fail(e, "copy indices");
     if ((e = alp::launch_option_terms(ctx->sp, ctx->tdev, q, 1, (uint2 *)ctx->rec.ptr,
-                                      (uint2 *)ctx->ext.ptr, ctx->stream)) != hipSuccess)
+                                      (uint2 *)ctx->ext.ptr, nullptr, ctx->stream)) != hipSuccess)
         return hip_fail(e, "option_terms launch");
     if ((e = alp::launch_eval(ctx->sp, q.cap1, (const uint2 *)ctx->rec.ptr, (const uint2 *)ctx->ext.ptr,
                               (const uint64_t *)ctx->idx.ptr, count, (alp_eval_t *)ctx->evals.ptr,
@@ -614,8 +616,8 @@ int32_t alp_set_launch(alp_ctx *ctx, uint32_t variant, uint32_t blocks_per_item,
 {
     if (!ctx)
         return fail(ALP_EINVAL, "ctx is NULL");
-    if (variant > 2)
-        return fail(ALP_EINVAL, "variant %u not in 0..2", variant);
+    if (variant > 3)
+        return fail(ALP_EINVAL, "variant %u not in 0..3", variant);
     if (threads_per_block && (threads_per_block % 64 || threads_per_block > 1024))
         return fail(ALP_EINVAL, "threads_per_block must be a multiple of 64, at most 1024");
     if (blocks_per_item > (1u << 24))
@@ -664,7 +666,7 @@ void alp_free(alp_ctx *ctx)
         if (ctx->ev[k])
             (void)hipEventDestroy(ctx->ev[k]);
     DevBuf *bufs[] = {&ctx->tables, &ctx->q_inst, &ctx->q_cap, &ctx->q_lambda, &ctx->rec,
-                      &ctx->ext, &ctx->winners, &ctx->results, &ctx->idx, &ctx->evals, &ctx->tmax};
+                      &ctx->ext, &ctx->inner, &ctx->winners, &ctx->results, &ctx->idx, &ctx->evals, &ctx->tmax};
     for (DevBuf *b : bufs)
         b->release();
     if (ctx->host_results)

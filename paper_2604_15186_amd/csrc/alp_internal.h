@@ -52,19 +52,20 @@ struct Winner {
 
 // Launch geometry of one scan.
 struct ScanGeometry {
-    uint32_t variant;          // 1: lane-per-last-option, 2: thread-per-candidate
+    uint32_t variant;          // 1: row-minimum, 2: thread-per-candidate, 3: exact-tracking lanes
     uint32_t threads;          // per block
     uint32_t blocks_per_item;
-    uint64_t rows;             // variant 1: rows of O prefixes per item
-    uint64_t rows_per_wave;    // variant 1
+    uint64_t rows;             // variants 1, 3: rows of O prefixes per item
+    uint64_t rows_per_wave;    // variants 1, 3
     uint64_t per_thread;       // variant 2: candidates per thread
-    uint32_t slots;            // variant 1: options of the last LLM per lane (1, 2, 4, 8)
+    uint32_t slots;            // variants 1, 3: options of the last LLM per lane (1, 2, 4, 8)
 };
 
 hipError_t launch_option_terms(const SpaceDev &sp, const TablesDev &tb, const QueryDev &q,
-                               uint32_t count, uint2 *rec, uint2 *ext, hipStream_t st);
+                               uint32_t count, uint2 *rec, uint2 *ext, uint2 *inner,
+                               hipStream_t st);
 hipError_t launch_scan(const SpaceDev &sp, const QueryDev &q, uint32_t count, const uint2 *rec,
-                       const ScanGeometry &g, Winner *winners, hipStream_t st);
+                       const uint2 *inner, const ScanGeometry &g, Winner *winners, hipStream_t st);
 hipError_t launch_final(const SpaceDev &sp, uint32_t count, uint32_t blocks_per_item,
                         const Winner *winners, const uint2 *ext, alp_result_t *out,
                         hipStream_t st);

@@ -4,9 +4,10 @@
 //   1. option_terms_kernel: per (item, LLM m, option o) the Eq. 1 contribution c and the share
 //      units u (replaced by a sentinel when the option is unusable at the target), plus the
 //      Eq. 2 normalised throughput tau and validity flags for result decoding.
-//   2. scan_lane_kernel<S> (or scan_flat_kernel): every candidate x = (o_0 .. o_{M-1}) is
-//      evaluated -- L_w = sum c, feasible iff sum u <= Q*G -- and the lexicographic (L_w, x)
-//      minimum is reduced per wave, per block, and written as one 16-byte winner per block.
+//   2. scan_min_kernel<S> (or, for cross-checks, scan_flat_kernel / scan_lane_kernel<S>): every
+//      candidate x = (o_0 .. o_{M-1}) is evaluated -- L_w = sum c, feasible iff sum u <= Q*G --
+//      and the lexicographic (L_w, x) minimum is reduced per wave, per block, and written as one
+//      16-byte winner per block.
 //   3. final_kernel: minimum over an item's block winners; decodes the winning index and
 //      recomputes T_w (Eq. 2) and the share units from the per-option records.
 // Everything is integer; results are bit-identical for every launch geometry.
@@ -88,9 +89,11 @@ __device__ __forceinline__ uint32_t query_value(const uint32_t *arr, uint32_t si
 // 1. Per-option terms.  One thread per (item, m, o).
 //    rec[item][m][o] = (c, usable ? u : sentinel), c = 0 when unusable
 //    ext[item][m][o] = (tau, u | ok << 16 | thr_ok << 17)
+//    inner[item][o]  = (c, capacity - (usable ? u : sentinel)) for m = M-2 (if inner != nullptr):
+//                      the share units left for the other LLMs once LLM M-2 takes option o
 __global__ void __launch_bounds__(256)
 option_terms_kernel(SpaceDev sp, TablesDev tb, QueryDev q, uint32_t count, uint2 *__restrict__ rec,
-                    uint2 *__restrict__ ext)
+                    uint2 *__restrict__ ext, uint2 *__restrict__ inner)
 {
     const uint64_t per_item = (uint64_t)sp.M * sp.O;
     const uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -137,12 +140,251 @@ option_terms_kernel(SpaceDev sp, TablesDev tb, QueryDev q, uint32_t count, uint2
     }
     const uint32_t u = (uint32_t)(tp * fq * d);
     const bool usable = ok && thr;
-    rec[t] = make_uint2(usable ? (uint32_t)c : 0u, usable ? u : kSentinelUnits);
+    const uint32_t units = usable ? u : kSentinelUnits;
+    rec[t] = make_uint2(usable ? (uint32_t)c : 0u, units);
     ext[t] = make_uint2((uint32_t)tau, u | ((uint32_t)ok << 16) | ((uint32_t)thr << 17));
+    if (inner && sp.M >= 2 && m == sp.M - 2) {
+        const int32_t capacity = (int32_t)query_value(q.capacity, q.cap1, item);
+        inner[(uint64_t)item * sp.O + o] =
+            make_uint2(usable ? (uint32_t)c : 0u, (uint32_t)(capacity - (int32_t)units));
+    }
+}
+
+
+// ---------------------------------------------------------------------------------------------
+// 2a. Row-minimum scan (default).
+//
+// Candidates are grouped in "rows": the digits o_0..o_{M-3} are fixed (their latency sum oc and
+// share units ou are wave-uniform, in SGPRs) and o_{M-2} (the "inner" LLM, index j) and
+// o_{M-1} (the "last" LLM) vary.  Lane l owns the last LLM's options l, l+64, ... (S per lane),
+// whose records stay in VGPRs for the whole kernel.  With w = u_last + ou per lane and the
+// inner record (c_j, y_j = capacity - u_j) read with scalar loads, candidate (j, lane option)
+// is feasible iff w <= y_j, and its latency is oc + c_last + c_j, where oc + c_last is the
+// same for all j of the row.  So the lane's best candidate of the row is found by
+//     bq = min over feasible j of c_j
+// which costs two VALU operations per candidate: v_cmpx (feasibility into EXEC) and v_min_u32
+// (EXEC restored by one scalar move).
+//
+// The argmin index is recovered exactly and only where it matters.  A wave walks its rows in
+// increasing index order, so a later row can only replace the wave's best (L, x) with a strictly
+// smaller L.  After each row the lanes compare oc + c_last + bq with the wave's best L; if any
+// lane beats it, the row is scanned again to find, per such lane-slot, the lowest j with
+// c_j = bq that is feasible (the lowest index reaching that lane-slot's row minimum), and the
+// wave's best becomes the lexicographic (L, x) minimum of those.  Rows that beat the running
+// best become rare as the scan proceeds.
+// One record (c, y) against every slot of the lane: exec = (w <= y), bq = min(bq, c), exec
+// restored.  The compiler treats each asm statement as opaque and separates consecutive ones
+// by a wait state, so the hot loop issues several records per statement.
+#define ALP_MIN_STEP(Y, C, W, B)                                                                   \
+    "v_cmpx_ge_i32_e32 vcc, %[" Y "], %[" W "]\n\t"                                                \
+    "v_min_u32_e32 %[" B "], %[" C "], %[" B "]\n\t"                                               \
+    "s_mov_b64 exec, %[full]\n\t"
+
+template <int S>
+__device__ __forceinline__ void masked_min_step(uint32_t (&bq)[S], const int32_t (&w)[S],
+                                                uint32_t y, uint32_t c, uint64_t full)
+{
+#pragma unroll
+    for (int s = 0; s < S; ++s)
+        asm volatile(ALP_MIN_STEP("y", "c", "w", "b")
+                     : [b] "+v"(bq[s])
+                     : [y] "s"(y), [w] "v"(w[s]), [c] "s"(c), [full] "s"(full)
+                     : "vcc");
+}
+
+// Eight consecutive records (v[0..7]) for lanes with one or two slots.
+__device__ __forceinline__ void masked_min_8(uint32_t (&bq)[1], const int32_t (&w)[1],
+                                             const uint2 (&v)[8], uint64_t full)
+{
+#define ALP_R1(T) ALP_MIN_STEP("y" #T, "c" #T, "w0", "b0")
+    asm volatile(ALP_R1(0) ALP_R1(1) ALP_R1(2) ALP_R1(3) ALP_R1(4) ALP_R1(5) ALP_R1(6) ALP_R1(7)
+                 : [b0] "+v"(bq[0])
+                 : [w0] "v"(w[0]), [full] "s"(full),
+                   [y0] "s"(v[0].y), [c0] "s"(v[0].x), [y1] "s"(v[1].y), [c1] "s"(v[1].x),
+                   [y2] "s"(v[2].y), [c2] "s"(v[2].x), [y3] "s"(v[3].y), [c3] "s"(v[3].x),
+                   [y4] "s"(v[4].y), [c4] "s"(v[4].x), [y5] "s"(v[5].y), [c5] "s"(v[5].x),
+                   [y6] "s"(v[6].y), [c6] "s"(v[6].x), [y7] "s"(v[7].y), [c7] "s"(v[7].x)
+                 : "vcc");
+#undef ALP_R1
+}
+
+__device__ __forceinline__ void masked_min_8(uint32_t (&bq)[2], const int32_t (&w)[2],
+                                             const uint2 (&v)[8], uint64_t full)
+{
+#define ALP_R2(T) ALP_MIN_STEP("y" #T, "c" #T, "w0", "b0") ALP_MIN_STEP("y" #T, "c" #T, "w1", "b1")
+    asm volatile(ALP_R2(0) ALP_R2(1) ALP_R2(2) ALP_R2(3) ALP_R2(4) ALP_R2(5) ALP_R2(6) ALP_R2(7)
+                 : [b0] "+v"(bq[0]), [b1] "+v"(bq[1])
+                 : [w0] "v"(w[0]), [w1] "v"(w[1]), [full] "s"(full),
+                   [y0] "s"(v[0].y), [c0] "s"(v[0].x), [y1] "s"(v[1].y), [c1] "s"(v[1].x),
+                   [y2] "s"(v[2].y), [c2] "s"(v[2].x), [y3] "s"(v[3].y), [c3] "s"(v[3].x),
+                   [y4] "s"(v[4].y), [c4] "s"(v[4].x), [y5] "s"(v[5].y), [c5] "s"(v[5].x),
+                   [y6] "s"(v[6].y), [c6] "s"(v[6].x), [y7] "s"(v[7].y), [c7] "s"(v[7].x)
+                 : "vcc");
+#undef ALP_R2
+}
+
+template <int S>
+__device__ __forceinline__ void masked_min_8(uint32_t (&bq)[S], const int32_t (&w)[S],
+                                             const uint2 (&v)[8], uint64_t full)
+{
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+        masked_min_step<S>(bq, w, v[t].y, v[t].x, full);
+}
+
+template <int S>
+__global__ void __launch_bounds__(1024)
+scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_all, QueryDev q,
+                uint32_t M, uint32_t O, uint64_t rows, uint64_t rows_per_wave,
+                uint32_t blocks_per_item, uint32_t nblocks, Winner *__restrict__ winners)
+{
+    const uint32_t lb = xcd_logical_block(blockIdx.x, nblocks);
+    const uint32_t item = lb / blocks_per_item;
+    const uint32_t sub = lb - item * blocks_per_item;
+    const int32_t capacity = (int32_t)query_value(q.capacity, q.cap1, item);
+    const uint2 *R = rec + (uint64_t)item * M * O;
+    const uint32_t lane = threadIdx.x & 63;
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const uint32_t wpb = blockDim.x >> 6;
+
+    const uint2 *last = R + (uint64_t)(M - 1) * O;
+    uint32_t c_last[S];
+    int32_t u_last[S];
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+        const uint32_t o = lane + 64u * s;
+        if (o < O) {
+            const uint2 v = last[o];
+            c_last[s] = v.x;
+            u_last[s] = (int32_t)v.y;
+        } else {
+            c_last[s] = 0;
+            u_last[s] = 1 << 28;              // above every capacity, even after adding ou
+        }
+    }
+    const bool has_inner = M >= 2;
+    const uint2 *inner = inner_all + (uint64_t)item * O;
+    const uint32_t n_inner = has_inner ? O : 1;
+    const uint32_t n_outer = M >= 2 ? M - 2 : 0;
+
+    uint32_t waveL = kNoLatency;
+    uint64_t waveX = ~0ull;
+    const uint64_t gw = (uint64_t)sub * wpb + wave;
+    const uint64_t r_begin = gw * rows_per_wave;
+    const uint64_t r_end = r_begin + rows_per_wave < rows ? r_begin + rows_per_wave : rows;
+
+    if (r_begin < r_end) {
+        const uint64_t full = __builtin_amdgcn_read_exec();
+        uint32_t digit[kMaxOuter];
+        {
+            uint64_t rr = r_begin;
+#pragma unroll
+            for (int k = (int)kMaxOuter - 1; k >= 0; --k) {
+                digit[k] = 0;
+                if ((uint32_t)k < n_outer) {
+                    digit[k] = (uint32_t)(rr % O);
+                    rr /= O;
+                }
+            }
+        }
+        for (uint64_t r = r_begin; r < r_end; ++r) {
+            uint32_t oc = 0;
+            int32_t ou = 0;
+#pragma unroll
+            for (uint32_t k = 0; k < kMaxOuter; ++k) {
+                if (k < n_outer) {
+                    const uint2 v = R[(uint64_t)k * O + digit[k]];
+                    oc += v.x;
+                    ou += (int32_t)v.y;
+                }
+            }
+            int32_t w[S];
+            uint32_t bq[S];
+#pragma unroll
+            for (int s = 0; s < S; ++s) {
+                w[s] = u_last[s] + ou;
+                bq[s] = kNoLatency;
+            }
+            if (has_inner) {
+                uint32_t jb = 0;
+                for (; jb + 8 <= n_inner; jb += 8) {
+                    uint2 v[8];
+#pragma unroll
+                    for (int t = 0; t < 8; ++t)
+                        v[t] = inner[jb + t];
+                    masked_min_8(bq, w, v, full);
+                }
+                for (; jb < n_inner; ++jb) {
+                    const uint2 v = inner[jb];
+                    masked_min_step<S>(bq, w, v.y, v.x, full);
+                }
+            } else {
+                masked_min_step<S>(bq, w, (uint32_t)capacity, 0u, full);
+            }
+
+            // Lane-slot minima of the row; does any beat the wave's best?
+            uint32_t L[S];
+            bool beats = false;
+#pragma unroll
+            for (int s = 0; s < S; ++s) {
+                L[s] = bq[s] == kNoLatency ? kNoLatency : bq[s] + c_last[s] + oc;
+                beats |= L[s] < waveL;
+            }
+            if (__any(beats)) {
+                bool need[S];
+                uint32_t jf[S];
+#pragma unroll
+                for (int s = 0; s < S; ++s) {
+                    need[s] = L[s] < waveL;
+                    jf[s] = has_inner ? kNoLatency : 0u;
+                }
+                if (has_inner) {
+                    for (uint32_t j = 0; j < n_inner; ++j) {
+                        const uint2 v = inner[j];
+#pragma unroll
+                        for (int s = 0; s < S; ++s) {
+                            if (need[s] && jf[s] == kNoLatency && (int32_t)v.y >= w[s] && v.x == bq[s])
+                                jf[s] = j;
+                        }
+                    }
+                }
+                uint32_t bl = kNoLatency;
+                uint64_t bx = ~0ull;
+#pragma unroll
+                for (int s = 0; s < S; ++s) {
+                    if (need[s]) {
+                        const uint64_t x = (r * n_inner + jf[s]) * (uint64_t)O + lane + 64u * s;
+                        if (lex_less(L[s], x, bl, bx)) {
+                            bl = L[s];
+                            bx = x;
+                        }
+                    }
+                }
+                wave_min(bl, bx);
+                // readfirstlane works on int: widen through uint32_t, never sign-extend.
+                waveL = (uint32_t)__builtin_amdgcn_readfirstlane(bl);
+                waveX = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(bx >> 32)) << 32) |
+                        (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)bx);
+            }
+
+            bool carry = true;
+#pragma unroll
+            for (int k = (int)kMaxOuter - 1; k >= 0; --k) {
+                if ((uint32_t)k < n_outer && carry) {
+                    ++digit[k];
+                    if (digit[k] == O)
+                        digit[k] = 0;
+                    else
+                        carry = false;
+                }
+            }
+        }
+    }
+    block_min_store(waveL, waveX, &winners[lb]);
 }
 
 // ---------------------------------------------------------------------------------------------
-// 2a. Lane-per-last-option scan.
+// 2c. Exact-tracking lane scan (cross-check variant).
 //
 // A wave walks "rows": fixed digits o_0..o_{M-3} (their c and u sums are wave-uniform and live
 // in SGPRs) and every o_{M-2} in turn (one uniform 8-byte record per step, fetched with scalar
@@ -284,7 +526,7 @@ scan_lane_kernel(const uint2 *__restrict__ rec, QueryDev q, uint32_t M, uint32_t
 }
 
 // ---------------------------------------------------------------------------------------------
-// 2b. Thread-per-candidate scan (cross-check variant and fallback): each thread evaluates a
+// 2b. Thread-per-candidate scan (cross-check variant): each thread evaluates a
 // contiguous index range from the LDS-staged option table, decoding the start index once and
 // counting the digits up from there.
 __global__ void __launch_bounds__(1024)
@@ -486,31 +728,36 @@ tmax_kernel(SpaceDev sp, QueryDev q, const uint2 *__restrict__ ext, uint32_t *__
 // Launchers.
 
 hipError_t launch_option_terms(const SpaceDev &sp, const TablesDev &tb, const QueryDev &q,
-                               uint32_t count, uint2 *rec, uint2 *ext, hipStream_t st)
+                               uint32_t count, uint2 *rec, uint2 *ext, uint2 *inner, hipStream_t st)
 {
     const uint64_t total = (uint64_t)count * sp.M * sp.O;
     if (total == 0)
         return hipSuccess;
     const uint32_t blocks = (uint32_t)((total + 255) / 256);
     hipLaunchKernelGGL(option_terms_kernel, dim3(blocks), dim3(256), 0, st, sp, tb, q, count, rec,
-                       ext);
+                       ext, inner);
     return hipGetLastError();
 }
 
 template <int S>
 static hipError_t launch_lane(const SpaceDev &sp, const QueryDev &q, uint32_t count,
-                              const uint2 *rec, const ScanGeometry &g, Winner *winners,
-                              hipStream_t st)
+                              const uint2 *rec, const uint2 *inner, const ScanGeometry &g,
+                              Winner *winners, hipStream_t st)
 {
     const uint32_t nblocks = count * g.blocks_per_item;
-    hipLaunchKernelGGL(HIP_KERNEL_NAME(scan_lane_kernel<S>), dim3(nblocks), dim3(g.threads), 0, st,
-                       rec, q, sp.M, sp.O, g.rows, g.rows_per_wave, g.blocks_per_item, nblocks,
-                       winners);
+    if (g.variant == 3)
+        hipLaunchKernelGGL(HIP_KERNEL_NAME(scan_lane_kernel<S>), dim3(nblocks), dim3(g.threads), 0,
+                           st, rec, q, sp.M, sp.O, g.rows, g.rows_per_wave, g.blocks_per_item,
+                           nblocks, winners);
+    else
+        hipLaunchKernelGGL(HIP_KERNEL_NAME(scan_min_kernel<S>), dim3(nblocks), dim3(g.threads), 0,
+                           st, rec, inner, q, sp.M, sp.O, g.rows, g.rows_per_wave,
+                           g.blocks_per_item, nblocks, winners);
     return hipGetLastError();
 }
 
 hipError_t launch_scan(const SpaceDev &sp, const QueryDev &q, uint32_t count, const uint2 *rec,
-                       const ScanGeometry &g, Winner *winners, hipStream_t st)
+                       const uint2 *inner, const ScanGeometry &g, Winner *winners, hipStream_t st)
 {
     if (count == 0)
         return hipSuccess;
@@ -525,10 +772,10 @@ hipError_t launch_scan(const SpaceDev &sp, const QueryDev &q, uint32_t count, co
         return hipGetLastError();
     }
     switch (g.slots) {
-    case 1: return launch_lane<1>(sp, q, count, rec, g, winners, st);
-    case 2: return launch_lane<2>(sp, q, count, rec, g, winners, st);
-    case 4: return launch_lane<4>(sp, q, count, rec, g, winners, st);
-    case 8: return launch_lane<8>(sp, q, count, rec, g, winners, st);
+    case 1: return launch_lane<1>(sp, q, count, rec, inner, g, winners, st);
+    case 2: return launch_lane<2>(sp, q, count, rec, inner, g, winners, st);
+    case 4: return launch_lane<4>(sp, q, count, rec, inner, g, winners, st);
+    case 8: return launch_lane<8>(sp, q, count, rec, inner, g, winners, st);
     default: return hipErrorInvalidValue;
     }
 }
@@ -573,11 +820,16 @@ int scan_blocks_per_cu(uint32_t variant, uint32_t slots, uint32_t threads, const
         e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_flat_kernel, (int)threads,
                                                          (size_t)sp.M * sp.O * sizeof(uint2));
     } else {
+        const bool exact = variant == 3;
         switch (slots) {
-        case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_lane_kernel<1>, (int)threads, 0); break;
-        case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_lane_kernel<2>, (int)threads, 0); break;
-        case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_lane_kernel<4>, (int)threads, 0); break;
-        case 8: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_lane_kernel<8>, (int)threads, 0); break;
+        case 1: e = exact ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_lane_kernel<1>, (int)threads, 0)
+                          : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<1>, (int)threads, 0); break;
+        case 2: e = exact ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_lane_kernel<2>, (int)threads, 0)
+                          : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<2>, (int)threads, 0); break;
+        case 4: e = exact ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_lane_kernel<4>, (int)threads, 0)
+                          : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<4>, (int)threads, 0); break;
+        case 8: e = exact ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_lane_kernel<8>, (int)threads, 0)
+                          : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<8>, (int)threads, 0); break;
         default: break;
         }
     }

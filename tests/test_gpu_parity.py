@@ -88,7 +88,7 @@ CASES = load_cases()
 def test_hand_cases(alp, case):
     b = case_batch(case)
     with alp.Context(b) as ctx:
-        for variant in (1, 2):
+        for variant in (1, 2, 3):
             ctx.set_launch(variant)
             for q in case["queries"]:
                 res = ctx.search(0, q["G"], q["lambda"])
@@ -171,7 +171,7 @@ def test_launch_geometry_and_variant_do_not_change_results(alp):
     b = make_batch(2, [g["inst"]])
     with alp.Context(b) as ctx:
         for variant, bpi, tpb in [(1, 0, 0), (1, 1, 64), (1, 7, 128), (1, 3000, 1024),
-                                  (2, 0, 0), (2, 5, 256), (0, 64, 512)]:
+                                  (2, 0, 0), (2, 5, 256), (0, 64, 512), (3, 0, 0), (3, 5, 128)]:
             ctx.set_launch(variant, bpi, tpb)
             res = ctx.search(0, g["G"], g["lambda"])
             check_result(b, 0, res, g["x"], g["L"], g["T"], g["U"])
@@ -209,7 +209,7 @@ def test_ragged_and_degenerate_spaces(alp, spec):
             for lam in sorted({1, target_from_tmax(int(b["u_ppm"][i]), t), t, t + 1}):
                 for g in (0, G // 2, G):
                     want = oracle_expect(b, i, g, lam)
-                    for variant in (1, 2):
+                    for variant in (1, 2, 3):
                         ctx.set_launch(variant)
                         check_result(b, i, ctx.search(i, g, lam), *want)
             ctx.set_launch(0)
@@ -243,3 +243,27 @@ def test_batch_edge_cases(alp):
             ctx.search(3, 16, 1)
         with pytest.raises(alp.AlpError):
             ctx.eval_candidates(0, 16, 1, [ctx.num_candidates])
+
+
+@pytest.mark.parametrize("seed", [41, 42, 43])
+def test_many_ties_keep_lowest_index(alp, seed):
+    """Load-independent, option-independent latencies: every feasible candidate ties, so the
+    answer is the lowest feasible index.  Exercises the tie-break at lane, wave, block and grid
+    level and the row re-scan."""
+    M, G = 4, 12
+    b = make_custom(seed, M, (1, 2, 4, 8), (1, 2, 3, 4), 8, 1, G, count=2)
+    for i in range(2):
+        for m in range(M):
+            b["lat"][i, m] = 1000 * (m + 1)
+            b["n"][i, m] = 1000
+            b["p"][i, m] = 1000
+    with alp.Context(b) as ctx:
+        for i in range(2):
+            inst = oracle.Instance(b, i)
+            t = oracle.tmax(inst, G)
+            for lam in (1, max(1, t // 3), t):
+                want = oracle_expect(b, i, G, lam)
+                assert want[0] is not None
+                for variant in (1, 2, 3):
+                    ctx.set_launch(variant)
+                    check_result(b, i, ctx.search(i, G, lam), *want)
