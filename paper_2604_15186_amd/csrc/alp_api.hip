@@ -227,18 +227,25 @@ alp::ScanGeometry plan_scan(const alp_ctx *c, uint32_t count)
     alp::ScanGeometry g{};
     const alp::SpaceDev &sp = c->sp;
     g.variant = c->variant ? c->variant : 1;
-    g.threads = c->tpb_override ? c->tpb_override : 256;
     g.slots = slots_for(sp.O);
-    const uint32_t wpb = g.threads / 64;
-    const uint64_t resident =
-        (uint64_t)(c->num_cus > 0 ? c->num_cus : 256) *
-        (uint64_t)alp::scan_blocks_per_cu(g.variant, g.slots, g.threads, sp);
-    const uint64_t want = count ? ceil_div(resident, count) : 1;
+    const uint64_t cus = c->num_cus > 0 ? (uint64_t)c->num_cus : 256;
     if (g.variant != 2) {
         g.rows = 1;
         for (uint32_t m = 2; m < sp.M; ++m)
             g.rows *= sp.O;
-        uint64_t bpi = c->bpi_override ? c->bpi_override : want;
+        // About one full round of resident waves over the whole batch: waves per item =
+        // resident waves / items, at least one, at most one per row.
+        const uint64_t resident_waves =
+            cus * (uint64_t)alp::scan_blocks_per_cu(g.variant, g.slots, 256, sp) * 4;
+        uint64_t per_item = count ? ceil_div(resident_waves, count) : 1;
+        if (per_item > g.rows)
+            per_item = g.rows;
+        if (per_item < 1)
+            per_item = 1;
+        g.threads = c->tpb_override ? c->tpb_override
+                                    : (per_item >= 4 ? 256u : (uint32_t)(64 * per_item));
+        const uint32_t wpb = g.threads / 64;
+        uint64_t bpi = c->bpi_override ? c->bpi_override : ceil_div(per_item, wpb);
         const uint64_t max_bpi = ceil_div(g.rows, wpb);
         if (!c->bpi_override && bpi > max_bpi)
             bpi = max_bpi;
@@ -249,7 +256,10 @@ alp::ScanGeometry plan_scan(const alp_ctx *c, uint32_t count)
             bpi = ceil_div(g.rows, g.rows_per_wave * wpb);
         g.blocks_per_item = (uint32_t)bpi;
     } else {
-        uint64_t bpi = c->bpi_override ? c->bpi_override : want;
+        g.threads = c->tpb_override ? c->tpb_override : 256;
+        const uint64_t resident =
+            cus * (uint64_t)alp::scan_blocks_per_cu(g.variant, g.slots, g.threads, sp);
+        uint64_t bpi = c->bpi_override ? c->bpi_override : (count ? ceil_div(resident, count) : 1);
         const uint64_t max_bpi = ceil_div(c->N, g.threads);
         if (!c->bpi_override && bpi > max_bpi)
             bpi = max_bpi;
@@ -293,7 +303,7 @@ int32_t run_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count)
         return hip_fail(e, "hipMalloc(rec)");
     if ((e = c->ext.ensure(items_bytes)) != hipSuccess)
         return hip_fail(e, "hipMalloc(ext)");
-    if ((e = c->inner.ensure((uint64_t)count * sp.O * sizeof(uint2))) != hipSuccess)
+    if ((e = c->inner.ensure((uint64_t)count * alp::inner_stride(sp.O) * sizeof(uint2))) != hipSuccess)
         return hip_fail(e, "hipMalloc(inner)");
     if ((e = c->winners.ensure(nwin * sizeof(alp::Winner))) != hipSuccess)
         return hip_fail(e, "hipMalloc(winners)");

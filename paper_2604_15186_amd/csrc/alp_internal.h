@@ -43,6 +43,9 @@ struct QueryDev {
     uint32_t inst1, cap1, lambda1;
 };
 
+// Records per item of the inner-LLM table: options rounded up to a multiple of 16.
+__host__ __device__ inline uint32_t inner_stride(uint32_t O) { return (O + 15u) & ~15u; }
+
 // Per-block winner of a scan: lexicographic (L, x) minimum; L = kNoLatency if none.
 struct Winner {
     uint32_t L;

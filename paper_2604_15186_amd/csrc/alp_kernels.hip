@@ -21,6 +21,7 @@ namespace alp {
 namespace {
 
 constexpr uint32_t kMaxOuter = ALP_MAX_LLMS - 2;   // digits above the last two LLMs
+constexpr int32_t kNeverFits = -(1 << 30);          // remaining units no lane can satisfy
 
 __device__ __forceinline__ bool lex_less(uint32_t aL, uint64_t ax, uint32_t bL, uint64_t bx)
 {
@@ -39,6 +40,29 @@ __device__ __forceinline__ void wave_min(uint32_t &L, uint64_t &x)
             x = ox;
         }
     }
+}
+
+// Wave-wide minima, returned as wave-uniform values.
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v)
+{
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        const uint32_t o = __shfl_xor(v, off, 64);
+        v = o < v ? o : v;
+    }
+    return (uint32_t)__builtin_amdgcn_readfirstlane(v);
+}
+
+__device__ __forceinline__ uint64_t wave_min_u64(uint64_t v)
+{
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        const uint64_t o = __shfl_xor((unsigned long long)v, off, 64);
+        v = o < v ? o : v;
+    }
+    // readfirstlane works on int: widen through uint32_t, never sign-extend.
+    return ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(v >> 32)) << 32) |
+           (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)v);
 }
 
 // Block-wide minimum; thread 0 writes the block's winner.
@@ -145,8 +169,12 @@ option_terms_kernel(SpaceDev sp, TablesDev tb, QueryDev q, uint32_t count, uint2
     ext[t] = make_uint2((uint32_t)tau, u | ((uint32_t)ok << 16) | ((uint32_t)thr << 17));
     if (inner && sp.M >= 2 && m == sp.M - 2) {
         const int32_t capacity = (int32_t)query_value(q.capacity, q.cap1, item);
-        inner[(uint64_t)item * sp.O + o] =
-            make_uint2(usable ? (uint32_t)c : 0u, (uint32_t)(capacity - (int32_t)units));
+        const uint32_t stride = inner_stride(sp.O);
+        uint2 *row = inner + (uint64_t)item * stride;
+        row[o] = make_uint2(usable ? (uint32_t)c : 0u, (uint32_t)(capacity - (int32_t)units));
+        // Padding up to a multiple of 16 records: never feasible (no lane's units fit).
+        for (uint32_t pad = sp.O + o; pad < stride; pad += sp.O)
+            row[pad] = make_uint2(0u, (uint32_t)kNeverFits);
     }
 }
 
@@ -165,13 +193,14 @@ option_terms_kernel(SpaceDev sp, TablesDev tb, QueryDev q, uint32_t count, uint2
 // which costs two VALU operations per candidate: v_cmpx (feasibility into EXEC) and v_min_u32
 // (EXEC restored by one scalar move).
 //
-// The argmin index is recovered exactly and only where it matters.  A wave walks its rows in
-// increasing index order, so a later row can only replace the wave's best (L, x) with a strictly
-// smaller L.  After each row the lanes compare oc + c_last + bq with the wave's best L; if any
-// lane beats it, the row is scanned again to find, per such lane-slot, the lowest j with
-// c_j = bq that is feasible (the lowest index reaching that lane-slot's row minimum), and the
-// wave's best becomes the lexicographic (L, x) minimum of those.  Rows that beat the running
-// best become rare as the scan proceeds.
+// The argmin index is recovered exactly at the end.  Candidate indices order as (row, j,
+// option), and a wave walks its rows in increasing order.  Each lane-slot keeps its smallest
+// row latency oc + c_last + bq and the first row reaching it (a later row replaces it only
+// when strictly smaller).  At the end the wave takes the smallest latency L*, the lowest row r*
+// in which any lane-slot reaches L*, and scans that one row again to find, for those
+// lane-slots, the lowest j with c_j = L* - oc - c_last that is feasible; the smallest (j,
+// option) among them completes the lowest index reaching L*.
+
 // One record (c, y) against every slot of the lane: exec = (w <= y), bq = min(bq, c), exec
 // restored.  The compiler treats each asm statement as opaque and separates consecutive ones
 // by a wait state, so the hot loop issues several records per statement.
@@ -232,8 +261,26 @@ __device__ __forceinline__ void masked_min_8(uint32_t (&bq)[S], const int32_t (&
         masked_min_step<S>(bq, w, v[t].y, v[t].x, full);
 }
 
+// Outer-digit latency and share-unit sums of row r (digits o_0..o_{M-3} of r, base O).
+__device__ __forceinline__ void outer_sums(const uint2 *R, uint32_t O, uint32_t n_outer,
+                                           uint64_t r, uint32_t &oc, int32_t &ou)
+{
+    oc = 0;
+    ou = 0;
+#pragma unroll
+    for (int k = (int)kMaxOuter - 1; k >= 0; --k) {
+        if ((uint32_t)k < n_outer) {
+            const uint32_t d = (uint32_t)(r % O);
+            r /= O;
+            const uint2 v = R[(uint64_t)k * O + d];
+            oc += v.x;
+            ou += (int32_t)v.y;
+        }
+    }
+}
+
 template <int S>
-__global__ void __launch_bounds__(1024)
+__global__ void __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 8 : 1)))
 scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_all, QueryDev q,
                 uint32_t M, uint32_t O, uint64_t rows, uint64_t rows_per_wave,
                 uint32_t blocks_per_item, uint32_t nblocks, Winner *__restrict__ winners)
@@ -263,7 +310,8 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
         }
     }
     const bool has_inner = M >= 2;
-    const uint2 *inner = inner_all + (uint64_t)item * O;
+    const uint32_t n_inner_padded = inner_stride(O);
+    const uint2 *inner = inner_all + (uint64_t)item * n_inner_padded;
     const uint32_t n_inner = has_inner ? O : 1;
     const uint32_t n_outer = M >= 2 ? M - 2 : 0;
 
@@ -275,6 +323,12 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
 
     if (r_begin < r_end) {
         const uint64_t full = __builtin_amdgcn_read_exec();
+        uint32_t bestL[S], bestR[S];          // per lane-slot: smallest row latency, its first row
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+            bestL[s] = kNoLatency;
+            bestR[s] = 0;
+        }
         uint32_t digit[kMaxOuter];
         {
             uint64_t rr = r_begin;
@@ -287,7 +341,7 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
                 }
             }
         }
-        for (uint64_t r = r_begin; r < r_end; ++r) {
+        for (uint32_t rr = 0; rr < (uint32_t)(r_end - r_begin); ++rr) {
             uint32_t oc = 0;
             int32_t ou = 0;
 #pragma unroll
@@ -306,67 +360,31 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
                 bq[s] = kNoLatency;
             }
             if (has_inner) {
-                uint32_t jb = 0;
-                for (; jb + 8 <= n_inner; jb += 8) {
-                    uint2 v[8];
+                // 16 records per iteration (the table is padded to a multiple of 16 with
+                // records no lane can use): two 64-byte scalar loads issued together, so the
+                // loop's own scalar work stays small next to the 2 x 16 x S VALU operations.
+                const uint2 *const end = inner + n_inner_padded;
+                for (const uint2 *p = inner; p != end; p += 16) {
+                    uint2 v0[8], v1[8];
 #pragma unroll
-                    for (int t = 0; t < 8; ++t)
-                        v[t] = inner[jb + t];
-                    masked_min_8(bq, w, v, full);
-                }
-                for (; jb < n_inner; ++jb) {
-                    const uint2 v = inner[jb];
-                    masked_min_step<S>(bq, w, v.y, v.x, full);
+                    for (int t = 0; t < 8; ++t) {
+                        v0[t] = p[t];
+                        v1[t] = p[8 + t];
+                    }
+                    masked_min_8(bq, w, v0, full);
+                    masked_min_8(bq, w, v1, full);
                 }
             } else {
                 masked_min_step<S>(bq, w, (uint32_t)capacity, 0u, full);
             }
-
-            // Lane-slot minima of the row; does any beat the wave's best?
-            uint32_t L[S];
-            bool beats = false;
+            // Row minimum per lane-slot (saturating: no feasible j leaves kNoLatency).
 #pragma unroll
             for (int s = 0; s < S; ++s) {
-                L[s] = bq[s] == kNoLatency ? kNoLatency : bq[s] + c_last[s] + oc;
-                beats |= L[s] < waveL;
+                const uint32_t L = __builtin_elementwise_add_sat(bq[s], c_last[s] + oc);
+                const bool better = L < bestL[s];
+                bestL[s] = better ? L : bestL[s];
+                bestR[s] = better ? rr : bestR[s];
             }
-            if (__any(beats)) {
-                bool need[S];
-                uint32_t jf[S];
-#pragma unroll
-                for (int s = 0; s < S; ++s) {
-                    need[s] = L[s] < waveL;
-                    jf[s] = has_inner ? kNoLatency : 0u;
-                }
-                if (has_inner) {
-                    for (uint32_t j = 0; j < n_inner; ++j) {
-                        const uint2 v = inner[j];
-#pragma unroll
-                        for (int s = 0; s < S; ++s) {
-                            if (need[s] && jf[s] == kNoLatency && (int32_t)v.y >= w[s] && v.x == bq[s])
-                                jf[s] = j;
-                        }
-                    }
-                }
-                uint32_t bl = kNoLatency;
-                uint64_t bx = ~0ull;
-#pragma unroll
-                for (int s = 0; s < S; ++s) {
-                    if (need[s]) {
-                        const uint64_t x = (r * n_inner + jf[s]) * (uint64_t)O + lane + 64u * s;
-                        if (lex_less(L[s], x, bl, bx)) {
-                            bl = L[s];
-                            bx = x;
-                        }
-                    }
-                }
-                wave_min(bl, bx);
-                // readfirstlane works on int: widen through uint32_t, never sign-extend.
-                waveL = (uint32_t)__builtin_amdgcn_readfirstlane(bl);
-                waveX = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(bx >> 32)) << 32) |
-                        (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)bx);
-            }
-
             bool carry = true;
 #pragma unroll
             for (int k = (int)kMaxOuter - 1; k >= 0; --k) {
@@ -378,6 +396,60 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
                         carry = false;
                 }
             }
+        }
+
+        // Wave minimum L*, then the lowest row r* reaching it.
+        uint32_t lmin = kNoLatency;
+#pragma unroll
+        for (int s = 0; s < S; ++s)
+            lmin = bestL[s] < lmin ? bestL[s] : lmin;
+        const uint32_t Lstar = wave_min_u32(lmin);
+        if (Lstar != kNoLatency) {
+            uint32_t rmin = 0xFFFFFFFFu;
+#pragma unroll
+            for (int s = 0; s < S; ++s)
+                if (bestL[s] == Lstar && bestR[s] < rmin)
+                    rmin = bestR[s];
+            const uint32_t rstar = wave_min_u32(rmin);
+            const uint64_t r = r_begin + rstar;
+            uint32_t oc;
+            int32_t ou;
+            outer_sums(R, O, n_outer, r, oc, ou);
+            // Lowest feasible j of row r* reaching L*, for each lane-slot that reaches it there.
+            bool need[S];
+            uint32_t target[S], jf[S];
+            int32_t w[S];
+#pragma unroll
+            for (int s = 0; s < S; ++s) {
+                need[s] = bestL[s] == Lstar && bestR[s] == rstar;
+                target[s] = Lstar - c_last[s] - oc;
+                w[s] = u_last[s] + ou;
+                jf[s] = has_inner ? kNoLatency : 0u;
+            }
+            if (has_inner) {
+                for (uint32_t j = 0; j < n_inner; ++j) {
+                    const uint2 v = inner[j];
+                    bool open = false;
+#pragma unroll
+                    for (int s = 0; s < S; ++s) {
+                        if (need[s] && jf[s] == kNoLatency && (int32_t)v.y >= w[s] && v.x == target[s])
+                            jf[s] = j;
+                        open |= need[s] && jf[s] == kNoLatency;
+                    }
+                    if (!__any(open))
+                        break;
+                }
+            }
+            uint64_t xmin = ~0ull;
+#pragma unroll
+            for (int s = 0; s < S; ++s) {
+                if (need[s]) {
+                    const uint64_t x = (r * n_inner + jf[s]) * (uint64_t)O + lane + 64u * s;
+                    xmin = x < xmin ? x : xmin;
+                }
+            }
+            waveL = Lstar;
+            waveX = wave_min_u64(xmin);
         }
     }
     block_min_store(waveL, waveX, &winners[lb]);
