@@ -32,7 +32,7 @@ from workloads import CONFIGS, make_batch, target_from_tmax  # noqa: E402
 PEAK_LANE_OPS = 256 * 64 * 2.4e9        # int32 VALU lane-ops/s of MI355X
 OPS_PER_CANDIDATE = 2                   # budget compare + objective min
 WORKLOADS = {"cfg2": 2, "cfg3": 3, "cfg4": 4, "cfg1": 1}
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "scan_traffic.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "scan_min_hbm_bytes.md")
 
 
 def _traffic(kernel_digest: str, workload: str):
@@ -40,11 +40,12 @@ def _traffic(kernel_digest: str, workload: str):
     on the current kernel source and this workload."""
     try:
         with open(TRAFFIC_FILE) as f:
-            t = json.load(f)
-    except (OSError, ValueError):
+            text = f.read()
+        t = json.loads(text.split("```json", 1)[1].split("```", 1)[0])
+    except (OSError, ValueError, IndexError):
         return None
     entry = t.get(workload)
-    if not entry or entry.get("kernel_source_sha256") != kernel_digest:
+    if not entry or t.get("kernel_source_sha256") != kernel_digest:
         return None
     return entry.get("bytes_per_launch")
 
