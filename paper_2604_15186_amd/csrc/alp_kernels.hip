@@ -279,7 +279,8 @@ __device__ __forceinline__ void outer_sums(const uint2 *R, uint32_t O, uint32_t 
     }
 }
 
-template <int S>
+// NOUT >= 0: the number of outer digits (M - 2) is fixed at compile time; NOUT < 0: any M.
+template <int S, int NOUT>
 __global__ void __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 8 : 1)))
 scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_all, QueryDev q,
                 uint32_t M, uint32_t O, uint64_t rows, uint64_t rows_per_wave,
@@ -313,7 +314,8 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
     const uint32_t n_inner_padded = inner_stride(O);
     const uint2 *inner = inner_all + (uint64_t)item * n_inner_padded;
     const uint32_t n_inner = has_inner ? O : 1;
-    const uint32_t n_outer = M >= 2 ? M - 2 : 0;
+    constexpr int NMAX = NOUT >= 0 ? NOUT : (int)kMaxOuter;
+    const uint32_t n_outer = NOUT >= 0 ? (uint32_t)NOUT : (M >= 2 ? M - 2 : 0);
 
     uint32_t waveL = kNoLatency;
     uint64_t waveX = ~0ull;
@@ -329,13 +331,13 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
             bestL[s] = kNoLatency;
             bestR[s] = 0;
         }
-        uint32_t digit[kMaxOuter];
+        uint32_t digit[NMAX > 0 ? NMAX : 1];
         {
             uint64_t rr = r_begin;
 #pragma unroll
-            for (int k = (int)kMaxOuter - 1; k >= 0; --k) {
+            for (int k = NMAX - 1; k >= 0; --k) {
                 digit[k] = 0;
-                if ((uint32_t)k < n_outer) {
+                if (NOUT >= 0 || (uint32_t)k < n_outer) {
                     digit[k] = (uint32_t)(rr % O);
                     rr /= O;
                 }
@@ -345,8 +347,8 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
             uint32_t oc = 0;
             int32_t ou = 0;
 #pragma unroll
-            for (uint32_t k = 0; k < kMaxOuter; ++k) {
-                if (k < n_outer) {
+            for (int k = 0; k < NMAX; ++k) {
+                if (NOUT >= 0 || (uint32_t)k < n_outer) {
                     const uint2 v = R[(uint64_t)k * O + digit[k]];
                     oc += v.x;
                     ou += (int32_t)v.y;
@@ -385,15 +387,14 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
                 bestL[s] = better ? L : bestL[s];
                 bestR[s] = better ? rr : bestR[s];
             }
-            bool carry = true;
+            // Next row: odometer on the outer digits, integer carry (stays in scalar registers).
+            uint32_t inc = 1;
 #pragma unroll
-            for (int k = (int)kMaxOuter - 1; k >= 0; --k) {
-                if ((uint32_t)k < n_outer && carry) {
-                    ++digit[k];
-                    if (digit[k] == O)
-                        digit[k] = 0;
-                    else
-                        carry = false;
+            for (int k = NMAX - 1; k >= 0; --k) {
+                if (NOUT >= 0 || (uint32_t)k < n_outer) {
+                    const uint32_t d = digit[k] + inc;
+                    inc = d == O ? 1u : 0u;
+                    digit[k] = inc ? 0u : d;
                 }
             }
         }
@@ -821,10 +822,21 @@ static hipError_t launch_lane(const SpaceDev &sp, const QueryDev &q, uint32_t co
         hipLaunchKernelGGL(HIP_KERNEL_NAME(scan_lane_kernel<S>), dim3(nblocks), dim3(g.threads), 0,
                            st, rec, q, sp.M, sp.O, g.rows, g.rows_per_wave, g.blocks_per_item,
                            nblocks, winners);
-    else
-        hipLaunchKernelGGL(HIP_KERNEL_NAME(scan_min_kernel<S>), dim3(nblocks), dim3(g.threads), 0,
-                           st, rec, inner, q, sp.M, sp.O, g.rows, g.rows_per_wave,
-                           g.blocks_per_item, nblocks, winners);
+    else {
+        const uint32_t n_outer = sp.M >= 2 ? sp.M - 2 : 0;
+#define ALP_LAUNCH_MIN(NO)                                                                         \
+    hipLaunchKernelGGL(HIP_KERNEL_NAME(scan_min_kernel<S, NO>), dim3(nblocks), dim3(g.threads), 0, \
+                       st, rec, inner, q, sp.M, sp.O, g.rows, g.rows_per_wave, g.blocks_per_item,  \
+                       nblocks, winners)
+        switch (n_outer) {
+        case 0: ALP_LAUNCH_MIN(0); break;
+        case 1: ALP_LAUNCH_MIN(1); break;
+        case 2: ALP_LAUNCH_MIN(2); break;
+        case 3: ALP_LAUNCH_MIN(3); break;
+        default: ALP_LAUNCH_MIN(-1); break;
+        }
+#undef ALP_LAUNCH_MIN
+    }
     return hipGetLastError();
 }
 
@@ -893,17 +905,21 @@ int scan_blocks_per_cu(uint32_t variant, uint32_t slots, uint32_t threads, const
                                                          (size_t)sp.M * sp.O * sizeof(uint2));
     } else {
         const bool exact = variant == 3;
+        const uint32_t no = sp.M >= 2 ? sp.M - 2 : 0;
+#define ALP_OCC_MIN(SL)                                                                            \
+    (no == 0 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<SL, 0>, (int)threads, 0) \
+   : no == 1 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<SL, 1>, (int)threads, 0) \
+   : no == 2 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<SL, 2>, (int)threads, 0) \
+   : no == 3 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<SL, 3>, (int)threads, 0) \
+             : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<SL, -1>, (int)threads, 0))
         switch (slots) {
-        case 1: e = exact ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_lane_kernel<1>, (int)threads, 0)
-                          : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<1>, (int)threads, 0); break;
-        case 2: e = exact ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_lane_kernel<2>, (int)threads, 0)
-                          : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<2>, (int)threads, 0); break;
-        case 4: e = exact ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_lane_kernel<4>, (int)threads, 0)
-                          : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<4>, (int)threads, 0); break;
-        case 8: e = exact ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_lane_kernel<8>, (int)threads, 0)
-                          : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<8>, (int)threads, 0); break;
+        case 1: e = exact ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_lane_kernel<1>, (int)threads, 0) : ALP_OCC_MIN(1); break;
+        case 2: e = exact ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_lane_kernel<2>, (int)threads, 0) : ALP_OCC_MIN(2); break;
+        case 4: e = exact ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_lane_kernel<4>, (int)threads, 0) : ALP_OCC_MIN(4); break;
+        case 8: e = exact ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_lane_kernel<8>, (int)threads, 0) : ALP_OCC_MIN(8); break;
         default: break;
         }
+#undef ALP_OCC_MIN
     }
     return (e == hipSuccess && n > 0) ? n : 1;
 }
