@@ -201,38 +201,75 @@ option_terms_kernel(SpaceDev sp, TablesDev tb, QueryDev q, uint32_t count, uint2
 // lane-slots, the lowest j with c_j = L* - oc - c_last that is feasible; the smallest (j,
 // option) among them completes the lowest index reaching L*.
 
-// One record (c, y) against every slot of the lane: exec = (w <= y), bq = min(bq, c), exec
-// restored.  The compiler treats each asm statement as opaque and separates consecutive ones
-// by a wait state, so the hot loop issues several records per statement.
-#define ALP_MIN_STEP(Y, C, W, B)                                                                   \
+// One record (c, y) against every slot of the lane.  A lane's slots are ordered by share units
+// (w_0 <= w_1 <= ...), so the feasible lanes of slot s+1 are a subset of those of slot s: each
+// v_cmpx narrows EXEC to (w_s <= y), v_min_u32 folds c into bq_s on exactly those lanes, and one
+// scalar move restores EXEC after the last slot.  Per candidate: one compare, one minimum.
+// The compiler treats each asm statement as opaque and separates consecutive ones by a wait
+// state, so the hot loop issues several records per statement.
+#define ALP_CM(Y, C, W, B)                                                                         \
     "v_cmpx_ge_i32_e32 vcc, %[" Y "], %[" W "]\n\t"                                                \
-    "v_min_u32_e32 %[" B "], %[" C "], %[" B "]\n\t"                                               \
-    "s_mov_b64 exec, %[full]\n\t"
+    "v_min_u32_e32 %[" B "], %[" C "], %[" B "]\n\t"
+#define ALP_RESTORE "s_mov_b64 exec, %[full]\n\t"
 
-template <int S>
-__device__ __forceinline__ void masked_min_step(uint32_t (&bq)[S], const int32_t (&w)[S],
+__device__ __forceinline__ void masked_min_step(uint32_t (&bq)[1], const int32_t (&w)[1],
                                                 uint32_t y, uint32_t c, uint64_t full)
 {
-#pragma unroll
-    for (int s = 0; s < S; ++s)
-        asm volatile(ALP_MIN_STEP("y", "c", "w", "b")
-                     : [b] "+v"(bq[s])
-                     : [y] "s"(y), [w] "v"(w[s]), [c] "s"(c), [full] "s"(full)
-                     : "vcc");
+    asm volatile(ALP_CM("y", "c", "w0", "b0") ALP_RESTORE
+                 : [b0] "+v"(bq[0])
+                 : [y] "s"(y), [c] "s"(c), [w0] "v"(w[0]), [full] "s"(full)
+                 : "vcc");
 }
+
+__device__ __forceinline__ void masked_min_step(uint32_t (&bq)[2], const int32_t (&w)[2],
+                                                uint32_t y, uint32_t c, uint64_t full)
+{
+    asm volatile(ALP_CM("y", "c", "w0", "b0") ALP_CM("y", "c", "w1", "b1") ALP_RESTORE
+                 : [b0] "+v"(bq[0]), [b1] "+v"(bq[1])
+                 : [y] "s"(y), [c] "s"(c), [w0] "v"(w[0]), [w1] "v"(w[1]), [full] "s"(full)
+                 : "vcc");
+}
+
+__device__ __forceinline__ void masked_min_step(uint32_t (&bq)[4], const int32_t (&w)[4],
+                                                uint32_t y, uint32_t c, uint64_t full)
+{
+    asm volatile(ALP_CM("y", "c", "w0", "b0") ALP_CM("y", "c", "w1", "b1")
+                 ALP_CM("y", "c", "w2", "b2") ALP_CM("y", "c", "w3", "b3") ALP_RESTORE
+                 : [b0] "+v"(bq[0]), [b1] "+v"(bq[1]), [b2] "+v"(bq[2]), [b3] "+v"(bq[3])
+                 : [y] "s"(y), [c] "s"(c), [w0] "v"(w[0]), [w1] "v"(w[1]), [w2] "v"(w[2]),
+                   [w3] "v"(w[3]), [full] "s"(full)
+                 : "vcc");
+}
+
+__device__ __forceinline__ void masked_min_step(uint32_t (&bq)[8], const int32_t (&w)[8],
+                                                uint32_t y, uint32_t c, uint64_t full)
+{
+    asm volatile(ALP_CM("y", "c", "w0", "b0") ALP_CM("y", "c", "w1", "b1")
+                 ALP_CM("y", "c", "w2", "b2") ALP_CM("y", "c", "w3", "b3")
+                 ALP_CM("y", "c", "w4", "b4") ALP_CM("y", "c", "w5", "b5")
+                 ALP_CM("y", "c", "w6", "b6") ALP_CM("y", "c", "w7", "b7") ALP_RESTORE
+                 : [b0] "+v"(bq[0]), [b1] "+v"(bq[1]), [b2] "+v"(bq[2]), [b3] "+v"(bq[3]),
+                   [b4] "+v"(bq[4]), [b5] "+v"(bq[5]), [b6] "+v"(bq[6]), [b7] "+v"(bq[7])
+                 : [y] "s"(y), [c] "s"(c), [w0] "v"(w[0]), [w1] "v"(w[1]), [w2] "v"(w[2]),
+                   [w3] "v"(w[3]), [w4] "v"(w[4]), [w5] "v"(w[5]), [w6] "v"(w[6]),
+                   [w7] "v"(w[7]), [full] "s"(full)
+                 : "vcc");
+}
+
+#define ALP_ARGS8(v)                                                                               \
+    [y0] "s"(v[0].y), [c0] "s"(v[0].x), [y1] "s"(v[1].y), [c1] "s"(v[1].x), [y2] "s"(v[2].y),      \
+        [c2] "s"(v[2].x), [y3] "s"(v[3].y), [c3] "s"(v[3].x), [y4] "s"(v[4].y), [c4] "s"(v[4].x),  \
+        [y5] "s"(v[5].y), [c5] "s"(v[5].x), [y6] "s"(v[6].y), [c6] "s"(v[6].x), [y7] "s"(v[7].y),  \
+        [c7] "s"(v[7].x)
 
 // Eight consecutive records (v[0..7]) for lanes with one or two slots.
 __device__ __forceinline__ void masked_min_8(uint32_t (&bq)[1], const int32_t (&w)[1],
                                              const uint2 (&v)[8], uint64_t full)
 {
-#define ALP_R1(T) ALP_MIN_STEP("y" #T, "c" #T, "w0", "b0")
+#define ALP_R1(T) ALP_CM("y" #T, "c" #T, "w0", "b0") ALP_RESTORE
     asm volatile(ALP_R1(0) ALP_R1(1) ALP_R1(2) ALP_R1(3) ALP_R1(4) ALP_R1(5) ALP_R1(6) ALP_R1(7)
                  : [b0] "+v"(bq[0])
-                 : [w0] "v"(w[0]), [full] "s"(full),
-                   [y0] "s"(v[0].y), [c0] "s"(v[0].x), [y1] "s"(v[1].y), [c1] "s"(v[1].x),
-                   [y2] "s"(v[2].y), [c2] "s"(v[2].x), [y3] "s"(v[3].y), [c3] "s"(v[3].x),
-                   [y4] "s"(v[4].y), [c4] "s"(v[4].x), [y5] "s"(v[5].y), [c5] "s"(v[5].x),
-                   [y6] "s"(v[6].y), [c6] "s"(v[6].x), [y7] "s"(v[7].y), [c7] "s"(v[7].x)
+                 : [w0] "v"(w[0]), [full] "s"(full), ALP_ARGS8(v)
                  : "vcc");
 #undef ALP_R1
 }
@@ -240,14 +277,10 @@ __device__ __forceinline__ void masked_min_8(uint32_t (&bq)[1], const int32_t (&
 __device__ __forceinline__ void masked_min_8(uint32_t (&bq)[2], const int32_t (&w)[2],
                                              const uint2 (&v)[8], uint64_t full)
 {
-#define ALP_R2(T) ALP_MIN_STEP("y" #T, "c" #T, "w0", "b0") ALP_MIN_STEP("y" #T, "c" #T, "w1", "b1")
+#define ALP_R2(T) ALP_CM("y" #T, "c" #T, "w0", "b0") ALP_CM("y" #T, "c" #T, "w1", "b1") ALP_RESTORE
     asm volatile(ALP_R2(0) ALP_R2(1) ALP_R2(2) ALP_R2(3) ALP_R2(4) ALP_R2(5) ALP_R2(6) ALP_R2(7)
                  : [b0] "+v"(bq[0]), [b1] "+v"(bq[1])
-                 : [w0] "v"(w[0]), [w1] "v"(w[1]), [full] "s"(full),
-                   [y0] "s"(v[0].y), [c0] "s"(v[0].x), [y1] "s"(v[1].y), [c1] "s"(v[1].x),
-                   [y2] "s"(v[2].y), [c2] "s"(v[2].x), [y3] "s"(v[3].y), [c3] "s"(v[3].x),
-                   [y4] "s"(v[4].y), [c4] "s"(v[4].x), [y5] "s"(v[5].y), [c5] "s"(v[5].x),
-                   [y6] "s"(v[6].y), [c6] "s"(v[6].x), [y7] "s"(v[7].y), [c7] "s"(v[7].x)
+                 : [w0] "v"(w[0]), [w1] "v"(w[1]), [full] "s"(full), ALP_ARGS8(v)
                  : "vcc");
 #undef ALP_R2
 }
@@ -258,7 +291,7 @@ __device__ __forceinline__ void masked_min_8(uint32_t (&bq)[S], const int32_t (&
 {
 #pragma unroll
     for (int t = 0; t < 8; ++t)
-        masked_min_step<S>(bq, w, v[t].y, v[t].x, full);
+        masked_min_step(bq, w, v[t].y, v[t].x, full);
 }
 
 // Outer-digit latency and share-unit sums of row r (digits o_0..o_{M-3} of r, base O).
@@ -295,12 +328,16 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
     const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const uint32_t wpb = blockDim.x >> 6;
 
+    // The last LLM's options of this lane: lane, lane + 64, ...  They are processed in order
+    // of share units (insertion sort of the S values held by the lane), which lets the hot
+    // loop nest the EXEC masks of the slots; o_last keeps each slot's option index.
     const uint2 *last = R + (uint64_t)(M - 1) * O;
-    uint32_t c_last[S];
+    uint32_t c_last[S], o_last[S];
     int32_t u_last[S];
 #pragma unroll
     for (int s = 0; s < S; ++s) {
         const uint32_t o = lane + 64u * s;
+        o_last[s] = o;
         if (o < O) {
             const uint2 v = last[o];
             c_last[s] = v.x;
@@ -308,6 +345,21 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
         } else {
             c_last[s] = 0;
             u_last[s] = 1 << 28;              // above every capacity, even after adding ou
+        }
+    }
+#pragma unroll
+    for (int a = 1; a < S; ++a) {
+#pragma unroll
+        for (int b = a; b > 0; --b) {
+            const bool swap = u_last[b] < u_last[b - 1];
+            const int32_t u0 = u_last[b - 1], u1 = u_last[b];
+            const uint32_t c0 = c_last[b - 1], c1 = c_last[b], o0 = o_last[b - 1], o1 = o_last[b];
+            u_last[b - 1] = swap ? u1 : u0;
+            u_last[b] = swap ? u0 : u1;
+            c_last[b - 1] = swap ? c1 : c0;
+            c_last[b] = swap ? c0 : c1;
+            o_last[b - 1] = swap ? o1 : o0;
+            o_last[b] = swap ? o0 : o1;
         }
     }
     const bool has_inner = M >= 2;
@@ -377,7 +429,7 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
                     masked_min_8(bq, w, v1, full);
                 }
             } else {
-                masked_min_step<S>(bq, w, (uint32_t)capacity, 0u, full);
+                masked_min_step(bq, w, (uint32_t)capacity, 0u, full);
             }
             // Row minimum per lane-slot (saturating: no feasible j leaves kNoLatency).
 #pragma unroll
@@ -445,7 +497,7 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
 #pragma unroll
             for (int s = 0; s < S; ++s) {
                 if (need[s]) {
-                    const uint64_t x = (r * n_inner + jf[s]) * (uint64_t)O + lane + 64u * s;
+                    const uint64_t x = (r * n_inner + jf[s]) * (uint64_t)O + o_last[s];
                     xmin = x < xmin ? x : xmin;
                 }
             }
