@@ -99,8 +99,9 @@ struct alp_ctx {
     DevBuf tables;                 // W | n | p | allowed | rate | lat
     alp::TablesDev tdev{};
 
-    DevBuf q_inst, q_cap, q_lambda, rec, ext, inner, winners, results, idx, evals, tmax;
-    alp_result_t *host_results = nullptr;   // pinned staging
+    DevBuf q_inst, q_cap, q_lambda, rec, ext, inner, done, winners, idx, evals, tmax;
+    alp_result_t *host_results = nullptr;   // pinned host memory the kernels write results to
+    alp_result_t *host_results_dev = nullptr;  // its device-visible address
     size_t host_results_cap = 0;
 
     uint32_t variant = 0, bpi_override = 0, tpb_override = 0;
@@ -278,17 +279,24 @@ int32_t ensure_host_results(alp_ctx *c, size_t count)
     if (c->host_results)
         (void)hipHostFree(c->host_results);
     c->host_results = nullptr;
+    c->host_results_dev = nullptr;
     c->host_results_cap = 0;
     hipError_t e = hipHostMalloc((void **)&c->host_results, count * sizeof(alp_result_t),
-                                 hipHostMallocDefault);
+                                 hipHostMallocMapped);
     if (e != hipSuccess)
         return hip_fail(e, "hipHostMalloc(results)");
+    e = hipHostGetDevicePointer((void **)&c->host_results_dev, c->host_results, 0);
+    if (e != hipSuccess) {
+        (void)hipHostFree(c->host_results);
+        c->host_results = nullptr;
+        return hip_fail(e, "hipHostGetDevicePointer(results)");
+    }
     c->host_results_cap = count;
     return ALP_OK;
 }
 
-// Runs option terms -> scan -> final for `count` items described by q; results land in
-// c->host_results[0..count).
+// Runs option terms -> scan (with the fused final reduction) for `count` items described by q;
+// the kernels write the results straight into c->host_results[0..count) (mapped pinned memory).
 int32_t run_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count)
 {
     const alp::SpaceDev &sp = c->sp;
@@ -305,40 +313,39 @@ int32_t run_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count)
         return hip_fail(e, "hipMalloc(ext)");
     if ((e = c->inner.ensure((uint64_t)count * alp::inner_stride(sp.O) * sizeof(uint2))) != hipSuccess)
         return hip_fail(e, "hipMalloc(inner)");
+    if ((e = c->done.ensure((uint64_t)count * sizeof(uint32_t))) != hipSuccess)
+        return hip_fail(e, "hipMalloc(done)");
     if ((e = c->winners.ensure(nwin * sizeof(alp::Winner))) != hipSuccess)
         return hip_fail(e, "hipMalloc(winners)");
-    if ((e = c->results.ensure((uint64_t)count * sizeof(alp_result_t))) != hipSuccess)
-        return hip_fail(e, "hipMalloc(results)");
     int32_t st = ensure_host_results(c, count);
     if (st != ALP_OK)
         return st;
 
     uint2 *rec = (uint2 *)c->rec.ptr, *ext = (uint2 *)c->ext.ptr, *inner = (uint2 *)c->inner.ptr;
     alp::Winner *win = (alp::Winner *)c->winners.ptr;
-    alp_result_t *res = (alp_result_t *)c->results.ptr;
+    alp::FinishArgs fa;
+    fa.sp = sp;
+    fa.ext = ext;
+    fa.done = (uint32_t *)c->done.ptr;
+    fa.out = c->host_results_dev;
     if (c->timing && (e = hipEventRecord(c->ev[0], c->stream)) != hipSuccess)
         return hip_fail(e, "hipEventRecord");
-    if ((e = alp::launch_option_terms(sp, c->tdev, q, count, rec, ext, inner, c->stream)) != hipSuccess)
+    if ((e = alp::launch_option_terms(sp, c->tdev, q, count, rec, ext, inner, fa.done, c->stream)) !=
+        hipSuccess)
         return hip_fail(e, "option_terms launch");
     if (c->timing && (e = hipEventRecord(c->ev[1], c->stream)) != hipSuccess)
         return hip_fail(e, "hipEventRecord");
-    if ((e = alp::launch_scan(sp, q, count, rec, inner, g, win, c->stream)) != hipSuccess)
+    if ((e = alp::launch_scan(sp, q, count, rec, inner, g, win, fa, c->stream)) != hipSuccess)
         return hip_fail(e, "scan launch");
     if (c->timing && (e = hipEventRecord(c->ev[2], c->stream)) != hipSuccess)
         return hip_fail(e, "hipEventRecord");
-    if ((e = alp::launch_final(sp, count, g.blocks_per_item, win, ext, res, c->stream)) != hipSuccess)
-        return hip_fail(e, "final launch");
-    if (c->timing && (e = hipEventRecord(c->ev[3], c->stream)) != hipSuccess)
-        return hip_fail(e, "hipEventRecord");
-    if ((e = hipMemcpyAsync(c->host_results, res, (size_t)count * sizeof(alp_result_t),
-                            hipMemcpyDeviceToHost, c->stream)) != hipSuccess)
-        return hip_fail(e, "copy results");
     if ((e = hipStreamSynchronize(c->stream)) != hipSuccess)
         return hip_fail(e, "hipStreamSynchronize");
     if (c->timing) {
-        for (int k = 0; k < 3; ++k)
+        for (int k = 0; k < 2; ++k)
             if ((e = hipEventElapsedTime(&c->last_ms[k], c->ev[k], c->ev[k + 1])) != hipSuccess)
                 return hip_fail(e, "hipEventElapsedTime");
+        c->last_ms[2] = 0.0f;
     }
     c->last_blocks = count * g.blocks_per_item;
     return ALP_OK;
@@ -558,7 +565,7 @@ int32_t alp_max_throughput(alp_ctx *ctx, uint32_t count, const uint32_t *instanc
     q.capacity = (const uint32_t *)ctx->q_cap.ptr;
     q.lambda = (const uint32_t *)ctx->q_lambda.ptr;
     if ((e = alp::launch_option_terms(ctx->sp, ctx->tdev, q, count, (uint2 *)ctx->rec.ptr,
-                                      (uint2 *)ctx->ext.ptr, nullptr, ctx->stream)) != hipSuccess)
+                                      (uint2 *)ctx->ext.ptr, nullptr, nullptr, ctx->stream)) != hipSuccess)
         return hip_fail(e, "option_terms launch");
     if ((e = alp::launch_tmax(ctx->sp, q, count, (const uint2 *)ctx->ext.ptr,
                               (uint32_t *)ctx->tmax.ptr, ctx->stream)) != hipSuccess)
@@ -607,7 +614,7 @@ int32_t alp_eval_candidates(alp_ctx *ctx, uint32_t instance, uint32_t gpu_budget
                             ctx->stream)) != hipSuccess)
         return hip_fail(e, "copy indices");
     if ((e = alp::launch_option_terms(ctx->sp, ctx->tdev, q, 1, (uint2 *)ctx->rec.ptr,
-                                      (uint2 *)ctx->ext.ptr, nullptr, ctx->stream)) != hipSuccess)
+                                      (uint2 *)ctx->ext.ptr, nullptr, nullptr, ctx->stream)) != hipSuccess)
         return hip_fail(e, "option_terms launch");
     if ((e = alp::launch_eval(ctx->sp, q.cap1, (const uint2 *)ctx->rec.ptr, (const uint2 *)ctx->ext.ptr,
                               (const uint64_t *)ctx->idx.ptr, count, (alp_eval_t *)ctx->evals.ptr,
@@ -676,7 +683,8 @@ void alp_free(alp_ctx *ctx)
         if (ctx->ev[k])
             (void)hipEventDestroy(ctx->ev[k]);
     DevBuf *bufs[] = {&ctx->tables, &ctx->q_inst, &ctx->q_cap, &ctx->q_lambda, &ctx->rec,
-                      &ctx->ext, &ctx->inner, &ctx->winners, &ctx->results, &ctx->idx, &ctx->evals, &ctx->tmax};
+                      &ctx->ext, &ctx->inner, &ctx->done, &ctx->winners, &ctx->idx, &ctx->evals,
+                      &ctx->tmax};
     for (DevBuf *b : bufs)
         b->release();
     if (ctx->host_results)

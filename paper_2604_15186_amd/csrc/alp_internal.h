@@ -3,6 +3,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <stddef.h>
 #include <stdint.h>
 
 #include "alp.h"
@@ -53,6 +54,22 @@ struct Winner {
     uint64_t x;
 };
 
+// The scan kernels write alp_result_t as six 64-bit words in this field order.
+static_assert(sizeof(alp_result_t) == 48, "alp_result_t layout");
+static_assert(offsetof(alp_result_t, latency_us) == 8 && offsetof(alp_result_t, throughput_milli) == 12 &&
+                  offsetof(alp_result_t, gpu_units) == 16 && offsetof(alp_result_t, status) == 20 &&
+                  offsetof(alp_result_t, tp) == 24 && offsetof(alp_result_t, frac_units) == 32 &&
+                  offsetof(alp_result_t, replicas) == 40,
+              "alp_result_t layout");
+
+// What the last block of an item needs to produce the item's result.
+struct FinishArgs {
+    SpaceDev sp;
+    const uint2 *ext;          // per-option (tau, u | flags) of the query
+    uint32_t *done;            // per-item finished-block counter, zeroed by the option-term kernel
+    alp_result_t *out;         // per-item results (device-visible, may be mapped host memory)
+};
+
 // Launch geometry of one scan.
 struct ScanGeometry {
     uint32_t variant;          // 1: row-minimum, 2: thread-per-candidate, 3: exact-tracking lanes
@@ -65,13 +82,11 @@ struct ScanGeometry {
 };
 
 hipError_t launch_option_terms(const SpaceDev &sp, const TablesDev &tb, const QueryDev &q,
-                               uint32_t count, uint2 *rec, uint2 *ext, uint2 *inner,
+                               uint32_t count, uint2 *rec, uint2 *ext, uint2 *inner, uint32_t *done,
                                hipStream_t st);
 hipError_t launch_scan(const SpaceDev &sp, const QueryDev &q, uint32_t count, const uint2 *rec,
-                       const uint2 *inner, const ScanGeometry &g, Winner *winners, hipStream_t st);
-hipError_t launch_final(const SpaceDev &sp, uint32_t count, uint32_t blocks_per_item,
-                        const Winner *winners, const uint2 *ext, alp_result_t *out,
-                        hipStream_t st);
+                       const uint2 *inner, const ScanGeometry &g, Winner *winners,
+                       const FinishArgs &fa, hipStream_t st);
 hipError_t launch_eval(const SpaceDev &sp, uint32_t capacity, const uint2 *rec, const uint2 *ext,
                        const uint64_t *idx, uint64_t count, alp_eval_t *out, hipStream_t st);
 hipError_t launch_tmax(const SpaceDev &sp, const QueryDev &q, uint32_t count, const uint2 *ext,

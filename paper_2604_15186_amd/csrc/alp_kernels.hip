@@ -8,8 +8,9 @@
 //      candidate x = (o_0 .. o_{M-1}) is evaluated -- L_w = sum c, feasible iff sum u <= Q*G --
 //      and the lexicographic (L_w, x) minimum is reduced per wave, per block, and written as one
 //      16-byte winner per block.
-//   3. final_kernel: minimum over an item's block winners; decodes the winning index and
-//      recomputes T_w (Eq. 2) and the share units from the per-option records.
+//   3. The last block of each item to finish (an agent-scope counter) takes the minimum over the
+//      item's block winners, decodes the winning index and recomputes T_w (Eq. 2) and the share
+//      units from the per-option records.
 // Everything is integer; results are bit-identical for every launch geometry.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -91,6 +92,78 @@ __device__ __forceinline__ void block_min_store(uint32_t L, uint64_t x, Winner *
     }
 }
 
+// Result of one item from its block winners, by one wave: the lexicographic (L, x) minimum,
+// the decoded per-LLM choices, T_w (Eq. 2: minimum over LLMs) and the share units.
+__device__ __forceinline__ void finish_item(const FinishArgs &fa, uint32_t item,
+                                            uint32_t blocks_per_item, const Winner *winners)
+{
+    const uint32_t lane = threadIdx.x & 63;
+    uint32_t L = kNoLatency;
+    uint64_t x = ~0ull;
+    for (uint32_t k = lane; k < blocks_per_item; k += 64) {
+        const Winner w = winners[(uint64_t)item * blocks_per_item + k];
+        if (lex_less(w.L, w.x, L, x)) {
+            L = w.L;
+            x = w.x;
+        }
+    }
+    wave_min(L, x);
+    if (lane != 0)
+        return;
+    // Assembled in registers as the six 64-bit words of alp_result_t (a local struct indexed at
+    // run time would be placed in memory for every thread of the block).
+    const SpaceDev &sp = fa.sp;
+    uint64_t word[6] = {ALP_NO_INDEX, 0, (uint64_t)ALP_INFEASIBLE << 32, 0, 0, 0};
+    if (L != kNoLatency) {
+        const uint2 *E = fa.ext + (uint64_t)item * sp.M * sp.O;
+        uint64_t rr = x;
+        uint32_t T = 0xFFFFFFFFu, U = 0;
+        uint64_t tp = 0, fq = 0, rep = 0;
+        for (int m = (int)sp.M - 1; m >= 0; --m) {
+            const uint32_t o = (uint32_t)(rr % sp.O);
+            rr /= sp.O;
+            const uint2 e = E[(uint64_t)m * sp.O + o];
+            T = e.x < T ? e.x : T;                      // Eq. 2: minimum over LLMs
+            U += e.y & 0xFFFFu;
+            const uint32_t ij = o / sp.D;
+            tp |= (uint64_t)(sp.tp[ij / sp.n_fq] & 0xFFu) << (8 * m);
+            fq |= (uint64_t)(sp.fq[ij % sp.n_fq] & 0xFFu) << (8 * m);
+            rep |= (uint64_t)((o % sp.D + 1) & 0xFFu) << (8 * m);
+        }
+        word[0] = x;
+        word[1] = (uint64_t)L | ((uint64_t)T << 32);
+        word[2] = (uint64_t)U | ((uint64_t)ALP_OK << 32);
+        word[3] = tp;
+        word[4] = fq;
+        word[5] = rep;
+    }
+    uint64_t *dst = reinterpret_cast<uint64_t *>(fa.out + item);
+#pragma unroll
+    for (int k = 0; k < 6; ++k)
+        dst[k] = word[k];
+}
+
+// Writes the block's winner; the last block of the item to finish (agent-scope fence and
+// counter, zeroed by option_terms_kernel before the scan) reduces the item's winners and
+// writes its result, so no separate reduction kernel is launched.
+__device__ __forceinline__ void block_finish(uint32_t L, uint64_t x, uint32_t item,
+                                             uint32_t sub, uint32_t blocks_per_item,
+                                             Winner *winners, const FinishArgs &fa)
+{
+    __shared__ uint32_t last_block;
+    block_min_store(L, x, &winners[(uint64_t)item * blocks_per_item + sub]);
+    if (threadIdx.x == 0) {
+        __threadfence();
+        const uint32_t prev = atomicAdd(&fa.done[item], 1u);
+        last_block = prev == blocks_per_item - 1 ? 1u : 0u;
+    }
+    __syncthreads();
+    if (last_block && threadIdx.x < 64) {
+        __threadfence();
+        finish_item(fa, item, blocks_per_item, winners);
+    }
+}
+
 // Workgroups are dispatched to the 8 XCDs round-robin; renumber them so that consecutive
 // logical blocks (the blocks of one item, which read the same few-KiB option table) share an
 // XCD and its L2.  A bijection on [0, nblocks).
@@ -115,9 +188,10 @@ __device__ __forceinline__ uint32_t query_value(const uint32_t *arr, uint32_t si
 //    ext[item][m][o] = (tau, u | ok << 16 | thr_ok << 17)
 //    inner[item][o]  = (c, capacity - (usable ? u : sentinel)) for m = M-2 (if inner != nullptr):
 //                      the share units left for the other LLMs once LLM M-2 takes option o
+//    done[item]      = 0 (if done != nullptr): the scan's finished-block counter
 __global__ void __launch_bounds__(256)
 option_terms_kernel(SpaceDev sp, TablesDev tb, QueryDev q, uint32_t count, uint2 *__restrict__ rec,
-                    uint2 *__restrict__ ext, uint2 *__restrict__ inner)
+                    uint2 *__restrict__ ext, uint2 *__restrict__ inner, uint32_t *__restrict__ done)
 {
     const uint64_t per_item = (uint64_t)sp.M * sp.O;
     const uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -126,6 +200,8 @@ option_terms_kernel(SpaceDev sp, TablesDev tb, QueryDev q, uint32_t count, uint2
     const uint32_t item = (uint32_t)(t / per_item);
     const uint32_t rem = (uint32_t)(t - (uint64_t)item * per_item);
     const uint32_t m = rem / sp.O, o = rem - m * sp.O;
+    if (done && rem == 0)
+        done[item] = 0;                              // block counter of the fused reduction
     const uint32_t inst = query_value(q.inst, q.inst1, item);
     const uint64_t lambda = query_value(q.lambda, q.lambda1, item);
 
@@ -317,7 +393,8 @@ template <int S, int NOUT>
 __global__ void __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 8 : 1)))
 scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_all, QueryDev q,
                 uint32_t M, uint32_t O, uint64_t rows, uint64_t rows_per_wave,
-                uint32_t blocks_per_item, uint32_t nblocks, Winner *__restrict__ winners)
+                uint32_t blocks_per_item, uint32_t nblocks, Winner *__restrict__ winners,
+                FinishArgs fa)
 {
     const uint32_t lb = xcd_logical_block(blockIdx.x, nblocks);
     const uint32_t item = lb / blocks_per_item;
@@ -505,7 +582,7 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
             waveX = wave_min_u64(xmin);
         }
     }
-    block_min_store(waveL, waveX, &winners[lb]);
+    block_finish(waveL, waveX, item, sub, blocks_per_item, winners, fa);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -524,7 +601,7 @@ template <int S>
 __global__ void __launch_bounds__(1024)
 scan_lane_kernel(const uint2 *__restrict__ rec, QueryDev q, uint32_t M, uint32_t O,
                  uint64_t rows, uint64_t rows_per_wave, uint32_t blocks_per_item,
-                 uint32_t nblocks, Winner *__restrict__ winners)
+                 uint32_t nblocks, Winner *__restrict__ winners, FinishArgs fa)
 {
     const uint32_t lb = xcd_logical_block(blockIdx.x, nblocks);
     const uint32_t item = lb / blocks_per_item;
@@ -647,7 +724,7 @@ scan_lane_kernel(const uint2 *__restrict__ rec, QueryDev q, uint32_t M, uint32_t
             }
         }
     }
-    block_min_store(bestL, bestX, &winners[lb]);
+    block_finish(bestL, bestX, item, sub, blocks_per_item, winners, fa);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -657,7 +734,7 @@ scan_lane_kernel(const uint2 *__restrict__ rec, QueryDev q, uint32_t M, uint32_t
 __global__ void __launch_bounds__(1024)
 scan_flat_kernel(const uint2 *__restrict__ rec, QueryDev q, uint32_t M, uint32_t O, uint64_t N,
                  uint64_t per_thread, uint32_t blocks_per_item, uint32_t nblocks,
-                 Winner *__restrict__ winners)
+                 Winner *__restrict__ winners, FinishArgs fa)
 {
     extern __shared__ uint2 table[];
     const uint32_t lb = xcd_logical_block(blockIdx.x, nblocks);
@@ -712,57 +789,7 @@ scan_flat_kernel(const uint2 *__restrict__ rec, QueryDev q, uint32_t M, uint32_t
             }
         }
     }
-    block_min_store(bestL, bestX, &winners[lb]);
-}
-
-// ---------------------------------------------------------------------------------------------
-// 3. Final reduction and result decoding, one 64-thread block per item.
-__global__ void __launch_bounds__(64)
-final_kernel(SpaceDev sp, uint32_t blocks_per_item, const Winner *__restrict__ winners,
-             const uint2 *__restrict__ ext, alp_result_t *__restrict__ out)
-{
-    const uint32_t item = blockIdx.x;
-    uint32_t L = kNoLatency;
-    uint64_t x = ~0ull;
-    for (uint32_t k = threadIdx.x; k < blocks_per_item; k += 64) {
-        const Winner w = winners[(uint64_t)item * blocks_per_item + k];
-        if (lex_less(w.L, w.x, L, x)) {
-            L = w.L;
-            x = w.x;
-        }
-    }
-    wave_min(L, x);
-    if (threadIdx.x != 0)
-        return;
-    alp_result_t res;
-    uint8_t *raw = reinterpret_cast<uint8_t *>(&res);
-    for (uint32_t b = 0; b < sizeof(res); ++b)
-        raw[b] = 0;
-    if (L == kNoLatency) {
-        res.index = ALP_NO_INDEX;
-        res.status = ALP_INFEASIBLE;
-    } else {
-        res.index = x;
-        res.latency_us = L;
-        res.status = ALP_OK;
-        const uint2 *E = ext + (uint64_t)item * sp.M * sp.O;
-        uint64_t rr = x;
-        uint32_t T = 0xFFFFFFFFu, U = 0;
-        for (int m = (int)sp.M - 1; m >= 0; --m) {
-            const uint32_t o = (uint32_t)(rr % sp.O);
-            rr /= sp.O;
-            const uint2 e = E[(uint64_t)m * sp.O + o];
-            T = e.x < T ? e.x : T;                      // Eq. 2: minimum over LLMs
-            U += e.y & 0xFFFFu;
-            const uint32_t ij = o / sp.D;
-            res.tp[m] = (uint8_t)sp.tp[ij / sp.n_fq];
-            res.frac_units[m] = (uint8_t)sp.fq[ij % sp.n_fq];
-            res.replicas[m] = (uint8_t)(o % sp.D + 1);
-        }
-        res.throughput_milli = T;
-        res.gpu_units = U;
-    }
-    out[item] = res;
+    block_finish(bestL, bestX, item, sub, blocks_per_item, winners, fa);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -853,33 +880,34 @@ tmax_kernel(SpaceDev sp, QueryDev q, const uint2 *__restrict__ ext, uint32_t *__
 // Launchers.
 
 hipError_t launch_option_terms(const SpaceDev &sp, const TablesDev &tb, const QueryDev &q,
-                               uint32_t count, uint2 *rec, uint2 *ext, uint2 *inner, hipStream_t st)
+                               uint32_t count, uint2 *rec, uint2 *ext, uint2 *inner, uint32_t *done,
+                               hipStream_t st)
 {
     const uint64_t total = (uint64_t)count * sp.M * sp.O;
     if (total == 0)
         return hipSuccess;
     const uint32_t blocks = (uint32_t)((total + 255) / 256);
     hipLaunchKernelGGL(option_terms_kernel, dim3(blocks), dim3(256), 0, st, sp, tb, q, count, rec,
-                       ext, inner);
+                       ext, inner, done);
     return hipGetLastError();
 }
 
 template <int S>
 static hipError_t launch_lane(const SpaceDev &sp, const QueryDev &q, uint32_t count,
                               const uint2 *rec, const uint2 *inner, const ScanGeometry &g,
-                              Winner *winners, hipStream_t st)
+                              Winner *winners, const FinishArgs &fa, hipStream_t st)
 {
     const uint32_t nblocks = count * g.blocks_per_item;
     if (g.variant == 3)
         hipLaunchKernelGGL(HIP_KERNEL_NAME(scan_lane_kernel<S>), dim3(nblocks), dim3(g.threads), 0,
                            st, rec, q, sp.M, sp.O, g.rows, g.rows_per_wave, g.blocks_per_item,
-                           nblocks, winners);
+                           nblocks, winners, fa);
     else {
         const uint32_t n_outer = sp.M >= 2 ? sp.M - 2 : 0;
 #define ALP_LAUNCH_MIN(NO)                                                                         \
     hipLaunchKernelGGL(HIP_KERNEL_NAME(scan_min_kernel<S, NO>), dim3(nblocks), dim3(g.threads), 0, \
                        st, rec, inner, q, sp.M, sp.O, g.rows, g.rows_per_wave, g.blocks_per_item,  \
-                       nblocks, winners)
+                       nblocks, winners, fa)
         switch (n_outer) {
         case 0: ALP_LAUNCH_MIN(0); break;
         case 1: ALP_LAUNCH_MIN(1); break;
@@ -893,7 +921,8 @@ static hipError_t launch_lane(const SpaceDev &sp, const QueryDev &q, uint32_t co
 }
 
 hipError_t launch_scan(const SpaceDev &sp, const QueryDev &q, uint32_t count, const uint2 *rec,
-                       const uint2 *inner, const ScanGeometry &g, Winner *winners, hipStream_t st)
+                       const uint2 *inner, const ScanGeometry &g, Winner *winners,
+                       const FinishArgs &fa, hipStream_t st)
 {
     if (count == 0)
         return hipSuccess;
@@ -904,27 +933,16 @@ hipError_t launch_scan(const SpaceDev &sp, const QueryDev &q, uint32_t count, co
         const uint32_t nblocks = count * g.blocks_per_item;
         const size_t lds = (size_t)sp.M * sp.O * sizeof(uint2);
         hipLaunchKernelGGL(scan_flat_kernel, dim3(nblocks), dim3(g.threads), lds, st, rec, q, sp.M,
-                           sp.O, N, g.per_thread, g.blocks_per_item, nblocks, winners);
+                           sp.O, N, g.per_thread, g.blocks_per_item, nblocks, winners, fa);
         return hipGetLastError();
     }
     switch (g.slots) {
-    case 1: return launch_lane<1>(sp, q, count, rec, inner, g, winners, st);
-    case 2: return launch_lane<2>(sp, q, count, rec, inner, g, winners, st);
-    case 4: return launch_lane<4>(sp, q, count, rec, inner, g, winners, st);
-    case 8: return launch_lane<8>(sp, q, count, rec, inner, g, winners, st);
+    case 1: return launch_lane<1>(sp, q, count, rec, inner, g, winners, fa, st);
+    case 2: return launch_lane<2>(sp, q, count, rec, inner, g, winners, fa, st);
+    case 4: return launch_lane<4>(sp, q, count, rec, inner, g, winners, fa, st);
+    case 8: return launch_lane<8>(sp, q, count, rec, inner, g, winners, fa, st);
     default: return hipErrorInvalidValue;
     }
-}
-
-hipError_t launch_final(const SpaceDev &sp, uint32_t count, uint32_t blocks_per_item,
-                        const Winner *winners, const uint2 *ext, alp_result_t *out,
-                        hipStream_t st)
-{
-    if (count == 0)
-        return hipSuccess;
-    hipLaunchKernelGGL(final_kernel, dim3(count), dim3(64), 0, st, sp, blocks_per_item, winners,
-                       ext, out);
-    return hipGetLastError();
 }
 
 hipError_t launch_eval(const SpaceDev &sp, uint32_t capacity, const uint2 *rec, const uint2 *ext,
