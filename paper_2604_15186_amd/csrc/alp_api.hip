@@ -99,12 +99,15 @@ struct alp_ctx {
     DevBuf tables;                 // W | n | p | allowed | rate | lat
     alp::TablesDev tdev{};
 
-    DevBuf q_inst, q_cap, q_lambda, rec, ext, inner, done, winners, idx, evals, tmax;
+    DevBuf q_inst, rec, ext, inner, done, winners, idx, evals, tmax;   // q_inst: inst | cap | lambda
+    uint32_t *host_query = nullptr;         // pinned staging of batch queries: inst | cap | lambda
+    size_t host_query_cap = 0;
     alp_result_t *host_results = nullptr;   // pinned host memory the kernels write results to
     alp_result_t *host_results_dev = nullptr;  // its device-visible address
     size_t host_results_cap = 0;
 
     uint32_t variant = 0, bpi_override = 0, tpb_override = 0;
+    int occupancy_cache[4][4][17] = {};   // [variant][log2 slots][threads / 64]: blocks per CU
     int timing = 0;
     hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
     float last_ms[3] = {0, 0, 0};
@@ -223,7 +226,17 @@ uint32_t slots_for(uint32_t O)
     return O <= 64 ? 1 : O <= 128 ? 2 : O <= 256 ? 4 : 8;
 }
 
-alp::ScanGeometry plan_scan(const alp_ctx *c, uint32_t count)
+// Resident blocks per CU of a scan kernel (occupancy query), cached per context.
+int blocks_per_cu(alp_ctx *c, uint32_t variant, uint32_t slots, uint32_t threads)
+{
+    const uint32_t ls = slots == 1 ? 0 : slots == 2 ? 1 : slots == 4 ? 2 : 3;
+    int &slot = c->occupancy_cache[variant & 3][ls][(threads / 64) & 15];
+    if (slot <= 0)
+        slot = alp::scan_blocks_per_cu(variant, slots, threads, c->sp);
+    return slot;
+}
+
+alp::ScanGeometry plan_scan(alp_ctx *c, uint32_t count)
 {
     alp::ScanGeometry g{};
     const alp::SpaceDev &sp = c->sp;
@@ -234,17 +247,22 @@ alp::ScanGeometry plan_scan(const alp_ctx *c, uint32_t count)
         g.rows = 1;
         for (uint32_t m = 2; m < sp.M; ++m)
             g.rows *= sp.O;
-        // About one full round of resident waves over the whole batch: waves per item =
-        // resident waves / items, at least one, at most one per row.
+        // Blocks of 8 waves (fewer blocks, fewer end-of-block reductions; measured best on the
+        // 4,096-instance batch), at most one wave per row; waves per item = resident waves /
+        // items, at least one block per item.
         const uint64_t resident_waves =
-            cus * (uint64_t)alp::scan_blocks_per_cu(g.variant, g.slots, 256, sp) * 4;
+            cus * (uint64_t)blocks_per_cu(c, g.variant, g.slots, 512) * 8;
+        // Each wave gets at least kMinRowsPerWave rows when the item has that many: a wave's
+        // fixed costs (setup, end-of-wave re-scan, block reduction) then stay small.
+        constexpr uint64_t kMinRowsPerWave = 8;
         uint64_t per_item = count ? ceil_div(resident_waves, count) : 1;
-        if (per_item > g.rows)
-            per_item = g.rows;
+        const uint64_t max_waves = g.rows >= kMinRowsPerWave ? g.rows / kMinRowsPerWave : 1;
+        if (per_item > max_waves)
+            per_item = max_waves;
         if (per_item < 1)
             per_item = 1;
         g.threads = c->tpb_override ? c->tpb_override
-                                    : (per_item >= 4 ? 256u : (uint32_t)(64 * per_item));
+                                    : (uint32_t)(64 * (g.rows < 8 ? g.rows : 8));
         const uint32_t wpb = g.threads / 64;
         uint64_t bpi = c->bpi_override ? c->bpi_override : ceil_div(per_item, wpb);
         const uint64_t max_bpi = ceil_div(g.rows, wpb);
@@ -259,7 +277,7 @@ alp::ScanGeometry plan_scan(const alp_ctx *c, uint32_t count)
     } else {
         g.threads = c->tpb_override ? c->tpb_override : 256;
         const uint64_t resident =
-            cus * (uint64_t)alp::scan_blocks_per_cu(g.variant, g.slots, g.threads, sp);
+            cus * (uint64_t)blocks_per_cu(c, g.variant, g.slots, g.threads);
         uint64_t bpi = c->bpi_override ? c->bpi_override : (count ? ceil_div(resident, count) : 1);
         const uint64_t max_bpi = ceil_div(c->N, g.threads);
         if (!c->bpi_override && bpi > max_bpi)
@@ -270,6 +288,47 @@ alp::ScanGeometry plan_scan(const alp_ctx *c, uint32_t count)
         g.blocks_per_item = (uint32_t)bpi;
     }
     return g;
+}
+
+int32_t ensure_host_query(alp_ctx *c, size_t count)
+{
+    if (count <= c->host_query_cap)
+        return ALP_OK;
+    if (c->host_query)
+        (void)hipHostFree(c->host_query);
+    c->host_query = nullptr;
+    c->host_query_cap = 0;
+    hipError_t e = hipHostMalloc((void **)&c->host_query, 3 * count * sizeof(uint32_t),
+                                 hipHostMallocDefault);
+    if (e != hipSuccess)
+        return hip_fail(e, "hipHostMalloc(queries)");
+    c->host_query_cap = count;
+    return ALP_OK;
+}
+
+// Uploads batch queries (instance, capacity, target) through pinned staging; q gets the device
+// arrays.
+int32_t upload_queries(alp_ctx *c, uint32_t count, const uint32_t *inst, const uint32_t *cap,
+                       const uint32_t *lambda, alp::QueryDev &q)
+{
+    int32_t st = ensure_host_query(c, count);
+    if (st != ALP_OK)
+        return st;
+    const size_t bytes = (size_t)count * sizeof(uint32_t);
+    hipError_t e;
+    if ((e = c->q_inst.ensure(3 * bytes)) != hipSuccess)
+        return hip_fail(e, "hipMalloc(queries)");
+    memcpy(c->host_query, inst, bytes);
+    memcpy(c->host_query + count, cap, bytes);
+    memcpy(c->host_query + 2 * (size_t)count, lambda, bytes);
+    if ((e = hipMemcpyAsync(c->q_inst.ptr, c->host_query, 3 * bytes, hipMemcpyHostToDevice,
+                            c->stream)) != hipSuccess)
+        return hip_fail(e, "copy queries");
+    q = alp::QueryDev{};
+    q.inst = (const uint32_t *)c->q_inst.ptr;
+    q.capacity = q.inst + count;
+    q.lambda = q.inst + 2 * (size_t)count;
+    return ALP_OK;
 }
 
 int32_t ensure_host_results(alp_ctx *c, size_t count)
@@ -509,21 +568,11 @@ int32_t alp_search_batch(alp_ctx *ctx, uint32_t count, const uint32_t *instances
     DeviceGuard guard(ctx->device);
     if (guard.status != hipSuccess)
         return hip_fail(guard.status, "hipSetDevice");
-    hipError_t e;
-    const size_t bytes = (size_t)count * sizeof(uint32_t);
-    if ((e = ctx->q_inst.ensure(bytes)) != hipSuccess || (e = ctx->q_cap.ensure(bytes)) != hipSuccess ||
-        (e = ctx->q_lambda.ensure(bytes)) != hipSuccess)
-        return hip_fail(e, "hipMalloc(queries)");
-    if ((e = hipMemcpyAsync(ctx->q_inst.ptr, inst.data(), bytes, hipMemcpyHostToDevice, ctx->stream)) != hipSuccess ||
-        (e = hipMemcpyAsync(ctx->q_cap.ptr, cap.data(), bytes, hipMemcpyHostToDevice, ctx->stream)) != hipSuccess ||
-        (e = hipMemcpyAsync(ctx->q_lambda.ptr, target_milli, bytes, hipMemcpyHostToDevice, ctx->stream)) != hipSuccess)
-        return hip_fail(e, "copy queries");
     alp::QueryDev q{};
-    q.inst = (const uint32_t *)ctx->q_inst.ptr;
-    q.capacity = (const uint32_t *)ctx->q_cap.ptr;
-    q.lambda = (const uint32_t *)ctx->q_lambda.ptr;
-    int32_t st = run_search(ctx, q, count);
+    int32_t st = upload_queries(ctx, count, inst.data(), cap.data(), target_milli, q);
     if (st != ALP_OK)
+        return st;
+    if ((st = run_search(ctx, q, count)) != ALP_OK)
         return st;
     memcpy(out, ctx->host_results, (size_t)count * sizeof(alp_result_t));
     return ALP_OK;
@@ -549,21 +598,16 @@ int32_t alp_max_throughput(alp_ctx *ctx, uint32_t count, const uint32_t *instanc
     DeviceGuard guard(ctx->device);
     if (guard.status != hipSuccess)
         return hip_fail(guard.status, "hipSetDevice");
+    alp::QueryDev q{};
+    int32_t st = upload_queries(ctx, count, inst.data(), cap.data(), zero.data(), q);
+    if (st != ALP_OK)
+        return st;
     hipError_t e;
     const size_t bytes = (size_t)count * sizeof(uint32_t);
     const uint64_t items_bytes = (uint64_t)count * ctx->sp.M * ctx->sp.O * sizeof(uint2);
-    if ((e = ctx->q_inst.ensure(bytes)) != hipSuccess || (e = ctx->q_cap.ensure(bytes)) != hipSuccess ||
-        (e = ctx->q_lambda.ensure(bytes)) != hipSuccess || (e = ctx->tmax.ensure(bytes)) != hipSuccess ||
-        (e = ctx->rec.ensure(items_bytes)) != hipSuccess || (e = ctx->ext.ensure(items_bytes)) != hipSuccess)
+    if ((e = ctx->tmax.ensure(bytes)) != hipSuccess || (e = ctx->rec.ensure(items_bytes)) != hipSuccess ||
+        (e = ctx->ext.ensure(items_bytes)) != hipSuccess)
         return hip_fail(e, "hipMalloc(max_throughput)");
-    if ((e = hipMemcpyAsync(ctx->q_inst.ptr, inst.data(), bytes, hipMemcpyHostToDevice, ctx->stream)) != hipSuccess ||
-        (e = hipMemcpyAsync(ctx->q_cap.ptr, cap.data(), bytes, hipMemcpyHostToDevice, ctx->stream)) != hipSuccess ||
-        (e = hipMemcpyAsync(ctx->q_lambda.ptr, zero.data(), bytes, hipMemcpyHostToDevice, ctx->stream)) != hipSuccess)
-        return hip_fail(e, "copy queries");
-    alp::QueryDev q{};
-    q.inst = (const uint32_t *)ctx->q_inst.ptr;
-    q.capacity = (const uint32_t *)ctx->q_cap.ptr;
-    q.lambda = (const uint32_t *)ctx->q_lambda.ptr;
     if ((e = alp::launch_option_terms(ctx->sp, ctx->tdev, q, count, (uint2 *)ctx->rec.ptr,
                                       (uint2 *)ctx->ext.ptr, nullptr, nullptr, ctx->stream)) != hipSuccess)
         return hip_fail(e, "option_terms launch");
@@ -682,13 +726,14 @@ void alp_free(alp_ctx *ctx)
     for (int k = 0; k < 4; ++k)
         if (ctx->ev[k])
             (void)hipEventDestroy(ctx->ev[k]);
-    DevBuf *bufs[] = {&ctx->tables, &ctx->q_inst, &ctx->q_cap, &ctx->q_lambda, &ctx->rec,
-                      &ctx->ext, &ctx->inner, &ctx->done, &ctx->winners, &ctx->idx, &ctx->evals,
-                      &ctx->tmax};
+    DevBuf *bufs[] = {&ctx->tables, &ctx->q_inst, &ctx->rec, &ctx->ext, &ctx->inner, &ctx->done,
+                      &ctx->winners, &ctx->idx, &ctx->evals, &ctx->tmax};
     for (DevBuf *b : bufs)
         b->release();
     if (ctx->host_results)
         (void)hipHostFree(ctx->host_results);
+    if (ctx->host_query)
+        (void)hipHostFree(ctx->host_query);
     delete ctx;
 }
 

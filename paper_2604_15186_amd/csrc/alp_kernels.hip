@@ -557,15 +557,26 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
                 jf[s] = has_inner ? kNoLatency : 0u;
             }
             if (has_inner) {
-                for (uint32_t j = 0; j < n_inner; ++j) {
-                    const uint2 v = inner[j];
+                // 16 records per step (two scalar loads), stop once every lane-slot has its j;
+                // the padding records are never feasible, so they never match.
+                for (uint32_t jb = 0; jb < n_inner_padded; jb += 16) {
+                    uint2 v[16];
+#pragma unroll
+                    for (int t = 0; t < 16; ++t)
+                        v[t] = inner[jb + t];
+#pragma unroll
+                    for (int t = 0; t < 16; ++t) {
+#pragma unroll
+                        for (int s = 0; s < S; ++s) {
+                            const bool hit = need[s] && jf[s] == kNoLatency &&
+                                             (int32_t)v[t].y >= w[s] && v[t].x == target[s];
+                            jf[s] = hit ? jb + t : jf[s];
+                        }
+                    }
                     bool open = false;
 #pragma unroll
-                    for (int s = 0; s < S; ++s) {
-                        if (need[s] && jf[s] == kNoLatency && (int32_t)v.y >= w[s] && v.x == target[s])
-                            jf[s] = j;
+                    for (int s = 0; s < S; ++s)
                         open |= need[s] && jf[s] == kNoLatency;
-                    }
                     if (!__any(open))
                         break;
                 }
