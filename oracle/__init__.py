@@ -77,8 +77,10 @@ def lib():
         L.orc_tmax_brute.argtypes = [P(_Inst), C.c_uint32, C.c_uint64, C.c_uint64,
                                      P(C.c_uint64)]
         L.orc_tmax_threshold.argtypes = [P(_Inst), C.c_uint32, C.c_void_p, P(C.c_uint64)]
+        L.orc_allocate.argtypes = [C.c_uint32, C.c_uint32, C.c_void_p, C.c_uint32, C.c_void_p,
+                                   P(C.c_uint64), P(C.c_uint64)]
         for f in (L.orc_option_term, L.orc_eval, L.orc_eval_many, L.orc_argmin, L.orc_tmax_brute,
-                  L.orc_tmax_threshold):
+                  L.orc_tmax_threshold, L.orc_allocate):
             f.restype = C.c_int
         _lib = L
     return _lib
@@ -177,3 +179,35 @@ def merge_argmin(parts: list) -> dict:
         if r["x"] is not None and (best["x"] is None or (r["L"], r["x"]) < (best["L"], best["x"])):
             best["x"], best["L"] = r["x"], r["L"]
     return best
+
+
+def workflow_latencies(batch: dict, lambdas, G_total: int) -> np.ndarray:
+    """L[w][g]: the search result's latency of workflow (instance) w at g GPUs, g = 0..G_total;
+    U64_NONE where infeasible.  Brute force per (w, g)."""
+    W = len(lambdas)
+    L = np.full((W, G_total + 1), U64_NONE, dtype=np.uint64)
+    for w in range(W):
+        inst = Instance(batch, w)
+        for g in range(G_total + 1):
+            r = argmin(inst, g, int(lambdas[w]))
+            if r["x"] is not None:
+                L[w, g] = r["L"]
+    return L
+
+
+EGALITARIAN, SOCIAL = 0, 1
+
+
+def allocate(L: np.ndarray, policy: int):
+    """Budget split over workflows for latency table L[w][g] (see orc_allocate).  Returns
+    (budgets, max latency, latency sum) or None if no split makes every workflow feasible."""
+    L = np.ascontiguousarray(L, dtype=np.uint64)
+    W, G1 = L.shape
+    g = np.zeros(W, dtype=np.uint32)
+    mx, sm = C.c_uint64(), C.c_uint64()
+    rc = lib().orc_allocate(W, G1 - 1, L.ctypes.data, policy, g.ctypes.data, C.byref(mx), C.byref(sm))
+    if rc < 0:
+        raise ValueError("bad arguments")
+    if rc == 1:
+        return None
+    return [int(v) for v in g], int(mx.value), int(sm.value)

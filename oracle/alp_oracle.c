@@ -267,3 +267,70 @@ int orc_tmax_threshold(const orc_instance *s, uint32_t G, orc_term *scratch /* [
     *out = best;
     return 0;
 }
+
+/* ---------------------------------------------------------------------------------------------
+ * Several workflows sharing a GPU pool (Section 5, "Scheduling multiple workflows"): every
+ * workflow w receives a whole number of GPUs g_w, sum g_w <= G, and its own search at budget g_w
+ * gives its latency L[w][g_w] (ORC_U64_NONE when infeasible).  The per-workflow utilities are
+ * combined by egalitarian welfare (policy 0: minimise the largest latency; ties by the smaller
+ * latency sum) or by social welfare (policy 1: minimise the latency sum); remaining ties go to
+ * the lexicographically smallest budget vector (g_0 first).
+ *
+ * Brute force: every budget vector in increasing lexicographic order, keeping a strictly better
+ * one.  L is row-major [W][G+1].  Returns 0 with g[] filled, 1 if no split makes every
+ * workflow feasible, -1 on bad arguments. */
+int orc_allocate(uint32_t W, uint32_t G, const uint64_t *L, uint32_t policy, uint32_t *g_out,
+                 uint64_t *max_out, uint64_t *sum_out)
+{
+    if (W == 0 || W > 16 || policy > 1)
+        return -1;
+    uint32_t g[16] = {0};
+    int found = 0;
+    uint64_t best_max = 0, best_sum = 0;
+    for (;;) {
+        uint32_t used = 0;
+        int ok = 1;
+        uint64_t mx = 0, sum = 0;
+        for (uint32_t w = 0; w < W; ++w) {
+            used += g[w];
+            uint64_t l = L[(size_t)w * (G + 1) + g[w]];
+            if (l == ORC_U64_NONE) {
+                ok = 0;
+                break;
+            }
+            if (l > mx)
+                mx = l;
+            sum += l;
+        }
+        if (ok && used <= G) {
+            int better;
+            if (!found)
+                better = 1;
+            else if (policy == 0)
+                better = mx < best_max || (mx == best_max && sum < best_sum);
+            else
+                better = sum < best_sum;
+            if (better) {
+                found = 1;
+                best_max = mx;
+                best_sum = sum;
+                for (uint32_t w = 0; w < W; ++w)
+                    g_out[w] = g[w];
+            }
+        }
+        /* next vector: the last workflow's budget varies fastest */
+        int w = (int)W - 1;
+        while (w >= 0 && g[w] == G) {
+            g[w] = 0;
+            --w;
+        }
+        if (w < 0)
+            break;
+        ++g[w];
+    }
+    if (!found)
+        return 1;
+    *max_out = best_max;
+    *sum_out = best_sum;
+    return 0;
+}

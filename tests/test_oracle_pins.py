@@ -301,3 +301,63 @@ def test_generator_is_deterministic():
     b = make_batch(2, [1])
     for k in ("W", "n", "p", "allowed", "rate", "lat", "u_ppm"):
         assert np.array_equal(a[k], b[k])
+
+
+# ------------------------------------------------------------------------------------------
+# Several workflows sharing a GPU pool (Section 5, scheduling multiple workflows).
+import json as _json  # noqa: E402
+import os as _os  # noqa: E402
+
+from alloc_dp import split as _split_dp  # noqa: E402
+
+_ALLOC = _json.load(open(_os.path.join(_os.path.dirname(__file__), "golden", "hand_cases.json")))[
+    "allocation_cases"]
+
+
+def _table(L):
+    return np.asarray([[oracle.U64_NONE if v is None else v for v in row] for row in L],
+                      dtype=np.uint64)
+
+
+def _expect(e):
+    return None if e is None else (e["g"], e["max"], e["sum"])
+
+
+@pytest.mark.parametrize("case", _ALLOC["tables"], ids=[c["id"] for c in _ALLOC["tables"]])
+def test_allocate_hand_tables(case):
+    for name, policy in (("egalitarian", oracle.EGALITARIAN), ("social", oracle.SOCIAL)):
+        got = oracle.allocate(_table(case["L"]), policy)
+        assert got == _expect(case[name]), (case["id"], name, got)
+        assert _split_dp(case["L"], case["G"], policy) == _expect(case[name])
+
+
+def test_allocate_hand_workflows():
+    spec = _ALLOC["workflows"]
+    cases = {c["id"]: c for c in CASES}
+    L = []
+    for cid, lam in zip(spec["cases"], spec["lambda"]):
+        inst = oracle.Instance(case_batch(cases[cid]), 0)
+        row = []
+        for g in range(len(spec["L"][0])):
+            r = oracle.argmin(inst, g, lam)
+            row.append(r["L"])
+        L.append(row)
+    assert L == spec["L"]
+    for q in spec["queries"]:
+        sub = [row[: q["G"] + 1] for row in L]
+        for name, policy in (("egalitarian", oracle.EGALITARIAN), ("social", oracle.SOCIAL)):
+            assert oracle.allocate(_table(sub), policy) == _expect(q[name]), (q, name)
+
+
+def test_allocate_brute_force_equals_threshold_dp():
+    rng = np.random.default_rng(5)
+    for trial in range(300):
+        W = int(rng.integers(1, 5))
+        G = int(rng.integers(0, 9))
+        L = []
+        for _ in range(W):
+            first = int(rng.integers(0, G + 2))           # fewest GPUs that make w feasible
+            vals = sorted(rng.integers(1, 40, size=G + 1).tolist(), reverse=True)
+            L.append([None if g < first else vals[g] for g in range(G + 1)])
+        for policy in (oracle.EGALITARIAN, oracle.SOCIAL):
+            assert oracle.allocate(_table(L), policy) == _split_dp(L, G, policy), (trial, L, G)
