@@ -150,6 +150,36 @@ int32_t alp_search_batch(alp_ctx *ctx, uint32_t count, const uint32_t *instances
 int32_t alp_max_throughput(alp_ctx *ctx, uint32_t count, const uint32_t *instances,
                            const uint32_t *gpu_budget, uint32_t *out_tmax);
 
+/* Several workflows sharing a pool of GPUs (Section 5, "Scheduling multiple workflows": the
+ * scheduler decides how many GPUs each workflow gets, searches each workflow's allocation
+ * independently, and combines the per-workflow utilities with egalitarian or social welfare).
+ * Workflow w is loaded instance instances[w] with target rate target_milli[w].  It gets g_w whole
+ * GPUs, sum g_w <= total_gpus, and its search result at budget g_w; its utility is minus that
+ * latency (a workflow with no feasible allocation makes the split infeasible).
+ *   ALP_WELFARE_EGALITARIAN: minimise the largest workflow latency, ties by the latency sum;
+ *   ALP_WELFARE_SOCIAL:      minimise the latency sum;
+ * remaining ties go to the lexicographically smallest budget vector (workflow 0 first), so GPUs
+ * that improve nothing stay unassigned. */
+#define ALP_WELFARE_EGALITARIAN 0u
+#define ALP_WELFARE_SOCIAL 1u
+
+/* Outcome of alp_allocate_workflows (24 bytes). */
+typedef struct {
+    uint32_t status;           /* ALP_OK or ALP_INFEASIBLE */
+    uint32_t policy;
+    uint32_t max_latency_us;   /* largest workflow latency of the split (0 if infeasible) */
+    uint32_t gpus_used;        /* sum of the budgets */
+    uint64_t sum_latency_us;   /* sum of the workflow latencies */
+} alp_plan_t;
+
+/* Runs every (workflow, budget 0..total_gpus) search in one batch on the device, then the
+ * split.  count in 1..16, total_gpus in 0..1024, instances may be NULL (0..count-1).
+ * On ALP_OK and ALP_INFEASIBLE writes *plan; on ALP_OK also gpus[w] and results[w] (workflow
+ * w's search result at g_w).  Returns ALP_INFEASIBLE if no split makes every workflow feasible. */
+int32_t alp_allocate_workflows(alp_ctx *ctx, uint32_t count, const uint32_t *instances,
+                               const uint32_t *target_milli, uint32_t total_gpus, uint32_t policy,
+                               alp_plan_t *plan, uint32_t *gpus, alp_result_t *results);
+
 /* Evaluates count given candidate indices (each < O^M, else EINVAL) of one instance. */
 int32_t alp_eval_candidates(alp_ctx *ctx, uint32_t instance, uint32_t gpu_budget,
                             uint32_t target_milli, const uint64_t *indices, uint64_t count,

@@ -21,7 +21,7 @@ MAX_LLMS = 8
 
 # Symbols declared in include/alp.h.
 EXPORTS = ("alp_load_profiles", "alp_search", "alp_search_batch", "alp_max_throughput",
-           "alp_eval_candidates", "alp_set_launch", "alp_set_timing", "alp_kernel_times",
+           "alp_allocate_workflows", "alp_eval_candidates", "alp_set_launch", "alp_set_timing", "alp_kernel_times",
            "alp_num_candidates", "alp_free", "alp_status_str", "alp_last_error")
 
 
@@ -44,7 +44,10 @@ RESULT_DTYPE = np.dtype([("index", np.uint64), ("latency_us", np.uint32),
                          ("replicas", np.uint8, 8)])
 EVAL_DTYPE = np.dtype([("flags", np.uint32), ("latency_us", np.uint32),
                        ("throughput_milli", np.uint32), ("gpu_units", np.uint32)])
-assert RESULT_DTYPE.itemsize == 48 and EVAL_DTYPE.itemsize == 16
+PLAN_DTYPE = np.dtype([("status", np.uint32), ("policy", np.uint32), ("max_latency_us", np.uint32),
+                       ("gpus_used", np.uint32), ("sum_latency_us", np.uint64)])
+assert RESULT_DTYPE.itemsize == 48 and EVAL_DTYPE.itemsize == 16 and PLAN_DTYPE.itemsize == 24
+WELFARE_EGALITARIAN, WELFARE_SOCIAL = 0, 1
 
 _lib = None
 
@@ -63,12 +66,13 @@ def lib():
         L.alp_search_batch.argtypes = [vp, u32, vp, vp, vp, vp]
         L.alp_max_throughput.argtypes = [vp, u32, vp, vp, vp]
         L.alp_eval_candidates.argtypes = [vp, u32, u32, u32, vp, u64, vp]
+        L.alp_allocate_workflows.argtypes = [vp, u32, vp, vp, u32, u32, vp, vp, vp]
         L.alp_set_launch.argtypes = [vp, u32, u32, u32]
         L.alp_set_timing.argtypes = [vp, i32]
         L.alp_kernel_times.argtypes = [vp, C.POINTER(C.c_float), C.POINTER(u32)]
         L.alp_num_candidates.argtypes = [vp, C.POINTER(u64)]
         for name in ("alp_load_profiles", "alp_search", "alp_search_batch", "alp_max_throughput",
-                     "alp_eval_candidates", "alp_set_launch", "alp_set_timing",
+                     "alp_allocate_workflows", "alp_eval_candidates", "alp_set_launch", "alp_set_timing",
                      "alp_kernel_times", "alp_num_candidates"):
             getattr(L, name).restype = i32
         L.alp_free.argtypes = [vp]
@@ -191,6 +195,23 @@ class Context:
         _check(lib().alp_max_throughput(self._ctx, len(G), None if inst is None else _ptr(inst),
                                         _ptr(G), _ptr(out)))
         return out
+
+    def allocate_workflows(self, target_milli, total_gpus: int, policy: int = WELFARE_EGALITARIAN,
+                           instances=None):
+        """Splits total_gpus over workflows (alp_allocate_workflows).  Returns (plan record,
+        budgets, per-workflow results); budgets and results are None when infeasible."""
+        lam = np.ascontiguousarray(target_milli, dtype=np.uint32)
+        W = len(lam)
+        inst = None if instances is None else np.ascontiguousarray(instances, dtype=np.uint32)
+        plan = np.zeros(1, dtype=PLAN_DTYPE)
+        gpus = np.zeros(W, dtype=np.uint32)
+        res = np.zeros(W, dtype=RESULT_DTYPE)
+        st = _check(lib().alp_allocate_workflows(self._ctx, W, None if inst is None else _ptr(inst),
+                                                 _ptr(lam), total_gpus, policy, _ptr(plan),
+                                                 _ptr(gpus), _ptr(res)), (ALP_OK, ALP_INFEASIBLE))
+        if st == ALP_INFEASIBLE:
+            return plan[0], None, None
+        return plan[0], gpus, res
 
     def eval_candidates(self, instance: int, gpu_budget: int, target_milli: int, indices) -> np.ndarray:
         idx = np.ascontiguousarray(indices, dtype=np.uint64)

@@ -100,6 +100,9 @@ struct alp_ctx {
     alp::TablesDev tdev{};
 
     DevBuf q_inst, rec, ext, inner, done, winners, idx, evals, tmax;   // q_inst: inst | cap | lambda
+    DevBuf split_dp;                        // allocate_kernel's knapsack table
+    uint32_t *host_split = nullptr;         // mapped pinned: alp_plan_t (6 words) + budgets[16]
+    uint32_t *host_split_dev = nullptr;
     uint32_t *host_query = nullptr;         // pinned staging of batch queries: inst | cap | lambda
     size_t host_query_cap = 0;
     alp_result_t *host_results = nullptr;   // pinned host memory the kernels write results to
@@ -623,6 +626,74 @@ int32_t alp_max_throughput(alp_ctx *ctx, uint32_t count, const uint32_t *instanc
     return ALP_OK;
 }
 
+int32_t alp_allocate_workflows(alp_ctx *ctx, uint32_t count, const uint32_t *instances,
+                               const uint32_t *target_milli, uint32_t total_gpus, uint32_t policy,
+                               alp_plan_t *plan, uint32_t *gpus, alp_result_t *results)
+{
+    if (!ctx)
+        return fail(ALP_EINVAL, "ctx is NULL");
+    if (count < 1 || count > 16)
+        return fail(ALP_EINVAL, "count %u outside 1..16", count);
+    if (total_gpus > 1024)
+        return fail(ALP_EINVAL, "total_gpus %u above 1024", total_gpus);
+    if (policy > ALP_WELFARE_SOCIAL)
+        return fail(ALP_EINVAL, "policy %u unknown", policy);
+    if (!target_milli || !plan || !gpus || !results)
+        return fail(ALP_EINVAL, "target_milli, plan, gpus or results is NULL");
+    const uint32_t G1 = total_gpus + 1, items = count * G1;
+    std::vector<uint32_t> inst(items), cap(items), lam(items);
+    for (uint32_t w = 0; w < count; ++w) {
+        const uint32_t iw = instances ? instances[w] : w;
+        int32_t st = check_instance(ctx, iw);
+        if (st != ALP_OK)
+            return st;
+        for (uint32_t g = 0; g < G1; ++g) {
+            inst[w * G1 + g] = iw;
+            cap[w * G1 + g] = capacity_of(ctx, g);
+            lam[w * G1 + g] = target_milli[w];
+        }
+    }
+    DeviceGuard guard(ctx->device);
+    if (guard.status != hipSuccess)
+        return hip_fail(guard.status, "hipSetDevice");
+    hipError_t e;
+    if (!ctx->host_split) {
+        if ((e = hipHostMalloc((void **)&ctx->host_split, 32 * sizeof(uint32_t), hipHostMallocMapped)) !=
+            hipSuccess)
+            return hip_fail(e, "hipHostMalloc(split)");
+        if ((e = hipHostGetDevicePointer((void **)&ctx->host_split_dev, ctx->host_split, 0)) != hipSuccess) {
+            (void)hipHostFree(ctx->host_split);
+            ctx->host_split = nullptr;
+            return hip_fail(e, "hipHostGetDevicePointer(split)");
+        }
+    }
+    if ((e = ctx->split_dp.ensure((uint64_t)(count + 1) * G1 * sizeof(uint64_t) +
+                                  2ull * count * G1 * sizeof(uint32_t))) != hipSuccess)
+        return hip_fail(e, "hipMalloc(split)");
+    alp::QueryDev q{};
+    int32_t st = upload_queries(ctx, items, inst.data(), cap.data(), lam.data(), q);
+    if (st != ALP_OK)
+        return st;
+    // All (workflow, budget) searches; run_search synchronises, so the results are complete.
+    if ((st = run_search(ctx, q, items)) != ALP_OK)
+        return st;
+    alp_plan_t *dplan = reinterpret_cast<alp_plan_t *>(ctx->host_split_dev);
+    uint32_t *dgpus = ctx->host_split_dev + 8;
+    if ((e = alp::launch_allocate(ctx->host_results_dev, count, total_gpus, policy,
+                                  (uint64_t *)ctx->split_dp.ptr, dplan, dgpus, ctx->stream)) != hipSuccess)
+        return hip_fail(e, "allocate launch");
+    if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess)
+        return hip_fail(e, "hipStreamSynchronize");
+    memcpy(plan, ctx->host_split, sizeof(alp_plan_t));
+    if (plan->status != ALP_OK)
+        return ALP_INFEASIBLE;
+    for (uint32_t w = 0; w < count; ++w) {
+        gpus[w] = ctx->host_split[8 + w];
+        results[w] = ctx->host_results[w * G1 + gpus[w]];
+    }
+    return ALP_OK;
+}
+
 int32_t alp_eval_candidates(alp_ctx *ctx, uint32_t instance, uint32_t gpu_budget,
                             uint32_t target_milli, const uint64_t *indices, uint64_t count,
                             alp_eval_t *out)
@@ -727,13 +798,15 @@ void alp_free(alp_ctx *ctx)
         if (ctx->ev[k])
             (void)hipEventDestroy(ctx->ev[k]);
     DevBuf *bufs[] = {&ctx->tables, &ctx->q_inst, &ctx->rec, &ctx->ext, &ctx->inner, &ctx->done,
-                      &ctx->winners, &ctx->idx, &ctx->evals, &ctx->tmax};
+                      &ctx->winners, &ctx->idx, &ctx->evals, &ctx->tmax, &ctx->split_dp};
     for (DevBuf *b : bufs)
         b->release();
     if (ctx->host_results)
         (void)hipHostFree(ctx->host_results);
     if (ctx->host_query)
         (void)hipHostFree(ctx->host_query);
+    if (ctx->host_split)
+        (void)hipHostFree(ctx->host_split);
     delete ctx;
 }
 

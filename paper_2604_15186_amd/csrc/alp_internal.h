@@ -92,6 +92,12 @@ hipError_t launch_eval(const SpaceDev &sp, uint32_t capacity, const uint2 *rec, 
 hipError_t launch_tmax(const SpaceDev &sp, const QueryDev &q, uint32_t count, const uint2 *ext,
                        uint32_t *out, hipStream_t st);
 
+// Budget split over W workflows from their per-budget search results (res[w * (G + 1) + g]),
+// see alp_allocate_workflows.  dp: device scratch of (W + 1) * (G + 1) uint64 followed by
+// 2 * W * (G + 1) uint32.  Writes *plan and gpus[0..W).
+hipError_t launch_allocate(const alp_result_t *res, uint32_t W, uint32_t G, uint32_t policy,
+                           uint64_t *dp, alp_plan_t *plan, uint32_t *gpus, hipStream_t st);
+
 // Resident blocks per CU of the scan kernels at a given block size (occupancy query).
 int scan_blocks_per_cu(uint32_t variant, uint32_t slots, uint32_t threads, const SpaceDev &sp);
 

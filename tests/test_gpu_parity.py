@@ -190,7 +190,9 @@ SHAPES = [
     (35, 2, (1, 2, 4, 8), (1, 2, 3, 4), 13, 8, 24, 2),     # O = 208 (four slots)
     (36, 2, (1, 2, 4, 8, 16), (1, 2, 4, 8), 16, 6, 40, 2),  # O = 320 (eight slots), Q = 8
     (37, 4, (1, 2), (4,), 4, 2, 8, 3),                      # O = 8, M = 4
-    (38, 6, (1, 2), (2, 4), 2, 2, 10, 1),                   # O = 8, M = 6 (three outer digits)
+    (38, 6, (1, 2), (2, 4), 2, 2, 10, 1),                   # O = 8, M = 6 (four outer digits)
+    (39, 8, (1, 2), (4,), 1, 2, 12, 1),                     # O = 2, M = 8 (largest M)
+    (40, 2, (1, 2, 4, 8), (1, 2, 3, 4, 5, 6, 7, 8), 16, 16, 48, 1),  # O = 512, K = 16 (maxima)
 ]
 
 
@@ -198,6 +200,8 @@ SHAPES = [
 def test_ragged_and_degenerate_spaces(alp, spec):
     seed, M, tps, fqs, D, K, G, count = spec
     Q = 8 if max(fqs) > 4 else 4
+    if len(fqs) == 8:
+        Q = 8
     b = make_custom(seed, M, tps, fqs, D, K, G, count=count, frac_den=Q, deny_prob=0.1,
                     param_range=(0.5e9, 400e9))
     with alp.Context(b) as ctx:
@@ -267,3 +271,49 @@ def test_many_ties_keep_lowest_index(alp, seed):
                 for variant in (1, 2, 3):
                     ctx.set_launch(variant)
                     check_result(b, i, ctx.search(i, G, lam), *want)
+
+
+# ------------------------------------------------------------------------------------------
+# Several workflows sharing a GPU pool.
+def _alloc_case(cfg, insts, G_total):
+    b = make_batch(cfg, insts)
+    W = len(insts)
+    share = G_total // W
+    lam = [target_from_tmax(int(b["u_ppm"][i]), oracle.tmax(oracle.Instance(b, i), share))
+           for i in range(W)]
+    return b, lam
+
+
+@pytest.mark.parametrize("cfg,insts,G_total", [(0, [3, 17, 42, 99], 20), (1, [0, 7, 21], 12),
+                                               (0, [5], 9), (1, [2, 11], 40)])
+def test_allocate_workflows_matches_oracle(alp, cfg, insts, G_total):
+    b, lam = _alloc_case(cfg, insts, G_total)
+    L = oracle.workflow_latencies(b, lam, G_total)
+    with alp.Context(b) as ctx:
+        for policy in (oracle.EGALITARIAN, oracle.SOCIAL):
+            want = oracle.allocate(L, policy)
+            plan, gpus, res = ctx.allocate_workflows(lam, G_total, policy)
+            assert int(plan["policy"]) == policy
+            if want is None:
+                assert int(plan["status"]) == 5 and gpus is None
+                continue
+            g, mx, sm = want
+            assert int(plan["status"]) == 0
+            assert [int(v) for v in gpus] == g
+            assert (int(plan["max_latency_us"]), int(plan["sum_latency_us"]),
+                    int(plan["gpus_used"])) == (mx, sm, sum(g))
+            for w in range(len(insts)):
+                check_result(b, w, res[w], *oracle_expect(b, w, g[w], lam[w]))
+
+
+def test_allocate_workflows_infeasible_and_edges(alp):
+    b, lam = _alloc_case(1, [0, 1, 2], 12)
+    with alp.Context(b) as ctx:
+        plan, gpus, res = ctx.allocate_workflows(lam, 0, oracle.EGALITARIAN)
+        assert int(plan["status"]) == 5 and gpus is None
+        plan, gpus, res = ctx.allocate_workflows([10**9, lam[1], lam[2]], 12, oracle.SOCIAL)
+        assert int(plan["status"]) == 5
+        with pytest.raises(alp.AlpError):
+            ctx.allocate_workflows(lam, 12, 7)
+        with pytest.raises(alp.AlpError):
+            ctx.allocate_workflows([1] * 17, 12)
