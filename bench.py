@@ -4,7 +4,8 @@
 
 One step = one complete search (alp_search: per-option terms, exhaustive scan of every
 candidate, final reduction and result decode, result copied to the host) over the synthetic
-workload.  The default workload is the 5-LLM space with G = 64 GPUs and 128 options per LLM
+workload; for ``--workload multi`` it is one alp_allocate_workflows call (every per-workflow
+budget searched exhaustively, then the budget split).  The default workload is the 5-LLM space with G = 64 GPUs and 128 options per LLM
 (2^35 = 34,359,738,368 candidates per step).  Inputs are resident in HBM before timing starts.
 Prints one JSON line.
 
@@ -31,7 +32,10 @@ from workloads import CONFIGS, make_batch, target_from_tmax  # noqa: E402
 
 PEAK_LANE_OPS = 256 * 64 * 2.4e9        # int32 VALU lane-ops/s of MI355X
 OPS_PER_CANDIDATE = 2                   # budget compare + objective min
-WORKLOADS = {"cfg2": 2, "cfg3": 3, "cfg4": 4, "cfg1": 1}
+WORKLOADS = {"cfg2": 2, "cfg3": 3, "cfg4": 4, "cfg1": 1, "multi": 2}
+# Several workflows sharing one GPU pool: four 4-LLM workflows drawn like the 4-LLM workload
+# split 32 GPUs under egalitarian welfare; each workflow's target is set at an even share.
+MULTI_WORKFLOWS, MULTI_GPUS = 4, 32
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "scan_min_hbm_bytes.md")
 
 
@@ -101,17 +105,26 @@ def main():
         sys.exit(1)
     cfg_id = WORKLOADS[args.workload]
     cfg = CONFIGS[cfg_id]
-    insts = list(range(cfg.num_instances)) if cfg_id == 4 else [0]
+    multi = args.workload == "multi"
+    if multi:
+        insts = list(range(MULTI_WORKFLOWS))
+    else:
+        insts = list(range(cfg.num_instances)) if cfg_id == 4 else [0]
     batch = make_batch(cfg_id, insts)
     ctx = alp.Context(batch)
     ctx.set_launch(args.variant)
     G = batch["G"]
+    if multi:
+        G = np.full(len(insts), MULTI_GPUS // MULTI_WORKFLOWS, dtype=np.uint32)
     tmax = ctx.max_throughput(G)
     lam = np.asarray([target_from_tmax(int(batch["u_ppm"][i]), int(tmax[i]))
                       for i in range(len(insts))], dtype=np.uint32)
-    per_step = ctx.num_candidates * len(insts)
+    per_step = ctx.num_candidates * len(insts) * ((MULTI_GPUS + 1) if multi else 1)
 
     def step():
+        if multi:
+            plan = ctx.allocate_workflows(lam, MULTI_GPUS, alp.WELFARE_EGALITARIAN)[0]
+            return int(plan["status"])
         if cfg_id == 4:
             out = ctx.search_batch(G, lam)
             return int(out["status"].max())
@@ -130,7 +143,7 @@ def main():
     elapsed = time.perf_counter() - t0
     ctx.set_timing(False)
     assert status in (0, 5)
-    terms_ms, _, _, blocks = ctx.kernel_times()
+    terms_ms, _, split_ms, blocks = ctx.kernel_times()
 
     value = per_step * args.steps / elapsed
     avg_scan_s = float(np.mean(scan_ms)) / 1e3
@@ -149,9 +162,13 @@ def main():
         "vs_baseline": None,
         "dtype": "u32",
         "data": "synthetic (seeded profile tables, see workloads/)",
-        "config": {"workload": f"{cfg.name}: {cfg.description}",
+        "config": {"workload": (f"{MULTI_WORKFLOWS} workflows of {cfg.num_llms} LLMs share "
+                                f"{MULTI_GPUS} GPUs (egalitarian welfare): all "
+                                f"{MULTI_WORKFLOWS * (MULTI_GPUS + 1)} per-workflow budget "
+                                "searches, then the budget split") if multi
+                   else f"{cfg.name}: {cfg.description}",
                    "candidates_per_step": per_step, "instances": len(insts),
-                   "llms": cfg.num_llms, "gpu_budget": cfg.gpu_budget,
+                   "llms": cfg.num_llms, "gpu_budget": MULTI_GPUS if multi else cfg.gpu_budget,
                    "options_per_llm": len(cfg.tp_values) * len(cfg.frac_q) * cfg.max_replicas,
                    "scan_blocks": blocks},
         "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_LANE_OPS / 1e12,
@@ -159,7 +176,7 @@ def main():
                      "traffic": _traffic(digest, args.workload),
                      "kernel": "scan", "kernel_ms": avg_scan_s * 1e3,
                      "ops_per_candidate": OPS_PER_CANDIDATE,
-                     "other_kernels_ms": {"option_terms": terms_ms}},
+                     "other_kernels_ms": {"option_terms": terms_ms, "budget_split": split_ms}},
         "cpu_baseline": None,
     }
     if not args.no_cpu_baseline:

@@ -194,8 +194,8 @@ int32_t alp_set_launch(alp_ctx *ctx, uint32_t variant, uint32_t blocks_per_item,
 /* Enables (1) or disables (0) HIP-event timing of the searches' kernels on the context stream.
  * alp_kernel_times writes, for the last search or batch, the milliseconds of the option-term
  * kernel (ms[0]) and of the candidate scan kernel, which includes the final reduction and the
- * result write (ms[1]); ms[2] is 0 (no separate reduction kernel).  *scan_blocks receives the
- * scan kernel's grid size in blocks. */
+ * result write (ms[1]); ms[2] is the budget-split kernel of alp_allocate_workflows, 0 after the
+ * other calls.  *scan_blocks receives the scan kernel's grid size in blocks. */
 int32_t alp_set_timing(alp_ctx *ctx, int32_t enable);
 int32_t alp_kernel_times(alp_ctx *ctx, float ms[3], uint32_t *scan_blocks);
 

@@ -227,7 +227,7 @@ class Context:
         _check(lib().alp_set_timing(self._ctx, 1 if enable else 0))
 
     def kernel_times(self):
-        """(option-term ms, scan ms, final ms, scan blocks) of the last search."""
+        """(option-term ms, scan ms, budget-split ms, scan blocks) of the last call."""
         ms = (C.c_float * 3)()
         blocks = C.c_uint32()
         _check(lib().alp_kernel_times(self._ctx, ms, C.byref(blocks)))

@@ -239,6 +239,34 @@ int blocks_per_cu(alp_ctx *c, uint32_t variant, uint32_t slots, uint32_t threads
     return slot;
 }
 
+// Blocks per item for a grid of `count` items.  Blocks are dispatched as resident slots free
+// up, so a grid runs in rounds of `resident` blocks; a last round that is only partly filled
+// leaves the chip idle while it runs, and one round alone ends with a long tail.  The grid is
+// sized for about kRounds full rounds: among the block counts that end exactly at a round
+// boundary (k * resident / count per item, k = 1 .. kRounds), the one with the least time per
+// unit of work -- (rounds + a quarter-round tail) / blocks -- is taken.
+uint64_t blocks_per_item_for_rounds(uint64_t count, uint64_t resident, uint64_t max_bpi)
+{
+    constexpr uint64_t kRounds = 4;
+    if (count == 0 || resident == 0)
+        return 1;
+    uint64_t best = 1;
+    double best_cost = (double)ceil_div(count, resident) + 0.25;
+    for (uint64_t k = 1; k <= kRounds; ++k) {
+        uint64_t bpi = k * resident / count;
+        if (bpi > max_bpi)
+            bpi = max_bpi;
+        if (bpi < 1)
+            continue;
+        const double cost = ((double)ceil_div(count * bpi, resident) + 0.25) / (double)bpi;
+        if (cost < best_cost) {
+            best_cost = cost;
+            best = bpi;
+        }
+    }
+    return best;
+}
+
 alp::ScanGeometry plan_scan(alp_ctx *c, uint32_t count)
 {
     alp::ScanGeometry g{};
@@ -250,29 +278,19 @@ alp::ScanGeometry plan_scan(alp_ctx *c, uint32_t count)
         g.rows = 1;
         for (uint32_t m = 2; m < sp.M; ++m)
             g.rows *= sp.O;
-        // Blocks of 8 waves (fewer blocks, fewer end-of-block reductions; measured best on the
-        // 4,096-instance batch), at most one wave per row; waves per item = resident waves /
-        // items, at least one block per item.
-        const uint64_t resident_waves =
-            cus * (uint64_t)blocks_per_cu(c, g.variant, g.slots, 512) * 8;
-        // Each wave gets at least kMinRowsPerWave rows when the item has that many: a wave's
-        // fixed costs (setup, end-of-wave re-scan, block reduction) then stay small.
+        // Blocks of 8 waves (fewer blocks, fewer end-of-block reductions), at most one wave per
+        // row.  Each wave gets at least kMinRowsPerWave rows when the item has that many, so a
+        // wave's fixed costs (setup, end-of-wave re-scan, block reduction) stay small.
         constexpr uint64_t kMinRowsPerWave = 8;
-        uint64_t per_item = count ? ceil_div(resident_waves, count) : 1;
-        const uint64_t max_waves = g.rows >= kMinRowsPerWave ? g.rows / kMinRowsPerWave : 1;
-        if (per_item > max_waves)
-            per_item = max_waves;
-        if (per_item < 1)
-            per_item = 1;
         g.threads = c->tpb_override ? c->tpb_override
                                     : (uint32_t)(64 * (g.rows < 8 ? g.rows : 8));
         const uint32_t wpb = g.threads / 64;
-        uint64_t bpi = c->bpi_override ? c->bpi_override : ceil_div(per_item, wpb);
-        const uint64_t max_bpi = ceil_div(g.rows, wpb);
-        if (!c->bpi_override && bpi > max_bpi)
-            bpi = max_bpi;
-        if (bpi < 1)
-            bpi = 1;
+        const uint64_t max_waves = g.rows >= kMinRowsPerWave ? g.rows / kMinRowsPerWave : 1;
+        const uint64_t max_bpi = ceil_div(max_waves, wpb);
+        uint64_t bpi = c->bpi_override;
+        if (!bpi)
+            bpi = blocks_per_item_for_rounds(
+                count, cus * (uint64_t)blocks_per_cu(c, g.variant, g.slots, g.threads), max_bpi);
         g.rows_per_wave = ceil_div(g.rows, bpi * wpb);
         if (!c->bpi_override)
             bpi = ceil_div(g.rows, g.rows_per_wave * wpb);
@@ -679,11 +697,17 @@ int32_t alp_allocate_workflows(alp_ctx *ctx, uint32_t count, const uint32_t *ins
         return st;
     alp_plan_t *dplan = reinterpret_cast<alp_plan_t *>(ctx->host_split_dev);
     uint32_t *dgpus = ctx->host_split_dev + 8;
+    if (ctx->timing && (e = hipEventRecord(ctx->ev[2], ctx->stream)) != hipSuccess)
+        return hip_fail(e, "hipEventRecord");
     if ((e = alp::launch_allocate(ctx->host_results_dev, count, total_gpus, policy,
                                   (uint64_t *)ctx->split_dp.ptr, dplan, dgpus, ctx->stream)) != hipSuccess)
         return hip_fail(e, "allocate launch");
+    if (ctx->timing && (e = hipEventRecord(ctx->ev[3], ctx->stream)) != hipSuccess)
+        return hip_fail(e, "hipEventRecord");
     if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess)
         return hip_fail(e, "hipStreamSynchronize");
+    if (ctx->timing && (e = hipEventElapsedTime(&ctx->last_ms[2], ctx->ev[2], ctx->ev[3])) != hipSuccess)
+        return hip_fail(e, "hipEventElapsedTime");
     memcpy(plan, ctx->host_split, sizeof(alp_plan_t));
     if (plan->status != ALP_OK)
         return ALP_INFEASIBLE;
