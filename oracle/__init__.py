@@ -53,6 +53,11 @@ class _Argmin(C.Structure):
                 ("sum_L", C.c_uint64)]
 
 
+class _Pruned(C.Structure):
+    _fields_ = [("best_x", C.c_uint64), ("best_L", C.c_uint64), ("vectors", C.c_uint64),
+                ("unpruned", C.c_uint64)]
+
+
 EVAL_DTYPE = np.dtype([("flags", np.uint32), ("L", np.uint64), ("T", np.uint64), ("U", np.uint64)],
                       align=True)
 
@@ -79,8 +84,16 @@ def lib():
         L.orc_tmax_threshold.argtypes = [P(_Inst), C.c_uint32, C.c_void_p, P(C.c_uint64)]
         L.orc_allocate.argtypes = [C.c_uint32, C.c_uint32, C.c_void_p, C.c_uint32, C.c_void_p,
                                    P(C.c_uint64), P(C.c_uint64)]
+        L.orc_pruned.argtypes = [P(_Inst), C.c_uint32, C.c_uint32, C.c_uint32, C.c_void_p,
+                                 P(_Pruned)]
+        L.orc_fits.argtypes = [C.c_uint32, C.c_uint64, C.c_uint64, C.c_uint64, C.c_uint64,
+                               C.c_uint64]
+        L.orc_count_fractions.argtypes = [C.c_uint32, C.c_uint64, C.c_void_p, C.c_int]
+        L.orc_count_fractions.restype = C.c_uint64
+        L.orc_binomial.argtypes = [C.c_uint64, C.c_uint64]
+        L.orc_binomial.restype = C.c_uint64
         for f in (L.orc_option_term, L.orc_eval, L.orc_eval_many, L.orc_argmin, L.orc_tmax_brute,
-                  L.orc_tmax_threshold, L.orc_allocate):
+                  L.orc_tmax_threshold, L.orc_allocate, L.orc_pruned, L.orc_fits):
             f.restype = C.c_int
         _lib = L
     return _lib
@@ -211,3 +224,32 @@ def allocate(L: np.ndarray, policy: int):
     if rc == 1:
         return None
     return [int(v) for v in g], int(mx.value), int(sm.value)
+
+
+PRUNE_ORDER, PRUNE_MIN = 1, 2
+
+
+def pruned(inst: Instance, G: int, lam: int, flags: int = PRUNE_ORDER | PRUNE_MIN) -> dict:
+    """The paper's pruned fraction-enumeration search (see orc_pruned)."""
+    r = _Pruned()
+    if lib().orc_pruned(C.byref(inst.c), G, lam, flags, inst._scratch, C.byref(r)) != 0:
+        raise ValueError("bad arguments")
+    none = r.best_x == U64_NONE
+    return {"x": None if none else int(r.best_x), "L": None if none else int(r.best_L),
+            "vectors": int(r.vectors), "unpruned": int(r.unpruned)}
+
+
+def fits(Q: int, a: int, f: int, tp: int, q: int, d: int) -> bool:
+    """Placement test of step 3 (see orc_fits)."""
+    return bool(lib().orc_fits(Q, a, f, tp, q, d))
+
+
+def count_fractions(M: int, total: int, lo, ordered: bool) -> int:
+    """Number of step-1 fraction vectors for lower bounds lo (per position)."""
+    lo = np.ascontiguousarray(lo, dtype=np.uint64)
+    assert len(lo) == M
+    return int(lib().orc_count_fractions(M, total, lo.ctypes.data, 1 if ordered else 0))
+
+
+def binomial(n: int, k: int) -> int:
+    return int(lib().orc_binomial(n, k))

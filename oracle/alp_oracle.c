@@ -16,7 +16,9 @@
  *     minimum fractions that hold the parameters), the target rate is sustained (T_w >= lambda,
  *     Section 3 "lowest latency within a target workflow-level arrival rate"), and the GPU
  *     budget is respected;
- *   - the search result: the feasible candidate of lowest L_w, ties broken by lowest index.
+ *   - the search result: the feasible candidate of lowest L_w, ties broken by lowest index;
+ *   - the paper's own pruned search over GPU fractions (Section 5, steps 1-3), and the split of
+ *     a GPU pool over several workflows (Section 5, scheduling multiple workflows).
  *
  * Fixed-point readings (the paper computes in reals):
  *   rates in milli-requests/s, latencies in microseconds, n_m and p_m in milli-units;
@@ -332,5 +334,218 @@ int orc_allocate(uint32_t W, uint32_t G, const uint64_t *L, uint32_t policy, uin
         return 1;
     *max_out = best_max;
     *sum_out = best_sum;
+    return 0;
+}
+
+/* ---------------------------------------------------------------------------------------------
+ * The paper's own pruned search (Section 5, steps 1-3).  It looks at a subset of the candidates
+ * and so need not reach the exhaustive optimum.  Read as follows.
+ *
+ *  1. Enumerate GPU fractions: LLM m receives f_m units of 1/Q GPU, sum f_m = Q*G.
+ *     ORC_PRUNE_ORDER: the LLMs are ordered by profiled latency ratio -- ref_m, the contribution
+ *     lat * n_m / p_m at the smallest TP degree, the largest share and the first profiled point,
+ *     largest first, ties by LLM index -- and no LLM receives more units than the one before it.
+ *     ORC_PRUNE_MIN: each LLM receives at least the units that hold its weights,
+ *     lo_m = max(1, ceil(W_m * Q / H)), and at most Q*G minus the lower bounds of the LLMs after
+ *     it in the order.  Without the flags the order is still used for packing, lo = 0 and the
+ *     upper bound is Q*G.
+ *  2. Pack the fractions contiguously in that order: the k-th LLM occupies units [a_k, a_k + f)
+ *     of the Q*G units laid out GPU after GPU.
+ *  3. Resolve parallelism: option (tp, q, d) is admissible for an LLM iff tp * q * d = f (the
+ *     fraction is used exactly, every rank with the same share) and d replicas of tp ranks of q
+ *     units each, the ranks of one replica on distinct GPUs, fit the LLM's packed GPUs.
+ *
+ * The result is the feasible admissible candidate of lowest L_w, ties to the lowest index.
+ * ------------------------------------------------------------------------------------------- */
+
+#define ORC_PRUNE_ORDER 1u
+#define ORC_PRUNE_MIN 2u
+
+typedef struct {
+    uint64_t best_x;    /* ORC_U64_NONE if no admissible candidate is feasible */
+    uint64_t best_L;
+    uint64_t vectors;   /* fraction vectors enumerated in step 1 */
+    uint64_t unpruned;  /* C(Q*G + M - 1, M - 1): every fraction vector, saturating */
+} orc_pruned_out;
+
+/* Does an LLM holding units [a, a + f) fit d replicas of tp ranks of q units, the ranks of a
+ * replica on distinct GPUs?  GPU g, holding h_g of the LLM's units, takes at most floor(h_g/q)
+ * ranks and at most one rank of each replica, so at most min(floor(h_g/q), d).  The sum of these
+ * reaching tp * d is also enough: list the ranks GPU by GPU and deal them to the replicas in
+ * turn; no GPU contributes more than d consecutive ranks, so no replica gets two on one GPU. */
+int orc_fits(uint32_t Q, uint64_t a, uint64_t f, uint64_t tp, uint64_t q, uint64_t d)
+{
+    uint64_t ranks = 0;
+    if (Q == 0 || q == 0)
+        return 0;
+    for (uint64_t g = a / Q; g * Q < a + f; ++g) {
+        uint64_t from = g * Q > a ? g * Q : a;
+        uint64_t to = (g + 1) * Q < a + f ? (g + 1) * Q : a + f;
+        uint64_t c = (to - from) / q;
+        ranks += c < d ? c : d;
+    }
+    return ranks >= tp * d;
+}
+
+uint64_t orc_binomial(uint64_t n, uint64_t k)
+{
+    if (k > n)
+        return 0;
+    unsigned __int128 c = 1;
+    for (uint64_t i = 1; i <= k; ++i) {
+        c = c * (n - k + i) / i;        /* exact: c is C(n - k + i, i) after this step */
+        if (c > ORC_U64_NONE)
+            return ORC_U64_NONE;
+    }
+    return (uint64_t)c;
+}
+
+typedef struct {
+    const orc_instance *s;
+    const orc_term *terms;     /* [M][O], NULL when only counting */
+    uint32_t M, Q;
+    uint32_t order[16];        /* LLM at each position */
+    uint64_t lo[16], hi[16];   /* bounds per position */
+    uint64_t f[16];            /* fraction per position */
+    int ordered;
+    uint64_t vectors, best_x, best_L;
+} orc_enum;
+
+/* Steps 2 and 3 for one fraction vector.  With the fractions fixed, the admissible options of
+ * each LLM do not depend on the others' choices and L_w is a sum, so the lowest (L_w, x) over the
+ * product of the admissible sets takes, per LLM, the smallest contribution and, among equal
+ * ones, the lowest option (x orders LLM 0 first). */
+static void orc_visit(orc_enum *e)
+{
+    e->vectors += 1;
+    if (!e->terms)
+        return;
+    const orc_instance *s = e->s;
+    uint32_t O = orc_num_options(s);
+    uint64_t start[16], size[16], a = 0;
+    for (uint32_t k = 0; k < e->M; ++k) {
+        start[e->order[k]] = a;
+        size[e->order[k]] = e->f[k];
+        a += e->f[k];
+    }
+    uint64_t L = 0, x = 0;
+    for (uint32_t m = 0; m < e->M; ++m) {
+        uint64_t best_c = ORC_U64_NONE;
+        uint32_t best_o = 0;
+        for (uint32_t o = 0; o < O; ++o) {
+            const orc_term *t = &e->terms[(size_t)m * O + o];
+            if (!t->ok || !t->thr_ok || t->u != size[m])
+                continue;
+            uint32_t d = o % s->D + 1, ij = o / s->D;
+            uint64_t tp = s->tp[ij / s->n_fq], q = s->fq[ij % s->n_fq];
+            if (!orc_fits(e->Q, start[m], size[m], tp, q, d))
+                continue;
+            if (t->c < best_c) {
+                best_c = t->c;
+                best_o = o;
+            }
+        }
+        if (best_c == ORC_U64_NONE)
+            return;
+        L += best_c;
+        x = x * O + best_o;
+    }
+    if (L < e->best_L || (L == e->best_L && x < e->best_x)) {
+        e->best_L = L;
+        e->best_x = x;
+    }
+}
+
+/* Step 1: every fraction vector, position by position; the last position takes the rest. */
+static void orc_enum_from(orc_enum *e, uint32_t k, uint64_t remaining)
+{
+    uint64_t lo = e->lo[k], hi = e->hi[k];
+    if (e->ordered && k > 0 && e->f[k - 1] < hi)
+        hi = e->f[k - 1];
+    if (k + 1 == e->M) {
+        if (remaining >= lo && remaining <= hi) {
+            e->f[k] = remaining;
+            orc_visit(e);
+        }
+        return;
+    }
+    for (uint64_t v = lo; v <= hi && v <= remaining; ++v) {
+        e->f[k] = v;
+        orc_enum_from(e, k + 1, remaining - v);
+    }
+}
+
+/* Bounds per position; returns 0 when the lower bounds alone exceed the total (no vector). */
+static int orc_enum_bounds(orc_enum *e, uint64_t total, const uint64_t *lo_pos)
+{
+    uint64_t after = 0;
+    for (uint32_t k = e->M; k-- > 0;) {
+        if (after + lo_pos[k] > total)
+            return 0;
+        e->lo[k] = lo_pos[k];
+        e->hi[k] = total - after;
+        after += lo_pos[k];
+    }
+    return 1;
+}
+
+/* Number of fraction vectors of step 1 for M positions, total units, lower bounds per position
+ * (upper bounds as in step 1), with or without the ordering. */
+uint64_t orc_count_fractions(uint32_t M, uint64_t total, const uint64_t *lo_pos, int ordered)
+{
+    orc_enum e = {0};
+    if (M == 0 || M > 16)
+        return 0;
+    e.M = M;
+    e.ordered = ordered;
+    if (orc_enum_bounds(&e, total, lo_pos))
+        orc_enum_from(&e, 0, total);
+    return e.vectors;
+}
+
+int orc_pruned(const orc_instance *s, uint32_t G, uint32_t lambda, uint32_t flags,
+               orc_term *scratch /* [M * O] */, orc_pruned_out *out)
+{
+    uint32_t O = orc_num_options(s);
+    if (s->M == 0 || s->M > 16 || flags > 3u)
+        return -1;
+    for (uint32_t m = 0; m < s->M; ++m)
+        for (uint32_t o = 0; o < O; ++o)
+            orc_option_term(s, m, o, lambda, &scratch[(size_t)m * O + o]);
+    orc_enum e = {0};
+    e.s = s;
+    e.terms = scratch;
+    e.M = s->M;
+    e.Q = s->Q;
+    e.ordered = (flags & ORC_PRUNE_ORDER) != 0;
+    e.best_x = ORC_U64_NONE;
+    e.best_L = ORC_U64_NONE;
+    /* latency ratios: contribution at tp[0], the largest share, the first profiled point */
+    uint64_t ref[16];
+    for (uint32_t m = 0; m < s->M; ++m) {
+        size_t tab = ((size_t)m * s->n_tp + 0) * s->n_fq + (s->n_fq - 1);
+        ref[m] = (uint64_t)s->lat[tab * s->K] * s->n[m] / s->p[m];
+        e.order[m] = m;
+    }
+    for (uint32_t a = 1; a < s->M; ++a) {                  /* insertion sort: ref desc, m asc */
+        uint32_t v = e.order[a], b = a;
+        while (b > 0 && ref[e.order[b - 1]] < ref[v]) {
+            e.order[b] = e.order[b - 1];
+            --b;
+        }
+        e.order[b] = v;
+    }
+    uint64_t total = (uint64_t)s->Q * G, lo_pos[16];
+    for (uint32_t k = 0; k < s->M; ++k) {
+        uint32_t m = e.order[k];
+        uint64_t need = (s->W[m] * (uint64_t)s->Q + s->H - 1) / s->H;
+        lo_pos[k] = (flags & ORC_PRUNE_MIN) ? (need > 1 ? need : 1) : 0;
+    }
+    if (orc_enum_bounds(&e, total, lo_pos))
+        orc_enum_from(&e, 0, total);
+    out->best_x = e.best_x;
+    out->best_L = e.best_x == ORC_U64_NONE ? ORC_U64_NONE : e.best_L;
+    out->vectors = e.vectors;
+    out->unpruned = orc_binomial(total + s->M - 1, s->M - 1);
     return 0;
 }

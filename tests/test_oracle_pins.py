@@ -361,3 +361,164 @@ def test_allocate_brute_force_equals_threshold_dp():
             L.append([None if g < first else vals[g] for g in range(G + 1)])
         for policy in (oracle.EGALITARIAN, oracle.SOCIAL):
             assert oracle.allocate(_table(L), policy) == _split_dp(L, G, policy), (trial, L, G)
+
+
+# ------------------------------------------------------------------------------------------
+# The paper's pruned search (Section 5, steps 1-3).
+import math as _math  # noqa: E402
+
+from pruned_ref import placeable as _placeable, pruned as _pruned_literal  # noqa: E402
+
+
+def test_pruned_unpruned_count_is_the_papers():
+    # Section 5, step 1: 5 LLMs, 16 GPUs, 10 fractions per GPU give C(164, 4), about 29 million.
+    assert oracle.count_fractions(5, 160, [0] * 5, False) == 29_051_001 == _math.comb(164, 4)
+    assert oracle.binomial(164, 4) == 29_051_001
+    for M, total in [(1, 7), (2, 9), (3, 12), (4, 10)]:
+        assert oracle.count_fractions(M, total, [0] * M, False) == _math.comb(total + M - 1, M - 1)
+
+
+def _partitions_at_most(n, k):
+    # partitions of n into at most k parts: p(n, k) = p(n, k - 1) + p(n - k, k)
+    if n == 0:
+        return 1
+    if n < 0 or k == 0:
+        return 0
+    return _partitions_at_most(n, k - 1) + _partitions_at_most(n - k, k)
+
+
+def test_pruned_ordered_count_is_partitions():
+    assert oracle.count_fractions(3, 10, [0] * 3, True) == 14
+    for M in range(1, 6):
+        for n in range(0, 30):
+            assert oracle.count_fractions(M, n, [0] * M, True) == _partitions_at_most(n, M)
+
+
+def test_pruned_count_with_bounds_by_brute_force():
+    rng = np.random.default_rng(5)
+    for _ in range(60):
+        M = int(rng.integers(1, 5))
+        total = int(rng.integers(0, 14))
+        lo = [int(v) for v in rng.integers(0, 4, size=M)]
+        for ordered in (False, True):
+            want = 0
+            for f in itertools.product(range(total + 1), repeat=M):
+                if sum(f) != total or any(f[k] < lo[k] for k in range(M)):
+                    continue
+                if any(f[k] > total - sum(lo[k + 1:]) for k in range(M)):
+                    continue
+                if ordered and any(f[k] > f[k - 1] for k in range(1, M)):
+                    continue
+                want += 1
+            assert oracle.count_fractions(M, total, lo, ordered) == want, (M, total, lo, ordered)
+
+
+def test_pruned_placement_rule_matches_backtracking():
+    checked = 0
+    for Q in (2, 4, 5):
+        for a in range(0, 2 * Q):
+            for f in range(1, 3 * Q + 1):
+                for tp in (1, 2, 3, 4):
+                    for q in range(1, Q + 1):
+                        for d in range(1, 5):
+                            want = _placeable(Q, a, f, tp, q, d)
+                            assert oracle.fits(Q, a, f, tp, q, d) == want, (Q, a, f, tp, q, d)
+                            checked += want
+    assert checked > 100
+
+
+def test_pruned_hand_case():
+    case = next(c for c in load_cases() if c["id"] == "H2")
+    b = case_batch(case)
+    inst = oracle.Instance(b, 0)
+    for q in case["pruned"]:
+        got = oracle.pruned(inst, q["G"], q["lambda"], q["flags"])
+        assert got["x"] == q["x"] and got["vectors"] == q["vectors"], (q, got)
+        assert got["unpruned"] == q["unpruned"]
+        if q["x"] is not None:
+            assert got["L"] == q["L"]
+        assert _pruned_literal(b, 0, q["G"], q["lambda"], q["flags"]) == \
+            {k: got[k] for k in ("x", "L", "vectors")}
+
+
+def _pruned_spaces():
+    # (seed, M, tp, fq, Q, D, K, G)
+    yield (11, 2, (1, 2), (1, 2, 4), 4, 3, 3, 3)
+    yield (12, 3, (1, 2), (2, 4), 4, 2, 2, 2)
+    yield (13, 2, (1, 2, 4), (1, 2, 3, 4), 4, 4, 4, 4)
+    yield (14, 3, (1,), (1, 2, 3), 3, 3, 1, 3)
+    yield (15, 1, (1, 2), (1, 2, 4), 4, 4, 3, 3)
+
+
+@pytest.mark.parametrize("spec", list(_pruned_spaces()), ids=lambda s: f"seed{s[0]}")
+def test_pruned_matches_literal_statement(spec):
+    seed, M, tps, fqs, Q, D, K, G = spec
+    b = make_custom(seed, M, tps, fqs, D, K, G, count=2, frac_den=Q, param_range=(0.5e9, 150e9))
+    for i in range(2):
+        inst = oracle.Instance(b, i)
+        tmax = oracle.tmax(inst, G)
+        for lam in sorted({1, max(1, tmax // 3), max(1, tmax // 2), tmax}):
+            for flags in (0, 1, 2, 3):
+                got = oracle.pruned(inst, G, lam, flags)
+                assert {k: got[k] for k in ("x", "L", "vectors")} == \
+                    _pruned_literal(b, i, G, lam, flags), (i, lam, flags)
+
+
+def _pruned_edge_batch(seed, variant):
+    """Spaces where the reading details of steps 1-2 change the answer.  "tie": LLM 1 copies
+    LLM 0 except at tp = 2, so the latency ratios tie (order by index) while the LLMs differ;
+    "flip": LLM 0's smallest share is 7x slower, so the order at the smallest share differs from
+    the order at the largest; "weightless": LLM 0 has no weights (lower bound of one unit).
+    Shares of 3 quarters make packed fractions straddle GPUs."""
+    fqs = [(1, 2, 3, 4), (1, 3, 4), (2, 3, 4)][seed % 3]
+    D, K, G = 3 + seed % 2, 1 + (seed // 2) % 2, 3 + (seed // 3) % 2
+    b = make_custom(seed, 3, (1, 2), fqs, D, K, G, count=1, param_range=(0.5e9, 150e9))
+    if variant == "tie":
+        for key in ("W", "n", "p", "allowed", "rate", "lat"):
+            b[key][:, 1] = b[key][:, 0]
+        b["lat"][:, 1, 1, :, :] *= 2
+    elif variant == "flip":
+        b["lat"][:, 0, :, 0, :] *= 7
+    elif variant == "weightless":
+        b["W"][:, 0] = 0
+    return b, G
+
+
+EDGE_SPACES = [(100, "flip"), (101, "tie"), (103, "tie"), (23, "weightless"), (104, "flip")]
+
+
+@pytest.mark.parametrize("seed,variant", EDGE_SPACES)
+def test_pruned_matches_literal_statement_on_edge_spaces(seed, variant):
+    b, G = _pruned_edge_batch(seed, variant)
+    inst = oracle.Instance(b, 0)
+    tmax = oracle.tmax(inst, G)
+    for lam in sorted({1, max(1, tmax // 4), max(1, tmax // 2), tmax}):
+        for flags in (0, 1, 2, 3):
+            got = oracle.pruned(inst, G, lam, flags)
+            assert {k: got[k] for k in ("x", "L", "vectors")} == \
+                _pruned_literal(b, 0, G, lam, flags), (seed, variant, lam, flags)
+
+
+@pytest.mark.parametrize("cfg,count", [(0, 40), (1, 16)])
+def test_pruned_result_is_a_full_budget_candidate_no_better_than_exhaustive(cfg, count):
+    b = make_batch(cfg, range(count))
+    found = missed = 0
+    for i in range(count):
+        inst = oracle.Instance(b, i)
+        G = int(b["G"][i])
+        lam = target_from_tmax(int(b["u_ppm"][i]), oracle.tmax(inst, G))
+        p = oracle.pruned(inst, G, lam)
+        ex = oracle.argmin(inst, G, lam)
+        assert p["unpruned"] == _math.comb(4 * G + inst.M - 1, inst.M - 1)
+        assert p["vectors"] <= p["unpruned"]
+        if p["x"] is None:
+            missed += ex["x"] is not None
+            continue
+        found += 1
+        e = oracle.evaluate(inst, G, lam, p["x"])
+        assert e["flags"] == 7 and e["L"] == p["L"] and e["U"] == 4 * G
+        assert ex["x"] is not None and ex["L"] <= p["L"]
+        missed += p["L"] > ex["L"]
+    assert found > count // 2
+    if cfg == 1:
+        assert missed > 0       # the pruned search is a heuristic: it misses some optima here
