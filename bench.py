@@ -54,11 +54,16 @@ def _traffic(kernel_digest: str, workload: str):
     return entry.get("bytes_per_launch")
 
 
+KERNEL_SOURCES = ("alp_kernels.hip", "alp_device.h", "alp_internal.h")
+
+
 def _kernel_digest() -> str:
+    """SHA-256 over the sources compiled into the scan kernel."""
     import hashlib
     h = hashlib.sha256()
-    with open(os.path.join(ROOT, "paper_2604_15186_amd", "csrc", "alp_kernels.hip"), "rb") as f:
-        h.update(f.read())
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2604_15186_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
     return h.hexdigest()
 
 

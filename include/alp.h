@@ -180,6 +180,41 @@ int32_t alp_allocate_workflows(alp_ctx *ctx, uint32_t count, const uint32_t *ins
                                const uint32_t *target_milli, uint32_t total_gpus, uint32_t policy,
                                alp_plan_t *plan, uint32_t *gpus, alp_result_t *results);
 
+/* ---- The paper's pruned search (Section 5, steps 1-3) ----------------------------------------
+ * The paper's own scheduler enumerates GPU fractions instead of every candidate, and so need not
+ * reach the exhaustive optimum; this entry point runs it on the device, for comparison.
+ *   Step 1: LLM m receives f_m units of 1/Q GPU with sum f_m = Q*G.  ALP_PRUNE_ORDER: LLMs are
+ *           ordered by profiled latency ratio (the Eq. 1 contribution at the smallest TP degree,
+ *           the largest share and the first profiled point, largest first, ties by LLM index) and
+ *           no LLM receives more units than the one before it.  ALP_PRUNE_MIN_FRACTION: each LLM
+ *           receives at least max(1, ceil(W_m * Q / H)) units (its weights), and at most Q*G
+ *           minus the lower bounds of the LLMs after it.
+ *   Step 2: the fractions are packed contiguously in that order over the Q*G units, GPU by GPU.
+ *   Step 3: option (tp, q, d) is admissible for an LLM iff tp * q * d equals its fraction and d
+ *           replicas of tp ranks of q units, the ranks of one replica on distinct GPUs, fit its
+ *           packed GPUs.
+ * The result is the feasible admissible candidate of lowest L_w, ties to the lowest index. */
+#define ALP_PRUNE_ORDER 1u
+#define ALP_PRUNE_MIN_FRACTION 2u
+#define ALP_PRUNED_MAX_UNITS 1024u           /* Q*G per query */
+#define ALP_PRUNED_MAX_VECTORS (1ull << 34)  /* step-1 vectors per query, before bounds */
+
+/* One pruned search (64 bytes). */
+typedef struct {
+    alp_result_t best;            /* as alp_search's result; ALP_INFEASIBLE if none */
+    uint64_t fraction_vectors;    /* fraction vectors enumerated in step 1 */
+    uint64_t unpruned_vectors;    /* C(Q*G + M - 1, M - 1): every split of Q*G units, saturating */
+} alp_pruned_t;
+
+/* Pruned searches of count queries (instances may be NULL: 0..count-1), one launch sequence.
+ * flags: any of ALP_PRUNE_ORDER | ALP_PRUNE_MIN_FRACTION (else EINVAL).  Each query needs
+ * Q * gpu_budget[i] <= ALP_PRUNED_MAX_UNITS (else EINVAL) and at most ALP_PRUNED_MAX_VECTORS
+ * step-1 vectors counted without the lower bounds (else ERANGE).  Writes out[0..count) on
+ * ALP_OK; each out[i].best.status is ALP_OK or ALP_INFEASIBLE. */
+int32_t alp_search_pruned(alp_ctx *ctx, uint32_t count, const uint32_t *instances,
+                          const uint32_t *gpu_budget, const uint32_t *target_milli, uint32_t flags,
+                          alp_pruned_t *out);
+
 /* Evaluates count given candidate indices (each < O^M, else EINVAL) of one instance. */
 int32_t alp_eval_candidates(alp_ctx *ctx, uint32_t instance, uint32_t gpu_budget,
                             uint32_t target_milli, const uint64_t *indices, uint64_t count,
@@ -195,7 +230,8 @@ int32_t alp_set_launch(alp_ctx *ctx, uint32_t variant, uint32_t blocks_per_item,
  * alp_kernel_times writes, for the last search or batch, the milliseconds of the option-term
  * kernel (ms[0]) and of the candidate scan kernel, which includes the final reduction and the
  * result write (ms[1]); ms[2] is the budget-split kernel of alp_allocate_workflows, 0 after the
- * other calls.  *scan_blocks receives the scan kernel's grid size in blocks. */
+ * other searches.  After alp_search_pruned: ms[1] is the fraction enumeration and ms[2] the
+ * admissible-option table.  *scan_blocks receives the scan (or enumeration) grid size. */
 int32_t alp_set_timing(alp_ctx *ctx, int32_t enable);
 int32_t alp_kernel_times(alp_ctx *ctx, float ms[3], uint32_t *scan_blocks);
 

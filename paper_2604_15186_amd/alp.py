@@ -21,7 +21,7 @@ MAX_LLMS = 8
 
 # Symbols declared in include/alp.h.
 EXPORTS = ("alp_load_profiles", "alp_search", "alp_search_batch", "alp_max_throughput",
-           "alp_allocate_workflows", "alp_eval_candidates", "alp_set_launch", "alp_set_timing", "alp_kernel_times",
+           "alp_allocate_workflows", "alp_search_pruned", "alp_eval_candidates", "alp_set_launch", "alp_set_timing", "alp_kernel_times",
            "alp_num_candidates", "alp_free", "alp_status_str", "alp_last_error")
 
 
@@ -46,8 +46,11 @@ EVAL_DTYPE = np.dtype([("flags", np.uint32), ("latency_us", np.uint32),
                        ("throughput_milli", np.uint32), ("gpu_units", np.uint32)])
 PLAN_DTYPE = np.dtype([("status", np.uint32), ("policy", np.uint32), ("max_latency_us", np.uint32),
                        ("gpus_used", np.uint32), ("sum_latency_us", np.uint64)])
+PRUNED_DTYPE = np.dtype([("best", RESULT_DTYPE), ("vectors", np.uint64), ("unpruned", np.uint64)])
 assert RESULT_DTYPE.itemsize == 48 and EVAL_DTYPE.itemsize == 16 and PLAN_DTYPE.itemsize == 24
+assert PRUNED_DTYPE.itemsize == 64
 WELFARE_EGALITARIAN, WELFARE_SOCIAL = 0, 1
+PRUNE_ORDER, PRUNE_MIN_FRACTION = 1, 2
 
 _lib = None
 
@@ -67,12 +70,14 @@ def lib():
         L.alp_max_throughput.argtypes = [vp, u32, vp, vp, vp]
         L.alp_eval_candidates.argtypes = [vp, u32, u32, u32, vp, u64, vp]
         L.alp_allocate_workflows.argtypes = [vp, u32, vp, vp, u32, u32, vp, vp, vp]
+        L.alp_search_pruned.argtypes = [vp, u32, vp, vp, vp, u32, vp]
         L.alp_set_launch.argtypes = [vp, u32, u32, u32]
         L.alp_set_timing.argtypes = [vp, i32]
         L.alp_kernel_times.argtypes = [vp, C.POINTER(C.c_float), C.POINTER(u32)]
         L.alp_num_candidates.argtypes = [vp, C.POINTER(u64)]
         for name in ("alp_load_profiles", "alp_search", "alp_search_batch", "alp_max_throughput",
-                     "alp_allocate_workflows", "alp_eval_candidates", "alp_set_launch", "alp_set_timing",
+                     "alp_allocate_workflows", "alp_search_pruned", "alp_eval_candidates",
+                     "alp_set_launch", "alp_set_timing",
                      "alp_kernel_times", "alp_num_candidates"):
             getattr(L, name).restype = i32
         L.alp_free.argtypes = [vp]
@@ -213,6 +218,18 @@ class Context:
             return plan[0], None, None
         return plan[0], gpus, res
 
+    def search_pruned(self, gpu_budget, target_milli, flags: int = PRUNE_ORDER | PRUNE_MIN_FRACTION,
+                      instances=None) -> np.ndarray:
+        """The paper's pruned search for each query (alp_search_pruned); PRUNED_DTYPE records."""
+        G = np.ascontiguousarray(gpu_budget, dtype=np.uint32)
+        lam = np.ascontiguousarray(target_milli, dtype=np.uint32)
+        assert len(lam) == len(G)
+        inst = None if instances is None else np.ascontiguousarray(instances, dtype=np.uint32)
+        out = np.zeros(len(G), dtype=PRUNED_DTYPE)
+        _check(lib().alp_search_pruned(self._ctx, len(G), None if inst is None else _ptr(inst),
+                                       _ptr(G), _ptr(lam), flags, _ptr(out)))
+        return out
+
     def eval_candidates(self, instance: int, gpu_budget: int, target_milli: int, indices) -> np.ndarray:
         idx = np.ascontiguousarray(indices, dtype=np.uint64)
         out = np.zeros(len(idx), dtype=EVAL_DTYPE)
@@ -227,7 +244,8 @@ class Context:
         _check(lib().alp_set_timing(self._ctx, 1 if enable else 0))
 
     def kernel_times(self):
-        """(option-term ms, scan ms, budget-split ms, scan blocks) of the last call."""
+        """(option-term ms, scan ms, third-kernel ms, grid blocks) of the last call; the third
+        kernel is the budget split or the pruned search's option table."""
         ms = (C.c_float * 3)()
         blocks = C.c_uint32()
         _check(lib().alp_kernel_times(self._ctx, ms, C.byref(blocks)))

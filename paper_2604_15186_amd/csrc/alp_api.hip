@@ -8,6 +8,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <new>
 #include <vector>
 
@@ -101,6 +102,10 @@ struct alp_ctx {
 
     DevBuf q_inst, rec, ext, inner, done, winners, idx, evals, tmax;   // q_inst: inst | cap | lambda
     DevBuf split_dp;                        // allocate_kernel's knapsack table
+    DevBuf pruned_table, pruned_counts;     // pruned search: option table, per-block counts
+    alp_pruned_t *host_pruned = nullptr;    // mapped pinned results of pruned searches
+    alp_pruned_t *host_pruned_dev = nullptr;
+    size_t host_pruned_cap = 0;
     uint32_t *host_split = nullptr;         // mapped pinned: alp_plan_t (6 words) + budgets[16]
     uint32_t *host_split_dev = nullptr;
     uint32_t *host_query = nullptr;         // pinned staging of batch queries: inst | cap | lambda
@@ -718,6 +723,143 @@ int32_t alp_allocate_workflows(alp_ctx *ctx, uint32_t count, const uint32_t *ins
     return ALP_OK;
 }
 
+namespace {
+
+// Step-1 vectors of F units over M LLMs without lower bounds (an upper bound of the count with
+// them): partitions of F into at most M parts when ordered, else C(F + M - 1, M - 1).
+// Saturating.
+uint64_t pruned_vector_bound(uint32_t F, uint32_t M, bool ordered)
+{
+    std::vector<uint64_t> row(F + 1, 0), prev(F + 1, 0);
+    if (ordered) {
+        prev[0] = 1;                                   // at most 0 parts
+        for (uint32_t k = 1; k <= M; ++k) {            // at most k parts
+            for (uint32_t n = 0; n <= F; ++n) {
+                uint64_t v = prev[n] + (n >= k ? row[n - k] : 0);
+                row[n] = v < prev[n] ? UINT64_MAX : v;
+            }
+            prev.swap(row);
+        }
+        return prev[F];
+    }
+    // C(F + M - 1, M - 1) by Pascal's rule
+    std::vector<uint64_t> c(M, 0);
+    c[0] = 1;
+    for (uint32_t i = 1; i <= F + M - 1; ++i)
+        for (uint32_t j = std::min<uint32_t>(i, M - 1); j >= 1; --j) {
+            const uint64_t v = c[j] + c[j - 1];
+            c[j] = v < c[j] ? UINT64_MAX : v;
+        }
+    return c[M - 1];
+}
+
+}  // namespace
+
+int32_t alp_search_pruned(alp_ctx *ctx, uint32_t count, const uint32_t *instances,
+                          const uint32_t *gpu_budget, const uint32_t *target_milli, uint32_t flags,
+                          alp_pruned_t *out)
+{
+    if (!ctx)
+        return fail(ALP_EINVAL, "ctx is NULL");
+    if (flags > (ALP_PRUNE_ORDER | ALP_PRUNE_MIN_FRACTION))
+        return fail(ALP_EINVAL, "flags 0x%x unknown", flags);
+    if (count == 0)
+        return ALP_OK;
+    if (!gpu_budget || !target_milli || !out)
+        return fail(ALP_EINVAL, "gpu_budget, target_milli or out is NULL");
+    const alp::SpaceDev &sp = ctx->sp;
+    std::vector<uint32_t> inst(count), cap(count);
+    uint32_t F_max = 0;
+    for (uint32_t i = 0; i < count; ++i) {
+        inst[i] = instances ? instances[i] : i;
+        int32_t st = check_instance(ctx, inst[i]);
+        if (st != ALP_OK)
+            return st;
+        const uint64_t F = (uint64_t)sp.Q * gpu_budget[i];
+        if (F > ALP_PRUNED_MAX_UNITS)
+            return fail(ALP_EINVAL, "query %u: Q*G = %llu above %u for the pruned search", i,
+                        (unsigned long long)F, ALP_PRUNED_MAX_UNITS);
+        if (pruned_vector_bound((uint32_t)F, sp.M, flags & ALP_PRUNE_ORDER) > ALP_PRUNED_MAX_VECTORS)
+            return fail(ALP_ERANGE, "query %u: more than 2^34 fraction vectors", i);
+        cap[i] = (uint32_t)F;
+        F_max = std::max(F_max, cap[i]);
+    }
+    const uint64_t F1 = (uint64_t)F_max + 1;
+    const uint64_t prefixes = sp.M >= 3 ? F1 * F1 : sp.M == 2 ? F1 : 1;
+    const uint32_t bpi = (uint32_t)ceil_div(prefixes, 256);
+    const uint64_t nblocks = (uint64_t)count * bpi;
+    if (nblocks >= (UINT64_C(1) << 31))
+        return fail(ALP_ERANGE, "batch too large for one launch (%llu blocks)",
+                    (unsigned long long)nblocks);
+    DeviceGuard guard(ctx->device);
+    if (guard.status != hipSuccess)
+        return hip_fail(guard.status, "hipSetDevice");
+    const uint64_t items_bytes = (uint64_t)count * sp.M * sp.O * sizeof(uint2);
+    hipError_t e;
+    if ((e = ctx->rec.ensure(items_bytes)) != hipSuccess || (e = ctx->ext.ensure(items_bytes)) != hipSuccess ||
+        (e = ctx->inner.ensure((uint64_t)count * alp::inner_stride(sp.O) * sizeof(uint2))) != hipSuccess ||
+        (e = ctx->done.ensure((uint64_t)count * sizeof(uint32_t))) != hipSuccess ||
+        (e = ctx->winners.ensure(nblocks * sizeof(alp::Winner))) != hipSuccess ||
+        (e = ctx->pruned_counts.ensure(nblocks * sizeof(uint64_t))) != hipSuccess ||
+        (e = ctx->pruned_table.ensure((uint64_t)count * sp.M * sp.Q * F1 * sizeof(uint2))) != hipSuccess)
+        return hip_fail(e, "hipMalloc(pruned search)");
+    if (count > ctx->host_pruned_cap) {
+        if (ctx->host_pruned)
+            (void)hipHostFree(ctx->host_pruned);
+        ctx->host_pruned = nullptr;
+        ctx->host_pruned_dev = nullptr;
+        ctx->host_pruned_cap = 0;
+        if ((e = hipHostMalloc((void **)&ctx->host_pruned, count * sizeof(alp_pruned_t),
+                               hipHostMallocMapped)) != hipSuccess)
+            return hip_fail(e, "hipHostMalloc(pruned results)");
+        if ((e = hipHostGetDevicePointer((void **)&ctx->host_pruned_dev, ctx->host_pruned, 0)) !=
+            hipSuccess) {
+            (void)hipHostFree(ctx->host_pruned);
+            ctx->host_pruned = nullptr;
+            return hip_fail(e, "hipHostGetDevicePointer(pruned results)");
+        }
+        ctx->host_pruned_cap = count;
+    }
+    alp::QueryDev q{};
+    int32_t st = upload_queries(ctx, count, inst.data(), cap.data(), target_milli, q);
+    if (st != ALP_OK)
+        return st;
+    uint2 *rec = (uint2 *)ctx->rec.ptr, *ext = (uint2 *)ctx->ext.ptr;
+    uint32_t *done = (uint32_t *)ctx->done.ptr;
+    if (ctx->timing && (e = hipEventRecord(ctx->ev[0], ctx->stream)) != hipSuccess)
+        return hip_fail(e, "hipEventRecord");
+    if ((e = alp::launch_option_terms(sp, ctx->tdev, q, count, rec, ext, (uint2 *)ctx->inner.ptr,
+                                      done, ctx->stream)) != hipSuccess)
+        return hip_fail(e, "option_terms launch");
+    if (ctx->timing && (e = hipEventRecord(ctx->ev[1], ctx->stream)) != hipSuccess)
+        return hip_fail(e, "hipEventRecord");
+    if ((e = alp::launch_pruned_table(sp, count, F_max, rec, (uint2 *)ctx->pruned_table.ptr,
+                                      ctx->stream)) != hipSuccess)
+        return hip_fail(e, "pruned table launch");
+    if (ctx->timing && (e = hipEventRecord(ctx->ev[2], ctx->stream)) != hipSuccess)
+        return hip_fail(e, "hipEventRecord");
+    if ((e = alp::launch_pruned_scan(sp, ctx->tdev, q, count, F_max, flags,
+                                     (const uint2 *)ctx->pruned_table.ptr, bpi,
+                                     (alp::Winner *)ctx->winners.ptr,
+                                     (uint64_t *)ctx->pruned_counts.ptr, ext, done,
+                                     ctx->host_pruned_dev, ctx->stream)) != hipSuccess)
+        return hip_fail(e, "pruned scan launch");
+    if (ctx->timing && (e = hipEventRecord(ctx->ev[3], ctx->stream)) != hipSuccess)
+        return hip_fail(e, "hipEventRecord");
+    if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess)
+        return hip_fail(e, "hipStreamSynchronize");
+    if (ctx->timing) {
+        // ms[0]: option terms, ms[1]: fraction enumeration, ms[2]: admissible-option table
+        if ((e = hipEventElapsedTime(&ctx->last_ms[0], ctx->ev[0], ctx->ev[1])) != hipSuccess ||
+            (e = hipEventElapsedTime(&ctx->last_ms[2], ctx->ev[1], ctx->ev[2])) != hipSuccess ||
+            (e = hipEventElapsedTime(&ctx->last_ms[1], ctx->ev[2], ctx->ev[3])) != hipSuccess)
+            return hip_fail(e, "hipEventElapsedTime");
+    }
+    ctx->last_blocks = (uint32_t)nblocks;
+    memcpy(out, ctx->host_pruned, count * sizeof(alp_pruned_t));
+    return ALP_OK;
+}
+
 int32_t alp_eval_candidates(alp_ctx *ctx, uint32_t instance, uint32_t gpu_budget,
                             uint32_t target_milli, const uint64_t *indices, uint64_t count,
                             alp_eval_t *out)
@@ -822,7 +964,8 @@ void alp_free(alp_ctx *ctx)
         if (ctx->ev[k])
             (void)hipEventDestroy(ctx->ev[k]);
     DevBuf *bufs[] = {&ctx->tables, &ctx->q_inst, &ctx->rec, &ctx->ext, &ctx->inner, &ctx->done,
-                      &ctx->winners, &ctx->idx, &ctx->evals, &ctx->tmax, &ctx->split_dp};
+                      &ctx->winners, &ctx->idx, &ctx->evals, &ctx->tmax, &ctx->split_dp,
+                      &ctx->pruned_table, &ctx->pruned_counts};
     for (DevBuf *b : bufs)
         b->release();
     if (ctx->host_results)
@@ -831,6 +974,8 @@ void alp_free(alp_ctx *ctx)
         (void)hipHostFree(ctx->host_query);
     if (ctx->host_split)
         (void)hipHostFree(ctx->host_split);
+    if (ctx->host_pruned)
+        (void)hipHostFree(ctx->host_pruned);
     delete ctx;
 }
 

@@ -98,6 +98,22 @@ hipError_t launch_tmax(const SpaceDev &sp, const QueryDev &q, uint32_t count, co
 hipError_t launch_allocate(const alp_result_t *res, uint32_t W, uint32_t G, uint32_t policy,
                            uint64_t *dp, alp_plan_t *plan, uint32_t *gpus, hipStream_t st);
 
+// The paper's pruned search for count items (see alp_search_pruned), after the option-term
+// kernel (rec, ext; it also zeroes done[]).  Table kernel: count * M * Q * (F_max + 1) entries.
+// Enumeration kernel: blocks_per_item blocks of 256 threads cover (F_max + 1)^min(2, M - 1)
+// prefixes per item; winners and counts hold count * blocks_per_item entries; writes
+// out[0..count).
+hipError_t launch_pruned_table(const SpaceDev &sp, uint32_t count, uint32_t F_max,
+                               const uint2 *rec, uint2 *table, hipStream_t st);
+hipError_t launch_pruned_scan(const SpaceDev &sp, const TablesDev &tb, const QueryDev &q,
+                              uint32_t count, uint32_t F_max, uint32_t flags, const uint2 *table,
+                              uint32_t blocks_per_item, Winner *winners, uint64_t *counts,
+                              const uint2 *ext, uint32_t *done, alp_pruned_t *out, hipStream_t st);
+
+static_assert(sizeof(alp_pruned_t) == 64 && offsetof(alp_pruned_t, fraction_vectors) == 48 &&
+                  offsetof(alp_pruned_t, unpruned_vectors) == 56,
+              "alp_pruned_t layout");
+
 // Resident blocks per CU of the scan kernels at a given block size (occupancy query).
 int scan_blocks_per_cu(uint32_t variant, uint32_t slots, uint32_t threads, const SpaceDev &sp);
 

@@ -15,6 +15,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "alp_device.h"
 #include "alp_internal.h"
 
 namespace alp {
@@ -23,162 +24,6 @@ namespace {
 
 constexpr uint32_t kMaxOuter = ALP_MAX_LLMS - 2;   // digits above the last two LLMs
 constexpr int32_t kNeverFits = -(1 << 30);          // remaining units no lane can satisfy
-
-__device__ __forceinline__ bool lex_less(uint32_t aL, uint64_t ax, uint32_t bL, uint64_t bx)
-{
-    return aL < bL || (aL == bL && ax < bx);
-}
-
-// Wave-wide lexicographic minimum of (L, x); every lane ends with the result.
-__device__ __forceinline__ void wave_min(uint32_t &L, uint64_t &x)
-{
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-        uint32_t oL = __shfl_xor(L, off, 64);
-        uint64_t ox = __shfl_xor((unsigned long long)x, off, 64);
-        if (lex_less(oL, ox, L, x)) {
-            L = oL;
-            x = ox;
-        }
-    }
-}
-
-// Wave-wide minima, returned as wave-uniform values.
-__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v)
-{
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-        const uint32_t o = __shfl_xor(v, off, 64);
-        v = o < v ? o : v;
-    }
-    return (uint32_t)__builtin_amdgcn_readfirstlane(v);
-}
-
-__device__ __forceinline__ uint64_t wave_min_u64(uint64_t v)
-{
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-        const uint64_t o = __shfl_xor((unsigned long long)v, off, 64);
-        v = o < v ? o : v;
-    }
-    // readfirstlane works on int: widen through uint32_t, never sign-extend.
-    return ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(v >> 32)) << 32) |
-           (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)v);
-}
-
-// Block-wide minimum; thread 0 writes the block's winner.
-__device__ __forceinline__ void block_min_store(uint32_t L, uint64_t x, Winner *dst)
-{
-    __shared__ uint32_t sL[16];
-    __shared__ uint64_t sx[16];
-    wave_min(L, x);
-    const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
-    if (lane == 0) {
-        sL[wave] = L;
-        sx[wave] = x;
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        for (uint32_t w = 1; w < nw; ++w)
-            if (lex_less(sL[w], sx[w], L, x)) {
-                L = sL[w];
-                x = sx[w];
-            }
-        Winner r;
-        r.L = L;
-        r.pad = 0;
-        r.x = x;
-        *dst = r;
-    }
-}
-
-// Result of one item from its block winners, by one wave: the lexicographic (L, x) minimum,
-// the decoded per-LLM choices, T_w (Eq. 2: minimum over LLMs) and the share units.
-__device__ __forceinline__ void finish_item(const FinishArgs &fa, uint32_t item,
-                                            uint32_t blocks_per_item, const Winner *winners)
-{
-    const uint32_t lane = threadIdx.x & 63;
-    uint32_t L = kNoLatency;
-    uint64_t x = ~0ull;
-    for (uint32_t k = lane; k < blocks_per_item; k += 64) {
-        const Winner w = winners[(uint64_t)item * blocks_per_item + k];
-        if (lex_less(w.L, w.x, L, x)) {
-            L = w.L;
-            x = w.x;
-        }
-    }
-    wave_min(L, x);
-    if (lane != 0)
-        return;
-    // Assembled in registers as the six 64-bit words of alp_result_t (a local struct indexed at
-    // run time would be placed in memory for every thread of the block).
-    const SpaceDev &sp = fa.sp;
-    uint64_t word[6] = {ALP_NO_INDEX, 0, (uint64_t)ALP_INFEASIBLE << 32, 0, 0, 0};
-    if (L != kNoLatency) {
-        const uint2 *E = fa.ext + (uint64_t)item * sp.M * sp.O;
-        uint64_t rr = x;
-        uint32_t T = 0xFFFFFFFFu, U = 0;
-        uint64_t tp = 0, fq = 0, rep = 0;
-        for (int m = (int)sp.M - 1; m >= 0; --m) {
-            const uint32_t o = (uint32_t)(rr % sp.O);
-            rr /= sp.O;
-            const uint2 e = E[(uint64_t)m * sp.O + o];
-            T = e.x < T ? e.x : T;                      // Eq. 2: minimum over LLMs
-            U += e.y & 0xFFFFu;
-            const uint32_t ij = o / sp.D;
-            tp |= (uint64_t)(sp.tp[ij / sp.n_fq] & 0xFFu) << (8 * m);
-            fq |= (uint64_t)(sp.fq[ij % sp.n_fq] & 0xFFu) << (8 * m);
-            rep |= (uint64_t)((o % sp.D + 1) & 0xFFu) << (8 * m);
-        }
-        word[0] = x;
-        word[1] = (uint64_t)L | ((uint64_t)T << 32);
-        word[2] = (uint64_t)U | ((uint64_t)ALP_OK << 32);
-        word[3] = tp;
-        word[4] = fq;
-        word[5] = rep;
-    }
-    uint64_t *dst = reinterpret_cast<uint64_t *>(fa.out + item);
-#pragma unroll
-    for (int k = 0; k < 6; ++k)
-        dst[k] = word[k];
-}
-
-// Writes the block's winner; the last block of the item to finish (agent-scope fence and
-// counter, zeroed by option_terms_kernel before the scan) reduces the item's winners and
-// writes its result, so no separate reduction kernel is launched.
-__device__ __forceinline__ void block_finish(uint32_t L, uint64_t x, uint32_t item,
-                                             uint32_t sub, uint32_t blocks_per_item,
-                                             Winner *winners, const FinishArgs &fa)
-{
-    __shared__ uint32_t last_block;
-    block_min_store(L, x, &winners[(uint64_t)item * blocks_per_item + sub]);
-    if (threadIdx.x == 0) {
-        __threadfence();
-        const uint32_t prev = atomicAdd(&fa.done[item], 1u);
-        last_block = prev == blocks_per_item - 1 ? 1u : 0u;
-    }
-    __syncthreads();
-    if (last_block && threadIdx.x < 64) {
-        __threadfence();
-        finish_item(fa, item, blocks_per_item, winners);
-    }
-}
-
-// Workgroups are dispatched to the 8 XCDs round-robin; renumber them so that consecutive
-// logical blocks (the blocks of one item, which read the same few-KiB option table) share an
-// XCD and its L2.  A bijection on [0, nblocks).
-__device__ __forceinline__ uint32_t xcd_logical_block(uint32_t b, uint32_t nblocks)
-{
-    const uint32_t per = nblocks >> 3;
-    if (b >= (per << 3))
-        return b;
-    return (b & 7u) * per + (b >> 3);
-}
-
-__device__ __forceinline__ uint32_t query_value(const uint32_t *arr, uint32_t single, uint32_t i)
-{
-    return arr ? arr[i] : single;
-}
 
 }  // namespace
 

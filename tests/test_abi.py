@@ -43,7 +43,10 @@ def test_struct_layout_matches_header(tmp_path):
 #include <stddef.h>
 #include "alp.h"
 int main(void) {
-  printf("%zu %zu %zu\n", sizeof(alp_space_t), sizeof(alp_result_t), sizeof(alp_eval_t));
+  printf("%zu %zu %zu %zu %zu\n", sizeof(alp_space_t), sizeof(alp_result_t), sizeof(alp_eval_t),
+         sizeof(alp_plan_t), sizeof(alp_pruned_t));
+  printf("%zu %zu %zu %zu\n", offsetof(alp_plan_t, max_latency_us), offsetof(alp_plan_t, sum_latency_us),
+         offsetof(alp_pruned_t, fraction_vectors), offsetof(alp_pruned_t, unpruned_vectors));
   printf("%zu %zu %zu %zu %zu %zu %zu %zu\n", offsetof(alp_result_t, index),
          offsetof(alp_result_t, latency_us), offsetof(alp_result_t, throughput_milli),
          offsetof(alp_result_t, gpu_units), offsetof(alp_result_t, status),
@@ -57,8 +60,12 @@ int main(void) {
                    check=True)
     lines = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split("\n")
     sizes = [int(v) for v in lines[0].split()]
-    assert sizes == [C.sizeof(alp.Space), alp.RESULT_DTYPE.itemsize, alp.EVAL_DTYPE.itemsize]
-    offs = [int(v) for v in lines[1].split()]
+    assert sizes == [C.sizeof(alp.Space), alp.RESULT_DTYPE.itemsize, alp.EVAL_DTYPE.itemsize,
+                     alp.PLAN_DTYPE.itemsize, alp.PRUNED_DTYPE.itemsize]
+    assert [int(v) for v in lines[1].split()] == [
+        alp.PLAN_DTYPE.fields["max_latency_us"][1], alp.PLAN_DTYPE.fields["sum_latency_us"][1],
+        alp.PRUNED_DTYPE.fields["vectors"][1], alp.PRUNED_DTYPE.fields["unpruned"][1]]
+    offs = [int(v) for v in lines[2].split()]
     names = ["index", "latency_us", "throughput_milli", "gpu_units", "status", "tp", "frac_units",
              "replicas"]
     assert offs == [alp.RESULT_DTYPE.fields[n][1] for n in names]
@@ -160,4 +167,6 @@ def test_null_arguments_rejected():
     assert lib.alp_search(None, 0, 1, 1, out.ctypes.data_as(C.c_void_p)) == alp.ALP_EINVAL
     assert lib.alp_search_batch(None, 1, None, None, None, None) == alp.ALP_EINVAL
     assert lib.alp_set_launch(None, 0, 0, 0) == alp.ALP_EINVAL
+    assert lib.alp_search_pruned(None, 1, None, None, None, 3, None) == alp.ALP_EINVAL
+    assert lib.alp_allocate_workflows(None, 1, None, None, 4, 0, None, None, None) == alp.ALP_EINVAL
     lib.alp_free(None)

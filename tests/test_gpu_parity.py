@@ -317,3 +317,114 @@ def test_allocate_workflows_infeasible_and_edges(alp):
             ctx.allocate_workflows(lam, 12, 7)
         with pytest.raises(alp.AlpError):
             ctx.allocate_workflows([1] * 17, 12)
+
+
+# ------------------------------------------------------------------------------------------
+# The paper's pruned search (Section 5, steps 1-3).
+from pruned_ref import EDGE_SPACES, edge_batch  # noqa: E402
+
+
+def _check_pruned(b, i, rec, G, lam, flags):
+    inst = oracle.Instance(b, i)
+    p = oracle.pruned(inst, G, lam, flags)
+    assert (int(rec["vectors"]), int(rec["unpruned"])) == (p["vectors"], p["unpruned"]), (i, G, lam, flags)
+    if p["x"] is None:
+        check_result(b, i, rec["best"], None, None)
+        return
+    ev = oracle.evaluate(inst, G, lam, p["x"])
+    check_result(b, i, rec["best"], p["x"], p["L"], ev["T"], ev["U"])
+
+
+def _targets(b, G):
+    return [target_from_tmax(int(b["u_ppm"][i]), oracle.tmax(oracle.Instance(b, i), int(G[i])))
+            for i in range(len(G))]
+
+
+def test_pruned_hand_case(alp):
+    case = next(c for c in load_cases() if c["id"] == "H2")
+    b = case_batch(case)
+    with alp.Context(b) as ctx:
+        for q in case["pruned"]:
+            rec = ctx.search_pruned([q["G"]], [q["lambda"]], q["flags"])[0]
+            assert int(rec["vectors"]) == q["vectors"] and int(rec["unpruned"]) == q["unpruned"]
+            if q["x"] is None:
+                assert int(rec["best"]["status"]) == 5
+            else:
+                assert (int(rec["best"]["index"]), int(rec["best"]["latency_us"])) == (q["x"], q["L"])
+
+
+@pytest.mark.parametrize("cfg,count", [(0, 1000), (4, 4096)])
+def test_pruned_batch_matches_oracle(alp, cfg, count):
+    b = make_batch(cfg, range(count))
+    G = np.asarray(b["G"], dtype=np.uint32)
+    lam = _targets(b, G)
+    with alp.Context(b) as ctx:
+        out = ctx.search_pruned(G, lam)
+        for i in range(count):
+            _check_pruned(b, i, out[i], int(G[i]), lam[i], 3)
+        sub = list(range(0, count, max(1, count // 64)))
+        for flags in (0, 1, 2):
+            out = ctx.search_pruned(G[sub], [lam[i] for i in sub], flags, instances=sub)
+            for k, i in enumerate(sub):
+                _check_pruned(b, i, out[k], int(G[i]), lam[i], flags)
+
+
+@pytest.mark.parametrize("cfg,insts", [(1, range(16)), (2, range(4)), (3, [0])])
+def test_pruned_larger_spaces_match_oracle(alp, cfg, insts):
+    insts = list(insts)
+    b = make_batch(cfg, insts)
+    G = np.asarray(b["G"], dtype=np.uint32)
+    lam = _targets(b, G)
+    with alp.Context(b) as ctx:
+        for flags in ((0, 1, 2, 3) if cfg < 3 else (3, 1)):
+            out = ctx.search_pruned(G, lam, flags)
+            for i in range(len(insts)):
+                _check_pruned(b, i, out[i], int(G[i]), lam[i], flags)
+
+
+@pytest.mark.parametrize("seed,variant", EDGE_SPACES)
+def test_pruned_edge_spaces(alp, seed, variant):
+    b, G = edge_batch(seed, variant)
+    inst = oracle.Instance(b, 0)
+    tmax = oracle.tmax(inst, G)
+    lams = sorted({1, max(1, tmax // 4), max(1, tmax // 2), tmax, tmax + 1})
+    with alp.Context(b) as ctx:
+        for flags in (0, 1, 2, 3):
+            out = ctx.search_pruned([G] * len(lams), lams, flags, instances=[0] * len(lams))
+            for k, lam in enumerate(lams):
+                _check_pruned(b, 0, out[k], G, lam, flags)
+        # budgets 0..G in one batch, mixed fraction ranges
+        Gs = list(range(0, G + 1))
+        out = ctx.search_pruned(Gs, [lams[1]] * len(Gs), 3, instances=[0] * len(Gs))
+        for k, g in enumerate(Gs):
+            _check_pruned(b, 0, out[k], g, lams[1], 3)
+
+
+def test_pruned_counts_the_papers_space(alp):
+    # Section 5 step 1: 5 LLMs, 16 GPUs, 10 fractions per GPU: C(164, 4) fraction vectors.
+    b = make_custom(50, 5, (1, 2, 4, 8), (1, 2, 5, 10), 2, 2, 16, count=1, frac_den=10,
+                    param_range=(0.5e9, 70e9))
+    inst = oracle.Instance(b, 0)
+    lam = max(1, oracle.tmax(inst, 16) // 2)
+    with alp.Context(b) as ctx:
+        rec = ctx.search_pruned([16], [lam], 0)[0]
+        assert int(rec["vectors"]) == 29_051_001 == int(rec["unpruned"])
+        _check_pruned(b, 0, rec, 16, lam, 0)
+        rec = ctx.search_pruned([16], [lam], 3)[0]
+        _check_pruned(b, 0, rec, 16, lam, 3)
+        assert int(rec["vectors"]) < 29_051_001
+
+
+def test_pruned_rejects_out_of_range(alp):
+    b = make_custom(51, 5, (1, 2), (1, 2, 4), 2, 2, 64, count=1, frac_den=16)
+    with alp.Context(b) as ctx:
+        with pytest.raises(alp.AlpError) as e:
+            ctx.search_pruned([65], [1], 3)            # Q*G = 1040 units
+        assert e.value.status == alp.ALP_EINVAL
+        with pytest.raises(alp.AlpError) as e:
+            ctx.search_pruned([64], [1], 0)            # C(1028, 4) > 2^34 vectors
+        assert e.value.status == alp.ALP_ERANGE
+        with pytest.raises(alp.AlpError) as e:
+            ctx.search_pruned([4], [1], 4)
+        assert e.value.status == alp.ALP_EINVAL
+        assert len(ctx.search_pruned([], [], 3)) == 0

@@ -367,6 +367,7 @@ def test_allocate_brute_force_equals_threshold_dp():
 # The paper's pruned search (Section 5, steps 1-3).
 import math as _math  # noqa: E402
 
+from pruned_ref import EDGE_SPACES, edge_batch as _pruned_edge_batch  # noqa: E402
 from pruned_ref import placeable as _placeable, pruned as _pruned_literal  # noqa: E402
 
 
@@ -464,27 +465,6 @@ def test_pruned_matches_literal_statement(spec):
                     _pruned_literal(b, i, G, lam, flags), (i, lam, flags)
 
 
-def _pruned_edge_batch(seed, variant):
-    """Spaces where the reading details of steps 1-2 change the answer.  "tie": LLM 1 copies
-    LLM 0 except at tp = 2, so the latency ratios tie (order by index) while the LLMs differ;
-    "flip": LLM 0's smallest share is 7x slower, so the order at the smallest share differs from
-    the order at the largest; "weightless": LLM 0 has no weights (lower bound of one unit).
-    Shares of 3 quarters make packed fractions straddle GPUs."""
-    fqs = [(1, 2, 3, 4), (1, 3, 4), (2, 3, 4)][seed % 3]
-    D, K, G = 3 + seed % 2, 1 + (seed // 2) % 2, 3 + (seed // 3) % 2
-    b = make_custom(seed, 3, (1, 2), fqs, D, K, G, count=1, param_range=(0.5e9, 150e9))
-    if variant == "tie":
-        for key in ("W", "n", "p", "allowed", "rate", "lat"):
-            b[key][:, 1] = b[key][:, 0]
-        b["lat"][:, 1, 1, :, :] *= 2
-    elif variant == "flip":
-        b["lat"][:, 0, :, 0, :] *= 7
-    elif variant == "weightless":
-        b["W"][:, 0] = 0
-    return b, G
-
-
-EDGE_SPACES = [(100, "flip"), (101, "tie"), (103, "tie"), (23, "weightless"), (104, "flip")]
 
 
 @pytest.mark.parametrize("seed,variant", EDGE_SPACES)
