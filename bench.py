@@ -5,15 +5,22 @@
 One step = one complete search (alp_search: per-option terms, exhaustive scan of every
 candidate, final reduction and result decode, result copied to the host) over the synthetic
 workload; for ``--workload multi`` it is one alp_allocate_workflows call (every per-workflow
-budget searched exhaustively, then the budget split).  The default workload is the 5-LLM space with G = 64 GPUs and 128 options per LLM
-(2^35 = 34,359,738,368 candidates per step).  Inputs are resident in HBM before timing starts.
-Prints one JSON line.
+budget searched exhaustively, then the budget split).  The default workload is the 5-LLM space
+with G = 64 GPUs and 128 options per LLM (2^35 = 34,359,738,368 candidates per step).  Inputs
+are resident in HBM before timing starts.  Prints one JSON line.
 
 ``value`` = candidates evaluated per second.  ``roofline`` relates the scan kernel (the dominant
 kernel) to the integer VALU peak of the chip: 2 int32 lane operations per candidate (the budget
 comparison and the objective minimum update), 256 CUs x 64 lanes x 2.4 GHz = 39.32 Tlane-op/s;
 the kernel duration is measured with HIP events on the stream the library launches on.
 ``cpu_baseline`` times the CPU oracle, single-threaded, on a bounded slice of the same space.
+
+The paper's own pruned search (alp_search_pruned) has two workloads of its own, where a step is
+one pruned search and ``value`` counts fraction vectors per second:
+  ``pruned``        the 4,096-instance batch of the exhaustive ``cfg4`` workload, with the
+                    optimality gap against the exhaustive results on the same instances;
+  ``pruned-paper``  the point of the paper's scheduler micro-benchmark: ``--llms`` LLMs,
+                    ``--budget`` GPUs, ``--fractions`` fractions per GPU (default 5, 16, 10).
 """
 from __future__ import annotations
 
@@ -28,15 +35,18 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-from workloads import CONFIGS, make_batch, target_from_tmax  # noqa: E402
+from workloads import CONFIGS, make_batch, make_custom, target_from_tmax  # noqa: E402
 
 PEAK_LANE_OPS = 256 * 64 * 2.4e9        # int32 VALU lane-ops/s of MI355X
 OPS_PER_CANDIDATE = 2                   # budget compare + objective min
-WORKLOADS = {"cfg2": 2, "cfg3": 3, "cfg4": 4, "cfg1": 1, "multi": 2}
+WORKLOADS = {"cfg2": 2, "cfg3": 3, "cfg4": 4, "cfg1": 1, "multi": 2, "pruned": 4,
+             "pruned-paper": None}
 # Several workflows sharing one GPU pool: four 4-LLM workflows drawn like the 4-LLM workload
 # split 32 GPUs under egalitarian welfare; each workflow's target is set at an even share.
 MULTI_WORKFLOWS, MULTI_GPUS = 4, 32
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "scan_min_hbm_bytes.md")
+KERNEL_SOURCES = ("alp_kernels.hip", "alp_device.h", "alp_internal.h")
+METRIC = "ALP candidate allocations evaluated/sec on 1 GPU"
 
 
 def _traffic(kernel_digest: str, workload: str):
@@ -52,9 +62,6 @@ def _traffic(kernel_digest: str, workload: str):
     if not entry or t.get("kernel_source_sha256") != kernel_digest:
         return None
     return entry.get("bytes_per_launch")
-
-
-KERNEL_SOURCES = ("alp_kernels.hip", "alp_device.h", "alp_internal.h")
 
 
 def _kernel_digest() -> str:
@@ -84,6 +91,64 @@ def cpu_baseline(batch, G, lam, seconds: float):
                       f"single-threaded C oracle ({dt:.1f} s)"}
 
 
+def cpu_baseline_pruned(batch, G, lam, seconds: float):
+    """Single-threaded oracle pruned search over the batch's first instances, ~seconds."""
+    import oracle
+    vectors, done, t0 = 0, 0, time.perf_counter()
+    while done < len(G) and time.perf_counter() - t0 < seconds:
+        vectors += oracle.pruned(oracle.Instance(batch, done), int(G[done]), int(lam[done]))["vectors"]
+        done += 1
+    dt = time.perf_counter() - t0
+    return {"value": vectors / dt, "unit": "fraction vectors/s", "cores": 1, "kind": "oracle",
+            "sample": f"pruned search of the first {done} instances ({vectors:,} fraction "
+                      f"vectors), single-threaded C oracle ({dt:.1f} s)"}
+
+
+def timed_steps(step, ctx, steps: int, warmup: int):
+    """Runs warmup + steps calls; returns (elapsed s, per-step kernel times, last output)."""
+    import torch
+    for _ in range(warmup):
+        step()
+    ctx.set_timing(True)
+    times = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        out = step()
+        times.append(ctx.kernel_times())
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ctx.set_timing(False)
+    return elapsed, times, out
+
+
+def gap_stats(pruned, exhaustive) -> dict:
+    """Pruned results against exhaustive ones on the same queries."""
+    ok_p = pruned["best"]["status"] == 0
+    ok_e = exhaustive["status"] == 0
+    both = ok_p & ok_e
+    Lp = pruned["best"]["latency_us"].astype(np.float64)
+    Le = exhaustive["latency_us"].astype(np.float64)
+    worse = both & (Lp > Le)
+    rel = (Lp[worse] / Le[worse] - 1.0) if worse.any() else np.zeros(0)
+    return {"queries": int(len(ok_e)), "exhaustive_feasible": int(ok_e.sum()),
+            "pruned_feasible": int(ok_p.sum()),
+            "same_optimum": int((both & (Lp == Le)).sum()),
+            "same_allocation": int((both & (pruned["best"]["index"] == exhaustive["index"])).sum()),
+            "worse": int(worse.sum()), "pruned_infeasible_only": int((ok_e & ~ok_p).sum()),
+            "mean_gap_when_worse": float(rel.mean()) if len(rel) else 0.0,
+            "max_gap": float(rel.max()) if len(rel) else 0.0}
+
+
+def paper_point(llms: int, budget: int, fractions: int):
+    """Synthetic instance at the paper's scheduler micro-benchmark point: llms LLMs drawn like
+    the 5-LLM workload (1B-70B parameters, Dirichlet 0.5 shares), budget GPUs, `fractions`
+    share units per GPU; shares are up to 8 values spread over 1..fractions, 4 replica counts."""
+    fq = sorted({max(1, round(fractions * k / 8)) for k in range(1, 9)})
+    return make_custom(2604, llms, (1, 2, 4, 8), fq, 4, 8, budget, count=1, frac_den=fractions,
+                       param_range=(1e9, 70e9), alpha=0.5)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -93,6 +158,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--variant", type=int, default=0)
+    ap.add_argument("--llms", type=int, default=5, help="pruned-paper: LLMs")
+    ap.add_argument("--budget", type=int, default=16, help="pruned-paper: GPUs")
+    ap.add_argument("--fractions", type=int, default=10, help="pruned-paper: fractions per GPU")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after timing, run one plain device copy of this size (for scaling "
                          "hardware byte counters)")
@@ -108,6 +176,29 @@ def main():
     if not torch.cuda.is_available():
         print("no GPU visible", file=sys.stderr)
         sys.exit(1)
+    if args.workload.startswith("pruned"):
+        line = run_pruned(args, alp)
+    else:
+        line = run_exhaustive(args, alp)
+    if args.calib_copy_mib:
+        src = torch.ones(args.calib_copy_mib << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        line["calib_copy_bytes"] = args.calib_copy_mib << 20
+    print(json.dumps(line), flush=True)
+
+
+def _line(args, value, unit, elapsed, dtype_cfg, roofline, cpu):
+    return {"metric": METRIC, "value": value, "unit": unit, "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": elapsed / args.steps * 1e3,
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u32",
+            "data": "synthetic (seeded profile tables, see workloads/)", "config": dtype_cfg,
+            "roofline": roofline, "cpu_baseline": cpu}
+
+
+def run_exhaustive(args, alp):
     cfg_id = WORKLOADS[args.workload]
     cfg = CONFIGS[cfg_id]
     multi = args.workload == "multi"
@@ -135,66 +226,81 @@ def main():
             return int(out["status"].max())
         return int(ctx.search(0, int(G[0]), int(lam[0]))["status"])
 
-    for _ in range(args.warmup):
-        step()
-    ctx.set_timing(True)
-    scan_ms = []
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        status = step()
-        scan_ms.append(ctx.kernel_times()[1])
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    ctx.set_timing(False)
+    elapsed, times, status = timed_steps(step, ctx, args.steps, args.warmup)
     assert status in (0, 5)
-    terms_ms, _, split_ms, blocks = ctx.kernel_times()
-
+    terms_ms, _, split_ms, blocks = times[-1]
     value = per_step * args.steps / elapsed
-    avg_scan_s = float(np.mean(scan_ms)) / 1e3
+    avg_scan_s = float(np.mean([t[1] for t in times])) / 1e3
     achieved = per_step * OPS_PER_CANDIDATE / avg_scan_s
-    digest = _kernel_digest()
-    line = {
-        "metric": "ALP candidate allocations evaluated/sec on 1 GPU",
-        "value": value,
-        "unit": "candidates/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": elapsed / args.steps * 1e3,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "u32",
-        "data": "synthetic (seeded profile tables, see workloads/)",
-        "config": {"workload": (f"{MULTI_WORKFLOWS} workflows of {cfg.num_llms} LLMs share "
-                                f"{MULTI_GPUS} GPUs (egalitarian welfare): all "
-                                f"{MULTI_WORKFLOWS * (MULTI_GPUS + 1)} per-workflow budget "
-                                "searches, then the budget split") if multi
-                   else f"{cfg.name}: {cfg.description}",
-                   "candidates_per_step": per_step, "instances": len(insts),
-                   "llms": cfg.num_llms, "gpu_budget": MULTI_GPUS if multi else cfg.gpu_budget,
-                   "options_per_llm": len(cfg.tp_values) * len(cfg.frac_q) * cfg.max_replicas,
-                   "scan_blocks": blocks},
-        "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_LANE_OPS / 1e12,
-                     "unit": "TOP/s", "frac": achieved / PEAK_LANE_OPS,
-                     "traffic": _traffic(digest, args.workload),
-                     "kernel": "scan", "kernel_ms": avg_scan_s * 1e3,
-                     "ops_per_candidate": OPS_PER_CANDIDATE,
-                     "other_kernels_ms": {"option_terms": terms_ms, "budget_split": split_ms}},
-        "cpu_baseline": None,
-    }
+    config = {"workload": (f"{MULTI_WORKFLOWS} workflows of {cfg.num_llms} LLMs share "
+                           f"{MULTI_GPUS} GPUs (egalitarian welfare): all "
+                           f"{MULTI_WORKFLOWS * (MULTI_GPUS + 1)} per-workflow budget "
+                           "searches, then the budget split") if multi
+              else f"{cfg.name}: {cfg.description}",
+              "candidates_per_step": per_step, "instances": len(insts),
+              "llms": cfg.num_llms, "gpu_budget": MULTI_GPUS if multi else cfg.gpu_budget,
+              "options_per_llm": len(cfg.tp_values) * len(cfg.frac_q) * cfg.max_replicas,
+              "scan_blocks": blocks}
+    roofline = {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_LANE_OPS / 1e12,
+                "unit": "TOP/s", "frac": achieved / PEAK_LANE_OPS,
+                "traffic": _traffic(_kernel_digest(), args.workload),
+                "kernel": "scan", "kernel_ms": avg_scan_s * 1e3,
+                "ops_per_candidate": OPS_PER_CANDIDATE,
+                "other_kernels_ms": {"option_terms": terms_ms, "budget_split": split_ms}}
+    cpu = None
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(batch, int(G[0]), int(lam[0]), args.cpu_seconds)
+        cpu = cpu_baseline(batch, int(G[0]), int(lam[0]), args.cpu_seconds)
     ctx.close()
-    if args.calib_copy_mib:
-        src = torch.ones(args.calib_copy_mib << 20, dtype=torch.uint8, device="cuda")
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        line["calib_copy_bytes"] = args.calib_copy_mib << 20
-    print(json.dumps(line), flush=True)
+    return _line(args, value, "candidates/s", elapsed, config, roofline, cpu)
+
+
+def run_pruned(args, alp):
+    if args.workload == "pruned":
+        cfg = CONFIGS[4]
+        batch = make_batch(4, range(cfg.num_instances))
+        what = (f"the paper's pruned search (Section 5 steps 1-3) on {cfg.name}: "
+                f"{cfg.num_instances} instances of 3 LLMs, G=16, 4 share units per GPU")
+    else:
+        batch = paper_point(args.llms, args.budget, args.fractions)
+        what = (f"the paper's pruned search at its scheduler micro-benchmark point: "
+                f"{args.llms} LLMs, {args.budget} GPUs, {args.fractions} fractions per GPU")
+    ctx = alp.Context(batch)
+    G = np.asarray(batch["G"], dtype=np.uint32)
+    tmax = ctx.max_throughput(G)
+    lam = np.asarray([target_from_tmax(int(batch["u_ppm"][i]), int(tmax[i]))
+                      for i in range(len(G))], dtype=np.uint32)
+    first = ctx.search_pruned(G, lam)
+    vectors = int(first["vectors"].sum())
+
+    def step():
+        return ctx.search_pruned(G, lam)
+
+    elapsed, times, out = timed_steps(step, ctx, args.steps, args.warmup)
+    assert (out["best"]["index"] == first["best"]["index"]).all()
+    avg_enum_s = float(np.mean([t[1] for t in times])) / 1e3
+    avg_table_ms = float(np.mean([t[2] for t in times]))
+    # exhaustive results of the same queries for the gap, outside the timed region (skipped
+    # beyond 2^36 candidates per query, a minute of scanning)
+    exhaustive = ctx.search_batch(G, lam) if ctx.num_candidates <= (1 << 36) else None
+    ops_per_vector = 2 * int(batch["space"]["M"])    # per LLM: add L, accumulate the index
+    achieved = vectors * ops_per_vector / avg_enum_s
+    config = {"workload": what, "instances": int(len(G)), "llms": int(batch["space"]["M"]),
+              "units_per_gpu": int(batch["space"]["Q"]), "gpu_budget": int(G[0]),
+              "fraction_vectors_per_step": vectors,
+              "unpruned_vectors_per_query": int(first["unpruned"][0]),
+              "gap_vs_exhaustive": None if exhaustive is None else gap_stats(out, exhaustive),
+              "enumeration_blocks": times[-1][3]}
+    roofline = {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_LANE_OPS / 1e12,
+                "unit": "TOP/s", "frac": achieved / PEAK_LANE_OPS, "traffic": None,
+                "kernel": "fraction enumeration", "kernel_ms": avg_enum_s * 1e3,
+                "ops_per_vector": ops_per_vector,
+                "other_kernels_ms": {"option_terms": times[-1][0], "option_table": avg_table_ms}}
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline_pruned(batch, G, lam, args.cpu_seconds)
+    ctx.close()
+    return _line(args, vectors * args.steps / elapsed, "fraction vectors/s", elapsed, config,
+                 roofline, cpu)
 
 
 if __name__ == "__main__":

@@ -196,7 +196,7 @@ int32_t alp_allocate_workflows(alp_ctx *ctx, uint32_t count, const uint32_t *ins
  * The result is the feasible admissible candidate of lowest L_w, ties to the lowest index. */
 #define ALP_PRUNE_ORDER 1u
 #define ALP_PRUNE_MIN_FRACTION 2u
-#define ALP_PRUNED_MAX_UNITS 1024u           /* Q*G per query */
+#define ALP_PRUNED_MAX_UNITS 2048u           /* Q*G per query */
 #define ALP_PRUNED_MAX_VECTORS (1ull << 34)  /* step-1 vectors per query, before bounds */
 
 /* One pruned search (64 bytes). */

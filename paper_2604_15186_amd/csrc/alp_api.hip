@@ -102,7 +102,7 @@ struct alp_ctx {
 
     DevBuf q_inst, rec, ext, inner, done, winners, idx, evals, tmax;   // q_inst: inst | cap | lambda
     DevBuf split_dp;                        // allocate_kernel's knapsack table
-    DevBuf pruned_table, pruned_counts;     // pruned search: option table, per-block counts
+    DevBuf pruned_table, pruned_orders, pruned_counts;   // pruned search scratch
     alp_pruned_t *host_pruned = nullptr;    // mapped pinned results of pruned searches
     alp_pruned_t *host_pruned_dev = nullptr;
     size_t host_pruned_cap = 0;
@@ -779,14 +779,14 @@ int32_t alp_search_pruned(alp_ctx *ctx, uint32_t count, const uint32_t *instance
         if (F > ALP_PRUNED_MAX_UNITS)
             return fail(ALP_EINVAL, "query %u: Q*G = %llu above %u for the pruned search", i,
                         (unsigned long long)F, ALP_PRUNED_MAX_UNITS);
-        if (pruned_vector_bound((uint32_t)F, sp.M, flags & ALP_PRUNE_ORDER) > ALP_PRUNED_MAX_VECTORS)
-            return fail(ALP_ERANGE, "query %u: more than 2^34 fraction vectors", i);
         cap[i] = (uint32_t)F;
         F_max = std::max(F_max, cap[i]);
     }
+    // the bound grows with the number of units: checking the largest query covers all
+    if (pruned_vector_bound(F_max, sp.M, flags & ALP_PRUNE_ORDER) > ALP_PRUNED_MAX_VECTORS)
+        return fail(ALP_ERANGE, "Q*G = %u: more than 2^34 fraction vectors per query", F_max);
     const uint64_t F1 = (uint64_t)F_max + 1;
-    const uint64_t prefixes = sp.M >= 3 ? F1 * F1 : sp.M == 2 ? F1 : 1;
-    const uint32_t bpi = (uint32_t)ceil_div(prefixes, 256);
+    const uint32_t bpi = (uint32_t)ceil_div(alp::pruned_prefixes(sp.M, F_max), 256);
     const uint64_t nblocks = (uint64_t)count * bpi;
     if (nblocks >= (UINT64_C(1) << 31))
         return fail(ALP_ERANGE, "batch too large for one launch (%llu blocks)",
@@ -801,7 +801,8 @@ int32_t alp_search_pruned(alp_ctx *ctx, uint32_t count, const uint32_t *instance
         (e = ctx->done.ensure((uint64_t)count * sizeof(uint32_t))) != hipSuccess ||
         (e = ctx->winners.ensure(nblocks * sizeof(alp::Winner))) != hipSuccess ||
         (e = ctx->pruned_counts.ensure(nblocks * sizeof(uint64_t))) != hipSuccess ||
-        (e = ctx->pruned_table.ensure((uint64_t)count * sp.M * sp.Q * F1 * sizeof(uint2))) != hipSuccess)
+        (e = ctx->pruned_table.ensure((uint64_t)count * sp.M * sp.Q * F1 * sizeof(uint64_t))) != hipSuccess ||
+        (e = ctx->pruned_orders.ensure((uint64_t)count * alp::pruned_order_bytes())) != hipSuccess)
         return hip_fail(e, "hipMalloc(pruned search)");
     if (count > ctx->host_pruned_cap) {
         if (ctx->host_pruned)
@@ -833,13 +834,14 @@ int32_t alp_search_pruned(alp_ctx *ctx, uint32_t count, const uint32_t *instance
         return hip_fail(e, "option_terms launch");
     if (ctx->timing && (e = hipEventRecord(ctx->ev[1], ctx->stream)) != hipSuccess)
         return hip_fail(e, "hipEventRecord");
-    if ((e = alp::launch_pruned_table(sp, count, F_max, rec, (uint2 *)ctx->pruned_table.ptr,
+    if ((e = alp::launch_pruned_table(sp, ctx->tdev, q, count, F_max, flags, rec,
+                                      (uint64_t *)ctx->pruned_table.ptr, ctx->pruned_orders.ptr,
                                       ctx->stream)) != hipSuccess)
         return hip_fail(e, "pruned table launch");
     if (ctx->timing && (e = hipEventRecord(ctx->ev[2], ctx->stream)) != hipSuccess)
         return hip_fail(e, "hipEventRecord");
-    if ((e = alp::launch_pruned_scan(sp, ctx->tdev, q, count, F_max, flags,
-                                     (const uint2 *)ctx->pruned_table.ptr, bpi,
+    if ((e = alp::launch_pruned_scan(sp, count, F_max, flags,
+                                     (const uint64_t *)ctx->pruned_table.ptr, ctx->pruned_orders.ptr, bpi,
                                      (alp::Winner *)ctx->winners.ptr,
                                      (uint64_t *)ctx->pruned_counts.ptr, ext, done,
                                      ctx->host_pruned_dev, ctx->stream)) != hipSuccess)
@@ -965,7 +967,7 @@ void alp_free(alp_ctx *ctx)
             (void)hipEventDestroy(ctx->ev[k]);
     DevBuf *bufs[] = {&ctx->tables, &ctx->q_inst, &ctx->rec, &ctx->ext, &ctx->inner, &ctx->done,
                       &ctx->winners, &ctx->idx, &ctx->evals, &ctx->tmax, &ctx->split_dp,
-                      &ctx->pruned_table, &ctx->pruned_counts};
+                      &ctx->pruned_table, &ctx->pruned_orders, &ctx->pruned_counts};
     for (DevBuf *b : bufs)
         b->release();
     if (ctx->host_results)

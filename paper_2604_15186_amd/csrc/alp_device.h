@@ -151,6 +151,12 @@ __device__ __forceinline__ bool block_store_last(uint32_t L, uint64_t x, uint32_
 {
     __shared__ uint32_t last_block;
     block_min_store(L, x, &winners[(uint64_t)item * blocks_per_item + sub]);
+    if (blocks_per_item == 1) {
+        // The block is the whole item: its own writes only need to reach its own threads.
+        __threadfence_block();
+        __syncthreads();
+        return true;
+    }
     if (threadIdx.x == 0) {
         __threadfence();
         const uint32_t prev = atomicAdd(&done[item], 1u);
@@ -172,6 +178,15 @@ __device__ __forceinline__ void block_finish(uint32_t L, uint64_t x, uint32_t it
 {
     __shared__ uint32_t last_block;
     block_min_store(L, x, &winners[(uint64_t)item * blocks_per_item + sub]);
+    if (blocks_per_item == 1) {
+        // The block is the whole item: no agent-scope fence (an L2 write-back across XCDs) or
+        // counter; its winner only needs to reach its own first wave.
+        __threadfence_block();
+        __syncthreads();
+        if (threadIdx.x < 64)
+            finish_item(fa, item, 1, winners);
+        return;
+    }
     if (threadIdx.x == 0) {
         __threadfence();
         const uint32_t prev = atomicAdd(&fa.done[item], 1u);

@@ -99,16 +99,20 @@ hipError_t launch_allocate(const alp_result_t *res, uint32_t W, uint32_t G, uint
                            uint64_t *dp, alp_plan_t *plan, uint32_t *gpus, hipStream_t st);
 
 // The paper's pruned search for count items (see alp_search_pruned), after the option-term
-// kernel (rec, ext; it also zeroes done[]).  Table kernel: count * M * Q * (F_max + 1) entries.
-// Enumeration kernel: blocks_per_item blocks of 256 threads cover (F_max + 1)^min(2, M - 1)
-// prefixes per item; winners and counts hold count * blocks_per_item entries; writes
-// out[0..count).
-hipError_t launch_pruned_table(const SpaceDev &sp, uint32_t count, uint32_t F_max,
-                               const uint2 *rec, uint2 *table, hipStream_t st);
-hipError_t launch_pruned_scan(const SpaceDev &sp, const TablesDev &tb, const QueryDev &q,
-                              uint32_t count, uint32_t F_max, uint32_t flags, const uint2 *table,
-                              uint32_t blocks_per_item, Winner *winners, uint64_t *counts,
-                              const uint2 *ext, uint32_t *done, alp_pruned_t *out, hipStream_t st);
+// kernel (rec, ext; it also zeroes done[]).  launch_pruned_table fills `table`
+// (count * M * Q * (F_max + 1) entries) and `orders` (count records of pruned_order_bytes());
+// launch_pruned_scan runs blocks_per_item blocks of 256 threads per item, covering
+// pruned_prefixes(M, F_max) threads; winners and counts hold count * blocks_per_item entries.
+// Writes out[0..count).
+uint64_t pruned_prefixes(uint32_t M, uint32_t F_max);
+size_t pruned_order_bytes();
+hipError_t launch_pruned_table(const SpaceDev &sp, const TablesDev &tb, const QueryDev &q,
+                               uint32_t count, uint32_t F_max, uint32_t flags, const uint2 *rec,
+                               uint64_t *table, void *orders, hipStream_t st);
+hipError_t launch_pruned_scan(const SpaceDev &sp, uint32_t count, uint32_t F_max, uint32_t flags,
+                              const uint64_t *table, const void *orders, uint32_t blocks_per_item,
+                              Winner *winners, uint64_t *counts, const uint2 *ext, uint32_t *done,
+                              alp_pruned_t *out, hipStream_t st);
 
 static_assert(sizeof(alp_pruned_t) == 64 && offsetof(alp_pruned_t, fraction_vectors) == 48 &&
                   offsetof(alp_pruned_t, unpruned_vectors) == 56,

@@ -11,15 +11,19 @@
 //           its packed GPUs.
 //
 // Kernels:
-//   pruned_table_kernel      per (item, LLM, first-unit offset mod Q, fraction f): the
-//                            admissible option of smallest Eq. 1 contribution (lowest index
-//                            among equal ones).  With the fraction vector fixed the LLMs are
-//                            independent and L_w is a sum, so this table decides every vector.
-//   pruned_scan_kernel<M>    one thread per prefix of the first two fractions; the remaining
-//                            fractions are enumerated in registers (compile-time depth), each
-//                            vector summed from the table; the lexicographic (L_w, x) minimum
-//                            and the vector count are reduced per block, and the item's last
-//                            block writes the result.
+//   pruned_prep_kernel       clears the option table and computes each item's step-1 order and
+//                            bounds.
+//   pruned_scatter_kernel    per (item, LLM, option): enters the option into the table entry
+//                            (item, LLM, first-unit offset mod Q, fraction = its units) of every
+//                            offset where it fits, keeping the smallest Eq. 1 contribution
+//                            (lowest option among equal ones).  With the fraction vector fixed
+//                            the LLMs are independent and L_w is a sum, so this table decides
+//                            every vector.
+//   pruned_scan_kernel<M>    one thread per prefix (the first fraction, or the first two beyond
+//                            3 LLMs); the remaining fractions are enumerated in registers
+//                            (compile-time depth), each vector summed from the table; the
+//                            lexicographic (L_w, x) minimum and the vector count are reduced per
+//                            block, and the item's last block writes the result.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -52,47 +56,107 @@ __device__ __forceinline__ bool placement_fits(uint32_t Q, uint32_t r, uint32_t 
     return ranks >= tp * d;
 }
 
-__global__ void __launch_bounds__(256)
-pruned_table_kernel(SpaceDev sp, const uint2 *__restrict__ rec, uint32_t count, uint32_t F1,
-                    uint2 *__restrict__ table)
-{
-    const uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const uint64_t total = (uint64_t)count * sp.M * sp.Q * F1;
-    if (t >= total)
-        return;
-    const uint32_t f = (uint32_t)(t % F1);
-    const uint64_t imr = t / F1;
-    const uint32_t r = (uint32_t)(imr % sp.Q);
-    const uint64_t im = imr / sp.Q;                    // item * M + m
-    const uint2 *R = rec + im * sp.O;
-    uint32_t best_c = kNoLatency, best_o = 0;
-    for (uint32_t o = 0; o < sp.O; ++o) {
-        const uint2 e = R[o];
-        if (e.y != f)                                  // unusable options carry the sentinel
-            continue;
-        const uint32_t ij = o / sp.D;
-        if (!placement_fits(sp.Q, r, f, sp.tp[ij / sp.n_fq], sp.fq[ij % sp.n_fq], o % sp.D + 1))
-            continue;
-        if (e.x < best_c) {
-            best_c = e.x;
-            best_o = o;
-        }
-    }
-    table[t] = make_uint2(best_c, best_o);
-}
+// Table entries pack (c << 32 | option): the 64-bit minimum is the smallest contribution, then
+// the lowest option.  No admissible option: all ones (c = kNoLatency).
+constexpr uint64_t kNoEntry = ~0ull;
 
-// Per-item constants of step 1, by position in the latency-ratio order.
-template <int M>
+// Per-item constants of step 1, by position in the latency-ratio order (first M entries used).
 struct Order {
-    uint32_t lo[M], hi[M], lo_after[M];
-    uint64_t pw[M];                 // O^(M-1-m) of the LLM at the position
-    uint64_t tab[M];                // offset of its table rows, in entries
+    uint32_t lo[ALP_MAX_LLMS], hi[ALP_MAX_LLMS], lo_after[ALP_MAX_LLMS];
+    uint64_t pw[ALP_MAX_LLMS];      // O^(M-1-m) of the LLM at the position
+    uint64_t tab[ALP_MAX_LLMS];     // offset of its table rows in the item's table, in entries
     uint32_t F, empty;
 };
 
-template <int M>
+// Fills the option table with kNoEntry and, in the first `count` threads, computes each item's
+// step-1 order: latency ratios (contribution at tp[0], the largest share, the first profiled
+// point), largest first with ties by LLM index, the lower bounds max(1, ceil(W Q / H)) with the
+// minimum-fraction flag, and the upper bounds Q*G minus the lower bounds after each position.
+__global__ void __launch_bounds__(256)
+pruned_prep_kernel(SpaceDev sp, TablesDev tb, QueryDev q, uint32_t count, uint32_t F1,
+                   uint32_t flags, uint64_t *__restrict__ table, Order *__restrict__ orders)
+{
+    const uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t < (uint64_t)count * sp.M * sp.Q * F1)
+        table[t] = kNoEntry;
+    if (t >= count)
+        return;
+    const uint32_t item = (uint32_t)t, M = sp.M;
+    const uint32_t inst = query_value(q.inst, q.inst1, item);
+    const uint32_t F = query_value(q.capacity, q.cap1, item);
+    uint64_t ref[ALP_MAX_LLMS];
+    uint32_t order[ALP_MAX_LLMS];
+    for (uint32_t m = 0; m < M; ++m) {
+        const uint64_t base = (uint64_t)inst * M + m;
+        const uint64_t cell = (base * sp.n_tp + 0) * sp.n_fq + (sp.n_fq - 1);
+        ref[m] = (uint64_t)tb.lat[cell * sp.K] * tb.n[base] / tb.p[base];
+        order[m] = m;
+    }
+    for (uint32_t a = 1; a < M; ++a) {
+        const uint32_t v = order[a];
+        uint32_t b = a;
+        while (b > 0 && ref[order[b - 1]] < ref[v]) {
+            order[b] = order[b - 1];
+            --b;
+        }
+        order[b] = v;
+    }
+    Order od;
+    uint64_t after = 0;
+    od.empty = 0;
+    for (int k = (int)M - 1; k >= 0; --k) {
+        const uint32_t m = order[k];
+        const uint64_t base = (uint64_t)inst * M + m;
+        uint64_t lo = 0;
+        if (flags & ALP_PRUNE_MIN_FRACTION) {
+            const uint64_t need = (tb.W[base] * sp.Q + tb.H - 1) / tb.H;
+            lo = need > 1 ? need : 1;
+        }
+        if (after + lo > F) {
+            od.empty = 1;
+            lo = 0;
+        }
+        od.lo[k] = (uint32_t)lo;
+        od.lo_after[k] = (uint32_t)after;
+        od.hi[k] = after <= F ? F - (uint32_t)after : 0u;
+        after += lo;
+        uint64_t pw = 1;
+        for (uint32_t j = m + 1; j < M; ++j)
+            pw *= sp.O;
+        od.pw[k] = pw;
+        od.tab[k] = (uint64_t)m * sp.Q * F1;
+    }
+    od.F = F;
+    orders[item] = od;
+}
+
+// One thread per (item, LLM, option): an option usable at the query (ok and within
+// saturation) with u units is admissible for fraction f = u at every first-unit offset r
+// (mod Q) where its replicas fit; it enters those entries by a 64-bit minimum.
+__global__ void __launch_bounds__(256)
+pruned_scatter_kernel(SpaceDev sp, const uint2 *__restrict__ rec, uint32_t count, uint32_t F1,
+                      uint64_t *__restrict__ table)
+{
+    const uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= (uint64_t)count * sp.M * sp.O)
+        return;
+    const uint32_t o = (uint32_t)(t % sp.O);
+    const uint64_t im = t / sp.O;                       // item * M + m
+    const uint2 e = rec[t];
+    const uint32_t u = e.y;                             // unusable options carry the sentinel
+    if (u >= F1)
+        return;
+    const uint32_t ij = o / sp.D;
+    const uint32_t tp = sp.tp[ij / sp.n_fq], q = sp.fq[ij % sp.n_fq], d = o % sp.D + 1;
+    const uint64_t key = ((uint64_t)e.x << 32) | o;
+    for (uint32_t r = 0; r < sp.Q; ++r)
+        if (placement_fits(sp.Q, r, u, tp, q, d))
+            atomicMin((unsigned long long *)&table[(im * sp.Q + r) * F1 + u],
+                      (unsigned long long)key);
+}
+
 struct Walk {
-    const uint2 *table;
+    const uint64_t *table;
     uint32_t Q, F1;
     bool ordered;
     uint32_t L;                     // running best (L, x) and vector count of the thread
@@ -103,7 +167,7 @@ struct Walk {
 // Position K receives v units starting at unit `offset`; returns false if v is outside the
 // position's range.  Adds the LLM's table entry when every LLM so far has an admissible option.
 template <int M, int K>
-__device__ __forceinline__ bool place_at(const Order<M> &od, const Walk<M> &w, uint32_t offset,
+__device__ __forceinline__ bool place_at(const Order &od, const Walk &w, uint32_t offset,
                                          uint32_t remaining, uint32_t prev, uint32_t v,
                                          uint32_t &L, uint64_t &x, bool &alive)
 {
@@ -113,19 +177,19 @@ __device__ __forceinline__ bool place_at(const Order<M> &od, const Walk<M> &w, u
     if (v < od.lo[K] || v > hi || v > remaining || remaining - v < od.lo_after[K])
         return false;
     if (alive) {
-        const uint2 e = w.table[od.tab[K] + (offset % w.Q) * w.F1 + v];
-        if (e.x == kNoLatency) {
+        const uint64_t e = w.table[od.tab[K] + (offset % w.Q) * w.F1 + v];
+        if (e == kNoEntry) {
             alive = false;
         } else {
-            L += e.x;
-            x += (uint64_t)e.y * od.pw[K];
+            L += (uint32_t)(e >> 32);
+            x += (uint64_t)(uint32_t)e * od.pw[K];
         }
     }
     return true;
 }
 
 template <int M, int K>
-__device__ __forceinline__ void walk_from(const Order<M> &od, Walk<M> &w, uint32_t offset,
+__device__ __forceinline__ void walk_from(const Order &od, Walk &w, uint32_t offset,
                                           uint32_t remaining, uint32_t prev, uint32_t L,
                                           uint64_t x, bool alive)
 {
@@ -180,69 +244,36 @@ __device__ uint64_t binomial_sat(uint32_t n, uint32_t k)
     return out;
 }
 
+// Fractions fixed per thread: the first one for up to 3 LLMs, the first two beyond.
+template <int M>
+constexpr int kPrefix = M <= 3 ? 1 : 2;
+
+// The item's table (M * Q * F1 entries) is copied to LDS first when `stage` is set (the
+// launch then provides that much dynamic LDS): the walk's loads are dependent, and LDS latency
+// is far below that of L2 or HBM.
 template <int M>
 __global__ void __launch_bounds__(256)
-pruned_scan_kernel(SpaceDev sp, TablesDev tb, QueryDev q, uint32_t F1, uint32_t flags,
-                   const uint2 *__restrict__ table, uint32_t blocks_per_item,
+pruned_scan_kernel(SpaceDev sp, const Order *__restrict__ orders, uint32_t F1, uint32_t flags,
+                   const uint64_t *__restrict__ table, uint32_t stage, uint32_t blocks_per_item,
                    Winner *__restrict__ winners, uint64_t *__restrict__ counts,
                    const uint2 *__restrict__ ext, uint32_t *__restrict__ done,
                    alp_pruned_t *__restrict__ out)
 {
-    __shared__ Order<M> s_od;
+    extern __shared__ __align__(8) unsigned char s_dyn[];
     const uint32_t item = blockIdx.x / blocks_per_item;
     const uint32_t sub = blockIdx.x % blocks_per_item;
-    if (threadIdx.x == 0) {
-        // Step 1 constants: latency ratios (contribution at tp[0], the largest share, the first
-        // profiled point), the order (largest first, ties by LLM index), the bounds.
-        const uint32_t inst = query_value(q.inst, q.inst1, item);
-        const uint32_t F = query_value(q.capacity, q.cap1, item);
-        uint64_t ref[M];
-        uint32_t order[M];
-        for (int m = 0; m < M; ++m) {
-            const uint64_t base = (uint64_t)inst * M + m;
-            const uint64_t cell = (base * sp.n_tp + 0) * sp.n_fq + (sp.n_fq - 1);
-            ref[m] = (uint64_t)tb.lat[cell * sp.K] * tb.n[base] / tb.p[base];
-            order[m] = (uint32_t)m;
-        }
-        for (int a = 1; a < M; ++a) {
-            const uint32_t v = order[a];
-            int b = a;
-            while (b > 0 && ref[order[b - 1]] < ref[v]) {
-                order[b] = order[b - 1];
-                --b;
-            }
-            order[b] = v;
-        }
-        uint64_t after = 0;
-        s_od.empty = 0;
-        for (int k = M - 1; k >= 0; --k) {
-            const uint32_t m = order[k];
-            const uint64_t base = (uint64_t)inst * M + m;
-            uint64_t lo = 0;
-            if (flags & ALP_PRUNE_MIN_FRACTION) {
-                const uint64_t need = (tb.W[base] * sp.Q + tb.H - 1) / tb.H;
-                lo = need > 1 ? need : 1;
-            }
-            if (after + lo > F) {
-                s_od.empty = 1;
-                lo = 0;
-            }
-            s_od.lo[k] = (uint32_t)lo;
-            s_od.lo_after[k] = (uint32_t)after;
-            s_od.hi[k] = after <= F ? F - (uint32_t)after : 0u;
-            after += lo;
-            uint64_t pw = 1;
-            for (int j = (int)m + 1; j < M; ++j)
-                pw *= sp.O;
-            s_od.pw[k] = pw;
-            s_od.tab[k] = (((uint64_t)item * M + m) * sp.Q) * F1;
-        }
-        s_od.F = F;
+    const Order od = orders[item];
+    const uint64_t per_item = (uint64_t)M * sp.Q * F1;
+    const uint64_t *tab = table + item * per_item;
+    if (stage) {
+        uint64_t *s_tab = reinterpret_cast<uint64_t *>(s_dyn);
+        for (uint32_t k = threadIdx.x; k < per_item; k += blockDim.x)
+            s_tab[k] = tab[k];
+        __syncthreads();
+        tab = s_tab;
     }
-    __syncthreads();
-    const Order<M> od = s_od;
-    Walk<M> w;
-    w.table = table;
+    Walk w;
+    w.table = tab;
     w.Q = sp.Q;
     w.F1 = F1;
     w.ordered = (flags & ALP_PRUNE_ORDER) != 0;
@@ -256,7 +287,7 @@ pruned_scan_kernel(SpaceDev sp, TablesDev tb, QueryDev q, uint32_t F1, uint32_t 
         if constexpr (M == 1) {
             if (t == 0)
                 walk_from<M, 0>(od, w, 0, F, 0, 0, 0, true);
-        } else if constexpr (M == 2) {
+        } else if constexpr (kPrefix<M> == 1) {
             if (t <= F) {
                 uint32_t L = 0;
                 uint64_t x = 0;
@@ -316,30 +347,52 @@ pruned_scan_kernel(SpaceDev sp, TablesDev tb, QueryDev q, uint32_t F1, uint32_t 
 
 }  // namespace
 
-hipError_t launch_pruned_table(const SpaceDev &sp, uint32_t count, uint32_t F_max,
-                               const uint2 *rec, uint2 *table, hipStream_t st)
+// Largest per-item table staged in LDS (with the static LDS, well inside the 64 KiB a block
+// gets without an opt-in).
+constexpr uint64_t kStageBytes = 48 * 1024;
+
+uint64_t pruned_prefixes(uint32_t M, uint32_t F_max)
 {
-    const uint64_t entries = (uint64_t)count * sp.M * sp.Q * (F_max + 1);
-    if (entries == 0)
+    const uint64_t F1 = (uint64_t)F_max + 1;
+    return M == 1 ? 1 : M <= 3 ? F1 : F1 * F1;
+}
+
+hipError_t launch_pruned_table(const SpaceDev &sp, const TablesDev &tb, const QueryDev &q,
+                               uint32_t count, uint32_t F_max, uint32_t flags, const uint2 *rec,
+                               uint64_t *table, void *orders, hipStream_t st)
+{
+    if (count == 0)
         return hipSuccess;
-    hipLaunchKernelGGL(pruned_table_kernel, dim3((uint32_t)((entries + 255) / 256)), dim3(256), 0,
-                       st, sp, rec, count, F_max + 1, table);
+    const uint32_t F1 = F_max + 1;
+    const uint64_t entries = (uint64_t)count * sp.M * sp.Q * F1;
+    hipLaunchKernelGGL(pruned_prep_kernel, dim3((uint32_t)((entries + 255) / 256)), dim3(256), 0,
+                       st, sp, tb, q, count, F1, flags, table, (Order *)orders);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess)
+        return e;
+    const uint64_t options = (uint64_t)count * sp.M * sp.O;
+    hipLaunchKernelGGL(pruned_scatter_kernel, dim3((uint32_t)((options + 255) / 256)), dim3(256),
+                       0, st, sp, rec, count, F1, table);
     return hipGetLastError();
 }
 
-hipError_t launch_pruned_scan(const SpaceDev &sp, const TablesDev &tb, const QueryDev &q,
-                              uint32_t count, uint32_t F_max, uint32_t flags, const uint2 *table,
-                              uint32_t blocks_per_item, Winner *winners, uint64_t *counts,
-                              const uint2 *ext, uint32_t *done, alp_pruned_t *out, hipStream_t st)
+hipError_t launch_pruned_scan(const SpaceDev &sp, uint32_t count, uint32_t F_max, uint32_t flags,
+                              const uint64_t *table, const void *orders, uint32_t blocks_per_item,
+                              Winner *winners, uint64_t *counts, const uint2 *ext, uint32_t *done,
+                              alp_pruned_t *out, hipStream_t st)
 {
     if (count == 0)
         return hipSuccess;
     const uint32_t F1 = F_max + 1;
     const dim3 grid(count * blocks_per_item), block(256);
+    const Order *od = (const Order *)orders;
+    const uint64_t item_bytes = (uint64_t)sp.M * sp.Q * F1 * sizeof(uint64_t);
+    const uint32_t stage = item_bytes <= kStageBytes ? 1u : 0u;
+    const size_t lds = stage ? (size_t)item_bytes : 0;
 #define ALP_PRUNED_CASE(MM)                                                                        \
     case MM:                                                                                       \
-        hipLaunchKernelGGL(pruned_scan_kernel<MM>, grid, block, 0, st, sp, tb, q, F1, flags,      \
-                           table, blocks_per_item, winners, counts, ext, done, out);              \
+        hipLaunchKernelGGL(pruned_scan_kernel<MM>, grid, block, lds, st, sp, od, F1, flags,       \
+                           table, stage, blocks_per_item, winners, counts, ext, done, out);       \
         break;
     switch (sp.M) {
         ALP_PRUNED_CASE(1)
@@ -356,5 +409,7 @@ hipError_t launch_pruned_scan(const SpaceDev &sp, const TablesDev &tb, const Que
 #undef ALP_PRUNED_CASE
     return hipGetLastError();
 }
+
+size_t pruned_order_bytes() { return sizeof(Order); }
 
 }  // namespace alp

@@ -419,7 +419,7 @@ def test_pruned_rejects_out_of_range(alp):
     b = make_custom(51, 5, (1, 2), (1, 2, 4), 2, 2, 64, count=1, frac_den=16)
     with alp.Context(b) as ctx:
         with pytest.raises(alp.AlpError) as e:
-            ctx.search_pruned([65], [1], 3)            # Q*G = 1040 units
+            ctx.search_pruned([129], [1], 3)           # Q*G = 2064 units
         assert e.value.status == alp.ALP_EINVAL
         with pytest.raises(alp.AlpError) as e:
             ctx.search_pruned([64], [1], 0)            # C(1028, 4) > 2^34 vectors
