@@ -17,8 +17,9 @@ the kernel duration is measured with HIP events on the stream the library launch
 
 The paper's own pruned search (alp_search_pruned) has two workloads of its own, where a step is
 one pruned search and ``value`` counts fraction vectors per second:
-  ``pruned``        the 4,096-instance batch of the exhaustive ``cfg4`` workload, with the
-                    optimality gap against the exhaustive results on the same instances;
+  ``pruned``        the 4,096-instance batch of the exhaustive ``cfg4`` workload (another
+                    workload's instances with ``--config``), with the optimality gap against
+                    the exhaustive results on the same instances;
   ``pruned-paper``  the point of the paper's scheduler micro-benchmark: ``--llms`` LLMs,
                     ``--budget`` GPUs, ``--fractions`` fractions per GPU (default 5, 16, 10).
 """
@@ -158,6 +159,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--variant", type=int, default=0)
+    ap.add_argument("--config", type=int, default=4, choices=sorted(CONFIGS),
+                    help="pruned: the workload whose instances are searched (default: the "
+                         "4,096-instance batch)")
     ap.add_argument("--llms", type=int, default=5, help="pruned-paper: LLMs")
     ap.add_argument("--budget", type=int, default=16, help="pruned-paper: GPUs")
     ap.add_argument("--fractions", type=int, default=10, help="pruned-paper: fractions per GPU")
@@ -256,10 +260,11 @@ def run_exhaustive(args, alp):
 
 def run_pruned(args, alp):
     if args.workload == "pruned":
-        cfg = CONFIGS[4]
-        batch = make_batch(4, range(cfg.num_instances))
+        cfg = CONFIGS[args.config]
+        batch = make_batch(args.config, range(cfg.num_instances))
         what = (f"the paper's pruned search (Section 5 steps 1-3) on {cfg.name}: "
-                f"{cfg.num_instances} instances of 3 LLMs, G=16, 4 share units per GPU")
+                f"{cfg.num_instances} instance(s) of {cfg.num_llms} LLMs, G={cfg.gpu_budget}, "
+                f"4 share units per GPU")
     else:
         batch = paper_point(args.llms, args.budget, args.fractions)
         what = (f"the paper's pruned search at its scheduler micro-benchmark point: "
