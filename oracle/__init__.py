@@ -92,8 +92,11 @@ def lib():
         L.orc_count_fractions.restype = C.c_uint64
         L.orc_binomial.argtypes = [C.c_uint64, C.c_uint64]
         L.orc_binomial.restype = C.c_uint64
+        L.orc_trace_stats.argtypes = [C.c_uint32, C.c_uint32, C.c_void_p, C.c_void_p, C.c_void_p,
+                                      C.c_void_p, C.c_void_p, C.c_void_p]
         for f in (L.orc_option_term, L.orc_eval, L.orc_eval_many, L.orc_argmin, L.orc_tmax_brute,
-                  L.orc_tmax_threshold, L.orc_allocate, L.orc_pruned, L.orc_fits):
+                  L.orc_tmax_threshold, L.orc_allocate, L.orc_pruned, L.orc_fits,
+                  L.orc_trace_stats):
             f.restype = C.c_int
         _lib = L
     return _lib
@@ -253,3 +256,23 @@ def count_fractions(M: int, total: int, lo, ordered: bool) -> int:
 
 def binomial(n: int, k: int) -> int:
     return int(lib().orc_binomial(n, k))
+
+
+STATS_DTYPE = np.dtype([("n_milli", np.uint32), ("p_milli", np.uint32), ("calls", np.uint64),
+                        ("busy_us", np.uint64), ("active_us", np.uint64)])
+
+
+def trace_stats(M: int, offsets, llm, start, end) -> np.ndarray:
+    """Workflow statistics n_m, p_m per LLM from traces (see orc_trace_stats)."""
+    offsets = np.ascontiguousarray(offsets, dtype=np.uint64)
+    llm = np.ascontiguousarray(llm, dtype=np.uint32)
+    start = np.ascontiguousarray(start, dtype=np.uint64)
+    end = np.ascontiguousarray(end, dtype=np.uint64)
+    R = len(offsets) - 1
+    longest = int(np.diff(offsets.astype(np.int64)).max()) if R > 0 else 0
+    scratch = np.zeros(2 * max(1, longest), dtype=np.uint64)
+    out = np.zeros(M, dtype=STATS_DTYPE)
+    if lib().orc_trace_stats(M, R, offsets.ctypes.data, llm.ctypes.data, start.ctypes.data,
+                             end.ctypes.data, scratch.ctypes.data, out.ctypes.data) != 0:
+        raise ValueError("malformed traces")
+    return out

@@ -37,6 +37,7 @@
  */
 #include <stdint.h>
 #include <stddef.h>
+#include <stdlib.h>
 
 #define ORC_U64_NONE UINT64_MAX
 
@@ -547,5 +548,85 @@ int orc_pruned(const orc_instance *s, uint32_t G, uint32_t lambda, uint32_t flag
     out->best_L = e.best_x == ORC_U64_NONE ? ORC_U64_NONE : e.best_L;
     out->vectors = e.vectors;
     out->unpruned = orc_binomial(total + s->M - 1, s->M - 1);
+    return 0;
+}
+
+/* ---------------------------------------------------------------------------------------------
+ * Workflow statistics from execution traces (Section 4, step 2).  A trace is one workflow
+ * request: the LLM-level calls it made, each with its LLM, start and end timestamp (half-open
+ * [start, end), microseconds).  For every LLM m:
+ *   n_m = average number of calls per workflow request = calls_m / traces;
+ *   p_m = average request-level parallelism, from overlapping timestamps: the calls' total
+ *         duration divided by the time during which at least one call of m runs, summed over
+ *         the traces.  (Then n_m * L_m / p_m of Eq. 1 is the time per request during which m is
+ *         active.)  Three concurrent beams give p = 3.
+ * Both in thousandths, rounded down; p = 1000 when m has calls but no measurable time, and
+ * n = p = 0 when m has no calls.
+ * ------------------------------------------------------------------------------------------- */
+
+typedef struct {
+    uint32_t n_milli, p_milli;
+    uint64_t calls, busy_us, active_us;
+} orc_stats;
+
+static int orc_cmp_u64(const void *a, const void *b)
+{
+    uint64_t x = *(const uint64_t *)a, y = *(const uint64_t *)b;
+    return x < y ? -1 : x > y;
+}
+
+/* offsets[R + 1] delimit each trace's calls.  scratch: 2 * (longest trace) uint64.  Returns 0, or
+ * -1 for a malformed input (offsets not ascending from 0, llm >= M, end < start). */
+int orc_trace_stats(uint32_t M, uint32_t R, const uint64_t *offsets, const uint32_t *llm,
+                    const uint64_t *start, const uint64_t *end, uint64_t *scratch,
+                    orc_stats *out)
+{
+    if (M == 0 || M > 16 || R == 0 || offsets[0] != 0)
+        return -1;
+    for (uint32_t m = 0; m < M; ++m) {
+        out[m].calls = out[m].busy_us = out[m].active_us = 0;
+    }
+    for (uint32_t r = 0; r < R; ++r) {
+        uint64_t lo = offsets[r], hi = offsets[r + 1];
+        if (hi < lo)
+            return -1;
+        for (uint32_t m = 0; m < M; ++m) {
+            /* this LLM's intervals in the trace, sorted by start (end as the tie-breaker) */
+            uint64_t k = 0;
+            for (uint64_t i = lo; i < hi; ++i) {
+                if (llm[i] >= M || end[i] < start[i])
+                    return -1;
+                if (llm[i] != m)
+                    continue;
+                scratch[2 * k] = start[i];
+                scratch[2 * k + 1] = end[i];
+                ++k;
+            }
+            qsort(scratch, k, 2 * sizeof(uint64_t), orc_cmp_u64);
+            /* sweep: the union grows by the part of each interval beyond the furthest end so far */
+            uint64_t reach = 0, active = 0, busy = 0;
+            for (uint64_t j = 0; j < k; ++j) {
+                uint64_t s = scratch[2 * j], e = scratch[2 * j + 1];
+                busy += e - s;
+                uint64_t from = (j == 0 || s > reach) ? s : reach;
+                if (e > from)
+                    active += e - from;
+                if (j == 0 || e > reach)
+                    reach = e;
+            }
+            out[m].calls += k;
+            out[m].busy_us += busy;
+            out[m].active_us += active;
+        }
+    }
+    for (uint32_t m = 0; m < M; ++m) {
+        out[m].n_milli = (uint32_t)(out[m].calls * 1000u / R);
+        if (out[m].calls == 0)
+            out[m].p_milli = 0;
+        else if (out[m].active_us == 0)
+            out[m].p_milli = 1000;
+        else
+            out[m].p_milli = (uint32_t)(out[m].busy_us * 1000u / out[m].active_us);
+    }
     return 0;
 }
