@@ -215,6 +215,48 @@ int32_t alp_search_pruned(alp_ctx *ctx, uint32_t count, const uint32_t *instance
                           const uint32_t *gpu_budget, const uint32_t *target_milli, uint32_t flags,
                           alp_pruned_t *out);
 
+/* ---- Workflow statistics from execution traces (Section 4, step 2) --------------------------
+ * A trace is one workflow-level request: the LLM-level calls it made, each with its LLM index
+ * and a half-open [start, end) interval in microseconds (tools and other non-LLM components are
+ * left out by the caller).  For every LLM m:
+ *   n_m = calls of m per workflow request = calls_m / traces;
+ *   p_m = request-level parallelism from overlapping timestamps = the total duration of m's
+ *         calls divided by the time during which at least one call of m runs, summed over the
+ *         traces (so that n_m * L_m / p_m in Eq. 1 is the time per request m is active).
+ * Both in thousandths, rounded down; p = 1000 if m has calls but none of positive length, and
+ * n = p = 0 if m has no calls.  The results are the n_milli / p_milli inputs of
+ * alp_load_profiles. */
+typedef struct {
+    uint32_t n_milli;
+    uint32_t p_milli;
+    uint64_t calls;        /* calls of the LLM over all traces */
+    uint64_t busy_us;      /* sum of their durations */
+    uint64_t active_us;    /* sum over traces of the time at least one of them runs */
+} alp_stats_t;
+
+typedef struct alp_stats_ctx alp_stats_ctx;
+
+/* A statistics context on `device`, ordering its work on hip_stream (NULL: the default
+ * stream).  It owns the device scratch of the computation until alp_stats_free. */
+int32_t alp_stats_create(alp_stats_ctx **out, int32_t device, void *hip_stream);
+
+/* Statistics of num_traces traces.  Device pointers: offsets[num_traces + 1] (ascending from 0;
+ * trace r's calls are [offsets[r], offsets[r + 1])), llm[E], start_us[E], end_us[E] with
+ * E = offsets[num_traces].  num_llms in 1..8; a trace has at most 2^24 calls; start < 2^60 and
+ * end - start < 2^32.  Writes out[0..num_llms) (host).  EINVAL for a malformed input (offsets,
+ * llm >= num_llms, end < start), ERANGE for out-of-range timestamps or a result of 2^31 or
+ * more.  Synchronous on the context's stream. */
+int32_t alp_trace_stats(alp_stats_ctx *ctx, uint32_t num_llms, uint32_t num_traces,
+                        const uint64_t *offsets, const uint32_t *llm, const uint64_t *start_us,
+                        const uint64_t *end_us, alp_stats_t *out);
+
+/* Enables HIP-event timing; alp_stats_time gives the milliseconds of the last computation's
+ * kernels (initialisation to final division). */
+int32_t alp_stats_set_timing(alp_stats_ctx *ctx, int32_t enable);
+int32_t alp_stats_time(alp_stats_ctx *ctx, float *ms);
+
+void alp_stats_free(alp_stats_ctx *ctx);
+
 /* Evaluates count given candidate indices (each < O^M, else EINVAL) of one instance. */
 int32_t alp_eval_candidates(alp_ctx *ctx, uint32_t instance, uint32_t gpu_budget,
                             uint32_t target_milli, const uint64_t *indices, uint64_t count,

@@ -21,8 +21,10 @@ MAX_LLMS = 8
 
 # Symbols declared in include/alp.h.
 EXPORTS = ("alp_load_profiles", "alp_search", "alp_search_batch", "alp_max_throughput",
-           "alp_allocate_workflows", "alp_search_pruned", "alp_eval_candidates", "alp_set_launch", "alp_set_timing", "alp_kernel_times",
-           "alp_num_candidates", "alp_free", "alp_status_str", "alp_last_error")
+           "alp_allocate_workflows", "alp_search_pruned", "alp_stats_create", "alp_trace_stats",
+           "alp_stats_set_timing", "alp_stats_time", "alp_stats_free", "alp_eval_candidates",
+           "alp_set_launch", "alp_set_timing", "alp_kernel_times", "alp_num_candidates", "alp_free",
+           "alp_status_str", "alp_last_error")
 
 
 class AlpError(RuntimeError):
@@ -49,6 +51,9 @@ PLAN_DTYPE = np.dtype([("status", np.uint32), ("policy", np.uint32), ("max_laten
 PRUNED_DTYPE = np.dtype([("best", RESULT_DTYPE), ("vectors", np.uint64), ("unpruned", np.uint64)])
 assert RESULT_DTYPE.itemsize == 48 and EVAL_DTYPE.itemsize == 16 and PLAN_DTYPE.itemsize == 24
 assert PRUNED_DTYPE.itemsize == 64
+STATS_DTYPE = np.dtype([("n_milli", np.uint32), ("p_milli", np.uint32), ("calls", np.uint64),
+                        ("busy_us", np.uint64), ("active_us", np.uint64)])
+assert STATS_DTYPE.itemsize == 32
 WELFARE_EGALITARIAN, WELFARE_SOCIAL = 0, 1
 PRUNE_ORDER, PRUNE_MIN_FRACTION = 1, 2
 
@@ -71,13 +76,20 @@ def lib():
         L.alp_eval_candidates.argtypes = [vp, u32, u32, u32, vp, u64, vp]
         L.alp_allocate_workflows.argtypes = [vp, u32, vp, vp, u32, u32, vp, vp, vp]
         L.alp_search_pruned.argtypes = [vp, u32, vp, vp, vp, u32, vp]
+        L.alp_stats_create.argtypes = [C.POINTER(vp), i32, vp]
+        L.alp_trace_stats.argtypes = [vp, u32, u32, vp, vp, vp, vp, vp]
+        L.alp_stats_set_timing.argtypes = [vp, i32]
+        L.alp_stats_time.argtypes = [vp, C.POINTER(C.c_float)]
+        L.alp_stats_free.argtypes = [vp]
+        L.alp_stats_free.restype = None
         L.alp_set_launch.argtypes = [vp, u32, u32, u32]
         L.alp_set_timing.argtypes = [vp, i32]
         L.alp_kernel_times.argtypes = [vp, C.POINTER(C.c_float), C.POINTER(u32)]
         L.alp_num_candidates.argtypes = [vp, C.POINTER(u64)]
         for name in ("alp_load_profiles", "alp_search", "alp_search_batch", "alp_max_throughput",
-                     "alp_allocate_workflows", "alp_search_pruned", "alp_eval_candidates",
-                     "alp_set_launch", "alp_set_timing",
+                     "alp_allocate_workflows", "alp_search_pruned", "alp_stats_create",
+                     "alp_trace_stats", "alp_stats_set_timing", "alp_stats_time",
+                     "alp_eval_candidates", "alp_set_launch", "alp_set_timing",
                      "alp_kernel_times", "alp_num_candidates"):
             getattr(L, name).restype = i32
         L.alp_free.argtypes = [vp]
@@ -250,6 +262,63 @@ class Context:
         blocks = C.c_uint32()
         _check(lib().alp_kernel_times(self._ctx, ms, C.byref(blocks)))
         return float(ms[0]), float(ms[1]), float(ms[2]), int(blocks.value)
+
+
+class StatsContext:
+    """Workflow statistics from execution traces on one GPU (alp_stats_create / alp_trace_stats).
+
+    ``compute`` takes torch tensors already on the device (offsets and timestamps 64-bit, llm
+    32-bit), or numpy arrays, which it copies to the device first with torch."""
+
+    def __init__(self, device: int = 0, stream: int | None = None):
+        self.device = device
+        self.stream = torch_stream(device) if stream is None else int(stream)
+        self._ctx = C.c_void_p()
+        _check(lib().alp_stats_create(C.byref(self._ctx), device, self.stream))
+
+    @staticmethod
+    def _device_array(a, dtype, device):
+        import torch
+        if isinstance(a, torch.Tensor):
+            assert a.is_cuda and a.is_contiguous() and a.element_size() == np.dtype(dtype).itemsize
+            return a
+        a = np.ascontiguousarray(a, dtype=dtype)
+        signed = {np.dtype(np.uint64): np.int64, np.dtype(np.uint32): np.int32}[a.dtype]
+        return torch.from_numpy(a.view(signed)).to(f"cuda:{device}")
+
+    def compute(self, num_llms: int, offsets, llm, start, end) -> np.ndarray:
+        dev = [self._device_array(a, t, self.device) for a, t in
+               ((offsets, np.uint64), (llm, np.uint32), (start, np.uint64), (end, np.uint64))]
+        out = np.zeros(num_llms, dtype=STATS_DTYPE)
+        R = int(dev[0].numel()) - 1
+        _check(lib().alp_trace_stats(self._ctx, num_llms, R,
+                                     *(C.c_void_p(t.data_ptr()) for t in dev), _ptr(out)))
+        return out
+
+    def set_timing(self, enable: bool):
+        _check(lib().alp_stats_set_timing(self._ctx, 1 if enable else 0))
+
+    def time_ms(self) -> float:
+        ms = C.c_float()
+        _check(lib().alp_stats_time(self._ctx, C.byref(ms)))
+        return float(ms.value)
+
+    def close(self):
+        if self._ctx:
+            lib().alp_stats_free(self._ctx)
+            self._ctx = C.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
 
 
 def result_dict(r) -> dict:

@@ -981,6 +981,171 @@ void alp_free(alp_ctx *ctx)
     delete ctx;
 }
 
+struct alp_stats_ctx {
+    int device = 0;
+    hipStream_t stream = nullptr;
+    DevBuf totals, long_list, long_base, scratch;
+    alp_stats_t *host_out = nullptr;        // mapped pinned: results
+    alp_stats_t *host_out_dev = nullptr;
+    std::vector<uint64_t> offsets;
+    int timing = 0;
+    hipEvent_t ev[2] = {nullptr, nullptr};
+    float last_ms = 0.0f;
+};
+
+int32_t alp_stats_create(alp_stats_ctx **out, int32_t device, void *hip_stream)
+{
+    if (!out)
+        return fail(ALP_EINVAL, "out is NULL");
+    *out = nullptr;
+    alp_stats_ctx *c = new (std::nothrow) alp_stats_ctx;
+    if (!c)
+        return fail(ALP_ENOMEM, "context allocation");
+    c->device = device;
+    c->stream = (hipStream_t)hip_stream;
+    DeviceGuard guard(device);
+    hipError_t e = guard.status;
+    if (e == hipSuccess)
+        e = hipHostMalloc((void **)&c->host_out, ALP_MAX_LLMS * sizeof(alp_stats_t),
+                          hipHostMallocMapped);
+    if (e == hipSuccess)
+        e = hipHostGetDevicePointer((void **)&c->host_out_dev, c->host_out, 0);
+    for (int k = 0; k < 2 && e == hipSuccess; ++k)
+        e = hipEventCreate(&c->ev[k]);
+    if (e == hipSuccess)
+        e = c->totals.ensure((3 * ALP_MAX_LLMS + 1) * sizeof(uint64_t));
+    if (e != hipSuccess) {
+        alp_stats_free(c);
+        return hip_fail(e, "statistics context");
+    }
+    *out = c;
+    return ALP_OK;
+}
+
+int32_t alp_trace_stats(alp_stats_ctx *c, uint32_t num_llms, uint32_t num_traces,
+                        const uint64_t *offsets, const uint32_t *llm, const uint64_t *start_us,
+                        const uint64_t *end_us, alp_stats_t *out)
+{
+    constexpr uint64_t kMaxTrace = 1ull << 24, kLdsMax = 2048;   // 2 x 2048 x 8 B of LDS
+    if (!c || !offsets || !out)
+        return fail(ALP_EINVAL, "ctx, offsets or out is NULL");
+    if (num_llms < 1 || num_llms > ALP_MAX_LLMS)
+        return fail(ALP_EINVAL, "num_llms %u outside 1..%d", num_llms, ALP_MAX_LLMS);
+    if (num_traces < 1 || num_traces >= (1u << 31))
+        return fail(ALP_EINVAL, "num_traces %u outside 1..2^31-1", num_traces);
+    DeviceGuard guard(c->device);
+    if (guard.status != hipSuccess)
+        return hip_fail(guard.status, "hipSetDevice");
+    hipError_t e;
+    c->offsets.resize((size_t)num_traces + 1);
+    if ((e = hipMemcpyAsync(c->offsets.data(), offsets, c->offsets.size() * sizeof(uint64_t),
+                            hipMemcpyDeviceToHost, c->stream)) != hipSuccess ||
+        (e = hipStreamSynchronize(c->stream)) != hipSuccess)
+        return hip_fail(e, "copy offsets");
+    if (c->offsets[0] != 0)
+        return fail(ALP_EINVAL, "offsets[0] = %llu, not 0", (unsigned long long)c->offsets[0]);
+    std::vector<uint32_t> longs;
+    std::vector<uint64_t> bases;
+    uint64_t max_short = 0, scratch_pairs = 0;
+    for (uint32_t r = 0; r < num_traces; ++r) {
+        if (c->offsets[r + 1] < c->offsets[r])
+            return fail(ALP_EINVAL, "offsets decrease at trace %u", r);
+        const uint64_t n = c->offsets[r + 1] - c->offsets[r];
+        if (n > kMaxTrace)
+            return fail(ALP_ERANGE, "trace %u has %llu calls (at most 2^24)", r, (unsigned long long)n);
+        if (n > kLdsMax) {
+            uint64_t P = 256;
+            while (P < n)
+                P <<= 1;
+            longs.push_back(r);
+            bases.push_back(scratch_pairs);
+            scratch_pairs += P;
+        } else if (n > max_short) {
+            max_short = n;
+        }
+    }
+    if (c->offsets[num_traces] > 0 && (!llm || !start_us || !end_us))
+        return fail(ALP_EINVAL, "llm, start_us or end_us is NULL");
+    uint32_t lds_cap = 256;
+    while (lds_cap < max_short)
+        lds_cap <<= 1;
+    if (!longs.empty()) {
+        if ((e = c->long_list.ensure(longs.size() * sizeof(uint32_t))) != hipSuccess ||
+            (e = c->long_base.ensure(bases.size() * sizeof(uint64_t))) != hipSuccess ||
+            (e = c->scratch.ensure(scratch_pairs * 2 * sizeof(uint64_t))) != hipSuccess)
+            return hip_fail(e, "hipMalloc(statistics scratch)");
+        if ((e = hipMemcpyAsync(c->long_list.ptr, longs.data(), longs.size() * sizeof(uint32_t),
+                                hipMemcpyHostToDevice, c->stream)) != hipSuccess ||
+            (e = hipMemcpyAsync(c->long_base.ptr, bases.data(), bases.size() * sizeof(uint64_t),
+                                hipMemcpyHostToDevice, c->stream)) != hipSuccess)
+            return hip_fail(e, "copy long traces");
+    }
+    uint64_t *totals = (uint64_t *)c->totals.ptr;
+    uint32_t *flags = (uint32_t *)(totals + 3 * ALP_MAX_LLMS);
+    if (c->timing && (e = hipEventRecord(c->ev[0], c->stream)) != hipSuccess)
+        return hip_fail(e, "hipEventRecord");
+    if ((e = alp::launch_trace_stats(num_llms, num_traces, offsets, llm, start_us, end_us, lds_cap,
+                                     (uint32_t)longs.size(), (const uint32_t *)c->long_list.ptr,
+                                     (const uint64_t *)c->long_base.ptr, (uint64_t *)c->scratch.ptr,
+                                     totals, flags, c->host_out_dev, c->stream)) != hipSuccess)
+        return hip_fail(e, "statistics launch");
+    if (c->timing && (e = hipEventRecord(c->ev[1], c->stream)) != hipSuccess)
+        return hip_fail(e, "hipEventRecord");
+    uint32_t host_flags = 0;
+    if ((e = hipMemcpyAsync(&host_flags, flags, sizeof(uint32_t), hipMemcpyDeviceToHost,
+                            c->stream)) != hipSuccess ||
+        (e = hipStreamSynchronize(c->stream)) != hipSuccess)
+        return hip_fail(e, "statistics");
+    if (c->timing && (e = hipEventElapsedTime(&c->last_ms, c->ev[0], c->ev[1])) != hipSuccess)
+        return hip_fail(e, "hipEventElapsedTime");
+    if (host_flags & 1u)
+        return fail(ALP_EINVAL, "a call's llm index is not below num_llms");
+    if (host_flags & 2u)
+        return fail(ALP_EINVAL, "a call ends before it starts");
+    if (host_flags & 4u)
+        return fail(ALP_ERANGE, "a start time of 2^60 us or more, or a duration of 2^32 us or more");
+    if (host_flags & 8u)
+        return fail(ALP_ERANGE, "n or p of 2^31 thousandths or more");
+    memcpy(out, c->host_out, num_llms * sizeof(alp_stats_t));
+    return ALP_OK;
+}
+
+int32_t alp_stats_set_timing(alp_stats_ctx *ctx, int32_t enable)
+{
+    if (!ctx)
+        return fail(ALP_EINVAL, "ctx is NULL");
+    ctx->timing = enable ? 1 : 0;
+    return ALP_OK;
+}
+
+int32_t alp_stats_time(alp_stats_ctx *ctx, float *ms)
+{
+    if (!ctx || !ms)
+        return fail(ALP_EINVAL, "ctx or ms is NULL");
+    *ms = ctx->last_ms;
+    return ALP_OK;
+}
+
+void alp_stats_free(alp_stats_ctx *c)
+{
+    if (!c)
+        return;
+    DeviceGuard guard(c->device);
+    if (c->stream)
+        (void)hipStreamSynchronize(c->stream);
+    else
+        (void)hipDeviceSynchronize();
+    for (int k = 0; k < 2; ++k)
+        if (c->ev[k])
+            (void)hipEventDestroy(c->ev[k]);
+    DevBuf *bufs[] = {&c->totals, &c->long_list, &c->long_base, &c->scratch};
+    for (DevBuf *b : bufs)
+        b->release();
+    if (c->host_out)
+        (void)hipHostFree(c->host_out);
+    delete c;
+}
+
 const char *alp_status_str(int32_t status)
 {
     switch (status) {

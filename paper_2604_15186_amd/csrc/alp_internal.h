@@ -114,9 +114,22 @@ hipError_t launch_pruned_scan(const SpaceDev &sp, uint32_t count, uint32_t F_max
                               Winner *winners, uint64_t *counts, const uint2 *ext, uint32_t *done,
                               alp_pruned_t *out, hipStream_t st);
 
+static_assert(sizeof(alp_stats_t) == 32 && offsetof(alp_stats_t, calls) == 8 &&
+                  offsetof(alp_stats_t, active_us) == 24,
+              "alp_stats_t layout");
 static_assert(sizeof(alp_pruned_t) == 64 && offsetof(alp_pruned_t, fraction_vectors) == 48 &&
                   offsetof(alp_pruned_t, unpruned_vectors) == 56,
               "alp_pruned_t layout");
+
+// Workflow statistics (see alp_trace_stats).  Traces up to lds_cap calls (a power of two,
+// 256..2048) are sorted in LDS; the num_long others (long_traces[]) in scratch, trace k at
+// 2 * long_base[k] words (2 * pow2(length) words each).  totals: 3 * ALP_MAX_LLMS + 1 words
+// (the last is the status flags).  Writes out[0..M).
+hipError_t launch_trace_stats(uint32_t M, uint32_t R, const uint64_t *offsets, const uint32_t *llm,
+                              const uint64_t *start, const uint64_t *end, uint32_t lds_cap,
+                              uint32_t num_long, const uint32_t *long_traces,
+                              const uint64_t *long_base, uint64_t *scratch, uint64_t *totals,
+                              uint32_t *flags, alp_stats_t *out, hipStream_t st);
 
 // Resident blocks per CU of the scan kernels at a given block size (occupancy query).
 int scan_blocks_per_cu(uint32_t variant, uint32_t slots, uint32_t threads, const SpaceDev &sp);

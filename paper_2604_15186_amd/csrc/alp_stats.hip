@@ -1,0 +1,247 @@
+// gfx950 kernels for the workflow statistics of Scepsy (arXiv 2604.15186, Section 4, step 2):
+// per LLM m, n_m = calls per workflow request and p_m = request-level parallelism, from
+// execution traces (one trace per workflow request; each LLM call has an LLM index and a
+// half-open [start, end) interval in microseconds).
+//
+//   p_m = (sum of m's call durations) / (sum over traces of the time at least one call of m
+//         runs), so that n_m * L_m / p_m (Eq. 1) is the time per request during which m is
+//         active.  n_m and p_m are reported in thousandths, rounded down.
+//
+// Kernels:
+//   stats_init_kernel        zeroes the per-LLM totals and the error flags.
+//   trace_stats_kernel<G>    one workgroup per trace: the calls are sorted by key
+//                            (llm << 60 | start) with a bitonic network (in LDS, or for long
+//                            traces in a global scratch region, G = true); the time covered by
+//                            each LLM follows from an exclusive prefix maximum of
+//                            (llm << 61 | end) -- an interval adds the part of it beyond the
+//                            furthest end of the same LLM's earlier intervals; per-LLM call
+//                            counts, durations and covered time are summed in LDS and added to
+//                            the global totals with 64-bit atomics (integer sums: the result
+//                            does not depend on their order).
+//   stats_finish_kernel      n and p per LLM from the totals, written with the error flags.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "alp_internal.h"
+
+namespace alp {
+
+namespace {
+
+constexpr uint64_t kPad = ~0ull;                       // sorts after every real key
+constexpr uint64_t kStartLimit = 1ull << 60;
+constexpr uint64_t kDurationLimit = 1ull << 32;
+constexpr uint32_t kThreads = 256;
+
+__global__ void stats_init_kernel(uint64_t *__restrict__ totals, uint32_t words)
+{
+    for (uint32_t k = threadIdx.x; k < words; k += blockDim.x)
+        totals[k] = 0;
+}
+
+// Exclusive maximum over the threads' values, in thread order (every thread gets the maximum
+// over the threads before it; 0 for thread 0).
+__device__ __forceinline__ uint64_t block_exclusive_max(uint64_t v)
+{
+    __shared__ uint64_t s_wave[kThreads / 64];
+    const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    uint64_t incl = v;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const uint64_t o = __shfl_up((unsigned long long)incl, off, 64);
+        if (lane >= (uint32_t)off)
+            incl = o > incl ? o : incl;
+    }
+    if (lane == 63)
+        s_wave[wave] = incl;
+    __syncthreads();
+    uint64_t excl = __shfl_up((unsigned long long)incl, 1, 64);
+    if (lane == 0)
+        excl = 0;
+    for (uint32_t w = 0; w < wave; ++w)
+        excl = s_wave[w] > excl ? s_wave[w] : excl;
+    return excl;
+}
+
+template <bool Global>
+__global__ void __launch_bounds__(kThreads)
+trace_stats_kernel(uint32_t M, const uint64_t *__restrict__ offsets,
+                   const uint32_t *__restrict__ llm, const uint64_t *__restrict__ start,
+                   const uint64_t *__restrict__ end, uint32_t lds_cap,
+                   const uint32_t *__restrict__ long_traces, const uint64_t *__restrict__ long_base,
+                   uint64_t *__restrict__ scratch, unsigned long long *__restrict__ totals,
+                   uint32_t *__restrict__ flags)
+{
+    extern __shared__ __align__(8) unsigned char s_dyn[];
+    __shared__ unsigned long long s_sum[3 * ALP_MAX_LLMS];   // per LLM: calls, busy, active
+    const uint32_t r = Global ? long_traces[blockIdx.x] : blockIdx.x;
+    const uint64_t lo = offsets[r], n = offsets[r + 1] - lo;
+    if (!Global && n > lds_cap)
+        return;                                        // long trace: the global pass takes it
+    uint32_t P = kThreads;                              // padded length: a power of two
+    while (P < n)
+        P <<= 1;
+    uint64_t *key = Global ? scratch + 2 * long_base[blockIdx.x]
+                           : reinterpret_cast<uint64_t *>(s_dyn);
+    uint64_t *val = key + P;
+    for (uint32_t k = threadIdx.x; k < 3 * ALP_MAX_LLMS; k += kThreads)
+        s_sum[k] = 0;
+    uint32_t bad = 0;
+    for (uint32_t i = threadIdx.x; i < P; i += kThreads) {
+        uint64_t kk = kPad, vv = 0;
+        if (i < n) {
+            const uint32_t m = llm[lo + i];
+            const uint64_t s = start[lo + i], e = end[lo + i];
+            if (m >= M)
+                bad |= 1u;
+            else if (e < s)
+                bad |= 2u;
+            else if (s >= kStartLimit || e - s >= kDurationLimit)
+                bad |= 4u;
+            else {
+                kk = ((uint64_t)m << 60) | s;
+                vv = e;
+            }
+        }
+        key[i] = kk;
+        val[i] = vv;
+    }
+    if (bad)
+        atomicOr(flags, bad);
+    __syncthreads();
+    // Bitonic sort of (key, val) pairs, ascending by key then val: calls grouped by LLM, each
+    // group in order of start.
+    for (uint32_t size = 2; size <= P; size <<= 1) {
+        for (uint32_t stride = size >> 1; stride > 0; stride >>= 1) {
+            for (uint32_t t = threadIdx.x; t < P / 2; t += kThreads) {
+                const uint32_t i = 2 * t - (t & (stride - 1));
+                const uint32_t j = i + stride;
+                const bool up = (i & size) == 0;
+                const uint64_t ki = key[i], kj = key[j], vi = val[i], vj = val[j];
+                const bool greater = ki > kj || (ki == kj && vi > vj);
+                if (greater == up) {
+                    key[i] = kj;
+                    key[j] = ki;
+                    val[i] = vj;
+                    val[j] = vi;
+                }
+            }
+            __syncthreads();
+        }
+    }
+    // Each thread takes a contiguous chunk.  Packed value of a call: (llm << 61 | end); the
+    // maximum of the packed values before a call has high bits equal to its LLM iff an earlier
+    // call of the same LLM exists, and then low bits equal to the furthest end among them.
+    const uint32_t per = P / kThreads, base = threadIdx.x * per;
+    uint64_t run = 0;
+    for (uint32_t k = 0; k < per; ++k) {
+        const uint64_t kk = key[base + k];
+        if (kk != kPad) {
+            const uint64_t pk = ((kk >> 60) << 61) | val[base + k];
+            run = pk > run ? pk : run;
+        }
+    }
+    uint64_t prev = block_exclusive_max(run);
+    constexpr uint64_t kLow61 = (1ull << 61) - 1;
+    uint32_t cur = ~0u;
+    uint64_t c_calls = 0, c_busy = 0, c_active = 0;
+    auto flush = [&]() {
+        if (cur != ~0u) {
+            atomicAdd(&s_sum[3 * cur + 0], (unsigned long long)c_calls);
+            atomicAdd(&s_sum[3 * cur + 1], (unsigned long long)c_busy);
+            atomicAdd(&s_sum[3 * cur + 2], (unsigned long long)c_active);
+        }
+        c_calls = c_busy = c_active = 0;
+    };
+    for (uint32_t k = 0; k < per; ++k) {
+        const uint64_t kk = key[base + k];
+        if (kk == kPad)
+            break;                                     // padding sorts last
+        const uint32_t m = (uint32_t)(kk >> 60);
+        const uint64_t s = kk & (kStartLimit - 1), e = val[base + k];
+        if (m != cur) {
+            flush();
+            cur = m;
+        }
+        uint64_t from = s;
+        if ((prev >> 61) == m) {
+            const uint64_t reach = prev & kLow61;
+            from = reach > s ? reach : s;
+        }
+        c_calls += 1;
+        c_busy += e - s;
+        c_active += e > from ? e - from : 0;
+        const uint64_t pk = ((uint64_t)m << 61) | e;
+        prev = pk > prev ? pk : prev;
+    }
+    flush();
+    __syncthreads();
+    for (uint32_t k = threadIdx.x; k < 3 * M; k += kThreads)
+        if (s_sum[k])
+            atomicAdd(&totals[k], s_sum[k]);
+}
+
+// n and p per LLM from the totals (calls, busy, active per LLM), R traces.  Status bits in
+// flags: 1 llm out of range, 2 end before start, 4 start or duration out of range, 8 a result
+// beyond 2^31 - 1 (it could not be loaded as an ALP input).
+__global__ void stats_finish_kernel(uint32_t M, uint32_t R,
+                                    const unsigned long long *__restrict__ totals,
+                                    uint32_t *__restrict__ flags, alp_stats_t *__restrict__ out)
+{
+    const uint32_t m = threadIdx.x;
+    if (m >= M)
+        return;
+    const uint64_t calls = totals[3 * m], busy = totals[3 * m + 1], active = totals[3 * m + 2];
+    uint64_t n = calls * 1000u / R, p;
+    if (calls == 0)
+        p = 0;
+    else if (active == 0)
+        p = 1000;
+    else if (busy >= (1ull << 53))
+        p = ~0ull;
+    else
+        p = busy * 1000u / active;
+    if (n >= (1u << 31) || p >= (1u << 31)) {
+        atomicOr(flags, 8u);
+        n = n >= (1u << 31) ? 0 : n;
+        p = p >= (1u << 31) ? 0 : p;
+    }
+    alp_stats_t st;
+    st.n_milli = (uint32_t)n;
+    st.p_milli = (uint32_t)p;
+    st.calls = calls;
+    st.busy_us = busy;
+    st.active_us = active;
+    out[m] = st;
+}
+
+}  // namespace
+
+hipError_t launch_trace_stats(uint32_t M, uint32_t R, const uint64_t *offsets, const uint32_t *llm,
+                              const uint64_t *start, const uint64_t *end, uint32_t lds_cap,
+                              uint32_t num_long, const uint32_t *long_traces,
+                              const uint64_t *long_base, uint64_t *scratch, uint64_t *totals,
+                              uint32_t *flags, alp_stats_t *out, hipStream_t st)
+{
+    hipLaunchKernelGGL(stats_init_kernel, dim3(1), dim3(64), 0, st, totals, 3 * ALP_MAX_LLMS + 1);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess)
+        return e;
+    unsigned long long *tot = reinterpret_cast<unsigned long long *>(totals);
+    const size_t lds = (size_t)2 * lds_cap * sizeof(uint64_t);
+    hipLaunchKernelGGL(trace_stats_kernel<false>, dim3(R), dim3(kThreads), lds, st, M, offsets,
+                       llm, start, end, lds_cap, long_traces, long_base, scratch, tot, flags);
+    if ((e = hipGetLastError()) != hipSuccess)
+        return e;
+    if (num_long) {
+        hipLaunchKernelGGL(trace_stats_kernel<true>, dim3(num_long), dim3(kThreads), 0, st, M,
+                           offsets, llm, start, end, lds_cap, long_traces, long_base, scratch,
+                           tot, flags);
+        if ((e = hipGetLastError()) != hipSuccess)
+            return e;
+    }
+    hipLaunchKernelGGL(stats_finish_kernel, dim3(1), dim3(64), 0, st, M, R, tot, flags, out);
+    return hipGetLastError();
+}
+
+}  // namespace alp

@@ -1,0 +1,106 @@
+"""Parity of the HIP workflow statistics (Section 4, step 2) with the oracle, through the C ABI.
+Needs an MI355X.  Every field of every LLM's record must be identical: n_m, p_m, call counts,
+summed durations and covered time."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import oracle
+from workloads.traces import make_traces
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2604_15186_amd import alp
+    with alp.StatsContext(0) as c:
+        yield c
+
+
+def _pack(traces):
+    offsets = [0]
+    llm, s, e = [], [], []
+    for tr in traces:
+        for m, a, b in tr:
+            llm.append(m), s.append(a), e.append(b)
+        offsets.append(len(llm))
+    return (np.asarray(offsets, np.uint64), np.asarray(llm, np.uint32), np.asarray(s, np.uint64),
+            np.asarray(e, np.uint64))
+
+
+def _same(ctx, M, offsets, llm, start, end):
+    got = ctx.compute(M, offsets, llm, start, end)
+    want = oracle.trace_stats(M, offsets, llm, start, end)
+    for f in want.dtype.names:
+        assert [int(v) for v in got[f]] == [int(v) for v in want[f]], f
+    return got
+
+
+@pytest.mark.parametrize("shape,R", [("beam", 300), ("rag", 2000), ("beam", 3000)])
+def test_synthetic_traces(ctx, shape, R):
+    tr = make_traces(shape, R, 11)
+    print(f"{shape} R={R} calls={len(tr['llm'])}", flush=True)
+    _same(ctx, tr["M"], tr["offsets"], tr["llm"], tr["start"], tr["end"])
+
+
+def test_long_traces_mixed_with_short(ctx):
+    rng = np.random.default_rng(5)
+    traces = []
+    for n in (3, 2048, 2049, 5000, 0, 20000, 700, 4096, 4097):
+        tr = []
+        for _ in range(n):
+            a = int(rng.integers(0, 1 << 22))
+            tr.append((int(rng.integers(0, 4)), a, a + int(rng.integers(0, 50_000))))
+        traces.append(tr)
+    _same(ctx, 4, *_pack(traces))
+
+
+def test_edge_cases(ctx):
+    # empty traces, zero-length calls, identical calls, unused LLMs, a single call
+    traces = [[], [(0, 5, 5), (0, 7, 7)], [(3, 0, 10)] * 7, [], [(5, 1 << 59, (1 << 59) + 3)],
+              [(1, 0, (1 << 32) - 1)]]
+    got = _same(ctx, 8, *_pack(traces))
+    assert int(got[2]["n_milli"]) == 0 and int(got[2]["p_milli"]) == 0
+    assert int(got[3]["p_milli"]) == 7000
+    _same(ctx, 1, *_pack([[]]))
+    _same(ctx, 1, *_pack([[(0, 0, 1)]]))
+
+
+def test_call_order_and_time_shift_do_not_matter(ctx):
+    tr = make_traces("beam", 200, 4)
+    base = _same(ctx, tr["M"], tr["offsets"], tr["llm"], tr["start"], tr["end"])
+    rng = np.random.default_rng(2)
+    off = tr["offsets"].astype(np.int64)
+    perm = np.concatenate([lo + rng.permutation(hi - lo) for lo, hi in zip(off[:-1], off[1:])])
+    shift = np.repeat(rng.integers(0, 1 << 30, len(off) - 1), np.diff(off)).astype(np.uint64)
+    got = ctx.compute(tr["M"], tr["offsets"], tr["llm"][perm], tr["start"][perm] + shift[perm],
+                      tr["end"][perm] + shift[perm])
+    assert (got == base).all()
+
+
+def test_malformed_input_is_rejected(ctx):
+    from paper_2604_15186_amd import alp
+    cases = [
+        (alp.ALP_EINVAL, 2, _pack([[(2, 0, 5)]])),                     # llm out of range
+        (alp.ALP_EINVAL, 2, _pack([[(0, 5, 4)]])),                     # ends before it starts
+        (alp.ALP_ERANGE, 2, _pack([[(0, 0, 1 << 32)]])),               # duration of 2^32 us
+        (alp.ALP_ERANGE, 2, _pack([[(0, 1 << 60, (1 << 60) + 1)]])),   # start beyond 2^60 us
+    ]
+    for status, M, arrays in cases:
+        with pytest.raises(alp.AlpError) as e:
+            ctx.compute(M, *arrays)
+        assert e.value.status == status
+    off, llm, s, e_ = _pack([[(0, 0, 5)], [(0, 1, 2)]])
+    for bad in (np.asarray([1, 1, 2], np.uint64), np.asarray([0, 2, 1], np.uint64)):
+        with pytest.raises(alp.AlpError) as e:
+            ctx.compute(1, bad, llm, s, e_)
+        assert e.value.status == alp.ALP_EINVAL
+    with pytest.raises(alp.AlpError):
+        ctx.compute(9, off, llm, s, e_)
+    # the context still works after rejected calls
+    _same(ctx, 1, off, llm, s, e_)
