@@ -22,6 +22,11 @@ one pruned search and ``value`` counts fraction vectors per second:
                     the exhaustive results on the same instances;
   ``pruned-paper``  the point of the paper's scheduler micro-benchmark: ``--llms`` LLMs,
                     ``--budget`` GPUs, ``--fractions`` fractions per GPU (default 5, 16, 10).
+
+``--workload stats`` times the workflow statistics (alp_trace_stats, Section 4 step 2) over
+20,000 synthetic beam-search traces (about 15 million LLM calls, resident on the device);
+``value`` counts trace calls per second and the roofline is HBM: 20 bytes read per call (LLM
+index and two timestamps) and 8 per trace offset.
 """
 from __future__ import annotations
 
@@ -41,7 +46,9 @@ from workloads import CONFIGS, make_batch, make_custom, target_from_tmax  # noqa
 PEAK_LANE_OPS = 256 * 64 * 2.4e9        # int32 VALU lane-ops/s of MI355X
 OPS_PER_CANDIDATE = 2                   # budget compare + objective min
 WORKLOADS = {"cfg2": 2, "cfg3": 3, "cfg4": 4, "cfg1": 1, "multi": 2, "pruned": 4,
-             "pruned-paper": None}
+             "pruned-paper": None, "stats": None}
+HBM_PEAK = 8.0e12                       # MI355X HBM3E bytes/s
+STATS_TRACES = 20_000                   # beam-search requests of the statistics workload
 # Several workflows sharing one GPU pool: four 4-LLM workflows drawn like the 4-LLM workload
 # split 32 GPUs under egalitarian welfare; each workflow's target is set at an even share.
 MULTI_WORKFLOWS, MULTI_GPUS = 4, 32
@@ -182,6 +189,8 @@ def main():
         sys.exit(1)
     if args.workload.startswith("pruned"):
         line = run_pruned(args, alp)
+    elif args.workload == "stats":
+        line = run_stats(args, alp)
     else:
         line = run_exhaustive(args, alp)
     if args.calib_copy_mib:
@@ -306,6 +315,72 @@ def run_pruned(args, alp):
     ctx.close()
     return _line(args, vectors * args.steps / elapsed, "fraction vectors/s", elapsed, config,
                  roofline, cpu)
+
+
+def cpu_baseline_stats(tr, seconds: float):
+    """Single-threaded oracle over the first traces, about `seconds` of work."""
+    import oracle
+    off = tr["offsets"]
+    R, done, t0 = len(off) - 1, 0, time.perf_counter()
+    step = 256
+    while done < R and time.perf_counter() - t0 < seconds:
+        hi = min(R, done + step)
+        lo_c, hi_c = int(off[done]), int(off[hi])
+        oracle.trace_stats(tr["M"], off[done:hi + 1] - off[done], tr["llm"][lo_c:hi_c],
+                           tr["start"][lo_c:hi_c], tr["end"][lo_c:hi_c])
+        done = hi
+    dt = time.perf_counter() - t0
+    calls = int(off[done])
+    return {"value": calls / dt, "unit": "trace calls/s", "cores": 1, "kind": "oracle",
+            "sample": f"the first {done} traces ({calls:,} calls), single-threaded C oracle "
+                      f"({dt:.1f} s)"}
+
+
+def run_stats(args, alp):
+    import torch
+    from workloads.traces import make_traces
+    tr = make_traces("beam", STATS_TRACES, 0)
+    calls = int(len(tr["llm"]))
+    dev = [torch.from_numpy(np.ascontiguousarray(tr[k]).view(t)).to("cuda:0")
+           for k, t in (("offsets", np.int64), ("llm", np.int32), ("start", np.int64),
+                        ("end", np.int64))]
+    torch.cuda.synchronize()
+    ctx = alp.StatsContext(0)
+
+    def step():
+        return ctx.compute(tr["M"], *dev)
+
+    import torch as _t
+    for _ in range(args.warmup):
+        step()
+    ctx.set_timing(True)
+    kernel_ms = []
+    _t.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        out = step()
+        kernel_ms.append(ctx.time_ms())
+    _t.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ctx.set_timing(False)
+    k_s = float(np.mean(kernel_ms)) / 1e3
+    alg_bytes = 20 * calls + 8 * (STATS_TRACES + 1)
+    achieved = alg_bytes / k_s
+    lengths = np.diff(tr["offsets"].astype(np.int64))
+    config = {"workload": f"workflow statistics (Section 4 step 2) of {STATS_TRACES} synthetic "
+                          f"beam-search traces: 2 LLMs, {calls:,} calls, 24-843 generator calls "
+                          "per request, 3 concurrent beams",
+              "traces": STATS_TRACES, "calls": calls, "longest_trace": int(lengths.max()),
+              "n_milli": [int(v) for v in out["n_milli"]],
+              "p_milli": [int(v) for v in out["p_milli"]]}
+    roofline = {"bound": "hbm", "achieved": achieved / 1e9, "peak": HBM_PEAK / 1e9,
+                "unit": "GB/s", "frac": achieved / HBM_PEAK, "traffic": None,
+                "kernel": "trace statistics (all kernels)", "kernel_ms": k_s * 1e3,
+                "bytes_per_call": 20}
+    cpu = None if args.no_cpu_baseline else cpu_baseline_stats(tr, args.cpu_seconds)
+    ctx.close()
+    return _line(args, calls * args.steps / elapsed, "trace calls/s", elapsed, config, roofline,
+                 cpu)
 
 
 if __name__ == "__main__":
