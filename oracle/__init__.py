@@ -53,6 +53,11 @@ class _Argmin(C.Structure):
                 ("sum_L", C.c_uint64)]
 
 
+class _Placement(C.Structure):
+    _fields_ = [("placed", C.c_uint32), ("replicas", C.c_uint32), ("gpus_used", C.c_uint32),
+                ("nodes_used", C.c_uint32), ("slot", C.c_uint16 * 128)]
+
+
 class _Pruned(C.Structure):
     _fields_ = [("best_x", C.c_uint64), ("best_L", C.c_uint64), ("vectors", C.c_uint64),
                 ("unpruned", C.c_uint64)]
@@ -92,6 +97,12 @@ def lib():
         L.orc_count_fractions.restype = C.c_uint64
         L.orc_binomial.argtypes = [C.c_uint64, C.c_uint64]
         L.orc_binomial.restype = C.c_uint64
+        L.orc_place.argtypes = [C.c_uint32, C.c_uint32, C.c_uint32, C.c_void_p, C.c_void_p,
+                                C.c_void_p, P(_Placement)]
+        L.orc_place_exact.argtypes = [C.c_uint32, C.c_uint32, C.c_uint32, C.c_void_p,
+                                      C.c_void_p, C.c_void_p]
+        L.orc_place.restype = C.c_int
+        L.orc_place_exact.restype = C.c_int
         L.orc_trace_stats.argtypes = [C.c_uint32, C.c_uint32, C.c_void_p, C.c_void_p, C.c_void_p,
                                       C.c_void_p, C.c_void_p, C.c_void_p]
         for f in (L.orc_option_term, L.orc_eval, L.orc_eval_many, L.orc_argmin, L.orc_tmax_brute,
@@ -276,3 +287,27 @@ def trace_stats(M: int, offsets, llm, start, end) -> np.ndarray:
                              end.ctypes.data, scratch.ctypes.data, out.ctypes.data) != 0:
         raise ValueError("malformed traces")
     return out
+
+
+def place(Q: int, G: int, tp, q, d) -> dict:
+    """The most-constrained-first placement of an allocation (see orc_place): placed flag,
+    replicas placed, GPUs and nodes used, and per replica (LLM-major) node << 8 | GPU mask
+    (0xFFFF if not placed)."""
+    M = len(tp)
+    a = [np.ascontiguousarray(v, dtype=np.uint32) for v in (tp, q, d)]
+    r = _Placement()
+    if lib().orc_place(Q, G, M, a[0].ctypes.data, a[1].ctypes.data, a[2].ctypes.data,
+                       C.byref(r)) != 0:
+        raise ValueError("bad allocation")
+    n = int(sum(int(v) for v in d))
+    return {"placed": bool(r.placed), "replicas": int(r.replicas), "gpus_used": int(r.gpus_used),
+            "nodes_used": int(r.nodes_used), "slot": [int(v) for v in r.slot[:n]]}
+
+
+def place_exact(Q: int, G: int, tp, q, d) -> bool:
+    """Whether any placement exists (backtracking; small cases)."""
+    a = [np.ascontiguousarray(v, dtype=np.uint32) for v in (tp, q, d)]
+    r = lib().orc_place_exact(Q, G, len(tp), a[0].ctypes.data, a[1].ctypes.data, a[2].ctypes.data)
+    if r < 0:
+        raise ValueError("bad allocation")
+    return bool(r)

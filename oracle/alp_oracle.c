@@ -630,3 +630,242 @@ int orc_trace_stats(uint32_t M, uint32_t R, const uint64_t *offsets, const uint3
     }
     return 0;
 }
+
+/* ---------------------------------------------------------------------------------------------
+ * Placement of an allocation on the GPUs of a budget (Section 6, hierarchical placement).  The
+ * G GPUs form nodes of 8 (the last node may hold fewer), every node one all-to-all xGMI domain,
+ * each GPU Q share units.  LLM m's allocation is d_m replicas of tp_m ranks of q_m units; the
+ * ranks of a replica sit on tp_m distinct GPUs of one node.
+ *
+ * The paper's most-constrained-first heuristic, read as follows.  Replicas are placed one by
+ * one: tensor-parallel replicas (tp > 1) before the others, larger replicas (tp * q units)
+ * first within each kind, ties by LLM index.  A tensor-parallel replica goes to tp GPUs of one
+ * node that each have q units free: in each node the GPUs with room are ordered by free units
+ * (then index), every run of tp consecutive ones is a candidate, scored by its imbalance (most
+ * minus least free units), then by the capacity of its domain (the node's free units; the
+ * least preferred, which keeps large domains for later), then by its own free units, then by
+ * node and position.  A single-GPU replica goes onto
+ * an already occupied GPU with room first, the one with the fewest free units (then the lowest
+ * index); failing that onto an empty GPU of the node with the fewest free units in total (then
+ * the lowest node), the lowest such GPU.  The allocation is placed if every replica finds room.
+ * ------------------------------------------------------------------------------------------- */
+
+#define ORC_NODE_GPUS 8u
+#define ORC_PLACE_MAX_GPUS 64u
+#define ORC_PLACE_MAX_REPLICAS 128u
+#define ORC_PLACE_NONE 0xFFFFu
+
+typedef struct {
+    uint32_t placed;          /* 1 if every replica was placed */
+    uint32_t replicas;        /* replicas placed */
+    uint32_t gpus_used, nodes_used;
+    uint16_t slot[ORC_PLACE_MAX_REPLICAS];  /* per replica (LLM-major): node << 8 | GPU mask */
+} orc_placement;
+
+static uint32_t orc_replica_order(uint32_t M, const uint32_t *tp, const uint32_t *q,
+                                  const uint32_t *d, uint32_t *order)
+{
+    uint32_t k = 0;
+    for (uint32_t m = 0; m < M; ++m)
+        if (d[m] > 0)
+            order[k++] = m;
+    for (uint32_t a = 1; a < k; ++a) {          /* insertion sort by (tp == 1, -tp*q, m) */
+        uint32_t v = order[a], b = a;
+        for (; b > 0; --b) {
+            uint32_t u = order[b - 1];
+            int u_tp1 = tp[u] == 1, v_tp1 = tp[v] == 1;
+            uint64_t us = (uint64_t)tp[u] * q[u], vs = (uint64_t)tp[v] * q[v];
+            int v_first = v_tp1 < u_tp1 || (v_tp1 == u_tp1 && (vs > us || (vs == us && v < u)));
+            if (!v_first)
+                break;
+            order[b] = u;
+        }
+        order[b] = v;
+    }
+    return k;
+}
+
+/* Places one replica; returns 0 and the slot, or -1 if there is no room. */
+static int orc_place_one(uint32_t Q, uint32_t G, uint32_t *free_u, uint32_t tp, uint32_t q,
+                         uint16_t *slot)
+{
+    uint32_t nodes = (G + ORC_NODE_GPUS - 1) / ORC_NODE_GPUS;
+    if (tp > 1) {
+        int found = 0;
+        uint32_t b_imb = 0, b_dom = 0, b_cap = 0, b_node = 0, b_mask = 0;
+        for (uint32_t n = 0; n < nodes; ++n) {
+            uint32_t E[ORC_NODE_GPUS], k = 0, dom = 0;
+            for (uint32_t g = n * ORC_NODE_GPUS; g < G && g < (n + 1) * ORC_NODE_GPUS; ++g) {
+                dom += free_u[g];
+                if (free_u[g] >= q)
+                    E[k++] = g;
+            }
+            for (uint32_t a = 1; a < k; ++a) {  /* by (free, index) */
+                uint32_t v = E[a], b = a;
+                while (b > 0 && (free_u[E[b - 1]] > free_u[v] ||
+                                 (free_u[E[b - 1]] == free_u[v] && E[b - 1] > v))) {
+                    E[b] = E[b - 1];
+                    --b;
+                }
+                E[b] = v;
+            }
+            for (uint32_t i = 0; i + tp <= k; ++i) {
+                uint32_t imb = free_u[E[i + tp - 1]] - free_u[E[i]], cap = 0, mask = 0;
+                for (uint32_t j = i; j < i + tp; ++j) {
+                    cap += free_u[E[j]];
+                    mask |= 1u << (E[j] - n * ORC_NODE_GPUS);
+                }
+                if (!found || imb < b_imb || (imb == b_imb && dom < b_dom) ||
+                    (imb == b_imb && dom == b_dom && cap < b_cap)) {
+                    found = 1;
+                    b_imb = imb;
+                    b_dom = dom;
+                    b_cap = cap;
+                    b_node = n;
+                    b_mask = mask;
+                }
+            }
+        }
+        if (!found)
+            return -1;
+        for (uint32_t j = 0; j < ORC_NODE_GPUS; ++j)
+            if (b_mask & (1u << j))
+                free_u[b_node * ORC_NODE_GPUS + j] -= q;
+        *slot = (uint16_t)(b_node << 8 | b_mask);
+        return 0;
+    }
+    /* a single GPU: an occupied one with room (fewest free units), else an empty one */
+    uint32_t best = G;
+    for (uint32_t g = 0; g < G; ++g)
+        if (free_u[g] < Q && free_u[g] >= q && (best == G || free_u[g] < free_u[best]))
+            best = g;
+    if (best == G) {
+        uint64_t best_node_free = 0;
+        for (uint32_t n = 0; n < nodes; ++n) {
+            uint32_t empty = G;
+            uint64_t node_free = 0;
+            for (uint32_t g = n * ORC_NODE_GPUS; g < G && g < (n + 1) * ORC_NODE_GPUS; ++g) {
+                node_free += free_u[g];
+                if (free_u[g] == Q && q <= Q && empty == G)
+                    empty = g;
+            }
+            if (empty != G && (best == G || node_free < best_node_free)) {
+                best = empty;
+                best_node_free = node_free;
+            }
+        }
+    }
+    if (best == G)
+        return -1;
+    free_u[best] -= q;
+    *slot = (uint16_t)((best / ORC_NODE_GPUS) << 8 | 1u << (best % ORC_NODE_GPUS));
+    return 0;
+}
+
+/* The heuristic.  tp, q, d per LLM (d = 0: the LLM has no replica).  Returns 0, or -1 for bad
+ * arguments (G above 64, more than 128 replicas, tp above 8, q outside 1..Q). */
+int orc_place(uint32_t Q, uint32_t G, uint32_t M, const uint32_t *tp, const uint32_t *q,
+              const uint32_t *d, orc_placement *out)
+{
+    uint32_t free_u[ORC_PLACE_MAX_GPUS], order[16], total = 0;
+    if (G > ORC_PLACE_MAX_GPUS || M == 0 || M > 16 || Q == 0)
+        return -1;
+    for (uint32_t m = 0; m < M; ++m) {
+        if (d[m] && (tp[m] == 0 || tp[m] > ORC_NODE_GPUS || q[m] == 0 || q[m] > Q))
+            return -1;
+        total += d[m];
+    }
+    if (total > ORC_PLACE_MAX_REPLICAS)
+        return -1;
+    for (uint32_t g = 0; g < G; ++g)
+        free_u[g] = Q;
+    for (uint32_t i = 0; i < ORC_PLACE_MAX_REPLICAS; ++i)
+        out->slot[i] = ORC_PLACE_NONE;
+    uint32_t first[16], acc = 0;                 /* slot index of each LLM's first replica */
+    for (uint32_t m = 0; m < M; ++m) {
+        first[m] = acc;
+        acc += d[m];
+    }
+    uint32_t k = orc_replica_order(M, tp, q, d, order);
+    out->placed = 1;
+    out->replicas = 0;
+    for (uint32_t a = 0; a < k && out->placed; ++a) {
+        uint32_t m = order[a];
+        for (uint32_t r = 0; r < d[m]; ++r) {
+            if (orc_place_one(Q, G, free_u, tp[m], q[m], &out->slot[first[m] + r]) != 0) {
+                out->placed = 0;
+                break;
+            }
+            out->replicas += 1;
+        }
+    }
+    out->gpus_used = out->nodes_used = 0;
+    for (uint32_t n = 0; n * ORC_NODE_GPUS < G; ++n) {
+        uint32_t used = 0;
+        for (uint32_t g = n * ORC_NODE_GPUS; g < G && g < (n + 1) * ORC_NODE_GPUS; ++g)
+            used += free_u[g] < Q;
+        out->gpus_used += used;
+        out->nodes_used += used > 0;
+    }
+    return 0;
+}
+
+/* Exact feasibility by backtracking (small cases only): every replica tries every node and
+ * every set of tp GPUs with room.  Returns 1 if some placement exists, 0 if none, -1 for bad
+ * arguments. */
+static int orc_place_rec(uint32_t Q, uint32_t G, uint32_t *free_u, uint32_t n_rep,
+                         const uint32_t *rtp, const uint32_t *rq, uint32_t i, uint32_t from)
+{
+    if (i == n_rep)
+        return 1;
+    uint32_t nodes = (G + ORC_NODE_GPUS - 1) / ORC_NODE_GPUS;
+    /* choices are numbered node * 256 + mask; replicas of the same kind are interchangeable,
+     * so a replica identical to the previous one takes a choice no smaller than its choice */
+    for (uint32_t n = 0; n < nodes; ++n) {
+        uint32_t lo = n * ORC_NODE_GPUS, hi = lo + ORC_NODE_GPUS < G ? lo + ORC_NODE_GPUS : G;
+        for (uint32_t mask = 1; mask < (1u << (hi - lo)); ++mask) {
+            uint32_t choice = n * 256 + mask;
+            if (choice < from || (uint32_t)__builtin_popcount(mask) != rtp[i])
+                continue;
+            int ok = 1;
+            for (uint32_t j = 0; j < hi - lo && ok; ++j)
+                if ((mask >> j & 1u) && free_u[lo + j] < rq[i])
+                    ok = 0;
+            if (!ok)
+                continue;
+            for (uint32_t j = 0; j < hi - lo; ++j)
+                if (mask >> j & 1u)
+                    free_u[lo + j] -= rq[i];
+            uint32_t next_from = 0;
+            if (i + 1 < n_rep && rtp[i + 1] == rtp[i] && rq[i + 1] == rq[i])
+                next_from = choice;
+            int r = orc_place_rec(Q, G, free_u, n_rep, rtp, rq, i + 1, next_from);
+            for (uint32_t j = 0; j < hi - lo; ++j)
+                if (mask >> j & 1u)
+                    free_u[lo + j] += rq[i];
+            if (r)
+                return 1;
+        }
+    }
+    return 0;
+}
+
+int orc_place_exact(uint32_t Q, uint32_t G, uint32_t M, const uint32_t *tp, const uint32_t *q,
+                    const uint32_t *d)
+{
+    uint32_t free_u[ORC_PLACE_MAX_GPUS], rtp[ORC_PLACE_MAX_REPLICAS], rq[ORC_PLACE_MAX_REPLICAS];
+    uint32_t n = 0;
+    if (G > ORC_PLACE_MAX_GPUS || M == 0 || M > 16)
+        return -1;
+    for (uint32_t m = 0; m < M; ++m)
+        for (uint32_t r = 0; r < d[m]; ++r) {
+            if (n == ORC_PLACE_MAX_REPLICAS || tp[m] == 0 || tp[m] > ORC_NODE_GPUS || q[m] > Q)
+                return -1;
+            rtp[n] = tp[m];
+            rq[n] = q[m];
+            ++n;
+        }
+    for (uint32_t g = 0; g < G; ++g)
+        free_u[g] = Q;
+    return orc_place_rec(Q, G, free_u, n, rtp, rq, 0, 0);
+}
