@@ -257,6 +257,42 @@ int32_t alp_stats_time(alp_stats_ctx *ctx, float *ms);
 
 void alp_stats_free(alp_stats_ctx *ctx);
 
+/* ---- Placement of allocations on GPU nodes (Section 6, hierarchical placement) -------------
+ * The search counts GPU share units only (sum tp * q * d <= Q * G); whether the allocation can
+ * be laid out on real GPUs is a packing question.  alp_place answers it with the paper's
+ * most-constrained-first heuristic.  The G GPUs of a budget form nodes of ALP_NODE_GPUS (the last
+ * may hold fewer), every node one all-to-all xGMI domain; each GPU holds Q units.  LLM m needs
+ * d_m replicas of tp_m ranks of q_m units, the ranks of a replica on distinct GPUs of one node.
+ * Replicas are placed tensor-parallel first, larger (tp * q) first, ties by LLM index.  A
+ * tensor-parallel replica takes, in some node, tp GPUs with room: among the node's GPUs with
+ * room ordered by (free units, index), a run of tp consecutive ones scored by imbalance (most
+ * minus least free units), then the node's free units (the smaller domain first, keeping large
+ * domains for larger models), then the run's free units, then node and position.  A single-GPU
+ * replica packs onto an occupied GPU with room (fewest free units, then lowest index), else onto
+ * the lowest empty GPU of the node with the fewest free units. */
+#define ALP_NODE_GPUS 8u
+#define ALP_PLACE_MAX_GPUS 64u
+#define ALP_PLACE_MAX_REPLICAS 128u
+#define ALP_PLACE_NONE 0xFFFFu
+
+/* One placement (272 bytes). */
+typedef struct {
+    uint32_t status;          /* ALP_OK: every replica placed; ALP_INFEASIBLE: one found no room,
+                                 or the allocation itself was infeasible */
+    uint32_t replicas;        /* replicas placed */
+    uint32_t gpus_used;       /* GPUs holding at least one rank */
+    uint32_t nodes_used;
+    uint16_t slot[ALP_PLACE_MAX_REPLICAS];  /* per replica, LLM 0's first: node << 8 | mask of
+                                               the node's GPUs; ALP_PLACE_NONE if not placed */
+} alp_placement_t;
+
+/* Places count allocations (search results of this context's space: tp, frac_units, replicas
+ * per LLM; an ALP_INFEASIBLE result places nothing) on gpu_budget[i] <= ALP_PLACE_MAX_GPUS GPUs
+ * each, one thread per allocation.  Host arrays; synchronous on the context's stream.  EINVAL for
+ * a budget above the maximum or a record whose choices are not of the space. */
+int32_t alp_place(alp_ctx *ctx, uint32_t count, const alp_result_t *allocations,
+                  const uint32_t *gpu_budget, alp_placement_t *out);
+
 /* Evaluates count given candidate indices (each < O^M, else EINVAL) of one instance. */
 int32_t alp_eval_candidates(alp_ctx *ctx, uint32_t instance, uint32_t gpu_budget,
                             uint32_t target_milli, const uint64_t *indices, uint64_t count,

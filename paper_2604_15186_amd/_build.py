@@ -8,7 +8,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libalp.so")
-SOURCES = ["alp_api.hip", "alp_kernels.hip", "alp_split.hip", "alp_pruned.hip", "alp_stats.hip"]
+SOURCES = ["alp_api.hip", "alp_kernels.hip", "alp_split.hip", "alp_pruned.hip", "alp_stats.hip", "alp_place.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

@@ -22,7 +22,8 @@ MAX_LLMS = 8
 # Symbols declared in include/alp.h.
 EXPORTS = ("alp_load_profiles", "alp_search", "alp_search_batch", "alp_max_throughput",
            "alp_allocate_workflows", "alp_search_pruned", "alp_stats_create", "alp_trace_stats",
-           "alp_stats_set_timing", "alp_stats_time", "alp_stats_free", "alp_eval_candidates",
+           "alp_stats_set_timing", "alp_stats_time", "alp_stats_free", "alp_place",
+           "alp_eval_candidates",
            "alp_set_launch", "alp_set_timing", "alp_kernel_times", "alp_num_candidates", "alp_free",
            "alp_status_str", "alp_last_error")
 
@@ -54,6 +55,11 @@ assert PRUNED_DTYPE.itemsize == 64
 STATS_DTYPE = np.dtype([("n_milli", np.uint32), ("p_milli", np.uint32), ("calls", np.uint64),
                         ("busy_us", np.uint64), ("active_us", np.uint64)])
 assert STATS_DTYPE.itemsize == 32
+PLACEMENT_DTYPE = np.dtype([("status", np.uint32), ("replicas", np.uint32),
+                            ("gpus_used", np.uint32), ("nodes_used", np.uint32),
+                            ("slot", np.uint16, 128)])
+assert PLACEMENT_DTYPE.itemsize == 272
+PLACE_NONE = 0xFFFF
 WELFARE_EGALITARIAN, WELFARE_SOCIAL = 0, 1
 PRUNE_ORDER, PRUNE_MIN_FRACTION = 1, 2
 
@@ -76,6 +82,7 @@ def lib():
         L.alp_eval_candidates.argtypes = [vp, u32, u32, u32, vp, u64, vp]
         L.alp_allocate_workflows.argtypes = [vp, u32, vp, vp, u32, u32, vp, vp, vp]
         L.alp_search_pruned.argtypes = [vp, u32, vp, vp, vp, u32, vp]
+        L.alp_place.argtypes = [vp, u32, vp, vp, vp]
         L.alp_stats_create.argtypes = [C.POINTER(vp), i32, vp]
         L.alp_trace_stats.argtypes = [vp, u32, u32, vp, vp, vp, vp, vp]
         L.alp_stats_set_timing.argtypes = [vp, i32]
@@ -88,7 +95,7 @@ def lib():
         L.alp_num_candidates.argtypes = [vp, C.POINTER(u64)]
         for name in ("alp_load_profiles", "alp_search", "alp_search_batch", "alp_max_throughput",
                      "alp_allocate_workflows", "alp_search_pruned", "alp_stats_create",
-                     "alp_trace_stats", "alp_stats_set_timing", "alp_stats_time",
+                     "alp_trace_stats", "alp_stats_set_timing", "alp_stats_time", "alp_place",
                      "alp_eval_candidates", "alp_set_launch", "alp_set_timing",
                      "alp_kernel_times", "alp_num_candidates"):
             getattr(L, name).restype = i32
@@ -240,6 +247,15 @@ class Context:
         out = np.zeros(len(G), dtype=PRUNED_DTYPE)
         _check(lib().alp_search_pruned(self._ctx, len(G), None if inst is None else _ptr(inst),
                                        _ptr(G), _ptr(lam), flags, _ptr(out)))
+        return out
+
+    def place(self, allocations, gpu_budget) -> np.ndarray:
+        """Places search results (RESULT_DTYPE records) on their GPU budgets (alp_place)."""
+        res = np.ascontiguousarray(allocations, dtype=RESULT_DTYPE)
+        G = np.ascontiguousarray(gpu_budget, dtype=np.uint32)
+        assert len(G) == len(res)
+        out = np.zeros(len(res), dtype=PLACEMENT_DTYPE)
+        _check(lib().alp_place(self._ctx, len(res), _ptr(res), _ptr(G), _ptr(out)))
         return out
 
     def eval_candidates(self, instance: int, gpu_budget: int, target_milli: int, indices) -> np.ndarray:

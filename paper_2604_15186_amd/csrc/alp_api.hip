@@ -103,6 +103,7 @@ struct alp_ctx {
     DevBuf q_inst, rec, ext, inner, done, winners, idx, evals, tmax;   // q_inst: inst | cap | lambda
     DevBuf split_dp;                        // allocate_kernel's knapsack table
     DevBuf pruned_table, pruned_orders, pruned_counts;   // pruned search scratch
+    DevBuf place_in, place_out;                          // placement records
     alp_pruned_t *host_pruned = nullptr;    // mapped pinned results of pruned searches
     alp_pruned_t *host_pruned_dev = nullptr;
     size_t host_pruned_cap = 0;
@@ -862,6 +863,75 @@ int32_t alp_search_pruned(alp_ctx *ctx, uint32_t count, const uint32_t *instance
     return ALP_OK;
 }
 
+int32_t alp_place(alp_ctx *ctx, uint32_t count, const alp_result_t *allocations,
+                  const uint32_t *gpu_budget, alp_placement_t *out)
+{
+    if (!ctx)
+        return fail(ALP_EINVAL, "ctx is NULL");
+    if (count == 0)
+        return ALP_OK;
+    if (!allocations || !gpu_budget || !out)
+        return fail(ALP_EINVAL, "allocations, gpu_budget or out is NULL");
+    const alp_space_t &sp = ctx->space;
+    std::vector<alp::PlaceIn> in(count);
+    for (uint32_t i = 0; i < count; ++i) {
+        const alp_result_t &r = allocations[i];
+        alp::PlaceIn &p = in[i];
+        memset(&p, 0, sizeof(p));
+        if (gpu_budget[i] > ALP_PLACE_MAX_GPUS)
+            return fail(ALP_EINVAL, "allocation %u: %u GPUs, at most %u", i, gpu_budget[i],
+                        ALP_PLACE_MAX_GPUS);
+        p.gpus = (uint8_t)gpu_budget[i];
+        p.llms = (uint8_t)sp.num_llms;
+        p.feasible = r.status == ALP_OK;
+        if (!p.feasible)
+            continue;
+        for (uint32_t m = 0; m < sp.num_llms; ++m) {
+            bool tp_ok = false, q_ok = false;
+            for (uint32_t j = 0; j < sp.num_tp; ++j)
+                tp_ok |= r.tp[m] == sp.tp_values[j];
+            for (uint32_t j = 0; j < sp.num_frac; ++j)
+                q_ok |= r.frac_units[m] == sp.frac_units[j];
+            if (!tp_ok || !q_ok || r.tp[m] > ALP_NODE_GPUS || r.replicas[m] < 1 ||
+                r.replicas[m] > sp.max_replicas)
+                return fail(ALP_EINVAL, "allocation %u: LLM %u's choice is not of the space", i, m);
+            p.tp[m] = r.tp[m];
+            p.q[m] = r.frac_units[m];
+            p.d[m] = r.replicas[m];
+        }
+    }
+    DeviceGuard guard(ctx->device);
+    if (guard.status != hipSuccess)
+        return hip_fail(guard.status, "hipSetDevice");
+    hipError_t e;
+    if ((e = ctx->place_in.ensure(count * sizeof(alp::PlaceIn))) != hipSuccess ||
+        (e = ctx->place_out.ensure(count * sizeof(alp_placement_t))) != hipSuccess)
+        return hip_fail(e, "hipMalloc(placement)");
+    if (ctx->timing && (e = hipEventRecord(ctx->ev[0], ctx->stream)) != hipSuccess)
+        return hip_fail(e, "hipEventRecord");
+    if ((e = hipMemcpyAsync(ctx->place_in.ptr, in.data(), count * sizeof(alp::PlaceIn),
+                            hipMemcpyHostToDevice, ctx->stream)) != hipSuccess)
+        return hip_fail(e, "copy allocations");
+    if (ctx->timing && (e = hipEventRecord(ctx->ev[1], ctx->stream)) != hipSuccess)
+        return hip_fail(e, "hipEventRecord");
+    if ((e = alp::launch_place(sp.units_per_gpu, count, (const alp::PlaceIn *)ctx->place_in.ptr,
+                               (alp_placement_t *)ctx->place_out.ptr, ctx->stream)) != hipSuccess)
+        return hip_fail(e, "placement launch");
+    if (ctx->timing && (e = hipEventRecord(ctx->ev[2], ctx->stream)) != hipSuccess)
+        return hip_fail(e, "hipEventRecord");
+    if ((e = hipMemcpyAsync(out, ctx->place_out.ptr, count * sizeof(alp_placement_t),
+                            hipMemcpyDeviceToHost, ctx->stream)) != hipSuccess ||
+        (e = hipStreamSynchronize(ctx->stream)) != hipSuccess)
+        return hip_fail(e, "placement");
+    if (ctx->timing) {
+        // ms[1]: the placement kernel
+        if ((e = hipEventElapsedTime(&ctx->last_ms[1], ctx->ev[1], ctx->ev[2])) != hipSuccess)
+            return hip_fail(e, "hipEventElapsedTime");
+        ctx->last_ms[0] = ctx->last_ms[2] = 0.0f;
+    }
+    return ALP_OK;
+}
+
 int32_t alp_eval_candidates(alp_ctx *ctx, uint32_t instance, uint32_t gpu_budget,
                             uint32_t target_milli, const uint64_t *indices, uint64_t count,
                             alp_eval_t *out)
@@ -967,7 +1037,8 @@ void alp_free(alp_ctx *ctx)
             (void)hipEventDestroy(ctx->ev[k]);
     DevBuf *bufs[] = {&ctx->tables, &ctx->q_inst, &ctx->rec, &ctx->ext, &ctx->inner, &ctx->done,
                       &ctx->winners, &ctx->idx, &ctx->evals, &ctx->tmax, &ctx->split_dp,
-                      &ctx->pruned_table, &ctx->pruned_orders, &ctx->pruned_counts};
+                      &ctx->pruned_table, &ctx->pruned_orders, &ctx->pruned_counts,
+                      &ctx->place_in, &ctx->place_out};
     for (DevBuf *b : bufs)
         b->release();
     if (ctx->host_results)

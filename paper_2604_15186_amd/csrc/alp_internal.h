@@ -131,6 +131,19 @@ hipError_t launch_trace_stats(uint32_t M, uint32_t R, const uint64_t *offsets, c
                               const uint64_t *long_base, uint64_t *scratch, uint64_t *totals,
                               uint32_t *flags, alp_stats_t *out, hipStream_t st);
 
+// One allocation to place: budget, LLM count, whether the search found it, per-LLM choices.
+struct PlaceIn {
+    uint8_t gpus, llms, feasible, pad;
+    uint8_t tp[ALP_MAX_LLMS], q[ALP_MAX_LLMS], d[ALP_MAX_LLMS];
+};
+
+// Placement of count allocations (see alp_place); Q share units per GPU.
+hipError_t launch_place(uint32_t Q, uint32_t count, const PlaceIn *in, alp_placement_t *out,
+                        hipStream_t st);
+
+static_assert(sizeof(alp_placement_t) == 272 && offsetof(alp_placement_t, slot) == 16,
+              "alp_placement_t layout");
+
 // Resident blocks per CU of the scan kernels at a given block size (occupancy query).
 int scan_blocks_per_cu(uint32_t variant, uint32_t slots, uint32_t threads, const SpaceDev &sp);
 

@@ -43,8 +43,8 @@ def test_struct_layout_matches_header(tmp_path):
 #include <stddef.h>
 #include "alp.h"
 int main(void) {
-  printf("%zu %zu %zu %zu %zu %zu\n", sizeof(alp_space_t), sizeof(alp_result_t), sizeof(alp_eval_t),
-         sizeof(alp_plan_t), sizeof(alp_pruned_t), sizeof(alp_stats_t));
+  printf("%zu %zu %zu %zu %zu %zu %zu\n", sizeof(alp_space_t), sizeof(alp_result_t), sizeof(alp_eval_t),
+         sizeof(alp_plan_t), sizeof(alp_pruned_t), sizeof(alp_stats_t), sizeof(alp_placement_t));
   printf("%zu %zu %zu %zu\n", offsetof(alp_plan_t, max_latency_us), offsetof(alp_plan_t, sum_latency_us),
          offsetof(alp_pruned_t, fraction_vectors), offsetof(alp_pruned_t, unpruned_vectors));
   printf("%zu %zu %zu %zu %zu %zu %zu %zu\n", offsetof(alp_result_t, index),
@@ -61,7 +61,8 @@ int main(void) {
     lines = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split("\n")
     sizes = [int(v) for v in lines[0].split()]
     assert sizes == [C.sizeof(alp.Space), alp.RESULT_DTYPE.itemsize, alp.EVAL_DTYPE.itemsize,
-                     alp.PLAN_DTYPE.itemsize, alp.PRUNED_DTYPE.itemsize, alp.STATS_DTYPE.itemsize]
+                     alp.PLAN_DTYPE.itemsize, alp.PRUNED_DTYPE.itemsize, alp.STATS_DTYPE.itemsize,
+                     alp.PLACEMENT_DTYPE.itemsize]
     assert [int(v) for v in lines[1].split()] == [
         alp.PLAN_DTYPE.fields["max_latency_us"][1], alp.PLAN_DTYPE.fields["sum_latency_us"][1],
         alp.PRUNED_DTYPE.fields["vectors"][1], alp.PRUNED_DTYPE.fields["unpruned"][1]]
@@ -170,6 +171,7 @@ def test_null_arguments_rejected():
     assert lib.alp_search_pruned(None, 1, None, None, None, 3, None) == alp.ALP_EINVAL
     assert lib.alp_trace_stats(None, 2, 1, None, None, None, None, None) == alp.ALP_EINVAL
     assert lib.alp_stats_create(None, 0, None) == alp.ALP_EINVAL
+    assert lib.alp_place(None, 1, None, None, None) == alp.ALP_EINVAL
     lib.alp_stats_free(None)
     assert lib.alp_allocate_workflows(None, 1, None, None, 4, 0, None, None, None) == alp.ALP_EINVAL
     lib.alp_free(None)
