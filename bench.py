@@ -23,6 +23,11 @@ one pruned search and ``value`` counts fraction vectors per second:
   ``pruned-paper``  the point of the paper's scheduler micro-benchmark: ``--llms`` LLMs,
                     ``--budget`` GPUs, ``--fractions`` fractions per GPU (default 5, 16, 10).
 
+``--workload place`` times alp_place (Section 6 placement) on the exhaustive search results of
+a workload's instances (``--config``, default the 4,096-instance batch), and reports how many of
+the searched optima, and of the pruned search's results, can be placed on the budget's 8-GPU
+nodes.
+
 ``--workload stats`` times the workflow statistics (alp_trace_stats, Section 4 step 2) over
 20,000 synthetic beam-search traces (about 15 million LLM calls, resident on the device);
 ``value`` counts trace calls per second and the roofline is HBM: 20 bytes read per call (LLM
@@ -46,7 +51,7 @@ from workloads import CONFIGS, make_batch, make_custom, target_from_tmax  # noqa
 PEAK_LANE_OPS = 256 * 64 * 2.4e9        # int32 VALU lane-ops/s of MI355X
 OPS_PER_CANDIDATE = 2                   # budget compare + objective min
 WORKLOADS = {"cfg2": 2, "cfg3": 3, "cfg4": 4, "cfg1": 1, "multi": 2, "pruned": 4,
-             "pruned-paper": None, "stats": None}
+             "pruned-paper": None, "stats": None, "place": 4}
 HBM_PEAK = 8.0e12                       # MI355X HBM3E bytes/s
 STATS_TRACES = 20_000                   # beam-search requests of the statistics workload
 # Several workflows sharing one GPU pool: four 4-LLM workflows drawn like the 4-LLM workload
@@ -191,6 +196,8 @@ def main():
         line = run_pruned(args, alp)
     elif args.workload == "stats":
         line = run_stats(args, alp)
+    elif args.workload == "place":
+        line = run_place(args, alp)
     else:
         line = run_exhaustive(args, alp)
     if args.calib_copy_mib:
@@ -315,6 +322,65 @@ def run_pruned(args, alp):
     ctx.close()
     return _line(args, vectors * args.steps / elapsed, "fraction vectors/s", elapsed, config,
                  roofline, cpu)
+
+
+def _place_args(res, M):
+    return ([int(v) for v in res["tp"][:M]], [int(v) for v in res["frac_units"][:M]],
+            [int(v) for v in res["replicas"][:M]])
+
+
+def cpu_baseline_place(batch, res, G, seconds: float):
+    """Single-threaded oracle placement of the results, about `seconds` of work."""
+    import oracle
+    Q, M = int(batch["space"]["Q"]), int(batch["space"]["M"])
+    done, t0 = 0, time.perf_counter()
+    while done < len(res) and time.perf_counter() - t0 < seconds:
+        if int(res[done]["status"]) == 0:
+            oracle.place(Q, int(G[done]), *_place_args(res[done], M))
+        done += 1
+    dt = time.perf_counter() - t0
+    return {"value": done / dt, "unit": "allocations/s", "cores": 1, "kind": "oracle",
+            "sample": f"placement of the first {done} results, single-threaded C oracle "
+                      f"({dt:.2f} s, including the Python call per allocation)"}
+
+
+def run_place(args, alp):
+    cfg = CONFIGS[args.config]
+    batch = make_batch(args.config, range(cfg.num_instances))
+    ctx = alp.Context(batch)
+    G = np.asarray(batch["G"], dtype=np.uint32)
+    tmax = ctx.max_throughput(G)
+    lam = np.asarray([target_from_tmax(int(batch["u_ppm"][i]), int(tmax[i]))
+                      for i in range(len(G))], dtype=np.uint32)
+    res = ctx.search_batch(G, lam)
+    pruned = ctx.search_pruned(G, lam)["best"]
+
+    def step():
+        return ctx.place(res, G)
+
+    elapsed, times, out = timed_steps(step, ctx, args.steps, args.warmup)
+    k_s = float(np.mean([t[1] for t in times])) / 1e3
+    out_p = ctx.place(pruned, G)
+    replicas = int(res["replicas"].sum())
+    ops = int(sum(int(res[i]["replicas"].sum()) * int(G[i]) for i in range(len(G))))
+    feasible = res["status"] == 0
+    config = {"workload": f"placement (Section 6) of the exhaustive optima of {cfg.name}: "
+                          f"{len(G)} allocation(s) on {int(G[0])} GPUs in nodes of 8",
+              "allocations": int(len(G)), "replicas": replicas,
+              "optima_placed": int((out["status"] == 0).sum()),
+              "optima_feasible": int(feasible.sum()),
+              "pruned_placed": int((out_p["status"] == 0).sum()),
+              "pruned_feasible": int((pruned["status"] == 0).sum()),
+              "mean_gpus_used": float(out["gpus_used"][out["status"] == 0].mean())
+              if (out["status"] == 0).any() else 0.0}
+    roofline = {"bound": "alu", "achieved": ops / k_s / 1e12, "peak": PEAK_LANE_OPS / 1e12,
+                "unit": "TOP/s", "frac": ops / k_s / PEAK_LANE_OPS, "traffic": None,
+                "kernel": "place", "kernel_ms": k_s * 1e3,
+                "ops": "one pass over the budget's GPUs per replica"}
+    cpu = None if args.no_cpu_baseline else cpu_baseline_place(batch, res, G, args.cpu_seconds)
+    ctx.close()
+    return _line(args, len(G) * args.steps / elapsed, "allocations/s", elapsed, config, roofline,
+                 cpu)
 
 
 def cpu_baseline_stats(tr, seconds: float):
