@@ -89,7 +89,7 @@ def lib():
         L.alp_stats_time.argtypes = [vp, C.POINTER(C.c_float)]
         L.alp_stats_free.argtypes = [vp]
         L.alp_stats_free.restype = None
-        L.alp_set_launch.argtypes = [vp, u32, u32, u32]
+        L.alp_set_launch.argtypes = [vp, u32, u32, u32, u32]
         L.alp_set_timing.argtypes = [vp, i32]
         L.alp_kernel_times.argtypes = [vp, C.POINTER(C.c_float), C.POINTER(u32)]
         L.alp_num_candidates.argtypes = [vp, C.POINTER(u64)]
@@ -265,8 +265,10 @@ class Context:
                                          len(idx), _ptr(out)))
         return out
 
-    def set_launch(self, variant: int = 0, blocks_per_item: int = 0, threads_per_block: int = 0):
-        _check(lib().alp_set_launch(self._ctx, variant, blocks_per_item, threads_per_block))
+    def set_launch(self, variant: int = 0, blocks_per_item: int = 0, threads_per_block: int = 0,
+                   inner_chunks: int = 0):
+        _check(lib().alp_set_launch(self._ctx, variant, blocks_per_item, threads_per_block,
+                                    inner_chunks))
 
     def set_timing(self, enable: bool):
         _check(lib().alp_set_timing(self._ctx, 1 if enable else 0))

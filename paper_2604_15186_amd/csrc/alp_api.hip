@@ -115,7 +115,7 @@ struct alp_ctx {
     alp_result_t *host_results_dev = nullptr;  // its device-visible address
     size_t host_results_cap = 0;
 
-    uint32_t variant = 0, bpi_override = 0, tpb_override = 0;
+    uint32_t variant = 0, bpi_override = 0, tpb_override = 0, chunks_override = 0;
     int occupancy_cache[4][4][17] = {};   // [variant][log2 slots][threads / 64]: blocks per CU
     int timing = 0;
     hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
@@ -284,19 +284,46 @@ alp::ScanGeometry plan_scan(alp_ctx *c, uint32_t count)
         g.rows = 1;
         for (uint32_t m = 2; m < sp.M; ++m)
             g.rows *= sp.O;
+        // Variant 1 may split each row into chunks of the inner LLM's records (sub-rows): an
+        // override applies here; the automatic choice is made below, once the rows per wave are
+        // known.
+        g.chunks = 1;
+        const bool chunked = g.variant == 1 && sp.M >= 2;
+        const uint32_t n16 = alp::inner_stride(sp.O) / 16;      // chunks must divide this
+        if (chunked && c->chunks_override) {
+            g.chunks = c->chunks_override;
+            g.rows *= g.chunks;
+        }
         // Blocks of 8 waves (fewer blocks, fewer end-of-block reductions), at most one wave per
-        // row.  Each wave gets at least kMinRowsPerWave rows when the item has that many, so a
-        // wave's fixed costs (setup, end-of-wave re-scan, block reduction) stay small.
-        constexpr uint64_t kMinRowsPerWave = 8;
+        // row.  Each wave gets at least kMinRecordsPerWave of the inner LLM's records (rows
+        // times records per row) when the item has that many, so that a wave's fixed costs
+        // (setup, end-of-wave re-scan, block reduction) stay small.
+        constexpr uint64_t kMinRecordsPerWave = 512;
+        const uint64_t per_row = sp.M >= 2 ? alp::inner_stride(sp.O) / g.chunks : 1;
+        const uint64_t min_rows = std::max<uint64_t>(1, kMinRecordsPerWave / per_row);
         g.threads = c->tpb_override ? c->tpb_override
                                     : (uint32_t)(64 * (g.rows < 8 ? g.rows : 8));
         const uint32_t wpb = g.threads / 64;
-        const uint64_t max_waves = g.rows >= kMinRowsPerWave ? g.rows / kMinRowsPerWave : 1;
+        const uint64_t max_waves = g.rows >= min_rows ? g.rows / min_rows : 1;
         const uint64_t max_bpi = ceil_div(max_waves, wpb);
         uint64_t bpi = c->bpi_override;
         if (!bpi)
             bpi = blocks_per_item_for_rounds(
                 count, cus * (uint64_t)blocks_per_cu(c, g.variant, g.slots, g.threads), max_bpi);
+        // Few rows per wave: split the rows so that a wave keeps at least 16 sub-rows; its
+        // records stay the same, but the end-of-wave re-scan covers one sub-row only.
+        if (chunked && !c->chunks_override) {
+            const uint64_t rpw = ceil_div(g.rows, bpi * wpb);
+            if (rpw < 16) {
+                g.chunks = n16;
+                for (uint32_t k = 1; k <= n16; ++k)
+                    if (n16 % k == 0 && rpw * k >= 16) {
+                        g.chunks = k;
+                        break;
+                    }
+                g.rows *= g.chunks;
+            }
+        }
         g.rows_per_wave = ceil_div(g.rows, bpi * wpb);
         if (!c->bpi_override)
             bpi = ceil_div(g.rows, g.rows_per_wave * wpb);
@@ -982,7 +1009,7 @@ int32_t alp_eval_candidates(alp_ctx *ctx, uint32_t instance, uint32_t gpu_budget
 }
 
 int32_t alp_set_launch(alp_ctx *ctx, uint32_t variant, uint32_t blocks_per_item,
-                       uint32_t threads_per_block)
+                       uint32_t threads_per_block, uint32_t inner_chunks)
 {
     if (!ctx)
         return fail(ALP_EINVAL, "ctx is NULL");
@@ -992,9 +1019,13 @@ int32_t alp_set_launch(alp_ctx *ctx, uint32_t variant, uint32_t blocks_per_item,
         return fail(ALP_EINVAL, "threads_per_block must be a multiple of 64, at most 1024");
     if (blocks_per_item > (1u << 24))
         return fail(ALP_EINVAL, "blocks_per_item too large");
+    const uint32_t n16 = alp::inner_stride(ctx->sp.O) / 16;
+    if (inner_chunks && (inner_chunks > n16 || n16 % inner_chunks))
+        return fail(ALP_EINVAL, "inner_chunks %u does not divide %u", inner_chunks, n16);
     ctx->variant = variant;
     ctx->bpi_override = blocks_per_item;
     ctx->tpb_override = threads_per_block;
+    ctx->chunks_override = inner_chunks;
     return ALP_OK;
 }
 

@@ -75,8 +75,10 @@ struct ScanGeometry {
     uint32_t variant;          // 1: row-minimum, 2: thread-per-candidate, 3: exact-tracking lanes
     uint32_t threads;          // per block
     uint32_t blocks_per_item;
-    uint64_t rows;             // variants 1, 3: rows of O prefixes per item
+    uint64_t rows;             // variants 1, 3: rows of O prefixes per item (variant 1: sub-rows,
+                               // rows times chunks)
     uint64_t rows_per_wave;    // variants 1, 3
+    uint32_t chunks;           // variant 1: ranges of the inner LLM's records per row
     uint64_t per_thread;       // variant 2: candidates per thread
     uint32_t slots;            // variants 1, 3: options of the last LLM per lane (1, 2, 4, 8)
 };

@@ -234,13 +234,19 @@ __device__ __forceinline__ void outer_sums(const uint2 *R, uint32_t O, uint32_t 
 }
 
 // NOUT >= 0: the number of outer digits (M - 2) is fixed at compile time; NOUT < 0: any M.
-template <int S, int NOUT>
+template <int S, int NOUT, bool CHUNKED>
 __global__ void __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 8 : 1)))
 scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_all, QueryDev q,
-                uint32_t M, uint32_t O, uint64_t rows, uint64_t rows_per_wave,
+                uint32_t M, uint32_t O, uint64_t rows, uint64_t rows_per_wave, uint32_t chunks,
                 uint32_t blocks_per_item, uint32_t nblocks, Winner *__restrict__ winners,
                 FinishArgs fa)
 {
+    // `rows` counts sub-rows: with CHUNKED each row (one choice of the outer digits) is split
+    // into `chunks` consecutive ranges of the inner LLM's records, so that small spaces still
+    // give every wave enough sub-rows; candidates stay in index order (row, record, option).
+    // Without it (chunks = 1) the bookkeeping compiles away.
+    if (!CHUNKED)
+        chunks = 1;
     const uint32_t lb = xcd_logical_block(blockIdx.x, nblocks);
     const uint32_t item = lb / blocks_per_item;
     const uint32_t sub = lb - item * blocks_per_item;
@@ -286,6 +292,7 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
     }
     const bool has_inner = M >= 2;
     const uint32_t n_inner_padded = inner_stride(O);
+    const uint32_t chunk_len = n_inner_padded / chunks;   // a multiple of 16
     const uint2 *inner = inner_all + (uint64_t)item * n_inner_padded;
     const uint32_t n_inner = has_inner ? O : 1;
     constexpr int NMAX = NOUT >= 0 ? NOUT : (int)kMaxOuter;
@@ -306,8 +313,9 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
             bestR[s] = 0;
         }
         uint32_t digit[NMAX > 0 ? NMAX : 1];
+        uint32_t chunk = CHUNKED ? (uint32_t)(r_begin % chunks) : 0u;
         {
-            uint64_t rr = r_begin;
+            uint64_t rr = CHUNKED ? r_begin / chunks : r_begin;
 #pragma unroll
             for (int k = NMAX - 1; k >= 0; --k) {
                 digit[k] = 0;
@@ -339,8 +347,9 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
                 // 16 records per iteration (the table is padded to a multiple of 16 with
                 // records no lane can use): two 64-byte scalar loads issued together, so the
                 // loop's own scalar work stays small next to the 2 x 16 x S VALU operations.
-                const uint2 *const end = inner + n_inner_padded;
-                for (const uint2 *p = inner; p != end; p += 16) {
+                const uint2 *const begin = CHUNKED ? inner + chunk * chunk_len : inner;
+                const uint2 *const end = CHUNKED ? begin + chunk_len : inner + n_inner_padded;
+                for (const uint2 *p = begin; p != end; p += 16) {
                     uint2 v0[8], v1[8];
 #pragma unroll
                     for (int t = 0; t < 8; ++t) {
@@ -361,7 +370,13 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
                 bestL[s] = better ? L : bestL[s];
                 bestR[s] = better ? rr : bestR[s];
             }
-            // Next row: odometer on the outer digits, integer carry (stays in scalar registers).
+            // Next sub-row; after the last chunk, the odometer on the outer digits moves on
+            // (integer carry, stays in scalar registers).
+            if (CHUNKED) {
+                if (++chunk < chunks)
+                    continue;
+                chunk = 0;
+            }
             uint32_t inc = 1;
 #pragma unroll
             for (int k = NMAX - 1; k >= 0; --k) {
@@ -386,7 +401,8 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
                 if (bestL[s] == Lstar && bestR[s] < rmin)
                     rmin = bestR[s];
             const uint32_t rstar = wave_min_u32(rmin);
-            const uint64_t r = r_begin + rstar;
+            const uint64_t r = CHUNKED ? (r_begin + rstar) / chunks : r_begin + rstar;
+            const uint32_t j0 = CHUNKED ? (uint32_t)((r_begin + rstar) % chunks) * chunk_len : 0u;
             uint32_t oc;
             int32_t ou;
             outer_sums(R, O, n_outer, r, oc, ou);
@@ -404,7 +420,7 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
             if (has_inner) {
                 // 16 records per step (two scalar loads), stop once every lane-slot has its j;
                 // the padding records are never feasible, so they never match.
-                for (uint32_t jb = 0; jb < n_inner_padded; jb += 16) {
+                for (uint32_t jb = j0; jb < j0 + chunk_len; jb += 16) {
                     uint2 v[16];
 #pragma unroll
                     for (int t = 0; t < 16; ++t)
@@ -761,9 +777,17 @@ static hipError_t launch_lane(const SpaceDev &sp, const QueryDev &q, uint32_t co
     else {
         const uint32_t n_outer = sp.M >= 2 ? sp.M - 2 : 0;
 #define ALP_LAUNCH_MIN(NO)                                                                         \
-    hipLaunchKernelGGL(HIP_KERNEL_NAME(scan_min_kernel<S, NO>), dim3(nblocks), dim3(g.threads), 0, \
-                       st, rec, inner, q, sp.M, sp.O, g.rows, g.rows_per_wave, g.blocks_per_item,  \
-                       nblocks, winners, fa)
+    do {                                                                                           \
+        if (g.chunks > 1)                                                                          \
+            hipLaunchKernelGGL(HIP_KERNEL_NAME(scan_min_kernel<S, NO, true>), dim3(nblocks),       \
+                               dim3(g.threads), 0, st, rec, inner, q, sp.M, sp.O, g.rows,          \
+                               g.rows_per_wave, g.chunks, g.blocks_per_item, nblocks, winners,    \
+                               fa);                                                                \
+        else                                                                                       \
+            hipLaunchKernelGGL(HIP_KERNEL_NAME(scan_min_kernel<S, NO, false>), dim3(nblocks),      \
+                               dim3(g.threads), 0, st, rec, inner, q, sp.M, sp.O, g.rows,          \
+                               g.rows_per_wave, 1u, g.blocks_per_item, nblocks, winners, fa);     \
+    } while (0)
         switch (n_outer) {
         case 0: ALP_LAUNCH_MIN(0); break;
         case 1: ALP_LAUNCH_MIN(1); break;
@@ -833,11 +857,11 @@ int scan_blocks_per_cu(uint32_t variant, uint32_t slots, uint32_t threads, const
         const bool exact = variant == 3;
         const uint32_t no = sp.M >= 2 ? sp.M - 2 : 0;
 #define ALP_OCC_MIN(SL)                                                                            \
-    (no == 0 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<SL, 0>, (int)threads, 0) \
-   : no == 1 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<SL, 1>, (int)threads, 0) \
-   : no == 2 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<SL, 2>, (int)threads, 0) \
-   : no == 3 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<SL, 3>, (int)threads, 0) \
-             : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<SL, -1>, (int)threads, 0))
+    (no == 0 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<SL, 0, false>, (int)threads, 0) \
+   : no == 1 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<SL, 1, false>, (int)threads, 0) \
+   : no == 2 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<SL, 2, false>, (int)threads, 0) \
+   : no == 3 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<SL, 3, false>, (int)threads, 0) \
+             : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<SL, -1, false>, (int)threads, 0))
         switch (slots) {
         case 1: e = exact ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_lane_kernel<1>, (int)threads, 0) : ALP_OCC_MIN(1); break;
         case 2: e = exact ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_lane_kernel<2>, (int)threads, 0) : ALP_OCC_MIN(2); break;

@@ -170,11 +170,17 @@ def test_launch_geometry_and_variant_do_not_change_results(alp):
     g = golden(2)["results"][1]
     b = make_batch(2, [g["inst"]])
     with alp.Context(b) as ctx:
-        for variant, bpi, tpb in [(1, 0, 0), (1, 1, 64), (1, 7, 128), (1, 3000, 1024),
-                                  (2, 0, 0), (2, 5, 256), (0, 64, 512), (3, 0, 0), (3, 5, 128)]:
-            ctx.set_launch(variant, bpi, tpb)
+        for variant, bpi, tpb, ch in [(1, 0, 0, 0), (1, 1, 64, 0), (1, 7, 128, 0),
+                                      (1, 3000, 1024, 0), (1, 0, 0, 1), (1, 0, 0, 2),
+                                      (1, 0, 0, 4), (1, 0, 0, 8), (1, 7, 128, 8),
+                                      (1, 3000, 1024, 2), (1, 1, 64, 4), (2, 0, 0, 0),
+                                      (2, 5, 256, 0), (0, 64, 512, 0), (3, 0, 0, 0),
+                                      (3, 5, 128, 0)]:
+            ctx.set_launch(variant, bpi, tpb, ch)
             res = ctx.search(0, g["G"], g["lambda"])
             check_result(b, 0, res, g["x"], g["L"], g["T"], g["U"])
+        with pytest.raises(alp.AlpError):
+            ctx.set_launch(1, 0, 0, 3)                 # 3 does not divide 128 / 16
         ctx.set_launch(0, 0, 0)
         first = ctx.search(0, g["G"], g["lambda"])
         for _ in range(3):
@@ -215,6 +221,10 @@ def test_ragged_and_degenerate_spaces(alp, spec):
                     want = oracle_expect(b, i, g, lam)
                     for variant in (1, 2, 3):
                         ctx.set_launch(variant)
+                        check_result(b, i, ctx.search(i, g, lam), *want)
+                    n16 = (inst.O + 15) // 16
+                    for ch in (c for c in range(2, n16 + 1) if n16 % c == 0):
+                        ctx.set_launch(1, 0, 0, ch)
                         check_result(b, i, ctx.search(i, g, lam), *want)
             ctx.set_launch(0)
             xs = np.arange(min(inst.N, 50_000), dtype=np.uint64)
