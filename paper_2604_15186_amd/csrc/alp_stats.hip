@@ -63,83 +63,79 @@ __device__ __forceinline__ uint64_t block_exclusive_max(uint64_t v)
     return excl;
 }
 
-template <bool Global>
-__global__ void __launch_bounds__(kThreads)
-trace_stats_kernel(uint32_t M, const uint64_t *__restrict__ offsets,
-                   const uint32_t *__restrict__ llm, const uint64_t *__restrict__ start,
-                   const uint64_t *__restrict__ end, uint32_t lds_cap,
-                   const uint32_t *__restrict__ long_traces, const uint64_t *__restrict__ long_base,
-                   uint64_t *__restrict__ scratch, unsigned long long *__restrict__ totals,
-                   uint32_t *__restrict__ flags)
+// Block-wide minimum and maximum of 64-bit values (every thread gets both).
+__device__ __forceinline__ void block_min_max(uint64_t &lo, uint64_t &hi)
 {
-    extern __shared__ __align__(8) unsigned char s_dyn[];
-    __shared__ unsigned long long s_sum[3 * ALP_MAX_LLMS];   // per LLM: calls, busy, active
-    const uint32_t r = Global ? long_traces[blockIdx.x] : blockIdx.x;
-    const uint64_t lo = offsets[r], n = offsets[r + 1] - lo;
-    if (!Global && n > lds_cap)
-        return;                                        // long trace: the global pass takes it
-    uint32_t P = kThreads;                              // padded length: a power of two
-    while (P < n)
-        P <<= 1;
-    uint64_t *key = Global ? scratch + 2 * long_base[blockIdx.x]
-                           : reinterpret_cast<uint64_t *>(s_dyn);
-    uint64_t *val = key + P;
-    for (uint32_t k = threadIdx.x; k < 3 * ALP_MAX_LLMS; k += kThreads)
-        s_sum[k] = 0;
-    uint32_t bad = 0;
-    for (uint32_t i = threadIdx.x; i < P; i += kThreads) {
-        uint64_t kk = kPad, vv = 0;
-        if (i < n) {
-            const uint32_t m = llm[lo + i];
-            const uint64_t s = start[lo + i], e = end[lo + i];
-            if (m >= M)
-                bad |= 1u;
-            else if (e < s)
-                bad |= 2u;
-            else if (s >= kStartLimit || e - s >= kDurationLimit)
-                bad |= 4u;
-            else {
-                kk = ((uint64_t)m << 60) | s;
-                vv = e;
-            }
-        }
-        key[i] = kk;
-        val[i] = vv;
+    __shared__ uint64_t s_lo[kThreads / 64], s_hi[kThreads / 64];
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        const uint64_t a = __shfl_xor((unsigned long long)lo, off, 64);
+        const uint64_t b = __shfl_xor((unsigned long long)hi, off, 64);
+        lo = a < lo ? a : lo;
+        hi = b > hi ? b : hi;
     }
-    if (bad)
-        atomicOr(flags, bad);
+    if ((threadIdx.x & 63) == 0) {
+        s_lo[threadIdx.x >> 6] = lo;
+        s_hi[threadIdx.x >> 6] = hi;
+    }
     __syncthreads();
-    // Bitonic sort of (key, val) pairs, ascending by key then val: calls grouped by LLM, each
-    // group in order of start.
+    for (uint32_t w = 0; w < kThreads / 64; ++w) {
+        lo = s_lo[w] < lo ? s_lo[w] : lo;
+        hi = s_hi[w] > hi ? s_hi[w] : hi;
+    }
+    __syncthreads();
+}
+
+// Bitonic sort of P (a power of two) entries in place, ascending by key then val when val is
+// given (keys only otherwise).
+template <bool WithVal>
+__device__ __forceinline__ void bitonic_sort(uint64_t *key, uint64_t *val, uint32_t P)
+{
     for (uint32_t size = 2; size <= P; size <<= 1) {
         for (uint32_t stride = size >> 1; stride > 0; stride >>= 1) {
             for (uint32_t t = threadIdx.x; t < P / 2; t += kThreads) {
                 const uint32_t i = 2 * t - (t & (stride - 1));
                 const uint32_t j = i + stride;
                 const bool up = (i & size) == 0;
-                const uint64_t ki = key[i], kj = key[j], vi = val[i], vj = val[j];
-                const bool greater = ki > kj || (ki == kj && vi > vj);
+                const uint64_t ki = key[i], kj = key[j];
+                bool greater = ki > kj;
+                uint64_t vi = 0, vj = 0;
+                if (WithVal) {
+                    vi = val[i];
+                    vj = val[j];
+                    greater = greater || (ki == kj && vi > vj);
+                }
                 if (greater == up) {
                     key[i] = kj;
                     key[j] = ki;
-                    val[i] = vj;
-                    val[j] = vi;
+                    if (WithVal) {
+                        val[i] = vj;
+                        val[j] = vi;
+                    }
                 }
             }
             __syncthreads();
         }
     }
-    // Each thread takes a contiguous chunk.  Packed value of a call: (llm << 61 | end); the
-    // maximum of the packed values before a call has high bits equal to its LLM iff an earlier
-    // call of the same LLM exists, and then low bits equal to the furthest end among them.
+}
+
+// The sweep over the sorted calls of one trace: each thread takes a contiguous chunk of the
+// first `valid` entries; get(i, m, s, e) yields entry i.  Packed value of a call: (llm << 61 |
+// end); the maximum of the packed values before a call has high bits equal to its LLM iff an
+// earlier call of the same LLM exists, and then low bits equal to the furthest end among them.
+// Per-LLM calls, durations and covered time are added to s_sum.
+template <class Get>
+__device__ __forceinline__ void sweep(uint32_t P, uint32_t valid, Get get,
+                                      unsigned long long *s_sum)
+{
     const uint32_t per = P / kThreads, base = threadIdx.x * per;
     uint64_t run = 0;
-    for (uint32_t k = 0; k < per; ++k) {
-        const uint64_t kk = key[base + k];
-        if (kk != kPad) {
-            const uint64_t pk = ((kk >> 60) << 61) | val[base + k];
-            run = pk > run ? pk : run;
-        }
+    for (uint32_t k = 0; k < per && base + k < valid; ++k) {
+        uint32_t m;
+        uint64_t s, e;
+        get(base + k, m, s, e);
+        const uint64_t pk = ((uint64_t)m << 61) | e;
+        run = pk > run ? pk : run;
     }
     uint64_t prev = block_exclusive_max(run);
     constexpr uint64_t kLow61 = (1ull << 61) - 1;
@@ -153,12 +149,10 @@ trace_stats_kernel(uint32_t M, const uint64_t *__restrict__ offsets,
         }
         c_calls = c_busy = c_active = 0;
     };
-    for (uint32_t k = 0; k < per; ++k) {
-        const uint64_t kk = key[base + k];
-        if (kk == kPad)
-            break;                                     // padding sorts last
-        const uint32_t m = (uint32_t)(kk >> 60);
-        const uint64_t s = kk & (kStartLimit - 1), e = val[base + k];
+    for (uint32_t k = 0; k < per && base + k < valid; ++k) {
+        uint32_t m;
+        uint64_t s, e;
+        get(base + k, m, s, e);
         if (m != cur) {
             flush();
             cur = m;
@@ -175,6 +169,136 @@ trace_stats_kernel(uint32_t M, const uint64_t *__restrict__ offsets,
         prev = pk > prev ? pk : prev;
     }
     flush();
+}
+
+// Largest trace the LDS path holds in registers while it loads (calls per thread).
+constexpr uint32_t kMaxPerThread = 8;
+
+template <bool Global>
+__global__ void __launch_bounds__(kThreads)
+trace_stats_kernel(uint32_t M, const uint64_t *__restrict__ offsets,
+                   const uint32_t *__restrict__ llm, const uint64_t *__restrict__ start,
+                   const uint64_t *__restrict__ end, uint32_t lds_cap,
+                   const uint32_t *__restrict__ long_traces, const uint64_t *__restrict__ long_base,
+                   uint64_t *__restrict__ scratch, unsigned long long *__restrict__ totals,
+                   uint32_t *__restrict__ flags)
+{
+    extern __shared__ __align__(8) unsigned char s_dyn[];
+    __shared__ unsigned long long s_sum[3 * ALP_MAX_LLMS];   // per LLM: calls, busy, active
+    __shared__ uint32_t s_valid;
+    const uint32_t r = Global ? long_traces[blockIdx.x] : blockIdx.x;
+    const uint64_t lo = offsets[r], n = offsets[r + 1] - lo;
+    if (!Global && n > lds_cap)
+        return;                                        // long trace: the global pass takes it
+    uint32_t P = kThreads;                              // padded length: a power of two
+    while (P < n)
+        P <<= 1;
+    uint64_t *key = Global ? scratch + 2 * long_base[blockIdx.x]
+                           : reinterpret_cast<uint64_t *>(s_dyn);
+    uint64_t *val = key + P;
+    for (uint32_t k = threadIdx.x; k < 3 * ALP_MAX_LLMS; k += kThreads)
+        s_sum[k] = 0;
+    if (threadIdx.x == 0)
+        s_valid = 0;
+    __syncthreads();                                   // counters zeroed before any adds
+    // Calls i = threadIdx.x + k * kThreads; out-of-range or invalid ones become padding.
+    uint32_t bad = 0, valid = 0;
+    auto load = [&](uint64_t i, uint32_t &m, uint64_t &s, uint64_t &e) -> bool {
+        if (i >= n)
+            return false;
+        m = llm[lo + i];
+        s = start[lo + i];
+        e = end[lo + i];
+        if (m >= M)
+            bad |= 1u;
+        else if (e < s)
+            bad |= 2u;
+        else if (s >= kStartLimit || e - s >= kDurationLimit)
+            bad |= 4u;
+        else
+            return true;
+        return false;
+    };
+    if (!Global) {
+        // Held in registers: the trace's first and last start decide whether a call packs
+        // into one 64-bit key, (llm << 61 | start - first << 32 | duration), which halves the
+        // sort's LDS traffic; traces spanning 2^29 us or more keep (key, end) pairs.
+        uint32_t rm[kMaxPerThread];
+        uint64_t rs[kMaxPerThread], re[kMaxPerThread];
+        bool ok[kMaxPerThread];
+        uint64_t smin = ~0ull, smax = 0;
+#pragma unroll
+        for (uint32_t k = 0; k < kMaxPerThread; ++k) {
+            ok[k] = load(threadIdx.x + (uint64_t)k * kThreads, rm[k], rs[k], re[k]);
+            if (ok[k]) {
+                valid += 1;
+                smin = rs[k] < smin ? rs[k] : smin;
+                smax = rs[k] > smax ? rs[k] : smax;
+            }
+        }
+        if (bad)
+            atomicOr(flags, bad);
+        atomicAdd(&s_valid, valid);
+        block_min_max(smin, smax);                      // includes the barriers s_valid needs
+        const uint32_t nvalid = s_valid;
+        if (nvalid == 0)
+            return;
+        if (smax - smin < (1ull << 29)) {
+#pragma unroll
+            for (uint32_t k = 0; k < kMaxPerThread; ++k) {
+                const uint32_t i = threadIdx.x + k * kThreads;
+                if (i < P)
+                    key[i] = ok[k] ? ((uint64_t)rm[k] << 61) | ((rs[k] - smin) << 32) | (re[k] - rs[k])
+                                   : kPad;
+            }
+            __syncthreads();
+            bitonic_sort<false>(key, nullptr, P);
+            sweep(P, nvalid, [&](uint32_t i, uint32_t &m, uint64_t &s, uint64_t &e) {
+                const uint64_t kk = key[i];
+                m = (uint32_t)(kk >> 61);
+                s = smin + ((kk >> 32) & ((1ull << 29) - 1));
+                e = s + (kk & 0xFFFFFFFFull);
+            }, s_sum);
+        } else {
+#pragma unroll
+            for (uint32_t k = 0; k < kMaxPerThread; ++k) {
+                const uint32_t i = threadIdx.x + k * kThreads;
+                if (i < P) {
+                    key[i] = ok[k] ? ((uint64_t)rm[k] << 60) | rs[k] : kPad;
+                    val[i] = ok[k] ? re[k] : 0;
+                }
+            }
+            __syncthreads();
+            bitonic_sort<true>(key, val, P);
+            sweep(P, nvalid, [&](uint32_t i, uint32_t &m, uint64_t &s, uint64_t &e) {
+                const uint64_t kk = key[i];
+                m = (uint32_t)(kk >> 60);
+                s = kk & (kStartLimit - 1);
+                e = val[i];
+            }, s_sum);
+        }
+    } else {
+        for (uint64_t i = threadIdx.x; i < P; i += kThreads) {
+            uint32_t m = 0;
+            uint64_t s = 0, e = 0;
+            const bool ok = load(i, m, s, e);
+            valid += ok;
+            key[i] = ok ? ((uint64_t)m << 60) | s : kPad;
+            val[i] = ok ? e : 0;
+        }
+        if (bad)
+            atomicOr(flags, bad);
+        atomicAdd(&s_valid, valid);
+        __syncthreads();
+        const uint32_t nvalid = s_valid;
+        bitonic_sort<true>(key, val, P);
+        sweep(P, nvalid, [&](uint32_t i, uint32_t &m, uint64_t &s, uint64_t &e) {
+            const uint64_t kk = key[i];
+            m = (uint32_t)(kk >> 60);
+            s = kk & (kStartLimit - 1);
+            e = val[i];
+        }, s_sum);
+    }
     __syncthreads();
     for (uint32_t k = threadIdx.x; k < 3 * M; k += kThreads)
         if (s_sum[k])

@@ -60,6 +60,21 @@ def test_long_traces_mixed_with_short(ctx):
     _same(ctx, 4, *_pack(traces))
 
 
+def test_wide_and_narrow_time_spans(ctx):
+    # short traces whose calls span more than 2^29 us take the (key, end) sort, narrow ones the
+    # packed key; both in one launch, with a long trace of each kind
+    rng = np.random.default_rng(9)
+    traces = []
+    for span_bits, n in ((40, 300), (22, 300), (31, 1500), (29, 2048), (30, 2), (35, 3000),
+                         (20, 5000), (28, 1)):
+        tr = []
+        for _ in range(n):
+            a = int(rng.integers(0, 1 << span_bits))
+            tr.append((int(rng.integers(0, 3)), a, a + int(rng.integers(0, 1 << 20))))
+        traces.append(tr)
+    _same(ctx, 3, *_pack(traces))
+
+
 def test_edge_cases(ctx):
     # empty traces, zero-length calls, identical calls, unused LLMs, a single call
     traces = [[], [(0, 5, 5), (0, 7, 7)], [(3, 0, 10)] * 7, [], [(5, 1 << 59, (1 << 59) + 3)],
