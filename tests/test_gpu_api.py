@@ -1,0 +1,94 @@
+"""The C ABI's promises about streams and contexts, on an MI355X: work ordered on a caller's
+HIP stream, distinct contexts independent (also from two threads at once), and results that
+do not depend on either."""
+from __future__ import annotations
+
+import threading
+
+import numpy as np
+import pytest
+
+from workloads import make_batch, target_from_tmax
+from workloads.traces import make_traces
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def alp():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2604_15186_amd import alp as binding
+    binding.lib()
+    return binding
+
+
+def _queries(alp, b):
+    G = np.asarray(b["G"], dtype=np.uint32)
+    with alp.Context(b) as ctx:
+        tmax = ctx.max_throughput(G)
+        lam = np.asarray([target_from_tmax(int(b["u_ppm"][i]), int(tmax[i]))
+                          for i in range(len(G))], dtype=np.uint32)
+        ref = ctx.search_batch(G, lam)
+    return G, lam, ref
+
+
+def test_search_on_a_caller_stream(alp):
+    import torch
+    b = make_batch(1, range(16))
+    G, lam, ref = _queries(alp, b)
+    s = torch.cuda.Stream()
+    with alp.Context(b, stream=s.cuda_stream) as ctx:
+        # device work queued on the caller's stream before the search must not disturb it
+        x = torch.ones(1 << 24, device="cuda")
+        with torch.cuda.stream(s):
+            y = x * 2
+        out = ctx.search_batch(G, lam)
+        assert out.tobytes() == ref.tobytes()
+        assert float(y[0]) == 2.0
+        one = ctx.search(5, int(G[5]), int(lam[5]))
+        assert one.tobytes() == ref[5].tobytes()
+        pr = ctx.search_pruned(G, lam)
+        assert (pr["best"]["status"] <= 5).all()
+
+
+def test_contexts_in_two_threads(alp):
+    import torch
+    batches = [make_batch(1, range(8)), make_batch(0, range(64))]
+    refs = [_queries(alp, b) for b in batches]
+    errors = []
+
+    def work(k):
+        try:
+            s = torch.cuda.Stream()
+            with alp.Context(batches[k], stream=s.cuda_stream) as ctx:
+                G, lam, ref = refs[k]
+                for _ in range(20):
+                    out = ctx.search_batch(G, lam)
+                    if out.tobytes() != ref.tobytes():
+                        errors.append(f"context {k}: results differ")
+                        return
+                with pytest.raises(alp.AlpError):
+                    ctx.search(10_000, 1, 1)               # instance out of range
+        except Exception as e:                              # reported by the main thread
+            errors.append(f"context {k}: {e!r}")
+
+    threads = [threading.Thread(target=work, args=(k,)) for k in range(2)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=120)
+    assert not any(t.is_alive() for t in threads)
+    assert errors == []
+
+
+def test_statistics_on_a_caller_stream(alp):
+    import torch
+    tr = make_traces("rag", 500, 2)
+    s = torch.cuda.Stream()
+    with alp.StatsContext(0) as c0, alp.StatsContext(0, stream=s.cuda_stream) as c1:
+        a = c0.compute(tr["M"], tr["offsets"], tr["llm"], tr["start"], tr["end"])
+        with torch.cuda.stream(s):
+            b = c1.compute(tr["M"], tr["offsets"], tr["llm"], tr["start"], tr["end"])
+        assert a.tobytes() == b.tobytes()
