@@ -50,6 +50,9 @@ from workloads import CONFIGS, make_batch, make_custom, target_from_tmax  # noqa
 
 PEAK_LANE_OPS = 256 * 64 * 2.4e9        # int32 VALU lane-ops/s of MI355X
 OPS_PER_CANDIDATE = 2                   # budget compare + objective min
+# The wider count of lane-ops per candidate (add the last term, compare the budget, compare the
+# best, select value and index), reported beside ``frac`` for comparison with that accounting.
+OPS_PER_CANDIDATE_WIDE = 5
 WORKLOADS = {"cfg2": 2, "cfg3": 3, "cfg4": 4, "cfg1": 1, "multi": 2, "pruned": 4,
              "pruned-paper": None, "stats": None, "place": 4}
 HBM_PEAK = 8.0e12                       # MI355X HBM3E bytes/s
@@ -266,6 +269,7 @@ def run_exhaustive(args, alp):
                 "traffic": _traffic(_kernel_digest(), args.workload),
                 "kernel": "scan", "kernel_ms": avg_scan_s * 1e3,
                 "ops_per_candidate": OPS_PER_CANDIDATE,
+                "frac_at_5_ops": per_step * OPS_PER_CANDIDATE_WIDE / avg_scan_s / PEAK_LANE_OPS,
                 "other_kernels_ms": {"option_terms": terms_ms, "budget_split": split_ms}}
     cpu = None
     if not args.no_cpu_baseline:

@@ -299,10 +299,12 @@ int32_t alp_eval_candidates(alp_ctx *ctx, uint32_t instance, uint32_t gpu_budget
                             alp_eval_t *out);
 
 /* Launch choices, for tests and tuning.  variant: 0 automatic (= 1), 1 row-minimum scan
- * (default), 2 thread-per-candidate scan, 3 exact-tracking lane scan.  blocks_per_item and
- * threads_per_block (a multiple of 64, at most 1024): 0 = automatic.  inner_chunks (variant 1):
- * ranges each row's inner-LLM records are split into, dividing ceil(O / 16); 0 = automatic.
- * Results do not depend on these choices. */
+ * (default), 2 thread-per-candidate scan, 3 exact-tracking lane scan, 4 row-minimum scan with
+ * fixed row ranges per wave, 5 row-minimum scan with rows handed out within each block (variant
+ * 1 picks between the two; rows can only be split with the second, so variant 4 ignores
+ * inner_chunks).  blocks_per_item and threads_per_block (a multiple of 64, at most 1024):
+ * 0 = automatic.  inner_chunks (variants 1, 5): ranges each row's inner-LLM records are split
+ * into, dividing ceil(O / 16); 0 = automatic.  Results do not depend on these choices. */
 int32_t alp_set_launch(alp_ctx *ctx, uint32_t variant, uint32_t blocks_per_item,
                        uint32_t threads_per_block, uint32_t inner_chunks);
 

@@ -277,53 +277,70 @@ alp::ScanGeometry plan_scan(alp_ctx *c, uint32_t count)
 {
     alp::ScanGeometry g{};
     const alp::SpaceDev &sp = c->sp;
-    g.variant = c->variant ? c->variant : 1;
+    // Variants 4 and 5 are the row-minimum scan with a fixed choice of work distribution.
+    g.variant = c->variant == 0 || c->variant >= 4 ? 1 : c->variant;
     g.slots = slots_for(sp.O);
     const uint64_t cus = c->num_cus > 0 ? (uint64_t)c->num_cus : 256;
     if (g.variant != 2) {
         g.rows = 1;
         for (uint32_t m = 2; m < sp.M; ++m)
             g.rows *= sp.O;
-        // Variant 1 may split each row into chunks of the inner LLM's records (sub-rows): an
-        // override applies here; the automatic choice is made below, once the rows per wave are
-        // known.
         g.chunks = 1;
-        const bool chunked = g.variant == 1 && sp.M >= 2;
-        const uint32_t n16 = alp::inner_stride(sp.O) / 16;      // chunks must divide this
-        if (chunked && c->chunks_override) {
-            g.chunks = c->chunks_override;
-            g.rows *= g.chunks;
-        }
-        // Blocks of 8 waves (fewer blocks, fewer end-of-block reductions), at most one wave per
-        // row.  Each wave gets at least kMinRecordsPerWave of the inner LLM's records (rows
-        // times records per row) when the item has that many, so that a wave's fixed costs
-        // (setup, end-of-wave re-scan, block reduction) stay small.
+        // Fixed ranges of whole rows per wave: blocks of 8 waves (fewer blocks, fewer
+        // end-of-block reductions), at most one wave per row, and each wave gets at least
+        // kMinRecordsPerWave of the inner LLM's records (rows times records per row) when the
+        // item has that many, so that a wave's fixed costs (setup, end-of-wave re-scan, block
+        // reduction) stay small.
         constexpr uint64_t kMinRecordsPerWave = 512;
-        const uint64_t per_row = sp.M >= 2 ? alp::inner_stride(sp.O) / g.chunks : 1;
+        const uint64_t per_row = sp.M >= 2 ? alp::inner_stride(sp.O) : 1;
         const uint64_t min_rows = std::max<uint64_t>(1, kMinRecordsPerWave / per_row);
         g.threads = c->tpb_override ? c->tpb_override
                                     : (uint32_t)(64 * (g.rows < 8 ? g.rows : 8));
-        const uint32_t wpb = g.threads / 64;
+        uint32_t wpb = g.threads / 64;
         const uint64_t max_waves = g.rows >= min_rows ? g.rows / min_rows : 1;
-        const uint64_t max_bpi = ceil_div(max_waves, wpb);
         uint64_t bpi = c->bpi_override;
         if (!bpi)
             bpi = blocks_per_item_for_rounds(
-                count, cus * (uint64_t)blocks_per_cu(c, g.variant, g.slots, g.threads), max_bpi);
-        // Few rows per wave: split the rows so that a wave keeps at least 16 sub-rows; its
-        // records stay the same, but the end-of-wave re-scan covers one sub-row only.
-        if (chunked && !c->chunks_override) {
-            const uint64_t rpw = ceil_div(g.rows, bpi * wpb);
-            if (rpw < 16) {
+                count, cus * (uint64_t)blocks_per_cu(c, g.variant, g.slots, g.threads),
+                ceil_div(max_waves, wpb));
+        // Rows handed out within each block instead (row-minimum scan, needs fewer than 2^32
+        // sub-rows per item): forced by variant 5 or a row split, else chosen when fixed ranges
+        // would leave a wave fewer than 16 rows.  Waves then finish together however the SIMD
+        // shares its issue slots among them, and rows may be split into sub-rows of the inner
+        // LLM's records.  Plan: at most 16 waves per CU over the whole batch and at least two
+        // of the finest sub-rows per wave; blocks of 8 waves while that leaves CUs without a
+        // block, else of 16; rows split so that a wave gets about 8 sub-rows.
+        const bool splittable = g.variant == 1 && sp.M >= 2;
+        const uint32_t n16 = alp::inner_stride(sp.O) / 16;      // chunks must divide this
+        bool dyn = g.variant == 1 && c->variant != 4 &&
+                   (c->variant == 5 || c->chunks_override > 1 ||
+                    ceil_div(g.rows, bpi * wpb) < 16);
+        if (dyn && g.rows * (splittable ? n16 : 1) >= (UINT64_C(1) << 32))
+            dyn = false;
+        if (dyn) {
+            const uint64_t finest = g.rows * (splittable ? n16 : 1);
+            const uint64_t items = std::max<uint64_t>(1, count);
+            const uint64_t waves = std::max<uint64_t>(
+                1, std::min<uint64_t>(cus * 16, items * std::max<uint64_t>(1, finest / 2)));
+            if (!c->tpb_override)
+                g.threads = (uint32_t)(64 * std::min<uint64_t>(waves <= cus * 8 ? 8 : 16,
+                                                               std::max<uint64_t>(1, finest)));
+            wpb = g.threads / 64;
+            if (!c->bpi_override)
+                bpi = std::max<uint64_t>(1, ceil_div(waves, items * wpb));
+            if (splittable && c->chunks_override) {
+                g.chunks = c->chunks_override;
+            } else if (splittable) {
                 g.chunks = n16;
                 for (uint32_t k = 1; k <= n16; ++k)
-                    if (n16 % k == 0 && rpw * k >= 16) {
+                    if (n16 % k == 0 && g.rows * k >= 8 * bpi * wpb) {
                         g.chunks = k;
                         break;
                     }
-                g.rows *= g.chunks;
             }
+            g.rows *= g.chunks;
         }
+        g.dynamic = dyn ? 1u : 0u;
         g.rows_per_wave = ceil_div(g.rows, bpi * wpb);
         if (!c->bpi_override)
             bpi = ceil_div(g.rows, g.rows_per_wave * wpb);
@@ -1013,8 +1030,8 @@ int32_t alp_set_launch(alp_ctx *ctx, uint32_t variant, uint32_t blocks_per_item,
 {
     if (!ctx)
         return fail(ALP_EINVAL, "ctx is NULL");
-    if (variant > 3)
-        return fail(ALP_EINVAL, "variant %u not in 0..3", variant);
+    if (variant > 5)
+        return fail(ALP_EINVAL, "variant %u not in 0..5", variant);
     if (threads_per_block && (threads_per_block % 64 || threads_per_block > 1024))
         return fail(ALP_EINVAL, "threads_per_block must be a multiple of 64, at most 1024");
     if (blocks_per_item > (1u << 24))

@@ -79,55 +79,91 @@ __device__ __forceinline__ void block_min_store(uint32_t L, uint64_t x, Winner *
 }
 
 // Lexicographic (L, x) minimum of an item's block winners, by one wave; every lane gets it.
+// Each lane issues up to eight winner loads before comparing any, so the item's winners arrive
+// in one memory round trip per 512 blocks.
 __device__ __forceinline__ void item_winner(uint32_t item, uint32_t blocks_per_item,
                                             const Winner *winners, uint32_t &L, uint64_t &x)
 {
     const uint32_t lane = threadIdx.x & 63;
+    const Winner *base = winners + (uint64_t)item * blocks_per_item;
     L = kNoLatency;
     x = ~0ull;
-    for (uint32_t k = lane; k < blocks_per_item; k += 64) {
-        const Winner w = winners[(uint64_t)item * blocks_per_item + k];
-        if (lex_less(w.L, w.x, L, x)) {
-            L = w.L;
-            x = w.x;
+    for (uint32_t k0 = 0; k0 < blocks_per_item; k0 += 8 * 64) {
+        uint32_t wL[8];
+        uint64_t wx[8];
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            const uint32_t k = k0 + 64u * t + lane;
+            wL[t] = kNoLatency;
+            wx[t] = ~0ull;
+            if (k < blocks_per_item) {
+                const Winner w = base[k];
+                wL[t] = w.L;
+                wx[t] = w.x;
+            }
         }
+#pragma unroll
+        for (int t = 0; t < 8; ++t)
+            if (lex_less(wL[t], wx[t], L, x)) {
+                L = wL[t];
+                x = wx[t];
+            }
     }
     wave_min(L, x);
 }
 
 // The result record of winner (L, x) -- decoded per-LLM choices, T_w (Eq. 2: minimum over LLMs)
-// and the share units, from the item's per-option records E -- written by one thread as the six
-// 64-bit words of alp_result_t.  (Assembled in registers: a local struct indexed at run time
-// would be placed in memory for every thread of the block.)
+// and the share units, from the item's per-option records E -- written as the six 64-bit words
+// of alp_result_t.  Called by all lanes of one wave with the same (L, x): lane m decodes LLM m's
+// digit and loads its record (one memory round trip for all LLMs), the wave combines them, and
+// lane 0 writes.
 __device__ __forceinline__ void write_result(const SpaceDev &sp, const uint2 *E, uint32_t L,
                                              uint64_t x, uint64_t *dst)
 {
-    uint64_t word[6] = {ALP_NO_INDEX, 0, (uint64_t)ALP_INFEASIBLE << 32, 0, 0, 0};
-    if (L != kNoLatency) {
-        uint64_t rr = x;
-        uint32_t T = 0xFFFFFFFFu, U = 0;
-        uint64_t tp = 0, fq = 0, rep = 0;
-        for (int m = (int)sp.M - 1; m >= 0; --m) {
-            const uint32_t o = (uint32_t)(rr % sp.O);
-            rr /= sp.O;
-            const uint2 e = E[(uint64_t)m * sp.O + o];
-            T = e.x < T ? e.x : T;                      // Eq. 2: minimum over LLMs
-            U += e.y & 0xFFFFu;
-            const uint32_t ij = o / sp.D;
-            tp |= (uint64_t)(sp.tp[ij / sp.n_fq] & 0xFFu) << (8 * m);
-            fq |= (uint64_t)(sp.fq[ij % sp.n_fq] & 0xFFu) << (8 * m);
-            rep |= (uint64_t)((o % sp.D + 1) & 0xFFu) << (8 * m);
-        }
-        word[0] = x;
-        word[1] = (uint64_t)L | ((uint64_t)T << 32);
-        word[2] = (uint64_t)U | ((uint64_t)ALP_OK << 32);
-        word[3] = tp;
-        word[4] = fq;
-        word[5] = rep;
+    const uint32_t lane = threadIdx.x & 63;
+    uint32_t T = 0xFFFFFFFFu, U = 0;
+    uint64_t tp = 0, fq = 0, rep = 0;
+    if (L != kNoLatency && lane < sp.M) {
+        // o_m = floor(x / O^(M-1-m)) mod O  (candidate index, LLM 0 most significant)
+        uint64_t scale = 1;
+        for (uint32_t k = lane + 1; k < sp.M; ++k)
+            scale *= sp.O;
+        const uint32_t o = (uint32_t)((x / scale) % sp.O);
+        const uint2 e = E[(uint64_t)lane * sp.O + o];
+        T = e.x;
+        U = e.y & 0xFFFFu;
+        const uint32_t ij = o / sp.D;
+        tp = (uint64_t)(sp.tp[ij / sp.n_fq] & 0xFFu) << (8 * lane);
+        fq = (uint64_t)(sp.fq[ij % sp.n_fq] & 0xFFu) << (8 * lane);
+        rep = (uint64_t)((o % sp.D + 1) & 0xFFu) << (8 * lane);
     }
+    // Combine the (at most 8) LLM lanes: Eq. 2 minimum, unit sum, disjoint byte fields.
 #pragma unroll
-    for (int k = 0; k < 6; ++k)
-        dst[k] = word[k];
+    for (int off = 1; off < ALP_MAX_LLMS; off <<= 1) {
+        const uint32_t oT = __shfl_xor(T, off, 64);
+        T = oT < T ? oT : T;
+        U += __shfl_xor(U, off, 64);
+        tp |= __shfl_xor((unsigned long long)tp, off, 64);
+        fq |= __shfl_xor((unsigned long long)fq, off, 64);
+        rep |= __shfl_xor((unsigned long long)rep, off, 64);
+    }
+    if (lane != 0)
+        return;
+    if (L == kNoLatency) {
+        dst[0] = ALP_NO_INDEX;
+        dst[1] = 0;
+        dst[2] = (uint64_t)ALP_INFEASIBLE << 32;
+        dst[3] = 0;
+        dst[4] = 0;
+        dst[5] = 0;
+        return;
+    }
+    dst[0] = x;
+    dst[1] = (uint64_t)L | ((uint64_t)T << 32);
+    dst[2] = (uint64_t)U | ((uint64_t)ALP_OK << 32);
+    dst[3] = tp;
+    dst[4] = fq;
+    dst[5] = rep;
 }
 
 // Result of one item from its block winners, by one wave.
@@ -137,9 +173,8 @@ __device__ __forceinline__ void finish_item(const FinishArgs &fa, uint32_t item,
     uint32_t L;
     uint64_t x;
     item_winner(item, blocks_per_item, winners, L, x);
-    if ((threadIdx.x & 63) == 0)
-        write_result(fa.sp, fa.ext + (uint64_t)item * fa.sp.M * fa.sp.O, L, x,
-                     reinterpret_cast<uint64_t *>(fa.out + item));
+    write_result(fa.sp, fa.ext + (uint64_t)item * fa.sp.M * fa.sp.O, L, x,
+                 reinterpret_cast<uint64_t *>(fa.out + item));
 }
 
 // Writes the block's winner and counts the block as finished (agent-scope fence and per-item

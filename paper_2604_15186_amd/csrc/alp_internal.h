@@ -79,6 +79,8 @@ struct ScanGeometry {
                                // rows times chunks)
     uint64_t rows_per_wave;    // variants 1, 3
     uint32_t chunks;           // variant 1: ranges of the inner LLM's records per row
+    uint32_t dynamic;          // variant 1: sub-rows handed out within each block (1) or fixed
+                               // per wave (0, requires chunks == 1)
     uint64_t per_thread;       // variant 2: candidates per thread
     uint32_t slots;            // variants 1, 3: options of the last LLM per lane (1, 2, 4, 8)
 };

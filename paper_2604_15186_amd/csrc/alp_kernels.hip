@@ -4,7 +4,7 @@
 //   1. option_terms_kernel: per (item, LLM m, option o) the Eq. 1 contribution c and the share
 //      units u (replaced by a sentinel when the option is unusable at the target), plus the
 //      Eq. 2 normalised throughput tau and validity flags for result decoding.
-//   2. scan_min_kernel<S> (or, for cross-checks, scan_flat_kernel / scan_lane_kernel<S>): every
+//   2. scan_min_kernel<S, ...> (or, for cross-checks, scan_flat_kernel / scan_lane_kernel<S>): every
 //      candidate x = (o_0 .. o_{M-1}) is evaluated -- L_w = sum c, feasible iff sum u <= Q*G --
 //      and the lexicographic (L_w, x) minimum is reduced per wave, per block, and written as one
 //      16-byte winner per block.
@@ -120,7 +120,15 @@ option_terms_kernel(SpaceDev sp, TablesDev tb, QueryDev q, uint32_t count, uint2
 // when strictly smaller).  At the end the wave takes the smallest latency L*, the lowest row r*
 // in which any lane-slot reaches L*, and scans that one row again to find, for those
 // lane-slots, the lowest j with c_j = L* - oc - c_last that is feasible; the smallest (j,
-// option) among them completes the lowest index reaching L*.
+// option) among them completes the lowest index reaching L*.  Only waves whose L* is their
+// block's minimum do this re-scan.
+//
+// Work distribution.  Either each wave owns a fixed range of whole rows, or (DYNAMIC) a block
+// owns a range of sub-rows -- a row may be split into consecutive ranges of the inner LLM's
+// records -- and its waves claim them one at a time from an LDS counter.  A SIMD favours its
+// older waves when issuing, so with fixed ranges the younger waves of a small search finish
+// late while the SIMD idles; claiming lets every wave of a block finish within one sub-row of
+// the others.
 
 // One record (c, y) against every slot of the lane.  A lane's slots are ordered by share units
 // (w_0 <= w_1 <= ...), so the feasible lanes of slot s+1 are a subset of those of slot s: each
@@ -215,9 +223,11 @@ __device__ __forceinline__ void masked_min_8(uint32_t (&bq)[S], const int32_t (&
         masked_min_step(bq, w, v[t].y, v[t].x, full);
 }
 
-// Outer-digit latency and share-unit sums of row r (digits o_0..o_{M-3} of r, base O).
-__device__ __forceinline__ void outer_sums(const uint2 *R, uint32_t O, uint32_t n_outer,
-                                           uint64_t r, uint32_t &oc, int32_t &ou)
+// Outer-digit latency and share-unit sums of row r (digits o_0..o_{M-3} of r, base O), least
+// significant digit (k = n_outer - 1) first.
+template <typename Int>
+__device__ __forceinline__ void outer_sums_t(const uint2 *R, uint32_t O, uint32_t n_outer, Int r,
+                                             uint32_t &oc, int32_t &ou)
 {
     oc = 0;
     ou = 0;
@@ -233,19 +243,48 @@ __device__ __forceinline__ void outer_sums(const uint2 *R, uint32_t O, uint32_t 
     }
 }
 
+// 32-bit division whenever r allows it.
+__device__ __forceinline__ void outer_sums(const uint2 *R, uint32_t O, uint32_t n_outer,
+                                           uint64_t r, uint32_t &oc, int32_t &ou)
+{
+    if ((r >> 32) == 0)
+        outer_sums_t<uint32_t>(R, O, n_outer, (uint32_t)r, oc, ou);
+    else
+        outer_sums_t<uint64_t>(R, O, n_outer, r, oc, ou);
+}
+
+// One record (c, y) at inner index j against every slot of the lane, for the end-of-wave
+// re-scan: where the slot is feasible (w_s <= y) and c equals the slot's target, jf_s takes
+// min(jf_s, j).  A slot that needs nothing has w_s above every y.
+template <int S>
+__device__ __forceinline__ void masked_find_step(uint32_t (&jf)[S], const int32_t (&w)[S],
+                                                 const uint32_t (&target)[S], uint32_t y,
+                                                 uint32_t c, uint32_t j, uint64_t full)
+{
+#pragma unroll
+    for (int s = 0; s < S; ++s)
+        asm volatile("v_cmpx_ge_i32_e32 vcc, %[y], %[w]\n\t"
+                     "v_cmpx_eq_u32_e32 vcc, %[c], %[t]\n\t"
+                     "v_min_u32_e32 %[f], %[j], %[f]\n\t" ALP_RESTORE
+                     : [f] "+v"(jf[s])
+                     : [y] "s"(y), [c] "s"(c), [j] "s"(j), [w] "v"(w[s]), [t] "v"(target[s]),
+                       [full] "s"(full)
+                     : "vcc");
+}
+
 // NOUT >= 0: the number of outer digits (M - 2) is fixed at compile time; NOUT < 0: any M.
-template <int S, int NOUT, bool CHUNKED>
+template <int S, int NOUT, bool DYNAMIC>
 __global__ void __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 8 : 1)))
 scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_all, QueryDev q,
                 uint32_t M, uint32_t O, uint64_t rows, uint64_t rows_per_wave, uint32_t chunks,
                 uint32_t blocks_per_item, uint32_t nblocks, Winner *__restrict__ winners,
                 FinishArgs fa)
 {
-    // `rows` counts sub-rows: with CHUNKED each row (one choice of the outer digits) is split
-    // into `chunks` consecutive ranges of the inner LLM's records, so that small spaces still
-    // give every wave enough sub-rows; candidates stay in index order (row, record, option).
-    // Without it (chunks = 1) the bookkeeping compiles away.
-    if (!CHUNKED)
+    // `rows` counts sub-rows: each row (one choice of the outer digits) may be split into
+    // `chunks` consecutive ranges of the inner LLM's records (DYNAMIC only), so that small
+    // spaces still give every wave several sub-rows; candidates stay in index order (row,
+    // record, option).  Without DYNAMIC, chunks = 1 and each wave walks a fixed range of rows.
+    if (!DYNAMIC)
         chunks = 1;
     const uint32_t lb = xcd_logical_block(blockIdx.x, nblocks);
     const uint32_t item = lb / blocks_per_item;
@@ -300,22 +339,48 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
 
     uint32_t waveL = kNoLatency;
     uint64_t waveX = ~0ull;
+    // Without DYNAMIC, wave gw owns the sub-rows [r_begin, r_end).  With DYNAMIC, the block owns
+    // [r_begin, r_end) (rows_per_wave * wpb sub-rows, fewer than 2^32) and hands them out one at
+    // a time from an LDS counter: waves that the SIMD issues less often (younger waves) simply
+    // take fewer sub-rows, so the waves of a block finish together.  Wave w starts with sub-row
+    // w; each wave's sub-rows increase, as the first-row bookkeeping below requires.
     const uint64_t gw = (uint64_t)sub * wpb + wave;
-    const uint64_t r_begin = gw * rows_per_wave;
-    const uint64_t r_end = r_begin + rows_per_wave < rows ? r_begin + rows_per_wave : rows;
+    const uint64_t per = DYNAMIC ? rows_per_wave * wpb : rows_per_wave;
+    const uint64_t r_begin = (DYNAMIC ? (uint64_t)sub : gw) * per;
+    const uint64_t r_end = r_begin + per < rows ? r_begin + per : rows;
+    __shared__ uint32_t s_next;
+    if (DYNAMIC) {
+        if (threadIdx.x == 0)
+            s_next = wpb;
+        __syncthreads();
+    }
+    const uint32_t first = DYNAMIC ? wave : 0u;
 
-    if (r_begin < r_end) {
-        const uint64_t full = __builtin_amdgcn_read_exec();
-        uint32_t bestL[S], bestR[S];          // per lane-slot: smallest row latency, its first row
+    const uint64_t full = __builtin_amdgcn_read_exec();
+    uint32_t bestL[S], bestR[S];              // per lane-slot: smallest row latency, its first row
 #pragma unroll
-        for (int s = 0; s < S; ++s) {
-            bestL[s] = kNoLatency;
-            bestR[s] = 0;
-        }
+    for (int s = 0; s < S; ++s) {
+        bestL[s] = kNoLatency;
+        bestR[s] = 0;
+    }
+    uint32_t Lstar = kNoLatency;              // the wave's smallest latency
+    if (r_begin + first < r_end) {
         uint32_t digit[NMAX > 0 ? NMAX : 1];
-        uint32_t chunk = CHUNKED ? (uint32_t)(r_begin % chunks) : 0u;
-        {
-            uint64_t rr = CHUNKED ? r_begin / chunks : r_begin;
+        uint32_t chunk = 0;
+        // Division by O and by chunks through reciprocals: q = mulhi(n, floor((2^32-1)/d)) is
+        // floor(n/d) or one less (n < 2^32), and one correction step makes it exact.
+        const uint32_t inv_o = 0xFFFFFFFFu / O, inv_ch = 0xFFFFFFFFu / chunks;
+        auto divmod = [](uint32_t n, uint32_t d, uint32_t inv, uint32_t &r) {
+            uint32_t q = __umulhi(n, inv);
+            r = n - q * d;
+            if (r >= d) {
+                ++q;
+                r -= d;
+            }
+            return q;
+        };
+        if (!DYNAMIC) {
+            uint64_t rr = r_begin;
 #pragma unroll
             for (int k = NMAX - 1; k >= 0; --k) {
                 digit[k] = 0;
@@ -325,7 +390,25 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
                 }
             }
         }
-        for (uint32_t rr = 0; rr < (uint32_t)(r_end - r_begin); ++rr) {
+        uint32_t cur = first, next = 0;
+        for (uint32_t rr = 0;; ++rr) {
+            if (DYNAMIC) {
+                if (r_begin + cur >= r_end)
+                    break;
+                // Claim the wave's next sub-row now; the answer is used after this one.
+                if (lane == 0)
+                    next = atomicAdd(&s_next, 1u);
+                uint32_t row = divmod((uint32_t)(r_begin + cur), chunks, inv_ch, chunk);
+#pragma unroll
+                for (int k = NMAX - 1; k >= 0; --k) {
+                    digit[k] = 0;
+                    if (NOUT >= 0 || (uint32_t)k < n_outer)
+                        row = divmod(row, O, inv_o, digit[k]);
+                }
+            } else if (rr >= (uint32_t)(r_end - r_begin)) {
+                break;
+            }
+            const uint32_t tag = DYNAMIC ? cur : rr;
             uint32_t oc = 0;
             int32_t ou = 0;
 #pragma unroll
@@ -347,8 +430,8 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
                 // 16 records per iteration (the table is padded to a multiple of 16 with
                 // records no lane can use): two 64-byte scalar loads issued together, so the
                 // loop's own scalar work stays small next to the 2 x 16 x S VALU operations.
-                const uint2 *const begin = CHUNKED ? inner + chunk * chunk_len : inner;
-                const uint2 *const end = CHUNKED ? begin + chunk_len : inner + n_inner_padded;
+                const uint2 *const begin = DYNAMIC ? inner + chunk * chunk_len : inner;
+                const uint2 *const end = DYNAMIC ? begin + chunk_len : inner + n_inner_padded;
                 for (const uint2 *p = begin; p != end; p += 16) {
                     uint2 v0[8], v1[8];
 #pragma unroll
@@ -368,15 +451,14 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
                 const uint32_t L = __builtin_elementwise_add_sat(bq[s], c_last[s] + oc);
                 const bool better = L < bestL[s];
                 bestL[s] = better ? L : bestL[s];
-                bestR[s] = better ? rr : bestR[s];
+                bestR[s] = better ? tag : bestR[s];
             }
-            // Next sub-row; after the last chunk, the odometer on the outer digits moves on
-            // (integer carry, stays in scalar registers).
-            if (CHUNKED) {
-                if (++chunk < chunks)
-                    continue;
-                chunk = 0;
+            if (DYNAMIC) {
+                cur = (uint32_t)__builtin_amdgcn_readfirstlane(next);
+                continue;
             }
+            // Next row: the odometer on the outer digits moves on (integer carry, stays in
+            // scalar registers).
             uint32_t inc = 1;
 #pragma unroll
             for (int k = NMAX - 1; k >= 0; --k) {
@@ -388,25 +470,37 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
             }
         }
 
-        // Wave minimum L*, then the lowest row r* reaching it.
         uint32_t lmin = kNoLatency;
 #pragma unroll
         for (int s = 0; s < S; ++s)
             lmin = bestL[s] < lmin ? bestL[s] : lmin;
-        const uint32_t Lstar = wave_min_u32(lmin);
-        if (Lstar != kNoLatency) {
+        Lstar = wave_min_u32(lmin);
+    }
+    // Only waves whose L* is the block's smallest can hold the block's winner: they alone look
+    // up their index (the others wait at the block reduction and leave their SIMD to them).
+    __shared__ uint32_t s_wave_L[16];
+    if (lane == 0)
+        s_wave_L[wave] = Lstar;
+    __syncthreads();
+    uint32_t Lblock = kNoLatency;
+    for (uint32_t k = 0; k < wpb; ++k)
+        Lblock = s_wave_L[k] < Lblock ? s_wave_L[k] : Lblock;
+    {
+        // The lowest row r* reaching L*; wave-uniform condition.
+        if (Lstar != kNoLatency && Lstar == Lblock) {
             uint32_t rmin = 0xFFFFFFFFu;
 #pragma unroll
             for (int s = 0; s < S; ++s)
                 if (bestL[s] == Lstar && bestR[s] < rmin)
                     rmin = bestR[s];
             const uint32_t rstar = wave_min_u32(rmin);
-            const uint64_t r = CHUNKED ? (r_begin + rstar) / chunks : r_begin + rstar;
-            const uint32_t j0 = CHUNKED ? (uint32_t)((r_begin + rstar) % chunks) * chunk_len : 0u;
+            const uint64_t r = DYNAMIC ? (r_begin + rstar) / chunks : r_begin + rstar;
+            const uint32_t j0 = DYNAMIC ? (uint32_t)((r_begin + rstar) % chunks) * chunk_len : 0u;
             uint32_t oc;
             int32_t ou;
             outer_sums(R, O, n_outer, r, oc, ou);
-            // Lowest feasible j of row r* reaching L*, for each lane-slot that reaches it there.
+            // Lowest feasible j of row r* reaching L*, for each lane-slot that reaches it there
+            // (its target is the row's minimum c over its feasible j).
             bool need[S];
             uint32_t target[S], jf[S];
             int32_t w[S];
@@ -414,7 +508,7 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
             for (int s = 0; s < S; ++s) {
                 need[s] = bestL[s] == Lstar && bestR[s] == rstar;
                 target[s] = Lstar - c_last[s] - oc;
-                w[s] = u_last[s] + ou;
+                w[s] = need[s] ? u_last[s] + ou : 0x7FFFFFFF;
                 jf[s] = has_inner ? kNoLatency : 0u;
             }
             if (has_inner) {
@@ -426,14 +520,8 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
                     for (int t = 0; t < 16; ++t)
                         v[t] = inner[jb + t];
 #pragma unroll
-                    for (int t = 0; t < 16; ++t) {
-#pragma unroll
-                        for (int s = 0; s < S; ++s) {
-                            const bool hit = need[s] && jf[s] == kNoLatency &&
-                                             (int32_t)v[t].y >= w[s] && v[t].x == target[s];
-                            jf[s] = hit ? jb + t : jf[s];
-                        }
-                    }
+                    for (int t = 0; t < 16; ++t)
+                        masked_find_step(jf, w, target, v[t].y, v[t].x, jb + t, full);
                     bool open = false;
 #pragma unroll
                     for (int s = 0; s < S; ++s)
@@ -778,7 +866,7 @@ static hipError_t launch_lane(const SpaceDev &sp, const QueryDev &q, uint32_t co
         const uint32_t n_outer = sp.M >= 2 ? sp.M - 2 : 0;
 #define ALP_LAUNCH_MIN(NO)                                                                         \
     do {                                                                                           \
-        if (g.chunks > 1)                                                                          \
+        if (g.dynamic)                                                                             \
             hipLaunchKernelGGL(HIP_KERNEL_NAME(scan_min_kernel<S, NO, true>), dim3(nblocks),       \
                                dim3(g.threads), 0, st, rec, inner, q, sp.M, sp.O, g.rows,          \
                                g.rows_per_wave, g.chunks, g.blocks_per_item, nblocks, winners,    \

@@ -337,10 +337,10 @@ pruned_scan_kernel(SpaceDev sp, const Order *__restrict__ orders, uint32_t F1, u
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1)
         total += __shfl_xor((unsigned long long)total, off, 64);
-    if (threadIdx.x != 0)
-        return;
     uint64_t *dst = reinterpret_cast<uint64_t *>(out + item);
     write_result(sp, ext + (uint64_t)item * M * sp.O, L, x, dst);
+    if (threadIdx.x != 0)
+        return;
     dst[6] = total;
     dst[7] = binomial_sat<M - 1>(F + M - 1, M - 1);
 }

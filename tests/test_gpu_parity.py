@@ -82,13 +82,16 @@ def oracle_expect(batch, i, G, lam):
 
 # --------------------------------------------------------------------------------------------
 CASES = load_cases()
+# Scan variants: row-minimum (automatic distribution), thread-per-candidate, exact-tracking lanes,
+# row-minimum with fixed per-wave rows, row-minimum with rows handed out within each block.
+VARIANTS = (1, 2, 3, 4, 5)
 
 
 @pytest.mark.parametrize("case", CASES, ids=[c["id"] for c in CASES])
 def test_hand_cases(alp, case):
     b = case_batch(case)
     with alp.Context(b) as ctx:
-        for variant in (1, 2, 3):
+        for variant in VARIANTS:
             ctx.set_launch(variant)
             for q in case["queries"]:
                 res = ctx.search(0, q["G"], q["lambda"])
@@ -140,11 +143,16 @@ def test_cfg4_batch_matches_golden(alp):
     with alp.Context(b) as ctx:
         tm = ctx.max_throughput([r["G"] for r in rows])
         assert [int(v) for v in tm] == [r["tmax"] for r in rows]
-        out = ctx.search_batch([r["G"] for r in rows], [r["lambda"] for r in rows])
-        bad = [i for i, r in enumerate(rows)
-               if (int(out[i]["index"]), int(out[i]["latency_us"]), int(out[i]["throughput_milli"]),
-                   int(out[i]["gpu_units"])) != (r["x"], r["L"], r["T"], r["U"])]
-        assert not bad, bad[:10]
+        want = [(r["x"], r["L"], r["T"], r["U"]) for r in rows]
+        # automatic launch, then rows handed out within blocks (several blocks per item, split
+        # rows), then fixed per-wave rows with one block per item
+        for launch in [(0, 0, 0, 0), (5, 3, 256, 4), (4, 1, 512, 0)]:
+            ctx.set_launch(*launch)
+            out = ctx.search_batch([r["G"] for r in rows], [r["lambda"] for r in rows])
+            bad = [i for i in range(len(rows))
+                   if (int(out[i]["index"]), int(out[i]["latency_us"]),
+                       int(out[i]["throughput_milli"]), int(out[i]["gpu_units"])) != want[i]]
+            assert not bad, (launch, bad[:10])
 
 
 @pytest.mark.parametrize("cfg,count", [(2, 1_000_000), (3, 10_000_000)])
@@ -175,7 +183,10 @@ def test_launch_geometry_and_variant_do_not_change_results(alp):
                                       (1, 0, 0, 4), (1, 0, 0, 8), (1, 7, 128, 8),
                                       (1, 3000, 1024, 2), (1, 1, 64, 4), (2, 0, 0, 0),
                                       (2, 5, 256, 0), (0, 64, 512, 0), (3, 0, 0, 0),
-                                      (3, 5, 128, 0)]:
+                                      (3, 5, 128, 0), (4, 0, 0, 0), (4, 7, 128, 4),
+                                      (4, 3000, 1024, 0), (5, 0, 0, 0), (5, 1, 64, 0),
+                                      (5, 7, 128, 8), (5, 256, 1024, 4), (5, 3000, 1024, 1),
+                                      (5, 512, 512, 2)]:
             ctx.set_launch(variant, bpi, tpb, ch)
             res = ctx.search(0, g["G"], g["lambda"])
             check_result(b, 0, res, g["x"], g["L"], g["T"], g["U"])
@@ -219,12 +230,12 @@ def test_ragged_and_degenerate_spaces(alp, spec):
             for lam in sorted({1, target_from_tmax(int(b["u_ppm"][i]), t), t, t + 1}):
                 for g in (0, G // 2, G):
                     want = oracle_expect(b, i, g, lam)
-                    for variant in (1, 2, 3):
+                    for variant in VARIANTS:
                         ctx.set_launch(variant)
                         check_result(b, i, ctx.search(i, g, lam), *want)
                     n16 = (inst.O + 15) // 16
-                    for ch in (c for c in range(2, n16 + 1) if n16 % c == 0):
-                        ctx.set_launch(1, 0, 0, ch)
+                    for ch in (c for c in range(1, n16 + 1) if n16 % c == 0):
+                        ctx.set_launch(1 if ch > 1 else 5, 0, 0, ch)
                         check_result(b, i, ctx.search(i, g, lam), *want)
             ctx.set_launch(0)
             xs = np.arange(min(inst.N, 50_000), dtype=np.uint64)
@@ -278,7 +289,7 @@ def test_many_ties_keep_lowest_index(alp, seed):
             for lam in (1, max(1, t // 3), t):
                 want = oracle_expect(b, i, G, lam)
                 assert want[0] is not None
-                for variant in (1, 2, 3):
+                for variant in VARIANTS:
                     ctx.set_launch(variant)
                     check_result(b, i, ctx.search(i, G, lam), *want)
 
