@@ -314,9 +314,12 @@ int32_t alp_set_launch(alp_ctx *ctx, uint32_t variant, uint32_t blocks_per_item,
  * result write (ms[1]); ms[2] is the budget-split kernel of alp_allocate_workflows, 0 after the
  * other searches.  After alp_search_pruned: ms[1] is the fraction enumeration and ms[2] the
  * admissible-option table.  After alp_place: ms[1] is the placement kernel, the others 0.
- * *scan_blocks receives the scan (or enumeration) grid size of the last search. */
+ * *scan_blocks receives the scan (or enumeration) grid size of the last search.
+ * alp_kernel_time_totals writes the sums of those three figures over every call since timing
+ * was last enabled (enabling resets them), so that a caller timing many calls reads them once. */
 int32_t alp_set_timing(alp_ctx *ctx, int32_t enable);
 int32_t alp_kernel_times(alp_ctx *ctx, float ms[3], uint32_t *scan_blocks);
+int32_t alp_kernel_time_totals(alp_ctx *ctx, double ms[3]);
 
 /* Candidates per instance, O^M. */
 int32_t alp_num_candidates(const alp_ctx *ctx, uint64_t *out);

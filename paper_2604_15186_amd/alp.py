@@ -24,7 +24,8 @@ EXPORTS = ("alp_load_profiles", "alp_search", "alp_search_batch", "alp_max_throu
            "alp_allocate_workflows", "alp_search_pruned", "alp_stats_create", "alp_trace_stats",
            "alp_stats_set_timing", "alp_stats_time", "alp_stats_free", "alp_place",
            "alp_eval_candidates",
-           "alp_set_launch", "alp_set_timing", "alp_kernel_times", "alp_num_candidates", "alp_free",
+           "alp_set_launch", "alp_set_timing", "alp_kernel_times", "alp_kernel_time_totals",
+           "alp_num_candidates", "alp_free",
            "alp_status_str", "alp_last_error")
 
 
@@ -92,12 +93,13 @@ def lib():
         L.alp_set_launch.argtypes = [vp, u32, u32, u32, u32]
         L.alp_set_timing.argtypes = [vp, i32]
         L.alp_kernel_times.argtypes = [vp, C.POINTER(C.c_float), C.POINTER(u32)]
+        L.alp_kernel_time_totals.argtypes = [vp, C.POINTER(C.c_double)]
         L.alp_num_candidates.argtypes = [vp, C.POINTER(u64)]
         for name in ("alp_load_profiles", "alp_search", "alp_search_batch", "alp_max_throughput",
                      "alp_allocate_workflows", "alp_search_pruned", "alp_stats_create",
                      "alp_trace_stats", "alp_stats_set_timing", "alp_stats_time", "alp_place",
                      "alp_eval_candidates", "alp_set_launch", "alp_set_timing",
-                     "alp_kernel_times", "alp_num_candidates"):
+                     "alp_kernel_times", "alp_kernel_time_totals", "alp_num_candidates"):
             getattr(L, name).restype = i32
         L.alp_free.argtypes = [vp]
         L.alp_free.restype = None
@@ -272,6 +274,12 @@ class Context:
 
     def set_timing(self, enable: bool):
         _check(lib().alp_set_timing(self._ctx, 1 if enable else 0))
+
+    def kernel_time_totals(self) -> np.ndarray:
+        """Sums of kernel_times()' three figures over every call since timing was enabled."""
+        ms = (C.c_double * 3)()
+        _check(lib().alp_kernel_time_totals(self._ctx, ms))
+        return np.array([ms[0], ms[1], ms[2]])
 
     def kernel_times(self):
         """(option-term ms, scan ms, third-kernel ms, grid blocks) of the last call; the third

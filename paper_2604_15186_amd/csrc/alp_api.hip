@@ -120,6 +120,8 @@ struct alp_ctx {
     int timing = 0;
     hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
     float last_ms[3] = {0, 0, 0};
+    double total_ms[3] = {0, 0, 0};     // sums of last_ms since timing was last enabled
+    void tally(int k) { total_ms[k] += last_ms[k]; }
     uint32_t last_blocks = 0;
 };
 
@@ -472,9 +474,11 @@ int32_t run_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count)
     if ((e = hipStreamSynchronize(c->stream)) != hipSuccess)
         return hip_fail(e, "hipStreamSynchronize");
     if (c->timing) {
-        for (int k = 0; k < 2; ++k)
+        for (int k = 0; k < 2; ++k) {
             if ((e = hipEventElapsedTime(&c->last_ms[k], c->ev[k], c->ev[k + 1])) != hipSuccess)
                 return hip_fail(e, "hipEventElapsedTime");
+            c->tally(k);
+        }
         c->last_ms[2] = 0.0f;
     }
     c->last_blocks = count * g.blocks_per_item;
@@ -756,8 +760,11 @@ int32_t alp_allocate_workflows(alp_ctx *ctx, uint32_t count, const uint32_t *ins
         return hip_fail(e, "hipEventRecord");
     if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess)
         return hip_fail(e, "hipStreamSynchronize");
-    if (ctx->timing && (e = hipEventElapsedTime(&ctx->last_ms[2], ctx->ev[2], ctx->ev[3])) != hipSuccess)
-        return hip_fail(e, "hipEventElapsedTime");
+    if (ctx->timing) {
+        if ((e = hipEventElapsedTime(&ctx->last_ms[2], ctx->ev[2], ctx->ev[3])) != hipSuccess)
+            return hip_fail(e, "hipEventElapsedTime");
+        ctx->tally(2);
+    }
     memcpy(plan, ctx->host_split, sizeof(alp_plan_t));
     if (plan->status != ALP_OK)
         return ALP_INFEASIBLE;
@@ -901,6 +908,8 @@ int32_t alp_search_pruned(alp_ctx *ctx, uint32_t count, const uint32_t *instance
             (e = hipEventElapsedTime(&ctx->last_ms[2], ctx->ev[1], ctx->ev[2])) != hipSuccess ||
             (e = hipEventElapsedTime(&ctx->last_ms[1], ctx->ev[2], ctx->ev[3])) != hipSuccess)
             return hip_fail(e, "hipEventElapsedTime");
+        for (int k = 0; k < 3; ++k)
+            ctx->tally(k);
     }
     ctx->last_blocks = (uint32_t)nblocks;
     memcpy(out, ctx->host_pruned, count * sizeof(alp_pruned_t));
@@ -972,6 +981,7 @@ int32_t alp_place(alp_ctx *ctx, uint32_t count, const alp_result_t *allocations,
         if ((e = hipEventElapsedTime(&ctx->last_ms[1], ctx->ev[1], ctx->ev[2])) != hipSuccess)
             return hip_fail(e, "hipEventElapsedTime");
         ctx->last_ms[0] = ctx->last_ms[2] = 0.0f;
+        ctx->tally(1);
     }
     return ALP_OK;
 }
@@ -1050,7 +1060,19 @@ int32_t alp_set_timing(alp_ctx *ctx, int32_t enable)
 {
     if (!ctx)
         return fail(ALP_EINVAL, "ctx is NULL");
+    if (enable)
+        for (int k = 0; k < 3; ++k)
+            ctx->total_ms[k] = 0.0;
     ctx->timing = enable ? 1 : 0;
+    return ALP_OK;
+}
+
+int32_t alp_kernel_time_totals(alp_ctx *ctx, double ms[3])
+{
+    if (!ctx || !ms)
+        return fail(ALP_EINVAL, "ctx or ms is NULL");
+    for (int k = 0; k < 3; ++k)
+        ms[k] = ctx->total_ms[k];
     return ALP_OK;
 }
 

@@ -92,3 +92,21 @@ def test_statistics_on_a_caller_stream(alp):
         with torch.cuda.stream(s):
             b = c1.compute(tr["M"], tr["offsets"], tr["llm"], tr["start"], tr["end"])
         assert a.tobytes() == b.tobytes()
+
+
+def test_kernel_time_totals_sum_the_calls(alp):
+    b = make_batch(1, range(2))
+    G, lam, _ = _queries(alp, b)
+    with alp.Context(b) as ctx:
+        ctx.set_timing(True)
+        per_call = np.zeros(3)
+        for _ in range(5):
+            ctx.search(0, int(G[0]), int(lam[0]))
+            per_call += np.asarray(ctx.kernel_times()[:3], dtype=np.float64)
+        tot = ctx.kernel_time_totals()
+        assert tot[1] > 0 and np.allclose(tot, per_call, rtol=1e-6, atol=1e-9)
+        ctx.set_timing(True)                           # enabling again starts new sums
+        assert (ctx.kernel_time_totals() == 0).all()
+        ctx.set_timing(False)
+        ctx.search(0, int(G[0]), int(lam[0]))          # untimed calls add nothing
+        assert (ctx.kernel_time_totals() == 0).all()
