@@ -22,6 +22,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "alp_internal.h"
 
 namespace alp {
@@ -63,27 +65,58 @@ __device__ __forceinline__ uint64_t block_exclusive_max(uint64_t v)
     return excl;
 }
 
-// Block-wide minimum and maximum of 64-bit values (every thread gets both).
-__device__ __forceinline__ void block_min_max(uint64_t &lo, uint64_t &hi)
+// The 32-bit value of lane (lane ^ Q), Q a power of two below 64: DPP quad permutations for 1
+// and 2, a swizzle within 32 lanes for 4..16, a lane permute for 32.
+template <int Q>
+__device__ __forceinline__ uint32_t lane_xor(uint32_t v)
+{
+    if constexpr (Q == 1)
+        return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false);
+    else if constexpr (Q == 2)
+        return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false);
+    else if constexpr (Q < 32)
+        return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, 0x1F | (Q << 10));
+    else
+        return (uint32_t)__builtin_amdgcn_ds_bpermute((int)((threadIdx.x ^ 32u) << 2), (int)v);
+}
+
+template <int Q>
+__device__ __forceinline__ uint64_t lane_xor64(uint64_t v)
+{
+    return (uint64_t)lane_xor<Q>((uint32_t)v) | ((uint64_t)lane_xor<Q>((uint32_t)(v >> 32)) << 32);
+}
+
+// Block-wide minimum and maximum of 64-bit values and sum of 32-bit counts (every thread gets
+// all three): butterflies within each wave, then the four waves' results through LDS.
+__device__ __forceinline__ void block_min_max_sum(uint64_t &lo, uint64_t &hi, uint32_t &cnt)
 {
     __shared__ uint64_t s_lo[kThreads / 64], s_hi[kThreads / 64];
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-        const uint64_t a = __shfl_xor((unsigned long long)lo, off, 64);
-        const uint64_t b = __shfl_xor((unsigned long long)hi, off, 64);
+    __shared__ uint32_t s_cnt[kThreads / 64];
+    auto step = [&](auto q_const) {
+        constexpr int Q = decltype(q_const)::value;
+        const uint64_t a = lane_xor64<Q>(lo), b = lane_xor64<Q>(hi);
         lo = a < lo ? a : lo;
         hi = b > hi ? b : hi;
-    }
+        cnt += lane_xor<Q>(cnt);
+    };
+    step(std::integral_constant<int, 32>{});
+    step(std::integral_constant<int, 16>{});
+    step(std::integral_constant<int, 8>{});
+    step(std::integral_constant<int, 4>{});
+    step(std::integral_constant<int, 2>{});
+    step(std::integral_constant<int, 1>{});
     if ((threadIdx.x & 63) == 0) {
         s_lo[threadIdx.x >> 6] = lo;
         s_hi[threadIdx.x >> 6] = hi;
+        s_cnt[threadIdx.x >> 6] = cnt;
     }
     __syncthreads();
+    cnt = 0;
     for (uint32_t w = 0; w < kThreads / 64; ++w) {
         lo = s_lo[w] < lo ? s_lo[w] : lo;
         hi = s_hi[w] > hi ? s_hi[w] : hi;
+        cnt += s_cnt[w];
     }
-    __syncthreads();
 }
 
 // Bitonic sort of P (a power of two) entries in place, ascending by key then val when val is
@@ -116,6 +149,139 @@ __device__ __forceinline__ void bitonic_sort(uint64_t *key, uint64_t *val, uint3
             }
             __syncthreads();
         }
+    }
+}
+
+// One compare-exchange of the bitonic network seen from one side: keep the minimum (else the
+// maximum) of the own and the partner's key.
+__device__ __forceinline__ uint64_t keep_one(uint64_t mine, uint64_t other, bool keep_min)
+{
+    const bool take = keep_min ? other < mine : other > mine;
+    return take ? other : mine;
+}
+
+// Position i is the pair's lower index iff bit `stride` of i is clear, and lies in a run of
+// `size` sorted ascending iff bit `size` of i is clear; the lower index of an ascending pair,
+// or the upper of a descending one, keeps the minimum.
+__device__ __forceinline__ bool keeps_min(uint32_t i, uint32_t stride, uint32_t size)
+{
+    return ((i & stride) == 0) == ((i & size) == 0);
+}
+
+// Exchanges with partner lane (lane ^ Q) for stride Q * E, if that stride occurs in this run.
+template <int E, int Q>
+__device__ __forceinline__ void lane_stage(uint64_t (&k)[E], uint32_t size)
+{
+    constexpr uint32_t stride = (uint32_t)(Q * E);
+    if (2 * stride > size)
+        return;
+    const bool km = keeps_min(threadIdx.x * E, stride, size);   // the same for all E slots
+#pragma unroll
+    for (int e = 0; e < E; ++e)
+        k[e] = keep_one(k[e], lane_xor64<Q>(k[e]), km);
+}
+
+// Bitonic sort of P = 256 E keys held E per thread in registers, ascending by position: thread
+// t holds positions t E .. t E + E - 1.  An exchange whose partner is in the same thread runs
+// in registers, one whose partner is in the same wave by cross-lane moves (lane ^ stride / E),
+// and only those whose partner is in another wave go through LDS, in a layout (slot e of
+// thread t at e * 256 + t) where a wave's 64 accesses are consecutive; two LDS buffers
+// alternate, so each such exchange needs one barrier.  buf holds 2 P keys.
+template <int E>
+__device__ __forceinline__ void bitonic_sort_regs(uint64_t (&k)[E], uint64_t *buf, uint32_t P)
+{
+    const uint32_t t = threadIdx.x;
+    uint32_t flip = 0;
+    for (uint32_t size = 2; size <= P; size <<= 1) {
+        for (uint32_t stride = size >> 1; stride >= (uint32_t)E * 64; stride >>= 1) {
+            uint64_t *b = buf + flip * P;
+            flip ^= 1u;
+#pragma unroll
+            for (int e = 0; e < E; ++e)
+                b[e * kThreads + t] = k[e];
+            __syncthreads();
+            const uint32_t pt = t ^ (stride / E);
+            const bool km = keeps_min(t * E, stride, size);
+#pragma unroll
+            for (int e = 0; e < E; ++e)
+                k[e] = keep_one(k[e], b[e * kThreads + pt], km);
+        }
+        lane_stage<E, 32>(k, size);
+        lane_stage<E, 16>(k, size);
+        lane_stage<E, 8>(k, size);
+        lane_stage<E, 4>(k, size);
+        lane_stage<E, 2>(k, size);
+        lane_stage<E, 1>(k, size);
+#pragma unroll
+        for (int st = E / 2; st >= 1; st >>= 1) {
+            if ((uint32_t)(2 * st) > size)
+                continue;
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                if (e & st)
+                    continue;
+                const uint64_t a = k[e], b = k[e | st];
+                const bool asc = ((t * E + e) & size) == 0;
+                const bool swap = asc ? a > b : a < b;
+                k[e] = swap ? b : a;
+                k[e | st] = swap ? a : b;
+            }
+        }
+    }
+}
+
+// The sweep below for keys held as bitonic_sort_regs leaves them: thread t's chunk is its own
+// E registers.  Packed key: (llm << 61 | start - smin << 32 | duration).
+template <int E>
+__device__ __forceinline__ void sweep_regs(const uint64_t (&k)[E], uint32_t valid, uint64_t smin,
+                                           unsigned long long *s_sum)
+{
+    const uint32_t base = threadIdx.x * E;
+    uint32_t m[E];
+    uint64_t s[E], e[E];
+    uint64_t run = 0;
+#pragma unroll
+    for (int j = 0; j < E; ++j) {
+        m[j] = (uint32_t)(k[j] >> 61);
+        s[j] = smin + ((k[j] >> 32) & ((1ull << 29) - 1));
+        e[j] = s[j] + (k[j] & 0xFFFFFFFFull);
+        if (base + j < valid) {
+            const uint64_t pk = ((uint64_t)m[j] << 61) | e[j];
+            run = pk > run ? pk : run;
+        }
+    }
+    uint64_t prev = block_exclusive_max(run);
+    constexpr uint64_t kLow61 = (1ull << 61) - 1;
+    uint32_t cur = ~0u;
+    uint64_t c_calls = 0, c_busy = 0, c_active = 0;
+#pragma unroll
+    for (int j = 0; j < E; ++j) {
+        if (base + j >= valid)
+            break;
+        if (m[j] != cur) {
+            if (cur != ~0u) {
+                atomicAdd(&s_sum[3 * cur + 0], (unsigned long long)c_calls);
+                atomicAdd(&s_sum[3 * cur + 1], (unsigned long long)c_busy);
+                atomicAdd(&s_sum[3 * cur + 2], (unsigned long long)c_active);
+            }
+            c_calls = c_busy = c_active = 0;
+            cur = m[j];
+        }
+        uint64_t from = s[j];
+        if ((prev >> 61) == m[j]) {
+            const uint64_t reach = prev & kLow61;
+            from = reach > s[j] ? reach : s[j];
+        }
+        c_calls += 1;
+        c_busy += e[j] - s[j];
+        c_active += e[j] > from ? e[j] - from : 0;
+        const uint64_t pk = ((uint64_t)m[j] << 61) | e[j];
+        prev = pk > prev ? pk : prev;
+    }
+    if (cur != ~0u) {
+        atomicAdd(&s_sum[3 * cur + 0], (unsigned long long)c_calls);
+        atomicAdd(&s_sum[3 * cur + 1], (unsigned long long)c_busy);
+        atomicAdd(&s_sum[3 * cur + 2], (unsigned long long)c_active);
     }
 }
 
@@ -238,27 +404,33 @@ trace_stats_kernel(uint32_t M, const uint64_t *__restrict__ offsets,
         }
         if (bad)
             atomicOr(flags, bad);
-        atomicAdd(&s_valid, valid);
-        block_min_max(smin, smax);                      // includes the barriers s_valid needs
-        const uint32_t nvalid = s_valid;
+        uint32_t nvalid = valid;
+        block_min_max_sum(smin, smax, nvalid);
         if (nvalid == 0)
             return;
         if (smax - smin < (1ull << 29)) {
+            // The thread's loaded calls k < P / 256 become its E sort positions (any placement
+            // of the inputs sorts the same); padding sorts last.
+            uint64_t pk[kMaxPerThread];
 #pragma unroll
-            for (uint32_t k = 0; k < kMaxPerThread; ++k) {
-                const uint32_t i = threadIdx.x + k * kThreads;
-                if (i < P)
-                    key[i] = ok[k] ? ((uint64_t)rm[k] << 61) | ((rs[k] - smin) << 32) | (re[k] - rs[k])
-                                   : kPad;
+            for (uint32_t k = 0; k < kMaxPerThread; ++k)
+                pk[k] = ok[k] ? ((uint64_t)rm[k] << 61) | ((rs[k] - smin) << 32) | (re[k] - rs[k])
+                              : kPad;
+            auto run = [&](auto e_const) {
+                constexpr int E = decltype(e_const)::value;
+                uint64_t kk[E];
+#pragma unroll
+                for (int j = 0; j < E; ++j)
+                    kk[j] = pk[j];
+                bitonic_sort_regs<E>(kk, key, P);
+                sweep_regs<E>(kk, nvalid, smin, s_sum);
+            };
+            switch (P) {
+            case kThreads: run(std::integral_constant<int, 1>{}); break;
+            case 2 * kThreads: run(std::integral_constant<int, 2>{}); break;
+            case 4 * kThreads: run(std::integral_constant<int, 4>{}); break;
+            default: run(std::integral_constant<int, 8>{}); break;
             }
-            __syncthreads();
-            bitonic_sort<false>(key, nullptr, P);
-            sweep(P, nvalid, [&](uint32_t i, uint32_t &m, uint64_t &s, uint64_t &e) {
-                const uint64_t kk = key[i];
-                m = (uint32_t)(kk >> 61);
-                s = smin + ((kk >> 32) & ((1ull << 29) - 1));
-                e = s + (kk & 0xFFFFFFFFull);
-            }, s_sum);
         } else {
 #pragma unroll
             for (uint32_t k = 0; k < kMaxPerThread; ++k) {
