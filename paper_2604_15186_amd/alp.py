@@ -125,8 +125,10 @@ def _check(status: int, allowed=(ALP_OK,)) -> int:
     return status
 
 
-def _ptr(a: np.ndarray):
-    return a.ctypes.data_as(C.c_void_p)
+def _ptr(a: np.ndarray) -> int:
+    # The address as an int (ctypes converts it for c_void_p arguments); data_as() costs several
+    # microseconds per call, which a single small search can notice.
+    return a.ctypes.data
 
 
 def space_struct(space: dict) -> Space:

@@ -119,3 +119,28 @@ def test_malformed_input_is_rejected(ctx):
         ctx.compute(9, off, llm, s, e_)
     # the context still works after rejected calls
     _same(ctx, 1, off, llm, s, e_)
+
+
+def test_every_sort_size_and_input_order(ctx):
+    """Trace lengths at each power-of-two boundary of the in-register sort (256, 512, 1,024 and
+    2,048 slots per workgroup), in sorted, reversed, constant and random order, with repeated
+    keys and all 8 LLM indices."""
+    rng = np.random.default_rng(23)
+    traces = []
+    for n in (1, 2, 255, 256, 257, 511, 512, 513, 1023, 1024, 1025, 2047, 2048):
+        m = rng.integers(0, 8, n)
+        s = rng.integers(0, 1 << 20, n)
+        s[: n // 4] = s[0]                               # repeated starts
+        d = rng.integers(0, 30_000, n)
+        for order in ("random", "sorted", "reversed", "constant"):
+            if order == "sorted":
+                idx = np.lexsort((s, m))
+            elif order == "reversed":
+                idx = np.lexsort((s, m))[::-1]
+            else:
+                idx = rng.permutation(n)
+            mm, ss, dd = m[idx], s[idx], d[idx]
+            if order == "constant":
+                mm, ss, dd = np.full(n, 3), np.full(n, 777), np.full(n, 5)
+            traces.append([(int(a), int(b), int(b + c)) for a, b, c in zip(mm, ss, dd)])
+    _same(ctx, 8, *_pack(traces))
