@@ -144,6 +144,22 @@ int32_t alp_search_batch(alp_ctx *ctx, uint32_t count, const uint32_t *instances
                          const uint32_t *gpu_budget, const uint32_t *target_milli,
                          alp_result_t *out);
 
+/* Batched searches with the queries and the results in device memory, queued on the context's
+ * HIP stream without waiting (Section 5, the same search as alp_search_batch).  instances
+ * (NULL = 0..count-1), gpu_budget and target_milli are device arrays of count entries; out is a
+ * device array of count records.  The call returns once the work is queued: the inputs must
+ * stay unchanged, and out is complete, only when the stream has reached the end of this work
+ * (synchronise the stream, or order later work after it on the same stream).  A query whose
+ * instance is out of range gets status ALP_EINVAL in its record and does not affect the others;
+ * the other records are as alp_search_batch writes them.  Returns ALP_EINVAL for a NULL ctx or
+ * array (instances aside), or the first error in queuing the work.  alp_kernel_times is not
+ * updated by this call.  Successive calls on one context, and calls of the synchronous
+ * functions after it, are ordered by the stream; a call that needs larger scratch buffers than
+ * earlier ones first waits for the stream. */
+int32_t alp_search_batch_async(alp_ctx *ctx, uint32_t count, const uint32_t *instances,
+                               const uint32_t *gpu_budget, const uint32_t *target_milli,
+                               alp_result_t *out);
+
 /* Largest workflow throughput T_w (Eq. 2) any candidate with deployable, fitting options
  * reaches within the budget, ignoring the target; 0 if none fits.  A target above it is
  * infeasible, a target at or below it is feasible.  instances may be NULL. */

@@ -20,9 +20,9 @@ NO_LATENCY = (1 << 32) - 1
 MAX_LLMS = 8
 
 # Symbols declared in include/alp.h.
-EXPORTS = ("alp_load_profiles", "alp_search", "alp_search_batch", "alp_max_throughput",
-           "alp_allocate_workflows", "alp_search_pruned", "alp_stats_create", "alp_trace_stats",
-           "alp_stats_set_timing", "alp_stats_time", "alp_stats_free", "alp_place",
+EXPORTS = ("alp_load_profiles", "alp_search", "alp_search_batch", "alp_search_batch_async",
+           "alp_max_throughput", "alp_allocate_workflows", "alp_search_pruned", "alp_stats_create",
+           "alp_trace_stats", "alp_stats_set_timing", "alp_stats_time", "alp_stats_free", "alp_place",
            "alp_eval_candidates",
            "alp_set_launch", "alp_set_timing", "alp_kernel_times", "alp_kernel_time_totals",
            "alp_num_candidates", "alp_free",
@@ -79,6 +79,7 @@ def lib():
                                         vp, u64, i32, vp]
         L.alp_search.argtypes = [vp, u32, u32, u32, vp]
         L.alp_search_batch.argtypes = [vp, u32, vp, vp, vp, vp]
+        L.alp_search_batch_async.argtypes = [vp, u32, vp, vp, vp, vp]
         L.alp_max_throughput.argtypes = [vp, u32, vp, vp, vp]
         L.alp_eval_candidates.argtypes = [vp, u32, u32, u32, vp, u64, vp]
         L.alp_allocate_workflows.argtypes = [vp, u32, vp, vp, u32, u32, vp, vp, vp]
@@ -95,7 +96,8 @@ def lib():
         L.alp_kernel_times.argtypes = [vp, C.POINTER(C.c_float), C.POINTER(u32)]
         L.alp_kernel_time_totals.argtypes = [vp, C.POINTER(C.c_double)]
         L.alp_num_candidates.argtypes = [vp, C.POINTER(u64)]
-        for name in ("alp_load_profiles", "alp_search", "alp_search_batch", "alp_max_throughput",
+        for name in ("alp_load_profiles", "alp_search", "alp_search_batch",
+                     "alp_search_batch_async", "alp_max_throughput",
                      "alp_allocate_workflows", "alp_search_pruned", "alp_stats_create",
                      "alp_trace_stats", "alp_stats_set_timing", "alp_stats_time", "alp_place",
                      "alp_eval_candidates", "alp_set_launch", "alp_set_timing",
@@ -215,6 +217,25 @@ class Context:
         _check(lib().alp_search_batch(self._ctx, count, None if inst is None else _ptr(inst),
                                       _ptr(G), _ptr(lam), _ptr(out)))
         return out
+
+    def search_batch_async(self, gpu_budget, target_milli, out, instances=None) -> None:
+        """alp_search_batch_async: torch tensors on the context's device -- gpu_budget,
+        target_milli (and instances) of int32 or uint32, out of uint8 with count * 48 bytes.
+        Queued on the context stream; read out after that stream's work is done (see
+        results_from_device)."""
+        count = int(gpu_budget.numel())
+        tensors = [gpu_budget, target_milli] + ([] if instances is None else [instances])
+        for t in tensors:
+            if not t.is_cuda or not t.is_contiguous() or t.element_size() != 4 or t.numel() != count:
+                raise ValueError("queries must be contiguous 32-bit device tensors of one length")
+        if not out.is_cuda or not out.is_contiguous() or out.numel() * out.element_size() < \
+                count * RESULT_DTYPE.itemsize:
+            raise ValueError(f"out must be a contiguous device tensor of {count} x "
+                             f"{RESULT_DTYPE.itemsize} bytes")
+        _check(lib().alp_search_batch_async(self._ctx, count,
+                                            None if instances is None else instances.data_ptr(),
+                                            gpu_budget.data_ptr(), target_milli.data_ptr(),
+                                            out.data_ptr()))
 
     def max_throughput(self, gpu_budget, instances=None) -> np.ndarray:
         G = np.ascontiguousarray(gpu_budget, dtype=np.uint32)
@@ -347,6 +368,14 @@ class StatsContext:
 
     def __exit__(self, *exc):
         self.close()
+
+
+def results_from_device(out, count: int) -> np.ndarray:
+    """The first count records of a device tensor written by search_batch_async (copies to the
+    host; call after the stream's work is done)."""
+    import torch
+    raw = out.reshape(-1).view(torch.uint8)[: count * RESULT_DTYPE.itemsize]
+    return raw.cpu().numpy().view(RESULT_DTYPE).copy()
 
 
 def result_dict(r) -> dict:

@@ -41,11 +41,19 @@ int32_t hip_fail(hipError_t e, const char *what)
 struct DevBuf {
     void *ptr = nullptr;
     size_t cap = 0;
+    bool guarded = false;           // work that may still use the buffer is queued on `stream`
+    hipStream_t stream = nullptr;
     hipError_t ensure(size_t bytes)
     {
         if (bytes <= cap)
             return hipSuccess;
         if (ptr) {
+            // Queued asynchronous searches may still read or write the old buffer.
+            if (guarded) {
+                hipError_t e = hipStreamSynchronize(stream);
+                if (e != hipSuccess)
+                    return e;
+            }
             hipError_t e = hipFree(ptr);
             ptr = nullptr;
             cap = 0;
@@ -429,7 +437,11 @@ int32_t ensure_host_results(alp_ctx *c, size_t count)
 
 // Runs option terms -> scan (with the fused final reduction) for `count` items described by q;
 // the kernels write the results straight into c->host_results[0..count) (mapped pinned memory).
-int32_t run_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count)
+// Queues the option-term and scan kernels of `count` searches on the context stream.  Results go
+// to `out` (device-visible), rejected queries (invalid != nullptr) to EINVAL records.  With
+// `timed`, HIP events bracket the two kernels (read by run_search after synchronising).
+int32_t launch_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count, alp_result_t *out,
+                      const uint32_t *invalid, bool timed)
 {
     const alp::SpaceDev &sp = c->sp;
     const alp::ScanGeometry g = plan_scan(c, count);
@@ -449,9 +461,6 @@ int32_t run_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count)
         return hip_fail(e, "hipMalloc(done)");
     if ((e = c->winners.ensure(nwin * sizeof(alp::Winner))) != hipSuccess)
         return hip_fail(e, "hipMalloc(winners)");
-    int32_t st = ensure_host_results(c, count);
-    if (st != ALP_OK)
-        return st;
 
     uint2 *rec = (uint2 *)c->rec.ptr, *ext = (uint2 *)c->ext.ptr, *inner = (uint2 *)c->inner.ptr;
     alp::Winner *win = (alp::Winner *)c->winners.ptr;
@@ -459,18 +468,32 @@ int32_t run_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count)
     fa.sp = sp;
     fa.ext = ext;
     fa.done = (uint32_t *)c->done.ptr;
-    fa.out = c->host_results_dev;
-    if (c->timing && (e = hipEventRecord(c->ev[0], c->stream)) != hipSuccess)
+    fa.out = out;
+    fa.invalid = invalid;
+    if (timed && (e = hipEventRecord(c->ev[0], c->stream)) != hipSuccess)
         return hip_fail(e, "hipEventRecord");
     if ((e = alp::launch_option_terms(sp, c->tdev, q, count, rec, ext, inner, fa.done, c->stream)) !=
         hipSuccess)
         return hip_fail(e, "option_terms launch");
-    if (c->timing && (e = hipEventRecord(c->ev[1], c->stream)) != hipSuccess)
+    if (timed && (e = hipEventRecord(c->ev[1], c->stream)) != hipSuccess)
         return hip_fail(e, "hipEventRecord");
     if ((e = alp::launch_scan(sp, q, count, rec, inner, g, win, fa, c->stream)) != hipSuccess)
         return hip_fail(e, "scan launch");
-    if (c->timing && (e = hipEventRecord(c->ev[2], c->stream)) != hipSuccess)
+    if (timed && (e = hipEventRecord(c->ev[2], c->stream)) != hipSuccess)
         return hip_fail(e, "hipEventRecord");
+    c->last_blocks = count * g.blocks_per_item;
+    return ALP_OK;
+}
+
+// Synchronous searches: results in the context's mapped host buffer.
+int32_t run_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count)
+{
+    int32_t st = ensure_host_results(c, count);
+    if (st != ALP_OK)
+        return st;
+    if ((st = launch_search(c, q, count, c->host_results_dev, nullptr, c->timing != 0)) != ALP_OK)
+        return st;
+    hipError_t e;
     if ((e = hipStreamSynchronize(c->stream)) != hipSuccess)
         return hip_fail(e, "hipStreamSynchronize");
     if (c->timing) {
@@ -481,7 +504,6 @@ int32_t run_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count)
         }
         c->last_ms[2] = 0.0f;
     }
-    c->last_blocks = count * g.blocks_per_item;
     return ALP_OK;
 }
 
@@ -531,6 +553,10 @@ int32_t alp_load_profiles(alp_ctx **out, const alp_space_t *space, uint32_t num_
         return fail(ALP_ENOMEM, "host allocation failed");
     c->device = device;
     c->stream = (hipStream_t)hip_stream;
+    for (DevBuf *b : {&c->q_inst, &c->rec, &c->ext, &c->inner, &c->done, &c->winners}) {
+        b->guarded = true;                              // used by alp_search_batch_async
+        b->stream = c->stream;
+    }
     c->space = *space;
     c->N = N;
     c->B = num_instances;
@@ -651,6 +677,36 @@ int32_t alp_search_batch(alp_ctx *ctx, uint32_t count, const uint32_t *instances
         return st;
     memcpy(out, ctx->host_results, (size_t)count * sizeof(alp_result_t));
     return ALP_OK;
+}
+
+int32_t alp_search_batch_async(alp_ctx *ctx, uint32_t count, const uint32_t *instances,
+                               const uint32_t *gpu_budget, const uint32_t *target_milli,
+                               alp_result_t *out)
+{
+    if (!ctx)
+        return fail(ALP_EINVAL, "ctx is NULL");
+    if (count == 0)
+        return ALP_OK;
+    if (!gpu_budget || !target_milli || !out)
+        return fail(ALP_EINVAL, "gpu_budget, target_milli or out is NULL");
+    DeviceGuard guard(ctx->device);
+    if (guard.status != hipSuccess)
+        return hip_fail(guard.status, "hipSetDevice");
+    hipError_t e;
+    // q_inst holds inst | cap | lambda, then the per-item rejection flags.
+    const size_t bytes = (size_t)count * sizeof(uint32_t);
+    if ((e = ctx->q_inst.ensure(4 * bytes)) != hipSuccess)
+        return hip_fail(e, "hipMalloc(queries)");
+    uint32_t *qi = (uint32_t *)ctx->q_inst.ptr;
+    if ((e = alp::launch_prepare_queries(count, ctx->B, ctx->space.units_per_gpu, instances,
+                                         gpu_budget, target_milli, qi, qi + count, qi + 2 * count,
+                                         qi + 3 * count, ctx->stream)) != hipSuccess)
+        return hip_fail(e, "prepare_queries launch");
+    alp::QueryDev q{};
+    q.inst = qi;
+    q.capacity = qi + count;
+    q.lambda = qi + 2 * (size_t)count;
+    return launch_search(ctx, q, count, out, qi + 3 * count, false);
 }
 
 int32_t alp_max_throughput(alp_ctx *ctx, uint32_t count, const uint32_t *instances,

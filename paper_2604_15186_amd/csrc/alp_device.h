@@ -118,7 +118,8 @@ __device__ __forceinline__ void item_winner(uint32_t item, uint32_t blocks_per_i
 // digit and loads its record (one memory round trip for all LLMs), the wave combines them, and
 // lane 0 writes.
 __device__ __forceinline__ void write_result(const SpaceDev &sp, const uint2 *E, uint32_t L,
-                                             uint64_t x, uint64_t *dst)
+                                             uint64_t x, uint64_t *dst,
+                                             uint32_t status_if_none = ALP_INFEASIBLE)
 {
     const uint32_t lane = threadIdx.x & 63;
     uint32_t T = 0xFFFFFFFFu, U = 0;
@@ -152,7 +153,7 @@ __device__ __forceinline__ void write_result(const SpaceDev &sp, const uint2 *E,
     if (L == kNoLatency) {
         dst[0] = ALP_NO_INDEX;
         dst[1] = 0;
-        dst[2] = (uint64_t)ALP_INFEASIBLE << 32;
+        dst[2] = (uint64_t)status_if_none << 32;
         dst[3] = 0;
         dst[4] = 0;
         dst[5] = 0;
@@ -173,8 +174,10 @@ __device__ __forceinline__ void finish_item(const FinishArgs &fa, uint32_t item,
     uint32_t L;
     uint64_t x;
     item_winner(item, blocks_per_item, winners, L, x);
-    write_result(fa.sp, fa.ext + (uint64_t)item * fa.sp.M * fa.sp.O, L, x,
-                 reinterpret_cast<uint64_t *>(fa.out + item));
+    const bool rejected = fa.invalid && fa.invalid[item];
+    write_result(fa.sp, fa.ext + (uint64_t)item * fa.sp.M * fa.sp.O, rejected ? kNoLatency : L, x,
+                 reinterpret_cast<uint64_t *>(fa.out + item),
+                 rejected ? (uint32_t)ALP_EINVAL : (uint32_t)ALP_INFEASIBLE);
 }
 
 // Writes the block's winner and counts the block as finished (agent-scope fence and per-item

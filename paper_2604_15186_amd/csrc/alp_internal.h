@@ -68,6 +68,8 @@ struct FinishArgs {
     const uint2 *ext;          // per-option (tau, u | flags) of the query
     uint32_t *done;            // per-item finished-block counter, zeroed by the option-term kernel
     alp_result_t *out;         // per-item results (device-visible, may be mapped host memory)
+    const uint32_t *invalid;   // per-item: nonzero = the query was rejected (result EINVAL);
+                               // nullptr = every query valid
 };
 
 // Launch geometry of one scan.
@@ -84,6 +86,14 @@ struct ScanGeometry {
     uint64_t per_thread;       // variant 2: candidates per thread
     uint32_t slots;            // variants 1, 3: options of the last LLM per lane (1, 2, 4, 8)
 };
+
+// Device-side query preparation for searches whose queries are in device memory: instance
+// (or the item index when inst is nullptr; an instance >= B is rejected and searched as 0),
+// share-unit capacity min(units_per_gpu * budget, kCapacityMax), target.
+hipError_t launch_prepare_queries(uint32_t count, uint32_t B, uint32_t units_per_gpu,
+                                  const uint32_t *inst, const uint32_t *budget,
+                                  const uint32_t *target, uint32_t *q_inst, uint32_t *q_cap,
+                                  uint32_t *q_lambda, uint32_t *invalid, hipStream_t st);
 
 hipError_t launch_option_terms(const SpaceDev &sp, const TablesDev &tb, const QueryDev &q,
                                uint32_t count, uint2 *rec, uint2 *ext, uint2 *inner, uint32_t *done,

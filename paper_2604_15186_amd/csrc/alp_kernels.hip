@@ -839,6 +839,41 @@ tmax_kernel(SpaceDev sp, QueryDev q, const uint2 *__restrict__ ext, uint32_t *__
 // ---------------------------------------------------------------------------------------------
 // Launchers.
 
+namespace {
+
+__global__ void __launch_bounds__(256)
+prepare_queries_kernel(uint32_t count, uint32_t B, uint32_t units_per_gpu,
+                       const uint32_t *__restrict__ inst, const uint32_t *__restrict__ budget,
+                       const uint32_t *__restrict__ target, uint32_t *__restrict__ q_inst,
+                       uint32_t *__restrict__ q_cap, uint32_t *__restrict__ q_lambda,
+                       uint32_t *__restrict__ invalid)
+{
+    const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= count)
+        return;
+    const uint32_t b = inst ? inst[i] : i;
+    const bool bad = b >= B;
+    q_inst[i] = bad ? 0u : b;
+    const uint64_t cap = (uint64_t)units_per_gpu * budget[i];
+    q_cap[i] = cap > kCapacityMax ? kCapacityMax : (uint32_t)cap;
+    q_lambda[i] = target[i];
+    invalid[i] = bad ? 1u : 0u;
+}
+
+}  // namespace
+
+hipError_t launch_prepare_queries(uint32_t count, uint32_t B, uint32_t units_per_gpu,
+                                  const uint32_t *inst, const uint32_t *budget,
+                                  const uint32_t *target, uint32_t *q_inst, uint32_t *q_cap,
+                                  uint32_t *q_lambda, uint32_t *invalid, hipStream_t st)
+{
+    if (count == 0)
+        return hipSuccess;
+    hipLaunchKernelGGL(prepare_queries_kernel, dim3((count + 255) / 256), dim3(256), 0, st, count,
+                       B, units_per_gpu, inst, budget, target, q_inst, q_cap, q_lambda, invalid);
+    return hipGetLastError();
+}
+
 hipError_t launch_option_terms(const SpaceDev &sp, const TablesDev &tb, const QueryDev &q,
                                uint32_t count, uint2 *rec, uint2 *ext, uint2 *inner, uint32_t *done,
                                hipStream_t st)

@@ -167,6 +167,7 @@ def test_null_arguments_rejected():
     out = np.zeros(1, alp.RESULT_DTYPE)
     assert lib.alp_search(None, 0, 1, 1, out.ctypes.data_as(C.c_void_p)) == alp.ALP_EINVAL
     assert lib.alp_search_batch(None, 1, None, None, None, None) == alp.ALP_EINVAL
+    assert lib.alp_search_batch_async(None, 1, None, None, None, None) == alp.ALP_EINVAL
     assert lib.alp_set_launch(None, 0, 0, 0, 0) == alp.ALP_EINVAL
     assert lib.alp_kernel_time_totals(None, (C.c_double * 3)()) == alp.ALP_EINVAL
     assert lib.alp_search_pruned(None, 1, None, None, None, 3, None) == alp.ALP_EINVAL

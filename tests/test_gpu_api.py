@@ -110,3 +110,57 @@ def test_kernel_time_totals_sum_the_calls(alp):
         ctx.set_timing(False)
         ctx.search(0, int(G[0]), int(lam[0]))          # untimed calls add nothing
         assert (ctx.kernel_time_totals() == 0).all()
+
+
+def test_async_batch_matches_the_synchronous_batch(alp):
+    import torch
+    b = make_batch(4, range(64))
+    G, lam, ref = _queries(alp, b)
+    dev = torch.device("cuda", 0)
+    s = torch.cuda.Stream()
+    with alp.Context(b, stream=s.cuda_stream) as ctx:
+        Gd = torch.from_numpy(G.view(np.int32)).to(dev)
+        Ld = torch.from_numpy(lam.view(np.int32)).to(dev)
+        torch.cuda.synchronize()
+        outs = []
+        # several calls queued back to back on the context stream, one wait at the end
+        for k in range(3):
+            o = torch.empty(len(G) * alp.RESULT_DTYPE.itemsize, dtype=torch.uint8, device=dev)
+            ctx.search_batch_async(Gd, Ld, o)
+            outs.append(o)
+        s.synchronize()
+        for o in outs:
+            assert alp.results_from_device(o, len(G)).tobytes() == ref.tobytes()
+        # then a synchronous search on the same context is ordered after them
+        assert ctx.search(3, int(G[3]), int(lam[3])).tobytes() == ref[3].tobytes()
+
+
+def test_async_batch_rejects_bad_instances_per_record(alp):
+    import torch
+    b = make_batch(1, range(4))
+    G, lam, ref = _queries(alp, b)
+    dev = torch.device("cuda", 0)
+    with alp.Context(b) as ctx:
+        inst = np.array([0, 1, 7, 3], dtype=np.uint32)           # 7: only 4 instances loaded
+        o = torch.empty(4 * alp.RESULT_DTYPE.itemsize, dtype=torch.uint8, device=dev)
+        ctx.search_batch_async(torch.from_numpy(G.view(np.int32)).to(dev),
+                               torch.from_numpy(lam.view(np.int32)).to(dev), o,
+                               instances=torch.from_numpy(inst.view(np.int32)).to(dev))
+        torch.cuda.synchronize()
+        got = alp.results_from_device(o, 4)
+        assert got[2]["status"] == alp.ALP_EINVAL and got[2]["index"] == (1 << 64) - 1
+        for i in (0, 1, 3):
+            assert got[i].tobytes() == ref[i].tobytes()
+        # a larger batch than before grows the scratch buffers (after waiting for the stream)
+        b2 = np.tile(G, 50)
+        l2 = np.tile(lam, 50)
+        o2 = torch.empty(len(b2) * alp.RESULT_DTYPE.itemsize, dtype=torch.uint8, device=dev)
+        ctx.search_batch_async(torch.from_numpy(b2.view(np.int32)).to(dev),
+                               torch.from_numpy(l2.view(np.int32)).to(dev), o2,
+                               instances=torch.from_numpy(np.tile(np.arange(4, dtype=np.uint32),
+                                                                  50).view(np.int32)).to(dev))
+        torch.cuda.synchronize()
+        assert alp.results_from_device(o2, len(b2)).tobytes() == np.tile(ref, 50).tobytes()
+        with pytest.raises(ValueError):
+            ctx.search_batch_async(torch.zeros(3, dtype=torch.int64, device=dev),
+                                   torch.zeros(3, dtype=torch.int64, device=dev), o)
