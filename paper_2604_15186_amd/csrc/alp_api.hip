@@ -9,6 +9,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <array>
 #include <new>
 #include <vector>
 
@@ -127,6 +128,9 @@ struct alp_ctx {
     int occupancy_cache[4][4][17] = {};   // [variant][log2 slots][threads / 64]: blocks per CU
     int timing = 0;
     hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
+    // Timed asynchronous searches: their events (before the option terms, between the kernels,
+    // after the scan) wait in `pending` until the times are read; spent ones are reused.
+    std::vector<std::array<hipEvent_t, 3>> ev_pending, ev_spare;
     float last_ms[3] = {0, 0, 0};
     double total_ms[3] = {0, 0, 0};     // sums of last_ms since timing was last enabled
     void tally(int k) { total_ms[k] += last_ms[k]; }
@@ -441,8 +445,9 @@ int32_t ensure_host_results(alp_ctx *c, size_t count)
 // to `out` (device-visible), rejected queries (invalid != nullptr) to EINVAL records.  With
 // `timed`, HIP events bracket the two kernels (read by run_search after synchronising).
 int32_t launch_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count, alp_result_t *out,
-                      const uint32_t *invalid, bool timed)
+                      const alp::RawQueries *raw, hipEvent_t *ev)
 {
+    const bool timed = ev != nullptr;
     const alp::SpaceDev &sp = c->sp;
     const alp::ScanGeometry g = plan_scan(c, count);
     const uint64_t items_bytes = (uint64_t)count * sp.M * sp.O * sizeof(uint2);
@@ -469,17 +474,17 @@ int32_t launch_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count, alp_re
     fa.ext = ext;
     fa.done = (uint32_t *)c->done.ptr;
     fa.out = out;
-    fa.invalid = invalid;
-    if (timed && (e = hipEventRecord(c->ev[0], c->stream)) != hipSuccess)
+    fa.invalid = raw ? raw->invalid : nullptr;
+    if (timed && (e = hipEventRecord(ev[0], c->stream)) != hipSuccess)
         return hip_fail(e, "hipEventRecord");
-    if ((e = alp::launch_option_terms(sp, c->tdev, q, count, rec, ext, inner, fa.done, c->stream)) !=
-        hipSuccess)
+    if ((e = alp::launch_option_terms(sp, c->tdev, q, count, rec, ext, inner, fa.done, c->stream,
+                                      raw)) != hipSuccess)
         return hip_fail(e, "option_terms launch");
-    if (timed && (e = hipEventRecord(c->ev[1], c->stream)) != hipSuccess)
+    if (timed && (e = hipEventRecord(ev[1], c->stream)) != hipSuccess)
         return hip_fail(e, "hipEventRecord");
     if ((e = alp::launch_scan(sp, q, count, rec, inner, g, win, fa, c->stream)) != hipSuccess)
         return hip_fail(e, "scan launch");
-    if (timed && (e = hipEventRecord(c->ev[2], c->stream)) != hipSuccess)
+    if (timed && (e = hipEventRecord(ev[2], c->stream)) != hipSuccess)
         return hip_fail(e, "hipEventRecord");
     c->last_blocks = count * g.blocks_per_item;
     return ALP_OK;
@@ -491,7 +496,8 @@ int32_t run_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count)
     int32_t st = ensure_host_results(c, count);
     if (st != ALP_OK)
         return st;
-    if ((st = launch_search(c, q, count, c->host_results_dev, nullptr, c->timing != 0)) != ALP_OK)
+    if ((st = launch_search(c, q, count, c->host_results_dev, nullptr, c->timing ? c->ev : nullptr)) !=
+        ALP_OK)
         return st;
     hipError_t e;
     if ((e = hipStreamSynchronize(c->stream)) != hipSuccess)
@@ -504,6 +510,25 @@ int32_t run_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count)
         }
         c->last_ms[2] = 0.0f;
     }
+    return ALP_OK;
+}
+
+// Reads the times of the timed asynchronous searches queued so far (waiting for them), adds
+// them to the totals and leaves the last one in last_ms.
+int32_t collect_async_times(alp_ctx *c)
+{
+    hipError_t e;
+    for (auto &t : c->ev_pending) {
+        if ((e = hipEventSynchronize(t[2])) != hipSuccess ||
+            (e = hipEventElapsedTime(&c->last_ms[0], t[0], t[1])) != hipSuccess ||
+            (e = hipEventElapsedTime(&c->last_ms[1], t[1], t[2])) != hipSuccess)
+            return hip_fail(e, "reading the times of queued searches");
+        c->last_ms[2] = 0.0f;
+        c->tally(0);
+        c->tally(1);
+        c->ev_spare.push_back(t);
+    }
+    c->ev_pending.clear();
     return ALP_OK;
 }
 
@@ -698,15 +723,35 @@ int32_t alp_search_batch_async(alp_ctx *ctx, uint32_t count, const uint32_t *ins
     if ((e = ctx->q_inst.ensure(4 * bytes)) != hipSuccess)
         return hip_fail(e, "hipMalloc(queries)");
     uint32_t *qi = (uint32_t *)ctx->q_inst.ptr;
-    if ((e = alp::launch_prepare_queries(count, ctx->B, ctx->space.units_per_gpu, instances,
-                                         gpu_budget, target_milli, qi, qi + count, qi + 2 * count,
-                                         qi + 3 * count, ctx->stream)) != hipSuccess)
-        return hip_fail(e, "prepare_queries launch");
+    alp::RawQueries raw{instances, gpu_budget, target_milli, ctx->B, ctx->space.units_per_gpu,
+                        qi, qi + count, qi + 2 * (size_t)count, qi + 3 * (size_t)count};
     alp::QueryDev q{};
     q.inst = qi;
     q.capacity = qi + count;
     q.lambda = qi + 2 * (size_t)count;
-    return launch_search(ctx, q, count, out, qi + 3 * count, false);
+    hipEvent_t *ev = nullptr;
+    if (ctx->timing) {
+        if (ctx->ev_spare.empty()) {
+            std::array<hipEvent_t, 3> t{};
+            for (auto &x : t)
+                if ((e = hipEventCreate(&x)) != hipSuccess) {
+                    for (auto &y : t)
+                        if (y)
+                            (void)hipEventDestroy(y);
+                    return hip_fail(e, "hipEventCreate");
+                }
+            ctx->ev_spare.push_back(t);
+        }
+        ctx->ev_pending.push_back(ctx->ev_spare.back());
+        ctx->ev_spare.pop_back();
+        ev = ctx->ev_pending.back().data();
+    }
+    int32_t st = launch_search(ctx, q, count, out, &raw, ev);
+    if (st != ALP_OK && ev) {                      // nothing (complete) was queued for them
+        ctx->ev_spare.push_back(ctx->ev_pending.back());
+        ctx->ev_pending.pop_back();
+    }
+    return st;
 }
 
 int32_t alp_max_throughput(alp_ctx *ctx, uint32_t count, const uint32_t *instances,
@@ -1116,6 +1161,9 @@ int32_t alp_set_timing(alp_ctx *ctx, int32_t enable)
 {
     if (!ctx)
         return fail(ALP_EINVAL, "ctx is NULL");
+    int32_t st = collect_async_times(ctx);
+    if (st != ALP_OK)
+        return st;
     if (enable)
         for (int k = 0; k < 3; ++k)
             ctx->total_ms[k] = 0.0;
@@ -1127,6 +1175,9 @@ int32_t alp_kernel_time_totals(alp_ctx *ctx, double ms[3])
 {
     if (!ctx || !ms)
         return fail(ALP_EINVAL, "ctx or ms is NULL");
+    int32_t st = collect_async_times(ctx);
+    if (st != ALP_OK)
+        return st;
     for (int k = 0; k < 3; ++k)
         ms[k] = ctx->total_ms[k];
     return ALP_OK;
@@ -1136,6 +1187,9 @@ int32_t alp_kernel_times(alp_ctx *ctx, float ms[3], uint32_t *scan_blocks)
 {
     if (!ctx || !ms)
         return fail(ALP_EINVAL, "ctx or ms is NULL");
+    int32_t st = collect_async_times(ctx);
+    if (st != ALP_OK)
+        return st;
     for (int k = 0; k < 3; ++k)
         ms[k] = ctx->last_ms[k];
     if (scan_blocks)
@@ -1156,11 +1210,14 @@ void alp_free(alp_ctx *ctx)
     if (!ctx)
         return;
     DeviceGuard guard(ctx->device);
-    if (ctx->stream)
-        (void)hipStreamSynchronize(ctx->stream);
+    (void)hipStreamSynchronize(ctx->stream);           // queued asynchronous searches included
     for (int k = 0; k < 4; ++k)
         if (ctx->ev[k])
             (void)hipEventDestroy(ctx->ev[k]);
+    for (auto *list : {&ctx->ev_pending, &ctx->ev_spare})
+        for (auto &t : *list)
+            for (hipEvent_t x : t)
+                (void)hipEventDestroy(x);
     DevBuf *bufs[] = {&ctx->tables, &ctx->q_inst, &ctx->rec, &ctx->ext, &ctx->inner, &ctx->done,
                       &ctx->winners, &ctx->idx, &ctx->evals, &ctx->tmax, &ctx->split_dp,
                       &ctx->pruned_table, &ctx->pruned_orders, &ctx->pruned_counts,

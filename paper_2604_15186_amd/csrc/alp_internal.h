@@ -87,17 +87,19 @@ struct ScanGeometry {
     uint32_t slots;            // variants 1, 3: options of the last LLM per lane (1, 2, 4, 8)
 };
 
-// Device-side query preparation for searches whose queries are in device memory: instance
-// (or the item index when inst is nullptr; an instance >= B is rejected and searched as 0),
-// share-unit capacity min(units_per_gpu * budget, kCapacityMax), target.
-hipError_t launch_prepare_queries(uint32_t count, uint32_t B, uint32_t units_per_gpu,
-                                  const uint32_t *inst, const uint32_t *budget,
-                                  const uint32_t *target, uint32_t *q_inst, uint32_t *q_cap,
-                                  uint32_t *q_lambda, uint32_t *invalid, hipStream_t st);
+// Queries of a search batch given in device memory, prepared by the option-term kernel: item i
+// searches instance inst[i] (i when inst is nullptr; one >= B is rejected and searched as
+// instance 0), capacity min(units_per_gpu * budget[i], kCapacityMax), target target[i].  The
+// kernel writes the prepared arrays (the QueryDev the scan reads) and the rejection flags.
+struct RawQueries {
+    const uint32_t *inst, *budget, *target;
+    uint32_t B, units_per_gpu;
+    uint32_t *q_inst, *q_cap, *q_lambda, *invalid;
+};
 
 hipError_t launch_option_terms(const SpaceDev &sp, const TablesDev &tb, const QueryDev &q,
                                uint32_t count, uint2 *rec, uint2 *ext, uint2 *inner, uint32_t *done,
-                               hipStream_t st);
+                               hipStream_t st, const RawQueries *raw = nullptr);
 hipError_t launch_scan(const SpaceDev &sp, const QueryDev &q, uint32_t count, const uint2 *rec,
                        const uint2 *inner, const ScanGeometry &g, Winner *winners,
                        const FinishArgs &fa, hipStream_t st);

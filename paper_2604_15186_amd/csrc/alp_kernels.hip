@@ -36,7 +36,8 @@ constexpr int32_t kNeverFits = -(1 << 30);          // remaining units no lane c
 //    done[item]      = 0 (if done != nullptr): the scan's finished-block counter
 __global__ void __launch_bounds__(256)
 option_terms_kernel(SpaceDev sp, TablesDev tb, QueryDev q, uint32_t count, uint2 *__restrict__ rec,
-                    uint2 *__restrict__ ext, uint2 *__restrict__ inner, uint32_t *__restrict__ done)
+                    uint2 *__restrict__ ext, uint2 *__restrict__ inner, uint32_t *__restrict__ done,
+                    RawQueries raw)
 {
     const uint64_t per_item = (uint64_t)sp.M * sp.O;
     const uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -47,8 +48,28 @@ option_terms_kernel(SpaceDev sp, TablesDev tb, QueryDev q, uint32_t count, uint2
     const uint32_t m = rem / sp.O, o = rem - m * sp.O;
     if (done && rem == 0)
         done[item] = 0;                              // block counter of the fused reduction
-    const uint32_t inst = query_value(q.inst, q.inst1, item);
-    const uint64_t lambda = query_value(q.lambda, q.lambda1, item);
+    uint32_t inst, capacity;
+    uint64_t lambda;
+    if (raw.budget) {
+        // Queries in device memory: prepared here; item's first thread writes what the scan and
+        // the result need.
+        inst = raw.inst ? raw.inst[item] : item;
+        const bool bad = inst >= raw.B;
+        inst = bad ? 0u : inst;
+        const uint64_t cap = (uint64_t)raw.units_per_gpu * raw.budget[item];
+        capacity = cap > kCapacityMax ? kCapacityMax : (uint32_t)cap;
+        lambda = raw.target[item];
+        if (rem == 0) {
+            raw.q_inst[item] = inst;
+            raw.q_cap[item] = capacity;
+            raw.q_lambda[item] = (uint32_t)lambda;
+            raw.invalid[item] = bad ? 1u : 0u;
+        }
+    } else {
+        inst = query_value(q.inst, q.inst1, item);
+        capacity = query_value(q.capacity, q.cap1, item);
+        lambda = query_value(q.lambda, q.lambda1, item);
+    }
 
     const uint32_t d = o % sp.D + 1;
     const uint32_t ij = o / sp.D;
@@ -89,10 +110,9 @@ option_terms_kernel(SpaceDev sp, TablesDev tb, QueryDev q, uint32_t count, uint2
     rec[t] = make_uint2(usable ? (uint32_t)c : 0u, units);
     ext[t] = make_uint2((uint32_t)tau, u | ((uint32_t)ok << 16) | ((uint32_t)thr << 17));
     if (inner && sp.M >= 2 && m == sp.M - 2) {
-        const int32_t capacity = (int32_t)query_value(q.capacity, q.cap1, item);
         const uint32_t stride = inner_stride(sp.O);
         uint2 *row = inner + (uint64_t)item * stride;
-        row[o] = make_uint2(usable ? (uint32_t)c : 0u, (uint32_t)(capacity - (int32_t)units));
+        row[o] = make_uint2(usable ? (uint32_t)c : 0u, (uint32_t)((int32_t)capacity - (int32_t)units));
         // Padding up to a multiple of 16 records: never feasible (no lane's units fit).
         for (uint32_t pad = sp.O + o; pad < stride; pad += sp.O)
             row[pad] = make_uint2(0u, (uint32_t)kNeverFits);
@@ -839,51 +859,17 @@ tmax_kernel(SpaceDev sp, QueryDev q, const uint2 *__restrict__ ext, uint32_t *__
 // ---------------------------------------------------------------------------------------------
 // Launchers.
 
-namespace {
-
-__global__ void __launch_bounds__(256)
-prepare_queries_kernel(uint32_t count, uint32_t B, uint32_t units_per_gpu,
-                       const uint32_t *__restrict__ inst, const uint32_t *__restrict__ budget,
-                       const uint32_t *__restrict__ target, uint32_t *__restrict__ q_inst,
-                       uint32_t *__restrict__ q_cap, uint32_t *__restrict__ q_lambda,
-                       uint32_t *__restrict__ invalid)
-{
-    const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= count)
-        return;
-    const uint32_t b = inst ? inst[i] : i;
-    const bool bad = b >= B;
-    q_inst[i] = bad ? 0u : b;
-    const uint64_t cap = (uint64_t)units_per_gpu * budget[i];
-    q_cap[i] = cap > kCapacityMax ? kCapacityMax : (uint32_t)cap;
-    q_lambda[i] = target[i];
-    invalid[i] = bad ? 1u : 0u;
-}
-
-}  // namespace
-
-hipError_t launch_prepare_queries(uint32_t count, uint32_t B, uint32_t units_per_gpu,
-                                  const uint32_t *inst, const uint32_t *budget,
-                                  const uint32_t *target, uint32_t *q_inst, uint32_t *q_cap,
-                                  uint32_t *q_lambda, uint32_t *invalid, hipStream_t st)
-{
-    if (count == 0)
-        return hipSuccess;
-    hipLaunchKernelGGL(prepare_queries_kernel, dim3((count + 255) / 256), dim3(256), 0, st, count,
-                       B, units_per_gpu, inst, budget, target, q_inst, q_cap, q_lambda, invalid);
-    return hipGetLastError();
-}
-
 hipError_t launch_option_terms(const SpaceDev &sp, const TablesDev &tb, const QueryDev &q,
                                uint32_t count, uint2 *rec, uint2 *ext, uint2 *inner, uint32_t *done,
-                               hipStream_t st)
+                               hipStream_t st, const RawQueries *raw)
 {
     const uint64_t total = (uint64_t)count * sp.M * sp.O;
     if (total == 0)
         return hipSuccess;
     const uint32_t blocks = (uint32_t)((total + 255) / 256);
+    RawQueries none{};
     hipLaunchKernelGGL(option_terms_kernel, dim3(blocks), dim3(256), 0, st, sp, tb, q, count, rec,
-                       ext, inner, done);
+                       ext, inner, done, raw ? *raw : none);
     return hipGetLastError();
 }
 

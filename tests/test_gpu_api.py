@@ -164,3 +164,23 @@ def test_async_batch_rejects_bad_instances_per_record(alp):
         with pytest.raises(ValueError):
             ctx.search_batch_async(torch.zeros(3, dtype=torch.int64, device=dev),
                                    torch.zeros(3, dtype=torch.int64, device=dev), o)
+
+
+def test_async_kernel_times_are_collected(alp):
+    import torch
+    b = make_batch(1, range(2))
+    G, lam, _ = _queries(alp, b)
+    dev = torch.device("cuda", 0)
+    Gd = torch.from_numpy(G.view(np.int32)).to(dev)
+    Ld = torch.from_numpy(lam.view(np.int32)).to(dev)
+    o = torch.empty(2 * alp.RESULT_DTYPE.itemsize, dtype=torch.uint8, device=dev)
+    with alp.Context(b) as ctx:
+        ctx.set_timing(True)
+        for _ in range(4):
+            ctx.search_batch_async(Gd, Ld, o)
+        tot = ctx.kernel_time_totals()                 # waits for the four queued searches
+        last = ctx.kernel_times()
+        assert tot[1] > 0 and tot[0] > 0 and tot[2] == 0
+        assert 0 < last[1] < tot[1]                      # one call's scan, four calls' sum
+        ctx.set_timing(True)
+        assert (ctx.kernel_time_totals() == 0).all()
