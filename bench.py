@@ -55,6 +55,10 @@ from workloads import CONFIGS, make_batch, make_custom, target_from_tmax  # noqa
 
 PEAK_LANE_OPS = 256 * 64 * 2.4e9        # int32 VALU lane-ops/s of MI355X
 OPS_PER_CANDIDATE = 2                   # budget compare + objective min
+# Kernel times are read from HIP events on the first and every TIME_EVERY-th timed step: an
+# event-stamped dispatch costs the GPU a few microseconds of idle time, which would otherwise
+# be part of every step of a small search.
+TIME_EVERY = 8
 # The wider count of lane-ops per candidate (add the last term, compare the budget, compare the
 # best, select value and index), reported beside ``frac`` for comparison with that accounting.
 OPS_PER_CANDIDATE_WIDE = 5
@@ -126,20 +130,22 @@ def cpu_baseline_pruned(batch, G, lam, seconds: float):
 
 
 def timed_steps(step, ctx, steps: int, warmup: int):
-    """Runs warmup + steps calls; returns (elapsed s, mean kernel ms per step [3] over the timed
-    steps, the last call's kernel_times(), last output).  The library sums the HIP-event kernel
-    times itself, so the timed loop holds nothing but the calls."""
+    """Runs warmup + steps calls; returns (elapsed s, mean kernel ms [3] over the timed calls,
+    the last timed call's kernel_times(), last output).  The library times the first and every
+    TIME_EVERY-th step of the timed region with HIP events stamped on the kernel dispatches and
+    sums the times itself, so the timed loop holds nothing but the calls."""
     import torch
     for _ in range(warmup):
         step()
-    ctx.set_timing(True)
+    ctx.set_timing(TIME_EVERY)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(steps):
         out = step()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    avg = ctx.kernel_time_totals() / steps
+    totals, timed = ctx.kernel_time_totals()
+    avg = totals / max(1, timed)
     last = ctx.kernel_times()
     ctx.set_timing(False)
     return elapsed, avg, last, out

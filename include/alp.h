@@ -325,18 +325,25 @@ int32_t alp_eval_candidates(alp_ctx *ctx, uint32_t instance, uint32_t gpu_budget
 int32_t alp_set_launch(alp_ctx *ctx, uint32_t variant, uint32_t blocks_per_item,
                        uint32_t threads_per_block, uint32_t inner_chunks);
 
-/* Enables (1) or disables (0) HIP-event timing of the searches' kernels on the context stream.
- * alp_kernel_times writes, for the last search or batch, the milliseconds of the option-term
- * kernel (ms[0]) and of the candidate scan kernel, which includes the final reduction and the
- * result write (ms[1]); ms[2] is the budget-split kernel of alp_allocate_workflows, 0 after the
- * other searches.  After alp_search_pruned: ms[1] is the fraction enumeration and ms[2] the
- * admissible-option table.  After alp_place: ms[1] is the placement kernel, the others 0.
+/* HIP-event timing of the searches' kernels on the context stream.  enable = 0: off; N >= 1: the
+ * calls of alp_search, alp_search_batch, alp_search_batch_async, alp_allocate_workflows,
+ * alp_search_pruned and alp_place are counted from this call on, and the first and every N-th
+ * after it are timed (the option-term and scan dispatches are stamped with their begin and end;
+ * stamping keeps the GPU idle for a few microseconds between the kernels, so timing a sample of
+ * the calls of a long run leaves the run's throughput nearly unchanged).  Setting resets the
+ * count and the sums below; a negative enable is ALP_EINVAL.
+ * alp_kernel_times writes, for the last timed search or batch, the milliseconds of the
+ * option-term kernel (ms[0]) and of the candidate scan kernel, which includes the final reduction
+ * and the result write (ms[1]); ms[2] is the budget-split kernel of alp_allocate_workflows, 0
+ * after the other searches.  After alp_search_pruned: ms[1] is the fraction enumeration and ms[2]
+ * the admissible-option table.  After alp_place: ms[1] is the placement kernel, the others 0.
  * *scan_blocks receives the scan (or enumeration) grid size of the last search.
- * alp_kernel_time_totals writes the sums of those three figures over every call since timing
- * was last enabled (enabling resets them), so that a caller timing many calls reads them once. */
+ * alp_kernel_time_totals writes the sums of those three figures over the timed calls since
+ * timing was last set, and (if timed_calls is not NULL) their number, so that a caller timing
+ * many calls reads them once. */
 int32_t alp_set_timing(alp_ctx *ctx, int32_t enable);
 int32_t alp_kernel_times(alp_ctx *ctx, float ms[3], uint32_t *scan_blocks);
-int32_t alp_kernel_time_totals(alp_ctx *ctx, double ms[3]);
+int32_t alp_kernel_time_totals(alp_ctx *ctx, double ms[3], uint64_t *timed_calls);
 
 /* Candidates per instance, O^M. */
 int32_t alp_num_candidates(const alp_ctx *ctx, uint64_t *out);

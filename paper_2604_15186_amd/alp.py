@@ -94,7 +94,7 @@ def lib():
         L.alp_set_launch.argtypes = [vp, u32, u32, u32, u32]
         L.alp_set_timing.argtypes = [vp, i32]
         L.alp_kernel_times.argtypes = [vp, C.POINTER(C.c_float), C.POINTER(u32)]
-        L.alp_kernel_time_totals.argtypes = [vp, C.POINTER(C.c_double)]
+        L.alp_kernel_time_totals.argtypes = [vp, C.POINTER(C.c_double), C.POINTER(u64)]
         L.alp_num_candidates.argtypes = [vp, C.POINTER(u64)]
         for name in ("alp_load_profiles", "alp_search", "alp_search_batch",
                      "alp_search_batch_async", "alp_max_throughput",
@@ -295,14 +295,16 @@ class Context:
         _check(lib().alp_set_launch(self._ctx, variant, blocks_per_item, threads_per_block,
                                     inner_chunks))
 
-    def set_timing(self, enable: bool):
-        _check(lib().alp_set_timing(self._ctx, 1 if enable else 0))
+    def set_timing(self, enable: bool | int):
+        """False/0: off; True/1: every call timed; N: the first and every N-th call timed."""
+        _check(lib().alp_set_timing(self._ctx, int(enable)))
 
-    def kernel_time_totals(self) -> np.ndarray:
-        """Sums of kernel_times()' three figures over every call since timing was enabled."""
+    def kernel_time_totals(self) -> tuple[np.ndarray, int]:
+        """(sums of kernel_times()' three figures, number of timed calls) since timing was set."""
         ms = (C.c_double * 3)()
-        _check(lib().alp_kernel_time_totals(self._ctx, ms))
-        return np.array([ms[0], ms[1], ms[2]])
+        calls = C.c_uint64()
+        _check(lib().alp_kernel_time_totals(self._ctx, ms, C.byref(calls)))
+        return np.array([ms[0], ms[1], ms[2]]), int(calls.value)
 
     def kernel_times(self):
         """(option-term ms, scan ms, third-kernel ms, grid blocks) of the last call; the third

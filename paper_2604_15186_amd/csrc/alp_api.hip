@@ -126,13 +126,15 @@ struct alp_ctx {
 
     uint32_t variant = 0, bpi_override = 0, tpb_override = 0, chunks_override = 0;
     int occupancy_cache[4][4][17] = {};   // [variant][log2 slots][threads / 64]: blocks per CU
-    int timing = 0;
+    uint32_t timing_every = 0;          // 0: no timing; N: every N-th timed-API call
+    uint64_t calls_seen = 0, timed_calls = 0;
+    int timing = 0;                     // the current call records its kernel times
     hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
-    // Timed asynchronous searches: their events (before the option terms, between the kernels,
-    // after the scan) wait in `pending` until the times are read; spent ones are reused.
-    std::vector<std::array<hipEvent_t, 3>> ev_pending, ev_spare;
+    // Timed asynchronous searches: their events (begin and end of the option terms, then of the
+    // scan) wait in `pending` until the times are read; spent ones are reused.
+    std::vector<std::array<hipEvent_t, 4>> ev_pending, ev_spare;
     float last_ms[3] = {0, 0, 0};
-    double total_ms[3] = {0, 0, 0};     // sums of last_ms since timing was last enabled
+    double total_ms[3] = {0, 0, 0};     // sums of last_ms since timing was last set
     void tally(int k) { total_ms[k] += last_ms[k]; }
     uint32_t last_blocks = 0;
 };
@@ -140,6 +142,15 @@ struct alp_ctx {
 namespace {
 
 uint64_t ceil_div(uint64_t a, uint64_t b) { return (a + b - 1) / b; }
+
+// Start of a call of an entry point whose kernels can be timed: it is timed if it is the first,
+// or an N-th after it, since timing was set to every N-th call.
+void begin_call(alp_ctx *c)
+{
+    c->timing = c->timing_every != 0 && c->calls_seen % c->timing_every == 0;
+    c->calls_seen += c->timing_every != 0;
+    c->timed_calls += c->timing;
+}
 
 int32_t validate_space(const alp_space_t *s, uint32_t *O_out, uint64_t *N_out)
 {
@@ -442,8 +453,9 @@ int32_t ensure_host_results(alp_ctx *c, size_t count)
 // Runs option terms -> scan (with the fused final reduction) for `count` items described by q;
 // the kernels write the results straight into c->host_results[0..count) (mapped pinned memory).
 // Queues the option-term and scan kernels of `count` searches on the context stream.  Results go
-// to `out` (device-visible), rejected queries (invalid != nullptr) to EINVAL records.  With
-// `timed`, HIP events bracket the two kernels (read by run_search after synchronising).
+// to `out` (device-visible); with device queries (raw), rejected ones to EINVAL records.  ev
+// (4 events or nullptr): begin and end of the option-term kernel, then of the scan, stamped by
+// the dispatches.
 int32_t launch_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count, alp_result_t *out,
                       const alp::RawQueries *raw, hipEvent_t *ev)
 {
@@ -475,17 +487,13 @@ int32_t launch_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count, alp_re
     fa.done = (uint32_t *)c->done.ptr;
     fa.out = out;
     fa.invalid = raw ? raw->invalid : nullptr;
-    if (timed && (e = hipEventRecord(ev[0], c->stream)) != hipSuccess)
-        return hip_fail(e, "hipEventRecord");
     if ((e = alp::launch_option_terms(sp, c->tdev, q, count, rec, ext, inner, fa.done, c->stream,
-                                      raw)) != hipSuccess)
+                                      raw, timed ? ev[0] : nullptr, timed ? ev[1] : nullptr)) !=
+        hipSuccess)
         return hip_fail(e, "option_terms launch");
-    if (timed && (e = hipEventRecord(ev[1], c->stream)) != hipSuccess)
-        return hip_fail(e, "hipEventRecord");
-    if ((e = alp::launch_scan(sp, q, count, rec, inner, g, win, fa, c->stream)) != hipSuccess)
+    if ((e = alp::launch_scan(sp, q, count, rec, inner, g, win, fa, c->stream,
+                              timed ? ev[2] : nullptr, timed ? ev[3] : nullptr)) != hipSuccess)
         return hip_fail(e, "scan launch");
-    if (timed && (e = hipEventRecord(ev[2], c->stream)) != hipSuccess)
-        return hip_fail(e, "hipEventRecord");
     c->last_blocks = count * g.blocks_per_item;
     return ALP_OK;
 }
@@ -504,7 +512,8 @@ int32_t run_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count)
         return hip_fail(e, "hipStreamSynchronize");
     if (c->timing) {
         for (int k = 0; k < 2; ++k) {
-            if ((e = hipEventElapsedTime(&c->last_ms[k], c->ev[k], c->ev[k + 1])) != hipSuccess)
+            if ((e = hipEventElapsedTime(&c->last_ms[k], c->ev[2 * k], c->ev[2 * k + 1])) !=
+                hipSuccess)
                 return hip_fail(e, "hipEventElapsedTime");
             c->tally(k);
         }
@@ -519,9 +528,9 @@ int32_t collect_async_times(alp_ctx *c)
 {
     hipError_t e;
     for (auto &t : c->ev_pending) {
-        if ((e = hipEventSynchronize(t[2])) != hipSuccess ||
+        if ((e = hipEventSynchronize(t[3])) != hipSuccess ||
             (e = hipEventElapsedTime(&c->last_ms[0], t[0], t[1])) != hipSuccess ||
-            (e = hipEventElapsedTime(&c->last_ms[1], t[1], t[2])) != hipSuccess)
+            (e = hipEventElapsedTime(&c->last_ms[1], t[2], t[3])) != hipSuccess)
             return hip_fail(e, "reading the times of queued searches");
         c->last_ms[2] = 0.0f;
         c->tally(0);
@@ -663,6 +672,7 @@ int32_t alp_search(alp_ctx *ctx, uint32_t instance, uint32_t gpu_budget, uint32_
     DeviceGuard guard(ctx->device);
     if (guard.status != hipSuccess)
         return hip_fail(guard.status, "hipSetDevice");
+    begin_call(ctx);
     alp::QueryDev q{};
     q.inst1 = instance;
     q.cap1 = capacity_of(ctx, gpu_budget);
@@ -694,6 +704,7 @@ int32_t alp_search_batch(alp_ctx *ctx, uint32_t count, const uint32_t *instances
     DeviceGuard guard(ctx->device);
     if (guard.status != hipSuccess)
         return hip_fail(guard.status, "hipSetDevice");
+    begin_call(ctx);
     alp::QueryDev q{};
     int32_t st = upload_queries(ctx, count, inst.data(), cap.data(), target_milli, q);
     if (st != ALP_OK)
@@ -717,6 +728,7 @@ int32_t alp_search_batch_async(alp_ctx *ctx, uint32_t count, const uint32_t *ins
     DeviceGuard guard(ctx->device);
     if (guard.status != hipSuccess)
         return hip_fail(guard.status, "hipSetDevice");
+    begin_call(ctx);
     hipError_t e;
     // q_inst holds inst | cap | lambda, then the per-item rejection flags.
     const size_t bytes = (size_t)count * sizeof(uint32_t);
@@ -732,7 +744,7 @@ int32_t alp_search_batch_async(alp_ctx *ctx, uint32_t count, const uint32_t *ins
     hipEvent_t *ev = nullptr;
     if (ctx->timing) {
         if (ctx->ev_spare.empty()) {
-            std::array<hipEvent_t, 3> t{};
+            std::array<hipEvent_t, 4> t{};
             for (auto &x : t)
                 if ((e = hipEventCreate(&x)) != hipSuccess) {
                     for (auto &y : t)
@@ -829,6 +841,7 @@ int32_t alp_allocate_workflows(alp_ctx *ctx, uint32_t count, const uint32_t *ins
     DeviceGuard guard(ctx->device);
     if (guard.status != hipSuccess)
         return hip_fail(guard.status, "hipSetDevice");
+    begin_call(ctx);
     hipError_t e;
     if (!ctx->host_split) {
         if ((e = hipHostMalloc((void **)&ctx->host_split, 32 * sizeof(uint32_t), hipHostMallocMapped)) !=
@@ -947,6 +960,7 @@ int32_t alp_search_pruned(alp_ctx *ctx, uint32_t count, const uint32_t *instance
     DeviceGuard guard(ctx->device);
     if (guard.status != hipSuccess)
         return hip_fail(guard.status, "hipSetDevice");
+    begin_call(ctx);
     const uint64_t items_bytes = (uint64_t)count * sp.M * sp.O * sizeof(uint2);
     hipError_t e;
     if ((e = ctx->rec.ensure(items_bytes)) != hipSuccess || (e = ctx->ext.ensure(items_bytes)) != hipSuccess ||
@@ -1057,6 +1071,7 @@ int32_t alp_place(alp_ctx *ctx, uint32_t count, const alp_result_t *allocations,
     DeviceGuard guard(ctx->device);
     if (guard.status != hipSuccess)
         return hip_fail(guard.status, "hipSetDevice");
+    begin_call(ctx);
     hipError_t e;
     if ((e = ctx->place_in.ensure(count * sizeof(alp::PlaceIn))) != hipSuccess ||
         (e = ctx->place_out.ensure(count * sizeof(alp_placement_t))) != hipSuccess)
@@ -1161,17 +1176,20 @@ int32_t alp_set_timing(alp_ctx *ctx, int32_t enable)
 {
     if (!ctx)
         return fail(ALP_EINVAL, "ctx is NULL");
+    if (enable < 0)
+        return fail(ALP_EINVAL, "enable %d is negative", enable);
     int32_t st = collect_async_times(ctx);
     if (st != ALP_OK)
         return st;
-    if (enable)
-        for (int k = 0; k < 3; ++k)
-            ctx->total_ms[k] = 0.0;
-    ctx->timing = enable ? 1 : 0;
+    for (int k = 0; k < 3; ++k)
+        ctx->total_ms[k] = 0.0;
+    ctx->timing_every = (uint32_t)enable;
+    ctx->calls_seen = ctx->timed_calls = 0;
+    ctx->timing = 0;
     return ALP_OK;
 }
 
-int32_t alp_kernel_time_totals(alp_ctx *ctx, double ms[3])
+int32_t alp_kernel_time_totals(alp_ctx *ctx, double ms[3], uint64_t *timed_calls)
 {
     if (!ctx || !ms)
         return fail(ALP_EINVAL, "ctx or ms is NULL");
@@ -1180,6 +1198,8 @@ int32_t alp_kernel_time_totals(alp_ctx *ctx, double ms[3])
         return st;
     for (int k = 0; k < 3; ++k)
         ms[k] = ctx->total_ms[k];
+    if (timed_calls)
+        *timed_calls = ctx->timed_calls;
     return ALP_OK;
 }
 

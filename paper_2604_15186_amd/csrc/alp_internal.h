@@ -99,10 +99,12 @@ struct RawQueries {
 
 hipError_t launch_option_terms(const SpaceDev &sp, const TablesDev &tb, const QueryDev &q,
                                uint32_t count, uint2 *rec, uint2 *ext, uint2 *inner, uint32_t *done,
-                               hipStream_t st, const RawQueries *raw = nullptr);
+                               hipStream_t st, const RawQueries *raw = nullptr,
+                               hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
 hipError_t launch_scan(const SpaceDev &sp, const QueryDev &q, uint32_t count, const uint2 *rec,
                        const uint2 *inner, const ScanGeometry &g, Winner *winners,
-                       const FinishArgs &fa, hipStream_t st);
+                       const FinishArgs &fa, hipStream_t st, hipEvent_t t0 = nullptr,
+                       hipEvent_t t1 = nullptr);
 hipError_t launch_eval(const SpaceDev &sp, uint32_t capacity, const uint2 *rec, const uint2 *ext,
                        const uint64_t *idx, uint64_t count, alp_eval_t *out, hipStream_t st);
 hipError_t launch_tmax(const SpaceDev &sp, const QueryDev &q, uint32_t count, const uint2 *ext,

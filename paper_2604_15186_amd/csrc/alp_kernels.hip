@@ -12,6 +12,7 @@
 //      item's block winners, decodes the winning index and recomputes T_w (Eq. 2) and the share
 //      units from the per-option records.
 // Everything is integer; results are bit-identical for every launch geometry.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -857,45 +858,50 @@ tmax_kernel(SpaceDev sp, QueryDev q, const uint2 *__restrict__ ext, uint32_t *__
 }
 
 // ---------------------------------------------------------------------------------------------
-// Launchers.
+// Launchers.  The option-term and scan launches take optional start/stop events that the
+// dispatch itself stamps with the kernel's begin and end (no separate event packets between
+// the kernels, which would leave the GPU idle for microseconds per search).
 
 hipError_t launch_option_terms(const SpaceDev &sp, const TablesDev &tb, const QueryDev &q,
                                uint32_t count, uint2 *rec, uint2 *ext, uint2 *inner, uint32_t *done,
-                               hipStream_t st, const RawQueries *raw)
+                               hipStream_t st, const RawQueries *raw, hipEvent_t t0,
+                               hipEvent_t t1)
 {
     const uint64_t total = (uint64_t)count * sp.M * sp.O;
     if (total == 0)
         return hipSuccess;
     const uint32_t blocks = (uint32_t)((total + 255) / 256);
     RawQueries none{};
-    hipLaunchKernelGGL(option_terms_kernel, dim3(blocks), dim3(256), 0, st, sp, tb, q, count, rec,
-                       ext, inner, done, raw ? *raw : none);
+    hipExtLaunchKernelGGL(option_terms_kernel, dim3(blocks), dim3(256), 0, st, t0, t1, 0, sp, tb, q,
+                          count, rec, ext, inner, done, raw ? *raw : none);
     return hipGetLastError();
 }
 
 template <int S>
 static hipError_t launch_lane(const SpaceDev &sp, const QueryDev &q, uint32_t count,
                               const uint2 *rec, const uint2 *inner, const ScanGeometry &g,
-                              Winner *winners, const FinishArgs &fa, hipStream_t st)
+                              Winner *winners, const FinishArgs &fa, hipStream_t st,
+                              hipEvent_t t0, hipEvent_t t1)
 {
     const uint32_t nblocks = count * g.blocks_per_item;
     if (g.variant == 3)
-        hipLaunchKernelGGL(HIP_KERNEL_NAME(scan_lane_kernel<S>), dim3(nblocks), dim3(g.threads), 0,
-                           st, rec, q, sp.M, sp.O, g.rows, g.rows_per_wave, g.blocks_per_item,
-                           nblocks, winners, fa);
+        hipExtLaunchKernelGGL(HIP_KERNEL_NAME(scan_lane_kernel<S>), dim3(nblocks), dim3(g.threads),
+                              0, st, t0, t1, 0, rec, q, sp.M, sp.O, g.rows, g.rows_per_wave,
+                              g.blocks_per_item, nblocks, winners, fa);
     else {
         const uint32_t n_outer = sp.M >= 2 ? sp.M - 2 : 0;
 #define ALP_LAUNCH_MIN(NO)                                                                         \
     do {                                                                                           \
         if (g.dynamic)                                                                             \
-            hipLaunchKernelGGL(HIP_KERNEL_NAME(scan_min_kernel<S, NO, true>), dim3(nblocks),       \
-                               dim3(g.threads), 0, st, rec, inner, q, sp.M, sp.O, g.rows,          \
-                               g.rows_per_wave, g.chunks, g.blocks_per_item, nblocks, winners,    \
-                               fa);                                                                \
+            hipExtLaunchKernelGGL(HIP_KERNEL_NAME(scan_min_kernel<S, NO, true>), dim3(nblocks),    \
+                                  dim3(g.threads), 0, st, t0, t1, 0, rec, inner, q, sp.M, sp.O,    \
+                                  g.rows, g.rows_per_wave, g.chunks, g.blocks_per_item, nblocks,   \
+                                  winners, fa);                                                    \
         else                                                                                       \
-            hipLaunchKernelGGL(HIP_KERNEL_NAME(scan_min_kernel<S, NO, false>), dim3(nblocks),      \
-                               dim3(g.threads), 0, st, rec, inner, q, sp.M, sp.O, g.rows,          \
-                               g.rows_per_wave, 1u, g.blocks_per_item, nblocks, winners, fa);     \
+            hipExtLaunchKernelGGL(HIP_KERNEL_NAME(scan_min_kernel<S, NO, false>), dim3(nblocks),   \
+                                  dim3(g.threads), 0, st, t0, t1, 0, rec, inner, q, sp.M, sp.O,    \
+                                  g.rows, g.rows_per_wave, 1u, g.blocks_per_item, nblocks,         \
+                                  winners, fa);                                                    \
     } while (0)
         switch (n_outer) {
         case 0: ALP_LAUNCH_MIN(0); break;
@@ -911,7 +917,7 @@ static hipError_t launch_lane(const SpaceDev &sp, const QueryDev &q, uint32_t co
 
 hipError_t launch_scan(const SpaceDev &sp, const QueryDev &q, uint32_t count, const uint2 *rec,
                        const uint2 *inner, const ScanGeometry &g, Winner *winners,
-                       const FinishArgs &fa, hipStream_t st)
+                       const FinishArgs &fa, hipStream_t st, hipEvent_t t0, hipEvent_t t1)
 {
     if (count == 0)
         return hipSuccess;
@@ -921,15 +927,16 @@ hipError_t launch_scan(const SpaceDev &sp, const QueryDev &q, uint32_t count, co
             N *= sp.O;
         const uint32_t nblocks = count * g.blocks_per_item;
         const size_t lds = (size_t)sp.M * sp.O * sizeof(uint2);
-        hipLaunchKernelGGL(scan_flat_kernel, dim3(nblocks), dim3(g.threads), lds, st, rec, q, sp.M,
-                           sp.O, N, g.per_thread, g.blocks_per_item, nblocks, winners, fa);
+        hipExtLaunchKernelGGL(scan_flat_kernel, dim3(nblocks), dim3(g.threads), lds, st, t0, t1, 0,
+                              rec, q, sp.M, sp.O, N, g.per_thread, g.blocks_per_item, nblocks,
+                              winners, fa);
         return hipGetLastError();
     }
     switch (g.slots) {
-    case 1: return launch_lane<1>(sp, q, count, rec, inner, g, winners, fa, st);
-    case 2: return launch_lane<2>(sp, q, count, rec, inner, g, winners, fa, st);
-    case 4: return launch_lane<4>(sp, q, count, rec, inner, g, winners, fa, st);
-    case 8: return launch_lane<8>(sp, q, count, rec, inner, g, winners, fa, st);
+    case 1: return launch_lane<1>(sp, q, count, rec, inner, g, winners, fa, st, t0, t1);
+    case 2: return launch_lane<2>(sp, q, count, rec, inner, g, winners, fa, st, t0, t1);
+    case 4: return launch_lane<4>(sp, q, count, rec, inner, g, winners, fa, st, t0, t1);
+    case 8: return launch_lane<8>(sp, q, count, rec, inner, g, winners, fa, st, t0, t1);
     default: return hipErrorInvalidValue;
     }
 }

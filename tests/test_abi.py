@@ -169,7 +169,8 @@ def test_null_arguments_rejected():
     assert lib.alp_search_batch(None, 1, None, None, None, None) == alp.ALP_EINVAL
     assert lib.alp_search_batch_async(None, 1, None, None, None, None) == alp.ALP_EINVAL
     assert lib.alp_set_launch(None, 0, 0, 0, 0) == alp.ALP_EINVAL
-    assert lib.alp_kernel_time_totals(None, (C.c_double * 3)()) == alp.ALP_EINVAL
+    assert lib.alp_kernel_time_totals(None, (C.c_double * 3)(), None) == alp.ALP_EINVAL
+    assert lib.alp_set_timing(None, 1) == alp.ALP_EINVAL
     assert lib.alp_search_pruned(None, 1, None, None, None, 3, None) == alp.ALP_EINVAL
     assert lib.alp_trace_stats(None, 2, 1, None, None, None, None, None) == alp.ALP_EINVAL
     assert lib.alp_stats_create(None, 0, None) == alp.ALP_EINVAL

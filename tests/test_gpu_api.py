@@ -103,13 +103,21 @@ def test_kernel_time_totals_sum_the_calls(alp):
         for _ in range(5):
             ctx.search(0, int(G[0]), int(lam[0]))
             per_call += np.asarray(ctx.kernel_times()[:3], dtype=np.float64)
-        tot = ctx.kernel_time_totals()
-        assert tot[1] > 0 and np.allclose(tot, per_call, rtol=1e-6, atol=1e-9)
-        ctx.set_timing(True)                           # enabling again starts new sums
-        assert (ctx.kernel_time_totals() == 0).all()
+        tot, calls = ctx.kernel_time_totals()
+        assert calls == 5 and tot[1] > 0 and np.allclose(tot, per_call, rtol=1e-6, atol=1e-9)
+        ctx.set_timing(True)                           # setting again starts new sums
+        assert (ctx.kernel_time_totals()[0] == 0).all()
         ctx.set_timing(False)
         ctx.search(0, int(G[0]), int(lam[0]))          # untimed calls add nothing
-        assert (ctx.kernel_time_totals() == 0).all()
+        tot, calls = ctx.kernel_time_totals()
+        assert (tot == 0).all() and calls == 0
+        ctx.set_timing(3)                              # calls 0, 3, 6 of the next 8 are timed
+        for _ in range(8):
+            ctx.search(0, int(G[0]), int(lam[0]))
+        tot, calls = ctx.kernel_time_totals()
+        assert calls == 3 and tot[1] > 0
+        with pytest.raises(alp.AlpError):
+            ctx.set_timing(-1)
 
 
 def test_async_batch_matches_the_synchronous_batch(alp):
@@ -178,9 +186,9 @@ def test_async_kernel_times_are_collected(alp):
         ctx.set_timing(True)
         for _ in range(4):
             ctx.search_batch_async(Gd, Ld, o)
-        tot = ctx.kernel_time_totals()                 # waits for the four queued searches
+        tot, calls = ctx.kernel_time_totals()          # waits for the four queued searches
         last = ctx.kernel_times()
-        assert tot[1] > 0 and tot[0] > 0 and tot[2] == 0
+        assert calls == 4 and tot[1] > 0 and tot[0] > 0 and tot[2] == 0
         assert 0 < last[1] < tot[1]                      # one call's scan, four calls' sum
         ctx.set_timing(True)
-        assert (ctx.kernel_time_totals() == 0).all()
+        assert (ctx.kernel_time_totals()[0] == 0).all()
