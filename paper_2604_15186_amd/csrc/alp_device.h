@@ -196,14 +196,14 @@ __device__ __forceinline__ bool block_store_last(uint32_t L, uint64_t x, uint32_
         return true;
     }
     if (threadIdx.x == 0) {
-        __threadfence();
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");   // the winner, before the count
         const uint32_t prev = atomicAdd(&done[item], 1u);
         last_block = prev == blocks_per_item - 1 ? 1u : 0u;
     }
     __syncthreads();
     const bool last = last_block != 0;
     if (last)
-        __threadfence();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");   // every block's winner
     return last;
 }
 
@@ -226,13 +226,16 @@ __device__ __forceinline__ void block_finish(uint32_t L, uint64_t x, uint32_t it
         return;
     }
     if (threadIdx.x == 0) {
-        __threadfence();
+        // Release: the block's winner is visible before its count (an L2 write-back; no
+        // invalidate needed here).
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
         const uint32_t prev = atomicAdd(&fa.done[item], 1u);
         last_block = prev == blocks_per_item - 1 ? 1u : 0u;
     }
     __syncthreads();
     if (last_block && threadIdx.x < 64) {
-        __threadfence();
+        // Acquire: every counted block's winner is visible (an invalidate; no write-back).
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
         finish_item(fa, item, blocks_per_item, winners);
     }
 }
