@@ -78,8 +78,9 @@ typedef struct {
     uint32_t num_points;
 } alp_space_t;
 
-/* Search result (48 bytes).  status is ALP_OK or ALP_INFEASIBLE; on INFEASIBLE index is
- * ALP_NO_INDEX and the other fields are 0.  latency_us = L_w (Eq. 1), throughput_milli = T_w
+/* Search result (48 bytes).  status is ALP_OK or ALP_INFEASIBLE (or ALP_EINVAL for a query
+ * alp_search_batch_async rejected); otherwise than ALP_OK, index is ALP_NO_INDEX and the other
+ * fields are 0.  latency_us = L_w (Eq. 1), throughput_milli = T_w
  * (Eq. 2), gpu_units = sum of tp * q * d; per LLM the chosen tp, share (units of 1/Q) and
  * replica count, entries beyond num_llms 0. */
 typedef struct {
