@@ -9,7 +9,11 @@
 //
 // Kernels:
 //   stats_init_kernel        zeroes the per-LLM totals and the error flags.
-//   trace_stats_kernel<G>    one workgroup per trace: the calls are sorted by key
+//   trace_stats_kernel<G>    one workgroup per trace.  A trace of at most 2,048 calls that is
+//                            already in order of end time (calls logged on completion) is swept
+//                            backwards without a sort: a call adds the part of it before the
+//                            earliest start of the same LLM's later calls.  Otherwise the calls
+//                            are sorted by key
 //                            (llm << 60 | start) with a bitonic network (in LDS, or for long
 //                            traces in a global scratch region, G = true); the time covered by
 //                            each LLM follows from an exclusive prefix maximum of
@@ -337,6 +341,117 @@ __device__ __forceinline__ void sweep(uint32_t P, uint32_t valid, Get get,
     flush();
 }
 
+// Per-LLM sums of one thread's calls (LLM m[j], duration e[j] - s[j], covered part act[j]) for
+// LLM 0..M-1, reduced over each wave by lane butterflies and added to s_sum by lane 0.
+template <int E>
+__device__ __forceinline__ void add_llm_sums(uint32_t M, const uint32_t (&m)[E],
+                                             const uint64_t (&s)[E], const uint64_t (&e)[E],
+                                             const uint64_t (&act)[E], const bool (&ok)[E],
+                                             unsigned long long *s_sum)
+{
+#pragma unroll
+    for (uint32_t q = 0; q < ALP_MAX_LLMS; ++q) {
+        if (q >= M)
+            break;
+        uint32_t calls = 0;
+        uint64_t busy = 0, active = 0;
+#pragma unroll
+        for (int j = 0; j < E; ++j) {
+            const bool mine = ok[j] && m[j] == q;
+            calls += mine ? 1u : 0u;
+            busy += mine ? e[j] - s[j] : 0u;
+            active += mine ? act[j] : 0u;
+        }
+        auto step = [&](auto q_const) {
+            constexpr int Q = decltype(q_const)::value;
+            calls += lane_xor<Q>(calls);
+            busy += lane_xor64<Q>(busy);
+            active += lane_xor64<Q>(active);
+        };
+        step(std::integral_constant<int, 32>{});
+        step(std::integral_constant<int, 16>{});
+        step(std::integral_constant<int, 8>{});
+        step(std::integral_constant<int, 4>{});
+        step(std::integral_constant<int, 2>{});
+        step(std::integral_constant<int, 1>{});
+        if ((threadIdx.x & 63) == 0 && calls) {
+            atomicAdd(&s_sum[3 * q + 0], (unsigned long long)calls);
+            atomicAdd(&s_sum[3 * q + 1], (unsigned long long)busy);
+            atomicAdd(&s_sum[3 * q + 2], (unsigned long long)active);
+        }
+    }
+}
+
+// Covered time of a trace whose calls are in order of end time (as a proxy logs them on
+// completion), without a sort.  Walking the calls backwards, the calls of LLM m that come after
+// call j (so end no earlier) cover, within (-inf, e_j], exactly [lo, e_j] where lo is their
+// smallest start (or nothing if lo > e_j); so call j of LLM m adds max(0, min(e_j, lo) - s_j).
+// Thread t holds calls t E .. t E + E - 1; lo per LLM past its last call comes from an exclusive
+// suffix minimum over the later threads (lane moves within a wave, LDS across the waves).
+template <int E>
+__device__ __forceinline__ void sweep_by_end(uint32_t M, const uint32_t (&m)[E],
+                                             const uint64_t (&s)[E], const uint64_t (&e)[E],
+                                             const bool (&ok)[E], unsigned long long *s_sum)
+{
+    __shared__ uint64_t s_wave_lo[kThreads / 64][ALP_MAX_LLMS];
+    const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    // The thread's smallest start per LLM.
+    uint64_t lo[ALP_MAX_LLMS];
+#pragma unroll
+    for (uint32_t q = 0; q < ALP_MAX_LLMS; ++q) {
+        lo[q] = ~0ull;
+#pragma unroll
+        for (int j = 0; j < E; ++j)
+            if (ok[j] && m[j] == q && s[j] < lo[q])
+                lo[q] = s[j];
+    }
+    // Inclusive suffix minimum over the wave's lanes (lane and later), then over later waves.
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+#pragma unroll
+        for (uint32_t q = 0; q < ALP_MAX_LLMS; ++q) {
+            if (q < M) {
+                const uint64_t o = __shfl_down((unsigned long long)lo[q], off, 64);
+                if (lane + off < 64 && o < lo[q])
+                    lo[q] = o;
+            }
+        }
+    }
+    if (lane == 0)
+#pragma unroll
+        for (uint32_t q = 0; q < ALP_MAX_LLMS; ++q)
+            s_wave_lo[wave][q] = lo[q];
+    __syncthreads();
+    // Exclusive: the next lane's inclusive value, and the later waves.
+#pragma unroll
+    for (uint32_t q = 0; q < ALP_MAX_LLMS; ++q) {
+        uint64_t v = q < M ? (uint64_t)__shfl_down((unsigned long long)lo[q], 1, 64) : ~0ull;
+        if (lane == 63)
+            v = ~0ull;
+        for (uint32_t w = wave + 1; w < kThreads / 64; ++w)
+            v = s_wave_lo[w][q] < v ? s_wave_lo[w][q] : v;
+        lo[q] = v;
+    }
+    // Walk the thread's calls backwards.
+    uint64_t act[E];
+#pragma unroll
+    for (int j = E - 1; j >= 0; --j) {
+        uint64_t cur = ~0ull;
+#pragma unroll
+        for (uint32_t q = 0; q < ALP_MAX_LLMS; ++q)
+            cur = m[j] == q ? lo[q] : cur;
+        const uint64_t right = e[j] < cur ? e[j] : cur;
+        act[j] = ok[j] && right > s[j] ? right - s[j] : 0u;
+        if (ok[j]) {
+#pragma unroll
+            for (uint32_t q = 0; q < ALP_MAX_LLMS; ++q)
+                if (m[j] == q && s[j] < lo[q])
+                    lo[q] = s[j];
+        }
+    }
+    add_llm_sums<E>(M, m, s, e, act, ok, s_sum);
+}
+
 // Largest trace the LDS path holds in registers while it loads (calls per thread).
 constexpr uint32_t kMaxPerThread = 8;
 
@@ -389,26 +504,64 @@ trace_stats_kernel(uint32_t M, const uint64_t *__restrict__ offsets,
         // Held in registers: the trace's first and last start decide whether a call packs
         // into one 64-bit key, (llm << 61 | start - first << 32 | duration), which halves the
         // sort's LDS traffic; traces spanning 2^29 us or more keep (key, end) pairs.
+        // Thread t holds calls t E .. t E + E - 1 (E = P / 256, a contiguous chunk).
+        const uint32_t E = P / kThreads;
         uint32_t rm[kMaxPerThread];
         uint64_t rs[kMaxPerThread], re[kMaxPerThread];
         bool ok[kMaxPerThread];
         uint64_t smin = ~0ull, smax = 0;
+        // Whether the calls are in order of end time: within the chunk, and (below) across
+        // chunk boundaries through s_first.
+        bool in_order = true;
+        uint64_t first_end = ~0ull, last_end = 0;
 #pragma unroll
         for (uint32_t k = 0; k < kMaxPerThread; ++k) {
-            ok[k] = load(threadIdx.x + (uint64_t)k * kThreads, rm[k], rs[k], re[k]);
+            ok[k] = k < E && load((uint64_t)threadIdx.x * E + k, rm[k], rs[k], re[k]);
             if (ok[k]) {
                 valid += 1;
                 smin = rs[k] < smin ? rs[k] : smin;
                 smax = rs[k] > smax ? rs[k] : smax;
+                in_order = in_order && re[k] >= last_end;
+                first_end = first_end == ~0ull ? re[k] : first_end;
+                last_end = re[k];
             }
         }
+        __shared__ uint64_t s_first[kThreads];
+        s_first[threadIdx.x] = first_end;
         if (bad)
             atomicOr(flags, bad);
         uint32_t nvalid = valid;
-        block_min_max_sum(smin, smax, nvalid);
+        block_min_max_sum(smin, smax, nvalid);          // its barrier also publishes s_first
         if (nvalid == 0)
             return;
-        if (smax - smin < (1ull << 29)) {
+        // The next chunk that holds a call must not end earlier (chunks with no call are
+        // padding and come last); malformed calls (bad) send the trace to the sort.
+        if (threadIdx.x + 1 < kThreads && s_first[threadIdx.x + 1] != ~0ull)
+            in_order = in_order && s_first[threadIdx.x + 1] >= last_end;
+        if (bad)
+            in_order = false;
+        if (__syncthreads_and(in_order ? 1 : 0)) {
+            auto run = [&](auto e_const) {
+                constexpr int EC = decltype(e_const)::value;
+                uint32_t m[EC];
+                uint64_t st[EC], en[EC];
+                bool okc[EC];
+#pragma unroll
+                for (int j = 0; j < EC; ++j) {
+                    m[j] = rm[j];
+                    st[j] = rs[j];
+                    en[j] = re[j];
+                    okc[j] = ok[j];
+                }
+                sweep_by_end<EC>(M, m, st, en, okc, s_sum);
+            };
+            switch (P) {
+            case kThreads: run(std::integral_constant<int, 1>{}); break;
+            case 2 * kThreads: run(std::integral_constant<int, 2>{}); break;
+            case 4 * kThreads: run(std::integral_constant<int, 4>{}); break;
+            default: run(std::integral_constant<int, 8>{}); break;
+            }
+        } else if (smax - smin < (1ull << 29)) {
             // The thread's loaded calls k < P / 256 become its E sort positions (any placement
             // of the inputs sorts the same); padding sorts last.
             uint64_t pk[kMaxPerThread];
@@ -434,8 +587,8 @@ trace_stats_kernel(uint32_t M, const uint64_t *__restrict__ offsets,
         } else {
 #pragma unroll
             for (uint32_t k = 0; k < kMaxPerThread; ++k) {
-                const uint32_t i = threadIdx.x + k * kThreads;
-                if (i < P) {
+                if (k < E) {
+                    const uint32_t i = threadIdx.x * E + k;
                     key[i] = ok[k] ? ((uint64_t)rm[k] << 60) | rs[k] : kPad;
                     val[i] = ok[k] ? re[k] : 0;
                 }

@@ -144,3 +144,32 @@ def test_every_sort_size_and_input_order(ctx):
                 mm, ss, dd = np.full(n, 3), np.full(n, 777), np.full(n, 5)
             traces.append([(int(a), int(b), int(b + c)) for a, b, c in zip(mm, ss, dd)])
     _same(ctx, 8, *_pack(traces))
+
+
+def test_traces_in_end_order(ctx):
+    """Traces already in order of end time (as logged on completion) take a sweep without a sort;
+    ties of end time, zero-length and nested calls, all 8 LLMs, spans above and below 2^29 us, at
+    each chunk size (1, 2, 4 and 8 calls per thread).  Copies with one pair of neighbours swapped
+    (inside a thread's chunk, across two threads, across two waves) must take the sort and agree."""
+    rng = np.random.default_rng(31)
+    traces = []
+    for n in (1, 2, 3, 255, 256, 257, 511, 512, 513, 1023, 1024, 1025, 2047, 2048):
+        for span_bits in (20, 34):
+            m = rng.integers(0, 8, n)
+            s = rng.integers(0, 1 << span_bits, n)
+            d = rng.integers(0, 40_000, n)
+            d[rng.random(n) < 0.1] = 0                       # zero-length calls
+            e = s + d
+            e[rng.random(n) < 0.2] = e[0] if n else 0        # ties of end time
+            s = np.maximum(np.minimum(s, e), e - np.minimum(e, 40_000))   # durations < 2^32
+            idx = np.lexsort((s, e))
+            calls = [(int(a), int(b), int(c)) for a, b, c in zip(m[idx], s[idx], e[idx])]
+            traces.append(calls)
+            for pos in (0, 63, 127, 255, 511, n // 2):      # swap calls pos and pos + 1
+                if pos + 1 < n and calls[pos][2] != calls[pos + 1][2]:
+                    sw = list(calls)
+                    sw[pos], sw[pos + 1] = sw[pos + 1], sw[pos]
+                    traces.append(sw)
+    # one LLM only, nested calls all ending together
+    traces.append([(0, 1000 - i, 1000) for i in range(700)])
+    _same(ctx, 8, *_pack(traces))
