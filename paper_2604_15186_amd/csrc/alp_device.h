@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "alp_internal.h"
 
 namespace alp {
@@ -15,41 +17,73 @@ __device__ __forceinline__ bool lex_less(uint32_t aL, uint64_t ax, uint32_t bL, 
     return aL < bL || (aL == bL && ax < bx);
 }
 
-// Wave-wide lexicographic minimum of (L, x); every lane ends with the result.
+// Cross-lane reductions by DPP moves (no LDS round trip per step); every lane of the wave must
+// be active.  dpp_mov returns, in each lane of the rows selected by ROWMASK, the value of the
+// lane that CTRL names; other rows keep `old`.
+template <int CTRL, int ROWMASK = 0xF>
+__device__ __forceinline__ uint32_t dpp_mov(uint32_t old, uint32_t v)
+{
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)v, CTRL, ROWMASK, 0xF, false);
+}
+
+// The six steps of a wave reduction; lane 63 ends with the whole wave's value.  Quad swaps
+// (lane ^ 1, lane ^ 2), the row's half mirror and mirror (every lane then holds its 16-lane
+// row's value), lane 15 of each row into rows 1 and 3, lane 31 into rows 2 and 3.
+template <class Step>
+__device__ __forceinline__ void wave_reduce_steps(Step step)
+{
+    step(std::integral_constant<int, 0xB1>{}, std::integral_constant<int, 0xF>{});
+    step(std::integral_constant<int, 0x4E>{}, std::integral_constant<int, 0xF>{});
+    step(std::integral_constant<int, 0x141>{}, std::integral_constant<int, 0xF>{});
+    step(std::integral_constant<int, 0x140>{}, std::integral_constant<int, 0xF>{});
+    step(std::integral_constant<int, 0x142>{}, std::integral_constant<int, 0xA>{});
+    step(std::integral_constant<int, 0x143>{}, std::integral_constant<int, 0xC>{});
+}
+
+__device__ __forceinline__ uint32_t lane63(uint32_t v)
+{
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+}
+
+// Wave-wide lexicographic minimum of (L, x); every lane ends with the result (wave-uniform).
 __device__ __forceinline__ void wave_min(uint32_t &L, uint64_t &x)
 {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-        uint32_t oL = __shfl_xor(L, off, 64);
-        uint64_t ox = __shfl_xor((unsigned long long)x, off, 64);
-        if (lex_less(oL, ox, L, x)) {
-            L = oL;
-            x = ox;
-        }
-    }
+    uint32_t xl = (uint32_t)x, xh = (uint32_t)(x >> 32);
+    wave_reduce_steps([&](auto c, auto m) {
+        constexpr int C = decltype(c)::value, RM = decltype(m)::value;
+        const uint32_t oL = dpp_mov<C, RM>(L, L);
+        const uint32_t ol = dpp_mov<C, RM>(xl, xl), oh = dpp_mov<C, RM>(xh, xh);
+        const bool take = lex_less(oL, ((uint64_t)oh << 32) | ol, L, ((uint64_t)xh << 32) | xl);
+        L = take ? oL : L;
+        xl = take ? ol : xl;
+        xh = take ? oh : xh;
+    });
+    L = lane63(L);
+    x = ((uint64_t)lane63(xh) << 32) | lane63(xl);
 }
 
 // Wave-wide minima, returned as wave-uniform values.
 __device__ __forceinline__ uint32_t wave_min_u32(uint32_t v)
 {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-        const uint32_t o = __shfl_xor(v, off, 64);
+    wave_reduce_steps([&](auto c, auto m) {
+        constexpr int C = decltype(c)::value, RM = decltype(m)::value;
+        const uint32_t o = dpp_mov<C, RM>(v, v);
         v = o < v ? o : v;
-    }
-    return (uint32_t)__builtin_amdgcn_readfirstlane(v);
+    });
+    return lane63(v);
 }
 
 __device__ __forceinline__ uint64_t wave_min_u64(uint64_t v)
 {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-        const uint64_t o = __shfl_xor((unsigned long long)v, off, 64);
-        v = o < v ? o : v;
-    }
-    // readfirstlane works on int: widen through uint32_t, never sign-extend.
-    return ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(v >> 32)) << 32) |
-           (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)v);
+    uint32_t l = (uint32_t)v, h = (uint32_t)(v >> 32);
+    wave_reduce_steps([&](auto c, auto m) {
+        constexpr int C = decltype(c)::value, RM = decltype(m)::value;
+        const uint32_t ol = dpp_mov<C, RM>(l, l), oh = dpp_mov<C, RM>(h, h);
+        const bool take = oh < h || (oh == h && ol < l);
+        l = take ? ol : l;
+        h = take ? oh : h;
+    });
+    return ((uint64_t)lane63(h) << 32) | lane63(l);
 }
 
 // Block-wide minimum; thread 0 writes the block's winner.
@@ -64,17 +98,18 @@ __device__ __forceinline__ void block_min_store(uint32_t L, uint64_t x, Winner *
         sx[wave] = x;
     }
     __syncthreads();
-    if (threadIdx.x == 0) {
-        for (uint32_t w = 1; w < nw; ++w)
-            if (lex_less(sL[w], sx[w], L, x)) {
-                L = sL[w];
-                x = sx[w];
-            }
-        Winner r;
-        r.L = L;
-        r.pad = 0;
-        r.x = x;
-        *dst = r;
+    if (wave == 0) {
+        // Lane w reads wave w's minimum; one more wave reduction.
+        L = lane < nw ? sL[lane] : kNoLatency;
+        x = lane < nw ? sx[lane] : ~0ull;
+        wave_min(L, x);
+        if (lane == 0) {
+            Winner r;
+            r.L = L;
+            r.pad = 0;
+            r.x = x;
+            *dst = r;
+        }
     }
 }
 
@@ -139,15 +174,25 @@ __device__ __forceinline__ void write_result(const SpaceDev &sp, const uint2 *E,
         rep = (uint64_t)((o % sp.D + 1) & 0xFFu) << (8 * lane);
     }
     // Combine the (at most 8) LLM lanes: Eq. 2 minimum, unit sum, disjoint byte fields.
-#pragma unroll
-    for (int off = 1; off < ALP_MAX_LLMS; off <<= 1) {
-        const uint32_t oT = __shfl_xor(T, off, 64);
+    // DPP steps within each 8-lane half row: lane ^ 1, lane ^ 2, then the half mirror (lane i
+    // and 7 - i); every lane 0..7 ends with the total.
+    auto combine = [&](auto c) {
+        constexpr int C = decltype(c)::value;
+        const uint32_t oT = dpp_mov<C>(T, T);
         T = oT < T ? oT : T;
-        U += __shfl_xor(U, off, 64);
-        tp |= __shfl_xor((unsigned long long)tp, off, 64);
-        fq |= __shfl_xor((unsigned long long)fq, off, 64);
-        rep |= __shfl_xor((unsigned long long)rep, off, 64);
-    }
+        U += dpp_mov<C>(U, U);
+        auto or64 = [](uint64_t v) {
+            return v | ((uint64_t)dpp_mov<C>((uint32_t)(v >> 32), (uint32_t)(v >> 32)) << 32) |
+                   dpp_mov<C>((uint32_t)v, (uint32_t)v);
+        };
+        tp = or64(tp);
+        fq = or64(fq);
+        rep = or64(rep);
+    };
+    static_assert(ALP_MAX_LLMS <= 8, "the combine covers one 8-lane half row");
+    combine(std::integral_constant<int, 0xB1>{});
+    combine(std::integral_constant<int, 0x4E>{});
+    combine(std::integral_constant<int, 0x141>{});
     if (lane != 0)
         return;
     if (L == kNoLatency) {

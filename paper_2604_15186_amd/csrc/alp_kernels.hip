@@ -138,11 +138,11 @@ option_terms_kernel(SpaceDev sp, TablesDev tb, QueryDev q, uint32_t count, uint2
 // The argmin index is recovered exactly at the end.  Candidate indices order as (row, j,
 // option), and a wave walks its rows in increasing order.  Each lane-slot keeps its smallest
 // row latency oc + c_last + bq and the first row reaching it (a later row replaces it only
-// when strictly smaller).  At the end the wave takes the smallest latency L*, the lowest row r*
-// in which any lane-slot reaches L*, and scans that one row again to find, for those
-// lane-slots, the lowest j with c_j = L* - oc - c_last that is feasible; the smallest (j,
-// option) among them completes the lowest index reaching L*.  Only waves whose L* is their
-// block's minimum do this re-scan.
+// when strictly smaller).  At the end each wave takes its smallest latency L* and the lowest
+// row reaching it; the block takes the smallest (L*, row) over its waves, (Lb, rb), and all of
+// its waves scan their share of row rb again for the lowest feasible j with c_j = Lb - oc -
+// c_last per lane-slot; the smallest (j, option) completes the block's lowest index reaching
+// Lb.
 //
 // Work distribution.  Either each wave owns a fixed range of whole rows, or (DYNAMIC) a block
 // owns a range of sub-rows -- a row may be split into consecutive ranges of the inner LLM's
@@ -497,71 +497,76 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
             lmin = bestL[s] < lmin ? bestL[s] : lmin;
         Lstar = wave_min_u32(lmin);
     }
-    // Only waves whose L* is the block's smallest can hold the block's winner: they alone look
-    // up their index (the others wait at the block reduction and leave their SIMD to them).
+    // The wave's lowest sub-row reaching L* (its lane-slots' first rows at L*), as a sub-row
+    // index of the item.
+    uint64_t rwave = ~0ull;
+    if (Lstar != kNoLatency) {
+        uint32_t rmin = 0xFFFFFFFFu;
+#pragma unroll
+        for (int s = 0; s < S; ++s)
+            if (bestL[s] == Lstar && bestR[s] < rmin)
+                rmin = bestR[s];
+        rwave = r_begin + wave_min_u32(rmin);
+    }
+    // The block's smallest latency Lb and the lowest sub-row rb reaching it: the (L*, row)
+    // minimum over the waves.  Sub-rows are in candidate-index order, so the block's winner
+    // is the lowest candidate of sub-row rb with latency Lb.
     __shared__ uint32_t s_wave_L[16];
-    if (lane == 0)
+    __shared__ uint64_t s_wave_R[16];
+    if (lane == 0) {
         s_wave_L[wave] = Lstar;
+        s_wave_R[wave] = rwave;
+    }
     __syncthreads();
-    uint32_t Lblock = kNoLatency;
-    for (uint32_t k = 0; k < wpb; ++k)
-        Lblock = s_wave_L[k] < Lblock ? s_wave_L[k] : Lblock;
-    {
-        // The lowest row r* reaching L*; wave-uniform condition.
-        if (Lstar != kNoLatency && Lstar == Lblock) {
-            uint32_t rmin = 0xFFFFFFFFu;
+    // Lane k reads wave k's pair; one wave reduction (in every wave) gives the block's.
+    uint32_t Lblock = lane < wpb ? s_wave_L[lane] : kNoLatency;
+    uint64_t rb = lane < wpb ? s_wave_R[lane] : ~0ull;
+    wave_min(Lblock, rb);
+    if (Lblock != kNoLatency) {
+        // Every wave of the block searches its share of sub-row rb (4 records per step,
+        // steps interleaved over the waves) for the lowest feasible j of each lane-slot with
+        // c_j = Lb - oc - c_last: no wave re-walks a whole sub-row alone.  A feasible match
+        // has latency exactly Lb, since no sum of usable terms reaches 2^32 - 1 (a wrapped
+        // target is never met).
+        const uint64_t r = DYNAMIC ? rb / chunks : rb;
+        const uint32_t j0 = DYNAMIC ? (uint32_t)(rb % chunks) * chunk_len : 0u;
+        uint32_t oc;
+        int32_t ou;
+        outer_sums(R, O, n_outer, r, oc, ou);
+        uint32_t target[S], jf[S];
+        int32_t w[S];
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+            target[s] = Lblock - c_last[s] - oc;
+            w[s] = u_last[s] + ou;
+            jf[s] = kNoLatency;
+        }
+        if (has_inner) {
+            for (uint32_t jb = j0 + 4u * wave; jb < j0 + chunk_len; jb += 4u * wpb) {
+                uint2 v[4];
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+                    v[t] = inner[jb + t];
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+                    masked_find_step(jf, w, target, v[t].y, v[t].x, jb + t, full);
+            }
+        } else if (wave == 0) {
+            // One LLM: the row is the last LLM's options alone (j = 0).
 #pragma unroll
             for (int s = 0; s < S; ++s)
-                if (bestL[s] == Lstar && bestR[s] < rmin)
-                    rmin = bestR[s];
-            const uint32_t rstar = wave_min_u32(rmin);
-            const uint64_t r = DYNAMIC ? (r_begin + rstar) / chunks : r_begin + rstar;
-            const uint32_t j0 = DYNAMIC ? (uint32_t)((r_begin + rstar) % chunks) * chunk_len : 0u;
-            uint32_t oc;
-            int32_t ou;
-            outer_sums(R, O, n_outer, r, oc, ou);
-            // Lowest feasible j of row r* reaching L*, for each lane-slot that reaches it there
-            // (its target is the row's minimum c over its feasible j).
-            bool need[S];
-            uint32_t target[S], jf[S];
-            int32_t w[S];
-#pragma unroll
-            for (int s = 0; s < S; ++s) {
-                need[s] = bestL[s] == Lstar && bestR[s] == rstar;
-                target[s] = Lstar - c_last[s] - oc;
-                w[s] = need[s] ? u_last[s] + ou : 0x7FFFFFFF;
-                jf[s] = has_inner ? kNoLatency : 0u;
-            }
-            if (has_inner) {
-                // 16 records per step (two scalar loads), stop once every lane-slot has its j;
-                // the padding records are never feasible, so they never match.
-                for (uint32_t jb = j0; jb < j0 + chunk_len; jb += 16) {
-                    uint2 v[16];
-#pragma unroll
-                    for (int t = 0; t < 16; ++t)
-                        v[t] = inner[jb + t];
-#pragma unroll
-                    for (int t = 0; t < 16; ++t)
-                        masked_find_step(jf, w, target, v[t].y, v[t].x, jb + t, full);
-                    bool open = false;
-#pragma unroll
-                    for (int s = 0; s < S; ++s)
-                        open |= need[s] && jf[s] == kNoLatency;
-                    if (!__any(open))
-                        break;
-                }
-            }
-            uint64_t xmin = ~0ull;
-#pragma unroll
-            for (int s = 0; s < S; ++s) {
-                if (need[s]) {
-                    const uint64_t x = (r * n_inner + jf[s]) * (uint64_t)O + o_last[s];
-                    xmin = x < xmin ? x : xmin;
-                }
-            }
-            waveL = Lstar;
-            waveX = wave_min_u64(xmin);
+                jf[s] = w[s] <= capacity && c_last[s] + oc == Lblock ? 0u : kNoLatency;
         }
+        uint64_t xmin = ~0ull;
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+            if (jf[s] != kNoLatency) {
+                const uint64_t x = (r * n_inner + jf[s]) * (uint64_t)O + o_last[s];
+                xmin = x < xmin ? x : xmin;
+            }
+        }
+        waveL = Lblock;
+        waveX = wave_min_u64(xmin);
     }
     block_finish(waveL, waveX, item, sub, blocks_per_item, winners, fa);
 }
