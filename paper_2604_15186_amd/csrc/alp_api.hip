@@ -334,7 +334,8 @@ alp::ScanGeometry plan_scan(alp_ctx *c, uint32_t count)
         // shares its issue slots among them, and rows may be split into sub-rows of the inner
         // LLM's records.  Plan: at most 16 waves per CU over the whole batch and at least two
         // of the finest sub-rows per wave; blocks of 8 waves while that leaves CUs without a
-        // block, else of 16; rows split so that a wave gets about 8 sub-rows.
+        // block, else of 16; rows split so that a wave gets about 4 sub-rows (a wave claims its next
+        // sub-row late, so whole sub-rows balance well and keep the per-sub-row work small).
         const bool splittable = g.variant == 1 && sp.M >= 2;
         const uint32_t n16 = alp::inner_stride(sp.O) / 16;      // chunks must divide this
         bool dyn = g.variant == 1 && c->variant != 4 &&
@@ -358,7 +359,7 @@ alp::ScanGeometry plan_scan(alp_ctx *c, uint32_t count)
             } else if (splittable) {
                 g.chunks = n16;
                 for (uint32_t k = 1; k <= n16; ++k)
-                    if (n16 % k == 0 && g.rows * k >= 8 * bpi * wpb) {
+                    if (n16 % k == 0 && g.rows * k >= 4 * bpi * wpb) {
                         g.chunks = k;
                         break;
                     }
@@ -474,7 +475,10 @@ int32_t launch_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count, alp_re
         return hip_fail(e, "hipMalloc(ext)");
     if ((e = c->inner.ensure((uint64_t)count * alp::inner_stride(sp.O) * sizeof(uint2))) != hipSuccess)
         return hip_fail(e, "hipMalloc(inner)");
-    if ((e = c->done.ensure((uint64_t)count * sizeof(uint32_t))) != hipSuccess)
+    // done[count], then best[count] at least 4 KiB further: the two per-item words take one
+    // atomic per block each, and counters in one line would queue behind each other.
+    const uint64_t best_at = ((uint64_t)count + 2047) / 1024 * 1024;
+    if ((e = c->done.ensure((best_at + count) * sizeof(uint32_t))) != hipSuccess)
         return hip_fail(e, "hipMalloc(done)");
     if ((e = c->winners.ensure(nwin * sizeof(alp::Winner))) != hipSuccess)
         return hip_fail(e, "hipMalloc(winners)");
@@ -485,9 +489,15 @@ int32_t launch_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count, alp_re
     fa.sp = sp;
     fa.ext = ext;
     fa.done = (uint32_t *)c->done.ptr;
+    fa.best = fa.done + best_at;
     fa.out = out;
     fa.invalid = raw ? raw->invalid : nullptr;
-    if ((e = alp::launch_option_terms(sp, c->tdev, q, count, rec, ext, inner, fa.done, c->stream,
+    alp::ScanReset reset;
+    reset.done = fa.done;
+    reset.best = fa.best;
+    reset.winners = win;
+    reset.n_winners = nwin;
+    if ((e = alp::launch_option_terms(sp, c->tdev, q, count, rec, ext, inner, reset, c->stream,
                                       raw, timed ? ev[0] : nullptr, timed ? ev[1] : nullptr)) !=
         hipSuccess)
         return hip_fail(e, "option_terms launch");
@@ -797,7 +807,8 @@ int32_t alp_max_throughput(alp_ctx *ctx, uint32_t count, const uint32_t *instanc
         (e = ctx->ext.ensure(items_bytes)) != hipSuccess)
         return hip_fail(e, "hipMalloc(max_throughput)");
     if ((e = alp::launch_option_terms(ctx->sp, ctx->tdev, q, count, (uint2 *)ctx->rec.ptr,
-                                      (uint2 *)ctx->ext.ptr, nullptr, nullptr, ctx->stream)) != hipSuccess)
+                                      (uint2 *)ctx->ext.ptr, nullptr, alp::ScanReset{}, ctx->stream)) !=
+        hipSuccess)
         return hip_fail(e, "option_terms launch");
     if ((e = alp::launch_tmax(ctx->sp, q, count, (const uint2 *)ctx->ext.ptr,
                               (uint32_t *)ctx->tmax.ptr, ctx->stream)) != hipSuccess)
@@ -996,8 +1007,10 @@ int32_t alp_search_pruned(alp_ctx *ctx, uint32_t count, const uint32_t *instance
     uint32_t *done = (uint32_t *)ctx->done.ptr;
     if (ctx->timing && (e = hipEventRecord(ctx->ev[0], ctx->stream)) != hipSuccess)
         return hip_fail(e, "hipEventRecord");
+    alp::ScanReset reset;
+    reset.done = done;                       // the pruned scan publishes every block's winner
     if ((e = alp::launch_option_terms(sp, ctx->tdev, q, count, rec, ext, (uint2 *)ctx->inner.ptr,
-                                      done, ctx->stream)) != hipSuccess)
+                                      reset, ctx->stream)) != hipSuccess)
         return hip_fail(e, "option_terms launch");
     if (ctx->timing && (e = hipEventRecord(ctx->ev[1], ctx->stream)) != hipSuccess)
         return hip_fail(e, "hipEventRecord");
@@ -1137,7 +1150,8 @@ int32_t alp_eval_candidates(alp_ctx *ctx, uint32_t instance, uint32_t gpu_budget
                             ctx->stream)) != hipSuccess)
         return hip_fail(e, "copy indices");
     if ((e = alp::launch_option_terms(ctx->sp, ctx->tdev, q, 1, (uint2 *)ctx->rec.ptr,
-                                      (uint2 *)ctx->ext.ptr, nullptr, nullptr, ctx->stream)) != hipSuccess)
+                                      (uint2 *)ctx->ext.ptr, nullptr, alp::ScanReset{}, ctx->stream)) !=
+        hipSuccess)
         return hip_fail(e, "option_terms launch");
     if ((e = alp::launch_eval(ctx->sp, q.cap1, (const uint2 *)ctx->rec.ptr, (const uint2 *)ctx->ext.ptr,
                               (const uint64_t *)ctx->idx.ptr, count, (alp_eval_t *)ctx->evals.ptr,

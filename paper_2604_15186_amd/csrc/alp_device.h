@@ -86,8 +86,9 @@ __device__ __forceinline__ uint64_t wave_min_u64(uint64_t v)
     return ((uint64_t)lane63(h) << 32) | lane63(l);
 }
 
-// Block-wide minimum; thread 0 writes the block's winner.
-__device__ __forceinline__ void block_min_store(uint32_t L, uint64_t x, Winner *dst)
+// Block-wide lexicographic minimum of (L, x); wave 0 ends with it (wave-uniform), other waves
+// keep their wave's minimum.
+__device__ __forceinline__ void block_min(uint32_t &L, uint64_t &x)
 {
     __shared__ uint32_t sL[16];
     __shared__ uint64_t sx[16];
@@ -103,14 +104,24 @@ __device__ __forceinline__ void block_min_store(uint32_t L, uint64_t x, Winner *
         L = lane < nw ? sL[lane] : kNoLatency;
         x = lane < nw ? sx[lane] : ~0ull;
         wave_min(L, x);
-        if (lane == 0) {
-            Winner r;
-            r.L = L;
-            r.pad = 0;
-            r.x = x;
-            *dst = r;
-        }
     }
+}
+
+__device__ __forceinline__ void store_winner(uint32_t L, uint64_t x, Winner *dst)
+{
+    Winner r;
+    r.L = L;
+    r.pad = 0;
+    r.x = x;
+    *dst = r;
+}
+
+// Block-wide minimum; thread 0 writes the block's winner.
+__device__ __forceinline__ void block_min_store(uint32_t L, uint64_t x, Winner *dst)
+{
+    block_min(L, x);
+    if (threadIdx.x == 0)
+        store_winner(L, x, dst);
 }
 
 // Lexicographic (L, x) minimum of an item's block winners, by one wave; every lane gets it.
@@ -160,11 +171,16 @@ __device__ __forceinline__ void write_result(const SpaceDev &sp, const uint2 *E,
     uint32_t T = 0xFFFFFFFFu, U = 0;
     uint64_t tp = 0, fq = 0, rep = 0;
     if (L != kNoLatency && lane < sp.M) {
-        // o_m = floor(x / O^(M-1-m)) mod O  (candidate index, LLM 0 most significant)
+        // o_m = floor(x / O^(M-1-m)) mod O  (candidate index, LLM 0 most significant); 32-bit
+        // division whenever x allows it.
         uint64_t scale = 1;
         for (uint32_t k = lane + 1; k < sp.M; ++k)
             scale *= sp.O;
-        const uint32_t o = (uint32_t)((x / scale) % sp.O);
+        uint32_t o;
+        if ((x >> 32) == 0)
+            o = (scale >> 32) != 0 ? 0u : (uint32_t)x / (uint32_t)scale % sp.O;
+        else
+            o = (uint32_t)((x / scale) % sp.O);
         const uint2 e = E[(uint64_t)lane * sp.O + o];
         T = e.x;
         U = e.y & 0xFFFFu;
@@ -212,6 +228,19 @@ __device__ __forceinline__ void write_result(const SpaceDev &sp, const uint2 *E,
     dst[5] = rep;
 }
 
+// Result record of one item whose winner is (L, x), by one wave.  E: the item's per-option
+// records, or nullptr for their copy in fa.ext.
+__device__ __forceinline__ void write_item_result(const FinishArgs &fa, uint32_t item, uint32_t L,
+                                                  uint64_t x, const uint2 *E = nullptr)
+{
+    const bool rejected = fa.invalid && fa.invalid[item];
+    if (!E)
+        E = fa.ext + (uint64_t)item * fa.sp.M * fa.sp.O;
+    write_result(fa.sp, E, rejected ? kNoLatency : L, x,
+                 reinterpret_cast<uint64_t *>(fa.out + item),
+                 rejected ? (uint32_t)ALP_EINVAL : (uint32_t)ALP_INFEASIBLE);
+}
+
 // Result of one item from its block winners, by one wave.
 __device__ __forceinline__ void finish_item(const FinishArgs &fa, uint32_t item,
                                             uint32_t blocks_per_item, const Winner *winners)
@@ -219,10 +248,7 @@ __device__ __forceinline__ void finish_item(const FinishArgs &fa, uint32_t item,
     uint32_t L;
     uint64_t x;
     item_winner(item, blocks_per_item, winners, L, x);
-    const bool rejected = fa.invalid && fa.invalid[item];
-    write_result(fa.sp, fa.ext + (uint64_t)item * fa.sp.M * fa.sp.O, rejected ? kNoLatency : L, x,
-                 reinterpret_cast<uint64_t *>(fa.out + item),
-                 rejected ? (uint32_t)ALP_EINVAL : (uint32_t)ALP_INFEASIBLE);
+    write_item_result(fa, item, L, x);
 }
 
 // Writes the block's winner and counts the block as finished (agent-scope fence and per-item
@@ -252,37 +278,72 @@ __device__ __forceinline__ bool block_store_last(uint32_t L, uint64_t x, uint32_
     return last;
 }
 
-// Writes the block's winner; the last block of the item to finish (agent-scope fence and
-// counter, zeroed by option_terms_kernel before the scan) reduces the item's winners and
-// writes its result, so no separate reduction kernel is launched.
+// Per-option records of one item the finishing block stages in LDS (M * O at most this many).
+constexpr uint32_t kFinishStage = 2048;
+
+// The block's winner and the item's completion: the last block of the item to finish reduces
+// the item's winners and writes its result, so no separate reduction kernel is launched.
+// Publishing a winner takes an agent-scope release (an L2 write-back), so a block first takes
+// the atomic minimum of the item's best latency: if an earlier block already reached a smaller
+// latency, this block cannot hold the item's winner and only counts itself (its slot keeps the
+// "no candidate" the option-term kernel wrote).  Blocks at or below the minimum so far store
+// their winner and release it before counting; later relaxed counts continue that release
+// sequence, so the last block's acquire sees every stored winner.  The counter, the minimum and
+// the slots are reset by option_terms_kernel before each scan.
+//
+// `hint`: the item's best latency as read earlier in this launch (kNoLatency if not read); the
+// minimum only falls, so a block above the hint skips the atomic minimum too (a plain load
+// does not queue at the atomic unit behind the other blocks' updates).
 __device__ __forceinline__ void block_finish(uint32_t L, uint64_t x, uint32_t item,
                                              uint32_t sub, uint32_t blocks_per_item,
-                                             Winner *winners, const FinishArgs &fa)
+                                             Winner *winners, const FinishArgs &fa,
+                                             uint32_t hint = kNoLatency)
 {
     __shared__ uint32_t last_block;
-    block_min_store(L, x, &winners[(uint64_t)item * blocks_per_item + sub]);
+    Winner *slot = &winners[(uint64_t)item * blocks_per_item + sub];
     if (blocks_per_item == 1) {
-        // The block is the whole item: no agent-scope fence (an L2 write-back across XCDs) or
-        // counter; its winner only needs to reach its own first wave.
+        // The block is the whole item: no agent-scope fence or counter; its winner only needs
+        // to reach its own first wave.
+        block_min_store(L, x, slot);
         __threadfence_block();
         __syncthreads();
         if (threadIdx.x < 64)
             finish_item(fa, item, 1, winners);
         return;
     }
+    block_min(L, x);
     if (threadIdx.x == 0) {
-        // Release: the block's winner is visible before its count (an L2 write-back; no
-        // invalidate needed here).
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        if (L != kNoLatency && L <= hint && L <= atomicMin(&fa.best[item], L)) {
+            store_winner(L, x, slot);
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        }
         const uint32_t prev = atomicAdd(&fa.done[item], 1u);
         last_block = prev == blocks_per_item - 1 ? 1u : 0u;
     }
     __syncthreads();
-    if (last_block && threadIdx.x < 64) {
-        // Acquire: every counted block's winner is visible (an invalidate; no write-back).
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-        finish_item(fa, item, blocks_per_item, winners);
+    if (!last_block)
+        return;
+    // The item's per-option records (written by the previous kernel) are staged in LDS by the
+    // other waves while wave 0 loads the winners, so the result's records cost no second
+    // memory round trip.
+    __shared__ uint2 s_ext[kFinishStage];
+    const uint32_t nE = fa.sp.M * fa.sp.O;
+    const bool staged = nE <= kFinishStage && blockDim.x > 64;
+    if (staged && threadIdx.x >= 64) {
+        const uint2 *E = fa.ext + (uint64_t)item * nE;
+        for (uint32_t k = threadIdx.x - 64; k < nE; k += blockDim.x - 64)
+            s_ext[k] = E[k];
     }
+    uint32_t Lw = kNoLatency;
+    uint64_t xw = ~0ull;
+    if (threadIdx.x < 64) {
+        // Acquire: every stored winner is visible (an invalidate; no write-back).
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        item_winner(item, blocks_per_item, winners, Lw, xw);
+    }
+    __syncthreads();
+    if (threadIdx.x < 64)
+        write_item_result(fa, item, Lw, xw, staged ? s_ext : nullptr);
 }
 
 // Workgroups are dispatched to the 8 XCDs round-robin; renumber them so that consecutive

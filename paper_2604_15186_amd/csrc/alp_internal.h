@@ -67,6 +67,8 @@ struct FinishArgs {
     SpaceDev sp;
     const uint2 *ext;          // per-option (tau, u | flags) of the query
     uint32_t *done;            // per-item finished-block counter, zeroed by the option-term kernel
+    uint32_t *best;            // per-item smallest block latency seen so far (atomic minimum),
+                               // kNoLatency from the option-term kernel
     alp_result_t *out;         // per-item results (device-visible, may be mapped host memory)
     const uint32_t *invalid;   // per-item: nonzero = the query was rejected (result EINVAL);
                                // nullptr = every query valid
@@ -97,9 +99,20 @@ struct RawQueries {
     uint32_t *q_inst, *q_cap, *q_lambda, *invalid;
 };
 
+// What the option-term kernel resets for the scan that follows it: per item, the finished-block
+// counter (done = 0) and the smallest block latency (best = kNoLatency, if best is set); every
+// block winner slot (winners[0..n_winners) = no candidate).
+struct ScanReset {
+    uint32_t *done = nullptr;
+    uint32_t *best = nullptr;
+    Winner *winners = nullptr;
+    uint64_t n_winners = 0;
+};
+
 hipError_t launch_option_terms(const SpaceDev &sp, const TablesDev &tb, const QueryDev &q,
-                               uint32_t count, uint2 *rec, uint2 *ext, uint2 *inner, uint32_t *done,
-                               hipStream_t st, const RawQueries *raw = nullptr,
+                               uint32_t count, uint2 *rec, uint2 *ext, uint2 *inner,
+                               const ScanReset &reset, hipStream_t st,
+                               const RawQueries *raw = nullptr,
                                hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
 hipError_t launch_scan(const SpaceDev &sp, const QueryDev &q, uint32_t count, const uint2 *rec,
                        const uint2 *inner, const ScanGeometry &g, Winner *winners,

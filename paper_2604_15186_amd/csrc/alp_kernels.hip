@@ -34,10 +34,10 @@ constexpr int32_t kNeverFits = -(1 << 30);          // remaining units no lane c
 //    ext[item][m][o] = (tau, u | ok << 16 | thr_ok << 17)
 //    inner[item][o]  = (c, capacity - (usable ? u : sentinel)) for m = M-2 (if inner != nullptr):
 //                      the share units left for the other LLMs once LLM M-2 takes option o
-//    done[item]      = 0 (if done != nullptr): the scan's finished-block counter
+//    done[item]      = 0, best[item] = kNoLatency, winners[] = no candidate (see ScanReset)
 __global__ void __launch_bounds__(256)
 option_terms_kernel(SpaceDev sp, TablesDev tb, QueryDev q, uint32_t count, uint2 *__restrict__ rec,
-                    uint2 *__restrict__ ext, uint2 *__restrict__ inner, uint32_t *__restrict__ done,
+                    uint2 *__restrict__ ext, uint2 *__restrict__ inner, ScanReset reset,
                     RawQueries raw)
 {
     const uint64_t per_item = (uint64_t)sp.M * sp.O;
@@ -47,8 +47,18 @@ option_terms_kernel(SpaceDev sp, TablesDev tb, QueryDev q, uint32_t count, uint2
     const uint32_t item = (uint32_t)(t / per_item);
     const uint32_t rem = (uint32_t)(t - (uint64_t)item * per_item);
     const uint32_t m = rem / sp.O, o = rem - m * sp.O;
-    if (done && rem == 0)
-        done[item] = 0;                              // block counter of the fused reduction
+    // State of the scan's fused reduction.
+    if (reset.done && rem == 0)
+        reset.done[item] = 0;
+    if (reset.best && rem == 0)
+        reset.best[item] = kNoLatency;
+    for (uint64_t i = t; i < reset.n_winners; i += per_item * count) {
+        Winner w;
+        w.L = kNoLatency;
+        w.pad = 0;
+        w.x = ~0ull;
+        reset.winners[i] = w;
+    }
     uint32_t inst, capacity;
     uint64_t lambda;
     if (raw.budget) {
@@ -416,9 +426,6 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
             if (DYNAMIC) {
                 if (r_begin + cur >= r_end)
                     break;
-                // Claim the wave's next sub-row now; the answer is used after this one.
-                if (lane == 0)
-                    next = atomicAdd(&s_next, 1u);
                 uint32_t row = divmod((uint32_t)(r_begin + cur), chunks, inv_ch, chunk);
 #pragma unroll
                 for (int k = NMAX - 1; k >= 0; --k) {
@@ -452,8 +459,9 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
                 // records no lane can use): two 64-byte scalar loads issued together, so the
                 // loop's own scalar work stays small next to the 2 x 16 x S VALU operations.
                 const uint2 *const begin = DYNAMIC ? inner + chunk * chunk_len : inner;
-                const uint2 *const end = DYNAMIC ? begin + chunk_len : inner + n_inner_padded;
-                for (const uint2 *p = begin; p != end; p += 16) {
+                const uint2 *const last16 =
+                    (DYNAMIC ? begin + chunk_len : inner + n_inner_padded) - 16;
+                auto batch = [&](const uint2 *p) {
                     uint2 v0[8], v1[8];
 #pragma unroll
                     for (int t = 0; t < 8; ++t) {
@@ -462,8 +470,18 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
                     }
                     masked_min_8(bq, w, v0, full);
                     masked_min_8(bq, w, v1, full);
-                }
+                };
+                for (const uint2 *p = begin; p != last16; p += 16)
+                    batch(p);
+                // Claim the wave's next sub-row before the last 16 records, which hide the
+                // claim's latency; claiming earlier would commit a slowly issued wave to
+                // more work than the others while the block's range runs out.
+                if (DYNAMIC && lane == 0)
+                    next = atomicAdd(&s_next, 1u);
+                batch(last16);
             } else {
+                if (DYNAMIC && lane == 0)
+                    next = atomicAdd(&s_next, 1u);
                 masked_min_step(bq, w, (uint32_t)capacity, 0u, full);
             }
             // Row minimum per lane-slot (saturating: no feasible j leaves kNoLatency).
@@ -497,9 +515,18 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
             lmin = bestL[s] < lmin ? bestL[s] : lmin;
         Lstar = wave_min_u32(lmin);
     }
+    // The item's best latency so far, loaded now so that the load overlaps the block's
+    // reductions (see block_finish).
+    uint32_t hint = kNoLatency;
+    if (threadIdx.x == 0 && blocks_per_item > 1)
+        hint = __hip_atomic_load(&fa.best[item], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     // The wave's lowest sub-row reaching L* (its lane-slots' first rows at L*), as a sub-row
     // index of the item.
+    // Its row's outer sums are loaded now, while the block's other waves finish (claimed
+    // sub-rows number fewer than 2^32).
     uint64_t rwave = ~0ull;
+    uint32_t oc_w = 0;
+    int32_t ou_w = 0;
     if (Lstar != kNoLatency) {
         uint32_t rmin = 0xFFFFFFFFu;
 #pragma unroll
@@ -507,32 +534,39 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
             if (bestL[s] == Lstar && bestR[s] < rmin)
                 rmin = bestR[s];
         rwave = r_begin + wave_min_u32(rmin);
+        outer_sums(R, O, n_outer, DYNAMIC ? (uint32_t)rwave / chunks : rwave, oc_w, ou_w);
     }
     // The block's smallest latency Lb and the lowest sub-row rb reaching it: the (L*, row)
     // minimum over the waves.  Sub-rows are in candidate-index order, so the block's winner
     // is the lowest candidate of sub-row rb with latency Lb.
-    __shared__ uint32_t s_wave_L[16];
+    __shared__ uint32_t s_wave_L[16], s_wave_oc[16];
+    __shared__ int32_t s_wave_ou[16];
     __shared__ uint64_t s_wave_R[16];
     if (lane == 0) {
         s_wave_L[wave] = Lstar;
         s_wave_R[wave] = rwave;
+        s_wave_oc[wave] = oc_w;
+        s_wave_ou[wave] = ou_w;
     }
     __syncthreads();
     // Lane k reads wave k's pair; one wave reduction (in every wave) gives the block's.
-    uint32_t Lblock = lane < wpb ? s_wave_L[lane] : kNoLatency;
-    uint64_t rb = lane < wpb ? s_wave_R[lane] : ~0ull;
+    const uint32_t mineL = lane < wpb ? s_wave_L[lane] : kNoLatency;
+    const uint64_t mineR = lane < wpb ? s_wave_R[lane] : ~0ull;
+    uint32_t Lblock = mineL;
+    uint64_t rb = mineR;
     wave_min(Lblock, rb);
     if (Lblock != kNoLatency) {
         // Every wave of the block searches its share of sub-row rb (4 records per step,
         // steps interleaved over the waves) for the lowest feasible j of each lane-slot with
         // c_j = Lb - oc - c_last: no wave re-walks a whole sub-row alone.  A feasible match
         // has latency exactly Lb, since no sum of usable terms reaches 2^32 - 1 (a wrapped
-        // target is never met).
-        const uint64_t r = DYNAMIC ? rb / chunks : rb;
-        const uint32_t j0 = DYNAMIC ? (uint32_t)(rb % chunks) * chunk_len : 0u;
-        uint32_t oc;
-        int32_t ou;
-        outer_sums(R, O, n_outer, r, oc, ou);
+        // target is never met).  Sub-rows are distinct across waves, so exactly one wave
+        // reported rb; its outer sums are taken from LDS.
+        const uint64_t r = DYNAMIC ? (uint32_t)rb / chunks : rb;
+        const uint32_t j0 = DYNAMIC ? (uint32_t)rb % chunks * chunk_len : 0u;
+        const uint32_t src = (uint32_t)__builtin_ctzll(__ballot(mineL == Lblock && mineR == rb));
+        const uint32_t oc = s_wave_oc[src];
+        const int32_t ou = s_wave_ou[src];
         uint32_t target[S], jf[S];
         int32_t w[S];
 #pragma unroll
@@ -568,7 +602,7 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
         waveL = Lblock;
         waveX = wave_min_u64(xmin);
     }
-    block_finish(waveL, waveX, item, sub, blocks_per_item, winners, fa);
+    block_finish(waveL, waveX, item, sub, blocks_per_item, winners, fa, hint);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -868,9 +902,9 @@ tmax_kernel(SpaceDev sp, QueryDev q, const uint2 *__restrict__ ext, uint32_t *__
 // the kernels, which would leave the GPU idle for microseconds per search).
 
 hipError_t launch_option_terms(const SpaceDev &sp, const TablesDev &tb, const QueryDev &q,
-                               uint32_t count, uint2 *rec, uint2 *ext, uint2 *inner, uint32_t *done,
-                               hipStream_t st, const RawQueries *raw, hipEvent_t t0,
-                               hipEvent_t t1)
+                               uint32_t count, uint2 *rec, uint2 *ext, uint2 *inner,
+                               const ScanReset &reset, hipStream_t st, const RawQueries *raw,
+                               hipEvent_t t0, hipEvent_t t1)
 {
     const uint64_t total = (uint64_t)count * sp.M * sp.O;
     if (total == 0)
@@ -878,7 +912,7 @@ hipError_t launch_option_terms(const SpaceDev &sp, const TablesDev &tb, const Qu
     const uint32_t blocks = (uint32_t)((total + 255) / 256);
     RawQueries none{};
     hipExtLaunchKernelGGL(option_terms_kernel, dim3(blocks), dim3(256), 0, st, t0, t1, 0, sp, tb, q,
-                          count, rec, ext, inner, done, raw ? *raw : none);
+                          count, rec, ext, inner, reset, raw ? *raw : none);
     return hipGetLastError();
 }
 
