@@ -1272,7 +1272,7 @@ void alp_free(alp_ctx *ctx)
 struct alp_stats_ctx {
     int device = 0;
     hipStream_t stream = nullptr;
-    DevBuf totals, long_list, long_base, scratch;
+    DevBuf totals, long_list, long_base, scratch, work;
     alp_stats_t *host_out = nullptr;        // mapped pinned: results
     alp_stats_t *host_out_dev = nullptr;
     std::vector<uint64_t> offsets;
@@ -1301,7 +1301,7 @@ int32_t alp_stats_create(alp_stats_ctx **out, int32_t device, void *hip_stream)
     for (int k = 0; k < 2 && e == hipSuccess; ++k)
         e = hipEventCreate(&c->ev[k]);
     if (e == hipSuccess)
-        e = c->totals.ensure((3 * ALP_MAX_LLMS + 1) * sizeof(uint64_t));
+        e = c->totals.ensure((alp::kStatsTotalsWords + 2) * sizeof(uint64_t));
     if (e != hipSuccess) {
         alp_stats_free(c);
         return hip_fail(e, "statistics context");
@@ -1368,14 +1368,17 @@ int32_t alp_trace_stats(alp_stats_ctx *c, uint32_t num_llms, uint32_t num_traces
                                 hipMemcpyHostToDevice, c->stream)) != hipSuccess)
             return hip_fail(e, "copy long traces");
     }
+    if ((e = c->work.ensure((uint64_t)num_traces * sizeof(uint32_t))) != hipSuccess)
+        return hip_fail(e, "hipMalloc(statistics work list)");
     uint64_t *totals = (uint64_t *)c->totals.ptr;
-    uint32_t *flags = (uint32_t *)(totals + 3 * ALP_MAX_LLMS);
+    uint32_t *flags = (uint32_t *)(totals + alp::kStatsTotalsWords);
     if (c->timing && (e = hipEventRecord(c->ev[0], c->stream)) != hipSuccess)
         return hip_fail(e, "hipEventRecord");
     if ((e = alp::launch_trace_stats(num_llms, num_traces, offsets, llm, start_us, end_us, lds_cap,
                                      (uint32_t)longs.size(), (const uint32_t *)c->long_list.ptr,
                                      (const uint64_t *)c->long_base.ptr, (uint64_t *)c->scratch.ptr,
-                                     totals, flags, c->host_out_dev, c->stream)) != hipSuccess)
+                                     totals, (uint32_t *)c->work.ptr, c->host_out_dev,
+                                     c->stream)) != hipSuccess)
         return hip_fail(e, "statistics launch");
     if (c->timing && (e = hipEventRecord(c->ev[1], c->stream)) != hipSuccess)
         return hip_fail(e, "hipEventRecord");
@@ -1426,7 +1429,7 @@ void alp_stats_free(alp_stats_ctx *c)
     for (int k = 0; k < 2; ++k)
         if (c->ev[k])
             (void)hipEventDestroy(c->ev[k]);
-    DevBuf *bufs[] = {&c->totals, &c->long_list, &c->long_base, &c->scratch};
+    DevBuf *bufs[] = {&c->totals, &c->long_list, &c->long_base, &c->scratch, &c->work};
     for (DevBuf *b : bufs)
         b->release();
     if (c->host_out)

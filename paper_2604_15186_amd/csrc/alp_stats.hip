@@ -8,26 +8,30 @@
 //         active.  n_m and p_m are reported in thousandths, rounded down.
 //
 // Kernels:
-//   stats_init_kernel        zeroes the per-LLM totals and the error flags.
-//   trace_stats_kernel<G>    one workgroup per trace.  A trace of at most 2,048 calls that is
-//                            already in order of end time (calls logged on completion) is swept
-//                            backwards without a sort: a call adds the part of it before the
-//                            earliest start of the same LLM's later calls.  Otherwise the calls
-//                            are sorted by key
-//                            (llm << 60 | start) with a bitonic network (in LDS, or for long
-//                            traces in a global scratch region, G = true); the time covered by
+//   stats_init_kernel        zeroes the per-LLM totals, the error flags and the work-list count.
+//   trace_sweep_kernel<MM>   one workgroup per trace of at most 2,048 calls (MM bounds the number
+//                            of LLMs, so the per-LLM state fits in few registers).  A trace already
+//                            in order of end time (calls logged on completion) is swept backwards
+//                            without a sort: a call adds the part of it before the earliest start
+//                            of the same LLM's later calls.  Other traces go to a work list.
+//   trace_sort_kernel        the work list: calls sorted by key (llm << 60 | start), packed into
+//                            one 64-bit key when the starts span under 2^29 us, with a bitonic
+//                            network in registers, across lanes and in LDS; the time covered by
 //                            each LLM follows from an exclusive prefix maximum of
 //                            (llm << 61 | end) -- an interval adds the part of it beyond the
-//                            furthest end of the same LLM's earlier intervals; per-LLM call
-//                            counts, durations and covered time are summed in LDS and added to
-//                            the global totals with 64-bit atomics (integer sums: the result
-//                            does not depend on their order).
+//                            furthest end of the same LLM's earlier intervals.
+//   trace_long_kernel        traces beyond 2,048 calls, sorted the same way in a global scratch
+//                            region.
+//   In each, per-LLM call counts, durations and covered time are summed per block and added to
+//   one of kStatsCopies copies of the totals with 64-bit atomics (integer sums: the result does
+//   not depend on their order).
 //   stats_finish_kernel      n and p per LLM from the totals, written with the error flags.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 #include <type_traits>
 
+#include "alp_device.h"
 #include "alp_internal.h"
 
 namespace alp {
@@ -96,25 +100,28 @@ __device__ __forceinline__ void block_min_max_sum(uint64_t &lo, uint64_t &hi, ui
 {
     __shared__ uint64_t s_lo[kThreads / 64], s_hi[kThreads / 64];
     __shared__ uint32_t s_cnt[kThreads / 64];
-    auto step = [&](auto q_const) {
-        constexpr int Q = decltype(q_const)::value;
-        const uint64_t a = lane_xor64<Q>(lo), b = lane_xor64<Q>(hi);
-        lo = a < lo ? a : lo;
-        hi = b > hi ? b : hi;
-        cnt += lane_xor<Q>(cnt);
-    };
-    step(std::integral_constant<int, 32>{});
-    step(std::integral_constant<int, 16>{});
-    step(std::integral_constant<int, 8>{});
-    step(std::integral_constant<int, 4>{});
-    step(std::integral_constant<int, 2>{});
-    step(std::integral_constant<int, 1>{});
-    if ((threadIdx.x & 63) == 0) {
-        s_lo[threadIdx.x >> 6] = lo;
-        s_hi[threadIdx.x >> 6] = hi;
+    // Wave reductions by DPP row moves; lane 63 ends with the wave's values.
+    uint32_t ll = (uint32_t)lo, lh = (uint32_t)(lo >> 32), hl = (uint32_t)hi, hh = (uint32_t)(hi >> 32);
+    wave_reduce_steps([&](auto c, auto m) {
+        constexpr int C = decltype(c)::value, RM = decltype(m)::value;
+        const uint64_t a = ((uint64_t)dpp_mov<C, RM>(lh, lh) << 32) | dpp_mov<C, RM>(ll, ll);
+        const uint64_t b = ((uint64_t)dpp_mov<C, RM>(hh, hh) << 32) | dpp_mov<C, RM>(hl, hl);
+        const uint64_t l = ((uint64_t)lh << 32) | ll, h = ((uint64_t)hh << 32) | hl;
+        const uint64_t nl = a < l ? a : l, nh = b > h ? b : h;
+        ll = (uint32_t)nl;
+        lh = (uint32_t)(nl >> 32);
+        hl = (uint32_t)nh;
+        hh = (uint32_t)(nh >> 32);
+        cnt += dpp_mov<C, RM>(0u, cnt);
+    });
+    if ((threadIdx.x & 63) == 63) {
+        s_lo[threadIdx.x >> 6] = ((uint64_t)lh << 32) | ll;
+        s_hi[threadIdx.x >> 6] = ((uint64_t)hh << 32) | hl;
         s_cnt[threadIdx.x >> 6] = cnt;
     }
     __syncthreads();
+    lo = ~0ull;
+    hi = 0;
     cnt = 0;
     for (uint32_t w = 0; w < kThreads / 64; ++w) {
         lo = s_lo[w] < lo ? s_lo[w] : lo;
@@ -341,44 +348,28 @@ __device__ __forceinline__ void sweep(uint32_t P, uint32_t valid, Get get,
     flush();
 }
 
-// Per-LLM sums of one thread's calls (LLM m[j], duration e[j] - s[j], covered part act[j]) for
-// LLM 0..M-1, reduced over each wave by lane butterflies and added to s_sum by lane 0.
-template <int E>
-__device__ __forceinline__ void add_llm_sums(uint32_t M, const uint32_t (&m)[E],
-                                             const uint64_t (&s)[E], const uint64_t (&e)[E],
-                                             const uint64_t (&act)[E], const bool (&ok)[E],
-                                             unsigned long long *s_sum)
+// 64-bit DPP move (both halves; lanes the move does not write get `old`).
+template <int C, int RM = 0xF>
+__device__ __forceinline__ uint64_t dpp_mov64(uint64_t old, uint64_t v)
 {
-#pragma unroll
-    for (uint32_t q = 0; q < ALP_MAX_LLMS; ++q) {
-        if (q >= M)
-            break;
-        uint32_t calls = 0;
-        uint64_t busy = 0, active = 0;
-#pragma unroll
-        for (int j = 0; j < E; ++j) {
-            const bool mine = ok[j] && m[j] == q;
-            calls += mine ? 1u : 0u;
-            busy += mine ? e[j] - s[j] : 0u;
-            active += mine ? act[j] : 0u;
-        }
-        auto step = [&](auto q_const) {
-            constexpr int Q = decltype(q_const)::value;
-            calls += lane_xor<Q>(calls);
-            busy += lane_xor64<Q>(busy);
-            active += lane_xor64<Q>(active);
-        };
-        step(std::integral_constant<int, 32>{});
-        step(std::integral_constant<int, 16>{});
-        step(std::integral_constant<int, 8>{});
-        step(std::integral_constant<int, 4>{});
-        step(std::integral_constant<int, 2>{});
-        step(std::integral_constant<int, 1>{});
-        if ((threadIdx.x & 63) == 0 && calls) {
-            atomicAdd(&s_sum[3 * q + 0], (unsigned long long)calls);
-            atomicAdd(&s_sum[3 * q + 1], (unsigned long long)busy);
-            atomicAdd(&s_sum[3 * q + 2], (unsigned long long)active);
-        }
+    return ((uint64_t)dpp_mov<C, RM>((uint32_t)(old >> 32), (uint32_t)(v >> 32)) << 32) |
+           dpp_mov<C, RM>((uint32_t)old, (uint32_t)v);
+}
+
+// One LLM's sums over the wave (DPP row moves; lane 63 ends with them), added to s_sum[3q..].
+__device__ __forceinline__ void wave_add_sums(uint32_t q, uint32_t calls, uint64_t busy,
+                                              uint64_t active, unsigned long long *s_sum)
+{
+    wave_reduce_steps([&](auto c, auto rm) {
+        constexpr int C = decltype(c)::value, RM = decltype(rm)::value;
+        calls += dpp_mov<C, RM>(0u, calls);
+        busy += dpp_mov64<C, RM>(0ull, busy);
+        active += dpp_mov64<C, RM>(0ull, active);
+    });
+    if ((threadIdx.x & 63) == 63 && calls) {
+        atomicAdd(&s_sum[3 * q + 0], (unsigned long long)calls);
+        atomicAdd(&s_sum[3 * q + 1], (unsigned long long)busy);
+        atomicAdd(&s_sum[3 * q + 2], (unsigned long long)active);
     }
 }
 
@@ -386,9 +377,11 @@ __device__ __forceinline__ void add_llm_sums(uint32_t M, const uint32_t (&m)[E],
 // completion), without a sort.  Walking the calls backwards, the calls of LLM m that come after
 // call j (so end no earlier) cover, within (-inf, e_j], exactly [lo, e_j] where lo is their
 // smallest start (or nothing if lo > e_j); so call j of LLM m adds max(0, min(e_j, lo) - s_j).
-// Thread t holds calls t E .. t E + E - 1; lo per LLM past its last call comes from an exclusive
-// suffix minimum over the later threads (lane moves within a wave, LDS across the waves).
-template <int E>
+// Thread t holds chunk 255 - t of the trace (calls (255 - t) E .. + E - 1), so the later calls
+// sit in the lower threads and lo past a thread's chunk is an exclusive prefix minimum per LLM:
+// DPP row shifts and row broadcasts within the wave, LDS across the four waves.  M <= MM: the
+// per-LLM state is sized at compile time.
+template <int E, int MM>
 __device__ __forceinline__ void sweep_by_end(uint32_t M, const uint32_t (&m)[E],
                                              const uint64_t (&s)[E], const uint64_t (&e)[E],
                                              const bool (&ok)[E], unsigned long long *s_sum)
@@ -396,85 +389,158 @@ __device__ __forceinline__ void sweep_by_end(uint32_t M, const uint32_t (&m)[E],
     __shared__ uint64_t s_wave_lo[kThreads / 64][ALP_MAX_LLMS];
     const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     // The thread's smallest start per LLM.
-    uint64_t lo[ALP_MAX_LLMS];
+    uint64_t lo[MM];
 #pragma unroll
-    for (uint32_t q = 0; q < ALP_MAX_LLMS; ++q) {
+    for (uint32_t q = 0; q < (uint32_t)MM; ++q) {
         lo[q] = ~0ull;
 #pragma unroll
         for (int j = 0; j < E; ++j)
             if (ok[j] && m[j] == q && s[j] < lo[q])
                 lo[q] = s[j];
     }
-    // Inclusive suffix minimum over the wave's lanes (lane and later), then over later waves.
+    // Inclusive prefix minimum over the wave's lanes (lane and lower): row shifts by 1, 2, 4
+    // and 8, then lane 15 into rows 1 and 3 and lane 31 into rows 2 and 3.  Lanes a move does
+    // not reach keep ~0, the identity.
 #pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-#pragma unroll
-        for (uint32_t q = 0; q < ALP_MAX_LLMS; ++q) {
-            if (q < M) {
-                const uint64_t o = __shfl_down((unsigned long long)lo[q], off, 64);
-                if (lane + off < 64 && o < lo[q])
-                    lo[q] = o;
-            }
-        }
-    }
-    if (lane == 0)
-#pragma unroll
-        for (uint32_t q = 0; q < ALP_MAX_LLMS; ++q)
-            s_wave_lo[wave][q] = lo[q];
-    __syncthreads();
-    // Exclusive: the next lane's inclusive value, and the later waves.
-#pragma unroll
-    for (uint32_t q = 0; q < ALP_MAX_LLMS; ++q) {
-        uint64_t v = q < M ? (uint64_t)__shfl_down((unsigned long long)lo[q], 1, 64) : ~0ull;
+    for (uint32_t q = 0; q < (uint32_t)MM; ++q) {
+        if (q >= M)
+            break;
+        uint64_t v = lo[q];
+        auto step = [&](auto c, auto rm) {
+            constexpr int C = decltype(c)::value, RM = decltype(rm)::value;
+            const uint64_t o = dpp_mov64<C, RM>(~0ull, v);
+            v = o < v ? o : v;
+        };
+        step(std::integral_constant<int, 0x111>{}, std::integral_constant<int, 0xF>{});
+        step(std::integral_constant<int, 0x112>{}, std::integral_constant<int, 0xF>{});
+        step(std::integral_constant<int, 0x114>{}, std::integral_constant<int, 0xF>{});
+        step(std::integral_constant<int, 0x118>{}, std::integral_constant<int, 0xF>{});
+        step(std::integral_constant<int, 0x142>{}, std::integral_constant<int, 0xA>{});
+        step(std::integral_constant<int, 0x143>{}, std::integral_constant<int, 0xC>{});
         if (lane == 63)
-            v = ~0ull;
-        for (uint32_t w = wave + 1; w < kThreads / 64; ++w)
-            v = s_wave_lo[w][q] < v ? s_wave_lo[w][q] : v;
-        lo[q] = v;
+            s_wave_lo[wave][q] = v;
+        // Exclusive: the previous lane's value (a whole-wave shift by one; lane 0 gets ~0).
+        lo[q] = dpp_mov64<0x138>(~0ull, v);
     }
-    // Walk the thread's calls backwards.
-    uint64_t act[E];
+    __syncthreads();
 #pragma unroll
-    for (int j = E - 1; j >= 0; --j) {
+    for (uint32_t q = 0; q < (uint32_t)MM; ++q) {
+        if (q >= M)
+            break;
+        for (uint32_t w = 0; w < wave; ++w)
+            lo[q] = s_wave_lo[w][q] < lo[q] ? s_wave_lo[w][q] : lo[q];
+    }
+    // Walk the thread's calls backwards.  Up to 4 LLMs, the per-LLM sums are kept as it goes;
+    // beyond, each call's covered part is kept and summed per LLM afterwards (fewer registers).
+    auto covered = [&](int j) {
         uint64_t cur = ~0ull;
 #pragma unroll
-        for (uint32_t q = 0; q < ALP_MAX_LLMS; ++q)
+        for (uint32_t q = 0; q < (uint32_t)MM; ++q)
             cur = m[j] == q ? lo[q] : cur;
         const uint64_t right = e[j] < cur ? e[j] : cur;
-        act[j] = ok[j] && right > s[j] ? right - s[j] : 0u;
-        if (ok[j]) {
+        return right > s[j] ? right - s[j] : 0ull;
+    };
+    if constexpr (MM <= 4) {
+        uint32_t calls[MM];
+        uint64_t busy[MM], active[MM];
 #pragma unroll
-            for (uint32_t q = 0; q < ALP_MAX_LLMS; ++q)
-                if (m[j] == q && s[j] < lo[q])
-                    lo[q] = s[j];
+        for (uint32_t q = 0; q < (uint32_t)MM; ++q) {
+            calls[q] = 0;
+            busy[q] = 0;
+            active[q] = 0;
+        }
+#pragma unroll
+        for (int j = E - 1; j >= 0; --j) {
+            if (!ok[j])
+                continue;
+            const uint64_t act = covered(j);
+#pragma unroll
+            for (uint32_t q = 0; q < (uint32_t)MM; ++q) {
+                if (m[j] == q) {
+                    calls[q] += 1;
+                    busy[q] += e[j] - s[j];
+                    active[q] += act;
+                    lo[q] = s[j] < lo[q] ? s[j] : lo[q];
+                }
+            }
+        }
+#pragma unroll
+        for (uint32_t q = 0; q < (uint32_t)MM; ++q)
+            if (q < M)
+                wave_add_sums(q, calls[q], busy[q], active[q], s_sum);
+    } else {
+        uint64_t act[E];
+#pragma unroll
+        for (int j = E - 1; j >= 0; --j) {
+            act[j] = ok[j] ? covered(j) : 0ull;
+            if (ok[j]) {
+#pragma unroll
+                for (uint32_t q = 0; q < (uint32_t)MM; ++q)
+                    if (m[j] == q && s[j] < lo[q])
+                        lo[q] = s[j];
+            }
+        }
+#pragma unroll
+        for (uint32_t q = 0; q < (uint32_t)MM; ++q) {
+            if (q >= M)
+                break;
+            uint32_t calls = 0;
+            uint64_t busy = 0, active = 0;
+#pragma unroll
+            for (int j = 0; j < E; ++j) {
+                const bool mine = ok[j] && m[j] == q;
+                calls += mine ? 1u : 0u;
+                busy += mine ? e[j] - s[j] : 0u;
+                active += mine ? act[j] : 0u;
+            }
+            wave_add_sums(q, calls, busy, active, s_sum);
         }
     }
-    add_llm_sums<E>(M, m, s, e, act, ok, s_sum);
 }
 
 // Largest trace the LDS path holds in registers while it loads (calls per thread).
 constexpr uint32_t kMaxPerThread = 8;
 
-template <bool Global>
-__global__ void __launch_bounds__(kThreads)
-trace_stats_kernel(uint32_t M, const uint64_t *__restrict__ offsets,
-                   const uint32_t *__restrict__ llm, const uint64_t *__restrict__ start,
-                   const uint64_t *__restrict__ end, uint32_t lds_cap,
-                   const uint32_t *__restrict__ long_traces, const uint64_t *__restrict__ long_base,
-                   uint64_t *__restrict__ scratch, unsigned long long *__restrict__ totals,
-                   uint32_t *__restrict__ flags)
+// The three passes over the traces.  kSweep: every trace of at most lds_cap calls, one block
+// each; traces in end order are swept without a sort, the others are appended to a work list.
+// kSort: the work list, sorted in registers or LDS.  kLong: traces beyond lds_cap, sorted in a
+// global scratch region.
+enum StatsPass { kSweep = 0, kSort = 1, kLong = 2 };
+
+struct StatsArgs {
+    uint32_t M, lds_cap;
+    const uint64_t *offsets;
+    const uint32_t *llm;
+    const uint64_t *start, *end;
+    const uint32_t *long_traces;      // kLong: trace of each block
+    const uint64_t *long_base;        // kLong: scratch offset of each block's trace (/ 2 words)
+    uint64_t *scratch;
+    unsigned long long *totals;       // kStatsCopies copies of the per-LLM sums
+    uint32_t *flags;
+    uint32_t *work;                   // kSweep appends, kSort reads: traces needing the sort
+    uint32_t *work_count;
+};
+
+// Statistics of trace r (slot = the block's trace slot in long_base for kLong) by one block.
+template <int Pass, int MM = ALP_MAX_LLMS>
+__device__ __forceinline__ void one_trace(const StatsArgs &a, uint32_t r, uint32_t slot,
+                                          unsigned char *s_dyn)
 {
-    extern __shared__ __align__(8) unsigned char s_dyn[];
+    constexpr bool Global = Pass == kLong;
+    const uint32_t M = a.M;
+    const uint32_t *__restrict__ llm = a.llm;
+    const uint64_t *__restrict__ start = a.start;
+    const uint64_t *__restrict__ end = a.end;
+    uint32_t *flags = a.flags;
     __shared__ unsigned long long s_sum[3 * ALP_MAX_LLMS];   // per LLM: calls, busy, active
     __shared__ uint32_t s_valid;
-    const uint32_t r = Global ? long_traces[blockIdx.x] : blockIdx.x;
-    const uint64_t lo = offsets[r], n = offsets[r + 1] - lo;
-    if (!Global && n > lds_cap)
+    const uint64_t lo = a.offsets[r], n = a.offsets[r + 1] - lo;
+    if (!Global && n > a.lds_cap)
         return;                                        // long trace: the global pass takes it
     uint32_t P = kThreads;                              // padded length: a power of two
     while (P < n)
         P <<= 1;
-    uint64_t *key = Global ? scratch + 2 * long_base[blockIdx.x]
+    uint64_t *key = Global ? a.scratch + 2 * a.long_base[slot]
                            : reinterpret_cast<uint64_t *>(s_dyn);
     uint64_t *val = key + P;
     for (uint32_t k = threadIdx.x; k < 3 * ALP_MAX_LLMS; k += kThreads)
@@ -504,8 +570,10 @@ trace_stats_kernel(uint32_t M, const uint64_t *__restrict__ offsets,
         // Held in registers: the trace's first and last start decide whether a call packs
         // into one 64-bit key, (llm << 61 | start - first << 32 | duration), which halves the
         // sort's LDS traffic; traces spanning 2^29 us or more keep (key, end) pairs.
-        // Thread t holds calls t E .. t E + E - 1 (E = P / 256, a contiguous chunk).
+        // Thread t holds chunk 255 - t: calls (255 - t) E .. + E - 1 (E = P / 256), so that
+        // later calls sit in lower threads (see sweep_by_end).
         const uint32_t E = P / kThreads;
+        const uint32_t chunk = kThreads - 1 - threadIdx.x;
         uint32_t rm[kMaxPerThread];
         uint64_t rs[kMaxPerThread], re[kMaxPerThread];
         bool ok[kMaxPerThread];
@@ -516,7 +584,7 @@ trace_stats_kernel(uint32_t M, const uint64_t *__restrict__ offsets,
         uint64_t first_end = ~0ull, last_end = 0;
 #pragma unroll
         for (uint32_t k = 0; k < kMaxPerThread; ++k) {
-            ok[k] = k < E && load((uint64_t)threadIdx.x * E + k, rm[k], rs[k], re[k]);
+            ok[k] = k < E && load((uint64_t)chunk * E + k, rm[k], rs[k], re[k]);
             if (ok[k]) {
                 valid += 1;
                 smin = rs[k] < smin ? rs[k] : smin;
@@ -534,13 +602,18 @@ trace_stats_kernel(uint32_t M, const uint64_t *__restrict__ offsets,
         block_min_max_sum(smin, smax, nvalid);          // its barrier also publishes s_first
         if (nvalid == 0)
             return;
-        // The next chunk that holds a call must not end earlier (chunks with no call are
-        // padding and come last); malformed calls (bad) send the trace to the sort.
-        if (threadIdx.x + 1 < kThreads && s_first[threadIdx.x + 1] != ~0ull)
-            in_order = in_order && s_first[threadIdx.x + 1] >= last_end;
+        // The next chunk (thread t - 1) that holds a call must not end earlier (chunks with
+        // no call are padding and come last); malformed calls (bad) send the trace to the sort.
+        if (threadIdx.x > 0 && s_first[threadIdx.x - 1] != ~0ull)
+            in_order = in_order && s_first[threadIdx.x - 1] >= last_end;
         if (bad)
             in_order = false;
-        if (__syncthreads_and(in_order ? 1 : 0)) {
+        if constexpr (Pass == kSweep) {
+            if (!__syncthreads_and(in_order ? 1 : 0)) {
+                if (threadIdx.x == 0)
+                    a.work[atomicAdd(a.work_count, 1u)] = r;
+                return;
+            }
             auto run = [&](auto e_const) {
                 constexpr int EC = decltype(e_const)::value;
                 uint32_t m[EC];
@@ -553,7 +626,7 @@ trace_stats_kernel(uint32_t M, const uint64_t *__restrict__ offsets,
                     en[j] = re[j];
                     okc[j] = ok[j];
                 }
-                sweep_by_end<EC>(M, m, st, en, okc, s_sum);
+                sweep_by_end<EC, MM>(M, m, st, en, okc, s_sum);
             };
             switch (P) {
             case kThreads: run(std::integral_constant<int, 1>{}); break;
@@ -588,7 +661,7 @@ trace_stats_kernel(uint32_t M, const uint64_t *__restrict__ offsets,
 #pragma unroll
             for (uint32_t k = 0; k < kMaxPerThread; ++k) {
                 if (k < E) {
-                    const uint32_t i = threadIdx.x * E + k;
+                    const uint32_t i = chunk * E + k;
                     key[i] = ok[k] ? ((uint64_t)rm[k] << 60) | rs[k] : kPad;
                     val[i] = ok[k] ? re[k] : 0;
                 }
@@ -625,12 +698,37 @@ trace_stats_kernel(uint32_t M, const uint64_t *__restrict__ offsets,
         }, s_sum);
     }
     __syncthreads();
+    unsigned long long *copy = a.totals + (uint64_t)(r % kStatsCopies) * kStatsCopyStride;
     for (uint32_t k = threadIdx.x; k < 3 * M; k += kThreads)
         if (s_sum[k])
-            atomicAdd(&totals[k], s_sum[k]);
+            atomicAdd(&copy[k], s_sum[k]);
 }
 
-// n and p per LLM from the totals (calls, busy, active per LLM), R traces.  Status bits in
+// MM: a bound on the number of LLMs (2, 4 or 8), so the per-LLM registers fit the workflow.
+template <int MM>
+__global__ void __launch_bounds__(kThreads) trace_sweep_kernel(StatsArgs a)
+{
+    one_trace<kSweep, MM>(a, blockIdx.x, 0, nullptr);
+}
+
+// Grid-stride over the work list the sweep pass wrote (every block reads the same count).
+__global__ void __launch_bounds__(kThreads) trace_sort_kernel(StatsArgs a)
+{
+    extern __shared__ __align__(8) unsigned char s_dyn[];
+    const uint32_t count = *a.work_count;
+    for (uint32_t i = blockIdx.x; i < count; i += gridDim.x) {
+        one_trace<kSort>(a, a.work[i], 0, s_dyn);
+        __syncthreads();                               // the next trace reuses shared memory
+    }
+}
+
+__global__ void __launch_bounds__(kThreads) trace_long_kernel(StatsArgs a)
+{
+    one_trace<kLong>(a, a.long_traces[blockIdx.x], blockIdx.x, nullptr);
+}
+
+// n and p per LLM from the totals (calls, busy, active per LLM, summed over the copies), R
+// traces.  Status bits in
 // flags: 1 llm out of range, 2 end before start, 4 start or duration out of range, 8 a result
 // beyond 2^31 - 1 (it could not be loaded as an ALP input).
 __global__ void stats_finish_kernel(uint32_t M, uint32_t R,
@@ -640,7 +738,13 @@ __global__ void stats_finish_kernel(uint32_t M, uint32_t R,
     const uint32_t m = threadIdx.x;
     if (m >= M)
         return;
-    const uint64_t calls = totals[3 * m], busy = totals[3 * m + 1], active = totals[3 * m + 2];
+    uint64_t calls = 0, busy = 0, active = 0;
+    for (uint32_t c = 0; c < kStatsCopies; ++c) {
+        const unsigned long long *t = totals + (uint64_t)c * kStatsCopyStride + 3 * m;
+        calls += t[0];
+        busy += t[1];
+        active += t[2];
+    }
     uint64_t n = calls * 1000u / R, p;
     if (calls == 0)
         p = 0;
@@ -670,26 +774,45 @@ hipError_t launch_trace_stats(uint32_t M, uint32_t R, const uint64_t *offsets, c
                               const uint64_t *start, const uint64_t *end, uint32_t lds_cap,
                               uint32_t num_long, const uint32_t *long_traces,
                               const uint64_t *long_base, uint64_t *scratch, uint64_t *totals,
-                              uint32_t *flags, alp_stats_t *out, hipStream_t st)
+                              uint32_t *work, alp_stats_t *out, hipStream_t st)
 {
-    hipLaunchKernelGGL(stats_init_kernel, dim3(1), dim3(64), 0, st, totals, 3 * ALP_MAX_LLMS + 1);
+    // totals: the copies of the sums, then the flags word, then the work-list count.
+    hipLaunchKernelGGL(stats_init_kernel, dim3(1), dim3(256), 0, st, totals, kStatsTotalsWords + 2);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;
-    unsigned long long *tot = reinterpret_cast<unsigned long long *>(totals);
+    StatsArgs a;
+    a.M = M;
+    a.lds_cap = lds_cap;
+    a.offsets = offsets;
+    a.llm = llm;
+    a.start = start;
+    a.end = end;
+    a.long_traces = long_traces;
+    a.long_base = long_base;
+    a.scratch = scratch;
+    a.totals = reinterpret_cast<unsigned long long *>(totals);
+    a.flags = reinterpret_cast<uint32_t *>(totals + kStatsTotalsWords);
+    a.work = work;
+    a.work_count = reinterpret_cast<uint32_t *>(totals + kStatsTotalsWords + 1);
+    if (M <= 2)
+        hipLaunchKernelGGL(trace_sweep_kernel<2>, dim3(R), dim3(kThreads), 0, st, a);
+    else if (M <= 4)
+        hipLaunchKernelGGL(trace_sweep_kernel<4>, dim3(R), dim3(kThreads), 0, st, a);
+    else
+        hipLaunchKernelGGL(trace_sweep_kernel<ALP_MAX_LLMS>, dim3(R), dim3(kThreads), 0, st, a);
+    if ((e = hipGetLastError()) != hipSuccess)
+        return e;
     const size_t lds = (size_t)2 * lds_cap * sizeof(uint64_t);
-    hipLaunchKernelGGL(trace_stats_kernel<false>, dim3(R), dim3(kThreads), lds, st, M, offsets,
-                       llm, start, end, lds_cap, long_traces, long_base, scratch, tot, flags);
+    hipLaunchKernelGGL(trace_sort_kernel, dim3(R < 1024 ? R : 1024), dim3(kThreads), lds, st, a);
     if ((e = hipGetLastError()) != hipSuccess)
         return e;
     if (num_long) {
-        hipLaunchKernelGGL(trace_stats_kernel<true>, dim3(num_long), dim3(kThreads), 0, st, M,
-                           offsets, llm, start, end, lds_cap, long_traces, long_base, scratch,
-                           tot, flags);
+        hipLaunchKernelGGL(trace_long_kernel, dim3(num_long), dim3(kThreads), 0, st, a);
         if ((e = hipGetLastError()) != hipSuccess)
             return e;
     }
-    hipLaunchKernelGGL(stats_finish_kernel, dim3(1), dim3(64), 0, st, M, R, tot, flags, out);
+    hipLaunchKernelGGL(stats_finish_kernel, dim3(1), dim3(64), 0, st, M, R, a.totals, a.flags, out);
     return hipGetLastError();
 }
 
