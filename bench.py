@@ -99,6 +99,20 @@ def _kernel_digest() -> str:
     return h.hexdigest()
 
 
+def host_cpu() -> str:
+    """The host's CPU model and logical CPU count (the oracle uses one of them)."""
+    model = "unknown CPU"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return f"{model}, {os.cpu_count()} logical CPUs"
+
+
 def cpu_baseline(batch, G, lam, seconds: float):
     """Single-threaded oracle argmin over the first indices of instance 0, sized to ~seconds."""
     import oracle
@@ -111,7 +125,7 @@ def cpu_baseline(batch, G, lam, seconds: float):
     t0 = time.perf_counter()
     oracle.argmin(inst, G, lam, 0, total)
     dt = time.perf_counter() - t0
-    return {"value": total / dt, "unit": "candidates/s", "cores": 1, "kind": "oracle",
+    return {"value": total / dt, "unit": "candidates/s", "cores": 1, "kind": "oracle", "host": host_cpu(),
             "sample": f"first {total:,} candidate indices of the same instance, exhaustive "
                       f"single-threaded C oracle ({dt:.1f} s)"}
 
@@ -124,7 +138,7 @@ def cpu_baseline_pruned(batch, G, lam, seconds: float):
         vectors += oracle.pruned(oracle.Instance(batch, done), int(G[done]), int(lam[done]))["vectors"]
         done += 1
     dt = time.perf_counter() - t0
-    return {"value": vectors / dt, "unit": "fraction vectors/s", "cores": 1, "kind": "oracle",
+    return {"value": vectors / dt, "unit": "fraction vectors/s", "cores": 1, "kind": "oracle", "host": host_cpu(),
             "sample": f"pruned search of the first {done} instances ({vectors:,} fraction "
                       f"vectors), single-threaded C oracle ({dt:.1f} s)"}
 
@@ -384,7 +398,7 @@ def cpu_baseline_place(batch, res, G, seconds: float):
             oracle.place(Q, int(G[done]), *_place_args(res[done], M))
         done += 1
     dt = time.perf_counter() - t0
-    return {"value": done / dt, "unit": "allocations/s", "cores": 1, "kind": "oracle",
+    return {"value": done / dt, "unit": "allocations/s", "cores": 1, "kind": "oracle", "host": host_cpu(),
             "sample": f"placement of the first {done} results, single-threaded C oracle "
                       f"({dt:.2f} s, including the Python call per allocation)"}
 
@@ -442,7 +456,7 @@ def cpu_baseline_stats(tr, seconds: float):
         done = hi
     dt = time.perf_counter() - t0
     calls = int(off[done])
-    return {"value": calls / dt, "unit": "trace calls/s", "cores": 1, "kind": "oracle",
+    return {"value": calls / dt, "unit": "trace calls/s", "cores": 1, "kind": "oracle", "host": host_cpu(),
             "sample": f"the first {done} traces ({calls:,} calls), single-threaded C oracle "
                       f"({dt:.1f} s)"}
 
