@@ -595,7 +595,8 @@ __device__ __forceinline__ void one_trace(const StatsArgs &a, uint32_t r, uint32
             }
         }
         __shared__ uint64_t s_first[kThreads];
-        s_first[threadIdx.x] = first_end;
+        if constexpr (Pass == kSweep)
+            s_first[threadIdx.x] = first_end;
         if (bad)
             atomicOr(flags, bad);
         uint32_t nvalid = valid;
@@ -604,11 +605,11 @@ __device__ __forceinline__ void one_trace(const StatsArgs &a, uint32_t r, uint32
             return;
         // The next chunk (thread t - 1) that holds a call must not end earlier (chunks with
         // no call are padding and come last); malformed calls (bad) send the trace to the sort.
-        if (threadIdx.x > 0 && s_first[threadIdx.x - 1] != ~0ull)
-            in_order = in_order && s_first[threadIdx.x - 1] >= last_end;
-        if (bad)
-            in_order = false;
         if constexpr (Pass == kSweep) {
+            if (threadIdx.x > 0 && s_first[threadIdx.x - 1] != ~0ull)
+                in_order = in_order && s_first[threadIdx.x - 1] >= last_end;
+            if (bad)
+                in_order = false;
             if (!__syncthreads_and(in_order ? 1 : 0)) {
                 if (threadIdx.x == 0)
                     a.work[atomicAdd(a.work_count, 1u)] = r;
@@ -711,15 +712,13 @@ __global__ void __launch_bounds__(kThreads) trace_sweep_kernel(StatsArgs a)
     one_trace<kSweep, MM>(a, blockIdx.x, 0, nullptr);
 }
 
-// Grid-stride over the work list the sweep pass wrote (every block reads the same count).
+// One block per entry of the work list the sweep pass wrote; the grid covers every trace, and
+// blocks beyond the list's length end at once.
 __global__ void __launch_bounds__(kThreads) trace_sort_kernel(StatsArgs a)
 {
     extern __shared__ __align__(8) unsigned char s_dyn[];
-    const uint32_t count = *a.work_count;
-    for (uint32_t i = blockIdx.x; i < count; i += gridDim.x) {
-        one_trace<kSort>(a, a.work[i], 0, s_dyn);
-        __syncthreads();                               // the next trace reuses shared memory
-    }
+    if (blockIdx.x < *a.work_count)
+        one_trace<kSort>(a, a.work[blockIdx.x], 0, s_dyn);
 }
 
 __global__ void __launch_bounds__(kThreads) trace_long_kernel(StatsArgs a)
@@ -804,7 +803,7 @@ hipError_t launch_trace_stats(uint32_t M, uint32_t R, const uint64_t *offsets, c
     if ((e = hipGetLastError()) != hipSuccess)
         return e;
     const size_t lds = (size_t)2 * lds_cap * sizeof(uint64_t);
-    hipLaunchKernelGGL(trace_sort_kernel, dim3(R < 1024 ? R : 1024), dim3(kThreads), lds, st, a);
+    hipLaunchKernelGGL(trace_sort_kernel, dim3(R), dim3(kThreads), lds, st, a);
     if ((e = hipGetLastError()) != hipSuccess)
         return e;
     if (num_long) {
