@@ -241,16 +241,6 @@ __device__ __forceinline__ void write_item_result(const FinishArgs &fa, uint32_t
                  rejected ? (uint32_t)ALP_EINVAL : (uint32_t)ALP_INFEASIBLE);
 }
 
-// Result of one item from its block winners, by one wave.
-__device__ __forceinline__ void finish_item(const FinishArgs &fa, uint32_t item,
-                                            uint32_t blocks_per_item, const Winner *winners)
-{
-    uint32_t L;
-    uint64_t x;
-    item_winner(item, blocks_per_item, winners, L, x);
-    write_item_result(fa, item, L, x);
-}
-
 // Writes the block's winner and counts the block as finished (agent-scope fence and per-item
 // counter, zeroed by option_terms_kernel); true in every thread of the item's last block, which
 // then sees every other block's writes.
@@ -302,13 +292,11 @@ __device__ __forceinline__ void block_finish(uint32_t L, uint64_t x, uint32_t it
     __shared__ uint32_t last_block;
     Winner *slot = &winners[(uint64_t)item * blocks_per_item + sub];
     if (blocks_per_item == 1) {
-        // The block is the whole item: no agent-scope fence or counter; its winner only needs
-        // to reach its own first wave.
-        block_min_store(L, x, slot);
-        __threadfence_block();
-        __syncthreads();
+        // The block is the whole item: its minimum, held by wave 0, is the item's winner (no
+        // fence, counter or winner slot).
+        block_min(L, x);
         if (threadIdx.x < 64)
-            finish_item(fa, item, 1, winners);
+            write_item_result(fa, item, L, x);
         return;
     }
     block_min(L, x);
