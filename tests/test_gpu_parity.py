@@ -403,6 +403,20 @@ def test_pruned_larger_spaces_match_oracle(alp, cfg, insts):
                 _check_pruned(b, i, out[i], int(G[i]), lam[i], flags)
 
 
+@pytest.mark.parametrize("M,G,Q", [(5, 16, 10), (5, 8, 10), (6, 4, 8)])
+def test_pruned_paper_point_and_six_llms(alp, M, G, Q):
+    """Five and six LLMs at the paper's scheduler point (M = 5, 16 GPUs, 10 fractions per GPU)
+    and smaller budgets: the walk below the two fixed fractions runs three levels deep."""
+    fq = sorted({max(1, round(Q * k / 8)) for k in range(1, 9)})
+    b = make_custom(2604, M, (1, 2, 4, 8), fq, 4, 8, G, count=1, frac_den=Q,
+                    param_range=(1e9, 70e9), alpha=0.5)
+    lam = _targets(b, [G])
+    with alp.Context(b) as ctx:
+        for flags in ((3, 1) if G * Q > 100 else (3, 1, 0)):     # flags 0: every vector
+            out = ctx.search_pruned([G], lam, flags)
+            _check_pruned(b, 0, out[0], G, lam[0], flags)
+
+
 @pytest.mark.parametrize("seed,variant", EDGE_SPACES)
 def test_pruned_edge_spaces(alp, seed, variant):
     b, G = edge_batch(seed, variant)
