@@ -1279,7 +1279,13 @@ struct alp_stats_ctx {
     int timing = 0;
     hipEvent_t ev[2] = {nullptr, nullptr};
     float last_ms = 0.0f;
+    // Calls left that sort every trace without the end-order sweep: set when a sweep found most
+    // traces out of end order (each such trace is then loaded twice), counted down per call, so
+    // that every kStatsProbeEvery-th call measures the order again.
+    uint32_t direct_left = 0;
 };
+
+constexpr uint32_t kStatsProbeEvery = 8;
 
 int32_t alp_stats_create(alp_stats_ctx **out, int32_t device, void *hip_stream)
 {
@@ -1371,22 +1377,29 @@ int32_t alp_trace_stats(alp_stats_ctx *c, uint32_t num_llms, uint32_t num_traces
     if ((e = c->work.ensure((uint64_t)num_traces * sizeof(uint32_t))) != hipSuccess)
         return hip_fail(e, "hipMalloc(statistics work list)");
     uint64_t *totals = (uint64_t *)c->totals.ptr;
-    uint32_t *flags = (uint32_t *)(totals + alp::kStatsTotalsWords);
+    const bool sweep = c->direct_left == 0;
+    if (!sweep)
+        --c->direct_left;
     if (c->timing && (e = hipEventRecord(c->ev[0], c->stream)) != hipSuccess)
         return hip_fail(e, "hipEventRecord");
     if ((e = alp::launch_trace_stats(num_llms, num_traces, offsets, llm, start_us, end_us, lds_cap,
                                      (uint32_t)longs.size(), (const uint32_t *)c->long_list.ptr,
                                      (const uint64_t *)c->long_base.ptr, (uint64_t *)c->scratch.ptr,
-                                     totals, (uint32_t *)c->work.ptr, c->host_out_dev,
+                                     totals, (uint32_t *)c->work.ptr, sweep, c->host_out_dev,
                                      c->stream)) != hipSuccess)
         return hip_fail(e, "statistics launch");
     if (c->timing && (e = hipEventRecord(c->ev[1], c->stream)) != hipSuccess)
         return hip_fail(e, "hipEventRecord");
-    uint32_t host_flags = 0;
-    if ((e = hipMemcpyAsync(&host_flags, flags, sizeof(uint32_t), hipMemcpyDeviceToHost,
-                            c->stream)) != hipSuccess ||
+    // The flags word, then the work list's length.
+    uint64_t tail[2] = {0, 0};
+    if ((e = hipMemcpyAsync(tail, totals + alp::kStatsTotalsWords, sizeof(tail),
+                            hipMemcpyDeviceToHost, c->stream)) != hipSuccess ||
         (e = hipStreamSynchronize(c->stream)) != hipSuccess)
         return hip_fail(e, "statistics");
+    const uint32_t host_flags = (uint32_t)tail[0];
+    const uint64_t short_traces = num_traces - longs.size();
+    if (sweep && 2 * (tail[1] & 0xFFFFFFFFu) > short_traces)
+        c->direct_left = kStatsProbeEvery - 1;
     if (c->timing && (e = hipEventElapsedTime(&c->last_ms, c->ev[0], c->ev[1])) != hipSuccess)
         return hip_fail(e, "hipEventElapsedTime");
     if (host_flags & 1u)

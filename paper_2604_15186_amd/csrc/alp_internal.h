@@ -157,8 +157,9 @@ static_assert(sizeof(alp_pruned_t) == 64 && offsetof(alp_pruned_t, fraction_vect
 // 2 * long_base[k] words (2 * pow2(length) words each).  totals: kStatsTotalsWords + 2 words:
 // kStatsCopies copies of the per-LLM sums, kStatsCopyStride words apart (trace r adds to copy
 // r mod kStatsCopies, so that thousands of traces do not queue on the same atomic words), then
-// the status flags, then the length of the work list.  work: R entries, the traces that need a
-// sort (not in end order, or malformed).  Writes out[0..M).
+// the status flags, then the length of the work list.  sweep: traces in end order are swept
+// without a sort and the others listed in work (R entries) for the sort pass; otherwise every
+// trace is sorted.  Writes out[0..M).
 constexpr uint32_t kStatsCopies = 64;
 constexpr uint32_t kStatsCopyStride = 32;                 // >= 3 * ALP_MAX_LLMS, 256 B apart
 constexpr uint32_t kStatsTotalsWords = kStatsCopies * kStatsCopyStride;
@@ -166,7 +167,7 @@ hipError_t launch_trace_stats(uint32_t M, uint32_t R, const uint64_t *offsets, c
                               const uint64_t *start, const uint64_t *end, uint32_t lds_cap,
                               uint32_t num_long, const uint32_t *long_traces,
                               const uint64_t *long_base, uint64_t *scratch, uint64_t *totals,
-                              uint32_t *work, alp_stats_t *out, hipStream_t st);
+                              uint32_t *work, bool sweep, alp_stats_t *out, hipStream_t st);
 
 // One allocation to place: budget, LLM count, whether the search found it, per-LLM choices.
 struct PlaceIn {

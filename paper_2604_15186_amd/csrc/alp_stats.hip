@@ -712,12 +712,14 @@ __global__ void __launch_bounds__(kThreads) trace_sweep_kernel(StatsArgs a)
     one_trace<kSweep, MM>(a, blockIdx.x, 0, nullptr);
 }
 
-// One block per entry of the work list the sweep pass wrote; the grid covers every trace, and
-// blocks beyond the list's length end at once.
+// One block per entry of the work list the sweep pass wrote (the grid covers every trace, and
+// blocks beyond the list's length end at once), or, without a work list, one per trace.
 __global__ void __launch_bounds__(kThreads) trace_sort_kernel(StatsArgs a)
 {
     extern __shared__ __align__(8) unsigned char s_dyn[];
-    if (blockIdx.x < *a.work_count)
+    if (!a.work)
+        one_trace<kSort>(a, blockIdx.x, 0, s_dyn);
+    else if (blockIdx.x < *a.work_count)
         one_trace<kSort>(a, a.work[blockIdx.x], 0, s_dyn);
 }
 
@@ -773,7 +775,7 @@ hipError_t launch_trace_stats(uint32_t M, uint32_t R, const uint64_t *offsets, c
                               const uint64_t *start, const uint64_t *end, uint32_t lds_cap,
                               uint32_t num_long, const uint32_t *long_traces,
                               const uint64_t *long_base, uint64_t *scratch, uint64_t *totals,
-                              uint32_t *work, alp_stats_t *out, hipStream_t st)
+                              uint32_t *work, bool sweep, alp_stats_t *out, hipStream_t st)
 {
     // totals: the copies of the sums, then the flags word, then the work-list count.
     hipLaunchKernelGGL(stats_init_kernel, dim3(1), dim3(256), 0, st, totals, kStatsTotalsWords + 2);
@@ -792,16 +794,19 @@ hipError_t launch_trace_stats(uint32_t M, uint32_t R, const uint64_t *offsets, c
     a.scratch = scratch;
     a.totals = reinterpret_cast<unsigned long long *>(totals);
     a.flags = reinterpret_cast<uint32_t *>(totals + kStatsTotalsWords);
-    a.work = work;
+    a.work = sweep ? work : nullptr;
     a.work_count = reinterpret_cast<uint32_t *>(totals + kStatsTotalsWords + 1);
-    if (M <= 2)
-        hipLaunchKernelGGL(trace_sweep_kernel<2>, dim3(R), dim3(kThreads), 0, st, a);
-    else if (M <= 4)
-        hipLaunchKernelGGL(trace_sweep_kernel<4>, dim3(R), dim3(kThreads), 0, st, a);
-    else
-        hipLaunchKernelGGL(trace_sweep_kernel<ALP_MAX_LLMS>, dim3(R), dim3(kThreads), 0, st, a);
-    if ((e = hipGetLastError()) != hipSuccess)
-        return e;
+    if (sweep) {
+        if (M <= 2)
+            hipLaunchKernelGGL(trace_sweep_kernel<2>, dim3(R), dim3(kThreads), 0, st, a);
+        else if (M <= 4)
+            hipLaunchKernelGGL(trace_sweep_kernel<4>, dim3(R), dim3(kThreads), 0, st, a);
+        else
+            hipLaunchKernelGGL(trace_sweep_kernel<ALP_MAX_LLMS>, dim3(R), dim3(kThreads), 0, st,
+                               a);
+        if ((e = hipGetLastError()) != hipSuccess)
+            return e;
+    }
     const size_t lds = (size_t)2 * lds_cap * sizeof(uint64_t);
     hipLaunchKernelGGL(trace_sort_kernel, dim3(R), dim3(kThreads), lds, st, a);
     if ((e = hipGetLastError()) != hipSuccess)

@@ -173,3 +173,23 @@ def test_traces_in_end_order(ctx):
     # one LLM only, nested calls all ending together
     traces.append([(0, 1000 - i, 1000) for i in range(700)])
     _same(ctx, 8, *_pack(traces))
+
+
+def test_order_adaptive_passes_agree():
+    """A context whose sweep finds most traces out of end order sorts every trace on its next
+    calls (then checks the order again): both kinds of call, on traces in either order, must
+    match the oracle."""
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2604_15186_amd import alp
+    tr = make_traces("beam", 300, 7)
+    off = tr["offsets"].astype(np.int64)
+    rng = np.random.default_rng(8)
+    perm = np.concatenate([lo + rng.permutation(hi - lo) for lo, hi in zip(off[:-1], off[1:])])
+    orders = [(tr["llm"][perm], tr["start"][perm], tr["end"][perm]),
+              (tr["llm"], tr["start"], tr["end"])]
+    with alp.StatsContext(0) as c:
+        for k in range(12):                    # shuffled, in order, shuffled, ...
+            llm, s, e = orders[k % 2]
+            _same(c, tr["M"], tr["offsets"], llm, s, e)
