@@ -521,9 +521,8 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
     if (threadIdx.x == 0 && blocks_per_item > 1)
         hint = __hip_atomic_load(&fa.best[item], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     // The wave's lowest sub-row reaching L* (its lane-slots' first rows at L*), as a sub-row
-    // index of the item.
-    // Its row's outer sums are loaded now, while the block's other waves finish (claimed
-    // sub-rows number fewer than 2^32).
+    // index of the item, and that row's outer sums, loaded now while the block's other waves
+    // finish (claimed sub-rows number fewer than 2^32).
     uint64_t rwave = ~0ull;
     uint32_t oc_w = 0;
     int32_t ou_w = 0;
