@@ -12,8 +12,9 @@
  *   T_w = min_m d_m * T_m / n_m                         (Eq. 2, T_m the saturation throughput)
  * and the search returns the allocation of lowest L_w that sustains the target workflow rate
  * (T_w >= lambda), fits every LLM's weights into its GPU share (Section 5, step 1) and uses at
- * most the GPU budget (Section 3, step 3: "lowest latency within a target workflow-level
- * arrival rate").  Every candidate of the space is evaluated; ties go to the lowest index.
+ * most the GPU budget (Section 3, step 3: the objective is the lowest latency that still meets
+ * the workflow's target rate).  Every candidate of the space is evaluated; ties go to the lowest
+ * index.
  *
  * Fixed point: rates in milli-requests/s, latencies in microseconds, n_m and p_m in thousandths.
  * Per-replica rate r = ceil(lambda * n / (1000 d)); latency at r is lat[0] for r <= rate[0],
@@ -168,7 +169,7 @@ int32_t alp_search_batch_async(alp_ctx *ctx, uint32_t count, const uint32_t *ins
 int32_t alp_max_throughput(alp_ctx *ctx, uint32_t count, const uint32_t *instances,
                            const uint32_t *gpu_budget, uint32_t *out_tmax);
 
-/* Several workflows sharing a pool of GPUs (Section 5, "Scheduling multiple workflows": the
+/* Several workflows sharing a pool of GPUs (Section 5, scheduling of several workflows: the
  * scheduler decides how many GPUs each workflow gets, searches each workflow's allocation
  * independently, and combines the per-workflow utilities with egalitarian or social welfare).
  * Workflow w is loaded instance instances[w] with target rate target_milli[w].  It gets g_w whole

@@ -14,7 +14,7 @@
  *     T_w = minimum of the normalised throughputs (Eq. 2), and the feasibility conditions:
  *     every LLM's option deployable and its weights fit in its GPU share (Section 5, step 1,
  *     minimum fractions that hold the parameters), the target rate is sustained (T_w >= lambda,
- *     Section 3 "lowest latency within a target workflow-level arrival rate"), and the GPU
+ *     Section 3: the lowest latency that still meets the workflow's target rate), and the GPU
  *     budget is respected;
  *   - the search result: the feasible candidate of lowest L_w, ties broken by lowest index;
  *   - the paper's own pruned search over GPU fractions (Section 5, steps 1-3), and the split of
@@ -272,7 +272,7 @@ int orc_tmax_threshold(const orc_instance *s, uint32_t G, orc_term *scratch /* [
 }
 
 /* ---------------------------------------------------------------------------------------------
- * Several workflows sharing a GPU pool (Section 5, "Scheduling multiple workflows"): every
+ * Several workflows sharing a GPU pool (Section 5, scheduling of several workflows): every
  * workflow w receives a whole number of GPUs g_w, sum g_w <= G, and its own search at budget g_w
  * gives its latency L[w][g_w] (ORC_U64_NONE when infeasible).  The per-workflow utilities are
  * combined by egalitarian welfare (policy 0: minimise the largest latency; ties by the smaller

@@ -1,9 +1,9 @@
 """Seeded synthetic workloads for the Aggregate LLM Pipeline (ALP) allocation search.
 
 This module only draws inputs: per-LLM throughput--latency profile tables (one table per
-tensor-parallel degree and GPU share, as produced by the profiling step of Section 4,
-"LLM Profiling"), per-LLM workflow statistics n_m and p_m (Section 4, "Statistical Workflow
-Aggregation"), model weight sizes for the memory-fit bound (Section 5, step 1), a GPU budget and
+tensor-parallel degree and GPU share, as produced by the profiling step of Section 4),
+per-LLM workflow statistics n_m and p_m (Section 4, the workflow statistics step), model weight
+sizes for the memory-fit bound (Section 5, step 1), a GPU budget and
 a target-rate fraction.  It contains none of the predictor's arithmetic (no Eq. 1 / Eq. 2
 terms, no feasibility, no argmin): those live, independently, in the oracle and in the HIP
 library.  The target workflow rate is stated here only as a fraction ``u_ppm`` (parts per
