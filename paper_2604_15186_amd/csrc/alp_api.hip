@@ -1275,7 +1275,8 @@ struct alp_stats_ctx {
     DevBuf totals, long_list, long_base, scratch, work;
     alp_stats_t *host_out = nullptr;        // mapped pinned: results
     alp_stats_t *host_out_dev = nullptr;
-    std::vector<uint64_t> offsets;
+    uint64_t *offsets = nullptr;            // pinned: the trace offsets, read for planning
+    size_t offsets_cap = 0;                 // entries
     int timing = 0;
     hipEvent_t ev[2] = {nullptr, nullptr};
     float last_ms = 0.0f;
@@ -1331,8 +1332,20 @@ int32_t alp_trace_stats(alp_stats_ctx *c, uint32_t num_llms, uint32_t num_traces
     if (guard.status != hipSuccess)
         return hip_fail(guard.status, "hipSetDevice");
     hipError_t e;
-    c->offsets.resize((size_t)num_traces + 1);
-    if ((e = hipMemcpyAsync(c->offsets.data(), offsets, c->offsets.size() * sizeof(uint64_t),
+    const size_t n_off = (size_t)num_traces + 1;
+    if (c->offsets_cap < n_off) {
+        // Pinned, so the copy goes straight to it (no staging through a bounce buffer).
+        if (c->offsets)
+            (void)hipHostFree(c->offsets);
+        c->offsets = nullptr;
+        c->offsets_cap = 0;
+        if ((e = hipHostMalloc((void **)&c->offsets, n_off * sizeof(uint64_t))) != hipSuccess) {
+            c->offsets = nullptr;
+            return hip_fail(e, "hipHostMalloc(offsets)");
+        }
+        c->offsets_cap = n_off;
+    }
+    if ((e = hipMemcpyAsync(c->offsets, offsets, n_off * sizeof(uint64_t),
                             hipMemcpyDeviceToHost, c->stream)) != hipSuccess ||
         (e = hipStreamSynchronize(c->stream)) != hipSuccess)
         return hip_fail(e, "copy offsets");
@@ -1447,6 +1460,8 @@ void alp_stats_free(alp_stats_ctx *c)
         b->release();
     if (c->host_out)
         (void)hipHostFree(c->host_out);
+    if (c->offsets)
+        (void)hipHostFree(c->offsets);
     delete c;
 }
 
