@@ -294,6 +294,23 @@ def test_many_ties_keep_lowest_index(alp, seed):
                     check_result(b, i, ctx.search(i, G, lam), *want)
 
 
+@pytest.mark.parametrize("G,lam_frac", [(1, 0), (2, 0), (3, 2), (6, 3)])
+def test_sparse_feasibility_multi_block(alp, G, lam_frac):
+    """Budgets so tight that few candidates of a 4-LLM space (64 options each, 2^24 candidates,
+    hundreds of blocks) fit: most blocks hold no feasible candidate, a few publish winners, and
+    the item's last block must still return the lowest index at the minimum latency."""
+    b = make_custom(77, 4, (1, 2, 4, 8), (1, 2, 3, 4), 4, 8, G, count=1, param_range=(0.5e9, 8e9))
+    inst = oracle.Instance(b, 0)
+    t = oracle.tmax(inst, G)
+    lam = max(1, t * lam_frac // 4)
+    want = oracle_expect(b, 0, G, lam)
+    with alp.Context(b) as ctx:
+        for launch in [(0, 0, 0, 0), (4, 0, 0, 0), (5, 0, 0, 0), (5, 64, 512, 0), (1, 0, 0, 4)]:
+            ctx.set_launch(*launch)
+            check_result(b, 0, ctx.search(0, G, lam), *want)
+        ctx.set_launch(0)
+
+
 # ------------------------------------------------------------------------------------------
 # Several workflows sharing a GPU pool.
 def _alloc_case(cfg, insts, G_total):
