@@ -290,7 +290,6 @@ __device__ __forceinline__ void block_finish(uint32_t L, uint64_t x, uint32_t it
                                              uint32_t hint = kNoLatency)
 {
     __shared__ uint32_t last_block;
-    Winner *slot = &winners[(uint64_t)item * blocks_per_item + sub];
     if (blocks_per_item == 1) {
         // The block is the whole item: its minimum, held by wave 0, is the item's winner (no
         // fence, counter or winner slot).
@@ -302,7 +301,7 @@ __device__ __forceinline__ void block_finish(uint32_t L, uint64_t x, uint32_t it
     block_min(L, x);
     if (threadIdx.x == 0) {
         if (L != kNoLatency && L <= hint && L <= atomicMin(&fa.best[item], L)) {
-            store_winner(L, x, slot);
+            store_winner(L, x, &winners[(uint64_t)item * blocks_per_item + sub]);
             __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
         }
         const uint32_t prev = atomicAdd(&fa.done[item], 1u);
