@@ -110,6 +110,7 @@ struct alp_ctx {
     alp::TablesDev tdev{};
 
     DevBuf q_inst, rec, ext, inner, done, winners, idx, evals, tmax;   // q_inst: inst | cap | lambda
+    DevBuf pair;                            // pair tables of the scan's pair form
     DevBuf split_dp;                        // allocate_kernel's knapsack table
     DevBuf pruned_table, pruned_orders, pruned_counts;   // pruned search scratch
     DevBuf place_in, place_out;                          // placement records
@@ -306,6 +307,46 @@ alp::ScanGeometry plan_scan(alp_ctx *c, uint32_t count)
     g.variant = c->variant == 0 || c->variant >= 4 ? 1 : c->variant;
     g.slots = slots_for(sp.O);
     const uint64_t cus = c->num_cus > 0 ? (uint64_t)c->num_cus : 256;
+    // Pair form (variant 1; forced by variant 6, chosen for 5 or more LLMs while the tables stay
+    // small): LLMs M-3 and M-2 folded into one inner table of O^2 records, so a row carries
+    // O^2 candidates per lane-slot and the per-row work is spread over 128 times more of them.
+    // Rows are split into sub-rows of at most 1,024 records, claimed within blocks of 16 waves,
+    // 32 waves per CU per round and four rounds of blocks, about 8 sub-rows per wave.
+    constexpr uint64_t kPairBytesMax = UINT64_C(64) << 20;
+    if (g.variant == 1 && sp.M >= 3 && (c->variant == 6 || (c->variant == 0 && sp.M >= 5)) &&
+        (uint64_t)count * alp::pair_stride(sp.O) * sizeof(uint2) <= kPairBytesMax) {
+        uint64_t rows = 1;
+        for (uint32_t m = 3; m < sp.M; ++m)
+            rows *= sp.O;
+        const uint32_t n16 = alp::pair_stride(sp.O) / 16;
+        uint32_t chunks = n16;
+        for (uint32_t k = 1; k <= n16; ++k)
+            if (n16 % k == 0 && alp::pair_stride(sp.O) / k <= 1024) {
+                chunks = k;
+                break;
+            }
+        if (c->chunks_override && n16 % c->chunks_override == 0)
+            chunks = c->chunks_override;
+        const uint64_t sub_rows = rows * chunks;
+        if (sub_rows < (UINT64_C(1) << 32)) {
+            g.pair = 1;
+            g.dynamic = 1;
+            g.chunks = chunks;
+            g.rows = sub_rows;
+            g.threads = c->tpb_override ? c->tpb_override : 1024;
+            const uint64_t wpb = g.threads / 64;
+            const uint64_t items = std::max<uint64_t>(1, count);
+            const uint64_t waves =
+                std::max<uint64_t>(1, std::min<uint64_t>(cus * 32 * 4, items * sub_rows / 8));
+            uint64_t bpi = c->bpi_override ? c->bpi_override
+                                           : std::max<uint64_t>(1, ceil_div(waves, items * wpb));
+            g.rows_per_wave = ceil_div(g.rows, bpi * wpb);
+            if (!c->bpi_override)
+                bpi = ceil_div(g.rows, g.rows_per_wave * wpb);
+            g.blocks_per_item = (uint32_t)bpi;
+            return g;
+        }
+    }
     if (g.variant != 2) {
         g.rows = 1;
         for (uint32_t m = 2; m < sp.M; ++m)
@@ -354,7 +395,7 @@ alp::ScanGeometry plan_scan(alp_ctx *c, uint32_t count)
             wpb = g.threads / 64;
             if (!c->bpi_override)
                 bpi = std::max<uint64_t>(1, ceil_div(waves, items * wpb));
-            if (splittable && c->chunks_override) {
+            if (splittable && c->chunks_override && n16 % c->chunks_override == 0) {
                 g.chunks = c->chunks_override;
             } else if (splittable) {
                 g.chunks = n16;
@@ -501,6 +542,15 @@ int32_t launch_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count, alp_re
                                       raw, timed ? ev[0] : nullptr, timed ? ev[1] : nullptr)) !=
         hipSuccess)
         return hip_fail(e, "option_terms launch");
+    if (g.pair) {
+        if ((e = c->pair.ensure((uint64_t)count * alp::pair_stride(sp.O) * sizeof(uint2))) !=
+            hipSuccess)
+            return hip_fail(e, "hipMalloc(pair table)");
+        inner = (uint2 *)c->pair.ptr;
+        if ((e = alp::launch_pair_terms(sp, count, rec, (const uint2 *)c->inner.ptr, inner,
+                                        c->stream)) != hipSuccess)
+            return hip_fail(e, "pair_terms launch");
+    }
     if ((e = alp::launch_scan(sp, q, count, rec, inner, g, win, fa, c->stream,
                               timed ? ev[2] : nullptr, timed ? ev[3] : nullptr)) != hipSuccess)
         return hip_fail(e, "scan launch");
@@ -597,7 +647,7 @@ int32_t alp_load_profiles(alp_ctx **out, const alp_space_t *space, uint32_t num_
         return fail(ALP_ENOMEM, "host allocation failed");
     c->device = device;
     c->stream = (hipStream_t)hip_stream;
-    for (DevBuf *b : {&c->q_inst, &c->rec, &c->ext, &c->inner, &c->done, &c->winners}) {
+    for (DevBuf *b : {&c->q_inst, &c->rec, &c->ext, &c->inner, &c->done, &c->winners, &c->pair}) {
         b->guarded = true;                              // used by alp_search_batch_async
         b->stream = c->stream;
     }
@@ -1170,15 +1220,19 @@ int32_t alp_set_launch(alp_ctx *ctx, uint32_t variant, uint32_t blocks_per_item,
 {
     if (!ctx)
         return fail(ALP_EINVAL, "ctx is NULL");
-    if (variant > 5)
-        return fail(ALP_EINVAL, "variant %u not in 0..5", variant);
+    if (variant > 6)
+        return fail(ALP_EINVAL, "variant %u not in 0..6", variant);
     if (threads_per_block && (threads_per_block % 64 || threads_per_block > 1024))
         return fail(ALP_EINVAL, "threads_per_block must be a multiple of 64, at most 1024");
     if (blocks_per_item > (1u << 24))
         return fail(ALP_EINVAL, "blocks_per_item too large");
+    // inner_chunks must divide the inner table's groups of 16 records (the pair table's, for
+    // variant 6); the planner uses it only where it divides the table the launch scans.
     const uint32_t n16 = alp::inner_stride(ctx->sp.O) / 16;
-    if (inner_chunks && (inner_chunks > n16 || n16 % inner_chunks))
-        return fail(ALP_EINVAL, "inner_chunks %u does not divide %u", inner_chunks, n16);
+    const uint32_t p16 = alp::pair_stride(ctx->sp.O) / 16;
+    const uint32_t d16 = variant == 6 ? p16 : n16;
+    if (inner_chunks && (inner_chunks > d16 || d16 % inner_chunks))
+        return fail(ALP_EINVAL, "inner_chunks %u does not divide %u", inner_chunks, d16);
     ctx->variant = variant;
     ctx->bpi_override = blocks_per_item;
     ctx->tpb_override = threads_per_block;
@@ -1255,7 +1309,7 @@ void alp_free(alp_ctx *ctx)
     DevBuf *bufs[] = {&ctx->tables, &ctx->q_inst, &ctx->rec, &ctx->ext, &ctx->inner, &ctx->done,
                       &ctx->winners, &ctx->idx, &ctx->evals, &ctx->tmax, &ctx->split_dp,
                       &ctx->pruned_table, &ctx->pruned_orders, &ctx->pruned_counts,
-                      &ctx->place_in, &ctx->place_out};
+                      &ctx->place_in, &ctx->place_out, &ctx->pair};
     for (DevBuf *b : bufs)
         b->release();
     if (ctx->host_results)

@@ -46,6 +46,9 @@ struct QueryDev {
 
 // Records per item of the inner-LLM table: options rounded up to a multiple of 16.
 __host__ __device__ inline uint32_t inner_stride(uint32_t O) { return (O + 15u) & ~15u; }
+// Records per item of the pair table (LLMs M-3 and M-2 folded into one inner LLM of O^2
+// options), padded to 16.
+__host__ __device__ inline uint32_t pair_stride(uint32_t O) { return (O * O + 15u) & ~15u; }
 
 // Per-block winner of a scan: lexicographic (L, x) minimum; L = kNoLatency if none.
 struct Winner {
@@ -87,6 +90,8 @@ struct ScanGeometry {
                                // per wave (0, requires chunks == 1)
     uint64_t per_thread;       // variant 2: candidates per thread
     uint32_t slots;            // variants 1, 3: options of the last LLM per lane (1, 2, 4, 8)
+    uint32_t pair;             // variant 1: the inner table is the pair table (rows fix M - 3
+                               // digits, O^2 records each)
 };
 
 // Queries of a search batch given in device memory, prepared by the option-term kernel: item i
@@ -114,6 +119,11 @@ hipError_t launch_option_terms(const SpaceDev &sp, const TablesDev &tb, const Qu
                                const ScanReset &reset, hipStream_t st,
                                const RawQueries *raw = nullptr,
                                hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
+// Pair table of count items: pair[item][j3 * O + j2] = (c of LLM M-3 option j3 + c of LLM M-2
+// option j2, Q*G - both share units), from the option-term kernel's rec and inner tables;
+// padding records never fit.
+hipError_t launch_pair_terms(const SpaceDev &sp, uint32_t count, const uint2 *rec,
+                             const uint2 *inner, uint2 *pair, hipStream_t st);
 hipError_t launch_scan(const SpaceDev &sp, const QueryDev &q, uint32_t count, const uint2 *rec,
                        const uint2 *inner, const ScanGeometry &g, Winner *winners,
                        const FinishArgs &fa, hipStream_t st, hipEvent_t t0 = nullptr,

@@ -309,8 +309,10 @@ __global__ void __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(S <= 
 scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_all, QueryDev q,
                 uint32_t M, uint32_t O, uint64_t rows, uint64_t rows_per_wave, uint32_t chunks,
                 uint32_t blocks_per_item, uint32_t nblocks, Winner *__restrict__ winners,
-                FinishArgs fa)
+                FinishArgs fa, uint32_t pair)
 {
+    // pair = 1: the inner table is the pair table of LLMs M-3 and M-2 (index j = j3 * O + j2,
+    // O^2 records), so rows fix the M - 3 outer digits; candidates keep their index order.
     // `rows` counts sub-rows: each row (one choice of the outer digits) may be split into
     // `chunks` consecutive ranges of the inner LLM's records (DYNAMIC only), so that small
     // spaces still give every wave several sub-rows; candidates stay in index order (row,
@@ -361,12 +363,13 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
         }
     }
     const bool has_inner = M >= 2;
-    const uint32_t n_inner_padded = inner_stride(O);
+    const uint32_t n_inner_padded = pair ? pair_stride(O) : inner_stride(O);
     const uint32_t chunk_len = n_inner_padded / chunks;   // a multiple of 16
     const uint2 *inner = inner_all + (uint64_t)item * n_inner_padded;
-    const uint32_t n_inner = has_inner ? O : 1;
+    const uint32_t n_inner = has_inner ? (pair ? O * O : O) : 1;
     constexpr int NMAX = NOUT >= 0 ? NOUT : (int)kMaxOuter;
-    const uint32_t n_outer = NOUT >= 0 ? (uint32_t)NOUT : (M >= 2 ? M - 2 : 0);
+    const uint32_t n_outer =
+        NOUT >= 0 ? (uint32_t)NOUT : (M >= 2 + pair ? M - 2 - pair : 0);
 
     uint32_t waveL = kNoLatency;
     uint64_t waveX = ~0ull;
@@ -900,6 +903,43 @@ tmax_kernel(SpaceDev sp, QueryDev q, const uint2 *__restrict__ ext, uint32_t *__
 // dispatch itself stamps with the kernel's begin and end (no separate event packets between
 // the kernels, which would leave the GPU idle for microseconds per search).
 
+namespace {
+
+// One thread per pair record: LLM M-3's record from rec (c, units or sentinel) and LLM M-2's
+// from inner (c, Q*G - units); the sum of two usable terms stays below 2^32 - 1, and any unusable
+// option leaves Q*G - units far below zero, so the pair never fits.
+__global__ void __launch_bounds__(256)
+pair_terms_kernel(uint32_t M, uint32_t O, uint32_t count, const uint2 *__restrict__ rec,
+                  const uint2 *__restrict__ inner, uint2 *__restrict__ pair)
+{
+    const uint32_t stride = pair_stride(O);
+    const uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= (uint64_t)count * stride)
+        return;
+    const uint32_t item = (uint32_t)(t / stride), j = (uint32_t)(t - (uint64_t)item * stride);
+    uint2 out = make_uint2(0u, (uint32_t)kNeverFits);
+    if (j < O * O) {
+        const uint32_t j3 = j / O, j2 = j - j3 * O;
+        const uint2 a = rec[((uint64_t)item * M + (M - 3)) * O + j3];
+        const uint2 b = inner[(uint64_t)item * inner_stride(O) + j2];
+        out = make_uint2(a.x + b.x, (uint32_t)((int32_t)b.y - (int32_t)a.y));
+    }
+    pair[t] = out;
+}
+
+}  // namespace
+
+hipError_t launch_pair_terms(const SpaceDev &sp, uint32_t count, const uint2 *rec,
+                             const uint2 *inner, uint2 *pair, hipStream_t st)
+{
+    const uint64_t total = (uint64_t)count * pair_stride(sp.O);
+    if (total == 0 || sp.M < 3)
+        return hipSuccess;
+    hipLaunchKernelGGL(pair_terms_kernel, dim3((uint32_t)((total + 255) / 256)), dim3(256), 0, st,
+                       sp.M, sp.O, count, rec, inner, pair);
+    return hipGetLastError();
+}
+
 hipError_t launch_option_terms(const SpaceDev &sp, const TablesDev &tb, const QueryDev &q,
                                uint32_t count, uint2 *rec, uint2 *ext, uint2 *inner,
                                const ScanReset &reset, hipStream_t st, const RawQueries *raw,
@@ -927,19 +967,19 @@ static hipError_t launch_lane(const SpaceDev &sp, const QueryDev &q, uint32_t co
                               0, st, t0, t1, 0, rec, q, sp.M, sp.O, g.rows, g.rows_per_wave,
                               g.blocks_per_item, nblocks, winners, fa);
     else {
-        const uint32_t n_outer = sp.M >= 2 ? sp.M - 2 : 0;
+        const uint32_t n_outer = sp.M >= 2 + g.pair ? sp.M - 2 - g.pair : 0;
 #define ALP_LAUNCH_MIN(NO)                                                                         \
     do {                                                                                           \
         if (g.dynamic)                                                                             \
             hipExtLaunchKernelGGL(HIP_KERNEL_NAME(scan_min_kernel<S, NO, true>), dim3(nblocks),    \
                                   dim3(g.threads), 0, st, t0, t1, 0, rec, inner, q, sp.M, sp.O,    \
                                   g.rows, g.rows_per_wave, g.chunks, g.blocks_per_item, nblocks,   \
-                                  winners, fa);                                                    \
+                                  winners, fa, g.pair);                                            \
         else                                                                                       \
             hipExtLaunchKernelGGL(HIP_KERNEL_NAME(scan_min_kernel<S, NO, false>), dim3(nblocks),   \
                                   dim3(g.threads), 0, st, t0, t1, 0, rec, inner, q, sp.M, sp.O,    \
                                   g.rows, g.rows_per_wave, 1u, g.blocks_per_item, nblocks,         \
-                                  winners, fa);                                                    \
+                                  winners, fa, g.pair);                                            \
     } while (0)
         switch (n_outer) {
         case 0: ALP_LAUNCH_MIN(0); break;

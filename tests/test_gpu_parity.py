@@ -83,8 +83,9 @@ def oracle_expect(batch, i, G, lam):
 # --------------------------------------------------------------------------------------------
 CASES = load_cases()
 # Scan variants: row-minimum (automatic distribution), thread-per-candidate, exact-tracking lanes,
-# row-minimum with fixed per-wave rows, row-minimum with rows handed out within each block.
-VARIANTS = (1, 2, 3, 4, 5)
+# row-minimum with fixed per-wave rows, row-minimum with rows handed out within each block,
+# row-minimum over the pair table of LLMs M-3 and M-2 (3 or more LLMs; otherwise automatic).
+VARIANTS = (1, 2, 3, 4, 5, 6)
 
 
 @pytest.mark.parametrize("case", CASES, ids=[c["id"] for c in CASES])
@@ -130,9 +131,13 @@ def test_full_space_matches_golden(alp, cfg):
     with alp.Context(b) as ctx:
         tm = ctx.max_throughput([r["G"] for r in rows])
         assert [int(v) for v in tm] == [r["tmax"] for r in rows]
-        for i, r in enumerate(rows):
-            res = ctx.search(i, r["G"], r["lambda"])
-            check_result(b, i, res, r["x"], r["L"], r["T"], r["U"])
+        # automatic launch (the pair table from 5 LLMs), the pair table forced, fixed row ranges
+        for variant in (0, 6, 4):
+            ctx.set_launch(variant)
+            for i, r in enumerate(rows):
+                res = ctx.search(i, r["G"], r["lambda"])
+                check_result(b, i, res, r["x"], r["L"], r["T"], r["U"])
+        ctx.set_launch(0)
 
 
 def test_cfg4_batch_matches_golden(alp):
