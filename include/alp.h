@@ -327,7 +327,7 @@ int32_t alp_eval_candidates(alp_ctx *ctx, uint32_t instance, uint32_t gpu_budget
  * between the two; rows can only be split with the second, so variant 4 ignores inner_chunks),
  * 6 row-minimum scan over the pair table (LLMs M-3 and M-2 folded into one inner LLM of O^2
  * options, 3 or more LLMs; variant 0 uses it for 5 or more LLMs while the batch's pair tables
- * stay within 64 MiB).  blocks_per_item and threads_per_block (a multiple of 64, at most 1024):
+ * stay within 4 MiB).  blocks_per_item and threads_per_block (a multiple of 64, at most 1024):
  * 0 = automatic.  inner_chunks (variants 1, 5, 6): ranges each row's inner-LLM records are
  * split into, dividing ceil(O / 16) (variant 6: the pair table's ceil(O^2 / 16)); 0 =
  * automatic.  Results do not depend on these choices. */

@@ -307,12 +307,13 @@ alp::ScanGeometry plan_scan(alp_ctx *c, uint32_t count)
     g.variant = c->variant == 0 || c->variant >= 4 ? 1 : c->variant;
     g.slots = slots_for(sp.O);
     const uint64_t cus = c->num_cus > 0 ? (uint64_t)c->num_cus : 256;
-    // Pair form (variant 1; forced by variant 6, chosen for 5 or more LLMs while the tables stay
-    // small): LLMs M-3 and M-2 folded into one inner table of O^2 records, so a row carries
-    // O^2 candidates per lane-slot and the per-row work is spread over 128 times more of them.
+    // Pair form (variant 1; forced by variant 6, chosen for 5 or more LLMs while the batch's
+    // tables stay within 4 MiB, i.e. resident in L2): LLMs M-3 and M-2 folded into one inner
+    // table of O^2 records, so a row carries O^2 candidates per lane-slot and the per-row work
+    // is spread over 128 times more of them.  (132 4-LLM items, 17 MiB of tables: slower.)
     // Rows are split into sub-rows of at most 1,024 records, claimed within blocks of 16 waves,
     // 32 waves per CU per round and four rounds of blocks, about 8 sub-rows per wave.
-    constexpr uint64_t kPairBytesMax = UINT64_C(64) << 20;
+    constexpr uint64_t kPairBytesMax = UINT64_C(4) << 20;
     if (g.variant == 1 && sp.M >= 3 && (c->variant == 6 || (c->variant == 0 && sp.M >= 5)) &&
         (uint64_t)count * alp::pair_stride(sp.O) * sizeof(uint2) <= kPairBytesMax) {
         uint64_t rows = 1;
