@@ -310,7 +310,8 @@ def test_sparse_feasibility_multi_block(alp, G, lam_frac):
     lam = max(1, t * lam_frac // 4)
     want = oracle_expect(b, 0, G, lam)
     with alp.Context(b) as ctx:
-        for launch in [(0, 0, 0, 0), (4, 0, 0, 0), (5, 0, 0, 0), (5, 64, 512, 0), (1, 0, 0, 4)]:
+        for launch in [(0, 0, 0, 0), (4, 0, 0, 0), (5, 0, 0, 0), (5, 64, 512, 0), (1, 0, 0, 4),
+                       (6, 0, 0, 0), (6, 16, 256, 64)]:
             ctx.set_launch(*launch)
             check_result(b, 0, ctx.search(0, G, lam), *want)
         ctx.set_launch(0)
