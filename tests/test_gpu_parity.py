@@ -191,12 +191,17 @@ def test_launch_geometry_and_variant_do_not_change_results(alp):
                                       (3, 5, 128, 0), (4, 0, 0, 0), (4, 7, 128, 4),
                                       (4, 3000, 1024, 0), (5, 0, 0, 0), (5, 1, 64, 0),
                                       (5, 7, 128, 8), (5, 256, 1024, 4), (5, 3000, 1024, 1),
-                                      (5, 512, 512, 2)]:
+                                      (5, 512, 512, 2), (6, 0, 0, 0), (6, 1, 64, 0),
+                                      (6, 7, 128, 16), (6, 300, 1024, 1024), (6, 3000, 256, 1)]:
             ctx.set_launch(variant, bpi, tpb, ch)
             res = ctx.search(0, g["G"], g["lambda"])
             check_result(b, 0, res, g["x"], g["L"], g["T"], g["U"])
-        with pytest.raises(alp.AlpError):
-            ctx.set_launch(1, 0, 0, 3)                 # 3 does not divide 128 / 16
+        for bad in ((1, 0, 0, 3),                      # 3 does not divide 128 / 16
+                    (1, 0, 0, 16),                     # 16 divides only the pair table's 1,024
+                    (6, 0, 0, 3),                      # 3 does not divide 128 * 128 / 16
+                    (7, 0, 0, 0), (0, 0, 96, 0)):      # no variant 7; 96 threads
+            with pytest.raises(alp.AlpError):
+                ctx.set_launch(*bad)
         ctx.set_launch(0, 0, 0)
         first = ctx.search(0, g["G"], g["lambda"])
         for _ in range(3):
