@@ -283,11 +283,13 @@ constexpr uint32_t kFinishStage = 2048;
 //
 // `hint`: the item's best latency as read earlier in this launch (kNoLatency if not read); the
 // minimum only falls, so a block above the hint skips the atomic minimum too (a plain load
-// does not queue at the atomic unit behind the other blocks' updates).
+// does not queue at the atomic unit behind the other blocks' updates).  `held` false (uniform
+// over the block) says that no wave holds a candidate at or below the hint: the block skips its
+// reduction and only counts itself.
 __device__ __forceinline__ void block_finish(uint32_t L, uint64_t x, uint32_t item,
                                              uint32_t sub, uint32_t blocks_per_item,
                                              Winner *winners, const FinishArgs &fa,
-                                             uint32_t hint = kNoLatency)
+                                             uint32_t hint = kNoLatency, bool held = true)
 {
     __shared__ uint32_t last_block;
     if (blocks_per_item == 1) {
@@ -298,9 +300,10 @@ __device__ __forceinline__ void block_finish(uint32_t L, uint64_t x, uint32_t it
             write_item_result(fa, item, L, x);
         return;
     }
-    block_min(L, x);
+    if (held)
+        block_min(L, x);
     if (threadIdx.x == 0) {
-        if (L != kNoLatency && L <= hint && L <= atomicMin(&fa.best[item], L)) {
+        if (held && L != kNoLatency && L <= hint && L <= atomicMin(&fa.best[item], L)) {
             store_winner(L, x, &winners[(uint64_t)item * blocks_per_item + sub]);
             __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
         }

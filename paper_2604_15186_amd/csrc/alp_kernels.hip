@@ -518,10 +518,11 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
             lmin = bestL[s] < lmin ? bestL[s] : lmin;
         Lstar = wave_min_u32(lmin);
     }
-    // The item's best latency so far, loaded now so that the load overlaps the block's
-    // reductions (see block_finish).
+    // The item's best latency so far as this wave sees it at the end of its loop (the loads of
+    // a block's last waves see what blocks that ended earlier published).  A block whose
+    // minimum lies above it cannot hold the item's winner and skips its re-scan.
     uint32_t hint = kNoLatency;
-    if (threadIdx.x == 0 && blocks_per_item > 1)
+    if (lane == 0 && blocks_per_item > 1)
         hint = __hip_atomic_load(&fa.best[item], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     // The wave's lowest sub-row reaching L* (its lane-slots' first rows at L*), as a sub-row
     // index of the item, and that row's outer sums, loaded now while the block's other waves
@@ -541,7 +542,7 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
     // The block's smallest latency Lb and the lowest sub-row rb reaching it: the (L*, row)
     // minimum over the waves.  Sub-rows are in candidate-index order, so the block's winner
     // is the lowest candidate of sub-row rb with latency Lb.
-    __shared__ uint32_t s_wave_L[16], s_wave_oc[16];
+    __shared__ uint32_t s_wave_L[16], s_wave_oc[16], s_wave_H[16];
     __shared__ int32_t s_wave_ou[16];
     __shared__ uint64_t s_wave_R[16];
     if (lane == 0) {
@@ -549,6 +550,7 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
         s_wave_R[wave] = rwave;
         s_wave_oc[wave] = oc_w;
         s_wave_ou[wave] = ou_w;
+        s_wave_H[wave] = hint;
     }
     __syncthreads();
     // Lane k reads wave k's pair; one wave reduction (in every wave) gives the block's.
@@ -557,7 +559,10 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
     uint32_t Lblock = mineL;
     uint64_t rb = mineR;
     wave_min(Lblock, rb);
-    if (Lblock != kNoLatency) {
+    const uint32_t block_hint = wave_min_u32(lane < wpb ? s_wave_H[lane] : kNoLatency);
+    // Uniform over the block: every wave reduced the same LDS words.
+    const bool held = Lblock != kNoLatency && Lblock <= block_hint;
+    if (held) {
         // Every wave of the block searches its share of sub-row rb (4 records per step,
         // steps interleaved over the waves) for the lowest feasible j of each lane-slot with
         // c_j = Lb - oc - c_last: no wave re-walks a whole sub-row alone.  A feasible match
@@ -604,7 +609,7 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
         waveL = Lblock;
         waveX = wave_min_u64(xmin);
     }
-    block_finish(waveL, waveX, item, sub, blocks_per_item, winners, fa, hint);
+    block_finish(waveL, waveX, item, sub, blocks_per_item, winners, fa, block_hint, held);
 }
 
 // ---------------------------------------------------------------------------------------------
