@@ -71,14 +71,16 @@ STATS_TRACES = 20_000                   # beam-search requests of the statistics
 MULTI_WORKFLOWS, MULTI_GPUS = 4, 32
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "scan_min_hbm_bytes.md")
 KERNEL_SOURCES = ("alp_kernels.hip", "alp_device.h", "alp_internal.h")
+STATS_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "trace_stats_hbm_bytes.md")
+STATS_SOURCES = ("alp_stats.hip", "alp_device.h", "alp_internal.h")
 METRIC = "ALP candidate allocations evaluated/sec on 1 GPU"
 
 
-def _traffic(kernel_digest: str, workload: str):
-    """HBM bytes per scan launch from the committed rocprofv3 counter summary, if it was taken
-    on the current kernel source and this workload."""
+def _traffic(kernel_digest: str, workload: str, path: str = TRAFFIC_FILE):
+    """HBM bytes per launch (per call for the statistics) from a committed rocprofv3 counter
+    summary, if it was taken on the current kernel source and this workload."""
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(path) as f:
             text = f.read()
         t = json.loads(text.split("```json", 1)[1].split("```", 1)[0])
     except (OSError, ValueError, IndexError):
@@ -89,11 +91,11 @@ def _traffic(kernel_digest: str, workload: str):
     return entry.get("bytes_per_launch")
 
 
-def _kernel_digest() -> str:
-    """SHA-256 over the sources compiled into the scan kernel."""
+def _kernel_digest(sources=KERNEL_SOURCES) -> str:
+    """SHA-256 over the sources compiled into the measured kernels (the scan by default)."""
     import hashlib
     h = hashlib.sha256()
-    for name in KERNEL_SOURCES:
+    for name in sources:
         with open(os.path.join(ROOT, "paper_2604_15186_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()
@@ -499,7 +501,8 @@ def run_stats(args, alp):
               "n_milli": [int(v) for v in out["n_milli"]],
               "p_milli": [int(v) for v in out["p_milli"]]}
     roofline = {"bound": "hbm", "achieved": achieved / 1e9, "peak": HBM_PEAK / 1e9,
-                "unit": "GB/s", "frac": achieved / HBM_PEAK, "traffic": None,
+                "unit": "GB/s", "frac": achieved / HBM_PEAK,
+                "traffic": _traffic(_kernel_digest(STATS_SOURCES), "stats", STATS_TRAFFIC_FILE),
                 "kernel": "trace statistics (all kernels)", "kernel_ms": k_s * 1e3,
                 "bytes_per_call": 20}
     cpu = None if args.no_cpu_baseline else cpu_baseline_stats(tr, args.cpu_seconds)
