@@ -232,10 +232,9 @@ class Context:
                 count * RESULT_DTYPE.itemsize:
             raise ValueError(f"out must be a contiguous device tensor of {count} x "
                              f"{RESULT_DTYPE.itemsize} bytes")
-        _check(lib().alp_search_batch_async(self._ctx, count,
-                                            None if instances is None else instances.data_ptr(),
-                                            gpu_budget.data_ptr(), target_milli.data_ptr(),
-                                            out.data_ptr()))
+        fn = lib().alp_search_batch_async
+        _check(fn(self._ctx, count, None if instances is None else instances.data_ptr(),
+                  gpu_budget.data_ptr(), target_milli.data_ptr(), out.data_ptr()))
 
     def max_throughput(self, gpu_budget, instances=None) -> np.ndarray:
         G = np.ascontiguousarray(gpu_budget, dtype=np.uint32)

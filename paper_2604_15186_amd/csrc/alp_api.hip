@@ -299,7 +299,11 @@ uint64_t blocks_per_item_for_rounds(uint64_t count, uint64_t resident, uint64_t 
     return best;
 }
 
-alp::ScanGeometry plan_scan(alp_ctx *c, uint32_t count)
+// Launch geometry of a scan of `count` items.  ERANGE when no launch can cover the space: the
+// fixed-range form counts a wave's rows in 32 bits, so a wave must get fewer than 2^32 rows
+// (the automatic plan adds blocks until it does; a blocks_per_item override that leaves a wave
+// more is rejected), and a launch holds fewer than 2^31 blocks.
+int32_t plan_scan(alp_ctx *c, uint32_t count, alp::ScanGeometry &out)
 {
     alp::ScanGeometry g{};
     const alp::SpaceDev &sp = c->sp;
@@ -344,8 +348,12 @@ alp::ScanGeometry plan_scan(alp_ctx *c, uint32_t count)
             g.rows_per_wave = ceil_div(g.rows, bpi * wpb);
             if (!c->bpi_override)
                 bpi = ceil_div(g.rows, g.rows_per_wave * wpb);
+            if (bpi * items >= (UINT64_C(1) << 31))
+                return fail(ALP_ERANGE, "batch too large for one launch (%llu blocks)",
+                            (unsigned long long)(bpi * items));
             g.blocks_per_item = (uint32_t)bpi;
-            return g;
+            out = g;
+            return ALP_OK;
         }
     }
     if (g.variant != 2) {
@@ -409,9 +417,21 @@ alp::ScanGeometry plan_scan(alp_ctx *c, uint32_t count)
             g.rows *= g.chunks;
         }
         g.dynamic = dyn ? 1u : 0u;
+        constexpr uint64_t kWaveRowsMax = UINT64_C(0xFFFFFFFF);
+        if (g.variant == 1 && !dyn && ceil_div(g.rows, bpi * wpb) > kWaveRowsMax) {
+            if (c->bpi_override)
+                return fail(ALP_ERANGE,
+                            "blocks_per_item %u leaves a wave %llu rows (at most 2^32 - 1); "
+                            "raise blocks_per_item", c->bpi_override,
+                            (unsigned long long)ceil_div(g.rows, bpi * wpb));
+            bpi = ceil_div(g.rows, kWaveRowsMax * wpb);
+        }
         g.rows_per_wave = ceil_div(g.rows, bpi * wpb);
         if (!c->bpi_override)
             bpi = ceil_div(g.rows, g.rows_per_wave * wpb);
+        if (bpi * std::max<uint64_t>(1, count) >= (UINT64_C(1) << 31))
+            return fail(ALP_ERANGE, "batch too large for one launch (%llu blocks)",
+                        (unsigned long long)(bpi * std::max<uint64_t>(1, count)));
         g.blocks_per_item = (uint32_t)bpi;
     } else {
         g.threads = c->tpb_override ? c->tpb_override : 256;
@@ -424,9 +444,13 @@ alp::ScanGeometry plan_scan(alp_ctx *c, uint32_t count)
         if (bpi < 1)
             bpi = 1;
         g.per_thread = ceil_div(c->N, bpi * g.threads);
+        if (bpi * std::max<uint64_t>(1, count) >= (UINT64_C(1) << 31))
+            return fail(ALP_ERANGE, "batch too large for one launch (%llu blocks)",
+                        (unsigned long long)(bpi * std::max<uint64_t>(1, count)));
         g.blocks_per_item = (uint32_t)bpi;
     }
-    return g;
+    out = g;
+    return ALP_OK;
 }
 
 int32_t ensure_host_query(alp_ctx *c, size_t count)
@@ -493,70 +517,115 @@ int32_t ensure_host_results(alp_ctx *c, size_t count)
     return ALP_OK;
 }
 
-// Runs option terms -> scan (with the fused final reduction) for `count` items described by q;
-// the kernels write the results straight into c->host_results[0..count) (mapped pinned memory).
-// Queues the option-term and scan kernels of `count` searches on the context stream.  Results go
-// to `out` (device-visible); with device queries (raw), rejected ones to EINVAL records.  ev
-// (4 events or nullptr): begin and end of the option-term kernel, then of the scan, stamped by
-// the dispatches.
-int32_t launch_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count, alp_result_t *out,
-                      const alp::RawQueries *raw, hipEvent_t *ev)
+// Device scratch of one search launch: per-option records, the inner (or pair) table, the
+// per-item counters and the block winners.
+struct SearchScratch {
+    uint2 *rec = nullptr, *ext = nullptr, *inner = nullptr, *pair = nullptr;
+    uint32_t *done = nullptr, *best = nullptr;
+    alp::Winner *winners = nullptr;
+};
+
+// Byte sizes of the scratch parts of a launch of `count` items with geometry g.  done[count],
+// then best[count] at least 4 KiB further: the two per-item words take one atomic per block
+// each, and counters in one line would queue behind each other.
+struct ScratchSizes {
+    uint64_t rec, inner, pair, counters, best_at, winners;
+};
+
+ScratchSizes scratch_sizes(const alp::SpaceDev &sp, uint32_t count, const alp::ScanGeometry &g)
+{
+    ScratchSizes z;
+    z.rec = (uint64_t)count * sp.M * sp.O * sizeof(uint2);
+    z.inner = (uint64_t)count * alp::inner_stride(sp.O) * sizeof(uint2);
+    z.pair = g.pair ? (uint64_t)count * alp::pair_stride(sp.O) * sizeof(uint2) : 0;
+    z.best_at = ((uint64_t)count + 2047) / 1024 * 1024;
+    z.counters = (z.best_at + count) * sizeof(uint32_t);
+    z.winners = (uint64_t)count * g.blocks_per_item * sizeof(alp::Winner);
+    return z;
+}
+
+// The context's own scratch buffers, grown to the launch's sizes.
+int32_t context_scratch(alp_ctx *c, uint32_t count, const alp::ScanGeometry &g, SearchScratch &s)
+{
+    const ScratchSizes z = scratch_sizes(c->sp, count, g);
+    hipError_t e;
+    if ((e = c->rec.ensure(z.rec)) != hipSuccess)
+        return hip_fail(e, "hipMalloc(rec)");
+    if ((e = c->ext.ensure(z.rec)) != hipSuccess)
+        return hip_fail(e, "hipMalloc(ext)");
+    if ((e = c->inner.ensure(z.inner)) != hipSuccess)
+        return hip_fail(e, "hipMalloc(inner)");
+    if ((e = c->done.ensure(z.counters)) != hipSuccess)
+        return hip_fail(e, "hipMalloc(done)");
+    if ((e = c->winners.ensure(z.winners)) != hipSuccess)
+        return hip_fail(e, "hipMalloc(winners)");
+    if (g.pair && (e = c->pair.ensure(z.pair)) != hipSuccess)
+        return hip_fail(e, "hipMalloc(pair table)");
+    s.rec = (uint2 *)c->rec.ptr;
+    s.ext = (uint2 *)c->ext.ptr;
+    s.inner = (uint2 *)c->inner.ptr;
+    s.pair = g.pair ? (uint2 *)c->pair.ptr : nullptr;
+    s.done = (uint32_t *)c->done.ptr;
+    s.best = s.done + z.best_at;
+    s.winners = (alp::Winner *)c->winners.ptr;
+    return ALP_OK;
+}
+
+// Queues the option-term and scan kernels (with the fused final reduction and result decode) of
+// `count` searches described by q on the context stream, using scratch s for geometry g.
+// Results go to `out` (device-visible); with device queries (raw), rejected ones to EINVAL
+// records.  ev (4 events or nullptr): begin and end of the option-term kernel, then of the scan,
+// stamped by the dispatches.
+int32_t launch_search_with(alp_ctx *c, const alp::QueryDev &q, uint32_t count, alp_result_t *out,
+                           const alp::RawQueries *raw, hipEvent_t *ev, const alp::ScanGeometry &g,
+                           const SearchScratch &s)
 {
     const bool timed = ev != nullptr;
     const alp::SpaceDev &sp = c->sp;
-    const alp::ScanGeometry g = plan_scan(c, count);
-    const uint64_t items_bytes = (uint64_t)count * sp.M * sp.O * sizeof(uint2);
     const uint64_t nwin = (uint64_t)count * g.blocks_per_item;
-    if (nwin >= (UINT64_C(1) << 31))
-        return fail(ALP_ERANGE, "batch too large for one launch (%llu blocks)",
-                    (unsigned long long)nwin);
-    hipError_t e;
-    if ((e = c->rec.ensure(items_bytes)) != hipSuccess)
-        return hip_fail(e, "hipMalloc(rec)");
-    if ((e = c->ext.ensure(items_bytes)) != hipSuccess)
-        return hip_fail(e, "hipMalloc(ext)");
-    if ((e = c->inner.ensure((uint64_t)count * alp::inner_stride(sp.O) * sizeof(uint2))) != hipSuccess)
-        return hip_fail(e, "hipMalloc(inner)");
-    // done[count], then best[count] at least 4 KiB further: the two per-item words take one
-    // atomic per block each, and counters in one line would queue behind each other.
-    const uint64_t best_at = ((uint64_t)count + 2047) / 1024 * 1024;
-    if ((e = c->done.ensure((best_at + count) * sizeof(uint32_t))) != hipSuccess)
-        return hip_fail(e, "hipMalloc(done)");
-    if ((e = c->winners.ensure(nwin * sizeof(alp::Winner))) != hipSuccess)
-        return hip_fail(e, "hipMalloc(winners)");
-
-    uint2 *rec = (uint2 *)c->rec.ptr, *ext = (uint2 *)c->ext.ptr, *inner = (uint2 *)c->inner.ptr;
-    alp::Winner *win = (alp::Winner *)c->winners.ptr;
     alp::FinishArgs fa;
     fa.sp = sp;
-    fa.ext = ext;
-    fa.done = (uint32_t *)c->done.ptr;
-    fa.best = fa.done + best_at;
+    fa.ext = s.ext;
+    fa.done = s.done;
+    fa.best = s.best;
     fa.out = out;
     fa.invalid = raw ? raw->invalid : nullptr;
     alp::ScanReset reset;
-    reset.done = fa.done;
-    reset.best = fa.best;
-    reset.winners = win;
+    reset.done = s.done;
+    reset.best = s.best;
+    reset.winners = s.winners;
     reset.n_winners = nwin;
-    if ((e = alp::launch_option_terms(sp, c->tdev, q, count, rec, ext, inner, reset, c->stream,
-                                      raw, timed ? ev[0] : nullptr, timed ? ev[1] : nullptr)) !=
-        hipSuccess)
+    hipError_t e;
+    if ((e = alp::launch_option_terms(sp, c->tdev, q, count, s.rec, s.ext, s.inner, reset,
+                                      c->stream, raw, timed ? ev[0] : nullptr,
+                                      timed ? ev[1] : nullptr)) != hipSuccess)
         return hip_fail(e, "option_terms launch");
+    const uint2 *inner = s.inner;
     if (g.pair) {
-        if ((e = c->pair.ensure((uint64_t)count * alp::pair_stride(sp.O) * sizeof(uint2))) !=
+        if ((e = alp::launch_pair_terms(sp, count, s.rec, s.inner, s.pair, c->stream)) !=
             hipSuccess)
-            return hip_fail(e, "hipMalloc(pair table)");
-        inner = (uint2 *)c->pair.ptr;
-        if ((e = alp::launch_pair_terms(sp, count, rec, (const uint2 *)c->inner.ptr, inner,
-                                        c->stream)) != hipSuccess)
             return hip_fail(e, "pair_terms launch");
+        inner = s.pair;
     }
-    if ((e = alp::launch_scan(sp, q, count, rec, inner, g, win, fa, c->stream,
+    if ((e = alp::launch_scan(sp, q, count, s.rec, inner, g, s.winners, fa, c->stream,
                               timed ? ev[2] : nullptr, timed ? ev[3] : nullptr)) != hipSuccess)
         return hip_fail(e, "scan launch");
-    c->last_blocks = count * g.blocks_per_item;
+    c->last_blocks = (uint32_t)nwin;
     return ALP_OK;
+}
+
+// launch_search_with on the context's own (growing) scratch buffers.
+int32_t launch_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count, alp_result_t *out,
+                      const alp::RawQueries *raw, hipEvent_t *ev)
+{
+    alp::ScanGeometry g;
+    int32_t st = plan_scan(c, count, g);
+    if (st != ALP_OK)
+        return st;
+    SearchScratch s;
+    if ((st = context_scratch(c, count, g, s)) != ALP_OK)
+        return st;
+    return launch_search_with(c, q, count, out, raw, ev, g, s);
 }
 
 // Synchronous searches: results in the context's mapped host buffer.

@@ -192,3 +192,25 @@ def test_async_kernel_times_are_collected(alp):
         assert 0 < last[1] < tot[1]                      # one call's scan, four calls' sum
         ctx.set_timing(True)
         assert (ctx.kernel_time_totals()[0] == 0).all()
+
+
+def test_wave_row_count_beyond_32_bits_is_rejected(alp):
+    """The fixed-range scan counts a wave's rows in 32 bits: an override that would give one
+    wave 2^32 rows or more (8 LLMs of 128 options, one 64-thread block: 128^6 = 2^42 rows) is
+    rejected with ERANGE before anything is launched, not answered."""
+    import torch
+    from workloads import make_custom
+    b = make_custom(3, 8, (1, 2, 4, 8), (1, 2, 3, 4), 8, 2, 64)
+    with alp.Context(b) as ctx:
+        assert ctx.num_candidates == 1 << 56
+        ctx.set_launch(4, 1, 64, 0)
+        with pytest.raises(alp.AlpError) as err:
+            ctx.search(0, 64, 1)
+        assert err.value.status == alp.ALP_ERANGE and "rows" in str(err.value)
+        G = torch.full((1,), 64, dtype=torch.int32, device="cuda")
+        out = torch.zeros(alp.RESULT_DTYPE.itemsize, dtype=torch.uint8, device="cuda")
+        with pytest.raises(alp.AlpError) as err:
+            ctx.search_batch_async(G, G, out)
+        assert err.value.status == alp.ALP_ERANGE
+        torch.cuda.synchronize()
+        assert int(out.sum()) == 0
