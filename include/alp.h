@@ -163,6 +163,27 @@ int32_t alp_search_batch_async(alp_ctx *ctx, uint32_t count, const uint32_t *ins
                                const uint32_t *gpu_budget, const uint32_t *target_milli,
                                alp_result_t *out);
 
+/* ---- Searches that allocate nothing ----------------------------------------------------------
+ * For callers that cannot allocate device memory: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc.  The same searches as alp_search_batch_async (same
+ * arguments, device-resident queries and results, queued on the context stream without waiting,
+ * the same result records), but every buffer the search needs beyond its inputs and outputs
+ * (prepared queries, per-option records, the inner or pair table, per-item counters, block
+ * winners) lives in one fixed device array of ALP_STATIC_SCRATCH_BYTES per GPU, whose address
+ * alp_load_profiles takes; the call itself allocates nothing, device or host, and creates no
+ * events (it is not counted or timed by alp_set_timing).  The kernels reset what must start at
+ * zero, so the array's leftover contents from the previous call do not matter.  The array is
+ * shared by every context and every call on its GPU: calls that overlap in time on one GPU (two
+ * streams, two contexts, two threads) race on it and give undefined results, so the caller
+ * serialises them (calls queued on one stream are ordered).  Returns ALP_ERANGE, before queuing
+ * anything, if the batch needs more than the array holds (alp_last_error states both sizes;
+ * about 11 KiB per 5-LLM search plus the 128 KiB pair table, 6 KiB per 3-LLM search), and
+ * ALP_EDEVICE if the array's address could not be taken at load. */
+#define ALP_STATIC_SCRATCH_BYTES (8u << 20)
+int32_t alp_search_batch_async_noalloc(alp_ctx *ctx, uint32_t count, const uint32_t *instances,
+                                       const uint32_t *gpu_budget, const uint32_t *target_milli,
+                                       alp_result_t *out);
+
 /* Largest workflow throughput T_w (Eq. 2) any candidate with deployable, fitting options
  * reaches within the budget, ignoring the target; 0 if none fits.  A target above it is
  * infeasible, a target at or below it is feasible.  instances may be NULL. */

@@ -17,7 +17,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libalp.so")
 SOURCES = ["alp_api.hip", "alp_kernels.hip", "alp_split.hip", "alp_pruned.hip", "alp_stats.hip",
-           "alp_place.hip"]
+           "alp_place.hip", "alp_static.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 COMPILE_FLAGS = [

@@ -21,6 +21,7 @@ MAX_LLMS = 8
 
 # Symbols declared in include/alp.h.
 EXPORTS = ("alp_load_profiles", "alp_search", "alp_search_batch", "alp_search_batch_async",
+           "alp_search_batch_async_noalloc",
            "alp_max_throughput", "alp_allocate_workflows", "alp_search_pruned", "alp_stats_create",
            "alp_trace_stats", "alp_stats_set_timing", "alp_stats_time", "alp_stats_free", "alp_place",
            "alp_eval_candidates",
@@ -80,6 +81,7 @@ def lib():
         L.alp_search.argtypes = [vp, u32, u32, u32, vp]
         L.alp_search_batch.argtypes = [vp, u32, vp, vp, vp, vp]
         L.alp_search_batch_async.argtypes = [vp, u32, vp, vp, vp, vp]
+        L.alp_search_batch_async_noalloc.argtypes = [vp, u32, vp, vp, vp, vp]
         L.alp_max_throughput.argtypes = [vp, u32, vp, vp, vp]
         L.alp_eval_candidates.argtypes = [vp, u32, u32, u32, vp, u64, vp]
         L.alp_allocate_workflows.argtypes = [vp, u32, vp, vp, u32, u32, vp, vp, vp]
@@ -97,7 +99,8 @@ def lib():
         L.alp_kernel_time_totals.argtypes = [vp, C.POINTER(C.c_double), C.POINTER(u64)]
         L.alp_num_candidates.argtypes = [vp, C.POINTER(u64)]
         for name in ("alp_load_profiles", "alp_search", "alp_search_batch",
-                     "alp_search_batch_async", "alp_max_throughput",
+                     "alp_search_batch_async", "alp_search_batch_async_noalloc",
+                     "alp_max_throughput",
                      "alp_allocate_workflows", "alp_search_pruned", "alp_stats_create",
                      "alp_trace_stats", "alp_stats_set_timing", "alp_stats_time", "alp_place",
                      "alp_eval_candidates", "alp_set_launch", "alp_set_timing",
@@ -218,11 +221,13 @@ class Context:
                                       _ptr(G), _ptr(lam), _ptr(out)))
         return out
 
-    def search_batch_async(self, gpu_budget, target_milli, out, instances=None) -> None:
+    def search_batch_async(self, gpu_budget, target_milli, out, instances=None,
+                           noalloc: bool = False) -> None:
         """alp_search_batch_async: torch tensors on the context's device -- gpu_budget,
         target_milli (and instances) of int32 or uint32, out of uint8 with count * 48 bytes.
         Queued on the context stream; read out after that stream's work is done (see
-        results_from_device)."""
+        results_from_device).  noalloc: alp_search_batch_async_noalloc instead (scratch in the
+        library's fixed device array)."""
         count = int(gpu_budget.numel())
         tensors = [gpu_budget, target_milli] + ([] if instances is None else [instances])
         for t in tensors:
@@ -232,7 +237,7 @@ class Context:
                 count * RESULT_DTYPE.itemsize:
             raise ValueError(f"out must be a contiguous device tensor of {count} x "
                              f"{RESULT_DTYPE.itemsize} bytes")
-        fn = lib().alp_search_batch_async
+        fn = lib().alp_search_batch_async_noalloc if noalloc else lib().alp_search_batch_async
         _check(fn(self._ctx, count, None if instances is None else instances.data_ptr(),
                   gpu_budget.data_ptr(), target_milli.data_ptr(), out.data_ptr()))
 

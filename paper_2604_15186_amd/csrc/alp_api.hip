@@ -138,6 +138,10 @@ struct alp_ctx {
     double total_ms[3] = {0, 0, 0};     // sums of last_ms since timing was last set
     void tally(int k) { total_ms[k] += last_ms[k]; }
     uint32_t last_blocks = 0;
+    // The fixed scratch array of alp_search_batch_async_noalloc on this context's device, or
+    // nullptr with static_status saying why its address could not be taken.
+    uint8_t *static_scratch = nullptr;
+    hipError_t static_status = hipSuccess;
 };
 
 namespace {
@@ -787,6 +791,11 @@ int32_t alp_load_profiles(alp_ctx **out, const alp_space_t *space, uint32_t num_
             return st;
         }
     }
+    // Set-up of the allocation-free entry point: the device address of this GPU's fixed scratch
+    // array (the device is current here).  A failure only disables that entry point.
+    void *fixed = nullptr;
+    c->static_status = alp::static_scratch_address(device, &fixed);
+    c->static_scratch = c->static_status == hipSuccess ? (uint8_t *)fixed : nullptr;
     *out = c;
     return ALP_OK;
 }
@@ -894,6 +903,58 @@ int32_t alp_search_batch_async(alp_ctx *ctx, uint32_t count, const uint32_t *ins
         ctx->ev_pending.pop_back();
     }
     return st;
+}
+
+int32_t alp_search_batch_async_noalloc(alp_ctx *ctx, uint32_t count, const uint32_t *instances,
+                                       const uint32_t *gpu_budget, const uint32_t *target_milli,
+                                       alp_result_t *out)
+{
+    if (!ctx)
+        return fail(ALP_EINVAL, "ctx is NULL");
+    if (count == 0)
+        return ALP_OK;
+    if (!gpu_budget || !target_milli || !out)
+        return fail(ALP_EINVAL, "gpu_budget, target_milli or out is NULL");
+    if (!ctx->static_scratch)
+        return fail(ALP_EDEVICE, "the fixed scratch array of device %d has no address: %s",
+                    ctx->device, hipGetErrorString(ctx->static_status));
+    alp::ScanGeometry g;
+    int32_t st = plan_scan(ctx, count, g);
+    if (st != ALP_OK)
+        return st;
+    // Carve the fixed array: queries (inst | cap | lambda | rejection flags), then the search
+    // scratch, each part 256-byte aligned.
+    const ScratchSizes z = scratch_sizes(ctx->sp, count, g);
+    auto align = [](uint64_t v) { return (v + 255) & ~UINT64_C(255); };
+    const uint64_t off_q = 0, off_rec = align(off_q + 4ull * count * sizeof(uint32_t)),
+                   off_ext = align(off_rec + z.rec), off_inner = align(off_ext + z.rec),
+                   off_pair = align(off_inner + z.inner), off_cnt = align(off_pair + z.pair),
+                   off_win = align(off_cnt + z.counters), total = off_win + z.winners;
+    if (total > ALP_STATIC_SCRATCH_BYTES)
+        return fail(ALP_ERANGE,
+                    "%u searches need %llu bytes of scratch; the fixed array holds %u "
+                    "(use alp_search_batch_async, or fewer searches per call)",
+                    count, (unsigned long long)total, (unsigned)ALP_STATIC_SCRATCH_BYTES);
+    DeviceGuard guard(ctx->device);
+    if (guard.status != hipSuccess)
+        return hip_fail(guard.status, "hipSetDevice");
+    uint8_t *base = ctx->static_scratch;
+    uint32_t *qi = (uint32_t *)(base + off_q);
+    alp::RawQueries raw{instances, gpu_budget, target_milli, ctx->B, ctx->space.units_per_gpu,
+                        qi, qi + count, qi + 2 * (size_t)count, qi + 3 * (size_t)count};
+    alp::QueryDev q{};
+    q.inst = qi;
+    q.capacity = qi + count;
+    q.lambda = qi + 2 * (size_t)count;
+    SearchScratch s;
+    s.rec = (uint2 *)(base + off_rec);
+    s.ext = (uint2 *)(base + off_ext);
+    s.inner = (uint2 *)(base + off_inner);
+    s.pair = g.pair ? (uint2 *)(base + off_pair) : nullptr;
+    s.done = (uint32_t *)(base + off_cnt);
+    s.best = s.done + z.best_at;
+    s.winners = (alp::Winner *)(base + off_win);
+    return launch_search_with(ctx, q, count, out, &raw, nullptr, g, s);
 }
 
 int32_t alp_max_throughput(alp_ctx *ctx, uint32_t count, const uint32_t *instances,

@@ -192,6 +192,10 @@ hipError_t launch_place(uint32_t Q, uint32_t count, const PlaceIn *in, alp_place
 static_assert(sizeof(alp_placement_t) == 272 && offsetof(alp_placement_t, slot) == 16,
               "alp_placement_t layout");
 
+// Device address of the fixed scratch array of alp_search_batch_async_noalloc on `device`, which
+// must be the current device.  Looked up once per device; later calls return the kept address.
+hipError_t static_scratch_address(int device, void **ptr);
+
 // Resident blocks per CU of the scan kernels at a given block size (occupancy query).
 int scan_blocks_per_cu(uint32_t variant, uint32_t slots, uint32_t threads, const SpaceDev &sp);
 
