@@ -15,10 +15,20 @@ space with G = 64 GPUs and 128 options per LLM (2^35 = 34,359,738,368 candidates
 Prints one JSON line.
 
 ``value`` = candidates evaluated per second.  ``roofline`` relates the scan kernel (the dominant
-kernel) to the integer VALU peak of the chip: 2 int32 lane operations per candidate (the budget
-comparison and the objective minimum update), 256 CUs x 64 lanes x 2.4 GHz = 39.32 Tlane-op/s;
-the kernel duration is measured with HIP events on the stream the library launches on.
-``cpu_baseline`` times the CPU oracle, single-threaded, on a bounded slice of the same space.
+kernel) to the integer VALU peak of the chip: 2 int32 lane operations per candidate, the work the
+kernel issues (the budget comparison and the objective minimum update), against CUs x 64 lanes x
+the maximum engine clock, both read from rocminfo in the run (256 CUs and 2.4 GHz on MI355X:
+39.32 Tlane-op/s).  The kernel duration is the median over separately timed steps after the timed
+region, from HIP events stamped on the scan dispatch on the stream the library launches on.
+``cpu_baseline`` times the CPU oracle on a bounded slice of the same space, in worker processes
+on every host core of the job (at most 16), before the benchmark touches the GPU.
+
+The default run also measures the other exhaustive workloads in the same process and reports
+them under ``config.other_workloads``: the single 4-LLM search (cfg2) and the 4,096-search batch
+(cfg4) with their scan-kernel medians and roofline fractions, and the 2- and 3-LLM searches
+(cfg0, cfg1) with their HBM-resident step and ``alp_search`` call latency.  ``--only`` skips them.
+``--oracle-full`` adds the oracle's full argmin of the workload's instance 0 across the host
+cores (wall time and core count; about a minute for the 5-LLM space).
 
 The paper's own pruned search (alp_search_pruned) has two workloads of its own, where a step is
 one pruned search and ``value`` counts fraction vectors per second:
@@ -53,16 +63,20 @@ sys.path.insert(0, ROOT)
 
 from workloads import CONFIGS, make_batch, make_custom, target_from_tmax  # noqa: E402
 
-PEAK_LANE_OPS = 256 * 64 * 2.4e9        # int32 VALU lane-ops/s of MI355X
-OPS_PER_CANDIDATE = 2                   # budget compare + objective min
-# Kernel times are read from HIP events on the first and every TIME_EVERY-th timed step: an
-# event-stamped dispatch costs the GPU a few microseconds of idle time, which would otherwise
-# be part of every step of a small search.
-TIME_EVERY = 8
+MI355X_CUS, MI355X_CLOCK_HZ = 256, 2.4e9    # published figures, used if rocminfo cannot be read
+OPS_PER_CANDIDATE = 2                   # budget compare + objective min: the work issued
+FRAC_BASIS = "issued VALU lane-ops (2 per candidate: budget compare, objective minimum)"
+# Kernel times come from a separate pass after the timed region, every step event-stamped (an
+# event-stamped dispatch costs the GPU a few microseconds of idle time, which must not be part
+# of the timed steps of a small search); the figure reported is the median.
+TIMING_SAMPLES = 9
 # The wider count of lane-ops per candidate (add the last term, compare the budget, compare the
 # best, select value and index), reported beside ``frac`` for comparison with that accounting.
 OPS_PER_CANDIDATE_WIDE = 5
-WORKLOADS = {"cfg2": 2, "cfg3": 3, "cfg4": 4, "cfg1": 1, "multi": 2, "pruned": 4,
+SQ_COUNTER_FILE = os.path.join(ROOT, "profiles", "scan_min_sq_counters.md")
+# Exhaustive workloads measured besides the headline one in the default run.
+OTHER_WORKLOADS = ("cfg2", "cfg4", "cfg1", "cfg0")
+WORKLOADS = {"cfg0": 0, "cfg2": 2, "cfg3": 3, "cfg4": 4, "cfg1": 1, "multi": 2, "pruned": 4,
              "pruned-paper": None, "stats": None, "place": 4}
 HBM_PEAK = 8.0e12                       # MI355X HBM3E bytes/s
 STATS_TRACES = 20_000                   # beam-search requests of the statistics workload
@@ -76,19 +90,54 @@ STATS_SOURCES = ("alp_stats.hip", "alp_device.h", "alp_internal.h")
 METRIC = "ALP candidate allocations evaluated/sec on 1 GPU"
 
 
-def _traffic(kernel_digest: str, workload: str, path: str = TRAFFIC_FILE):
-    """HBM bytes per launch (per call for the statistics) from a committed rocprofv3 counter
-    summary, if it was taken on the current kernel source and this workload."""
+def _counter_entry(kernel_digest: str, workload: str, path: str):
+    """A workload's entry of the machine-readable block of a committed rocprofv3 counter
+    summary, if the counters were taken on the current kernel source."""
     try:
         with open(path) as f:
             text = f.read()
         t = json.loads(text.split("```json", 1)[1].split("```", 1)[0])
     except (OSError, ValueError, IndexError):
         return None
-    entry = t.get(workload)
-    if not entry or t.get("kernel_source_sha256") != kernel_digest:
+    if t.get("kernel_source_sha256") != kernel_digest:
         return None
-    return entry.get("bytes_per_launch")
+    return t.get(workload)
+
+
+def _traffic(kernel_digest: str, workload: str, path: str = TRAFFIC_FILE):
+    """HBM bytes per launch (per call for the statistics) from the counter summary."""
+    entry = _counter_entry(kernel_digest, workload, path)
+    return entry.get("bytes_per_launch") if entry else None
+
+
+def _lane_ops_per_candidate(kernel_digest: str, workload: str):
+    """VALU lane-ops the scan issued per candidate (SQ_INSTS_VALU x 64 / candidates) from the
+    instruction-counter summary."""
+    entry = _counter_entry(kernel_digest, workload, SQ_COUNTER_FILE)
+    return entry.get("valu_lane_ops_per_candidate") if entry else None
+
+
+def chip_peak():
+    """(CUs, maximum engine clock in Hz, source) of the gfx950 agent, read from rocminfo;
+    the published MI355X figures if it cannot be read.  Runs rocminfo as a child process."""
+    import subprocess
+    try:
+        out = subprocess.run(["rocminfo"], capture_output=True, text=True, timeout=120).stdout
+    except (OSError, subprocess.SubprocessError):
+        out = ""
+    for agent in out.split("Agent ")[1:]:
+        if "gfx950" not in agent:
+            continue
+        cus = clock = None
+        for line in agent.splitlines():
+            key, _, val = line.strip().partition(":")
+            if key.strip() == "Compute Unit" and cus is None:
+                cus = int(val.split()[0])
+            elif key.strip() == "Max Clock Freq. (MHz)" and clock is None:
+                clock = float(val.split()[0]) * 1e6
+        if cus and clock:
+            return cus, clock, "rocminfo"
+    return MI355X_CUS, MI355X_CLOCK_HZ, "published MI355X figures (rocminfo not readable)"
 
 
 def _kernel_digest(sources=KERNEL_SOURCES) -> str:
@@ -115,21 +164,115 @@ def host_cpu() -> str:
     return f"{model}, {os.cpu_count()} logical CPUs"
 
 
-def cpu_baseline(batch, G, lam, seconds: float):
-    """Single-threaded oracle argmin over the first indices of instance 0, sized to ~seconds."""
+def host_cores() -> int:
+    """Cores the job may use: the CPU affinity set, at most 16 (one GPU's share of its host)."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def _oracle_slice(task):
+    """Worker: the oracle's argmin over [lo, hi) of one workload instance (wall seconds, x, L)."""
+    cfg_id, inst, G, lam, lo, hi = task
     import oracle
-    inst = oracle.Instance(batch, 0)
+    b = make_batch(cfg_id, [inst])
+    t0 = time.perf_counter()
+    r = oracle.argmin(oracle.Instance(b, 0), G, lam, lo, hi)
+    return time.perf_counter() - t0, r["x"], r["L"]
+
+
+def _oracle_query(cfg_id: int):
+    """Instance 0 of a workload with its target rate, from the oracle alone (T_max by the
+    threshold method)."""
+    import oracle
+    b = make_batch(cfg_id, [0])
+    inst = oracle.Instance(b, 0)
+    G = int(b["G"][0])
+    lam = target_from_tmax(int(b["u_ppm"][0]), oracle.tmax(inst, G))
+    return b, inst, G, lam
+
+
+def _parallel_slices(cfg_id, G, lam, bounds, cores):
+    from concurrent.futures import ProcessPoolExecutor
+    from multiprocessing import get_context
+    tasks = [(cfg_id, 0, G, lam, lo, hi) for lo, hi in bounds]
+    t0 = time.perf_counter()
+    with ProcessPoolExecutor(cores, mp_context=get_context("spawn")) as ex:
+        res = list(ex.map(_oracle_slice, tasks))
+    return time.perf_counter() - t0, res
+
+
+def cpu_baseline(cfg_id: int, seconds: float):
+    """The oracle's exhaustive argmin over a bounded slice of instance 0, split into equal
+    contiguous slices over every host core of the job (worker processes, started before the
+    benchmark touches the GPU); about `seconds` of wall time."""
+    import oracle
+    _, inst, G, lam = _oracle_query(cfg_id)
     n = 1 << 20
     t0 = time.perf_counter()
     oracle.argmin(inst, G, lam, 0, n)
-    dt = time.perf_counter() - t0
-    total = min(inst.N, max(n, int(n * seconds / max(dt, 1e-6))))
+    rate1 = n / max(time.perf_counter() - t0, 1e-6)
+    cores = host_cores()
+    per = max(n, int(rate1 * seconds))
+    total = min(inst.N, per * cores)
+    per = -(-total // cores)
+    bounds = [(k * per, min(total, (k + 1) * per)) for k in range(cores) if k * per < total]
+    wall, _ = _parallel_slices(cfg_id, G, lam, bounds, len(bounds))
+    return {"value": total / wall, "unit": "candidates/s", "cores": len(bounds), "kind": "oracle",
+            "host": host_cpu(), "single_core_value": rate1,
+            "sample": f"first {total:,} candidate indices of the same instance in {len(bounds)} "
+                      f"contiguous slices, one per worker process, exhaustive C oracle "
+                      f"({wall:.1f} s wall including process start)"}
+
+
+def _oracle_instances(task):
+    """Worker: the oracle's full argmin of instances [a, b) of a workload (wall s, [x, ...])."""
+    cfg_id, a, b, lam = task
+    import oracle
+    batch = make_batch(cfg_id, range(a, b))
     t0 = time.perf_counter()
-    oracle.argmin(inst, G, lam, 0, total)
-    dt = time.perf_counter() - t0
-    return {"value": total / dt, "unit": "candidates/s", "cores": 1, "kind": "oracle", "host": host_cpu(),
-            "sample": f"first {total:,} candidate indices of the same instance, exhaustive "
-                      f"single-threaded C oracle ({dt:.1f} s)"}
+    xs = [oracle.argmin(oracle.Instance(batch, i), int(batch["G"][i]), int(lam[i]))["x"]
+          for i in range(b - a)]
+    return time.perf_counter() - t0, xs
+
+
+def oracle_full(cfg_id: int):
+    """The oracle's full argmin of the workload across the host cores, in worker processes:
+    a single instance in 8 contiguous index slices per core (slice winners merge on (L, x)), a
+    batch as per-instance jobs.  Wall time including process start."""
+    import oracle
+    from concurrent.futures import ProcessPoolExecutor
+    from multiprocessing import get_context
+    cores = host_cores()
+    cfg = CONFIGS[cfg_id]
+    if cfg_id == 4:
+        batch = make_batch(cfg_id, range(cfg.num_instances))
+        lam = [target_from_tmax(int(batch["u_ppm"][i]),
+                                oracle.tmax(oracle.Instance(batch, i), int(batch["G"][i])))
+               for i in range(cfg.num_instances)]
+        step = 64
+        tasks = [(cfg_id, a, min(a + step, cfg.num_instances), lam[a:a + step])
+                 for a in range(0, cfg.num_instances, step)]
+        t0 = time.perf_counter()
+        with ProcessPoolExecutor(cores, mp_context=get_context("spawn")) as ex:
+            res = list(ex.map(_oracle_instances, tasks))
+        wall = time.perf_counter() - t0
+        xs = [x for _, part in res for x in part]
+        total = cfg.num_instances * oracle.Instance(batch, 0).N
+        return {"candidates": total, "cores": cores, "wall_s": wall, "value": total / wall,
+                "unit": "candidates/s", "jobs": f"{len(tasks)} jobs of {step} instances",
+                "host": host_cpu(), "_indices": xs}
+    _, inst, G, lam = _oracle_query(cfg_id)
+    parts = 8 * cores
+    per = -(-inst.N // parts)
+    bounds = [(k * per, min(inst.N, (k + 1) * per)) for k in range(parts) if k * per < inst.N]
+    wall, res = _parallel_slices(cfg_id, G, lam, bounds, cores)
+    best = min(((L, x) for _, x, L in res if x is not None), default=(None, None))
+    return {"candidates": inst.N, "cores": cores, "wall_s": wall, "value": inst.N / wall,
+            "unit": "candidates/s", "jobs": f"{len(bounds)} index slices", "x": best[1],
+            "L": best[0], "host": host_cpu()}
 
 
 def cpu_baseline_pruned(batch, G, lam, seconds: float):
@@ -145,26 +288,29 @@ def cpu_baseline_pruned(batch, G, lam, seconds: float):
                       f"vectors), single-threaded C oracle ({dt:.1f} s)"}
 
 
-def timed_steps(step, ctx, steps: int, warmup: int):
-    """Runs warmup + steps calls; returns (elapsed s, mean kernel ms [3] over the timed calls,
-    the last timed call's kernel_times(), last output).  The library times the first and every
-    TIME_EVERY-th step of the timed region with HIP events stamped on the kernel dispatches and
-    sums the times itself, so the timed loop holds nothing but the calls."""
+def timed_steps(step, ctx, steps: int, warmup: int, samples: int = TIMING_SAMPLES):
+    """Runs warmup + steps calls with no timing inside the timed region, then `samples` more
+    calls each timed with HIP events stamped on the kernel dispatches.  Returns (elapsed s of
+    the timed region, median kernel ms [3] over the samples, the last sample's kernel_times(),
+    the last timed-region output)."""
     import torch
     for _ in range(warmup):
         step()
-    ctx.set_timing(TIME_EVERY)
+    ctx.set_timing(False)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(steps):
         out = step()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    totals, timed = ctx.kernel_time_totals()
-    avg = totals / max(1, timed)
-    last = ctx.kernel_times()
+    ctx.set_timing(1)
+    per_call = []
+    for _ in range(samples):
+        step()
+        per_call.append(ctx.kernel_times())
     ctx.set_timing(False)
-    return elapsed, avg, last, out
+    med = np.median(np.asarray([t[:3] for t in per_call], dtype=np.float64), axis=0)
+    return elapsed, med, per_call[-1], out
 
 
 def gap_stats(pruned, exhaustive) -> dict:
@@ -212,11 +358,28 @@ def main():
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after timing, run one plain device copy of this size (for scaling "
                          "hardware byte counters)")
+    ap.add_argument("--only", action="store_true",
+                    help="measure the named workload alone (no other workloads in the line)")
+    ap.add_argument("--no-oracle-full", action="store_true",
+                    help="skip the oracle's full argmin across host cores (5-LLM search and "
+                         "4,096-search batch)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the search runs on a single MI355X; "
               "multi-GPU sharding is not built (run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
+
+    # Before anything touches the GPU: the chip's peak from rocminfo and the oracle legs of the
+    # exhaustive workloads, which run in worker processes.
+    peak_info = chip_peak()
+    exhaustive = not (args.workload.startswith("pruned") or args.workload in ("stats", "place"))
+    cpu, full = None, {}
+    if exhaustive:
+        if not args.no_cpu_baseline:
+            cpu = cpu_baseline(WORKLOADS[args.workload], args.cpu_seconds)
+        if not args.no_oracle_full and args.workload == "cfg3":
+            for name in ("cfg3", "cfg4") if not args.only else ("cfg3",):
+                full[name] = oracle_full(WORKLOADS[name])
 
     import torch
     from paper_2604_15186_amd import alp
@@ -224,14 +387,15 @@ def main():
     if not torch.cuda.is_available():
         print("no GPU visible", file=sys.stderr)
         sys.exit(1)
+    peak = peak_info[0] * 64 * peak_info[1]
     if args.workload.startswith("pruned"):
-        line = run_pruned(args, alp)
+        line = run_pruned(args, alp, peak)
     elif args.workload == "stats":
         line = run_stats(args, alp)
     elif args.workload == "place":
-        line = run_place(args, alp)
+        line = run_place(args, alp, peak)
     else:
-        line = run_exhaustive(args, alp)
+        line = run_exhaustive(args, alp, peak_info, cpu, full)
     if args.calib_copy_mib:
         src = torch.ones(args.calib_copy_mib << 20, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
@@ -250,17 +414,18 @@ def _line(args, value, unit, elapsed, dtype_cfg, roofline, cpu):
             "roofline": roofline, "cpu_baseline": cpu}
 
 
-def run_exhaustive(args, alp):
-    cfg_id = WORKLOADS[args.workload]
+def measure_exhaustive(alp, cfg_id: int, steps: int, warmup: int, variant: int, peak: float,
+                       multi: bool = False) -> dict:
+    """One exhaustive workload: the timed HBM-resident steps, the kernel medians, the roofline
+    fraction and the host-buffer call latency."""
     cfg = CONFIGS[cfg_id]
-    multi = args.workload == "multi"
     if multi:
         insts = list(range(MULTI_WORKFLOWS))
     else:
         insts = list(range(cfg.num_instances)) if cfg_id == 4 else [0]
     batch = make_batch(cfg_id, insts)
     ctx = alp.Context(batch)
-    ctx.set_launch(args.variant)
+    ctx.set_launch(variant)
     G = batch["G"]
     if multi:
         G = np.full(len(insts), MULTI_GPUS // MULTI_WORKFLOWS, dtype=np.uint32)
@@ -268,13 +433,13 @@ def run_exhaustive(args, alp):
     lam = np.asarray([target_from_tmax(int(batch["u_ppm"][i]), int(tmax[i]))
                       for i in range(len(insts))], dtype=np.uint32)
     per_step = ctx.num_candidates * len(insts) * ((MULTI_GPUS + 1) if multi else 1)
-    sync_api = None
+    sync_api, argmin = None, None
     if multi:
         def step():
             plan = ctx.allocate_workflows(lam, MULTI_GPUS, alp.WELFARE_EGALITARIAN)[0]
             return int(plan["status"])
 
-        elapsed, avg, last, status = timed_steps(step, ctx, args.steps, args.warmup)
+        elapsed, med, last, status = timed_steps(step, ctx, steps, warmup)
         assert status in (0, 5)
     else:
         # Queries and results resident in HBM: the searches are queued on the stream back to back
@@ -288,54 +453,109 @@ def run_exhaustive(args, alp):
         def step():
             ctx.search_batch_async(Gd, Ld, out)
 
-        elapsed, avg, last, _ = timed_steps(step, ctx, args.steps, args.warmup)
+        elapsed, med, last, _ = timed_steps(step, ctx, steps, warmup)
         got = alp.results_from_device(out, len(insts))
         ref = ctx.search_batch(G, lam)                  # host-buffer path, outside the timing
         assert got.tobytes() == ref.tobytes() and set(got["status"]) <= {0, 5}
         # The same searches through the host-buffer entry points (query scalars or arrays from
         # host memory, result records to mapped host memory, one synchronisation per call).
-        n_sync = max(5, args.steps // 2)
-        t0 = time.perf_counter()
+        n_sync = max(9, steps // 2)
+        times = []
         for _ in range(n_sync):
+            t0 = time.perf_counter()
             if len(insts) == 1:
                 ctx.search(0, int(G[0]), int(lam[0]))
             else:
                 ctx.search_batch(G, lam)
-        dt = (time.perf_counter() - t0) / n_sync
-        sync_api = {"ms_per_call": dt * 1e3, "value": per_step / dt,
+            times.append(time.perf_counter() - t0)
+        dt = float(np.median(times))
+        if len(insts) == 1:
+            argmin = {"index": int(got[0]["index"]), "latency_us": int(got[0]["latency_us"])}
+        sync_api = {"ms_per_call": dt * 1e3, "value": per_step / dt, "calls": n_sync,
+                    "statistic": "median",
                     "entry_point": "alp_search" if len(insts) == 1 else "alp_search_batch"}
-    terms_ms, split_ms, blocks = float(avg[0]), float(avg[2]), last[3]
-    value = per_step * args.steps / elapsed
-    avg_scan_s = float(avg[1]) / 1e3
-    achieved = per_step * OPS_PER_CANDIDATE / avg_scan_s
-    config = {"workload": (f"{MULTI_WORKFLOWS} workflows of {cfg.num_llms} LLMs share "
-                           f"{MULTI_GPUS} GPUs (egalitarian welfare): all "
-                           f"{MULTI_WORKFLOWS * (MULTI_GPUS + 1)} per-workflow budget "
-                           "searches, then the budget split") if multi
-              else f"{cfg.name}: {cfg.description}",
-              "candidates_per_step": per_step, "instances": len(insts),
-              "llms": cfg.num_llms, "gpu_budget": MULTI_GPUS if multi else cfg.gpu_budget,
-              "options_per_llm": len(cfg.tp_values) * len(cfg.frac_q) * cfg.max_replicas,
-              "scan_blocks": blocks,
-              "queries_and_results": "host memory (alp_allocate_workflows)" if multi
-              else "HBM (alp_search_batch_async)"}
-    if sync_api is not None:
-        config["host_buffer_api"] = sync_api
-    roofline = {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_LANE_OPS / 1e12,
-                "unit": "TOP/s", "frac": achieved / PEAK_LANE_OPS,
-                "traffic": _traffic(_kernel_digest(), args.workload),
-                "kernel": "scan", "kernel_ms": avg_scan_s * 1e3,
-                "ops_per_candidate": OPS_PER_CANDIDATE,
-                "frac_at_5_ops": per_step * OPS_PER_CANDIDATE_WIDE / avg_scan_s / PEAK_LANE_OPS,
-                "other_kernels_ms": {"option_terms": terms_ms, "budget_split": split_ms}}
-    cpu = None
-    if not args.no_cpu_baseline:
-        cpu = cpu_baseline(batch, int(G[0]), int(lam[0]), args.cpu_seconds)
+    scan_s = float(med[1]) / 1e3
     ctx.close()
-    return _line(args, value, "candidates/s", elapsed, config, roofline, cpu)
+    r = {"workload": (f"{MULTI_WORKFLOWS} workflows of {cfg.num_llms} LLMs share "
+                      f"{MULTI_GPUS} GPUs (egalitarian welfare): all "
+                      f"{MULTI_WORKFLOWS * (MULTI_GPUS + 1)} per-workflow budget "
+                      "searches, then the budget split") if multi
+         else f"{cfg.name}: {cfg.description}",
+         "candidates_per_step": per_step, "instances": len(insts), "llms": cfg.num_llms,
+         "gpu_budget": MULTI_GPUS if multi else cfg.gpu_budget,
+         "options_per_llm": len(cfg.tp_values) * len(cfg.frac_q) * cfg.max_replicas,
+         "scan_blocks": last[3], "ms_per_step": elapsed / steps * 1e3,
+         "value": per_step * steps / elapsed,
+         "scan_kernel_ms": scan_s * 1e3, "option_terms_ms": float(med[0]),
+         "budget_split_ms": float(med[2]), "kernel_samples": TIMING_SAMPLES,
+         "frac": per_step * OPS_PER_CANDIDATE / scan_s / peak,
+         "queries_and_results": "host memory (alp_allocate_workflows)" if multi
+         else "HBM (alp_search_batch_async)"}
+    if sync_api is not None:
+        r["host_buffer_api"] = sync_api
+    if argmin is not None:
+        r["argmin"] = argmin
+    if not multi and len(insts) > 1:
+        r["_indices"] = got["index"].copy()
+    return r
 
 
-def run_pruned(args, alp):
+def run_exhaustive(args, alp, peak_info, cpu, full):
+    cus, clock, source = peak_info
+    peak = cus * 64 * clock
+    multi = args.workload == "multi"
+    cfg_id = WORKLOADS[args.workload]
+    m = measure_exhaustive(alp, cfg_id, args.steps, args.warmup, args.variant, peak, multi)
+    digest = _kernel_digest()
+    config = {k: m[k] for k in ("workload", "candidates_per_step", "instances", "llms",
+                                "gpu_budget", "options_per_llm", "scan_blocks",
+                                "queries_and_results") if k in m}
+    if "argmin" in m:
+        config["argmin"] = m["argmin"]
+    if "host_buffer_api" in m:
+        config["host_buffer_api"] = m["host_buffer_api"]
+    if not args.only and not multi and args.workload == "cfg3":
+        others = {}
+        for name in OTHER_WORKLOADS:
+            o = measure_exhaustive(alp, WORKLOADS[name], args.steps, args.warmup, args.variant,
+                                   peak)
+            o["valu_lane_ops_per_candidate"] = _lane_ops_per_candidate(digest, name)
+            others[name] = o
+        config["other_workloads"] = others
+    if full:
+        # The oracle's full argmins, against the GPU results of the same searches.
+        out = {}
+        for name, f in full.items():
+            f = dict(f)
+            if name == args.workload:
+                f["matches_gpu"] = f["x"] == m.get("argmin", {}).get("index")
+            else:
+                xs = f.pop("_indices")
+                gpu = config.get("other_workloads", {}).get(name, {}).pop("_indices", None)
+                f["matches_gpu"] = gpu is not None and [int(v) for v in gpu] == [
+                    int(v) if v is not None else (1 << 64) - 1 for v in xs]
+            out[name] = f
+        config["oracle_full_argmin"] = out
+    for o in config.get("other_workloads", {}).values():
+        o.pop("_indices", None)
+    scan_s = m["scan_kernel_ms"] / 1e3
+    achieved = m["candidates_per_step"] * OPS_PER_CANDIDATE / scan_s
+    roofline = {"bound": "alu", "achieved": achieved / 1e12, "peak": peak / 1e12,
+                "unit": "TOP/s", "frac": achieved / peak,
+                "traffic": _traffic(digest, args.workload),
+                "kernel": "scan", "kernel_ms": m["scan_kernel_ms"],
+                "kernel_ms_statistic": f"median of {TIMING_SAMPLES} event-stamped steps",
+                "frac_basis": FRAC_BASIS, "ops_per_candidate": OPS_PER_CANDIDATE,
+                "valu_lane_ops_per_candidate": _lane_ops_per_candidate(digest, args.workload),
+                "peak_source": f"{cus} CUs x 64 lanes x {clock / 1e9:.2f} GHz ({source})",
+                "frac_at_5_ops": m["candidates_per_step"] * OPS_PER_CANDIDATE_WIDE / scan_s / peak,
+                "other_kernels_ms": {"option_terms": m["option_terms_ms"],
+                                     "budget_split": m["budget_split_ms"]}}
+    return _line(args, m["value"], "candidates/s", m["ms_per_step"] / 1e3 * args.steps, config,
+                 roofline, cpu)
+
+
+def run_pruned(args, alp, peak: float):
     if args.workload == "pruned":
         cfg = CONFIGS[args.config]
         batch = make_batch(args.config, range(cfg.num_instances))
@@ -372,8 +592,8 @@ def run_pruned(args, alp):
               "unpruned_vectors_per_query": int(first["unpruned"][0]),
               "gap_vs_exhaustive": None if exhaustive is None else gap_stats(out, exhaustive),
               "enumeration_blocks": last[3]}
-    roofline = {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_LANE_OPS / 1e12,
-                "unit": "TOP/s", "frac": achieved / PEAK_LANE_OPS, "traffic": None,
+    roofline = {"bound": "alu", "achieved": achieved / 1e12, "peak": peak / 1e12,
+                "unit": "TOP/s", "frac": achieved / peak, "traffic": None,
                 "kernel": "fraction enumeration", "kernel_ms": avg_enum_s * 1e3,
                 "ops_per_vector": ops_per_vector,
                 "other_kernels_ms": {"option_terms": float(avg[0]), "option_table": avg_table_ms}}
@@ -405,7 +625,7 @@ def cpu_baseline_place(batch, res, G, seconds: float):
                       f"({dt:.2f} s, including the Python call per allocation)"}
 
 
-def run_place(args, alp):
+def run_place(args, alp, peak: float):
     cfg = CONFIGS[args.config]
     batch = make_batch(args.config, range(cfg.num_instances))
     ctx = alp.Context(batch)
@@ -434,8 +654,8 @@ def run_place(args, alp):
               "pruned_feasible": int((pruned["status"] == 0).sum()),
               "mean_gpus_used": float(out["gpus_used"][out["status"] == 0].mean())
               if (out["status"] == 0).any() else 0.0}
-    roofline = {"bound": "alu", "achieved": ops / k_s / 1e12, "peak": PEAK_LANE_OPS / 1e12,
-                "unit": "TOP/s", "frac": ops / k_s / PEAK_LANE_OPS, "traffic": None,
+    roofline = {"bound": "alu", "achieved": ops / k_s / 1e12, "peak": peak / 1e12,
+                "unit": "TOP/s", "frac": ops / k_s / peak, "traffic": None,
                 "kernel": "place", "kernel_ms": k_s * 1e3,
                 "ops": "one pass over the budget's GPUs per replica"}
     cpu = None if args.no_cpu_baseline else cpu_baseline_place(batch, res, G, args.cpu_seconds)

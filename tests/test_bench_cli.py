@@ -45,3 +45,18 @@ def test_json_line(workload):
     assert 0 < roof["frac"] == pytest.approx(roof["achieved"] / roof["peak"])
     cpu = out["cpu_baseline"]
     assert cpu["kind"] == "oracle" and cpu["value"] > 0 and cpu["cores"] >= 1 and cpu["sample"]
+    if workload == "cfg2":
+        assert roof["frac_basis"].startswith("issued VALU lane-ops")
+        assert "median" in roof["kernel_ms_statistic"] and roof["kernel_ms"] > 0
+
+
+@pytest.mark.gpu
+def test_default_line_carries_the_other_workloads():
+    out = _run("--workload", "cfg3", "--cpu-seconds", "1", "--no-oracle-full")
+    others = out["config"]["other_workloads"]
+    assert set(others) == {"cfg0", "cfg1", "cfg2", "cfg4"}
+    for name, o in others.items():
+        assert o["scan_kernel_ms"] > 0 and 0 < o["frac"] < 1.5, name
+        assert o["host_buffer_api"]["ms_per_call"] > 0
+        assert o["ms_per_step"] > 0
+    assert out["config"]["argmin"]["index"] >= 0
