@@ -31,6 +31,11 @@
  * Out-parameters are written only on ALP_OK (and ALP_INFEASIBLE where stated).  A failed call
  * leaves the context usable and unchanged.  A context is not thread-safe; distinct contexts are
  * independent.  alp_last_error() describes the last failure of the calling thread.
+ *
+ * Test hook: while the environment variable ALP_TEST_FAIL_ALLOC is set (to anything but "0"),
+ * every device and pinned host allocation the library attempts fails, and the call returns
+ * ALP_ENOMEM; buffers a context already holds are kept, so later calls that need no larger ones
+ * still succeed.
  */
 #ifndef ALP_H
 #define ALP_H

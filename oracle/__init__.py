@@ -17,18 +17,21 @@ import subprocess
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "liborc.so")
+SOURCE = os.path.join(_HERE, "alp_oracle.c")
+BUILT_PATH = os.path.join(_HERE, "liborc.so")
+# ALP_ORACLE_LIB names another build of the same source to load instead (the test suite uses it
+# for sanitizer builds and for planted-mistake copies of the oracle).
+LIB_PATH = os.environ.get("ALP_ORACLE_LIB", BUILT_PATH)
 U64_NONE = (1 << 64) - 1
 
 
 def build() -> str:
     """Compile ``liborc.so`` with gcc (always rebuilds)."""
-    src = os.path.join(_HERE, "alp_oracle.c")
-    tmp = LIB_PATH + ".tmp"
-    subprocess.run(["gcc", "-std=c11", "-O2", "-Wall", "-Wextra", "-shared", "-fPIC", src, "-o", tmp],
-                   check=True)
-    os.replace(tmp, LIB_PATH)
-    return LIB_PATH
+    tmp = BUILT_PATH + ".tmp"
+    subprocess.run(["gcc", "-std=c11", "-O2", "-Wall", "-Wextra", "-shared", "-fPIC", SOURCE, "-o",
+                    tmp], check=True)
+    os.replace(tmp, BUILT_PATH)
+    return BUILT_PATH
 
 
 class _Inst(C.Structure):
@@ -72,7 +75,7 @@ _lib = None
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB_PATH):
+        if not os.path.exists(LIB_PATH) and LIB_PATH == BUILT_PATH:
             build()
         L = C.CDLL(LIB_PATH)
         P = C.POINTER

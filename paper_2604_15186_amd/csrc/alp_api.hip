@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <stdarg.h>
+#include <stdlib.h>
 #include <stdint.h>
 #include <stdio.h>
 #include <string.h>
@@ -38,7 +39,33 @@ int32_t hip_fail(hipError_t e, const char *what)
     return fail(ALP_EDEVICE, "%s: %s", what, hipGetErrorString(e));
 }
 
-// Device buffer that only grows.
+// Test hook: while the environment variable ALP_TEST_FAIL_ALLOC is set to a value other than
+// "0", every device and pinned host allocation of the library fails as if memory were exhausted,
+// so that tests reach the ALP_ENOMEM paths.
+bool forced_alloc_failure()
+{
+    const char *v = getenv("ALP_TEST_FAIL_ALLOC");
+    return v && v[0] && !(v[0] == '0' && v[1] == 0);
+}
+
+hipError_t alloc_device(void **ptr, size_t bytes)
+{
+    *ptr = nullptr;
+    if (forced_alloc_failure())
+        return hipErrorOutOfMemory;
+    return hipMalloc(ptr, bytes);
+}
+
+hipError_t alloc_pinned(void **ptr, size_t bytes, unsigned flags)
+{
+    *ptr = nullptr;
+    if (forced_alloc_failure())
+        return hipErrorOutOfMemory;
+    return hipHostMalloc(ptr, bytes, flags);
+}
+
+// Device buffer that only grows.  The larger buffer is allocated before the old one is
+// released, so a failed growth leaves the buffer as it was.
 struct DevBuf {
     void *ptr = nullptr;
     size_t cap = 0;
@@ -48,25 +75,21 @@ struct DevBuf {
     {
         if (bytes <= cap)
             return hipSuccess;
+        void *grown = nullptr;
+        hipError_t e = alloc_device(&grown, bytes);
+        if (e != hipSuccess)
+            return e;
         if (ptr) {
             // Queued asynchronous searches may still read or write the old buffer.
-            if (guarded) {
-                hipError_t e = hipStreamSynchronize(stream);
-                if (e != hipSuccess)
-                    return e;
-            }
-            hipError_t e = hipFree(ptr);
-            ptr = nullptr;
-            cap = 0;
-            if (e != hipSuccess)
+            if (guarded && (e = hipStreamSynchronize(stream)) != hipSuccess) {
+                (void)hipFree(grown);
                 return e;
+            }
+            (void)hipFree(ptr);
         }
-        hipError_t e = hipMalloc(&ptr, bytes);
-        if (e == hipSuccess)
-            cap = bytes;
-        else
-            ptr = nullptr;
-        return e;
+        ptr = grown;
+        cap = bytes;
+        return hipSuccess;
     }
     void release()
     {
@@ -461,14 +484,13 @@ int32_t ensure_host_query(alp_ctx *c, size_t count)
 {
     if (count <= c->host_query_cap)
         return ALP_OK;
-    if (c->host_query)
-        (void)hipHostFree(c->host_query);
-    c->host_query = nullptr;
-    c->host_query_cap = 0;
-    hipError_t e = hipHostMalloc((void **)&c->host_query, 3 * count * sizeof(uint32_t),
-                                 hipHostMallocDefault);
+    void *grown = nullptr;
+    hipError_t e = alloc_pinned(&grown, 3 * count * sizeof(uint32_t), hipHostMallocDefault);
     if (e != hipSuccess)
         return hip_fail(e, "hipHostMalloc(queries)");
+    if (c->host_query)
+        (void)hipHostFree(c->host_query);
+    c->host_query = (uint32_t *)grown;
     c->host_query_cap = count;
     return ALP_OK;
 }
@@ -502,21 +524,18 @@ int32_t ensure_host_results(alp_ctx *c, size_t count)
 {
     if (count <= c->host_results_cap)
         return ALP_OK;
-    if (c->host_results)
-        (void)hipHostFree(c->host_results);
-    c->host_results = nullptr;
-    c->host_results_dev = nullptr;
-    c->host_results_cap = 0;
-    hipError_t e = hipHostMalloc((void **)&c->host_results, count * sizeof(alp_result_t),
-                                 hipHostMallocMapped);
+    void *grown = nullptr, *grown_dev = nullptr;
+    hipError_t e = alloc_pinned(&grown, count * sizeof(alp_result_t), hipHostMallocMapped);
     if (e != hipSuccess)
         return hip_fail(e, "hipHostMalloc(results)");
-    e = hipHostGetDevicePointer((void **)&c->host_results_dev, c->host_results, 0);
-    if (e != hipSuccess) {
-        (void)hipHostFree(c->host_results);
-        c->host_results = nullptr;
+    if ((e = hipHostGetDevicePointer(&grown_dev, grown, 0)) != hipSuccess) {
+        (void)hipHostFree(grown);
         return hip_fail(e, "hipHostGetDevicePointer(results)");
     }
+    if (c->host_results)
+        (void)hipHostFree(c->host_results);
+    c->host_results = (alp_result_t *)grown;
+    c->host_results_dev = (alp_result_t *)grown_dev;
     c->host_results_cap = count;
     return ALP_OK;
 }
@@ -1036,7 +1055,7 @@ int32_t alp_allocate_workflows(alp_ctx *ctx, uint32_t count, const uint32_t *ins
     begin_call(ctx);
     hipError_t e;
     if (!ctx->host_split) {
-        if ((e = hipHostMalloc((void **)&ctx->host_split, 32 * sizeof(uint32_t), hipHostMallocMapped)) !=
+        if ((e = alloc_pinned((void **)&ctx->host_split, 32 * sizeof(uint32_t), hipHostMallocMapped)) !=
             hipSuccess)
             return hip_fail(e, "hipHostMalloc(split)");
         if ((e = hipHostGetDevicePointer((void **)&ctx->host_split_dev, ctx->host_split, 0)) != hipSuccess) {
@@ -1164,20 +1183,18 @@ int32_t alp_search_pruned(alp_ctx *ctx, uint32_t count, const uint32_t *instance
         (e = ctx->pruned_orders.ensure((uint64_t)count * alp::pruned_order_bytes())) != hipSuccess)
         return hip_fail(e, "hipMalloc(pruned search)");
     if (count > ctx->host_pruned_cap) {
-        if (ctx->host_pruned)
-            (void)hipHostFree(ctx->host_pruned);
-        ctx->host_pruned = nullptr;
-        ctx->host_pruned_dev = nullptr;
-        ctx->host_pruned_cap = 0;
-        if ((e = hipHostMalloc((void **)&ctx->host_pruned, count * sizeof(alp_pruned_t),
-                               hipHostMallocMapped)) != hipSuccess)
+        void *grown = nullptr, *grown_dev = nullptr;
+        if ((e = alloc_pinned(&grown, count * sizeof(alp_pruned_t), hipHostMallocMapped)) !=
+            hipSuccess)
             return hip_fail(e, "hipHostMalloc(pruned results)");
-        if ((e = hipHostGetDevicePointer((void **)&ctx->host_pruned_dev, ctx->host_pruned, 0)) !=
-            hipSuccess) {
-            (void)hipHostFree(ctx->host_pruned);
-            ctx->host_pruned = nullptr;
+        if ((e = hipHostGetDevicePointer(&grown_dev, grown, 0)) != hipSuccess) {
+            (void)hipHostFree(grown);
             return hip_fail(e, "hipHostGetDevicePointer(pruned results)");
         }
+        if (ctx->host_pruned)
+            (void)hipHostFree(ctx->host_pruned);
+        ctx->host_pruned = (alp_pruned_t *)grown;
+        ctx->host_pruned_dev = (alp_pruned_t *)grown_dev;
         ctx->host_pruned_cap = count;
     }
     alp::QueryDev q{};
@@ -1486,8 +1503,8 @@ int32_t alp_stats_create(alp_stats_ctx **out, int32_t device, void *hip_stream)
     DeviceGuard guard(device);
     hipError_t e = guard.status;
     if (e == hipSuccess)
-        e = hipHostMalloc((void **)&c->host_out, ALP_MAX_LLMS * sizeof(alp_stats_t),
-                          hipHostMallocMapped);
+        e = alloc_pinned((void **)&c->host_out, ALP_MAX_LLMS * sizeof(alp_stats_t),
+                         hipHostMallocMapped);
     if (e == hipSuccess)
         e = hipHostGetDevicePointer((void **)&c->host_out_dev, c->host_out, 0);
     for (int k = 0; k < 2 && e == hipSuccess; ++k)
@@ -1520,14 +1537,13 @@ int32_t alp_trace_stats(alp_stats_ctx *c, uint32_t num_llms, uint32_t num_traces
     const size_t n_off = (size_t)num_traces + 1;
     if (c->offsets_cap < n_off) {
         // Pinned, so the copy goes straight to it (no staging through a bounce buffer).
+        void *grown = nullptr;
+        if ((e = alloc_pinned(&grown, n_off * sizeof(uint64_t), hipHostMallocDefault)) !=
+            hipSuccess)
+            return hip_fail(e, "hipHostMalloc(offsets)");
         if (c->offsets)
             (void)hipHostFree(c->offsets);
-        c->offsets = nullptr;
-        c->offsets_cap = 0;
-        if ((e = hipHostMalloc((void **)&c->offsets, n_off * sizeof(uint64_t))) != hipSuccess) {
-            c->offsets = nullptr;
-            return hip_fail(e, "hipHostMalloc(offsets)");
-        }
+        c->offsets = (uint64_t *)grown;
         c->offsets_cap = n_off;
     }
     if ((e = hipMemcpyAsync(c->offsets, offsets, n_off * sizeof(uint64_t),

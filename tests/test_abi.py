@@ -149,6 +149,18 @@ def test_objective_overflow_is_erange():
     assert "32-bit" in alp.last_error()
 
 
+@pytest.mark.skipif(os.path.exists("/dev/kfd"), reason="a GPU driver is present on this machine")
+def test_no_device_is_edevice():
+    """Without a GPU driver no HIP device can be visible: a valid load is EDEVICE, exactly, and
+    so is a statistics context."""
+    st, ctx = _load(BASE, _arrays())
+    assert st == alp.ALP_EDEVICE and not ctx.value
+    assert "device" in alp.last_error()
+    sctx = C.c_void_p()
+    assert alp.lib().alp_stats_create(C.byref(sctx), 0, None) == alp.ALP_EDEVICE
+    assert not sctx.value
+
+
 def test_unfit_options_do_not_count_towards_overflow():
     a = _arrays()
     a["lat"][:] = (1 << 31) - 1
