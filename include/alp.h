@@ -138,8 +138,16 @@ int32_t alp_load_profiles(alp_ctx **out, const alp_space_t *space, uint32_t num_
                           uint64_t hbm_bytes_per_gpu, int32_t device, void *hip_stream);
 
 /* Exhaustive constrained argmin for one instance at GPU budget gpu_budget (whole GPUs) and
- * target workflow rate target_milli.  Synchronous on the context stream.  Returns ALP_OK with
- * the result, or ALP_INFEASIBLE with out->status = ALP_INFEASIBLE.  EINVAL: bad instance. */
+ * target workflow rate target_milli: the search objective of Section 3 (the lowest latency at
+ * which the workflow sustains its target rate), with the latency of every candidate predicted by
+ * Eq. 1 and its throughput by Eq. 2 (Section 4), over every candidate of the space; among equal
+ * latencies the lowest candidate index.  A candidate is feasible iff every LLM's option is
+ * deployable and its weights fit its share (Section 5, step 1), T_w >= target_milli, and
+ * sum tp * q * d <= units_per_gpu * gpu_budget.  Synchronous on the context stream.  Returns
+ * ALP_OK with the result in *out, or ALP_INFEASIBLE with out->status = ALP_INFEASIBLE and
+ * out->index = ALP_NO_INDEX.  EINVAL: ctx or out NULL, or instance >= num_instances (nothing
+ * written).  ERANGE: the space cannot be covered by one launch.  ENOMEM/EDEVICE: allocation or
+ * HIP failure. */
 int32_t alp_search(alp_ctx *ctx, uint32_t instance, uint32_t gpu_budget, uint32_t target_milli,
                    alp_result_t *out);
 
@@ -342,7 +350,13 @@ typedef struct {
 int32_t alp_place(alp_ctx *ctx, uint32_t count, const alp_result_t *allocations,
                   const uint32_t *gpu_budget, alp_placement_t *out);
 
-/* Evaluates count given candidate indices (each < O^M, else EINVAL) of one instance. */
+/* The predictor at listed candidates (the element-wise check of the search): for each index
+ * x of indices[0..count) (host array, each < O^M, else EINVAL and nothing written) of
+ * `instance`, at gpu_budget and target_milli, out[i] (host) gets the flags and values of
+ * alp_eval_t: L_w by Eq. 1 with every LLM at its per-replica load (Section 4, step 5), T_w by
+ * Eq. 2, the share units, and the feasibility conditions the search applies (Section 5, step 1;
+ * the target rate and the budget, Section 3).  Synchronous on the context stream.  count = 0 is
+ * a no-op. */
 int32_t alp_eval_candidates(alp_ctx *ctx, uint32_t instance, uint32_t gpu_budget,
                             uint32_t target_milli, const uint64_t *indices, uint64_t count,
                             alp_eval_t *out);

@@ -26,6 +26,38 @@ def test_header_and_binding_agree():
     assert declared_functions() == sorted(alp.EXPORTS)
 
 
+def _prototype(name: str) -> str:
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    m = re.search(r"([\w\s\*]+?)\b" + name + r"\s*\(([^)]*)\)\s*;", text)
+    assert m, name
+    return " ".join((m.group(1) + " " + name + "(" + m.group(2) + ")").split())
+
+
+def test_documented_boundary_form():
+    """The load call takes the six tables as flat arrays and every status comes back as int32_t
+    (the form the design documents in place of a per-instance struct and an enum return)."""
+    assert _prototype("alp_load_profiles") == (
+        "int32_t alp_load_profiles(alp_ctx **out, const alp_space_t *space, uint32_t "
+        "num_instances, const uint64_t *weight_bytes, const uint32_t *n_milli, const uint32_t "
+        "*p_milli, const uint8_t *allowed, const uint32_t *rate_milli, const uint32_t *lat_us, "
+        "uint64_t hbm_bytes_per_gpu, int32_t device, void *hip_stream)")
+    assert _prototype("alp_search") == (
+        "int32_t alp_search(alp_ctx *ctx, uint32_t instance, uint32_t gpu_budget, uint32_t "
+        "target_milli, alp_result_t *out)")
+    assert _prototype("alp_eval_candidates") == (
+        "int32_t alp_eval_candidates(alp_ctx *ctx, uint32_t instance, uint32_t gpu_budget, "
+        "uint32_t target_milli, const uint64_t *indices, uint64_t count, alp_eval_t *out)")
+    void_or_str = {"alp_free", "alp_stats_free", "alp_status_str", "alp_last_error"}
+    for name in declared_functions():
+        if name not in void_or_str:
+            assert _prototype(name).startswith("int32_t "), name
+    text = open(HEADER).read()
+    for name, cite in (("alp_search", "Eq. 1"), ("alp_search", "Section 3"),
+                       ("alp_eval_candidates", "Eq. 2")):
+        block = text[:text.index("int32_t " + name + "(")]
+        assert cite in block[block.rindex("/*"):], (name, cite)
+
+
 def test_library_exports_every_declared_symbol():
     lib = alp.lib()
     for name in declared_functions():
