@@ -73,6 +73,16 @@ __device__ __forceinline__ uint32_t wave_min_u32(uint32_t v)
     return lane63(v);
 }
 
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v)
+{
+    wave_reduce_steps([&](auto c, auto m) {
+        constexpr int C = decltype(c)::value, RM = decltype(m)::value;
+        const uint32_t o = dpp_mov<C, RM>(v, v);
+        v = o > v ? o : v;
+    });
+    return lane63(v);
+}
+
 __device__ __forceinline__ uint64_t wave_min_u64(uint64_t v)
 {
     uint32_t l = (uint32_t)v, h = (uint32_t)(v >> 32);

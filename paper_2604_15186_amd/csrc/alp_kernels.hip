@@ -853,54 +853,134 @@ eval_kernel(SpaceDev sp, uint32_t capacity, const uint2 *__restrict__ rec,
 
 // ---------------------------------------------------------------------------------------------
 // Largest reachable T_w within the budget, one block per item.  T_w >= t is reachable iff the
-// cheapest options with tau >= t of all LLMs together fit; the maximum is one of the taus.
-__global__ void __launch_bounds__(256)
+// cheapest deployable, fitting options with tau >= t of all LLMs together fit:
+// need(t) = sum_m min{u : ok, tau >= t} <= capacity.  The maximum is one of the options' own
+// taus.  Per LLM, the deployable options are ranked by tau descending (ties by option index)
+// and a running minimum of their units is taken along that order; need(t) for each candidate
+// t then costs one binary search per LLM.  O(M * O * (O + M log O)) work per item, in LDS; one
+// thread per option where the block allows.
+constexpr uint32_t kTmaxStride = 8;     // options per LLM padded to this, for 8-wide LDS reads
+
+__host__ __device__ inline uint32_t tmax_stride(uint32_t O)
+{
+    return (O + kTmaxStride - 1) / kTmaxStride * kTmaxStride;
+}
+
+__global__ void __launch_bounds__(1024)
 tmax_kernel(SpaceDev sp, QueryDev q, const uint2 *__restrict__ ext, uint32_t *__restrict__ out)
 {
-    extern __shared__ uint2 e[];
-    __shared__ uint32_t red[256];
+    extern __shared__ uint4 t_lds4[];
+    constexpr uint16_t kUnusable = 0xFFFFu;   // share units are at most 64 * 16 * 16 = 16384
     const uint32_t item = blockIdx.x;
-    const uint32_t MO = sp.M * sp.O;
+    const uint32_t O = sp.O, MO = sp.M * O, P = tmax_stride(O), MP = sp.M * P;
+    uint32_t *tau = reinterpret_cast<uint32_t *>(t_lds4);   // [M][P] option tau
+    uint32_t *stau = tau + MP;                           // [M][P] deployable taus, descending
+    uint16_t *units = (uint16_t *)(stau + MP);           // [M][P] share units, or kUnusable
+    uint16_t *smin = units + MP;                         // [M][P] running minimum of units
+    __shared__ uint32_t s_count[ALP_MAX_LLMS];
+    __shared__ uint32_t s_best[16];
     const uint2 *E = ext + (uint64_t)item * MO;
-    for (uint32_t a = threadIdx.x; a < MO; a += blockDim.x)
-        e[a] = E[a];
+    if (threadIdx.x < ALP_MAX_LLMS)
+        s_count[threadIdx.x] = 0;
+    for (uint32_t a = threadIdx.x; a < MP; a += blockDim.x) {
+        const uint32_t m = a / P, o = a - m * P;
+        uint2 e = make_uint2(0u, 0u);                    // padding: not deployable
+        if (o < O)
+            e = E[m * O + o];
+        tau[a] = e.x;
+        units[a] = ((e.y >> 16) & 1u) ? (uint16_t)(e.y & 0xFFFFu) : kUnusable;
+    }
+    __syncthreads();
+    // Rank of each deployable option within its LLM, tau descending then index ascending; the
+    // LLM's taus and units are read 8 at a time.
+    for (uint32_t a = threadIdx.x; a < MP; a += blockDim.x) {
+        if (units[a] == kUnusable)
+            continue;
+        const uint32_t m = a / P, o = a - m * P, t = tau[a];
+        const uint4 *T4 = reinterpret_cast<const uint4 *>(tau + m * P);
+        const uint4 *U4 = reinterpret_cast<const uint4 *>(units + m * P);
+        uint32_t rank = 0;
+        for (uint32_t j8 = 0; j8 < P / 8; ++j8) {
+            const uint4 ta = T4[2 * j8], tb = T4[2 * j8 + 1], uu = U4[j8];
+            const uint32_t tv[8] = {ta.x, ta.y, ta.z, ta.w, tb.x, tb.y, tb.z, tb.w};
+            const uint32_t uw[4] = {uu.x, uu.y, uu.z, uu.w};
+#pragma unroll
+            for (uint32_t k = 0; k < 8; ++k) {
+                const uint32_t j = 8 * j8 + k;
+                const bool usable = ((uw[k / 2] >> (16 * (k & 1))) & 0xFFFFu) != kUnusable;
+                rank += usable && (tv[k] > t || (tv[k] == t && j < o));
+            }
+        }
+        stau[m * P + rank] = t;
+        smin[m * P + rank] = units[a];
+        atomicAdd(&s_count[m], 1u);
+    }
+    __syncthreads();
+    // Running minimum along each LLM's order: wave w takes LLMs w, w + waves, ...; lane l holds
+    // a contiguous run of the order, minimum within the run, then a prefix minimum of the runs
+    // across the lanes.
+    const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    for (uint32_t m = wave; m < sp.M; m += nw) {
+        const uint32_t n = s_count[m], per = (n + 63) / 64;
+        uint16_t *S = smin + m * P;
+        const uint32_t lo = lane * per, hi = lo + per < n ? lo + per : n;
+        uint32_t run = 0xFFFFFFFFu;
+        for (uint32_t k = lo; k < hi; ++k)
+            run = S[k] < run ? S[k] : run;
+        uint32_t before = run;                     // inclusive prefix minimum over lanes
+        for (uint32_t d = 1; d < 64; d <<= 1) {
+            const uint32_t o = (uint32_t)__shfl_up((int)before, d);
+            if (lane >= d)
+                before = o < before ? o : before;
+        }
+        uint32_t acc = (uint32_t)__shfl_up((int)before, 1);
+        if (lane == 0)
+            acc = 0xFFFFFFFFu;
+        for (uint32_t k = lo; k < hi; ++k) {
+            acc = S[k] < acc ? S[k] : acc;
+            S[k] = (uint16_t)acc;
+        }
+    }
     __syncthreads();
     const uint64_t capacity = (uint64_t)query_value(q.capacity, q.cap1, item);
     uint32_t best = 0;
-    for (uint32_t a = threadIdx.x; a < MO; a += blockDim.x) {
-        if (!((e[a].y >> 16) & 1u))
+    for (uint32_t a = threadIdx.x; a < MP; a += blockDim.x) {
+        if (units[a] == kUnusable)
             continue;
-        const uint32_t t = e[a].x;
+        const uint32_t t = tau[a];
         if (t <= best)
             continue;
         uint64_t need = 0;
         bool reachable = true;
         for (uint32_t m = 0; m < sp.M && reachable; ++m) {
-            uint32_t cheapest = 0xFFFFFFFFu;
-            for (uint32_t o = 0; o < sp.O; ++o) {
-                const uint2 v = e[m * sp.O + o];
-                const uint32_t u = v.y & 0xFFFFu;
-                if (((v.y >> 16) & 1u) && v.x >= t && u < cheapest)
-                    cheapest = u;
+            // options of m with tau >= t: the first c of its descending order
+            uint32_t lo = 0, hi = s_count[m];
+            const uint32_t *S = stau + m * P;
+            while (lo < hi) {
+                const uint32_t mid = (lo + hi) >> 1;
+                if (S[mid] >= t)
+                    lo = mid + 1;
+                else
+                    hi = mid;
             }
-            if (cheapest == 0xFFFFFFFFu)
+            if (lo == 0)
                 reachable = false;
             else
-                need += cheapest;
+                need += smin[m * P + lo - 1];
         }
         if (reachable && need <= capacity)
             best = t;
     }
-    red[threadIdx.x] = best;
+    best = wave_max_u32(best);
+    if (lane == 0)
+        s_best[wave] = best;
     __syncthreads();
-    for (uint32_t s = blockDim.x / 2; s > 0; s >>= 1) {
-        if (threadIdx.x < s)
-            red[threadIdx.x] = red[threadIdx.x] > red[threadIdx.x + s] ? red[threadIdx.x]
-                                                                        : red[threadIdx.x + s];
-        __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t b = 0;
+        for (uint32_t w = 0; w < nw; ++w)
+            b = s_best[w] > b ? s_best[w] : b;
+        out[item] = b;
     }
-    if (threadIdx.x == 0)
-        out[item] = red[0];
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -1040,8 +1120,11 @@ hipError_t launch_tmax(const SpaceDev &sp, const QueryDev &q, uint32_t count, co
 {
     if (count == 0)
         return hipSuccess;
-    const size_t lds = (size_t)sp.M * sp.O * sizeof(uint2);
-    hipLaunchKernelGGL(tmax_kernel, dim3(count), dim3(256), lds, st, sp, q, ext, out);
+    const uint32_t MP = sp.M * tmax_stride(sp.O);
+    const size_t lds = (size_t)MP * (2 * sizeof(uint32_t) + 2 * sizeof(uint16_t));
+    // one thread per option (padded), in whole waves, 64..1024
+    const uint32_t threads = MP >= 1024 ? 1024u : (MP + 63) / 64 * 64;
+    hipLaunchKernelGGL(tmax_kernel, dim3(count), dim3(threads), lds, st, sp, q, ext, out);
     return hipGetLastError();
 }
 
