@@ -361,13 +361,20 @@ int32_t alp_eval_candidates(alp_ctx *ctx, uint32_t instance, uint32_t gpu_budget
                             uint32_t target_milli, const uint64_t *indices, uint64_t count,
                             alp_eval_t *out);
 
+/* Added to variant 0, 1, 4 or 5 of alp_set_launch: the option terms run in their own kernel
+ * before the scan (the two-launch form), also where one launch would do. */
+#define ALP_LAUNCH_SEPARATE_TERMS 16u
+
 /* Launch choices, for tests and tuning.  variant: 0 automatic, 1 row-minimum scan (default),
  * 2 thread-per-candidate scan, 3 exact-tracking lane scan, 4 row-minimum scan with fixed row
  * ranges per wave, 5 row-minimum scan with rows handed out within each block (variant 1 picks
  * between the two; rows can only be split with the second, so variant 4 ignores inner_chunks),
  * 6 row-minimum scan over the pair table (LLMs M-3 and M-2 folded into one inner LLM of O^2
  * options, 3 or more LLMs; variant 0 uses it for 5 or more LLMs while the batch's pair tables
- * stay within 4 MiB).  blocks_per_item and threads_per_block (a multiple of 64, at most 1024):
+ * stay within 4 MiB).  Spaces of fewer than 2^32 candidates searched with the row-minimum scan
+ * without the pair table run in one launch: every block computes its item's option terms itself
+ * (unless ALP_LAUNCH_SEPARATE_TERMS is added).  blocks_per_item and threads_per_block (a multiple
+ * of 64, at most 1024):
  * 0 = automatic.  inner_chunks (variants 1, 5, 6): ranges each row's inner-LLM records are
  * split into, dividing ceil(O / 16) (variant 6: the pair table's ceil(O^2 / 16)); 0 =
  * automatic.  Results do not depend on these choices. */
@@ -382,8 +389,8 @@ int32_t alp_set_launch(alp_ctx *ctx, uint32_t variant, uint32_t blocks_per_item,
  * the calls of a long run leaves the run's throughput nearly unchanged).  Setting resets the
  * count and the sums below; a negative enable is ALP_EINVAL.
  * alp_kernel_times writes, for the last timed search or batch, the milliseconds of the
- * option-term kernel (ms[0]) and of the candidate scan kernel, which includes the final reduction
- * and the result write (ms[1]); ms[2] is the budget-split kernel of alp_allocate_workflows, 0
+ * option-term kernel (ms[0]; 0 when the search ran in one launch) and of the candidate scan
+ * kernel, which includes the final reduction and the result write (ms[1]); ms[2] is the budget-split kernel of alp_allocate_workflows, 0
  * after the other searches.  After alp_search_pruned: ms[1] is the fraction enumeration and ms[2]
  * the admissible-option table.  After alp_place: ms[1] is the placement kernel, the others 0.
  * *scan_blocks receives the scan (or enumeration) grid size of the last search.

@@ -70,6 +70,7 @@ struct DevBuf {
     void *ptr = nullptr;
     size_t cap = 0;
     bool guarded = false;           // work that may still use the buffer is queued on `stream`
+    bool zeroed = false;            // a grown buffer is cleared (on `stream`) before its first use
     hipStream_t stream = nullptr;
     hipError_t ensure(size_t bytes)
     {
@@ -79,6 +80,10 @@ struct DevBuf {
         hipError_t e = alloc_device(&grown, bytes);
         if (e != hipSuccess)
             return e;
+        if (zeroed && (e = hipMemsetAsync(grown, 0, bytes, stream)) != hipSuccess) {
+            (void)hipFree(grown);
+            return e;
+        }
         if (ptr) {
             // Queued asynchronous searches may still read or write the old buffer.
             if (guarded && (e = hipStreamSynchronize(stream)) != hipSuccess) {
@@ -134,6 +139,9 @@ struct alp_ctx {
 
     DevBuf q_inst, rec, ext, inner, done, winners, idx, evals, tmax;   // q_inst: inst | cap | lambda
     DevBuf pair;                            // pair tables of the scan's pair form
+    DevBuf fused_regions;                   // one-launch scan: per-block option records
+    DevBuf fused_words;                     // one-launch scan: per-item best word and counter,
+                                            // 0 between launches
     DevBuf split_dp;                        // allocate_kernel's knapsack table
     DevBuf pruned_table, pruned_orders, pruned_counts;   // pruned search scratch
     DevBuf place_in, place_out;                          // placement records
@@ -157,6 +165,9 @@ struct alp_ctx {
     // Timed asynchronous searches: their events (begin and end of the option terms, then of the
     // scan) wait in `pending` until the times are read; spent ones are reused.
     std::vector<std::array<hipEvent_t, 4>> ev_pending, ev_spare;
+    std::vector<uint8_t> ev_pending_terms;  // per pending entry: its first two events are stamped
+                                            // (a separate option-term kernel ran)
+    bool last_terms = true;                 // the last launch_search ran the option-term kernel
     float last_ms[3] = {0, 0, 0};
     double total_ms[3] = {0, 0, 0};     // sums of last_ms since timing was last set
     void tally(int k) { total_ms[k] += last_ms[k]; }
@@ -330,12 +341,14 @@ uint64_t blocks_per_item_for_rounds(uint64_t count, uint64_t resident, uint64_t 
 // fixed-range form counts a wave's rows in 32 bits, so a wave must get fewer than 2^32 rows
 // (the automatic plan adds blocks until it does; a blocks_per_item override that leaves a wave
 // more is rejected), and a launch holds fewer than 2^31 blocks.
-int32_t plan_scan(alp_ctx *c, uint32_t count, alp::ScanGeometry &out)
+int32_t plan_scan(alp_ctx *c, uint32_t count, alp::ScanGeometry &out, bool allow_fused = true)
 {
     alp::ScanGeometry g{};
     const alp::SpaceDev &sp = c->sp;
-    // Variants 4 and 5 are the row-minimum scan with a fixed choice of work distribution.
-    g.variant = c->variant == 0 || c->variant >= 4 ? 1 : c->variant;
+    // Variants 4 and 5 are the row-minimum scan with a fixed choice of work distribution;
+    // ALP_LAUNCH_SEPARATE_TERMS added to 0, 1, 4 or 5 keeps the option terms in their own kernel.
+    const uint32_t variant = c->variant & ~ALP_LAUNCH_SEPARATE_TERMS;
+    g.variant = variant == 0 || variant >= 4 ? 1 : variant;
     g.slots = slots_for(sp.O);
     const uint64_t cus = c->num_cus > 0 ? (uint64_t)c->num_cus : 256;
     // Pair form (variant 1; forced by variant 6, chosen for 5 or more LLMs while the batch's
@@ -345,7 +358,7 @@ int32_t plan_scan(alp_ctx *c, uint32_t count, alp::ScanGeometry &out)
     // Rows are split into sub-rows of at most 1,024 records, claimed within blocks of 16 waves,
     // 32 waves per CU per round and four rounds of blocks, about 8 sub-rows per wave.
     constexpr uint64_t kPairBytesMax = UINT64_C(4) << 20;
-    if (g.variant == 1 && sp.M >= 3 && (c->variant == 6 || (c->variant == 0 && sp.M >= 5)) &&
+    if (g.variant == 1 && sp.M >= 3 && (variant == 6 || (variant == 0 && sp.M >= 5)) &&
         (uint64_t)count * alp::pair_stride(sp.O) * sizeof(uint2) <= kPairBytesMax) {
         uint64_t rows = 1;
         for (uint32_t m = 3; m < sp.M; ++m)
@@ -415,8 +428,8 @@ int32_t plan_scan(alp_ctx *c, uint32_t count, alp::ScanGeometry &out)
         // sub-row late, so whole sub-rows balance well and keep the per-sub-row work small).
         const bool splittable = g.variant == 1 && sp.M >= 2;
         const uint32_t n16 = alp::inner_stride(sp.O) / 16;      // chunks must divide this
-        bool dyn = g.variant == 1 && c->variant != 4 &&
-                   (c->variant == 5 || c->chunks_override > 1 ||
+        bool dyn = g.variant == 1 && variant != 4 &&
+                   (variant == 5 || c->chunks_override > 1 ||
                     ceil_div(g.rows, bpi * wpb) < 16);
         if (dyn && g.rows * (splittable ? n16 : 1) >= (UINT64_C(1) << 32))
             dyn = false;
@@ -460,6 +473,10 @@ int32_t plan_scan(alp_ctx *c, uint32_t count, alp::ScanGeometry &out)
             return fail(ALP_ERANGE, "batch too large for one launch (%llu blocks)",
                         (unsigned long long)(bpi * std::max<uint64_t>(1, count)));
         g.blocks_per_item = (uint32_t)bpi;
+        // One launch for spaces of fewer than 2^32 candidates (the winner fits one 64-bit word),
+        // unless the option terms are asked to run in their own kernel.
+        g.fused = g.variant == 1 && allow_fused && c->N < (UINT64_C(1) << 32) &&
+                  !(c->variant & ALP_LAUNCH_SEPARATE_TERMS) ? 1u : 0u;
     } else {
         g.threads = c->tpb_override ? c->tpb_override : 256;
         const uint64_t resident =
@@ -546,6 +563,9 @@ struct SearchScratch {
     uint2 *rec = nullptr, *ext = nullptr, *inner = nullptr, *pair = nullptr;
     uint32_t *done = nullptr, *best = nullptr;
     alp::Winner *winners = nullptr;
+    uint2 *regions = nullptr;                  // one-launch form
+    uint32_t *fdone = nullptr, *fgroup = nullptr;
+    unsigned long long *fbest = nullptr;
 };
 
 // Byte sizes of the scratch parts of a launch of `count` items with geometry g.  done[count],
@@ -570,8 +590,23 @@ ScratchSizes scratch_sizes(const alp::SpaceDev &sp, uint32_t count, const alp::S
 // The context's own scratch buffers, grown to the launch's sizes.
 int32_t context_scratch(alp_ctx *c, uint32_t count, const alp::ScanGeometry &g, SearchScratch &s)
 {
-    const ScratchSizes z = scratch_sizes(c->sp, count, g);
     hipError_t e;
+    if (g.fused) {
+        // Per block: its option records; per item: the best word (8 B), then the counters.
+        const uint64_t blocks = (uint64_t)count * g.blocks_per_item;
+        if ((e = c->fused_regions.ensure(blocks * alp::fused_region(c->sp.M, c->sp.O) *
+                                         sizeof(uint2))) != hipSuccess)
+            return hip_fail(e, "hipMalloc(block records)");
+        const uint64_t groups = (g.blocks_per_item + alp::kFusedGroup - 1) / alp::kFusedGroup;
+        if ((e = c->fused_words.ensure((uint64_t)count * (12 + 4 * groups))) != hipSuccess)
+            return hip_fail(e, "hipMalloc(item words)");
+        s.regions = (uint2 *)c->fused_regions.ptr;
+        s.fbest = (unsigned long long *)c->fused_words.ptr;
+        s.fdone = (uint32_t *)(s.fbest + count);
+        s.fgroup = s.fdone + count;
+        return ALP_OK;
+    }
+    const ScratchSizes z = scratch_sizes(c->sp, count, g);
     if ((e = c->rec.ensure(z.rec)) != hipSuccess)
         return hip_fail(e, "hipMalloc(rec)");
     if ((e = c->ext.ensure(z.rec)) != hipSuccess)
@@ -606,6 +641,28 @@ int32_t launch_search_with(alp_ctx *c, const alp::QueryDev &q, uint32_t count, a
     const bool timed = ev != nullptr;
     const alp::SpaceDev &sp = c->sp;
     const uint64_t nwin = (uint64_t)count * g.blocks_per_item;
+    hipError_t e;
+    c->last_terms = !g.fused;
+    if (g.fused) {
+        alp::FinishArgs fa{};
+        fa.sp = sp;
+        fa.out = out;
+        alp::FusedArgs fz{};
+        fz.tb = c->tdev;
+        if (raw)
+            fz.raw = *raw;
+        fz.regions = s.regions;
+        fz.region = alp::fused_region(sp.M, sp.O);
+        fz.done = s.fdone;
+        fz.group_done = s.fgroup;
+        fz.best = s.fbest;
+        if ((e = alp::launch_scan(sp, q, count, nullptr, nullptr, g, nullptr, fa, c->stream,
+                                  timed ? ev[2] : nullptr, timed ? ev[3] : nullptr, &fz)) !=
+            hipSuccess)
+            return hip_fail(e, "scan launch");
+        c->last_blocks = (uint32_t)nwin;
+        return ALP_OK;
+    }
     alp::FinishArgs fa;
     fa.sp = sp;
     fa.ext = s.ext;
@@ -618,7 +675,6 @@ int32_t launch_search_with(alp_ctx *c, const alp::QueryDev &q, uint32_t count, a
     reset.best = s.best;
     reset.winners = s.winners;
     reset.n_winners = nwin;
-    hipError_t e;
     if ((e = alp::launch_option_terms(sp, c->tdev, q, count, s.rec, s.ext, s.inner, reset,
                                       c->stream, raw, timed ? ev[0] : nullptr,
                                       timed ? ev[1] : nullptr)) != hipSuccess)
@@ -664,7 +720,8 @@ int32_t run_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count)
     if ((e = hipStreamSynchronize(c->stream)) != hipSuccess)
         return hip_fail(e, "hipStreamSynchronize");
     if (c->timing) {
-        for (int k = 0; k < 2; ++k) {
+        c->last_ms[0] = 0.0f;                  // no option-term kernel in the one-launch form
+        for (int k = c->last_terms ? 0 : 1; k < 2; ++k) {
             if ((e = hipEventElapsedTime(&c->last_ms[k], c->ev[2 * k], c->ev[2 * k + 1])) !=
                 hipSuccess)
                 return hip_fail(e, "hipEventElapsedTime");
@@ -680,9 +737,12 @@ int32_t run_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count)
 int32_t collect_async_times(alp_ctx *c)
 {
     hipError_t e;
-    for (auto &t : c->ev_pending) {
+    for (size_t i = 0; i < c->ev_pending.size(); ++i) {
+        auto &t = c->ev_pending[i];
+        const bool terms = c->ev_pending_terms[i] != 0;
+        c->last_ms[0] = 0.0f;
         if ((e = hipEventSynchronize(t[3])) != hipSuccess ||
-            (e = hipEventElapsedTime(&c->last_ms[0], t[0], t[1])) != hipSuccess ||
+            (terms && (e = hipEventElapsedTime(&c->last_ms[0], t[0], t[1])) != hipSuccess) ||
             (e = hipEventElapsedTime(&c->last_ms[1], t[2], t[3])) != hipSuccess)
             return hip_fail(e, "reading the times of queued searches");
         c->last_ms[2] = 0.0f;
@@ -691,6 +751,7 @@ int32_t collect_async_times(alp_ctx *c)
         c->ev_spare.push_back(t);
     }
     c->ev_pending.clear();
+    c->ev_pending_terms.clear();
     return ALP_OK;
 }
 
@@ -740,10 +801,12 @@ int32_t alp_load_profiles(alp_ctx **out, const alp_space_t *space, uint32_t num_
         return fail(ALP_ENOMEM, "host allocation failed");
     c->device = device;
     c->stream = (hipStream_t)hip_stream;
-    for (DevBuf *b : {&c->q_inst, &c->rec, &c->ext, &c->inner, &c->done, &c->winners, &c->pair}) {
+    for (DevBuf *b : {&c->q_inst, &c->rec, &c->ext, &c->inner, &c->done, &c->winners, &c->pair,
+                      &c->fused_regions, &c->fused_words}) {
         b->guarded = true;                              // used by alp_search_batch_async
         b->stream = c->stream;
     }
+    c->fused_words.zeroed = true;
     c->space = *space;
     c->N = N;
     c->B = num_instances;
@@ -920,6 +983,8 @@ int32_t alp_search_batch_async(alp_ctx *ctx, uint32_t count, const uint32_t *ins
     if (st != ALP_OK && ev) {                      // nothing (complete) was queued for them
         ctx->ev_spare.push_back(ctx->ev_pending.back());
         ctx->ev_pending.pop_back();
+    } else if (ev) {
+        ctx->ev_pending_terms.push_back(ctx->last_terms ? 1 : 0);
     }
     return st;
 }
@@ -937,8 +1002,11 @@ int32_t alp_search_batch_async_noalloc(alp_ctx *ctx, uint32_t count, const uint3
     if (!ctx->static_scratch)
         return fail(ALP_EDEVICE, "the fixed scratch array of device %d has no address: %s",
                     ctx->device, hipGetErrorString(ctx->static_status));
+    // The one-launch form needs its per-item words to be 0 between launches, which a shared
+    // array carved differently from call to call cannot promise: the option terms run in their
+    // own kernel here, which resets what the scan needs.
     alp::ScanGeometry g;
-    int32_t st = plan_scan(ctx, count, g);
+    int32_t st = plan_scan(ctx, count, g, false);
     if (st != ALP_OK)
         return st;
     // Carve the fixed array: queries (inst | cap | lambda | rejection flags), then the search
@@ -1368,8 +1436,11 @@ int32_t alp_set_launch(alp_ctx *ctx, uint32_t variant, uint32_t blocks_per_item,
 {
     if (!ctx)
         return fail(ALP_EINVAL, "ctx is NULL");
-    if (variant > 6)
-        return fail(ALP_EINVAL, "variant %u not in 0..6", variant);
+    const uint32_t base_variant = variant & ~ALP_LAUNCH_SEPARATE_TERMS;
+    if (base_variant > 6 || ((variant & ALP_LAUNCH_SEPARATE_TERMS) && base_variant != 0 &&
+                             base_variant != 1 && base_variant != 4 && base_variant != 5))
+        return fail(ALP_EINVAL, "variant %u is not one of 0..6, or 0, 1, 4, 5 with "
+                                "ALP_LAUNCH_SEPARATE_TERMS", variant);
     if (threads_per_block && (threads_per_block % 64 || threads_per_block > 1024))
         return fail(ALP_EINVAL, "threads_per_block must be a multiple of 64, at most 1024");
     if (blocks_per_item > (1u << 24))
@@ -1378,7 +1449,7 @@ int32_t alp_set_launch(alp_ctx *ctx, uint32_t variant, uint32_t blocks_per_item,
     // variant 6); the planner uses it only where it divides the table the launch scans.
     const uint32_t n16 = alp::inner_stride(ctx->sp.O) / 16;
     const uint32_t p16 = alp::pair_stride(ctx->sp.O) / 16;
-    const uint32_t d16 = variant == 6 ? p16 : n16;
+    const uint32_t d16 = base_variant == 6 ? p16 : n16;
     if (inner_chunks && (inner_chunks > d16 || d16 % inner_chunks))
         return fail(ALP_EINVAL, "inner_chunks %u does not divide %u", inner_chunks, d16);
     ctx->variant = variant;
@@ -1457,7 +1528,8 @@ void alp_free(alp_ctx *ctx)
     DevBuf *bufs[] = {&ctx->tables, &ctx->q_inst, &ctx->rec, &ctx->ext, &ctx->inner, &ctx->done,
                       &ctx->winners, &ctx->idx, &ctx->evals, &ctx->tmax, &ctx->split_dp,
                       &ctx->pruned_table, &ctx->pruned_orders, &ctx->pruned_counts,
-                      &ctx->place_in, &ctx->place_out, &ctx->pair};
+                      &ctx->place_in, &ctx->place_out, &ctx->pair, &ctx->fused_regions,
+                      &ctx->fused_words};
     for (DevBuf *b : bufs)
         b->release();
     if (ctx->host_results)

@@ -168,36 +168,36 @@ __device__ __forceinline__ void item_winner(uint32_t item, uint32_t blocks_per_i
     wave_min(L, x);
 }
 
-// The result record of winner (L, x) -- decoded per-LLM choices, T_w (Eq. 2: minimum over LLMs)
-// and the share units, from the item's per-option records E -- written as the six 64-bit words
-// of alp_result_t.  Called by all lanes of one wave with the same (L, x): lane m decodes LLM m's
-// digit and loads its record (one memory round trip for all LLMs), the wave combines them, and
-// lane 0 writes.
-__device__ __forceinline__ void write_result(const SpaceDev &sp, const uint2 *E, uint32_t L,
-                                             uint64_t x, uint64_t *dst,
-                                             uint32_t status_if_none = ALP_INFEASIBLE)
+// Option index of LLM `m` in candidate x: floor(x / O^(M-1-m)) mod O (LLM 0 most significant),
+// with 32-bit division whenever x allows it.
+__device__ __forceinline__ uint32_t candidate_digit(const SpaceDev &sp, uint64_t x, uint32_t m)
+{
+    uint64_t scale = 1;
+    for (uint32_t k = m + 1; k < sp.M; ++k)
+        scale *= sp.O;
+    if ((x >> 32) == 0)
+        return (scale >> 32) != 0 ? 0u : (uint32_t)x / (uint32_t)scale % sp.O;
+    return (uint32_t)((x / scale) % sp.O);
+}
+
+// The result record of winner (L, x) written as the six 64-bit words of alp_result_t, by all
+// lanes of one wave with the same (L, x): lane m < M holds LLM m's option o, its normalised
+// throughput T (Eq. 2 term) and share units U; the wave takes T_w as their minimum (Eq. 2) and
+// sums U, and lane 0 writes.
+__device__ __forceinline__ void write_result_lanes(const SpaceDev &sp, uint32_t o, uint32_t T,
+                                                   uint32_t U, uint32_t L, uint64_t x,
+                                                   uint64_t *dst, uint32_t status_if_none)
 {
     const uint32_t lane = threadIdx.x & 63;
-    uint32_t T = 0xFFFFFFFFu, U = 0;
     uint64_t tp = 0, fq = 0, rep = 0;
     if (L != kNoLatency && lane < sp.M) {
-        // o_m = floor(x / O^(M-1-m)) mod O  (candidate index, LLM 0 most significant); 32-bit
-        // division whenever x allows it.
-        uint64_t scale = 1;
-        for (uint32_t k = lane + 1; k < sp.M; ++k)
-            scale *= sp.O;
-        uint32_t o;
-        if ((x >> 32) == 0)
-            o = (scale >> 32) != 0 ? 0u : (uint32_t)x / (uint32_t)scale % sp.O;
-        else
-            o = (uint32_t)((x / scale) % sp.O);
-        const uint2 e = E[(uint64_t)lane * sp.O + o];
-        T = e.x;
-        U = e.y & 0xFFFFu;
         const uint32_t ij = o / sp.D;
         tp = (uint64_t)(sp.tp[ij / sp.n_fq] & 0xFFu) << (8 * lane);
         fq = (uint64_t)(sp.fq[ij % sp.n_fq] & 0xFFu) << (8 * lane);
         rep = (uint64_t)((o % sp.D + 1) & 0xFFu) << (8 * lane);
+    } else {
+        T = 0xFFFFFFFFu;
+        U = 0;
     }
     // Combine the (at most 8) LLM lanes: Eq. 2 minimum, unit sum, disjoint byte fields.
     // DPP steps within each 8-lane half row: lane ^ 1, lane ^ 2, then the half mirror (lane i
@@ -236,6 +236,23 @@ __device__ __forceinline__ void write_result(const SpaceDev &sp, const uint2 *E,
     dst[3] = tp;
     dst[4] = fq;
     dst[5] = rep;
+}
+
+// The result record of winner (L, x), with the per-LLM choices decoded from x and T and U read
+// from the item's per-option records E (lane m loads LLM m's: one memory round trip for all).
+__device__ __forceinline__ void write_result(const SpaceDev &sp, const uint2 *E, uint32_t L,
+                                             uint64_t x, uint64_t *dst,
+                                             uint32_t status_if_none = ALP_INFEASIBLE)
+{
+    const uint32_t lane = threadIdx.x & 63;
+    uint32_t o = 0, T = 0xFFFFFFFFu, U = 0;
+    if (L != kNoLatency && lane < sp.M) {
+        o = candidate_digit(sp, x, lane);
+        const uint2 e = E[(uint64_t)lane * sp.O + o];
+        T = e.x;
+        U = e.y & 0xFFFFu;
+    }
+    write_result_lanes(sp, o, T, U, L, x, dst, status_if_none);
 }
 
 // Result record of one item whose winner is (L, x), by one wave.  E: the item's per-option
@@ -344,6 +361,179 @@ __device__ __forceinline__ void block_finish(uint32_t L, uint64_t x, uint32_t it
     __syncthreads();
     if (threadIdx.x < 64)
         write_item_result(fa, item, Lw, xw, staged ? s_ext : nullptr);
+}
+
+// ALP terms of option o of LLM m of instance `inst` at target rate lambda (Eq. 1 and Eq. 2
+// terms, the memory fit of Section 5 step 1):
+//   ok     the (tp, share) pair is deployable and W * Q <= tp * q * H (weights sharded over tp fit
+//          the share q / Q of one GPU's memory);
+//   tau    floor(1000 d T / n), d replicas of saturation throughput T = rate[K-1], saturated at
+//          2^32 - 1 (Eq. 2);
+//   thr    the per-replica load r = ceil(lambda n / (1000 d)) does not exceed T;
+//   c      floor(ell(r) n / p), ell the profile latency at r: lat[0] up to rate[0], linear between
+//          points, rounded down (Eq. 1; 0 unless thr);
+//   u      tp * q * d share units.
+struct OptionTerm {
+    uint32_t c, u, tau;
+    bool ok, thr;
+};
+
+// floor(x / d) for x < 2^63 and 0 < d < 2^32, exactly: a double-precision quotient (within 2^11
+// of the true one, the dividend rounded to 53 bits), corrected by the exact 64-bit remainder
+// divided in double precision (|remainder| < 2^44, exact in a double), then by one last step
+// for the rounding of that second quotient.  Shorter than the general 64-bit division.
+__device__ __forceinline__ uint64_t udiv_u64_u32(uint64_t x, uint64_t d)
+{
+    if ((x >> 32) == 0)
+        return (uint32_t)x / (uint32_t)d;
+    const double dd = (double)d;
+    uint64_t q = (uint64_t)((double)x / dd);
+    int64_t r = (int64_t)(x - q * d);
+    q += (int64_t)floor((double)r / dd);
+    r = (int64_t)(x - q * d);
+    if (r < 0)
+        --q;
+    else if (r >= (int64_t)d)
+        ++q;
+    return q;
+}
+
+// The terms from the option's inputs: its profile curve (rate and lat, K points each; global or
+// LDS memory), whether the (tp, share) pair is deployable, and the LLM's W, n, p.  Every
+// division has a dividend below 2^63 and a divisor below 2^31 (inputs below 2^31, d <= 16).
+__device__ __forceinline__ OptionTerm option_term_from(const SpaceDev &sp, uint64_t H, uint32_t o,
+                                                       const uint32_t *rate, const uint32_t *lat,
+                                                       bool allowed, uint64_t W, uint64_t n,
+                                                       uint64_t p, uint64_t lambda)
+{
+    const uint32_t d = o % sp.D + 1;
+    const uint32_t ij = o / sp.D;
+    const uint32_t j = ij % sp.n_fq, i = ij / sp.n_fq;
+    const uint64_t tp = sp.tp[i], fq = sp.fq[j];
+    OptionTerm t;
+    t.ok = allowed && W * sp.Q <= tp * fq * H;
+    const uint64_t T = rate[sp.K - 1];
+    const uint64_t tau = udiv_u64_u32(1000ull * d * T, n);
+    t.tau = tau > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)tau;
+    const uint64_t dd = 1000ull * d;
+    const uint64_t r = udiv_u64_u32(lambda * n + dd - 1, dd);
+    t.thr = r <= T;
+    uint64_t c = 0;
+    if (t.thr) {
+        uint64_t ell = lat[0];
+        if (r > rate[0]) {
+            uint32_t k = 1;
+            while (r > rate[k])
+                ++k;
+            const uint64_t r0 = rate[k - 1], r1 = rate[k];
+            ell = udiv_u64_u32((uint64_t)lat[k - 1] * (r1 - r) + (uint64_t)lat[k] * (r - r0),
+                               r1 - r0);
+        }
+        c = udiv_u64_u32(ell * n, p);
+    }
+    t.c = (uint32_t)c;
+    t.u = (uint32_t)(tp * fq * d);
+    return t;
+}
+
+__device__ __forceinline__ OptionTerm option_term(const SpaceDev &sp, const TablesDev &tb,
+                                                  uint32_t inst, uint32_t m, uint32_t o,
+                                                  uint64_t lambda)
+{
+    const uint32_t ij = o / sp.D;
+    const uint32_t j = ij % sp.n_fq, i = ij / sp.n_fq;
+    const uint64_t lm = (uint64_t)inst * sp.M + m;
+    const uint64_t tab = (lm * sp.n_tp + i) * sp.n_fq + j;
+    return option_term_from(sp, tb.H, o, tb.rate + tab * sp.K, tb.lat + tab * sp.K,
+                            tb.allowed[tab] != 0, tb.W[lm], tb.n[lm], tb.p[lm], lambda);
+}
+
+// The item's profile inputs a one-launch block keeps in LDS: every (LLM, tp, share) curve (rate
+// then lat, K points each), the curves' allowed flags and each LLM's (W, n << 32 | p).
+struct FusedLds {
+    const uint32_t *curve;
+    const uint8_t *allowed;
+    const ulonglong2 *llm;
+    const uint2 *ext;          // every option's (tau, share units), written by the prologue
+    __device__ __forceinline__ OptionTerm term(const SpaceDev &sp, uint64_t H, uint32_t m,
+                                               uint32_t o, uint64_t lambda) const
+    {
+        const uint32_t curves = sp.M * sp.n_tp * sp.n_fq;
+        const uint32_t c = m * sp.n_tp * sp.n_fq + o / sp.D;
+        const ulonglong2 wl = llm[m];
+        return option_term_from(sp, H, o, curve + c * sp.K, curve + (curves + c) * sp.K,
+                                allowed[c] != 0, wl.x, wl.y >> 32, wl.y & 0xFFFFFFFFu, lambda);
+    }
+};
+
+// Result record of a one-launch item whose winner is (L, x), by one wave: lane m reads LLM m's
+// option terms of the winner from the block's LDS.  A rejected query gets ALP_EINVAL.
+__device__ __forceinline__ void write_fused_result(const SpaceDev &sp, uint64_t H,
+                                                   const FusedLds &lds, uint64_t lambda,
+                                                   bool rejected, uint32_t L, uint64_t x,
+                                                   alp_result_t *dst)
+{
+    const uint32_t lane = threadIdx.x & 63;
+    if (rejected)
+        L = kNoLatency;
+    uint32_t o = 0, T = 0xFFFFFFFFu, U = 0;
+    if (L != kNoLatency && lane < sp.M) {
+        o = candidate_digit(sp, x, lane);
+        const uint2 e = lds.ext[lane * sp.O + o];
+        T = e.x;
+        U = e.y;
+    }
+    write_result_lanes(sp, o, T, U, L, x, reinterpret_cast<uint64_t *>(dst),
+                       rejected ? (uint32_t)ALP_EINVAL : (uint32_t)ALP_INFEASIBLE);
+}
+
+// End of a one-launch block: the block's lowest (L, x) (x < 2^32) joins the item's word by an
+// atomic maximum of ~(L << 32 | x), performed (returned) before the block counts itself.  Blocks
+// count in groups of kFusedGroup (sub / kFusedGroup); the last block of a group counts the group
+// in the item's counter, and the block completing the last group reads the item's lowest
+// candidate from the word, resets the words and writes the result.  `hint` and `held` as in
+// block_finish.
+__device__ __forceinline__ void block_finish_fused(uint32_t L, uint64_t x, uint32_t item,
+                                                   uint32_t sub, uint32_t blocks_per_item,
+                                                   const FinishArgs &fa, const FusedArgs &fz,
+                                                   const FusedLds &lds, uint64_t lambda,
+                                                   bool rejected, uint32_t hint, bool held)
+{
+    __shared__ uint32_t last_block;
+    __shared__ unsigned long long s_word;
+    if (blocks_per_item == 1) {
+        block_min(L, x);
+        if (threadIdx.x < 64)
+            write_fused_result(fa.sp, fz.tb.H, lds, lambda, rejected, L, x, fa.out + item);
+        return;
+    }
+    if (held)
+        block_min(L, x);
+    if (threadIdx.x == 0) {
+        if (held && L != kNoLatency && L <= hint) {
+            (void)atomicMax(&fz.best[item], ~(((unsigned long long)L << 32) | x));
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        }
+        const uint32_t groups = (blocks_per_item + kFusedGroup - 1) / kFusedGroup;
+        const uint32_t g = sub / kFusedGroup;
+        const uint32_t in_group = g + 1 < groups ? kFusedGroup : blocks_per_item - g * kFusedGroup;
+        uint32_t *gd = fz.group_done + (uint64_t)item * groups + g;
+        last_block = 0;
+        if (atomicAdd(gd, 1u) == in_group - 1) {
+            (void)atomicExch(gd, 0u);              // the group's count, 0 for the next launch
+            if (atomicAdd(&fz.done[item], 1u) == groups - 1) {
+                s_word = atomicExch(&fz.best[item], 0ull);
+                (void)atomicExch(&fz.done[item], 0u);
+                last_block = 1;
+            }
+        }
+    }
+    __syncthreads();
+    if (!last_block || threadIdx.x >= 64)
+        return;
+    const unsigned long long w = ~s_word;
+    const uint32_t Lw = s_word ? (uint32_t)(w >> 32) : kNoLatency;
+    write_fused_result(fa.sp, fz.tb.H, lds, lambda, rejected, Lw, (uint32_t)w, fa.out + item);
 }
 
 // Workgroups are dispatched to the 8 XCDs round-robin; renumber them so that consecutive

@@ -92,6 +92,9 @@ struct ScanGeometry {
     uint32_t slots;            // variants 1, 3: options of the last LLM per lane (1, 2, 4, 8)
     uint32_t pair;             // variant 1: the inner table is the pair table (rows fix M - 3
                                // digits, O^2 records each)
+    uint32_t fused;            // variant 1: one launch -- every block computes its item's option
+                               // terms itself, and the item's winner is one 64-bit word (spaces of
+                               // fewer than 2^32 candidates, never with the pair table)
 };
 
 // Queries of a search batch given in device memory, prepared by the option-term kernel: item i
@@ -103,6 +106,25 @@ struct RawQueries {
     uint32_t B, units_per_gpu;
     uint32_t *q_inst, *q_cap, *q_lambda, *invalid;
 };
+
+// The one-launch form of the scan (ScanGeometry::fused): each block computes the option terms
+// of its item from the tables into its own region of device memory and reads them back through
+// the scalar cache; the item's best candidate so far is the word best[item] = ~(L << 32 | x)
+// (x < 2^32), raised by an atomic maximum, 0 for none; done[item] counts finished blocks.  The
+// last block of an item resets both words to 0, so they are 0 between launches (the host zeroes
+// them when it allocates them).
+struct FusedArgs {
+    TablesDev tb;
+    RawQueries raw;            // device queries when raw.budget is set (the QueryDev otherwise)
+    uint2 *regions;            // per block: M * O option records, then inner_stride(O) records
+    uint32_t region;           // records per block region
+    uint32_t *done;            // per item: finished block groups
+    uint32_t *group_done;      // per item and group of kFusedGroup blocks: finished blocks
+    unsigned long long *best;
+};
+// Blocks of an item counted together before the item's count (two-level counting, so that at
+// most this many blocks update one counter word).
+constexpr uint32_t kFusedGroup = 32;
 
 // What the option-term kernel resets for the scan that follows it: per item, the finished-block
 // counter (done = 0) and the smallest block latency (best = kNoLatency, if best is set); every
@@ -124,10 +146,37 @@ hipError_t launch_option_terms(const SpaceDev &sp, const TablesDev &tb, const Qu
 // padding records never fit.
 hipError_t launch_pair_terms(const SpaceDev &sp, uint32_t count, const uint2 *rec,
                              const uint2 *inner, uint2 *pair, hipStream_t st);
+// fz: the one-launch form's arguments (g.fused), else nullptr.
 hipError_t launch_scan(const SpaceDev &sp, const QueryDev &q, uint32_t count, const uint2 *rec,
                        const uint2 *inner, const ScanGeometry &g, Winner *winners,
                        const FinishArgs &fa, hipStream_t st, hipEvent_t t0 = nullptr,
-                       hipEvent_t t1 = nullptr);
+                       hipEvent_t t1 = nullptr, const FusedArgs *fz = nullptr);
+// Dynamic LDS of a one-launch scan block: the item's profile curves (rate and lat of every
+// (LLM, tp, share), K points each) and their allowed flags ...
+__host__ __device__ inline size_t fused_lds_curves(const SpaceDev &sp)
+{
+    return (size_t)sp.M * sp.n_tp * sp.n_fq;
+}
+// ... followed by the inner LLM's records (inner_stride(O) of them), 8-byte aligned.
+__host__ __device__ inline size_t fused_lds_inner_offset(const SpaceDev &sp)
+{
+    const size_t curves = fused_lds_curves(sp);
+    return (2 * curves * sp.K * sizeof(uint32_t) + curves + 7) & ~(size_t)7;
+}
+// ... then every option's (tau, share units) for the result record.
+__host__ __device__ inline size_t fused_lds_ext_offset(const SpaceDev &sp)
+{
+    return fused_lds_inner_offset(sp) + (size_t)inner_stride(sp.O) * 8;
+}
+__host__ __device__ inline size_t fused_lds_bytes(const SpaceDev &sp)
+{
+    return fused_lds_ext_offset(sp) + (size_t)sp.M * sp.O * 8;
+}
+// Records per block region of the one-launch form.
+__host__ __device__ inline uint32_t fused_region(uint32_t M, uint32_t O)
+{
+    return (M * O + inner_stride(O) + 7u) & ~7u;    // 64-byte multiple
+}
 hipError_t launch_eval(const SpaceDev &sp, uint32_t capacity, const uint2 *rec, const uint2 *ext,
                        const uint64_t *idx, uint64_t count, alp_eval_t *out, hipStream_t st);
 hipError_t launch_tmax(const SpaceDev &sp, const QueryDev &q, uint32_t count, const uint2 *ext,

@@ -82,40 +82,11 @@ option_terms_kernel(SpaceDev sp, TablesDev tb, QueryDev q, uint32_t count, uint2
         lambda = query_value(q.lambda, q.lambda1, item);
     }
 
-    const uint32_t d = o % sp.D + 1;
-    const uint32_t ij = o / sp.D;
-    const uint32_t j = ij % sp.n_fq, i = ij / sp.n_fq;
-    const uint64_t tp = sp.tp[i], fq = sp.fq[j];
-    const uint64_t lm = (uint64_t)inst * sp.M + m;
-    const uint64_t tab = (lm * sp.n_tp + i) * sp.n_fq + j;
-    const uint32_t *rate = tb.rate + tab * sp.K;
-    const uint32_t *lat = tb.lat + tab * sp.K;
-    const uint64_t n = tb.n[lm], p = tb.p[lm];
-
-    // Deployable and the weights, sharded over tp, fit the share fq/Q of one GPU's memory.
-    const bool ok = tb.allowed[tab] != 0 && tb.W[lm] * sp.Q <= tp * fq * tb.H;
-    // Eq. 2 term: d replicas of saturation throughput T, per workflow request.
-    const uint64_t T = rate[sp.K - 1];
-    uint64_t tau = 1000ull * d * T / n;
-    tau = tau > 0xFFFFFFFFull ? 0xFFFFFFFFull : tau;
-    // Each replica receives lambda * n / d (rounded up).
-    const uint64_t dd = 1000ull * d;
-    const uint64_t r = (lambda * n + dd - 1) / dd;
-    const bool thr = r <= T;
-    uint64_t c = 0;
-    if (thr) {
-        // Eq. 1 term: latency at the replica's load, scaled by n / p.
-        uint64_t ell = lat[0];
-        if (r > rate[0]) {
-            uint32_t k = 1;
-            while (r > rate[k])
-                ++k;
-            const uint64_t r0 = rate[k - 1], r1 = rate[k];
-            ell = ((uint64_t)lat[k - 1] * (r1 - r) + (uint64_t)lat[k] * (r - r0)) / (r1 - r0);
-        }
-        c = ell * n / p;
-    }
-    const uint32_t u = (uint32_t)(tp * fq * d);
+    const OptionTerm term = option_term(sp, tb, inst, m, o, lambda);
+    const uint64_t c = term.c;
+    const bool ok = term.ok, thr = term.thr;
+    const uint32_t tau = term.tau;
+    const uint32_t u = term.u;
     const bool usable = ok && thr;
     const uint32_t units = usable ? u : kSentinelUnits;
     rec[t] = make_uint2(usable ? (uint32_t)c : 0u, units);
@@ -304,12 +275,59 @@ __device__ __forceinline__ void masked_find_step(uint32_t (&jf)[S], const int32_
 }
 
 // NOUT >= 0: the number of outer digits (M - 2) is fixed at compile time; NOUT < 0: any M.
-template <int S, int NOUT, bool DYNAMIC>
+// Scalar loads of records the same kernel wrote (the one-launch form): the compiler would read
+// memory written earlier in the kernel with vector loads and move every value to a scalar
+// register on its own, so these loads are spelled out.  The block's stores have reached L2
+// (waited for before its barrier) and no scalar cache line of the region was read before them.
+typedef uint32_t u32x16 __attribute__((ext_vector_type(16)));
+
+// A wave-uniform address as a scalar value (every lane holds the same pointer).
+__device__ __forceinline__ const uint2 *uniform_ptr(const uint2 *p)
+{
+    const uint64_t a = (uint64_t)p;
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32));
+    return (const uint2 *)(((uint64_t)hi << 32) | lo);
+}
+
+__device__ __forceinline__ void scalar_load16(const uint2 *p, uint2 (&a)[8], uint2 (&b)[8])
+{
+    u32x16 x, y;
+    asm volatile("s_load_dwordx16 %0, %2, 0x0\n\t"
+                 "s_load_dwordx16 %1, %2, 0x40\n\t"
+                 "s_waitcnt lgkmcnt(0)"
+                 : "=s"(x), "=s"(y)
+                 : "s"(uniform_ptr(p))
+                 : "memory");
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+        a[t] = make_uint2(x[2 * t], x[2 * t + 1]);
+        b[t] = make_uint2(y[2 * t], y[2 * t + 1]);
+    }
+}
+
+__device__ __forceinline__ uint2 scalar_load1(const uint2 *p)
+{
+    uint64_t v;
+    asm volatile("s_load_dwordx2 %0, %1, 0x0\n\t"
+                 "s_waitcnt lgkmcnt(0)"
+                 : "=s"(v)
+                 : "s"(uniform_ptr(p))
+                 : "memory");
+    return make_uint2((uint32_t)v, (uint32_t)(v >> 32));
+}
+
+// FUSED: the one-launch form (see FusedArgs) -- the block first computes its item's option
+// terms into its own region (the inner LLM's records with the query's capacity folded in, as
+// the option-term kernel writes them), waits for the stores to reach L2 and reads them back
+// through the scalar cache like the separate kernel's; the finish keeps the item's winner in one
+// 64-bit word.  Requires no pair table and fewer than 2^32 candidates per item.
+template <int S, int NOUT, bool DYNAMIC, bool FUSED>
 __global__ void __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 8 : 1)))
 scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_all, QueryDev q,
                 uint32_t M, uint32_t O, uint64_t rows, uint64_t rows_per_wave, uint32_t chunks,
                 uint32_t blocks_per_item, uint32_t nblocks, Winner *__restrict__ winners,
-                FinishArgs fa, uint32_t pair)
+                FinishArgs fa, uint32_t pair, FusedArgs fz)
 {
     // pair = 1: the inner table is the pair table of LLMs M-3 and M-2 (index j = j3 * O + j2,
     // O^2 records), so rows fix the M - 3 outer digits; candidates keep their index order.
@@ -322,11 +340,93 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
     const uint32_t lb = xcd_logical_block(blockIdx.x, nblocks);
     const uint32_t item = lb / blocks_per_item;
     const uint32_t sub = lb - item * blocks_per_item;
-    const int32_t capacity = (int32_t)query_value(q.capacity, q.cap1, item);
-    const uint2 *R = rec + (uint64_t)item * M * O;
     const uint32_t lane = threadIdx.x & 63;
     const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const uint32_t wpb = blockDim.x >> 6;
+    int32_t capacity;
+    const uint2 *R, *inner;
+    uint32_t f_inst = 0;          // FUSED: the query
+    uint64_t f_lambda = 0;
+    bool f_rejected = false;
+    FusedLds flds{};
+    const uint2 *s_inner = nullptr;     // FUSED: the inner LLM's records, in LDS
+    __shared__ uint2 s_last[FUSED ? ALP_MAX_OPTIONS : 1];
+    // FUSED: the item's profile curves (rate, then lat: 2 * curves * K words) and the curves'
+    // allowed flags in dynamic LDS (fused_lds_bytes), each LLM's W, n, p.
+    extern __shared__ uint32_t s_curve[];
+    __shared__ ulonglong2 s_llm[FUSED ? ALP_MAX_LLMS : 1];
+    if constexpr (FUSED) {
+        uint32_t cap;
+        if (fz.raw.budget) {
+            f_inst = fz.raw.inst ? fz.raw.inst[item] : item;
+            f_rejected = f_inst >= fz.raw.B;
+            f_inst = f_rejected ? 0u : f_inst;
+            const uint64_t c64 = (uint64_t)fz.raw.units_per_gpu * fz.raw.budget[item];
+            cap = c64 > kCapacityMax ? kCapacityMax : (uint32_t)c64;
+            f_lambda = fz.raw.target[item];
+        } else {
+            f_inst = query_value(q.inst, q.inst1, item);
+            cap = query_value(q.capacity, q.cap1, item);
+            f_lambda = query_value(q.lambda, q.lambda1, item);
+        }
+        capacity = (int32_t)cap;
+        uint2 *blk = fz.regions + (uint64_t)blockIdx.x * fz.region;
+        uint2 *blk_inner = blk + M * O;
+        const uint32_t stride = inner_stride(O);
+        // The item's profile curves (one per LLM, tp and share; shared by the replica counts)
+        // staged in LDS by one load per point, all in flight together, with each LLM's W, n, p.
+        const SpaceDev &sp = fa.sp;
+        const uint32_t K = sp.K, curves = M * sp.n_tp * sp.n_fq;
+        const uint64_t base = (uint64_t)f_inst * curves;
+        uint8_t *s_allowed = reinterpret_cast<uint8_t *>(s_curve + 2 * curves * K);
+        uint2 *s_inner_w = reinterpret_cast<uint2 *>(reinterpret_cast<uint8_t *>(s_curve) +
+                                                     fused_lds_inner_offset(sp));
+        uint2 *s_ext_w = reinterpret_cast<uint2 *>(reinterpret_cast<uint8_t *>(s_curve) +
+                                                   fused_lds_ext_offset(sp));
+        flds = FusedLds{s_curve, s_allowed, s_llm, s_ext_w};
+        s_inner = s_inner_w;
+        for (uint32_t a = threadIdx.x; a < curves * K; a += blockDim.x) {
+            s_curve[a] = fz.tb.rate[base * K + a];
+            s_curve[curves * K + a] = fz.tb.lat[base * K + a];
+        }
+        for (uint32_t a = threadIdx.x; a < curves; a += blockDim.x)
+            s_allowed[a] = fz.tb.allowed[base + a];
+        if (threadIdx.x < M) {
+            const uint64_t lm = (uint64_t)f_inst * M + threadIdx.x;
+            s_llm[threadIdx.x] = make_ulonglong2(fz.tb.W[lm],
+                                                 (uint64_t)fz.tb.n[lm] << 32 | fz.tb.p[lm]);
+        }
+        __syncthreads();
+        for (uint32_t a = threadIdx.x; a < M * O; a += blockDim.x) {
+            const uint32_t m = a / O, o = a - m * O;
+            const OptionTerm t = flds.term(sp, fz.tb.H, m, o, f_lambda);
+            s_ext_w[a] = make_uint2(t.tau, t.u);
+            const bool usable = t.ok && t.thr;
+            const uint2 r = make_uint2(usable ? t.c : 0u, usable ? t.u : kSentinelUnits);
+            blk[a] = r;
+            if (m == M - 1)
+                s_last[o] = r;
+            if (M >= 2 && m == M - 2) {
+                const uint2 in = make_uint2(r.x, (uint32_t)((int32_t)cap - (int32_t)r.y));
+                blk_inner[o] = in;
+                s_inner_w[o] = in;
+            }
+        }
+        for (uint32_t a = O + threadIdx.x; a < stride; a += blockDim.x) {
+            blk_inner[a] = make_uint2(0u, (uint32_t)kNeverFits);
+            s_inner_w[a] = make_uint2(0u, (uint32_t)kNeverFits);
+        }
+        // The region is read back through the scalar cache, which reads L2: wait until every
+        // store has reached it, then let the other waves go.
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        R = blk;
+        inner = blk_inner;
+    } else {
+        capacity = (int32_t)query_value(q.capacity, q.cap1, item);
+        R = rec + (uint64_t)item * M * O;
+        inner = inner_all + (uint64_t)item * (pair ? pair_stride(O) : inner_stride(O));
+    }
 
     // The last LLM's options of this lane: lane, lane + 64, ...  They are processed in order
     // of share units (insertion sort of the S values held by the lane), which lets the hot
@@ -339,7 +439,7 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
         const uint32_t o = lane + 64u * s;
         o_last[s] = o;
         if (o < O) {
-            const uint2 v = last[o];
+            const uint2 v = FUSED ? s_last[o] : last[o];
             c_last[s] = v.x;
             u_last[s] = (int32_t)v.y;
         } else {
@@ -365,7 +465,6 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
     const bool has_inner = M >= 2;
     const uint32_t n_inner_padded = pair ? pair_stride(O) : inner_stride(O);
     const uint32_t chunk_len = n_inner_padded / chunks;   // a multiple of 16
-    const uint2 *inner = inner_all + (uint64_t)item * n_inner_padded;
     const uint32_t n_inner = has_inner ? (pair ? O * O : O) : 1;
     constexpr int NMAX = NOUT >= 0 ? NOUT : (int)kMaxOuter;
     const uint32_t n_outer =
@@ -382,12 +481,12 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
     const uint64_t per = DYNAMIC ? rows_per_wave * wpb : rows_per_wave;
     const uint64_t r_begin = (DYNAMIC ? (uint64_t)sub : gw) * per;
     const uint64_t r_end = r_begin + per < rows ? r_begin + per : rows;
-    __shared__ uint32_t s_next;
-    if (DYNAMIC) {
-        if (threadIdx.x == 0)
-            s_next = wpb;
-        __syncthreads();
+    __shared__ uint32_t s_next, s_ended;
+    if (threadIdx.x == 0) {
+        s_next = wpb;
+        s_ended = 0;
     }
+    __syncthreads();
     const uint32_t first = DYNAMIC ? wave : 0u;
 
     const uint64_t full = __builtin_amdgcn_read_exec();
@@ -445,7 +544,8 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
 #pragma unroll
             for (int k = 0; k < NMAX; ++k) {
                 if (NOUT >= 0 || (uint32_t)k < n_outer) {
-                    const uint2 v = R[(uint64_t)k * O + digit[k]];
+                    const uint2 *rp = R + (uint64_t)k * O + digit[k];
+                    const uint2 v = FUSED ? scalar_load1(rp) : *rp;
                     oc += v.x;
                     ou += (int32_t)v.y;
                 }
@@ -466,10 +566,14 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
                     (DYNAMIC ? begin + chunk_len : inner + n_inner_padded) - 16;
                 auto batch = [&](const uint2 *p) {
                     uint2 v0[8], v1[8];
+                    if constexpr (FUSED) {
+                        scalar_load16(p, v0, v1);
+                    } else {
 #pragma unroll
-                    for (int t = 0; t < 8; ++t) {
-                        v0[t] = p[t];
-                        v1[t] = p[8 + t];
+                        for (int t = 0; t < 8; ++t) {
+                            v0[t] = p[t];
+                            v1[t] = p[8 + t];
+                        }
                     }
                     masked_min_8(bq, w, v0, full);
                     masked_min_8(bq, w, v1, full);
@@ -521,9 +625,18 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
     // The item's best latency so far as this wave sees it at the end of its loop (the loads of
     // a block's last waves see what blocks that ended earlier published).  A block whose
     // minimum lies above it cannot hold the item's winner and skips its re-scan.
+    // Only the block's last wave to end its loop reads it: one coherent load per block, taken
+    // as late as the block allows.
     uint32_t hint = kNoLatency;
-    if (lane == 0 && blocks_per_item > 1)
-        hint = __hip_atomic_load(&fa.best[item], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (lane == 0 && blocks_per_item > 1 && atomicAdd(&s_ended, 1u) == wpb - 1) {
+        if constexpr (FUSED) {
+            const unsigned long long w =
+                __hip_atomic_load(&fz.best[item], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            hint = w ? (uint32_t)(~w >> 32) : kNoLatency;
+        } else {
+            hint = __hip_atomic_load(&fa.best[item], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
     // The wave's lowest sub-row reaching L* (its lane-slots' first rows at L*), as a sub-row
     // index of the item, and that row's outer sums, loaded now while the block's other waves
     // finish (claimed sub-rows number fewer than 2^32).
@@ -586,8 +699,16 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
             for (uint32_t jb = j0 + 4u * wave; jb < j0 + chunk_len; jb += 4u * wpb) {
                 uint2 v[4];
 #pragma unroll
-                for (int t = 0; t < 4; ++t)
-                    v[t] = inner[jb + t];
+                for (int t = 0; t < 4; ++t) {
+                    if constexpr (FUSED) {
+                        // the same LDS word in every lane: move it to scalar registers
+                        const uint2 l = s_inner[jb + t];
+                        v[t] = make_uint2((uint32_t)__builtin_amdgcn_readfirstlane((int)l.x),
+                                          (uint32_t)__builtin_amdgcn_readfirstlane((int)l.y));
+                    } else {
+                        v[t] = inner[jb + t];
+                    }
+                }
 #pragma unroll
                 for (int t = 0; t < 4; ++t)
                     masked_find_step(jf, w, target, v[t].y, v[t].x, jb + t, full);
@@ -609,7 +730,11 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
         waveL = Lblock;
         waveX = wave_min_u64(xmin);
     }
-    block_finish(waveL, waveX, item, sub, blocks_per_item, winners, fa, block_hint, held);
+    if constexpr (FUSED)
+        block_finish_fused(waveL, waveX, item, sub, blocks_per_item, fa, fz, flds, f_lambda,
+                           f_rejected, block_hint, held);
+    else
+        block_finish(waveL, waveX, item, sub, blocks_per_item, winners, fa, block_hint, held);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -633,11 +758,11 @@ scan_lane_kernel(const uint2 *__restrict__ rec, QueryDev q, uint32_t M, uint32_t
     const uint32_t lb = xcd_logical_block(blockIdx.x, nblocks);
     const uint32_t item = lb / blocks_per_item;
     const uint32_t sub = lb - item * blocks_per_item;
-    const int32_t capacity = (int32_t)query_value(q.capacity, q.cap1, item);
-    const uint2 *R = rec + (uint64_t)item * M * O;
     const uint32_t lane = threadIdx.x & 63;
     const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const uint32_t wpb = blockDim.x >> 6;
+    const int32_t capacity = (int32_t)query_value(q.capacity, q.cap1, item);
+    const uint2 *R = rec + (uint64_t)item * M * O;
 
     // The last LLM's options owned by this lane.
     const uint2 *last = R + (uint64_t)(M - 1) * O;
@@ -1044,8 +1169,11 @@ template <int S>
 static hipError_t launch_lane(const SpaceDev &sp, const QueryDev &q, uint32_t count,
                               const uint2 *rec, const uint2 *inner, const ScanGeometry &g,
                               Winner *winners, const FinishArgs &fa, hipStream_t st,
-                              hipEvent_t t0, hipEvent_t t1)
+                              hipEvent_t t0, hipEvent_t t1, const FusedArgs *fzp)
 {
+    FusedArgs fz{};
+    if (fzp)
+        fz = *fzp;
     const uint32_t nblocks = count * g.blocks_per_item;
     if (g.variant == 3)
         hipExtLaunchKernelGGL(HIP_KERNEL_NAME(scan_lane_kernel<S>), dim3(nblocks), dim3(g.threads),
@@ -1053,18 +1181,24 @@ static hipError_t launch_lane(const SpaceDev &sp, const QueryDev &q, uint32_t co
                               g.blocks_per_item, nblocks, winners, fa);
     else {
         const uint32_t n_outer = sp.M >= 2 + g.pair ? sp.M - 2 - g.pair : 0;
+#define ALP_LAUNCH_MIN_DF(NO, DYN, FU)                                                             \
+    hipExtLaunchKernelGGL(HIP_KERNEL_NAME(scan_min_kernel<S, NO, DYN, FU>), dim3(nblocks),         \
+                          dim3(g.threads), FU ? fused_lds_bytes(sp) : 0, st, t0, t1, 0, rec,       \
+                          inner, q, sp.M, sp.O, g.rows,                                            \
+                          g.rows_per_wave, DYN ? g.chunks : 1u, g.blocks_per_item, nblocks,        \
+                          winners, fa, g.pair, fz)
 #define ALP_LAUNCH_MIN(NO)                                                                         \
     do {                                                                                           \
-        if (g.dynamic)                                                                             \
-            hipExtLaunchKernelGGL(HIP_KERNEL_NAME(scan_min_kernel<S, NO, true>), dim3(nblocks),    \
-                                  dim3(g.threads), 0, st, t0, t1, 0, rec, inner, q, sp.M, sp.O,    \
-                                  g.rows, g.rows_per_wave, g.chunks, g.blocks_per_item, nblocks,   \
-                                  winners, fa, g.pair);                                            \
-        else                                                                                       \
-            hipExtLaunchKernelGGL(HIP_KERNEL_NAME(scan_min_kernel<S, NO, false>), dim3(nblocks),   \
-                                  dim3(g.threads), 0, st, t0, t1, 0, rec, inner, q, sp.M, sp.O,    \
-                                  g.rows, g.rows_per_wave, 1u, g.blocks_per_item, nblocks,         \
-                                  winners, fa, g.pair);                                            \
+        if (g.fused) {                                                                             \
+            if (g.dynamic)                                                                         \
+                ALP_LAUNCH_MIN_DF(NO, true, true);                                                 \
+            else                                                                                   \
+                ALP_LAUNCH_MIN_DF(NO, false, true);                                                \
+        } else if (g.dynamic) {                                                                    \
+            ALP_LAUNCH_MIN_DF(NO, true, false);                                                    \
+        } else {                                                                                   \
+            ALP_LAUNCH_MIN_DF(NO, false, false);                                                   \
+        }                                                                                          \
     } while (0)
         switch (n_outer) {
         case 0: ALP_LAUNCH_MIN(0); break;
@@ -1074,14 +1208,18 @@ static hipError_t launch_lane(const SpaceDev &sp, const QueryDev &q, uint32_t co
         default: ALP_LAUNCH_MIN(-1); break;
         }
 #undef ALP_LAUNCH_MIN
+#undef ALP_LAUNCH_MIN_DF
     }
     return hipGetLastError();
 }
 
 hipError_t launch_scan(const SpaceDev &sp, const QueryDev &q, uint32_t count, const uint2 *rec,
                        const uint2 *inner, const ScanGeometry &g, Winner *winners,
-                       const FinishArgs &fa, hipStream_t st, hipEvent_t t0, hipEvent_t t1)
+                       const FinishArgs &fa, hipStream_t st, hipEvent_t t0, hipEvent_t t1,
+                       const FusedArgs *fz)
 {
+    if (g.fused && (!fz || g.variant != 1 || g.pair))
+        return hipErrorInvalidValue;
     if (count == 0)
         return hipSuccess;
     if (g.variant == 2) {
@@ -1096,10 +1234,10 @@ hipError_t launch_scan(const SpaceDev &sp, const QueryDev &q, uint32_t count, co
         return hipGetLastError();
     }
     switch (g.slots) {
-    case 1: return launch_lane<1>(sp, q, count, rec, inner, g, winners, fa, st, t0, t1);
-    case 2: return launch_lane<2>(sp, q, count, rec, inner, g, winners, fa, st, t0, t1);
-    case 4: return launch_lane<4>(sp, q, count, rec, inner, g, winners, fa, st, t0, t1);
-    case 8: return launch_lane<8>(sp, q, count, rec, inner, g, winners, fa, st, t0, t1);
+    case 1: return launch_lane<1>(sp, q, count, rec, inner, g, winners, fa, st, t0, t1, fz);
+    case 2: return launch_lane<2>(sp, q, count, rec, inner, g, winners, fa, st, t0, t1, fz);
+    case 4: return launch_lane<4>(sp, q, count, rec, inner, g, winners, fa, st, t0, t1, fz);
+    case 8: return launch_lane<8>(sp, q, count, rec, inner, g, winners, fa, st, t0, t1, fz);
     default: return hipErrorInvalidValue;
     }
 }
@@ -1139,11 +1277,11 @@ int scan_blocks_per_cu(uint32_t variant, uint32_t slots, uint32_t threads, const
         const bool exact = variant == 3;
         const uint32_t no = sp.M >= 2 ? sp.M - 2 : 0;
 #define ALP_OCC_MIN(SL)                                                                            \
-    (no == 0 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<SL, 0, false>, (int)threads, 0) \
-   : no == 1 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<SL, 1, false>, (int)threads, 0) \
-   : no == 2 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<SL, 2, false>, (int)threads, 0) \
-   : no == 3 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<SL, 3, false>, (int)threads, 0) \
-             : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<SL, -1, false>, (int)threads, 0))
+    (no == 0 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<SL, 0, false, false>, (int)threads, 0) \
+   : no == 1 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<SL, 1, false, false>, (int)threads, 0) \
+   : no == 2 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<SL, 2, false, false>, (int)threads, 0) \
+   : no == 3 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<SL, 3, false, false>, (int)threads, 0) \
+             : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_min_kernel<SL, -1, false, false>, (int)threads, 0))
         switch (slots) {
         case 1: e = exact ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_lane_kernel<1>, (int)threads, 0) : ALP_OCC_MIN(1); break;
         case 2: e = exact ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, scan_lane_kernel<2>, (int)threads, 0) : ALP_OCC_MIN(2); break;

@@ -183,15 +183,18 @@ def test_async_kernel_times_are_collected(alp):
     Ld = torch.from_numpy(lam.view(np.int32)).to(dev)
     o = torch.empty(2 * alp.RESULT_DTYPE.itemsize, dtype=torch.uint8, device=dev)
     with alp.Context(b) as ctx:
-        ctx.set_timing(True)
-        for _ in range(4):
-            ctx.search_batch_async(Gd, Ld, o)
-        tot, calls = ctx.kernel_time_totals()          # waits for the four queued searches
-        last = ctx.kernel_times()
-        assert calls == 4 and tot[1] > 0 and tot[0] > 0 and tot[2] == 0
-        assert 0 < last[1] < tot[1]                      # one call's scan, four calls' sum
-        ctx.set_timing(True)
-        assert (ctx.kernel_time_totals()[0] == 0).all()
+        # one launch (no option-term kernel), then the two-launch form
+        for variant, terms in ((0, False), (16, True)):
+            ctx.set_launch(variant)
+            ctx.set_timing(True)
+            for _ in range(4):
+                ctx.search_batch_async(Gd, Ld, o)
+            tot, calls = ctx.kernel_time_totals()      # waits for the four queued searches
+            last = ctx.kernel_times()
+            assert calls == 4 and tot[1] > 0 and (tot[0] > 0) == terms and tot[2] == 0
+            assert 0 < last[1] < tot[1]                  # one call's scan, four calls' sum
+            ctx.set_timing(True)
+            assert (ctx.kernel_time_totals()[0] == 0).all()
 
 
 def test_wave_row_count_beyond_32_bits_is_rejected(alp):

@@ -85,7 +85,10 @@ CASES = load_cases()
 # Scan variants: row-minimum (automatic distribution), thread-per-candidate, exact-tracking lanes,
 # row-minimum with fixed per-wave rows, row-minimum with rows handed out within each block,
 # row-minimum over the pair table of LLMs M-3 and M-2 (3 or more LLMs; otherwise automatic).
-VARIANTS = (1, 2, 3, 4, 5, 6)
+SEP = 16                       # ALP_LAUNCH_SEPARATE_TERMS: option terms in their own kernel
+# Spaces below 2^32 candidates run the row-minimum scan in one launch; SEP variants keep the
+# two-launch form of each work distribution.
+VARIANTS = (1, 2, 3, 4, 5, 6, 1 | SEP, 4 | SEP, 5 | SEP)
 
 
 @pytest.mark.parametrize("case", CASES, ids=[c["id"] for c in CASES])
@@ -151,7 +154,8 @@ def test_cfg4_batch_matches_golden(alp):
         want = [(r["x"], r["L"], r["T"], r["U"]) for r in rows]
         # automatic launch, then rows handed out within blocks (several blocks per item, split
         # rows), then fixed per-wave rows with one block per item
-        for launch in [(0, 0, 0, 0), (5, 3, 256, 4), (4, 1, 512, 0)]:
+        for launch in [(0, 0, 0, 0), (5, 3, 256, 4), (4, 1, 512, 0), (SEP, 0, 0, 0),
+                       (5 | SEP, 3, 256, 4)]:
             ctx.set_launch(*launch)
             out = ctx.search_batch([r["G"] for r in rows], [r["lambda"] for r in rows])
             bad = [i for i in range(len(rows))
@@ -192,14 +196,17 @@ def test_launch_geometry_and_variant_do_not_change_results(alp):
                                       (4, 3000, 1024, 0), (5, 0, 0, 0), (5, 1, 64, 0),
                                       (5, 7, 128, 8), (5, 256, 1024, 4), (5, 3000, 1024, 1),
                                       (5, 512, 512, 2), (6, 0, 0, 0), (6, 1, 64, 0),
-                                      (6, 7, 128, 16), (6, 300, 1024, 1024), (6, 3000, 256, 1)]:
+                                      (6, 7, 128, 16), (6, 300, 1024, 1024), (6, 3000, 256, 1),
+                                      (SEP, 0, 0, 0), (1 | SEP, 7, 128, 8), (4 | SEP, 7, 128, 0),
+                                      (5 | SEP, 3000, 1024, 1), (5 | SEP, 1, 64, 4)]:
             ctx.set_launch(variant, bpi, tpb, ch)
             res = ctx.search(0, g["G"], g["lambda"])
             check_result(b, 0, res, g["x"], g["L"], g["T"], g["U"])
         for bad in ((1, 0, 0, 3),                      # 3 does not divide 128 / 16
                     (1, 0, 0, 16),                     # 16 divides only the pair table's 1,024
                     (6, 0, 0, 3),                      # 3 does not divide 128 * 128 / 16
-                    (7, 0, 0, 0), (0, 0, 96, 0)):      # no variant 7; 96 threads
+                    (7, 0, 0, 0), (0, 0, 96, 0),       # no variant 7; 96 threads
+                    (2 | SEP, 0, 0, 0), (6 | SEP, 0, 0, 0)):   # one launch never applies there
             with pytest.raises(alp.AlpError):
                 ctx.set_launch(*bad)
         ctx.set_launch(0, 0, 0)
@@ -316,7 +323,8 @@ def test_sparse_feasibility_multi_block(alp, G, lam_frac):
     want = oracle_expect(b, 0, G, lam)
     with alp.Context(b) as ctx:
         for launch in [(0, 0, 0, 0), (4, 0, 0, 0), (5, 0, 0, 0), (5, 64, 512, 0), (1, 0, 0, 4),
-                       (6, 0, 0, 0), (6, 16, 256, 64)]:
+                       (6, 0, 0, 0), (6, 16, 256, 64), (SEP, 0, 0, 0), (5 | SEP, 64, 512, 0),
+                       (4 | SEP, 0, 0, 0)]:
             ctx.set_launch(*launch)
             check_result(b, 0, ctx.search(0, G, lam), *want)
         ctx.set_launch(0)
