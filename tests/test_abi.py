@@ -28,7 +28,7 @@ def test_header_and_binding_agree():
 
 def _prototype(name: str) -> str:
     text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
-    m = re.search(r"([\w\s\*]+?)\b" + name + r"\s*\(([^)]*)\)\s*;", text)
+    m = re.search(r"^([\w \*]+?)\b" + name + r"\s*\(([^)]*)\)\s*;", text, re.M)
     assert m, name
     return " ".join((m.group(1) + " " + name + "(" + m.group(2) + ")").split())
 
