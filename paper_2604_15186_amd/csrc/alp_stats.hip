@@ -9,11 +9,12 @@
 //
 // Kernels:
 //   stats_init_kernel        zeroes the per-LLM totals, the error flags and the work-list count.
-//   trace_sweep_kernel<MM>   one workgroup per trace of at most 2,048 calls (MM bounds the number
-//                            of LLMs, so the per-LLM state fits in few registers).  A trace already
+//   trace_sweep_kernel<MM>   one wave per trace of at most 2,048 calls (MM bounds the number of
+//                            LLMs, so the per-LLM state fits in few registers).  A trace already
 //                            in order of end time (calls logged on completion) is swept backwards
-//                            without a sort: a call adds the part of it before the earliest start
-//                            of the same LLM's later calls.  Other traces go to a work list.
+//                            in rows of 64 consecutive calls, without a sort: a call adds the part
+//                            of it before the earliest start of the same LLM's later calls.  Other
+//                            traces go to a work list.
 //   trace_sort_kernel        the work list: calls sorted by key (llm << 60 | start), packed into
 //                            one 64-bit key when the starts span under 2^29 us, with a bitonic
 //                            network in registers, across lanes and in LDS; the time covered by
@@ -42,6 +43,7 @@ constexpr uint64_t kPad = ~0ull;                       // sorts after every real
 constexpr uint64_t kStartLimit = 1ull << 60;
 constexpr uint64_t kDurationLimit = 1ull << 32;
 constexpr uint32_t kThreads = 256;
+constexpr uint32_t kSortBlocks = 2048;                 // grid of the work-list sort
 
 __global__ void stats_init_kernel(uint64_t *__restrict__ totals, uint32_t words)
 {
@@ -373,142 +375,16 @@ __device__ __forceinline__ void wave_add_sums(uint32_t q, uint32_t calls, uint64
     }
 }
 
-// Covered time of a trace whose calls are in order of end time (as a proxy logs them on
-// completion), without a sort.  Walking the calls backwards, the calls of LLM m that come after
-// call j (so end no earlier) cover, within (-inf, e_j], exactly [lo, e_j] where lo is their
-// smallest start (or nothing if lo > e_j); so call j of LLM m adds max(0, min(e_j, lo) - s_j).
-// Thread t holds chunk 255 - t of the trace (calls (255 - t) E .. + E - 1), so the later calls
-// sit in the lower threads and lo past a thread's chunk is an exclusive prefix minimum per LLM:
-// DPP row shifts and row broadcasts within the wave, LDS across the four waves.  M <= MM: the
-// per-LLM state is sized at compile time.
-template <int E, int MM>
-__device__ __forceinline__ void sweep_by_end(uint32_t M, const uint32_t (&m)[E],
-                                             const uint64_t (&s)[E], const uint64_t (&e)[E],
-                                             const bool (&ok)[E], unsigned long long *s_sum)
-{
-    __shared__ uint64_t s_wave_lo[kThreads / 64][ALP_MAX_LLMS];
-    const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    // The thread's smallest start per LLM.
-    uint64_t lo[MM];
-#pragma unroll
-    for (uint32_t q = 0; q < (uint32_t)MM; ++q) {
-        lo[q] = ~0ull;
-#pragma unroll
-        for (int j = 0; j < E; ++j)
-            if (ok[j] && m[j] == q && s[j] < lo[q])
-                lo[q] = s[j];
-    }
-    // Inclusive prefix minimum over the wave's lanes (lane and lower): row shifts by 1, 2, 4
-    // and 8, then lane 15 into rows 1 and 3 and lane 31 into rows 2 and 3.  Lanes a move does
-    // not reach keep ~0, the identity.
-#pragma unroll
-    for (uint32_t q = 0; q < (uint32_t)MM; ++q) {
-        if (q >= M)
-            break;
-        uint64_t v = lo[q];
-        auto step = [&](auto c, auto rm) {
-            constexpr int C = decltype(c)::value, RM = decltype(rm)::value;
-            const uint64_t o = dpp_mov64<C, RM>(~0ull, v);
-            v = o < v ? o : v;
-        };
-        step(std::integral_constant<int, 0x111>{}, std::integral_constant<int, 0xF>{});
-        step(std::integral_constant<int, 0x112>{}, std::integral_constant<int, 0xF>{});
-        step(std::integral_constant<int, 0x114>{}, std::integral_constant<int, 0xF>{});
-        step(std::integral_constant<int, 0x118>{}, std::integral_constant<int, 0xF>{});
-        step(std::integral_constant<int, 0x142>{}, std::integral_constant<int, 0xA>{});
-        step(std::integral_constant<int, 0x143>{}, std::integral_constant<int, 0xC>{});
-        if (lane == 63)
-            s_wave_lo[wave][q] = v;
-        // Exclusive: the previous lane's value (a whole-wave shift by one; lane 0 gets ~0).
-        lo[q] = dpp_mov64<0x138>(~0ull, v);
-    }
-    __syncthreads();
-#pragma unroll
-    for (uint32_t q = 0; q < (uint32_t)MM; ++q) {
-        if (q >= M)
-            break;
-        for (uint32_t w = 0; w < wave; ++w)
-            lo[q] = s_wave_lo[w][q] < lo[q] ? s_wave_lo[w][q] : lo[q];
-    }
-    // Walk the thread's calls backwards.  Up to 4 LLMs, the per-LLM sums are kept as it goes;
-    // beyond, each call's covered part is kept and summed per LLM afterwards (fewer registers).
-    auto covered = [&](int j) {
-        uint64_t cur = ~0ull;
-#pragma unroll
-        for (uint32_t q = 0; q < (uint32_t)MM; ++q)
-            cur = m[j] == q ? lo[q] : cur;
-        const uint64_t right = e[j] < cur ? e[j] : cur;
-        return right > s[j] ? right - s[j] : 0ull;
-    };
-    if constexpr (MM <= 4) {
-        uint32_t calls[MM];
-        uint64_t busy[MM], active[MM];
-#pragma unroll
-        for (uint32_t q = 0; q < (uint32_t)MM; ++q) {
-            calls[q] = 0;
-            busy[q] = 0;
-            active[q] = 0;
-        }
-#pragma unroll
-        for (int j = E - 1; j >= 0; --j) {
-            if (!ok[j])
-                continue;
-            const uint64_t act = covered(j);
-#pragma unroll
-            for (uint32_t q = 0; q < (uint32_t)MM; ++q) {
-                if (m[j] == q) {
-                    calls[q] += 1;
-                    busy[q] += e[j] - s[j];
-                    active[q] += act;
-                    lo[q] = s[j] < lo[q] ? s[j] : lo[q];
-                }
-            }
-        }
-#pragma unroll
-        for (uint32_t q = 0; q < (uint32_t)MM; ++q)
-            if (q < M)
-                wave_add_sums(q, calls[q], busy[q], active[q], s_sum);
-    } else {
-        uint64_t act[E];
-#pragma unroll
-        for (int j = E - 1; j >= 0; --j) {
-            act[j] = ok[j] ? covered(j) : 0ull;
-            if (ok[j]) {
-#pragma unroll
-                for (uint32_t q = 0; q < (uint32_t)MM; ++q)
-                    if (m[j] == q && s[j] < lo[q])
-                        lo[q] = s[j];
-            }
-        }
-#pragma unroll
-        for (uint32_t q = 0; q < (uint32_t)MM; ++q) {
-            if (q >= M)
-                break;
-            uint32_t calls = 0;
-            uint64_t busy = 0, active = 0;
-#pragma unroll
-            for (int j = 0; j < E; ++j) {
-                const bool mine = ok[j] && m[j] == q;
-                calls += mine ? 1u : 0u;
-                busy += mine ? e[j] - s[j] : 0u;
-                active += mine ? act[j] : 0u;
-            }
-            wave_add_sums(q, calls, busy, active, s_sum);
-        }
-    }
-}
-
 // Largest trace the LDS path holds in registers while it loads (calls per thread).
 constexpr uint32_t kMaxPerThread = 8;
 
-// The three passes over the traces.  kSweep: every trace of at most lds_cap calls, one block
-// each; traces in end order are swept without a sort, the others are appended to a work list.
-// kSort: the work list, sorted in registers or LDS.  kLong: traces beyond lds_cap, sorted in a
-// global scratch region.
-enum StatsPass { kSweep = 0, kSort = 1, kLong = 2 };
+// The passes that sort (the sweep of end-ordered traces is trace_sweep_kernel below).  kSort:
+// the work list (or every trace of at most lds_cap calls), sorted in registers or LDS.  kLong:
+// traces beyond lds_cap, sorted in a global scratch region.
+enum StatsPass { kSort = 1, kLong = 2 };
 
 struct StatsArgs {
-    uint32_t M, lds_cap;
+    uint32_t M, lds_cap, R;
     const uint64_t *offsets;
     const uint32_t *llm;
     const uint64_t *start, *end;
@@ -517,7 +393,7 @@ struct StatsArgs {
     uint64_t *scratch;
     unsigned long long *totals;       // kStatsCopies copies of the per-LLM sums
     uint32_t *flags;
-    uint32_t *work;                   // kSweep appends, kSort reads: traces needing the sort
+    uint32_t *work;                   // the sweep appends, kSort reads: traces needing the sort
     uint32_t *work_count;
 };
 
@@ -569,73 +445,30 @@ __device__ __forceinline__ void one_trace(const StatsArgs &a, uint32_t r, uint32
     if (!Global) {
         // Held in registers: the trace's first and last start decide whether a call packs
         // into one 64-bit key, (llm << 61 | start - first << 32 | duration), which halves the
-        // sort's LDS traffic; traces spanning 2^29 us or more keep (key, end) pairs.
-        // Thread t holds chunk 255 - t: calls (255 - t) E .. + E - 1 (E = P / 256), so that
-        // later calls sit in lower threads (see sweep_by_end).
+        // sort's LDS traffic; traces spanning 2^29 us or more keep (key, end) pairs.  Thread t
+        // loads calls k * 256 + t (k < P / 256), so each load instruction reads consecutive
+        // calls; where a call starts out does not matter to the sort.
         const uint32_t E = P / kThreads;
-        const uint32_t chunk = kThreads - 1 - threadIdx.x;
         uint32_t rm[kMaxPerThread];
         uint64_t rs[kMaxPerThread], re[kMaxPerThread];
         bool ok[kMaxPerThread];
         uint64_t smin = ~0ull, smax = 0;
-        // Whether the calls are in order of end time: within the chunk, and (below) across
-        // chunk boundaries through s_first.
-        bool in_order = true;
-        uint64_t first_end = ~0ull, last_end = 0;
 #pragma unroll
         for (uint32_t k = 0; k < kMaxPerThread; ++k) {
-            ok[k] = k < E && load((uint64_t)chunk * E + k, rm[k], rs[k], re[k]);
+            ok[k] = k < E && load((uint64_t)k * kThreads + threadIdx.x, rm[k], rs[k], re[k]);
             if (ok[k]) {
                 valid += 1;
                 smin = rs[k] < smin ? rs[k] : smin;
                 smax = rs[k] > smax ? rs[k] : smax;
-                in_order = in_order && re[k] >= last_end;
-                first_end = first_end == ~0ull ? re[k] : first_end;
-                last_end = re[k];
             }
         }
-        __shared__ uint64_t s_first[kThreads];
-        if constexpr (Pass == kSweep)
-            s_first[threadIdx.x] = first_end;
         if (bad)
             atomicOr(flags, bad);
         uint32_t nvalid = valid;
-        block_min_max_sum(smin, smax, nvalid);          // its barrier also publishes s_first
+        block_min_max_sum(smin, smax, nvalid);
         if (nvalid == 0)
             return;
-        // The next chunk (thread t - 1) that holds a call must not end earlier (chunks with
-        // no call are padding and come last); malformed calls (bad) send the trace to the sort.
-        if constexpr (Pass == kSweep) {
-            if (threadIdx.x > 0 && s_first[threadIdx.x - 1] != ~0ull)
-                in_order = in_order && s_first[threadIdx.x - 1] >= last_end;
-            if (bad)
-                in_order = false;
-            if (!__syncthreads_and(in_order ? 1 : 0)) {
-                if (threadIdx.x == 0)
-                    a.work[atomicAdd(a.work_count, 1u)] = r;
-                return;
-            }
-            auto run = [&](auto e_const) {
-                constexpr int EC = decltype(e_const)::value;
-                uint32_t m[EC];
-                uint64_t st[EC], en[EC];
-                bool okc[EC];
-#pragma unroll
-                for (int j = 0; j < EC; ++j) {
-                    m[j] = rm[j];
-                    st[j] = rs[j];
-                    en[j] = re[j];
-                    okc[j] = ok[j];
-                }
-                sweep_by_end<EC, MM>(M, m, st, en, okc, s_sum);
-            };
-            switch (P) {
-            case kThreads: run(std::integral_constant<int, 1>{}); break;
-            case 2 * kThreads: run(std::integral_constant<int, 2>{}); break;
-            case 4 * kThreads: run(std::integral_constant<int, 4>{}); break;
-            default: run(std::integral_constant<int, 8>{}); break;
-            }
-        } else if (smax - smin < (1ull << 29)) {
+        if (smax - smin < (1ull << 29)) {
             // The thread's loaded calls k < P / 256 become its E sort positions (any placement
             // of the inputs sorts the same); padding sorts last.
             uint64_t pk[kMaxPerThread];
@@ -662,7 +495,7 @@ __device__ __forceinline__ void one_trace(const StatsArgs &a, uint32_t r, uint32
 #pragma unroll
             for (uint32_t k = 0; k < kMaxPerThread; ++k) {
                 if (k < E) {
-                    const uint32_t i = chunk * E + k;
+                    const uint32_t i = k * kThreads + threadIdx.x;
                     key[i] = ok[k] ? ((uint64_t)rm[k] << 60) | rs[k] : kPad;
                     val[i] = ok[k] ? re[k] : 0;
                 }
@@ -705,22 +538,153 @@ __device__ __forceinline__ void one_trace(const StatsArgs &a, uint32_t r, uint32
             atomicAdd(&copy[k], s_sum[k]);
 }
 
-// MM: a bound on the number of LLMs (2, 4 or 8), so the per-LLM registers fit the workflow.
-template <int MM>
-__global__ void __launch_bounds__(kThreads) trace_sweep_kernel(StatsArgs a)
+constexpr uint32_t kSweepWaves = 4;     // traces per workgroup of the sweep, one per wave
+constexpr uint32_t kSweepBatch = 8;     // rows of 64 calls loaded together
+
+// Inclusive maximum over lanes 0..L: row shifts by 1, 2, 4 and 8, then lane 15 into rows 1 and
+// 3 and lane 31 into rows 2 and 3 (lanes a move does not reach keep 0, the identity).
+__device__ __forceinline__ uint32_t wave_prefix_max(uint32_t v)
 {
-    one_trace<kSweep, MM>(a, blockIdx.x, 0, nullptr);
+    auto step = [&](auto c, auto rm) {
+        constexpr int C = decltype(c)::value, RM = decltype(rm)::value;
+        const uint32_t o = dpp_mov<C, RM>(0u, v);
+        v = o > v ? o : v;
+    };
+    step(std::integral_constant<int, 0x111>{}, std::integral_constant<int, 0xF>{});
+    step(std::integral_constant<int, 0x112>{}, std::integral_constant<int, 0xF>{});
+    step(std::integral_constant<int, 0x114>{}, std::integral_constant<int, 0xF>{});
+    step(std::integral_constant<int, 0x118>{}, std::integral_constant<int, 0xF>{});
+    step(std::integral_constant<int, 0x142>{}, std::integral_constant<int, 0xA>{});
+    step(std::integral_constant<int, 0x143>{}, std::integral_constant<int, 0xC>{});
+    return v;
 }
 
-// One block per entry of the work list the sweep pass wrote (the grid covers every trace, and
-// blocks beyond the list's length end at once), or, without a work list, one per trace.
+struct SweepRows {
+    uint32_t m[kSweepBatch];
+    uint64_t s[kSweepBatch], e[kSweepBatch];
+};
+
+// Covered time of the traces whose calls are in order of end time (as a proxy logs them on
+// completion), without a sort: one wave per trace of at most lds_cap calls.  Walking the calls
+// backwards, the calls of LLM m after call j (ending no earlier) cover, within (-inf, e_j],
+// exactly [lo, e_j], lo their earliest start (nothing if lo > e_j); so call j adds
+// max(0, min(e_j, lo) - s_j).  The wave takes rows of 64 calls from the end: lane L of row k
+// holds call n - 1 - 64 k - L, so a call's later calls are the lower lanes of its row and the
+// rows already swept, and each load instruction reads 64 consecutive calls.  Times count back
+// from the last call's end E, a = E - s and b = E - e, in 32 bits: then call j adds
+// max(0, a_j - max(b_j, h)), h the largest a among m's later calls (0 if none) -- a prefix
+// maximum over the lanes, per LLM, joined with the maximum carried over the rows before.  A
+// trace out of end order, with a malformed call, reaching 2^60 us or spanning 2^32 us or more
+// goes to the work list instead (the sort pass reports malformed calls).  MM bounds the number
+// of LLMs (2, 4 or 8), so the per-LLM registers fit the workflow.
+template <int MM>
+__global__ void __launch_bounds__(64 * kSweepWaves) trace_sweep_kernel(StatsArgs a)
+{
+    const uint32_t lane = threadIdx.x & 63;
+    const uint32_t r = (uint32_t)__builtin_amdgcn_readfirstlane(
+        (int)(blockIdx.x * kSweepWaves + (threadIdx.x >> 6)));
+    if (r >= a.R)
+        return;                                        // uniform over the wave
+    const uint64_t lo = a.offsets[r], n64 = a.offsets[r + 1] - lo;
+    if (n64 == 0 || n64 > a.lds_cap)
+        return;                                        // empty, or the global pass takes it
+    const uint32_t n = (uint32_t)n64, M = a.M, rows = (n + 63) >> 6;
+    const uint64_t E = a.end[lo + n - 1];
+    bool bad = E >= kStartLimit;
+    auto load = [&](SweepRows &R, uint32_t k0) {
+#pragma unroll
+        for (uint32_t j = 0; j < kSweepBatch; ++j) {
+            if (k0 + j >= rows)
+                break;                                 // uniform
+            const int32_t idx = (int32_t)n - 1 - (int32_t)(64 * (k0 + j) + lane);
+            const uint64_t i = lo + (uint64_t)(idx < 0 ? 0 : idx);   // lanes past the first call
+            R.m[j] = a.llm[i];
+            R.s[j] = a.start[i];
+            R.e[j] = a.end[i];
+        }
+    };
+    uint32_t calls[MM], carry[MM];
+    uint64_t busy[MM], active[MM];
+#pragma unroll
+    for (int q = 0; q < MM; ++q) {
+        calls[q] = carry[q] = 0;
+        busy[q] = active[q] = 0;
+    }
+    uint32_t next_b = 0;                               // b of the call after the row's lane 0
+    auto sweep_rows = [&](const SweepRows &R, uint32_t k0) {
+#pragma unroll
+        for (uint32_t j = 0; j < kSweepBatch; ++j) {
+            if (k0 + j >= rows)
+                break;                                 // uniform
+            const bool valid = 64 * (k0 + j) + lane < n;
+            const uint32_t m = R.m[j];
+            const uint64_t a64 = E - R.s[j], b64 = E - R.e[j];
+            const uint32_t av = (uint32_t)a64, bv = (uint32_t)b64;
+            // In order: this call ends no later than the next one (lane - 1, or the previous
+            // row's lane 63).
+            const uint32_t bn = dpp_mov<0x138>(next_b, bv);
+            const bool good = m < M && (a64 >> 32) == 0 && (b64 >> 32) == 0 && av >= bv &&
+                              bv >= bn;
+            bad = bad || __ballot(valid && !good) != 0;
+            next_b = lane63(bv);
+            uint32_t h = 0;
+#pragma unroll
+            for (int q = 0; q < MM; ++q) {
+                if ((uint32_t)q >= M)
+                    break;
+                const uint32_t v = wave_prefix_max(valid && m == (uint32_t)q ? av : 0u);
+                const uint32_t ex = dpp_mov<0x138>(0u, v);   // lanes below this one
+                const uint32_t later = ex > carry[q] ? ex : carry[q];
+                h = m == (uint32_t)q ? later : h;
+                const uint32_t tot = lane63(v);
+                carry[q] = tot > carry[q] ? tot : carry[q];
+            }
+            const uint32_t t = bv > h ? bv : h;
+            const uint32_t act = av > t ? av - t : 0u;
+#pragma unroll
+            for (int q = 0; q < MM; ++q) {
+                if (valid && m == (uint32_t)q) {
+                    calls[q] += 1;
+                    busy[q] += av - bv;
+                    active[q] += act;
+                }
+            }
+        }
+    };
+    // A batch of rows is loaded at once (up to 8 x 1.25 KB in flight per wave), then swept;
+    // the other waves of the SIMD sweep while this one waits.
+    for (uint32_t k0 = 0; k0 < rows && !bad; k0 += kSweepBatch) {
+        SweepRows R;
+        load(R, k0);
+        sweep_rows(R, k0);
+    }
+    if (bad) {
+        if (lane == 0)
+            a.work[atomicAdd(a.work_count, 1u)] = r;
+        return;
+    }
+    unsigned long long *copy = a.totals + (uint64_t)(r % kStatsCopies) * kStatsCopyStride;
+#pragma unroll
+    for (int q = 0; q < MM; ++q)
+        if ((uint32_t)q < M)
+            wave_add_sums((uint32_t)q, calls[q], busy[q], active[q], copy);
+}
+
+// Sorts the traces of the work list the sweep wrote, a grid of blocks taking its entries in
+// turn; without a work list, one block per trace.
 __global__ void __launch_bounds__(kThreads) trace_sort_kernel(StatsArgs a)
 {
     extern __shared__ __align__(8) unsigned char s_dyn[];
-    if (!a.work)
+    if (!a.work) {
         one_trace<kSort>(a, blockIdx.x, 0, s_dyn);
-    else if (blockIdx.x < *a.work_count)
-        one_trace<kSort>(a, a.work[blockIdx.x], 0, s_dyn);
+        return;
+    }
+    const uint32_t listed = *a.work_count;
+    for (uint32_t w = blockIdx.x; w < listed; w += gridDim.x) {
+        if (w != blockIdx.x)
+            __syncthreads();                           // the previous trace's sums are read
+        one_trace<kSort>(a, a.work[w], 0, s_dyn);
+    }
 }
 
 __global__ void __launch_bounds__(kThreads) trace_long_kernel(StatsArgs a)
@@ -785,6 +749,7 @@ hipError_t launch_trace_stats(uint32_t M, uint32_t R, const uint64_t *offsets, c
     StatsArgs a;
     a.M = M;
     a.lds_cap = lds_cap;
+    a.R = R;
     a.offsets = offsets;
     a.llm = llm;
     a.start = start;
@@ -797,18 +762,21 @@ hipError_t launch_trace_stats(uint32_t M, uint32_t R, const uint64_t *offsets, c
     a.work = sweep ? work : nullptr;
     a.work_count = reinterpret_cast<uint32_t *>(totals + kStatsTotalsWords + 1);
     if (sweep) {
+        const dim3 grid((R + kSweepWaves - 1) / kSweepWaves), block(64 * kSweepWaves);
         if (M <= 2)
-            hipLaunchKernelGGL(trace_sweep_kernel<2>, dim3(R), dim3(kThreads), 0, st, a);
+            hipLaunchKernelGGL(trace_sweep_kernel<2>, grid, block, 0, st, a);
         else if (M <= 4)
-            hipLaunchKernelGGL(trace_sweep_kernel<4>, dim3(R), dim3(kThreads), 0, st, a);
+            hipLaunchKernelGGL(trace_sweep_kernel<4>, grid, block, 0, st, a);
         else
-            hipLaunchKernelGGL(trace_sweep_kernel<ALP_MAX_LLMS>, dim3(R), dim3(kThreads), 0, st,
-                               a);
+            hipLaunchKernelGGL(trace_sweep_kernel<ALP_MAX_LLMS>, grid, block, 0, st, a);
         if ((e = hipGetLastError()) != hipSuccess)
             return e;
     }
+    // The work list's length is known only on the device: a grid of at most kSortBlocks
+    // blocks takes its entries in turn (an empty list costs one short launch).
     const size_t lds = (size_t)2 * lds_cap * sizeof(uint64_t);
-    hipLaunchKernelGGL(trace_sort_kernel, dim3(R), dim3(kThreads), lds, st, a);
+    const uint32_t sort_blocks = sweep && R > kSortBlocks ? kSortBlocks : R;
+    hipLaunchKernelGGL(trace_sort_kernel, dim3(sort_blocks), dim3(kThreads), lds, st, a);
     if ((e = hipGetLastError()) != hipSuccess)
         return e;
     if (num_long) {

@@ -147,14 +147,17 @@ def test_every_sort_size_and_input_order(ctx):
 
 
 def test_traces_in_end_order(ctx):
-    """Traces already in order of end time (as logged on completion) take a sweep without a sort;
-    ties of end time, zero-length and nested calls, all 8 LLMs, spans above and below 2^29 us, at
-    each chunk size (1, 2, 4 and 8 calls per thread).  Copies with one pair of neighbours swapped
-    (inside a thread's chunk, across two threads, across two waves) must take the sort and agree."""
+    """Traces already in order of end time (as logged on completion) take a sweep without a sort
+    (one wave per trace, rows of 64 calls from the end); ties of end time, zero-length and nested
+    calls, all 8 LLMs, spans below 2^29 us, just below 2^32 us (the sweep's 32-bit times) and
+    above, at row boundaries (1, 63, 64, 65, ... 2,048 calls).  Copies with one pair of
+    neighbours swapped (inside a row, across two rows, at either end) must take the sort and
+    agree.  Traces whose calls lie 2^32 - 1 and 2^32 us before the last end, or whose last call
+    ends at 2^60 us or later, must agree as well."""
     rng = np.random.default_rng(31)
     traces = []
-    for n in (1, 2, 3, 255, 256, 257, 511, 512, 513, 1023, 1024, 1025, 2047, 2048):
-        for span_bits in (20, 34):
+    for n in (1, 2, 3, 63, 64, 65, 255, 256, 257, 511, 512, 513, 1023, 1024, 1025, 2047, 2048):
+        for span_bits in (20, 31, 34):
             m = rng.integers(0, 8, n)
             s = rng.integers(0, 1 << span_bits, n)
             d = rng.integers(0, 40_000, n)
@@ -165,13 +168,21 @@ def test_traces_in_end_order(ctx):
             idx = np.lexsort((s, e))
             calls = [(int(a), int(b), int(c)) for a, b, c in zip(m[idx], s[idx], e[idx])]
             traces.append(calls)
-            for pos in (0, 63, 127, 255, 511, n // 2):      # swap calls pos and pos + 1
+            for pos in (0, 63, 127, 255, 511, n // 2, n - 2, n - 65, n - 66, n - 129):
+                # swap calls pos and pos + 1
+                if pos < 0:
+                    continue
                 if pos + 1 < n and calls[pos][2] != calls[pos + 1][2]:
                     sw = list(calls)
                     sw[pos], sw[pos + 1] = sw[pos + 1], sw[pos]
                     traces.append(sw)
     # one LLM only, nested calls all ending together
     traces.append([(0, 1000 - i, 1000) for i in range(700)])
+    # the first call starts 2^32 - 1 us (sweep) or 2^32 us (sort) before the last end
+    for last in ((1 << 32) - 1, 1 << 32):
+        traces.append([(0, 0, 5), (1, 3, 9), (0, last - 10, last - 2), (1, last - 7, last)])
+    # the last call ends at 2^60 us or later (starts below it): the sort takes the trace
+    traces.append([(0, (1 << 60) - 10, (1 << 60) - 5), (1, (1 << 60) - 8, (1 << 60) + 3)])
     _same(ctx, 8, *_pack(traces))
 
 
