@@ -697,43 +697,56 @@ def run_stats(args, alp):
     from workloads.traces import make_traces
     tr = make_traces("beam", STATS_TRACES, 0)
     calls = int(len(tr["llm"]))
-    dev = [torch.from_numpy(np.ascontiguousarray(tr[k]).view(t)).to("cuda:0")
-           for k, t in (("offsets", np.int64), ("llm", np.int32), ("start", np.int64),
-                        ("end", np.int64))]
-    torch.cuda.synchronize()
     ctx = alp.StatsContext(0)
 
-    def step():
-        return ctx.compute(tr["M"], *dev)
+    def timed(order):
+        """Median kernel time (HIP events around the launches) over the timed steps, the wall
+        time of those steps and the last result, for the calls taken in the given order."""
+        dev = [torch.from_numpy(np.ascontiguousarray(tr[k][order]).view(t)).to("cuda:0")
+               for k, t in (("llm", np.int32), ("start", np.int64), ("end", np.int64))]
+        off = torch.from_numpy(tr["offsets"].view(np.int64)).to("cuda:0")
+        torch.cuda.synchronize()
+        for _ in range(args.warmup):
+            ctx.compute(tr["M"], off, *dev)
+        ctx.set_timing(True)
+        kernel_ms = []
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            out = ctx.compute(tr["M"], off, *dev)
+            kernel_ms.append(ctx.time_ms())
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+        ctx.set_timing(False)
+        return float(np.median(kernel_ms)), elapsed, out
 
-    import torch as _t
-    for _ in range(args.warmup):
-        step()
-    ctx.set_timing(True)
-    kernel_ms = []
-    _t.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        out = step()
-        kernel_ms.append(ctx.time_ms())
-    _t.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    ctx.set_timing(False)
-    k_s = float(np.mean(kernel_ms)) / 1e3
     alg_bytes = 20 * calls + 8 * (STATS_TRACES + 1)
-    achieved = alg_bytes / k_s
-    lengths = np.diff(tr["offsets"].astype(np.int64))
+    # As logged (in order of end time): the sweep without a sort.
+    k_ms, elapsed, out = timed(np.arange(calls))
+    # The same calls shuffled within each trace: every trace is sorted (the context sees that the
+    # traces are not in end order and sorts directly, checking the order again every 8th call).
+    rng = np.random.default_rng(5)
+    off = tr["offsets"].astype(np.int64)
+    perm = np.concatenate([lo + rng.permutation(hi - lo) for lo, hi in zip(off[:-1], off[1:])])
+    s_ms, s_elapsed, s_out = timed(perm)
+    if not (s_out == out).all():
+        raise SystemExit("shuffled traces gave different statistics")
+    achieved = alg_bytes / (k_ms / 1e3)
+    lengths = np.diff(off)
     config = {"workload": f"workflow statistics (Section 4 step 2) of {STATS_TRACES} synthetic "
                           f"beam-search traces: 2 LLMs, {calls:,} calls, 24-843 generator calls "
                           "per request, 3 concurrent beams",
               "traces": STATS_TRACES, "calls": calls, "longest_trace": int(lengths.max()),
               "n_milli": [int(v) for v in out["n_milli"]],
-              "p_milli": [int(v) for v in out["p_milli"]]}
+              "p_milli": [int(v) for v in out["p_milli"]],
+              "shuffled": {"order": "calls shuffled within each trace (sorted on the GPU)",
+                           "value": calls * args.steps / s_elapsed, "unit": "trace calls/s",
+                           "kernel_ms": s_ms, "frac": alg_bytes / (s_ms / 1e3) / HBM_PEAK}}
     roofline = {"bound": "hbm", "achieved": achieved / 1e9, "peak": HBM_PEAK / 1e9,
                 "unit": "GB/s", "frac": achieved / HBM_PEAK,
                 "traffic": _traffic(_kernel_digest(STATS_SOURCES), "stats", STATS_TRAFFIC_FILE),
-                "kernel": "trace statistics (all kernels)", "kernel_ms": k_s * 1e3,
-                "bytes_per_call": 20}
+                "kernel": "trace statistics (all kernels)", "kernel_ms": k_ms,
+                "kernel_ms_stat": "median over the timed steps", "bytes_per_call": 20}
     cpu = None if args.no_cpu_baseline else cpu_baseline_stats(tr, args.cpu_seconds)
     ctx.close()
     return _line(args, calls * args.steps / elapsed, "trace calls/s", elapsed, config, roofline,

@@ -1547,8 +1547,11 @@ struct alp_stats_ctx {
     int device = 0;
     hipStream_t stream = nullptr;
     DevBuf totals, long_list, long_base, scratch, work;
-    alp_stats_t *host_out = nullptr;        // mapped pinned: results
+    alp_stats_t *host_out = nullptr;        // mapped pinned: results, then the StatsTail
     alp_stats_t *host_out_dev = nullptr;
+    // Whether the device totals and counters are zero (the kernels leave them so); false for
+    // fresh memory and after a failed launch, when the next call zeroes them first.
+    bool counters_clean = false;
     uint64_t *offsets = nullptr;            // pinned: the trace offsets, read for planning
     size_t offsets_cap = 0;                 // entries
     int timing = 0;
@@ -1575,14 +1578,14 @@ int32_t alp_stats_create(alp_stats_ctx **out, int32_t device, void *hip_stream)
     DeviceGuard guard(device);
     hipError_t e = guard.status;
     if (e == hipSuccess)
-        e = alloc_pinned((void **)&c->host_out, ALP_MAX_LLMS * sizeof(alp_stats_t),
+        e = alloc_pinned((void **)&c->host_out, (ALP_MAX_LLMS + 1) * sizeof(alp_stats_t),
                          hipHostMallocMapped);
     if (e == hipSuccess)
         e = hipHostGetDevicePointer((void **)&c->host_out_dev, c->host_out, 0);
     for (int k = 0; k < 2 && e == hipSuccess; ++k)
         e = hipEventCreate(&c->ev[k]);
     if (e == hipSuccess)
-        e = c->totals.ensure((alp::kStatsTotalsWords + 2) * sizeof(uint64_t));
+        e = c->totals.ensure((alp::kStatsTotalsWords + alp::kStatsTailWords) * sizeof(uint64_t));
     if (e != hipSuccess) {
         alp_stats_free(c);
         return hip_fail(e, "statistics context");
@@ -1668,23 +1671,25 @@ int32_t alp_trace_stats(alp_stats_ctx *c, uint32_t num_llms, uint32_t num_traces
         --c->direct_left;
     if (c->timing && (e = hipEventRecord(c->ev[0], c->stream)) != hipSuccess)
         return hip_fail(e, "hipEventRecord");
+    const bool zero_first = !c->counters_clean;
+    c->counters_clean = false;                       // until the kernels have run to the end
     if ((e = alp::launch_trace_stats(num_llms, num_traces, offsets, llm, start_us, end_us, lds_cap,
                                      (uint32_t)longs.size(), (const uint32_t *)c->long_list.ptr,
                                      (const uint64_t *)c->long_base.ptr, (uint64_t *)c->scratch.ptr,
-                                     totals, (uint32_t *)c->work.ptr, sweep, c->host_out_dev,
-                                     c->stream)) != hipSuccess)
+                                     totals, (uint32_t *)c->work.ptr, sweep, zero_first,
+                                     c->host_out_dev, c->stream)) != hipSuccess)
         return hip_fail(e, "statistics launch");
     if (c->timing && (e = hipEventRecord(c->ev[1], c->stream)) != hipSuccess)
         return hip_fail(e, "hipEventRecord");
-    // The flags word, then the work list's length.
-    uint64_t tail[2] = {0, 0};
-    if ((e = hipMemcpyAsync(tail, totals + alp::kStatsTotalsWords, sizeof(tail),
-                            hipMemcpyDeviceToHost, c->stream)) != hipSuccess ||
-        (e = hipStreamSynchronize(c->stream)) != hipSuccess)
+    if ((e = hipStreamSynchronize(c->stream)) != hipSuccess)
         return hip_fail(e, "statistics");
-    const uint32_t host_flags = (uint32_t)tail[0];
+    c->counters_clean = true;
+    // The status and the work list's length, written by the last block after the records.
+    alp::StatsTail tail;
+    memcpy(&tail, c->host_out + ALP_MAX_LLMS, sizeof(tail));
+    const uint32_t host_flags = tail.flags;
     const uint64_t short_traces = num_traces - longs.size();
-    if (sweep && 2 * (tail[1] & 0xFFFFFFFFu) > short_traces)
+    if (sweep && 2 * (uint64_t)tail.listed > short_traces)
         c->direct_left = kStatsProbeEvery - 1;
     if (c->timing && (e = hipEventElapsedTime(&c->last_ms, c->ev[0], c->ev[1])) != hipSuccess)
         return hip_fail(e, "hipEventElapsedTime");

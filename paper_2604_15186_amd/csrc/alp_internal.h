@@ -212,21 +212,33 @@ static_assert(sizeof(alp_pruned_t) == 64 && offsetof(alp_pruned_t, fraction_vect
               "alp_pruned_t layout");
 
 // Workflow statistics (see alp_trace_stats).  Traces up to lds_cap calls (a power of two,
-// 256..2048) are sorted in LDS; the num_long others (long_traces[]) in scratch, trace k at
-// 2 * long_base[k] words (2 * pow2(length) words each).  totals: kStatsTotalsWords + 2 words:
-// kStatsCopies copies of the per-LLM sums, kStatsCopyStride words apart (trace r adds to copy
-// r mod kStatsCopies, so that thousands of traces do not queue on the same atomic words), then
-// the status flags, then the length of the work list.  sweep: traces in end order are swept
-// without a sort and the others listed in work (R entries) for the sort pass; otherwise every
-// trace is sorted.  Writes out[0..M).
+// 256..2048) are swept or sorted in LDS; the num_long others (long_traces[]) are sorted in
+// scratch, trace k at 2 * long_base[k] words (2 * pow2(length) words each).  totals:
+// kStatsTotalsWords + kStatsTailWords words: kStatsCopies copies of the per-LLM sums,
+// kStatsCopyStride words apart (trace r adds to copy r mod kStatsCopies, so that thousands of
+// traces do not queue on the same atomic words), then the status flags (one word), the length
+// of the work list and the count of finished slots (the low and high half of the next), and
+// kStatsSlots 32-bit counters of finished blocks.  They must be zero when the kernels start; the last block leaves them zero,
+// so zero_first is needed only for fresh memory or after a failed launch.  sweep: traces in end order are swept without a sort and the others listed in work
+// (R entries) for the sort pass; otherwise every trace is sorted.  Writes out[0..M) and the
+// StatsTail at out[ALP_MAX_LLMS].
 constexpr uint32_t kStatsCopies = 64;
 constexpr uint32_t kStatsCopyStride = 32;                 // >= 3 * ALP_MAX_LLMS, 256 B apart
 constexpr uint32_t kStatsTotalsWords = kStatsCopies * kStatsCopyStride;
+constexpr uint32_t kStatsSlots = 64;
+constexpr uint32_t kStatsTailWords = 2 + kStatsSlots / 2;
+struct StatsTail {
+    uint32_t flags;                   // status bits (see alp_trace_stats)
+    uint32_t listed;                  // traces the sweep left to the sort pass
+    uint32_t pad[6];
+};
+static_assert(sizeof(StatsTail) == sizeof(alp_stats_t), "the tail takes one record's place");
 hipError_t launch_trace_stats(uint32_t M, uint32_t R, const uint64_t *offsets, const uint32_t *llm,
                               const uint64_t *start, const uint64_t *end, uint32_t lds_cap,
                               uint32_t num_long, const uint32_t *long_traces,
                               const uint64_t *long_base, uint64_t *scratch, uint64_t *totals,
-                              uint32_t *work, bool sweep, alp_stats_t *out, hipStream_t st);
+                              uint32_t *work, bool sweep, bool zero_first, alp_stats_t *out,
+                              hipStream_t st);
 
 // One allocation to place: budget, LLM count, whether the search found it, per-LLM choices.
 struct PlaceIn {

@@ -8,7 +8,8 @@
 //         active.  n_m and p_m are reported in thousandths, rounded down.
 //
 // Kernels:
-//   stats_init_kernel        zeroes the per-LLM totals, the error flags and the work-list count.
+//   stats_init_kernel        zeroes the per-LLM totals, the error flags and the counters (once;
+//                            afterwards the last block of each computation leaves them zeroed).
 //   trace_sweep_kernel<MM>   one wave per trace of at most 2,048 calls (MM bounds the number of
 //                            LLMs, so the per-LLM state fits in few registers).  A trace already
 //                            in order of end time (calls logged on completion) is swept backwards
@@ -23,10 +24,10 @@
 //                            furthest end of the same LLM's earlier intervals.
 //   trace_long_kernel        traces beyond 2,048 calls, sorted the same way in a global scratch
 //                            region.
-//   In each, per-LLM call counts, durations and covered time are summed per block and added to
+//   In each, per-LLM call counts, durations and covered time are summed per trace and added to
 //   one of kStatsCopies copies of the totals with 64-bit atomics (integer sums: the result does
-//   not depend on their order).
-//   stats_finish_kernel      n and p per LLM from the totals, written with the error flags.
+//   not depend on their order).  The last block of the sort and long passes computes n and p
+//   per LLM from the totals and writes them with the error flags.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -43,7 +44,7 @@ constexpr uint64_t kPad = ~0ull;                       // sorts after every real
 constexpr uint64_t kStartLimit = 1ull << 60;
 constexpr uint64_t kDurationLimit = 1ull << 32;
 constexpr uint32_t kThreads = 256;
-constexpr uint32_t kSortBlocks = 2048;                 // grid of the work-list sort
+constexpr uint32_t kSortBlocks = 1024;                 // grid of the work-list sort
 
 __global__ void stats_init_kernel(uint64_t *__restrict__ totals, uint32_t words)
 {
@@ -395,6 +396,10 @@ struct StatsArgs {
     uint32_t *flags;
     uint32_t *work;                   // the sweep appends, kSort reads: traces needing the sort
     uint32_t *work_count;
+    uint32_t *done;                   // participants of the sort and long passes done
+    uint32_t *slot_done;              // kStatsSlots counters of those participants
+    uint32_t sort_grid, num_long;     // blocks of the sort and long launches
+    alp_stats_t *out;                 // M records, then the StatsTail
 };
 
 // Statistics of trace r (slot = the block's trace slot in long_base for kLong) by one block.
@@ -670,67 +675,123 @@ __global__ void __launch_bounds__(64 * kSweepWaves) trace_sweep_kernel(StatsArgs
             wave_add_sums((uint32_t)q, calls[q], busy[q], active[q], copy);
 }
 
+
+// Called, once its traces are summed, by every block of the sort and long passes that had
+// work: participant i of P.  The last of them (over both launches) takes the totals -- reading
+// each word and zeroing it for the next call, as it zeroes the flags, the work-list length and
+// the counters -- and writes n and p per LLM, then the status and the work-list length for the
+// host.  Participants count themselves in kStatsSlots counters (i mod kStatsSlots) and the last
+// of each slot in one more, so that no counter takes more than a share of the increments.
+// Every sum, flag and count is added and read by atomics, performed where all blocks see them;
+// a block's own atomics have completed (its vector memory count drained) before it counts
+// itself, so no cache needs writing back or invalidating (a device-wide fence per block would
+// cost both for every block).  Status bits: 1 llm out of range, 2 end before start, 4 start or
+// duration out of range, 8 a result beyond 2^31 - 1 (it could not be loaded as an ALP input).
+__device__ __forceinline__ void finish_block(const StatsArgs &a, uint32_t i, uint32_t P)
+{
+    __shared__ uint32_t s_last, s_flags;
+    __shared__ unsigned long long s_tot[3 * ALP_MAX_LLMS];
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this thread's atomics are done
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const uint32_t slot = i % kStatsSlots;
+        const uint32_t in_slot = (P - slot + kStatsSlots - 1) / kStatsSlots;
+        uint32_t last = 0;
+        if (atomicAdd(&a.slot_done[slot], 1u) == in_slot - 1) {
+            (void)atomicExch(&a.slot_done[slot], 0u);
+            const uint32_t slots = P < kStatsSlots ? P : kStatsSlots;
+            if (atomicAdd(a.done, 1u) == slots - 1) {
+                (void)atomicExch(a.done, 0u);
+                last = 1;
+            }
+        }
+        s_last = last;
+        s_flags = 0;
+    }
+    if (threadIdx.x < 3 * ALP_MAX_LLMS)
+        s_tot[threadIdx.x] = 0;
+    __syncthreads();
+    if (!s_last)
+        return;                                        // uniform over the block
+    const uint32_t W = 3 * a.M;
+    for (uint32_t k = threadIdx.x; k < kStatsCopies * W; k += kThreads) {
+        const uint32_t c = k / W, f = k - c * W;
+        const unsigned long long v =
+            atomicExch(a.totals + (uint64_t)c * kStatsCopyStride + f, 0ull);
+        if (v)
+            atomicAdd(&s_tot[f], v);
+    }
+    __syncthreads();
+    const uint32_t m = threadIdx.x;
+    if (m < a.M) {
+        const uint64_t calls = s_tot[3 * m], busy = s_tot[3 * m + 1], active = s_tot[3 * m + 2];
+        uint64_t n = calls * 1000u / a.R, p;
+        if (calls == 0)
+            p = 0;
+        else if (active == 0)
+            p = 1000;
+        else if (busy >= (1ull << 53))
+            p = ~0ull;
+        else
+            p = busy * 1000u / active;
+        if (n >= (1u << 31) || p >= (1u << 31)) {
+            atomicOr(&s_flags, 8u);
+            n = n >= (1u << 31) ? 0 : n;
+            p = p >= (1u << 31) ? 0 : p;
+        }
+        alp_stats_t st;
+        st.n_milli = (uint32_t)n;
+        st.p_milli = (uint32_t)p;
+        st.calls = calls;
+        st.busy_us = busy;
+        st.active_us = active;
+        a.out[m] = st;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        StatsTail t = {};
+        t.flags = atomicExch(a.flags, 0u) | s_flags;
+        t.listed = atomicExch(a.work_count, 0u);
+        *reinterpret_cast<StatsTail *>(a.out + ALP_MAX_LLMS) = t;
+    }
+}
+
 // Sorts the traces of the work list the sweep wrote, a grid of blocks taking its entries in
 // turn; without a work list, one block per trace.
+// Blocks of the sort launch that have work: every block without a work list; with one, the
+// first min(listed, grid) blocks, and block 0 always (it finishes when nothing is listed).
+__device__ __forceinline__ uint32_t sort_participants(const StatsArgs &a)
+{
+    if (!a.work)
+        return a.sort_grid;
+    const uint32_t listed = *a.work_count;
+    return listed == 0 ? 1u : (listed < a.sort_grid ? listed : a.sort_grid);
+}
+
 __global__ void __launch_bounds__(kThreads) trace_sort_kernel(StatsArgs a)
 {
     extern __shared__ __align__(8) unsigned char s_dyn[];
+    const uint32_t P = sort_participants(a);
+    if (blockIdx.x >= P)
+        return;                                        // nothing listed for this block
     if (!a.work) {
         one_trace<kSort>(a, blockIdx.x, 0, s_dyn);
-        return;
+    } else {
+        const uint32_t listed = *a.work_count;
+        for (uint32_t w = blockIdx.x; w < listed; w += gridDim.x) {
+            if (w != blockIdx.x)
+                __syncthreads();                       // the previous trace's sums are read
+            one_trace<kSort>(a, a.work[w], 0, s_dyn);
+        }
     }
-    const uint32_t listed = *a.work_count;
-    for (uint32_t w = blockIdx.x; w < listed; w += gridDim.x) {
-        if (w != blockIdx.x)
-            __syncthreads();                           // the previous trace's sums are read
-        one_trace<kSort>(a, a.work[w], 0, s_dyn);
-    }
+    finish_block(a, blockIdx.x, P + a.num_long);
 }
 
 __global__ void __launch_bounds__(kThreads) trace_long_kernel(StatsArgs a)
 {
     one_trace<kLong>(a, a.long_traces[blockIdx.x], blockIdx.x, nullptr);
-}
-
-// n and p per LLM from the totals (calls, busy, active per LLM, summed over the copies), R
-// traces.  Status bits in
-// flags: 1 llm out of range, 2 end before start, 4 start or duration out of range, 8 a result
-// beyond 2^31 - 1 (it could not be loaded as an ALP input).
-__global__ void stats_finish_kernel(uint32_t M, uint32_t R,
-                                    const unsigned long long *__restrict__ totals,
-                                    uint32_t *__restrict__ flags, alp_stats_t *__restrict__ out)
-{
-    const uint32_t m = threadIdx.x;
-    if (m >= M)
-        return;
-    uint64_t calls = 0, busy = 0, active = 0;
-    for (uint32_t c = 0; c < kStatsCopies; ++c) {
-        const unsigned long long *t = totals + (uint64_t)c * kStatsCopyStride + 3 * m;
-        calls += t[0];
-        busy += t[1];
-        active += t[2];
-    }
-    uint64_t n = calls * 1000u / R, p;
-    if (calls == 0)
-        p = 0;
-    else if (active == 0)
-        p = 1000;
-    else if (busy >= (1ull << 53))
-        p = ~0ull;
-    else
-        p = busy * 1000u / active;
-    if (n >= (1u << 31) || p >= (1u << 31)) {
-        atomicOr(flags, 8u);
-        n = n >= (1u << 31) ? 0 : n;
-        p = p >= (1u << 31) ? 0 : p;
-    }
-    alp_stats_t st;
-    st.n_milli = (uint32_t)n;
-    st.p_milli = (uint32_t)p;
-    st.calls = calls;
-    st.busy_us = busy;
-    st.active_us = active;
-    out[m] = st;
+    const uint32_t P = sort_participants(a);           // the list is still intact here
+    finish_block(a, P + blockIdx.x, P + a.num_long);
 }
 
 }  // namespace
@@ -739,13 +800,16 @@ hipError_t launch_trace_stats(uint32_t M, uint32_t R, const uint64_t *offsets, c
                               const uint64_t *start, const uint64_t *end, uint32_t lds_cap,
                               uint32_t num_long, const uint32_t *long_traces,
                               const uint64_t *long_base, uint64_t *scratch, uint64_t *totals,
-                              uint32_t *work, bool sweep, alp_stats_t *out, hipStream_t st)
+                              uint32_t *work, bool sweep, bool zero_first, alp_stats_t *out,
+                              hipStream_t st)
 {
-    // totals: the copies of the sums, then the flags word, then the work-list count.
-    hipLaunchKernelGGL(stats_init_kernel, dim3(1), dim3(256), 0, st, totals, kStatsTotalsWords + 2);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess)
-        return e;
+    hipError_t e;
+    if (zero_first) {
+        hipLaunchKernelGGL(stats_init_kernel, dim3(1), dim3(256), 0, st, totals,
+                           kStatsTotalsWords + kStatsTailWords);
+        if ((e = hipGetLastError()) != hipSuccess)
+            return e;
+    }
     StatsArgs a;
     a.M = M;
     a.lds_cap = lds_cap;
@@ -761,6 +825,9 @@ hipError_t launch_trace_stats(uint32_t M, uint32_t R, const uint64_t *offsets, c
     a.flags = reinterpret_cast<uint32_t *>(totals + kStatsTotalsWords);
     a.work = sweep ? work : nullptr;
     a.work_count = reinterpret_cast<uint32_t *>(totals + kStatsTotalsWords + 1);
+    a.done = reinterpret_cast<uint32_t *>(totals + kStatsTotalsWords + 1) + 1;
+    a.slot_done = reinterpret_cast<uint32_t *>(totals + kStatsTotalsWords + 2);
+    a.out = out;
     if (sweep) {
         const dim3 grid((R + kSweepWaves - 1) / kSweepWaves), block(64 * kSweepWaves);
         if (M <= 2)
@@ -776,6 +843,8 @@ hipError_t launch_trace_stats(uint32_t M, uint32_t R, const uint64_t *offsets, c
     // blocks takes its entries in turn (an empty list costs one short launch).
     const size_t lds = (size_t)2 * lds_cap * sizeof(uint64_t);
     const uint32_t sort_blocks = sweep && R > kSortBlocks ? kSortBlocks : R;
+    a.sort_grid = sort_blocks;
+    a.num_long = num_long;
     hipLaunchKernelGGL(trace_sort_kernel, dim3(sort_blocks), dim3(kThreads), lds, st, a);
     if ((e = hipGetLastError()) != hipSuccess)
         return e;
@@ -784,8 +853,7 @@ hipError_t launch_trace_stats(uint32_t M, uint32_t R, const uint64_t *offsets, c
         if ((e = hipGetLastError()) != hipSuccess)
             return e;
     }
-    hipLaunchKernelGGL(stats_finish_kernel, dim3(1), dim3(64), 0, st, M, R, a.totals, a.flags, out);
-    return hipGetLastError();
+    return hipSuccess;
 }
 
 }  // namespace alp
