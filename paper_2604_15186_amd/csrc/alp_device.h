@@ -422,9 +422,13 @@ __device__ __forceinline__ OptionTerm option_term_from(const SpaceDev &sp, uint6
     if (t.thr) {
         uint64_t ell = lat[0];
         if (r > rate[0]) {
-            uint32_t k = 1;
-            while (r > rate[k])
-                ++k;
+            // The segment [rate[k-1], rate[k]] holding r: k counts the points below r (rates
+            // ascend strictly and r <= rate[K-1]); the K reads are independent, so they are
+            // in flight together rather than one after another.
+            uint32_t k = 0;
+#pragma unroll
+            for (uint32_t q = 0; q < ALP_MAX_POINTS; ++q)
+                k += q < sp.K && rate[q] < r ? 1u : 0u;
             const uint64_t r0 = rate[k - 1], r1 = rate[k];
             ell = udiv_u64_u32((uint64_t)lat[k - 1] * (r1 - r) + (uint64_t)lat[k] * (r - r0),
                                r1 - r0);
@@ -490,9 +494,9 @@ __device__ __forceinline__ void write_fused_result(const SpaceDev &sp, uint64_t 
 // End of a one-launch block: the block's lowest (L, x) (x < 2^32) joins the item's word by an
 // atomic maximum of ~(L << 32 | x), performed (returned) before the block counts itself.  Blocks
 // count in groups of kFusedGroup (sub / kFusedGroup); the last block of a group counts the group
-// in the item's counter, and the block completing the last group reads the item's lowest
-// candidate from the word, resets the words and writes the result.  `hint` and `held` as in
-// block_finish.
+// in the item's counter (an item of one group counts its blocks there directly), and the block
+// completing the last group reads the item's lowest candidate from the word, resets the words
+// and writes the result.  `hint` and `held` as in block_finish.
 __device__ __forceinline__ void block_finish_fused(uint32_t L, uint64_t x, uint32_t item,
                                                    uint32_t sub, uint32_t blocks_per_item,
                                                    const FinishArgs &fa, const FusedArgs &fz,
@@ -519,9 +523,12 @@ __device__ __forceinline__ void block_finish_fused(uint32_t L, uint64_t x, uint3
         const uint32_t in_group = g + 1 < groups ? kFusedGroup : blocks_per_item - g * kFusedGroup;
         uint32_t *gd = fz.group_done + (uint64_t)item * groups + g;
         last_block = 0;
-        if (atomicAdd(gd, 1u) == in_group - 1) {
-            (void)atomicExch(gd, 0u);              // the group's count, 0 for the next launch
-            if (atomicAdd(&fz.done[item], 1u) == groups - 1) {
+        // One group: the blocks count in the item's counter directly (one atomic fewer on the
+        // way to the result).
+        if (groups == 1 || atomicAdd(gd, 1u) == in_group - 1) {
+            if (groups > 1)
+                (void)atomicExch(gd, 0u);          // the group's count, 0 for the next launch
+            if (atomicAdd(&fz.done[item], 1u) == (groups > 1 ? groups : blocks_per_item) - 1) {
                 s_word = atomicExch(&fz.best[item], 0ull);
                 (void)atomicExch(&fz.done[item], 0u);
                 last_block = 1;

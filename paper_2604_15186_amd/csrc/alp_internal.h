@@ -124,7 +124,7 @@ struct FusedArgs {
 };
 // Blocks of an item counted together before the item's count (two-level counting, so that at
 // most this many blocks update one counter word).
-constexpr uint32_t kFusedGroup = 32;
+constexpr uint32_t kFusedGroup = 64;
 
 // What the option-term kernel resets for the scan that follows it: per item, the finished-block
 // counter (done = 0) and the smallest block latency (best = kNoLatency, if best is set); every
