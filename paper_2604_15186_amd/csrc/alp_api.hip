@@ -1320,14 +1320,20 @@ int32_t alp_place(alp_ctx *ctx, uint32_t count, const alp_result_t *allocations,
     if (!allocations || !gpu_budget || !out)
         return fail(ALP_EINVAL, "allocations, gpu_budget or out is NULL");
     const alp_space_t &sp = ctx->space;
+    // Budgets of at most 16 GPUs first (four to a wave), then the others.
     std::vector<alp::PlaceIn> in(count);
+    uint32_t small = 0;
+    for (uint32_t i = 0; i < count; ++i)
+        small += gpu_budget[i] <= 16;
+    uint32_t next_small = 0, next_large = small;
     for (uint32_t i = 0; i < count; ++i) {
         const alp_result_t &r = allocations[i];
-        alp::PlaceIn &p = in[i];
-        memset(&p, 0, sizeof(p));
         if (gpu_budget[i] > ALP_PLACE_MAX_GPUS)
             return fail(ALP_EINVAL, "allocation %u: %u GPUs, at most %u", i, gpu_budget[i],
                         ALP_PLACE_MAX_GPUS);
+        alp::PlaceIn &p = in[gpu_budget[i] <= 16 ? next_small++ : next_large++];
+        memset(&p, 0, sizeof(p));
+        p.dst = i;
         p.gpus = (uint8_t)gpu_budget[i];
         p.llms = (uint8_t)sp.num_llms;
         p.feasible = r.status == ALP_OK;
@@ -1362,7 +1368,8 @@ int32_t alp_place(alp_ctx *ctx, uint32_t count, const alp_result_t *allocations,
         return hip_fail(e, "copy allocations");
     if (ctx->timing && (e = hipEventRecord(ctx->ev[1], ctx->stream)) != hipSuccess)
         return hip_fail(e, "hipEventRecord");
-    if ((e = alp::launch_place(sp.units_per_gpu, count, (const alp::PlaceIn *)ctx->place_in.ptr,
+    if ((e = alp::launch_place(sp.units_per_gpu, small, count - small,
+                               (const alp::PlaceIn *)ctx->place_in.ptr,
                                (alp_placement_t *)ctx->place_out.ptr, ctx->stream)) != hipSuccess)
         return hip_fail(e, "placement launch");
     if (ctx->timing && (e = hipEventRecord(ctx->ev[2], ctx->stream)) != hipSuccess)

@@ -240,15 +240,19 @@ hipError_t launch_trace_stats(uint32_t M, uint32_t R, const uint64_t *offsets, c
                               uint32_t *work, bool sweep, bool zero_first, alp_stats_t *out,
                               hipStream_t st);
 
-// One allocation to place: budget, LLM count, whether the search found it, per-LLM choices.
+// One allocation to place: budget, LLM count, whether the search found it, per-LLM choices,
+// and the index of its output record.
 struct PlaceIn {
     uint8_t gpus, llms, feasible, pad;
     uint8_t tp[ALP_MAX_LLMS], q[ALP_MAX_LLMS], d[ALP_MAX_LLMS];
+    uint32_t dst;
 };
 
-// Placement of count allocations (see alp_place); Q share units per GPU.
-hipError_t launch_place(uint32_t Q, uint32_t count, const PlaceIn *in, alp_placement_t *out,
-                        hipStream_t st);
+// Placement (see alp_place); Q share units per GPU.  in[0..small) have budgets of at most 16
+// GPUs (placed four to a wave), in[small..small + large) the others (one to a wave); each
+// writes out[in[i].dst].
+hipError_t launch_place(uint32_t Q, uint32_t small, uint32_t large, const PlaceIn *in,
+                        alp_placement_t *out, hipStream_t st);
 
 static_assert(sizeof(alp_placement_t) == 272 && offsetof(alp_placement_t, slot) == 16,
               "alp_placement_t layout");

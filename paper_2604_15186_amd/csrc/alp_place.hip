@@ -1,5 +1,7 @@
 // gfx950 kernel that places allocations on the GPUs of their budgets (Scepsy, arXiv 2604.15186,
-// Section 6, hierarchical placement), one wave per allocation, lane g holding GPU g.
+// Section 6, hierarchical placement): one wave per allocation, or one 16-lane row of a wave
+// for budgets of at most 16 GPUs (four allocations per wave); lane g of the allocation's lanes
+// holds GPU g.
 //
 // G <= 64 GPUs form nodes of 8 (the last may hold fewer), each node one all-to-all xGMI domain;
 // a GPU holds Q share units.  LLM m's allocation is d_m replicas of tp_m ranks of q_m units, the
@@ -14,8 +16,8 @@
 //     index); failing that, onto the lowest empty GPU of the node with the fewest free units.
 // Replicas are placed one after the other (each sees the units the earlier ones took); within a
 // replica every lane scores its own GPU, or the run its GPU starts, from its node's free units
-// (kept by every lane of the node, one byte per GPU), and a wave minimum over one packed 32-bit
-// key per lane picks the choice with the order above.
+// (kept by every lane of the node, one byte per GPU), and a minimum over the allocation's lanes
+// of one packed 32-bit key per lane picks the choice with the order above.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -32,21 +34,19 @@ constexpr uint32_t kNone = 0xFFFFFFFFu;
 static_assert(ALP_PLACE_MAX_GPUS == 64, "one lane per GPU of a wave");
 static_assert(kNode == 8, "a node is an 8-lane group of the wave");
 
-// Free units of the 8 GPUs of a node, one byte each (GPU j of the node in byte j of lo for
-// j < 4, of hi for j >= 4): every lane of the node keeps the same copy, so scoring a replica
-// needs no cross-lane traffic.
+// Free units of the 8 GPUs of a node, one byte each (GPU j of the node in byte j): every lane
+// of the node keeps the same copy, so scoring a replica needs no cross-lane traffic.  One 64-bit
+// value, shifted by the GPU (a choice between two halves would be compiled as an index into a
+// per-lane array, kept in LDS).
 struct NodeFree {
-    uint32_t lo, hi;
+    uint64_t v;
     __device__ __forceinline__ uint32_t get(uint32_t j) const
     {
-        return __builtin_amdgcn_ubfe(j < 4 ? lo : hi, 8 * (j & 3), 8);
+        return (uint32_t)(v >> (8 * j)) & 0xFFu;
     }
-    __device__ __forceinline__ void sub(uint32_t j, uint32_t v)
+    __device__ __forceinline__ void sub(uint32_t j, uint32_t x)
     {
-        if (j < 4)
-            lo -= v << (8 * j);
-        else
-            hi -= v << (8 * (j - 4));
+        v -= (uint64_t)x << (8 * j);
     }
 };
 
@@ -67,63 +67,124 @@ __device__ __forceinline__ void sort8(uint32_t (&k)[8])
     cs(3, 4);
 }
 
+// Minimum over the L lanes of this lane's allocation, in every one of them: the whole wave (L =
+// 64, a wave-uniform value) or its 16-lane row (quad swaps, then the row's half mirror and
+// mirror).
+template <uint32_t L>
+__device__ __forceinline__ uint32_t group_min(uint32_t v)
+{
+    if constexpr (L == 64) {
+        return wave_min_u32(v);
+    } else {
+        static_assert(L == 16, "an allocation takes the wave or one 16-lane row");
+        auto step = [&](auto c) {
+            constexpr int C = decltype(c)::value;
+            const uint32_t o = dpp_mov<C>(v, v);
+            v = o < v ? o : v;
+        };
+        step(std::integral_constant<int, 0xB1>{});
+        step(std::integral_constant<int, 0x4E>{});
+        step(std::integral_constant<int, 0x141>{});
+        step(std::integral_constant<int, 0x140>{});
+        return v;
+    }
+}
+
+// v of lane `src` of the wave (src the same within each allocation's lanes).
+template <uint32_t L>
+__device__ __forceinline__ uint32_t group_read(uint32_t v, uint32_t src)
+{
+    if constexpr (L == 64)
+        return (uint32_t)__builtin_amdgcn_readlane((int)v, (int)src);
+    else
+        return (uint32_t)__builtin_amdgcn_ds_bpermute((int)(src << 2), (int)v);
+}
+
+// L lanes per allocation: 64 (one allocation per wave, G <= 64) or 16 (four per wave, one per
+// 16-lane row, G <= 16); lane g of an allocation's lanes holds its GPU g.  Every decision below
+// depends only on the allocation, so its lanes take the same path.
+template <uint32_t L>
 __global__ void __launch_bounds__(64 * kWavesPerBlock)
 place_kernel(uint32_t Q, uint32_t count, const PlaceIn *__restrict__ in,
              alp_placement_t *__restrict__ out)
 {
+    constexpr uint32_t kPerWave = 64 / L, kWords = 64 / L;   // allocations, slot words per lane
     const uint32_t lane = threadIdx.x & 63;
-    const uint32_t t = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+    const uint32_t gl = lane % L, first_lane = lane - gl;
+    const uint32_t t = (blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6)) * kPerWave + lane / L;
     if (t >= count)
-        return;                                        // uniform over the wave
+        return;                                        // uniform over the allocation's lanes
+    // The allocation's fields as packed words (byte m of tp, q, d is LLM m's), so that nothing
+    // below is indexed in a per-lane array: such arrays would be kept in LDS at an offset from
+    // the flat thread index, whose workgroup size is read from the dispatch packet in host
+    // memory -- a PCIe round trip that every wave would wait for.
     const PlaceIn a = in[t];
     const uint32_t G = a.gpus, M = a.llms;
-    const uint32_t node = lane / kNode, pos = lane % kNode;
-    const bool gpu = lane < G;
+    auto bytes64 = [](const uint8_t (&b)[ALP_MAX_LLMS]) {
+        uint64_t v = 0;
+#pragma unroll
+        for (uint32_t m = 0; m < ALP_MAX_LLMS; ++m)
+            v |= (uint64_t)b[m] << (8 * m);
+        return v;
+    };
+    const uint64_t tp_w = bytes64(a.tp), q_w = bytes64(a.q), d_w = bytes64(a.d);
+    auto byte_of = [](uint64_t v, uint32_t m) { return (uint32_t)(v >> (8 * m)) & 0xFFu; };
+    const uint32_t node = gl / kNode, pos = gl % kNode;
+    const bool gpu = gl < G;
     // GPUs of this lane's node (the last node may hold fewer), and the node's free units.
     const uint32_t node_gpus = G > node * kNode ? (G - node * kNode < kNode ? G - node * kNode : kNode)
                                                 : 0u;
-    NodeFree F{0u, 0u};
+    NodeFree F{0ull};
     for (uint32_t j = 0; j < node_gpus; ++j)
-        F.sub(j, 0u - Q);                              // adds Q to byte j
-    // Lane L keeps slots 2L and 2L + 1 (128 16-bit slots, "not placed" until set) and stores
-    // them once at the end.
-    uint32_t slots = 0xFFFFFFFFu;
+        F.v += (uint64_t)Q << (8 * j);
+    // Lane g keeps slots 2 kWords g .. 2 kWords g + 2 kWords - 1 (128 16-bit slots, "not
+    // placed" until set) and stores them once at the end.
+    uint32_t slots[kWords];
+#pragma unroll
+    for (uint32_t k = 0; k < kWords; ++k)
+        slots[k] = 0xFFFFFFFFu;
     auto set_slot = [&](uint32_t s, uint32_t v) {
-        if (lane == s >> 1)
-            slots = s & 1u ? (slots & 0xFFFFu) | v << 16 : (slots & 0xFFFF0000u) | v;
-    };
-    uint32_t first[ALP_MAX_LLMS], total = 0;
-    for (uint32_t m = 0; m < M; ++m) {
-        first[m] = total;
-        total += a.d[m];
-    }
-    // Most-constrained-first order of the LLMs (their replicas are placed together); the same
-    // in every lane.
-    uint32_t order[ALP_MAX_LLMS], k = 0;
-    for (uint32_t m = 0; m < M; ++m)
-        if (a.d[m])
-            order[k++] = m;
-    for (uint32_t i = 1; i < k; ++i) {
-        const uint32_t v = order[i];
-        const uint32_t vkind = a.tp[v] == 1, vsize = (uint32_t)a.tp[v] * a.q[v];
-        uint32_t j = i;
-        while (j > 0) {
-            const uint32_t u = order[j - 1];
-            const uint32_t ukind = a.tp[u] == 1, usize = (uint32_t)a.tp[u] * a.q[u];
-            const bool before = vkind < ukind || (vkind == ukind && (vsize > usize ||
-                                                 (vsize == usize && v < u)));
-            if (!before)
-                break;
-            order[j] = u;
-            --j;
+        if (gl == s / (2 * kWords)) {
+            const uint32_t k = (s / 2) % kWords;
+#pragma unroll
+            for (uint32_t kk = 0; kk < kWords; ++kk)
+                if (kk == k)
+                    slots[kk] = s & 1u ? (slots[kk] & 0xFFFFu) | v << 16
+                                       : (slots[kk] & 0xFFFF0000u) | v;
         }
-        order[j] = v;
+    };
+    // First slot of each LLM's replicas (byte m; at most 8 x 16 replicas in all).
+    uint64_t first_w = 0;
+    uint32_t total = 0;
+#pragma unroll
+    for (uint32_t m = 0; m < ALP_MAX_LLMS; ++m) {
+        first_w |= (uint64_t)total << (8 * m);
+        total += m < M ? byte_of(d_w, m) : 0u;
+    }
+    // Most-constrained-first order of the LLMs with replicas (their replicas are placed
+    // together): ascending keys (single-GPU replicas after tensor-parallel ones, then larger
+    // replicas first, then the LLM index), sorted by the network; order_w holds the LLMs, four
+    // bits each.
+    uint32_t keys[ALP_MAX_LLMS];
+#pragma unroll
+    for (uint32_t m = 0; m < ALP_MAX_LLMS; ++m) {
+        const uint32_t tpm = byte_of(tp_w, m), size = tpm * byte_of(q_w, m);   // <= 128
+        keys[m] = m < M && byte_of(d_w, m) ? (uint32_t)(tpm == 1) << 16 | (0xFFu - size) << 8 | m
+                                           : 0xFFFFFFFFu;
+    }
+    sort8(keys);
+    uint32_t order_w = 0, k = 0;
+#pragma unroll
+    for (uint32_t i = 0; i < ALP_MAX_LLMS; ++i) {
+        order_w |= (keys[i] & 7u) << (4 * i);
+        k += keys[i] != 0xFFFFFFFFu;
     }
     bool placed = a.feasible != 0;
     uint32_t done = 0;
     for (uint32_t i = 0; i < k && placed; ++i) {
-        const uint32_t m = order[i], tp = a.tp[m], q = a.q[m];
-        for (uint32_t r = 0; r < a.d[m]; ++r) {
+        const uint32_t m = (order_w >> (4 * i)) & 7u, tp = byte_of(tp_w, m), q = byte_of(q_w, m);
+        const uint32_t dm = byte_of(d_w, m), fm = byte_of(first_w, m);
+        for (uint32_t r = 0; r < dm; ++r) {
             const uint32_t f = F.get(pos);
             uint32_t fj[kNode], dom = 0;
 #pragma unroll
@@ -159,20 +220,19 @@ place_kernel(uint32_t Q, uint32_t count, const PlaceIn *__restrict__ in,
                 key = room && rank + tp <= rooms
                           ? (fmax - f) << 24 | dom << 16 | cap << 8 | node << 3 | rank
                           : kNone;
-                const uint32_t best = wave_min_u32(key);
+                const uint32_t best = group_min<L>(key);
                 if (best == kNone) {
                     placed = false;
                     break;
                 }
                 // The winning run, as seen by the lane that proposed it.
                 bn = (best >> 3) & 7u;
-                const uint64_t won = __ballot(key == best);
-                mask = (uint32_t)__builtin_amdgcn_readlane((int)run,
-                                                           (int)__builtin_ctzll(won));
+                const uint64_t won = __ballot(key == best) >> first_lane;
+                mask = group_read<L>(run, first_lane + (uint32_t)__builtin_ctzll(won));
             } else {
                 // An occupied GPU with room, fewest free units, lowest index.
-                key = gpu && f < Q && f >= q ? f << 8 | lane : kNone;
-                uint32_t best = wave_min_u32(key), g = best & 0xFFu;
+                key = gpu && f < Q && f >= q ? f << 8 | gl : kNone;
+                uint32_t best = group_min<L>(key), g = best & 0xFFu;
                 if (best == kNone) {
                     // The lowest empty GPU of the node with the fewest free units.
                     uint32_t empty = 0;
@@ -181,7 +241,7 @@ place_kernel(uint32_t Q, uint32_t count, const PlaceIn *__restrict__ in,
                         empty |= (uint32_t)(j < node_gpus && fj[j] == Q) << j;
                     key = pos == 0 && empty ? dom << 8 | node << 3 | (uint32_t)__builtin_ctz(empty)
                                             : kNone;
-                    best = wave_min_u32(key);
+                    best = group_min<L>(key);
                     if (best == kNone) {
                         placed = false;
                         break;
@@ -197,33 +257,46 @@ place_kernel(uint32_t Q, uint32_t count, const PlaceIn *__restrict__ in,
                     if (mask >> j & 1u)
                         F.sub(j, q);
             }
-            set_slot(first[m] + r, bn << 8 | mask);
+            set_slot(fm + r, bn << 8 | mask);
             ++done;
         }
     }
-    reinterpret_cast<uint32_t *>(out[t].slot)[lane] = slots;
-    const uint64_t used = __ballot(gpu && F.get(pos) < Q);
+    alp_placement_t *dst = out + a.dst;
+#pragma unroll
+    for (uint32_t kk = 0; kk < kWords; ++kk)
+        reinterpret_cast<uint32_t *>(dst->slot)[gl * kWords + kk] = slots[kk];
+    const uint64_t used_all = __ballot(gpu && F.get(pos) < Q) >> first_lane;
+    const uint64_t used = L == 64 ? used_all : used_all & ((1ull << L) - 1);
     uint32_t used_nodes = 0;
-    for (uint32_t n = 0; n < ALP_PLACE_MAX_GPUS / kNode; ++n)
+    for (uint32_t n = 0; n < L / kNode; ++n)
         used_nodes += (used >> (n * kNode) & 0xFFu) != 0;
-    if (lane == 0) {
-        out[t].status = placed ? ALP_OK : ALP_INFEASIBLE;
-        out[t].replicas = done;
-        out[t].gpus_used = (uint32_t)__popcll(used);
-        out[t].nodes_used = used_nodes;
+    if (gl == 0) {
+        dst->status = placed ? ALP_OK : ALP_INFEASIBLE;
+        dst->replicas = done;
+        dst->gpus_used = (uint32_t)__popcll(used);
+        dst->nodes_used = used_nodes;
     }
 }
 
 }  // namespace
 
-hipError_t launch_place(uint32_t Q, uint32_t count, const PlaceIn *in, alp_placement_t *out,
-                        hipStream_t st)
+hipError_t launch_place(uint32_t Q, uint32_t small, uint32_t large, const PlaceIn *in,
+                        alp_placement_t *out, hipStream_t st)
 {
-    if (count == 0)
-        return hipSuccess;
-    hipLaunchKernelGGL(place_kernel, dim3((count + kWavesPerBlock - 1) / kWavesPerBlock),
-                       dim3(64 * kWavesPerBlock), 0, st, Q, count, in, out);
-    return hipGetLastError();
+    if (small) {
+        const uint32_t per_block = kWavesPerBlock * 4;
+        hipLaunchKernelGGL(place_kernel<16>, dim3((small + per_block - 1) / per_block),
+                           dim3(64 * kWavesPerBlock), 0, st, Q, small, in, out);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess)
+            return e;
+    }
+    if (large) {
+        hipLaunchKernelGGL(place_kernel<64>, dim3((large + kWavesPerBlock - 1) / kWavesPerBlock),
+                           dim3(64 * kWavesPerBlock), 0, st, Q, large, in + small, out);
+        return hipGetLastError();
+    }
+    return hipSuccess;
 }
 
 }  // namespace alp
