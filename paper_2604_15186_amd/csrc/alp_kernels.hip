@@ -984,7 +984,7 @@ eval_kernel(SpaceDev sp, uint32_t capacity, const uint2 *__restrict__ rec,
 // and a running minimum of their units is taken along that order; need(t) for each candidate
 // t then costs one binary search per LLM.  O(M * O * (O + M log O)) work per item, in LDS; one
 // thread per option where the block allows.
-constexpr uint32_t kTmaxStride = 8;     // options per LLM padded to this, for 8-wide LDS reads
+constexpr uint32_t kTmaxStride = 8;     // options per LLM padded to this (whole 16-byte reads)
 
 __host__ __device__ inline uint32_t tmax_stride(uint32_t O)
 {
@@ -996,10 +996,13 @@ tmax_kernel(SpaceDev sp, QueryDev q, const uint2 *__restrict__ ext, uint32_t *__
 {
     extern __shared__ uint4 t_lds4[];
     constexpr uint16_t kUnusable = 0xFFFFu;   // share units are at most 64 * 16 * 16 = 16384
+    constexpr uint64_t kNoKey = ~0ull;        // not deployable (or padding): ranks last
     const uint32_t item = blockIdx.x;
     const uint32_t O = sp.O, MO = sp.M * O, P = tmax_stride(O), MP = sp.M * P;
-    uint32_t *tau = reinterpret_cast<uint32_t *>(t_lds4);   // [M][P] option tau
-    uint32_t *stau = tau + MP;                           // [M][P] deployable taus, descending
+    // Each option's rank key: (2^32 - 1 - tau) << 32 | index, so that ascending keys are tau
+    // descending then index ascending, and one 64-bit compare orders two options.
+    uint64_t *key = reinterpret_cast<uint64_t *>(t_lds4);   // [M][P]
+    uint32_t *stau = reinterpret_cast<uint32_t *>(key + MP); // [M][P] deployable taus, descending
     uint16_t *units = (uint16_t *)(stau + MP);           // [M][P] share units, or kUnusable
     uint16_t *smin = units + MP;                         // [M][P] running minimum of units
     __shared__ uint32_t s_count[ALP_MAX_LLMS];
@@ -1012,31 +1015,27 @@ tmax_kernel(SpaceDev sp, QueryDev q, const uint2 *__restrict__ ext, uint32_t *__
         uint2 e = make_uint2(0u, 0u);                    // padding: not deployable
         if (o < O)
             e = E[m * O + o];
-        tau[a] = e.x;
-        units[a] = ((e.y >> 16) & 1u) ? (uint16_t)(e.y & 0xFFFFu) : kUnusable;
+        const bool usable = (e.y >> 16) & 1u;
+        key[a] = usable ? (uint64_t)(0xFFFFFFFFu - e.x) << 32 | o : kNoKey;
+        units[a] = usable ? (uint16_t)(e.y & 0xFFFFu) : kUnusable;
     }
     __syncthreads();
-    // Rank of each deployable option within its LLM, tau descending then index ascending; the
-    // LLM's taus and units are read 8 at a time.
+    // Rank of each deployable option within its LLM: the keys of the LLM below its own, read
+    // two at a time (a compare and an add each).
     for (uint32_t a = threadIdx.x; a < MP; a += blockDim.x) {
-        if (units[a] == kUnusable)
+        const uint64_t mine = key[a];
+        if (mine == kNoKey)
             continue;
-        const uint32_t m = a / P, o = a - m * P, t = tau[a];
-        const uint4 *T4 = reinterpret_cast<const uint4 *>(tau + m * P);
-        const uint4 *U4 = reinterpret_cast<const uint4 *>(units + m * P);
+        const uint32_t m = a / P;
+        const uint4 *K2 = reinterpret_cast<const uint4 *>(key + m * P);
         uint32_t rank = 0;
-        for (uint32_t j8 = 0; j8 < P / 8; ++j8) {
-            const uint4 ta = T4[2 * j8], tb = T4[2 * j8 + 1], uu = U4[j8];
-            const uint32_t tv[8] = {ta.x, ta.y, ta.z, ta.w, tb.x, tb.y, tb.z, tb.w};
-            const uint32_t uw[4] = {uu.x, uu.y, uu.z, uu.w};
-#pragma unroll
-            for (uint32_t k = 0; k < 8; ++k) {
-                const uint32_t j = 8 * j8 + k;
-                const bool usable = ((uw[k / 2] >> (16 * (k & 1))) & 0xFFFFu) != kUnusable;
-                rank += usable && (tv[k] > t || (tv[k] == t && j < o));
-            }
+#pragma unroll 4
+        for (uint32_t j2 = 0; j2 < P / 2; ++j2) {
+            const uint4 kk = K2[j2];
+            rank += ((uint64_t)kk.y << 32 | kk.x) < mine;
+            rank += ((uint64_t)kk.w << 32 | kk.z) < mine;
         }
-        stau[m * P + rank] = t;
+        stau[m * P + rank] = 0xFFFFFFFFu - (uint32_t)(mine >> 32);
         smin[m * P + rank] = units[a];
         atomicAdd(&s_count[m], 1u);
     }
@@ -1052,15 +1051,22 @@ tmax_kernel(SpaceDev sp, QueryDev q, const uint2 *__restrict__ ext, uint32_t *__
         uint32_t run = 0xFFFFFFFFu;
         for (uint32_t k = lo; k < hi; ++k)
             run = S[k] < run ? S[k] : run;
-        uint32_t before = run;                     // inclusive prefix minimum over lanes
-        for (uint32_t d = 1; d < 64; d <<= 1) {
-            const uint32_t o = (uint32_t)__shfl_up((int)before, d);
-            if (lane >= d)
-                before = o < before ? o : before;
-        }
-        uint32_t acc = (uint32_t)__shfl_up((int)before, 1);
-        if (lane == 0)
-            acc = 0xFFFFFFFFu;
+        // Inclusive prefix minimum over the lanes by DPP (row shifts by 1, 2, 4, 8, then lane
+        // 15 into rows 1 and 3 and lane 31 into rows 2 and 3; lanes a move does not reach keep
+        // the identity), then the exclusive one by a shift of the whole wave.
+        uint32_t before = run;
+        auto step = [&](auto c, auto rm) {
+            constexpr int C = decltype(c)::value, RM = decltype(rm)::value;
+            const uint32_t o = dpp_mov<C, RM>(0xFFFFFFFFu, before);
+            before = o < before ? o : before;
+        };
+        step(std::integral_constant<int, 0x111>{}, std::integral_constant<int, 0xF>{});
+        step(std::integral_constant<int, 0x112>{}, std::integral_constant<int, 0xF>{});
+        step(std::integral_constant<int, 0x114>{}, std::integral_constant<int, 0xF>{});
+        step(std::integral_constant<int, 0x118>{}, std::integral_constant<int, 0xF>{});
+        step(std::integral_constant<int, 0x142>{}, std::integral_constant<int, 0xA>{});
+        step(std::integral_constant<int, 0x143>{}, std::integral_constant<int, 0xC>{});
+        uint32_t acc = dpp_mov<0x138>(0xFFFFFFFFu, before);
         for (uint32_t k = lo; k < hi; ++k) {
             acc = S[k] < acc ? S[k] : acc;
             S[k] = (uint16_t)acc;
@@ -1070,9 +1076,9 @@ tmax_kernel(SpaceDev sp, QueryDev q, const uint2 *__restrict__ ext, uint32_t *__
     const uint64_t capacity = (uint64_t)query_value(q.capacity, q.cap1, item);
     uint32_t best = 0;
     for (uint32_t a = threadIdx.x; a < MP; a += blockDim.x) {
-        if (units[a] == kUnusable)
+        if (key[a] == kNoKey)
             continue;
-        const uint32_t t = tau[a];
+        const uint32_t t = 0xFFFFFFFFu - (uint32_t)(key[a] >> 32);
         if (t <= best)
             continue;
         uint64_t need = 0;
@@ -1259,7 +1265,7 @@ hipError_t launch_tmax(const SpaceDev &sp, const QueryDev &q, uint32_t count, co
     if (count == 0)
         return hipSuccess;
     const uint32_t MP = sp.M * tmax_stride(sp.O);
-    const size_t lds = (size_t)MP * (2 * sizeof(uint32_t) + 2 * sizeof(uint16_t));
+    const size_t lds = (size_t)MP * (sizeof(uint64_t) + sizeof(uint32_t) + 2 * sizeof(uint16_t));
     // one thread per option (padded), in whole waves, 64..1024
     const uint32_t threads = MP >= 1024 ? 1024u : (MP + 63) / 64 * 64;
     hipLaunchKernelGGL(tmax_kernel, dim3(count), dim3(threads), lds, st, sp, q, ext, out);
