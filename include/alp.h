@@ -299,10 +299,11 @@ int32_t alp_stats_create(alp_stats_ctx **out, int32_t device, void *hip_stream);
  * end - start < 2^32.  Writes out[0..num_llms) (host).  EINVAL for a malformed input (offsets,
  * llm >= num_llms, end < start), ERANGE for out-of-range timestamps or a result of 2^31 or
  * more.  Synchronous on the context's stream.  Any call order within a trace gives the same
- * result; traces whose calls are in order of end time (as logged on completion) take the fast
- * path (no sort).  A context whose call finds most traces out of end order sorts every trace
- * directly on its next 7 calls, then checks the order again.  The context's scratch grows to 4 bytes per trace plus, for traces beyond
- * 2,048 calls, 16 bytes per call rounded up to a power of two per trace. */
+ * result; traces whose calls are in order of end time (as logged on completion) and that span
+ * under 2^32 us take the fast path (no sort).  A context whose call finds most traces out of
+ * end order sorts every trace directly on its next 7 calls, then checks the order again.  The
+ * context's scratch grows to 4 bytes per trace plus, for traces beyond 2,048 calls, 16 bytes
+ * per call rounded up to a power of two per trace. */
 int32_t alp_trace_stats(alp_stats_ctx *ctx, uint32_t num_llms, uint32_t num_traces,
                         const uint64_t *offsets, const uint32_t *llm, const uint64_t *start_us,
                         const uint64_t *end_us, alp_stats_t *out);
