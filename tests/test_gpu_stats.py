@@ -204,3 +204,31 @@ def test_order_adaptive_passes_agree():
         for k in range(12):                    # shuffled, in order, shuffled, ...
             llm, s, e = orders[k % 2]
             _same(c, tr["M"], tr["offsets"], llm, s, e)
+
+
+def test_work_list_longer_than_the_sort_grid_with_long_traces():
+    """On a fresh context the first call sweeps: 2,500 of 3,000 beam traces shuffled within the
+    trace fill a work list longer than the sort pass's grid of 1,024 blocks (blocks take several
+    entries in turn), and three traces beyond 2,048 calls make the long-trace pass the one whose
+    last block finishes.  The next calls sort every trace directly (most were out of order),
+    with the long traces again; every call must match the oracle."""
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2604_15186_amd import alp
+    tr = make_traces("beam", 3000, 13)
+    off = tr["offsets"].astype(np.int64)
+    rng = np.random.default_rng(14)
+    parts = []
+    for r, (lo, hi) in enumerate(zip(off[:-1], off[1:])):
+        idx = lo + (rng.permutation(hi - lo) if r < 2500 else np.arange(hi - lo))
+        parts.append([(int(tr["llm"][i]), int(tr["start"][i]), int(tr["end"][i])) for i in idx])
+    for n in (2049, 6000, 4096):                       # long traces, in random order
+        t0 = int(rng.integers(0, 1 << 30))
+        s = t0 + rng.integers(0, 1 << 24, n)
+        parts.append([(int(m), int(a), int(a + d)) for m, a, d in
+                      zip(rng.integers(0, 2, n), s, rng.integers(0, 100_000, n))])
+    arrays = _pack(parts)
+    with alp.StatsContext(0) as c:
+        for _ in range(3):                             # sweep + list, then direct sorts
+            _same(c, tr["M"], *arrays)
