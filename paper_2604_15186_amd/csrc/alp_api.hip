@@ -475,7 +475,11 @@ int32_t plan_scan(alp_ctx *c, uint32_t count, alp::ScanGeometry &out, bool allow
         g.blocks_per_item = (uint32_t)bpi;
         // One launch for spaces of fewer than 2^32 candidates (the winner fits one 64-bit word),
         // unless the option terms are asked to run in their own kernel.
+        // The block keeps the item's curves and records in LDS: at most 56 KiB of them, with
+        // the kernel's own few KiB within 64 KiB (every space of fewer than 2^32 candidates
+        // fits; the test only guards the layout).
         g.fused = g.variant == 1 && allow_fused && c->N < (UINT64_C(1) << 32) &&
+                  alp::fused_lds_bytes(sp) <= (UINT64_C(56) << 10) &&
                   !(c->variant & ALP_LAUNCH_SEPARATE_TERMS) ? 1u : 0u;
     } else {
         g.threads = c->tpb_override ? c->tpb_override : 256;
@@ -819,10 +823,13 @@ int32_t alp_load_profiles(alp_ctx **out, const alp_space_t *space, uint32_t num_
     sp.K = space->num_points;
     sp.Q = space->units_per_gpu;
     sp.O = O;
-    for (uint32_t i = 0; i < ALP_MAX_TP; ++i)
-        sp.tp[i] = i < sp.n_tp ? space->tp_values[i] : 0;
-    for (uint32_t j = 0; j < ALP_MAX_FRAC; ++j)
-        sp.fq[j] = j < sp.n_fq ? space->frac_units[j] : 0;
+    sp.mul_O = alp::div_multiplier(O);
+    sp.mul_D = alp::div_multiplier(sp.D);
+    sp.tp8 = sp.fq8 = 0;
+    for (uint32_t i = 0; i < sp.n_tp; ++i)
+        sp.tp8 |= (uint64_t)space->tp_values[i] << (8 * i);
+    for (uint32_t j = 0; j < sp.n_fq; ++j)
+        sp.fq8 |= (uint64_t)space->frac_units[j] << (8 * j);
     hipDeviceProp_t prop;
     if (hipGetDeviceProperties(&prop, device) == hipSuccess)
         c->num_cus = prop.multiProcessorCount;

@@ -192,8 +192,8 @@ __device__ __forceinline__ void write_result_lanes(const SpaceDev &sp, uint32_t 
     uint64_t tp = 0, fq = 0, rep = 0;
     if (L != kNoLatency && lane < sp.M) {
         const uint32_t ij = o / sp.D;
-        tp = (uint64_t)(sp.tp[ij / sp.n_fq] & 0xFFu) << (8 * lane);
-        fq = (uint64_t)(sp.fq[ij % sp.n_fq] & 0xFFu) << (8 * lane);
+        tp = (uint64_t)sp.tp(ij / sp.n_fq) << (8 * lane);
+        fq = (uint64_t)sp.fq(ij % sp.n_fq) << (8 * lane);
         rep = (uint64_t)((o % sp.D + 1) & 0xFFu) << (8 * lane);
     } else {
         T = 0xFFFFFFFFu;
@@ -378,95 +378,180 @@ struct OptionTerm {
     bool ok, thr;
 };
 
-// floor(x / d) for x < 2^63 and 0 < d < 2^32, exactly: a double-precision quotient (within 2^11
-// of the true one, the dividend rounded to 53 bits), corrected by the exact 64-bit remainder
-// divided in double precision (|remainder| < 2^44, exact in a double), then by one last step
-// for the rounding of that second quotient.  Shorter than the general 64-bit division.
-__device__ __forceinline__ uint64_t udiv_u64_u32(uint64_t x, uint64_t d)
+// A reciprocal of d (0 < d < 2^31) in double precision biased low: (1 - e) / d with
+// 0.85 * 2^-B < e < 1.15 * 2^-B.  The single-precision hardware reciprocal (within 1 ulp, so a
+// relative error below 2^-22 with the rounding of d to a float) starts S Newton steps; a step
+// squares the relative error (below 2^-44 after one, 2^-88 after two) and rounds once (2^-53),
+// and the last step forms its residual against 1 - 2^-B instead of 1, which subtracts 2^-B.
+// The bounds hold for (S, B) = (1, 40) and (2, 50).
+template <int S, int B>
+__device__ __forceinline__ double recip_low(uint32_t d)
 {
-    if ((x >> 32) == 0)
-        return (uint32_t)x / (uint32_t)d;
-    const double dd = (double)d;
-    uint64_t q = (uint64_t)((double)x / dd);
-    int64_t r = (int64_t)(x - q * d);
-    q += (int64_t)floor((double)r / dd);
-    r = (int64_t)(x - q * d);
-    if (r < 0)
-        --q;
-    else if (r >= (int64_t)d)
-        ++q;
-    return q;
+    static_assert((S == 1 && B == 40) || (S == 2 && B == 50), "bounds stated for these");
+    constexpr double kOneLow = 1.0 - 1.0 / (double)(1ull << B);
+    const double D = (double)d;
+    double y = (double)__builtin_amdgcn_rcpf((float)d);
+    if constexpr (S == 2)
+        y = fma(y, fma(-D, y, 1.0), y);
+    return fma(y, fma(-D, y, kOneLow), y);
 }
 
-// The terms from the option's inputs: its profile curve (rate and lat, K points each; global or
-// LDS memory), whether the (tp, share) pair is deployable, and the LLM's W, n, p.  Every
-// division has a dividend below 2^63 and a divisor below 2^31 (inputs below 2^31, d <= 16).
-__device__ __forceinline__ OptionTerm option_term_from(const SpaceDev &sp, uint64_t H, uint32_t o,
-                                                       const uint32_t *rate, const uint32_t *lat,
-                                                       bool allowed, uint64_t W, uint64_t n,
-                                                       uint64_t p, uint64_t lambda)
+// floor(x / d) for 0 < d <= 2^31 and a quotient below 2^32 - 1, given x as a double xf (exact
+// or rounded once) and modulo 2^32 (x_lo), and inv = recip_low<1, 40>(d) (or <2, 50>).  The
+// estimate xf * inv is below x / d (the bias outweighs the roundings of x and of the product,
+// 2^-53 each) by less than 2^-7 (1.15 * 2^-40 + 2^-52 of a quotient below 2^32), so its integer
+// part q is the quotient or one less; the remainder x - q d then lies in [0, 2 d), exact modulo
+// 2^32, and one comparison with d decides.  Outside the domain the result is some value,
+// without undefined behaviour (the estimate is clamped before its conversion).
+__device__ __forceinline__ uint32_t udiv_low(double xf, uint32_t x_lo, uint32_t d, double inv)
 {
-    const uint32_t d = o % sp.D + 1;
-    const uint32_t ij = o / sp.D;
-    const uint32_t j = ij % sp.n_fq, i = ij / sp.n_fq;
-    const uint64_t tp = sp.tp[i], fq = sp.fq[j];
-    OptionTerm t;
-    t.ok = allowed && W * sp.Q <= tp * fq * H;
-    const uint64_t T = rate[sp.K - 1];
-    const uint64_t tau = udiv_u64_u32(1000ull * d * T, n);
-    t.tau = tau > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)tau;
-    const uint64_t dd = 1000ull * d;
-    const uint64_t r = udiv_u64_u32(lambda * n + dd - 1, dd);
-    t.thr = r <= T;
-    uint64_t c = 0;
-    if (t.thr) {
-        uint64_t ell = lat[0];
-        if (r > rate[0]) {
-            // The segment [rate[k-1], rate[k]] holding r: k counts the points below r (rates
-            // ascend strictly and r <= rate[K-1]); the K reads are independent, so they are
-            // in flight together rather than one after another.
-            uint32_t k = 0;
+    const uint32_t q = (uint32_t)fmin(xf * inv, 4294967295.0);
+    return q + (x_lo - q * d >= d ? 1u : 0u);
+}
+
+// An LLM's inputs to its option terms: n and p (milli) with their reciprocals.
+struct LlmInputs {
+    double inv_n;              // recip_low<2, 50>(n): tau's quotient reaches 2^45
+    double inv_p;              // recip_low<1, 40>(p)
+    uint32_t n, p;
+};
+
+__device__ __forceinline__ LlmInputs llm_inputs(uint32_t n, uint32_t p)
+{
+    return LlmInputs{recip_low<2, 50>(n), recip_low<1, 40>(p), n, p};
+}
+
+// Whether an (LLM, tp, share) curve's options are deployable: the pair is allowed and the
+// weights sharded over tp fit the share q / Q of one GPU (W * Q <= tp * q * H).
+__device__ __forceinline__ bool deployable(const SpaceDev &sp, uint64_t H, bool allowed,
+                                           uint64_t W, uint32_t tpq)
+{
+    return allowed && W * sp.Q <= (uint64_t)tpq * H;
+}
+
+// A profile curve in device memory: rate and lat, K points each.  The point count below r is
+// taken over ALP_MAX_POINTS reads at indices clamped to K - 1 (a clamped read repeats the last
+// rate, which is not below r), so that all reads are in flight together with no test between.
+struct CurveK {
+    const uint32_t *rate, *lat;
+    uint32_t K;
+    __device__ __forceinline__ uint32_t last_rate() const { return rate[K - 1]; }
+    __device__ __forceinline__ uint32_t points_below(uint32_t r) const
+    {
+        uint32_t k = 0;
 #pragma unroll
-            for (uint32_t q = 0; q < ALP_MAX_POINTS; ++q)
-                k += q < sp.K && rate[q] < r ? 1u : 0u;
-            const uint64_t r0 = rate[k - 1], r1 = rate[k];
-            ell = udiv_u64_u32((uint64_t)lat[k - 1] * (r1 - r) + (uint64_t)lat[k] * (r - r0),
-                               r1 - r0);
-        }
-        c = udiv_u64_u32(ell * n, p);
+        for (uint32_t q = 0; q < ALP_MAX_POINTS; ++q)
+            k += rate[q < K ? q : K - 1] < r ? 1u : 0u;
+        return k;
     }
-    t.c = (uint32_t)c;
-    t.u = (uint32_t)(tp * fq * d);
+};
+
+// A profile curve in LDS: rate padded to ALP_MAX_POINTS points with its last value (16-byte
+// aligned, read as four vectors), lat with K points.  Rates and r are below 2^31, so rate - r
+// has its top bit set exactly when rate < r; the count adds those bits.
+struct CurveLds {
+    const uint32_t *rate, *lat;
+    uint32_t K;
+    __device__ __forceinline__ uint32_t last_rate() const { return rate[K - 1]; }
+    __device__ __forceinline__ uint32_t points_below(uint32_t r) const
+    {
+        const uint4 *r4 = reinterpret_cast<const uint4 *>(rate);
+        uint32_t k = 0;
+#pragma unroll
+        for (uint32_t q = 0; q < ALP_MAX_POINTS / 4; ++q) {
+            const uint4 v = r4[q];
+            k += ((v.x - r) >> 31) + ((v.y - r) >> 31) + ((v.z - r) >> 31) + ((v.w - r) >> 31);
+        }
+        return k;
+    }
+};
+
+// The terms of an option with d replicas of its LLM, from the LLM's profile curve for the
+// option's (tp, share) pair, whether that curve is deployable, tpq = tp * q, the LLM's inputs,
+// the target lambda and inv_dd = recip_low<1, 40>(1000 d).  Every quotient is one udiv_low:
+//   * tau < 2^45 with the <2, 50> reciprocal of n (an estimate below the quotient by less than
+//     1.3 * 2^-50 * 2^45 < 2^-4): an estimate at or above 2^32 saturates, below it is the
+//     quotient or one less, and a quotient of 2^32 saturates too;
+//   * thr is lambda n <= 1000 d T (for an integer T, ceil(y) <= T iff y <= T), a product test;
+//     with thr, r <= T < 2^31 and lambda n + 1000 d - 1 < 2^46 is an exact double;
+//   * ell < 2^31 lies between two latencies;
+//   * c of a deployable option is below 2^32 - 1 by the bound alp_load_profiles checks (every
+//     latency term of a deployable option at most the instance's latency bound), and the
+//     record of an undeployable option ignores c.
+// Lanes without thr compute r, ell and c from out-of-range values and drop them.
+template <class Curve>
+__device__ __forceinline__ OptionTerm option_term_core(uint32_t d, const Curve &cv,
+                                                       bool deployable, uint32_t tpq,
+                                                       const LlmInputs &l, uint32_t lambda,
+                                                       double inv_dd)
+{
+    OptionTerm t;
+    t.ok = deployable;
+    t.u = tpq * d;
+    const uint32_t dd = 1000u * d;
+    const uint32_t T = cv.last_rate();
+    const uint64_t dT = (uint64_t)dd * T;
+    const double n_f = (double)l.n;
+    const double tau_est = ((double)dd * (double)T) * l.inv_n;      // dT exact in a double
+    const uint32_t tq = (uint32_t)fmin(tau_est, 4294967295.0);
+    const bool tau_up = (uint32_t)dT - tq * l.n >= l.n && tq != 0xFFFFFFFFu;
+    t.tau = tau_est >= 4294967296.0 ? 0xFFFFFFFFu : tq + (tau_up ? 1u : 0u);
+    const uint64_t load = (uint64_t)lambda * l.n;
+    t.thr = load <= dT;
+    const uint32_t r = udiv_low(fma((double)lambda, n_f, (double)(dd - 1)),
+                                (uint32_t)load + dd - 1, dd, inv_dd);
+    // ell, the latency at r: linear between the points (r0, l0) and (r1, l1) of the segment
+    // holding r, taken at rc = max(r, r0) and rounded down; k counts the points below r (rates
+    // ascend strictly, r <= rate[K-1]).  k = 0 (r at or below rate[0]) evaluates the first
+    // segment at r0, giving lat[0]; a one-point curve (r0 = r1) takes a unit-width segment from
+    // r0, again lat[0].
+    const uint32_t k = cv.points_below(r);
+    const uint32_t k1 = k > 1 ? k : 1u;
+    const uint32_t i1 = k1 < cv.K ? k1 : cv.K - 1, i0 = k1 - 1;
+    const uint32_t r0 = cv.rate[i0], r1 = cv.rate[i1];
+    const uint32_t l0 = cv.lat[i0], l1 = cv.lat[i1];
+    const uint32_t w = r1 > r0 ? r1 - r0 : 1u;
+    const uint32_t rc = r > r0 ? r : r0;
+    const uint64_t num = (uint64_t)l0 * (r0 + w - rc) + (uint64_t)l1 * (rc - r0);
+    const uint32_t ell = udiv_low((double)num, (uint32_t)num, w, recip_low<1, 40>(w));
+    const uint32_t c = udiv_low((double)ell * n_f, ell * l.n, l.p, l.inv_p);
+    t.c = t.thr ? c : 0u;
     return t;
 }
 
 __device__ __forceinline__ OptionTerm option_term(const SpaceDev &sp, const TablesDev &tb,
                                                   uint32_t inst, uint32_t m, uint32_t o,
-                                                  uint64_t lambda)
+                                                  uint32_t lambda)
 {
-    const uint32_t ij = o / sp.D;
-    const uint32_t j = ij % sp.n_fq, i = ij / sp.n_fq;
+    const uint32_t ij = div_by(o, sp.mul_D), d = o - ij * sp.D + 1;
+    const uint32_t i = ij / sp.n_fq, j = ij - i * sp.n_fq;
     const uint64_t lm = (uint64_t)inst * sp.M + m;
     const uint64_t tab = (lm * sp.n_tp + i) * sp.n_fq + j;
-    return option_term_from(sp, tb.H, o, tb.rate + tab * sp.K, tb.lat + tab * sp.K,
-                            tb.allowed[tab] != 0, tb.W[lm], tb.n[lm], tb.p[lm], lambda);
+    const uint32_t tpq = sp.tp(i) * sp.fq(j);
+    const CurveK cv{tb.rate + tab * sp.K, tb.lat + tab * sp.K, sp.K};
+    return option_term_core(d, cv, deployable(sp, tb.H, tb.allowed[tab] != 0, tb.W[lm], tpq),
+                            tpq, llm_inputs(tb.n[lm], tb.p[lm]), lambda,
+                            recip_low<1, 40>(1000u * d));
 }
 
-// The item's profile inputs a one-launch block keeps in LDS: every (LLM, tp, share) curve (rate
-// then lat, K points each), the curves' allowed flags and each LLM's (W, n << 32 | p).
+// The item's profile inputs a one-launch block keeps in LDS: every (LLM, tp, share) curve's
+// rate (padded, as CurveLds reads it), lat and deployability, tp * q of every (tp, share) pair,
+// each LLM's inputs and the reciprocals of 1000 d.
 struct FusedLds {
-    const uint32_t *curve;
-    const uint8_t *allowed;
-    const ulonglong2 *llm;
+    const uint32_t *rate;
+    const uint32_t *lat;
+    const uint8_t *deploy;
+    const uint32_t *tpq;
+    const LlmInputs *llm;
+    const double *inv_dd;      // [d - 1]
     const uint2 *ext;          // every option's (tau, share units), written by the prologue
-    __device__ __forceinline__ OptionTerm term(const SpaceDev &sp, uint64_t H, uint32_t m,
-                                               uint32_t o, uint64_t lambda) const
+    __device__ __forceinline__ OptionTerm term(const SpaceDev &sp, uint32_t m, uint32_t o,
+                                               uint32_t lambda) const
     {
-        const uint32_t curves = sp.M * sp.n_tp * sp.n_fq;
-        const uint32_t c = m * sp.n_tp * sp.n_fq + o / sp.D;
-        const ulonglong2 wl = llm[m];
-        return option_term_from(sp, H, o, curve + c * sp.K, curve + (curves + c) * sp.K,
-                                allowed[c] != 0, wl.x, wl.y >> 32, wl.y & 0xFFFFFFFFu, lambda);
+        const uint32_t ij = div_by(o, sp.mul_D), d = o - ij * sp.D + 1;
+        const uint32_t c = m * (sp.n_tp * sp.n_fq) + ij;
+        const CurveLds cv{rate + c * ALP_MAX_POINTS, lat + c * sp.K, sp.K};
+        return option_term_core(d, cv, deploy[c] != 0, tpq[ij], llm[m], lambda, inv_dd[d - 1]);
     }
 };
 

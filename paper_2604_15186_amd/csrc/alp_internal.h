@@ -18,12 +18,32 @@ constexpr uint32_t kSentinelUnits = 1u << 24;
 constexpr uint32_t kCapacityMax = kSentinelUnits - 1;
 constexpr uint32_t kNoLatency = 0xFFFFFFFFu;
 
-// Search-space shape passed by value to kernels.
+// Search-space shape passed by value to kernels.  mul_O and mul_D are the multipliers of
+// div_by(): ceil(2^32 / O) and ceil(2^32 / D), 0 for a divisor of 1.  The tensor-parallel
+// degrees (at most 64) and GPU shares (at most 16 units) are bytes of tp8 and fq8 (byte i the
+// i-th value), so that a lane picks its own by a shift: a by-value array indexed differently
+// by different lanes is read from the kernel-argument memory, one slow round trip.
 struct SpaceDev {
     uint32_t M, n_tp, n_fq, D, K, Q, O;
-    uint32_t tp[ALP_MAX_TP];
-    uint32_t fq[ALP_MAX_FRAC];
+    uint32_t mul_O, mul_D;
+    uint64_t tp8, fq8;
+    __host__ __device__ uint32_t tp(uint32_t i) const { return (uint32_t)(tp8 >> (8 * i)) & 0xFFu; }
+    __host__ __device__ uint32_t fq(uint32_t j) const { return (uint32_t)(fq8 >> (8 * j)) & 0xFFu; }
 };
+
+// The multiplier div_by() takes for divisor v (1 <= v < 2^32).
+__host__ __device__ inline uint32_t div_multiplier(uint32_t v)
+{
+    return v > 1 ? (uint32_t)((UINT64_C(0xFFFFFFFF) + v) / v) : 0u;
+}
+
+// floor(a / v) for a * v < 2^32, given mul = div_multiplier(v): with mul = (2^32 + e) / v,
+// 0 <= e < v, a * mul / 2^32 = a / v + a e / (v 2^32) and the added part is below 1 / v, less
+// than the distance from a / v to the next integer.
+__host__ __device__ inline uint32_t div_by(uint32_t a, uint32_t mul)
+{
+    return mul ? (uint32_t)(((uint64_t)a * mul) >> 32) : a;
+}
 
 // Device copies of the profile tables of all instances (layouts as in alp_load_profiles).
 struct TablesDev {
@@ -151,17 +171,25 @@ hipError_t launch_scan(const SpaceDev &sp, const QueryDev &q, uint32_t count, co
                        const uint2 *inner, const ScanGeometry &g, Winner *winners,
                        const FinishArgs &fa, hipStream_t st, hipEvent_t t0 = nullptr,
                        hipEvent_t t1 = nullptr, const FusedArgs *fz = nullptr);
-// Dynamic LDS of a one-launch scan block: the item's profile curves (rate and lat of every
-// (LLM, tp, share), K points each) and their allowed flags ...
+// Dynamic LDS of a one-launch scan block: the item's profile curves (for every (LLM, tp,
+// share): rate padded to ALP_MAX_POINTS points, then -- after all rates -- lat, K points) and
+// their deployability flags ...
 __host__ __device__ inline size_t fused_lds_curves(const SpaceDev &sp)
 {
     return (size_t)sp.M * sp.n_tp * sp.n_fq;
 }
+__host__ __device__ inline size_t fused_lds_lat_offset(const SpaceDev &sp)
+{
+    return fused_lds_curves(sp) * ALP_MAX_POINTS * sizeof(uint32_t);
+}
+__host__ __device__ inline size_t fused_lds_deploy_offset(const SpaceDev &sp)
+{
+    return fused_lds_lat_offset(sp) + fused_lds_curves(sp) * sp.K * sizeof(uint32_t);
+}
 // ... followed by the inner LLM's records (inner_stride(O) of them), 8-byte aligned.
 __host__ __device__ inline size_t fused_lds_inner_offset(const SpaceDev &sp)
 {
-    const size_t curves = fused_lds_curves(sp);
-    return (2 * curves * sp.K * sizeof(uint32_t) + curves + 7) & ~(size_t)7;
+    return (fused_lds_deploy_offset(sp) + fused_lds_curves(sp) + 7) & ~(size_t)7;
 }
 // ... then every option's (tau, share units) for the result record.
 __host__ __device__ inline size_t fused_lds_ext_offset(const SpaceDev &sp)

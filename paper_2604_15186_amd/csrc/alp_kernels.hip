@@ -46,7 +46,7 @@ option_terms_kernel(SpaceDev sp, TablesDev tb, QueryDev q, uint32_t count, uint2
         return;
     const uint32_t item = (uint32_t)(t / per_item);
     const uint32_t rem = (uint32_t)(t - (uint64_t)item * per_item);
-    const uint32_t m = rem / sp.O, o = rem - m * sp.O;
+    const uint32_t m = div_by(rem, sp.mul_O), o = rem - m * sp.O;
     // State of the scan's fused reduction.
     if (reset.done && rem == 0)
         reset.done[item] = 0;
@@ -82,7 +82,7 @@ option_terms_kernel(SpaceDev sp, TablesDev tb, QueryDev q, uint32_t count, uint2
         lambda = query_value(q.lambda, q.lambda1, item);
     }
 
-    const OptionTerm term = option_term(sp, tb, inst, m, o, lambda);
+    const OptionTerm term = option_term(sp, tb, inst, m, o, (uint32_t)lambda);
     const uint64_t c = term.c;
     const bool ok = term.ok, thr = term.thr;
     const uint32_t tau = term.tau;
@@ -351,10 +351,13 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
     FusedLds flds{};
     const uint2 *s_inner = nullptr;     // FUSED: the inner LLM's records, in LDS
     __shared__ uint2 s_last[FUSED ? ALP_MAX_OPTIONS : 1];
-    // FUSED: the item's profile curves (rate, then lat: 2 * curves * K words) and the curves'
-    // allowed flags in dynamic LDS (fused_lds_bytes), each LLM's W, n, p.
-    extern __shared__ uint32_t s_curve[];
-    __shared__ ulonglong2 s_llm[FUSED ? ALP_MAX_LLMS : 1];
+    // FUSED: the item's profile curves and their deployability in dynamic LDS (layout as
+    // fused_lds_bytes counts it); tp * q of every (tp, share) pair, each LLM's inputs and the
+    // reciprocals of 1000 d (see FusedLds).
+    extern __shared__ uint4 s_dyn[];
+    __shared__ LlmInputs s_llm[FUSED ? ALP_MAX_LLMS : 1];
+    __shared__ uint32_t s_tpq[FUSED ? ALP_MAX_TP * ALP_MAX_FRAC : 1];
+    __shared__ double s_inv_dd[FUSED ? ALP_MAX_REPLICAS : 1];
     if constexpr (FUSED) {
         uint32_t cap;
         if (fz.raw.budget) {
@@ -374,32 +377,66 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
         uint2 *blk_inner = blk + M * O;
         const uint32_t stride = inner_stride(O);
         // The item's profile curves (one per LLM, tp and share; shared by the replica counts)
-        // staged in LDS by one load per point, all in flight together, with each LLM's W, n, p.
+        // staged in LDS by one load per point, all in flight together, the rates padded to
+        // ALP_MAX_POINTS points with the last one; each curve's deployability, tp * q of every
+        // pair, each LLM's inputs and the reciprocals of 1000 d.
         const SpaceDev &sp = fa.sp;
-        const uint32_t K = sp.K, curves = M * sp.n_tp * sp.n_fq;
+        const uint32_t K = sp.K, curves = M * sp.n_tp * sp.n_fq, pairs = sp.n_tp * sp.n_fq;
         const uint64_t base = (uint64_t)f_inst * curves;
-        uint8_t *s_allowed = reinterpret_cast<uint8_t *>(s_curve + 2 * curves * K);
-        uint2 *s_inner_w = reinterpret_cast<uint2 *>(reinterpret_cast<uint8_t *>(s_curve) +
-                                                     fused_lds_inner_offset(sp));
-        uint2 *s_ext_w = reinterpret_cast<uint2 *>(reinterpret_cast<uint8_t *>(s_curve) +
-                                                   fused_lds_ext_offset(sp));
-        flds = FusedLds{s_curve, s_allowed, s_llm, s_ext_w};
+        uint8_t *s_base = reinterpret_cast<uint8_t *>(s_dyn);
+        uint32_t *s_rate = reinterpret_cast<uint32_t *>(s_base);
+        uint32_t *s_lat = reinterpret_cast<uint32_t *>(s_base + fused_lds_lat_offset(sp));
+        uint8_t *s_deploy = s_base + fused_lds_deploy_offset(sp);
+        uint2 *s_inner_w = reinterpret_cast<uint2 *>(s_base + fused_lds_inner_offset(sp));
+        uint2 *s_ext_w = reinterpret_cast<uint2 *>(s_base + fused_lds_ext_offset(sp));
+        flds = FusedLds{s_rate, s_lat, s_deploy, s_tpq, s_llm, s_inv_dd, s_ext_w};
         s_inner = s_inner_w;
-        for (uint32_t a = threadIdx.x; a < curves * K; a += blockDim.x) {
-            s_curve[a] = fz.tb.rate[base * K + a];
-            s_curve[curves * K + a] = fz.tb.lat[base * K + a];
+        // Stores point a (rate padded past K - 1).
+        const uint64_t lm0 = (uint64_t)f_inst * M;
+        auto put_point = [&](uint32_t a, uint32_t rate, uint32_t lat) {
+            const uint32_t c = a / K, k = a - c * K;
+            s_lat[a] = lat;
+            s_rate[c * ALP_MAX_POINTS + k] = rate;
+            if (k == K - 1)
+                for (uint32_t kk = K; kk < ALP_MAX_POINTS; ++kk)
+                    s_rate[c * ALP_MAX_POINTS + kk] = rate;
+        };
+        // tp and q of curve (or pair) a.
+        auto curve_tp = [&](uint32_t a) { return sp.tp(a % pairs / sp.n_fq); };
+        auto curve_fq = [&](uint32_t a) { return sp.fq(a % pairs % sp.n_fq); };
+        // Every thread's first point, curve, pair and LLM are read together, at indices clamped
+        // into the item's tables (a thread past the end reads the last entry and stores
+        // nothing), so that the reads are in flight at once; further points and curves (blocks
+        // smaller than the item's tables) follow.
+        {
+            const uint32_t t = threadIdx.x, points = curves * K;
+            const uint32_t ap = t < points ? t : points - 1, ac = t < curves ? t : curves - 1;
+            const uint32_t am = t < M ? t : M - 1;
+            const uint32_t rate = fz.tb.rate[base * K + ap], lat = fz.tb.lat[base * K + ap];
+            const uint8_t allowed = fz.tb.allowed[base + ac];
+            const uint64_t W = fz.tb.W[lm0 + ac / pairs];
+            const uint32_t n = fz.tb.n[lm0 + am], p = fz.tb.p[lm0 + am];
+            const uint32_t tp = curve_tp(ac), fq = curve_fq(ac);
+            if (t < sp.D)
+                s_inv_dd[t] = recip_low<1, 40>(1000u * (t + 1));
+            if (t < points)
+                put_point(t, rate, lat);
+            if (t < curves)
+                s_deploy[t] = deployable(sp, fz.tb.H, allowed != 0, W, tp * fq);
+            if (t < pairs)
+                s_tpq[t] = tp * fq;                  // curve t < pairs is pair t's
+            if (t < M)
+                s_llm[t] = llm_inputs(n, p);
         }
-        for (uint32_t a = threadIdx.x; a < curves; a += blockDim.x)
-            s_allowed[a] = fz.tb.allowed[base + a];
-        if (threadIdx.x < M) {
-            const uint64_t lm = (uint64_t)f_inst * M + threadIdx.x;
-            s_llm[threadIdx.x] = make_ulonglong2(fz.tb.W[lm],
-                                                 (uint64_t)fz.tb.n[lm] << 32 | fz.tb.p[lm]);
-        }
+        for (uint32_t a = threadIdx.x + blockDim.x; a < curves * K; a += blockDim.x)
+            put_point(a, fz.tb.rate[base * K + a], fz.tb.lat[base * K + a]);
+        for (uint32_t a = threadIdx.x + blockDim.x; a < curves; a += blockDim.x)
+            s_deploy[a] = deployable(sp, fz.tb.H, fz.tb.allowed[base + a] != 0,
+                                     fz.tb.W[lm0 + a / pairs], curve_tp(a) * curve_fq(a));
         __syncthreads();
         for (uint32_t a = threadIdx.x; a < M * O; a += blockDim.x) {
-            const uint32_t m = a / O, o = a - m * O;
-            const OptionTerm t = flds.term(sp, fz.tb.H, m, o, f_lambda);
+            const uint32_t m = div_by(a, sp.mul_O), o = a - m * O;
+            const OptionTerm t = flds.term(sp, m, o, (uint32_t)f_lambda);
             s_ext_w[a] = make_uint2(t.tau, t.u);
             const bool usable = t.ok && t.thr;
             const uint2 r = make_uint2(usable ? t.c : 0u, usable ? t.u : kSentinelUnits);

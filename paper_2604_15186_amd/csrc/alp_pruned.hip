@@ -147,7 +147,7 @@ pruned_scatter_kernel(SpaceDev sp, const uint2 *__restrict__ rec, uint32_t count
     if (u >= F1)
         return;
     const uint32_t ij = o / sp.D;
-    const uint32_t tp = sp.tp[ij / sp.n_fq], q = sp.fq[ij % sp.n_fq], d = o % sp.D + 1;
+    const uint32_t tp = sp.tp(ij / sp.n_fq), q = sp.fq(ij % sp.n_fq), d = o % sp.D + 1;
     const uint64_t key = ((uint64_t)e.x << 32) | o;
     for (uint32_t r = 0; r < sp.Q; ++r)
         if (placement_fits(sp.Q, r, u, tp, q, d))

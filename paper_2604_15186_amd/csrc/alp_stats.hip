@@ -602,7 +602,8 @@ __global__ void __launch_bounds__(64 * kSweepWaves) trace_sweep_kernel(StatsArgs
             if (k0 + j >= rows)
                 break;                                 // uniform
             const int32_t idx = (int32_t)n - 1 - (int32_t)(64 * (k0 + j) + lane);
-            const uint64_t i = lo + (uint64_t)(idx < 0 ? 0 : idx);   // lanes past the first call
+            // a lane before the trace's first call reads that call again (masked below)
+            const uint64_t i = lo + (uint64_t)(idx < 0 ? 0 : idx);
             R.m[j] = a.llm[i];
             R.s[j] = a.start[i];
             R.e[j] = a.end[i];
@@ -674,7 +675,6 @@ __global__ void __launch_bounds__(64 * kSweepWaves) trace_sweep_kernel(StatsArgs
         if ((uint32_t)q < M)
             wave_add_sums((uint32_t)q, calls[q], busy[q], active[q], copy);
 }
-
 
 // Called, once its traces are summed, by every block of the sort and long passes that had
 // work: participant i of P.  The last of them (over both launches) takes the totals -- reading

@@ -264,6 +264,91 @@ def test_ragged_and_degenerate_spaces(alp, spec):
                                   np.where(want["L"] == (1 << 64) - 1, NONE32, want["L"]))
 
 
+def _extreme_batch(seed, K, count=2):
+    """Instances whose inputs span the documented ranges rather than a workload's: n and p from
+    1 to 2^31 - 1 (with both ends), rates anywhere below 2^31 with gaps of 1 as well as wide
+    ones, latencies in any order up to what the 32-bit latency bound allows (2^31 - 1 where p / n
+    permits, 0 where it does not), weights from 1 byte to 2^40 (some do not fit) and denied
+    pairs.  3 LLMs of 60 options: 216,000 candidates per instance."""
+    rng = np.random.default_rng([2604, 15186, 77, seed, K])
+    tps, fqs, Q, D, M = (1, 2, 4, 8), (1, 2, 4), 4, 5, 3
+    nt, nf, B = len(tps), len(fqs), count
+
+    def logu(lo, hi, size):
+        v = np.exp(rng.uniform(np.log(lo), np.log(hi + 1.0), size)).astype(np.int64)
+        return np.clip(v, lo, hi)
+
+    n = logu(1, 2**31 - 1, (B, M))
+    p = logu(1, 2**31 - 1, (B, M))
+    n[0, 0], p[0, 0], n[0, 1], p[0, 1] = 1, 2**31 - 1, 2**31 - 1, 2**31 - 1
+    W = logu(1, 2**40, (B, M))
+    allowed = (rng.uniform(size=(B, M, nt, nf)) < 0.85).astype(np.uint8)
+    rate = np.zeros((B, M, nt, nf, K), np.int64)
+    lat = np.zeros((B, M, nt, nf, K), np.int64)
+    for b in range(B):
+        for m in range(M):
+            # every latency term of the LLM stays within (2^32 - 2) / M, so the instance passes
+            # the load-time bound on the latency sum
+            lmax = min(2**31 - 1, ((2**32 - 2) // M) * int(p[b, m]) // int(n[b, m]))
+            for i in range(nt):
+                for j in range(nf):
+                    r = [int(logu(1, 2**29, 1)[0])]
+                    for _ in range(K - 1):
+                        gap = 1 if rng.uniform() < 0.3 else int(logu(1, 2**27, 1)[0])
+                        r.append(min(r[-1] + gap, 2**31 - 1 - (K - len(r))))
+                    rate[b, m, i, j] = r
+                    top = lmax if rng.uniform() < 0.3 else int(rng.integers(0, lmax + 1))
+                    lat[b, m, i, j] = rng.integers(0, top + 1, K)
+    space = {"M": M, "tp": np.asarray(tps, np.uint32), "fq": np.asarray(fqs, np.uint32), "Q": Q,
+             "D": D, "K": K}
+    return {"space": space, "H": 1 << 40, "W": W.astype(np.uint64), "n": n.astype(np.uint32),
+            "p": p.astype(np.uint32), "allowed": allowed, "rate": rate.astype(np.uint32),
+            "lat": lat.astype(np.uint32), "u_ppm": np.full(B, 500_000, np.uint32),
+            "G": np.full(B, 64, np.uint32), "cfg": None, "instances": list(range(B)),
+            "name": f"extreme-{seed}-{K}"}
+
+
+@pytest.mark.parametrize("K", [1, 2, 7, 16])
+def test_option_terms_over_the_input_ranges(alp, K):
+    """Every candidate's evaluation, the argmin (one launch and separate option terms) and the
+    maximum throughput against the oracle, on inputs at the edges of their ranges: saturated
+    normalised throughputs (n = 1), thresholds hit exactly (lambda = floor(1000 d T / n) and one
+    more), loads on profile points and in unit-width segments, latency terms near the 32-bit
+    bound, one-point curves."""
+    b = _extreme_batch(5 + K, K)
+    rng = np.random.default_rng([2604, 15186, 78, K])
+    sp = b["space"]
+    O = len(sp["tp"]) * len(sp["fq"]) * sp["D"]
+    with alp.Context(b) as ctx:
+        tms = ctx.max_throughput([64, 64])
+        for i in range(2):
+            inst = oracle.Instance(b, i)
+            assert int(tms[i]) == oracle.tmax(inst, 64)
+            lams = {1, 2**32 - 1, int(tms[i]) or 1}
+            lams |= {int(v) for v in np.exp(rng.uniform(0, np.log(2.0**32 - 1), 4))}
+            for _ in range(3):
+                m, o = int(rng.integers(0, 3)), int(rng.integers(0, O))
+                d, ij = o % sp["D"] + 1, o // sp["D"]
+                T = int(b["rate"][i, m, ij // len(sp["fq"]), ij % len(sp["fq"]), K - 1])
+                edge = 1000 * d * T // int(b["n"][i, m])
+                lams |= {v for v in (edge, edge + 1) if 1 <= v < 2**32}
+            xs = np.arange(inst.N, dtype=np.uint64)
+            for lam in sorted(lams):
+                want = oracle.evaluate_many(inst, 64, lam, xs)
+                got = ctx.eval_candidates(i, 64, lam, xs)
+                assert np.array_equal(got["flags"], want["flags"]), lam
+                assert np.array_equal(got["latency_us"].astype(np.uint64),
+                                      np.where(want["L"] == (1 << 64) - 1, NONE32, want["L"])), lam
+                assert np.array_equal(got["throughput_milli"].astype(np.uint64), want["T"]), lam
+                assert np.array_equal(got["gpu_units"].astype(np.uint64), want["U"]), lam
+                for g in (8, 64):
+                    expect = oracle_expect(b, i, g, lam)
+                    for variant in (0, 1 | SEP):
+                        ctx.set_launch(variant)
+                        check_result(b, i, ctx.search(i, g, lam), *expect)
+                    ctx.set_launch(0)
+
+
 def test_batch_edge_cases(alp):
     b = make_batch(1, range(3))
     with alp.Context(b) as ctx:
