@@ -11,6 +11,7 @@
 
 #include <algorithm>
 #include <array>
+#include <chrono>
 #include <new>
 #include <vector>
 
@@ -155,6 +156,9 @@ struct alp_ctx {
     alp_result_t *host_results = nullptr;   // pinned host memory the kernels write results to
     alp_result_t *host_results_dev = nullptr;  // its device-visible address
     size_t host_results_cap = 0;
+    uint32_t *host_signal = nullptr;        // mapped word a single search's record signals in
+    uint32_t *host_signal_dev = nullptr;    // (FinishArgs::signal), and its device address
+    uint32_t call_seq = 0;                  // the last sequence number signalled
 
     uint32_t variant = 0, bpi_override = 0, tpb_override = 0, chunks_override = 0;
     int occupancy_cache[4][4][17] = {};   // [variant][log2 slots][threads / 64]: blocks per CU
@@ -543,6 +547,19 @@ int32_t upload_queries(alp_ctx *c, uint32_t count, const uint32_t *inst, const u
 
 int32_t ensure_host_results(alp_ctx *c, size_t count)
 {
+    if (!c->host_signal) {
+        void *h = nullptr, *d = nullptr;
+        hipError_t e = alloc_pinned(&h, 64, hipHostMallocMapped);
+        if (e != hipSuccess)
+            return hip_fail(e, "hipHostMalloc(signal)");
+        if ((e = hipHostGetDevicePointer(&d, h, 0)) != hipSuccess) {
+            (void)hipHostFree(h);
+            return hip_fail(e, "hipHostGetDevicePointer(signal)");
+        }
+        c->host_signal = (uint32_t *)h;
+        c->host_signal_dev = (uint32_t *)d;
+        __atomic_store_n(c->host_signal, 0u, __ATOMIC_RELEASE);
+    }
     if (count <= c->host_results_cap)
         return ALP_OK;
     void *grown = nullptr, *grown_dev = nullptr;
@@ -640,7 +657,7 @@ int32_t context_scratch(alp_ctx *c, uint32_t count, const alp::ScanGeometry &g, 
 // stamped by the dispatches.
 int32_t launch_search_with(alp_ctx *c, const alp::QueryDev &q, uint32_t count, alp_result_t *out,
                            const alp::RawQueries *raw, hipEvent_t *ev, const alp::ScanGeometry &g,
-                           const SearchScratch &s)
+                           const SearchScratch &s, uint32_t *signal = nullptr, uint32_t seq = 0)
 {
     const bool timed = ev != nullptr;
     const alp::SpaceDev &sp = c->sp;
@@ -651,6 +668,8 @@ int32_t launch_search_with(alp_ctx *c, const alp::QueryDev &q, uint32_t count, a
         alp::FinishArgs fa{};
         fa.sp = sp;
         fa.out = out;
+        fa.signal = signal;
+        fa.seq = seq;
         alp::FusedArgs fz{};
         fz.tb = c->tdev;
         if (raw)
@@ -674,6 +693,8 @@ int32_t launch_search_with(alp_ctx *c, const alp::QueryDev &q, uint32_t count, a
     fa.best = s.best;
     fa.out = out;
     fa.invalid = raw ? raw->invalid : nullptr;
+    fa.signal = signal;
+    fa.seq = seq;
     alp::ScanReset reset;
     reset.done = s.done;
     reset.best = s.best;
@@ -699,7 +720,8 @@ int32_t launch_search_with(alp_ctx *c, const alp::QueryDev &q, uint32_t count, a
 
 // launch_search_with on the context's own (growing) scratch buffers.
 int32_t launch_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count, alp_result_t *out,
-                      const alp::RawQueries *raw, hipEvent_t *ev)
+                      const alp::RawQueries *raw, hipEvent_t *ev, uint32_t *signal = nullptr,
+                      uint32_t seq = 0)
 {
     alp::ScanGeometry g;
     int32_t st = plan_scan(c, count, g);
@@ -708,20 +730,45 @@ int32_t launch_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count, alp_re
     SearchScratch s;
     if ((st = context_scratch(c, count, g, s)) != ALP_OK)
         return st;
-    return launch_search_with(c, q, count, out, raw, ev, g, s);
+    return launch_search_with(c, q, count, out, raw, ev, g, s, signal, seq);
 }
 
-// Synchronous searches: results in the context's mapped host buffer.
+// Synchronous searches: results in the context's mapped host buffer.  A single untimed search
+// has its record signalled in host memory (FinishArgs::signal): the caller reads it as soon as
+// the kernel's last block has written it, rather than after the kernel's completion reaches
+// the host.  After the first millisecond the wait also polls the stream, once a millisecond
+// (a poll costs microseconds, so it stays off the path of short searches); a stream that ends
+// (or fails) without the signal falls back to the synchronisation, which reports any error.
 int32_t run_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count)
 {
     int32_t st = ensure_host_results(c, count);
     if (st != ALP_OK)
         return st;
-    if ((st = launch_search(c, q, count, c->host_results_dev, nullptr, c->timing ? c->ev : nullptr)) !=
-        ALP_OK)
+    const bool signalled = count == 1 && !c->timing;
+    uint32_t seq = 0;
+    if (signalled && ++c->call_seq == 0)
+        ++c->call_seq;                         // 0 is the word's initial value
+    if (signalled)
+        seq = c->call_seq;
+    if ((st = launch_search(c, q, count, c->host_results_dev, nullptr, c->timing ? c->ev : nullptr,
+                            signalled ? c->host_signal_dev : nullptr, seq)) != ALP_OK)
         return st;
-    hipError_t e;
-    if ((e = hipStreamSynchronize(c->stream)) != hipSuccess)
+    hipError_t e = hipSuccess;
+    bool seen = false;
+    auto poll_at = std::chrono::steady_clock::now() + std::chrono::milliseconds(1);
+    for (uint32_t k = 1; signalled; ++k) {
+        if (__atomic_load_n(c->host_signal, __ATOMIC_ACQUIRE) == seq) {
+            seen = true;
+            break;
+        }
+        if ((k & 255) == 0 && std::chrono::steady_clock::now() >= poll_at) {
+            if (hipStreamQuery(c->stream) != hipErrorNotReady)
+                break;
+            poll_at = std::chrono::steady_clock::now() + std::chrono::milliseconds(1);
+        }
+        __builtin_ia32_pause();
+    }
+    if (!seen && (e = hipStreamSynchronize(c->stream)) != hipSuccess)
         return hip_fail(e, "hipStreamSynchronize");
     if (c->timing) {
         c->last_ms[0] = 0.0f;                  // no option-term kernel in the one-launch form
@@ -1548,6 +1595,8 @@ void alp_free(alp_ctx *ctx)
         b->release();
     if (ctx->host_results)
         (void)hipHostFree(ctx->host_results);
+    if (ctx->host_signal)
+        (void)hipHostFree(ctx->host_signal);
     if (ctx->host_query)
         (void)hipHostFree(ctx->host_query);
     if (ctx->host_split)

@@ -186,7 +186,8 @@ __device__ __forceinline__ uint32_t candidate_digit(const SpaceDev &sp, uint64_t
 // sums U, and lane 0 writes.
 __device__ __forceinline__ void write_result_lanes(const SpaceDev &sp, uint32_t o, uint32_t T,
                                                    uint32_t U, uint32_t L, uint64_t x,
-                                                   uint64_t *dst, uint32_t status_if_none)
+                                                   uint64_t *dst, uint32_t status_if_none,
+                                                   uint32_t *signal = nullptr, uint32_t seq = 0)
 {
     const uint32_t lane = threadIdx.x & 63;
     uint64_t tp = 0, fq = 0, rep = 0;
@@ -221,28 +222,23 @@ __device__ __forceinline__ void write_result_lanes(const SpaceDev &sp, uint32_t 
     combine(std::integral_constant<int, 0x141>{});
     if (lane != 0)
         return;
-    if (L == kNoLatency) {
-        dst[0] = ALP_NO_INDEX;
-        dst[1] = 0;
-        dst[2] = (uint64_t)status_if_none << 32;
-        dst[3] = 0;
-        dst[4] = 0;
-        dst[5] = 0;
-        return;
-    }
-    dst[0] = x;
-    dst[1] = (uint64_t)L | ((uint64_t)T << 32);
-    dst[2] = (uint64_t)U | ((uint64_t)ALP_OK << 32);
-    dst[3] = tp;
-    dst[4] = fq;
-    dst[5] = rep;
+    const bool none = L == kNoLatency;
+    dst[0] = none ? ALP_NO_INDEX : x;
+    dst[1] = none ? 0 : (uint64_t)L | ((uint64_t)T << 32);
+    dst[2] = none ? (uint64_t)status_if_none << 32 : (uint64_t)U | ((uint64_t)ALP_OK << 32);
+    dst[3] = none ? 0 : tp;
+    dst[4] = none ? 0 : fq;
+    dst[5] = none ? 0 : rep;
+    if (signal)
+        __hip_atomic_store(signal, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
 // The result record of winner (L, x), with the per-LLM choices decoded from x and T and U read
 // from the item's per-option records E (lane m loads LLM m's: one memory round trip for all).
 __device__ __forceinline__ void write_result(const SpaceDev &sp, const uint2 *E, uint32_t L,
                                              uint64_t x, uint64_t *dst,
-                                             uint32_t status_if_none = ALP_INFEASIBLE)
+                                             uint32_t status_if_none = ALP_INFEASIBLE,
+                                             uint32_t *signal = nullptr, uint32_t seq = 0)
 {
     const uint32_t lane = threadIdx.x & 63;
     uint32_t o = 0, T = 0xFFFFFFFFu, U = 0;
@@ -252,7 +248,7 @@ __device__ __forceinline__ void write_result(const SpaceDev &sp, const uint2 *E,
         T = e.x;
         U = e.y & 0xFFFFu;
     }
-    write_result_lanes(sp, o, T, U, L, x, dst, status_if_none);
+    write_result_lanes(sp, o, T, U, L, x, dst, status_if_none, signal, seq);
 }
 
 // Result record of one item whose winner is (L, x), by one wave.  E: the item's per-option
@@ -265,7 +261,7 @@ __device__ __forceinline__ void write_item_result(const FinishArgs &fa, uint32_t
         E = fa.ext + (uint64_t)item * fa.sp.M * fa.sp.O;
     write_result(fa.sp, E, rejected ? kNoLatency : L, x,
                  reinterpret_cast<uint64_t *>(fa.out + item),
-                 rejected ? (uint32_t)ALP_EINVAL : (uint32_t)ALP_INFEASIBLE);
+                 rejected ? (uint32_t)ALP_EINVAL : (uint32_t)ALP_INFEASIBLE, fa.signal, fa.seq);
 }
 
 // Writes the block's winner and counts the block as finished (agent-scope fence and per-item
@@ -557,11 +553,11 @@ struct FusedLds {
 
 // Result record of a one-launch item whose winner is (L, x), by one wave: lane m reads LLM m's
 // option terms of the winner from the block's LDS.  A rejected query gets ALP_EINVAL.
-__device__ __forceinline__ void write_fused_result(const SpaceDev &sp, uint64_t H,
-                                                   const FusedLds &lds, uint64_t lambda,
+__device__ __forceinline__ void write_fused_result(const FinishArgs &fa, const FusedLds &lds,
                                                    bool rejected, uint32_t L, uint64_t x,
-                                                   alp_result_t *dst)
+                                                   uint32_t item)
 {
+    const SpaceDev &sp = fa.sp;
     const uint32_t lane = threadIdx.x & 63;
     if (rejected)
         L = kNoLatency;
@@ -572,8 +568,9 @@ __device__ __forceinline__ void write_fused_result(const SpaceDev &sp, uint64_t 
         T = e.x;
         U = e.y;
     }
-    write_result_lanes(sp, o, T, U, L, x, reinterpret_cast<uint64_t *>(dst),
-                       rejected ? (uint32_t)ALP_EINVAL : (uint32_t)ALP_INFEASIBLE);
+    write_result_lanes(sp, o, T, U, L, x, reinterpret_cast<uint64_t *>(fa.out + item),
+                       rejected ? (uint32_t)ALP_EINVAL : (uint32_t)ALP_INFEASIBLE, fa.signal,
+                       fa.seq);
 }
 
 // End of a one-launch block: the block's lowest (L, x) (x < 2^32) joins the item's word by an
@@ -585,15 +582,15 @@ __device__ __forceinline__ void write_fused_result(const SpaceDev &sp, uint64_t 
 __device__ __forceinline__ void block_finish_fused(uint32_t L, uint64_t x, uint32_t item,
                                                    uint32_t sub, uint32_t blocks_per_item,
                                                    const FinishArgs &fa, const FusedArgs &fz,
-                                                   const FusedLds &lds, uint64_t lambda,
-                                                   bool rejected, uint32_t hint, bool held)
+                                                   const FusedLds &lds, bool rejected,
+                                                   uint32_t hint, bool held)
 {
     __shared__ uint32_t last_block;
     __shared__ unsigned long long s_word;
     if (blocks_per_item == 1) {
         block_min(L, x);
         if (threadIdx.x < 64)
-            write_fused_result(fa.sp, fz.tb.H, lds, lambda, rejected, L, x, fa.out + item);
+            write_fused_result(fa, lds, rejected, L, x, item);
         return;
     }
     if (held)
@@ -625,7 +622,7 @@ __device__ __forceinline__ void block_finish_fused(uint32_t L, uint64_t x, uint3
         return;
     const unsigned long long w = ~s_word;
     const uint32_t Lw = s_word ? (uint32_t)(w >> 32) : kNoLatency;
-    write_fused_result(fa.sp, fz.tb.H, lds, lambda, rejected, Lw, (uint32_t)w, fa.out + item);
+    write_fused_result(fa, lds, rejected, Lw, (uint32_t)w, item);
 }
 
 // Workgroups are dispatched to the 8 XCDs round-robin; renumber them so that consecutive

@@ -95,6 +95,11 @@ struct FinishArgs {
     alp_result_t *out;         // per-item results (device-visible, may be mapped host memory)
     const uint32_t *invalid;   // per-item: nonzero = the query was rejected (result EINVAL);
                                // nullptr = every query valid
+    // A search of one item whose caller waits for its record in host memory: once the record is
+    // written, seq is stored to *signal (mapped host memory) with a release at system scope, so
+    // a host that reads seq there also reads the whole record.  nullptr: no signal.
+    uint32_t *signal = nullptr;
+    uint32_t seq = 0;
 };
 
 // Launch geometry of one scan.

@@ -407,9 +407,11 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
         // Every thread's first point, curve, pair and LLM are read together, at indices clamped
         // into the item's tables (a thread past the end reads the last entry and stores
         // nothing), so that the reads are in flight at once; further points and curves (blocks
-        // smaller than the item's tables) follow.
-        {
-            const uint32_t t = threadIdx.x, points = curves * K;
+        // smaller than the item's tables) follow.  Waves past every table (points are the most
+        // entries, but for the D reciprocals) skip it.
+        const uint32_t points = curves * K;
+        if (wave * 64 < (points > sp.D ? points : sp.D)) {
+            const uint32_t t = threadIdx.x;
             const uint32_t ap = t < points ? t : points - 1, ac = t < curves ? t : curves - 1;
             const uint32_t am = t < M ? t : M - 1;
             const uint32_t rate = fz.tb.rate[base * K + ap], lat = fz.tb.lat[base * K + ap];
@@ -768,8 +770,8 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
         waveX = wave_min_u64(xmin);
     }
     if constexpr (FUSED)
-        block_finish_fused(waveL, waveX, item, sub, blocks_per_item, fa, fz, flds, f_lambda,
-                           f_rejected, block_hint, held);
+        block_finish_fused(waveL, waveX, item, sub, blocks_per_item, fa, fz, flds, f_rejected,
+                           block_hint, held);
     else
         block_finish(waveL, waveX, item, sub, blocks_per_item, winners, fa, block_hint, held);
 }
