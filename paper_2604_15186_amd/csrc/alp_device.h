@@ -641,5 +641,21 @@ __device__ __forceinline__ uint32_t query_value(const uint32_t *arr, uint32_t si
     return arr ? arr[i] : single;
 }
 
+// Item i's query (instance, capacity, target): the three reads under one test, in flight
+// together (a test per read would wait for each before the next).
+__device__ __forceinline__ void load_query(const QueryDev &q, uint32_t i, uint32_t &inst,
+                                           uint32_t &cap, uint32_t &lambda)
+{
+    if (q.inst) {
+        inst = q.inst[i];
+        cap = q.capacity[i];
+        lambda = q.lambda[i];
+    } else {
+        inst = q.inst1;
+        cap = q.cap1;
+        lambda = q.lambda1;
+    }
+}
+
 }  // namespace
 }  // namespace alp

@@ -57,6 +57,7 @@ struct TablesDev {
 };
 
 // Per-item query: device arrays for batches, or by-value scalars for a single query.
+// The three arrays are set together or not at all.
 struct QueryDev {
     const uint32_t *inst;       // instance of item i, or nullptr -> inst1
     const uint32_t *capacity;   // share-unit capacity Q*G of item i (clamped), or nullptr -> cap1

@@ -64,12 +64,13 @@ option_terms_kernel(SpaceDev sp, TablesDev tb, QueryDev q, uint32_t count, uint2
     if (raw.budget) {
         // Queries in device memory: prepared here; item's first thread writes what the scan and
         // the result need.
+        // (budget and target first, as in the one-launch scan)
+        const uint64_t cap = (uint64_t)raw.units_per_gpu * raw.budget[item];
+        lambda = raw.target[item];
         inst = raw.inst ? raw.inst[item] : item;
         const bool bad = inst >= raw.B;
         inst = bad ? 0u : inst;
-        const uint64_t cap = (uint64_t)raw.units_per_gpu * raw.budget[item];
         capacity = cap > kCapacityMax ? kCapacityMax : (uint32_t)cap;
-        lambda = raw.target[item];
         if (rem == 0) {
             raw.q_inst[item] = inst;
             raw.q_cap[item] = capacity;
@@ -77,9 +78,9 @@ option_terms_kernel(SpaceDev sp, TablesDev tb, QueryDev q, uint32_t count, uint2
             raw.invalid[item] = bad ? 1u : 0u;
         }
     } else {
-        inst = query_value(q.inst, q.inst1, item);
-        capacity = query_value(q.capacity, q.cap1, item);
-        lambda = query_value(q.lambda, q.lambda1, item);
+        uint32_t lam;
+        load_query(q, item, inst, capacity, lam);
+        lambda = lam;
     }
 
     const OptionTerm term = option_term(sp, tb, inst, m, o, (uint32_t)lambda);
@@ -335,6 +336,16 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
     // `chunks` consecutive ranges of the inner LLM's records (DYNAMIC only), so that small
     // spaces still give every wave several sub-rows; candidates stay in index order (row,
     // record, option).  Without DYNAMIC, chunks = 1 and each wave walks a fixed range of rows.
+    if constexpr (FUSED) {
+        // Kernel arguments are read through the scalar cache, a memory round trip for each
+        // 64-byte line first read.  One field of every line the prologue reads (the space, M
+        // and O, the block regions, the queries and tables, the block size) is taken here as
+        // an input of an empty statement, so all lines arrive in the first round trip rather
+        // than one after another, some after the query.
+        asm volatile("" ::"s"(M), "s"(rows), "s"(nblocks), "s"(fa.sp.tp8), "s"(fa.out),
+                     "s"(fz.tb.rate), "s"(fz.raw.budget), "s"(fz.regions), "s"(fz.best),
+                     "s"(blockDim.x));
+    }
     if (!DYNAMIC)
         chunks = 1;
     const uint32_t lb = xcd_logical_block(blockIdx.x, nblocks);
@@ -361,16 +372,18 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
     if constexpr (FUSED) {
         uint32_t cap;
         if (fz.raw.budget) {
+            // budget and target read first: the instance's read is conditional, and a
+            // conditional read is waited for where the paths join
+            const uint64_t c64 = (uint64_t)fz.raw.units_per_gpu * fz.raw.budget[item];
+            f_lambda = fz.raw.target[item];
             f_inst = fz.raw.inst ? fz.raw.inst[item] : item;
             f_rejected = f_inst >= fz.raw.B;
             f_inst = f_rejected ? 0u : f_inst;
-            const uint64_t c64 = (uint64_t)fz.raw.units_per_gpu * fz.raw.budget[item];
             cap = c64 > kCapacityMax ? kCapacityMax : (uint32_t)c64;
-            f_lambda = fz.raw.target[item];
         } else {
-            f_inst = query_value(q.inst, q.inst1, item);
-            cap = query_value(q.capacity, q.cap1, item);
-            f_lambda = query_value(q.lambda, q.lambda1, item);
+            uint32_t lam;
+            load_query(q, item, f_inst, cap, lam);
+            f_lambda = lam;
         }
         capacity = (int32_t)cap;
         uint2 *blk = fz.regions + (uint64_t)blockIdx.x * fz.region;
