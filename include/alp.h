@@ -143,7 +143,9 @@ int32_t alp_load_profiles(alp_ctx **out, const alp_space_t *space, uint32_t num_
  * Eq. 1 and its throughput by Eq. 2 (Section 4), over every candidate of the space; among equal
  * latencies the lowest candidate index.  A candidate is feasible iff every LLM's option is
  * deployable and its weights fit its share (Section 5, step 1), T_w >= target_milli, and
- * sum tp * q * d <= units_per_gpu * gpu_budget.  Synchronous on the context stream.  Returns
+ * sum tp * q * d <= units_per_gpu * gpu_budget.  Synchronous: returns once the search's last
+ * block has written the result to host memory (its exit may still be in flight on the context
+ * stream, ahead of any later work queued there).  Returns
  * ALP_OK with the result in *out, or ALP_INFEASIBLE with out->status = ALP_INFEASIBLE and
  * out->index = ALP_NO_INDEX.  EINVAL: ctx or out NULL, or instance >= num_instances (nothing
  * written).  ERANGE: the space cannot be covered by one launch.  ENOMEM/EDEVICE: allocation or
