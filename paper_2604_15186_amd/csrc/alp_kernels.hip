@@ -307,6 +307,28 @@ __device__ __forceinline__ void scalar_load16(const uint2 *p, uint2 (&a)[8], uin
     }
 }
 
+// The same, and lane 0 claims a sub-row meanwhile (see piped_min_8_claim): one wait for both.
+__device__ __forceinline__ void scalar_load16_claim(const uint2 *p, uint2 (&a)[8], uint2 (&b)[8],
+                                                    uint32_t la, uint64_t full,
+                                                    uint32_t &claimed)
+{
+    u32x16 x, y;
+    asm volatile("s_load_dwordx16 %[x], %[p], 0x0\n\t"
+                 "s_load_dwordx16 %[y], %[p], 0x40\n\t"
+                 "s_mov_b64 exec, 1\n\t"
+                 "ds_add_rtn_u32 %[cl], %[la], %[one]\n\t"
+                 "s_mov_b64 exec, %[full]\n\t"
+                 "s_waitcnt lgkmcnt(0)"
+                 : [x] "=&s"(x), [y] "=&s"(y), [cl] "=&v"(claimed)
+                 : [p] "s"(uniform_ptr(p)), [la] "v"(la), [one] "v"(1u), [full] "s"(full)
+                 : "memory");
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+        a[t] = make_uint2(x[2 * t], x[2 * t + 1]);
+        b[t] = make_uint2(y[2 * t], y[2 * t + 1]);
+    }
+}
+
 __device__ __forceinline__ uint2 scalar_load1(const uint2 *p)
 {
     uint64_t v;
@@ -316,6 +338,159 @@ __device__ __forceinline__ uint2 scalar_load1(const uint2 *p)
                  : "s"(uniform_ptr(p))
                  : "memory");
     return make_uint2((uint32_t)v, (uint32_t)(v >> 32));
+}
+
+// Software-pipelined record loop (one or two slots per lane): each statement loads the next 8
+// records while it processes the current 8 (x[2t] = c, x[2t + 1] = y of record t), and waits for
+// the load only at its end, so a wave waits for the scalar cache once per row rather than once
+// per 16 records.  Loaded registers are complete when the statement ends: nothing in flight
+// crosses a statement.
+#define ALP_ARGSX(x)                                                                               \
+    [c0] "s"(x[0]), [y0] "s"(x[1]), [c1] "s"(x[2]), [y1] "s"(x[3]), [c2] "s"(x[4]),                \
+        [y2] "s"(x[5]), [c3] "s"(x[6]), [y3] "s"(x[7]), [c4] "s"(x[8]), [y4] "s"(x[9]),            \
+        [c5] "s"(x[10]), [y5] "s"(x[11]), [c6] "s"(x[12]), [y6] "s"(x[13]), [c7] "s"(x[14]),       \
+        [y7] "s"(x[15])
+#define ALP_P1(T) ALP_CM("y" #T, "c" #T, "w0", "b0") ALP_RESTORE
+#define ALP_P2(T) ALP_CM("y" #T, "c" #T, "w0", "b0") ALP_CM("y" #T, "c" #T, "w1", "b1") ALP_RESTORE
+#define ALP_P1_8 ALP_P1(0) ALP_P1(1) ALP_P1(2) ALP_P1(3) ALP_P1(4) ALP_P1(5) ALP_P1(6) ALP_P1(7)
+#define ALP_P2_8 ALP_P2(0) ALP_P2(1) ALP_P2(2) ALP_P2(3) ALP_P2(4) ALP_P2(5) ALP_P2(6) ALP_P2(7)
+
+__device__ __forceinline__ u32x16 piped_min_8(uint32_t (&bq)[1], const int32_t (&w)[1],
+                                              const u32x16 &x, uint64_t full, const uint2 *pn)
+{
+    u32x16 nx;
+    asm volatile("s_load_dwordx16 %[nx], %[pn], 0x0\n\t" ALP_P1_8 "s_waitcnt lgkmcnt(0)"
+                 : [nx] "=&s"(nx), [b0] "+v"(bq[0])
+                 : [pn] "s"(uniform_ptr(pn)), [w0] "v"(w[0]), [full] "s"(full), ALP_ARGSX(x)
+                 : "vcc", "memory");
+    return nx;
+}
+
+__device__ __forceinline__ u32x16 piped_min_8(uint32_t (&bq)[2], const int32_t (&w)[2],
+                                              const u32x16 &x, uint64_t full, const uint2 *pn)
+{
+    u32x16 nx;
+    asm volatile("s_load_dwordx16 %[nx], %[pn], 0x0\n\t" ALP_P2_8 "s_waitcnt lgkmcnt(0)"
+                 : [nx] "=&s"(nx), [b0] "+v"(bq[0]), [b1] "+v"(bq[1])
+                 : [pn] "s"(uniform_ptr(pn)), [w0] "v"(w[0]), [w1] "v"(w[1]), [full] "s"(full),
+                   ALP_ARGSX(x)
+                 : "vcc", "memory");
+    return nx;
+}
+
+// The same, and lane 0 claims the wave's next sub-row meanwhile: an LDS atomic add of 1 at byte
+// address la (lane 0's result in claimed), complete when the statement ends.
+__device__ __forceinline__ u32x16 piped_min_8_claim(uint32_t (&bq)[1], const int32_t (&w)[1],
+                                                    const u32x16 &x, uint64_t full,
+                                                    const uint2 *pn, uint32_t la,
+                                                    uint32_t &claimed)
+{
+    u32x16 nx;
+    asm volatile("s_load_dwordx16 %[nx], %[pn], 0x0\n\t"
+                 "s_mov_b64 exec, 1\n\t"
+                 "ds_add_rtn_u32 %[cl], %[la], %[one]\n\t"
+                 "s_mov_b64 exec, %[full]\n\t" ALP_P1_8 "s_waitcnt lgkmcnt(0)"
+                 : [nx] "=&s"(nx), [cl] "=&v"(claimed), [b0] "+v"(bq[0])
+                 : [pn] "s"(uniform_ptr(pn)), [la] "v"(la), [one] "v"(1u), [w0] "v"(w[0]),
+                   [full] "s"(full), ALP_ARGSX(x)
+                 : "vcc", "memory");
+    return nx;
+}
+
+__device__ __forceinline__ u32x16 piped_min_8_claim(uint32_t (&bq)[2], const int32_t (&w)[2],
+                                                    const u32x16 &x, uint64_t full,
+                                                    const uint2 *pn, uint32_t la,
+                                                    uint32_t &claimed)
+{
+    u32x16 nx;
+    asm volatile("s_load_dwordx16 %[nx], %[pn], 0x0\n\t"
+                 "s_mov_b64 exec, 1\n\t"
+                 "ds_add_rtn_u32 %[cl], %[la], %[one]\n\t"
+                 "s_mov_b64 exec, %[full]\n\t" ALP_P2_8 "s_waitcnt lgkmcnt(0)"
+                 : [nx] "=&s"(nx), [cl] "=&v"(claimed), [b0] "+v"(bq[0]), [b1] "+v"(bq[1])
+                 : [pn] "s"(uniform_ptr(pn)), [la] "v"(la), [one] "v"(1u), [w0] "v"(w[0]),
+                   [w1] "v"(w[1]), [full] "s"(full), ALP_ARGSX(x)
+                 : "vcc", "memory");
+    return nx;
+}
+
+// The last 8 records of a row (nothing more to load).
+__device__ __forceinline__ void piped_last_8(uint32_t (&bq)[1], const int32_t (&w)[1],
+                                             const u32x16 &x, uint64_t full)
+{
+    asm volatile(ALP_P1_8
+                 : [b0] "+v"(bq[0])
+                 : [w0] "v"(w[0]), [full] "s"(full), ALP_ARGSX(x)
+                 : "vcc");
+}
+
+__device__ __forceinline__ void piped_last_8(uint32_t (&bq)[2], const int32_t (&w)[2],
+                                             const u32x16 &x, uint64_t full)
+{
+    asm volatile(ALP_P2_8
+                 : [b0] "+v"(bq[0]), [b1] "+v"(bq[1])
+                 : [w0] "v"(w[0]), [w1] "v"(w[1]), [full] "s"(full), ALP_ARGSX(x)
+                 : "vcc");
+}
+#undef ALP_P1_8
+#undef ALP_P2_8
+#undef ALP_P1
+#undef ALP_P2
+#undef ALP_ARGSX
+
+// A row's first 8 inner records and its NOUT outer records (digits o_0..o_{NOUT-1}) in one
+// round trip; the outer records' latency and share-unit sums go to oc and ou.
+template <int NOUT, int N>
+__device__ __forceinline__ u32x16 row_start_loads(const uint2 *R, uint32_t O,
+                                                  const uint32_t (&digit)[N], const uint2 *first,
+                                                  uint32_t &oc, int32_t &ou)
+{
+    static_assert(NOUT >= 0 && NOUT <= 3 && NOUT <= N, "outer digits loaded together");
+    u32x16 x;
+    uint64_t o[3] = {0, 0, 0};
+    const uint2 *pa = uniform_ptr(first);
+    if constexpr (NOUT == 0) {
+        asm volatile("s_load_dwordx16 %[a], %[pa], 0x0\n\t"
+                     "s_waitcnt lgkmcnt(0)"
+                     : [a] "=&s"(x)
+                     : [pa] "s"(pa)
+                     : "memory");
+    } else if constexpr (NOUT == 1) {
+        asm volatile("s_load_dwordx2 %[o0], %[p0], 0x0\n\t"
+                     "s_load_dwordx16 %[a], %[pa], 0x0\n\t"
+                     "s_waitcnt lgkmcnt(0)"
+                     : [a] "=&s"(x), [o0] "=&s"(o[0])
+                     : [pa] "s"(pa), [p0] "s"(uniform_ptr(R + digit[0]))
+                     : "memory");
+    } else if constexpr (NOUT == 2) {
+        asm volatile("s_load_dwordx2 %[o0], %[p0], 0x0\n\t"
+                     "s_load_dwordx2 %[o1], %[p1], 0x0\n\t"
+                     "s_load_dwordx16 %[a], %[pa], 0x0\n\t"
+                     "s_waitcnt lgkmcnt(0)"
+                     : [a] "=&s"(x), [o0] "=&s"(o[0]), [o1] "=&s"(o[1])
+                     : [pa] "s"(pa), [p0] "s"(uniform_ptr(R + digit[0])),
+                       [p1] "s"(uniform_ptr(R + O + digit[1]))
+                     : "memory");
+    } else {
+        asm volatile("s_load_dwordx2 %[o0], %[p0], 0x0\n\t"
+                     "s_load_dwordx2 %[o1], %[p1], 0x0\n\t"
+                     "s_load_dwordx2 %[o2], %[p2], 0x0\n\t"
+                     "s_load_dwordx16 %[a], %[pa], 0x0\n\t"
+                     "s_waitcnt lgkmcnt(0)"
+                     : [a] "=&s"(x), [o0] "=&s"(o[0]), [o1] "=&s"(o[1]), [o2] "=&s"(o[2])
+                     : [pa] "s"(pa), [p0] "s"(uniform_ptr(R + digit[0])),
+                       [p1] "s"(uniform_ptr(R + O + digit[1])),
+                       [p2] "s"(uniform_ptr(R + 2 * O + digit[2]))
+                     : "memory");
+    }
+    oc = 0;
+    ou = 0;
+#pragma unroll
+    for (int k = 0; k < NOUT; ++k) {
+        oc += (uint32_t)o[k];
+        ou += (int32_t)(uint32_t)(o[k] >> 32);
+    }
+    return x;
 }
 
 // FUSED: the one-launch form (see FusedArgs) -- the block first computes its item's option
@@ -519,6 +694,11 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
     const uint32_t chunk_len = n_inner_padded / chunks;   // a multiple of 16
     const uint32_t n_inner = has_inner ? (pair ? O * O : O) : 1;
     constexpr int NMAX = NOUT >= 0 ? NOUT : (int)kMaxOuter;
+    // One or two slots and at most three outer digits: the pipelined record loop -- except
+    // for the one-launch form with claimed sub-rows (the single small searches, rows of a few
+    // hundred records at 4 waves per SIMD), where its extra scalar registers cost more reloads
+    // per row than the loads it overlaps save.
+    constexpr bool kPiped = S <= 2 && NOUT >= 0 && NOUT <= 3 && !(FUSED && DYNAMIC);
     const uint32_t n_outer =
         NOUT >= 0 ? (uint32_t)NOUT : (M >= 2 + pair ? M - 2 - pair : 0);
 
@@ -591,31 +771,62 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
                 break;
             }
             const uint32_t tag = DYNAMIC ? cur : rr;
+            // The row's inner records (the table is padded to a multiple of 16 with records no
+            // lane can use).
+            const uint2 *const begin = DYNAMIC ? inner + chunk * chunk_len : inner;
+            const uint2 *const last16 = (DYNAMIC ? begin + chunk_len : inner + n_inner_padded) - 16;
             uint32_t oc = 0;
             int32_t ou = 0;
-#pragma unroll
-            for (int k = 0; k < NMAX; ++k) {
-                if (NOUT >= 0 || (uint32_t)k < n_outer) {
-                    const uint2 *rp = R + (uint64_t)k * O + digit[k];
-                    const uint2 v = FUSED ? scalar_load1(rp) : *rp;
-                    oc += v.x;
-                    ou += (int32_t)v.y;
-                }
-            }
             int32_t w[S];
             uint32_t bq[S];
+            auto row_init = [&]() {
 #pragma unroll
-            for (int s = 0; s < S; ++s) {
-                w[s] = u_last[s] + ou;
-                bq[s] = kNoLatency;
+                for (int s = 0; s < S; ++s) {
+                    w[s] = u_last[s] + ou;
+                    bq[s] = kNoLatency;
+                }
+            };
+            bool done_row = false;
+            if constexpr (kPiped) {
+                if (has_inner) {
+                    // 8 records per statement, the next 8 loading meanwhile.  The claim goes
+                    // out 8 records before the row's end, within a statement that completes
+                    // it.
+                    u32x16 a = row_start_loads<NOUT>(R, O, digit, begin, oc, ou);
+                    row_init();
+                    const uint2 *p = begin;
+                    for (; p != last16; p += 16) {
+                        const u32x16 b = piped_min_8(bq, w, a, full, p + 8);
+                        a = piped_min_8(bq, w, b, full, p + 16);
+                    }
+                    if constexpr (DYNAMIC) {
+                        typedef __attribute__((address_space(3))) uint32_t lds_u32;
+                        const uint32_t la = (uint32_t)(uintptr_t)(lds_u32 *)&s_next;
+                        const u32x16 b = piped_min_8_claim(bq, w, a, full, p + 8, la, next);
+                        piped_last_8(bq, w, b, full);
+                    } else {
+                        const u32x16 b = piped_min_8(bq, w, a, full, p + 8);
+                        piped_last_8(bq, w, b, full);
+                    }
+                    done_row = true;
+                }
             }
-            if (has_inner) {
-                // 16 records per iteration (the table is padded to a multiple of 16 with
-                // records no lane can use): two 64-byte scalar loads issued together, so the
+            if (!done_row) {
+#pragma unroll
+                for (int k = 0; k < NMAX; ++k) {
+                    if (NOUT >= 0 || (uint32_t)k < n_outer) {
+                        const uint2 *rp = R + (uint64_t)k * O + digit[k];
+                        const uint2 v = FUSED ? scalar_load1(rp) : *rp;
+                        oc += v.x;
+                        ou += (int32_t)v.y;
+                    }
+                }
+                row_init();
+            }
+            if (done_row) {
+            } else if (has_inner) {
+                // 16 records per iteration: two 64-byte scalar loads issued together, so the
                 // loop's own scalar work stays small next to the 2 x 16 x S VALU operations.
-                const uint2 *const begin = DYNAMIC ? inner + chunk * chunk_len : inner;
-                const uint2 *const last16 =
-                    (DYNAMIC ? begin + chunk_len : inner + n_inner_padded) - 16;
                 auto batch = [&](const uint2 *p) {
                     uint2 v0[8], v1[8];
                     if constexpr (FUSED) {
@@ -632,12 +843,22 @@ scan_min_kernel(const uint2 *__restrict__ rec, const uint2 *__restrict__ inner_a
                 };
                 for (const uint2 *p = begin; p != last16; p += 16)
                     batch(p);
-                // Claim the wave's next sub-row before the last 16 records, which hide the
-                // claim's latency; claiming earlier would commit a slowly issued wave to
-                // more work than the others while the block's range runs out.
-                if (DYNAMIC && lane == 0)
-                    next = atomicAdd(&s_next, 1u);
-                batch(last16);
+                // Claim the wave's next sub-row with the last 16 records; claiming earlier
+                // would commit a slowly issued wave to more work than the others while the
+                // block's range runs out.  The one-launch form issues the claim with the
+                // records' loads, under one wait.
+                if constexpr (FUSED && DYNAMIC) {
+                    typedef __attribute__((address_space(3))) uint32_t lds_u32;
+                    const uint32_t la = (uint32_t)(uintptr_t)(lds_u32 *)&s_next;
+                    uint2 v0[8], v1[8];
+                    scalar_load16_claim(last16, v0, v1, la, full, next);
+                    masked_min_8(bq, w, v0, full);
+                    masked_min_8(bq, w, v1, full);
+                } else {
+                    if (DYNAMIC && lane == 0)
+                        next = atomicAdd(&s_next, 1u);
+                    batch(last16);
+                }
             } else {
                 if (DYNAMIC && lane == 0)
                     next = atomicAdd(&s_next, 1u);
