@@ -16,6 +16,11 @@
 //                            in rows of 64 consecutive calls, without a sort: a call adds the part
 //                            of it before the earliest start of the same LLM's later calls.  Other
 //                            traces go to a work list.
+//   trace_wave_kernel        instead of the sweep, when the traces come out of end order: one
+//                            wave per trace of at most 2,048 calls sorts its calls by packed key
+//                            (llm << 61 | start << 32 | duration, starts within 2^29 us of a
+//                            reference) in registers and across lanes -- no LDS, no barrier --
+//                            and sweeps them as below; other traces go to the work list.
 //   trace_sort_kernel        the work list: calls sorted by key (llm << 60 | start), packed into
 //                            one 64-bit key when the starts span under 2^29 us, with a bitonic
 //                            network in registers, across lanes and in LDS; the time covered by
@@ -184,27 +189,28 @@ __device__ __forceinline__ bool keeps_min(uint32_t i, uint32_t stride, uint32_t 
 
 // Exchanges with partner lane (lane ^ Q) for stride Q * E, if that stride occurs in this run.
 template <int E, int Q>
-__device__ __forceinline__ void lane_stage(uint64_t (&k)[E], uint32_t size)
+__device__ __forceinline__ void lane_stage(uint64_t (&k)[E], uint32_t size, uint32_t t)
 {
     constexpr uint32_t stride = (uint32_t)(Q * E);
     if (2 * stride > size)
         return;
-    const bool km = keeps_min(threadIdx.x * E, stride, size);   // the same for all E slots
+    const bool km = keeps_min(t * E, stride, size);   // the same for all E slots
 #pragma unroll
     for (int e = 0; e < E; ++e)
         k[e] = keep_one(k[e], lane_xor64<Q>(k[e]), km);
 }
 
 // Bitonic sort of P = 256 E keys held E per thread in registers, ascending by position: thread
-// t holds positions t E .. t E + E - 1.  An exchange whose partner is in the same thread runs
+// t holds positions t E .. t E + E - 1 (t = threadIdx.x; a sort within one wave takes P = 64 E
+// and t = the lane, so that no exchange reaches another wave).  An exchange whose partner is in the same thread runs
 // in registers, one whose partner is in the same wave by cross-lane moves (lane ^ stride / E),
 // and only those whose partner is in another wave go through LDS, in a layout (slot e of
 // thread t at e * 256 + t) where a wave's 64 accesses are consecutive; two LDS buffers
 // alternate, so each such exchange needs one barrier.  buf holds 2 P keys.
 template <int E>
-__device__ __forceinline__ void bitonic_sort_regs(uint64_t (&k)[E], uint64_t *buf, uint32_t P)
+__device__ __forceinline__ void bitonic_sort_regs(uint64_t (&k)[E], uint64_t *buf, uint32_t P,
+                                                  uint32_t t)
 {
-    const uint32_t t = threadIdx.x;
     uint32_t flip = 0;
     for (uint32_t size = 2; size <= P; size <<= 1) {
         for (uint32_t stride = size >> 1; stride >= (uint32_t)E * 64; stride >>= 1) {
@@ -220,12 +226,12 @@ __device__ __forceinline__ void bitonic_sort_regs(uint64_t (&k)[E], uint64_t *bu
             for (int e = 0; e < E; ++e)
                 k[e] = keep_one(k[e], b[e * kThreads + pt], km);
         }
-        lane_stage<E, 32>(k, size);
-        lane_stage<E, 16>(k, size);
-        lane_stage<E, 8>(k, size);
-        lane_stage<E, 4>(k, size);
-        lane_stage<E, 2>(k, size);
-        lane_stage<E, 1>(k, size);
+        lane_stage<E, 32>(k, size, t);
+        lane_stage<E, 16>(k, size, t);
+        lane_stage<E, 8>(k, size, t);
+        lane_stage<E, 4>(k, size, t);
+        lane_stage<E, 2>(k, size, t);
+        lane_stage<E, 1>(k, size, t);
 #pragma unroll
         for (int st = E / 2; st >= 1; st >>= 1) {
             if ((uint32_t)(2 * st) > size)
@@ -487,7 +493,7 @@ __device__ __forceinline__ void one_trace(const StatsArgs &a, uint32_t r, uint32
 #pragma unroll
                 for (int j = 0; j < E; ++j)
                     kk[j] = pk[j];
-                bitonic_sort_regs<E>(kk, key, P);
+                bitonic_sort_regs<E>(kk, key, P, threadIdx.x);
                 sweep_regs<E>(kk, nvalid, smin, s_sum);
             };
             switch (P) {
@@ -756,14 +762,194 @@ __device__ __forceinline__ void finish_block(const StatsArgs &a, uint32_t i, uin
     }
 }
 
-// Sorts the traces of the work list the sweep wrote, a grid of blocks taking its entries in
-// turn; without a work list, one block per trace.
-// Blocks of the sort launch that have work: every block without a work list; with one, the
-// first min(listed, grid) blocks, and block 0 always (it finishes when nothing is listed).
+// Wave-wide sum of 32-bit values (every lane gets it).
+__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v)
+{
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1)
+        v += (uint32_t)__shfl_xor((int)v, off, 64);
+    return v;
+}
+
+// Exclusive maximum over the lanes of one wave (lane 0 gets 0).
+__device__ __forceinline__ uint64_t wave_exclusive_max(uint64_t v, uint32_t lane)
+{
+    uint64_t incl = v;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const uint64_t o = __shfl_up((unsigned long long)incl, off, 64);
+        if (lane >= (uint32_t)off)
+            incl = o > incl ? o : incl;
+    }
+    const uint64_t excl = __shfl_up((unsigned long long)incl, 1, 64);
+    return lane == 0 ? 0 : excl;
+}
+
+// The sweep of sweep_regs for one wave's sorted keys (lane l holds positions l E .. l E + E - 1
+// of the trace's valid calls and padding), the prefix maximum taken over the wave.  Key of a
+// call: (llm << 61 | start - base << 32 | duration), the field start - base below 2^29.  The
+// calls' fields are unpacked again where they are used rather than held, so that the largest E
+// keeps few registers.
+template <int E>
+__device__ __forceinline__ void wave_sweep_regs(const uint64_t (&k)[E], uint32_t valid,
+                                                uint64_t base, unsigned long long *s_sum,
+                                                uint32_t lane)
+{
+    const uint32_t first = lane * E;
+    auto llm_of = [](uint64_t kk) { return (uint32_t)(kk >> 61); };
+    auto start_of = [&](uint64_t kk) { return base + ((kk >> 32) & ((1ull << 29) - 1)); };
+    auto end_of = [&](uint64_t kk) { return start_of(kk) + (kk & 0xFFFFFFFFull); };
+    uint64_t run = 0;
+#pragma unroll
+    for (int j = 0; j < E; ++j) {
+        if (first + j < valid) {
+            const uint64_t pk = ((uint64_t)llm_of(k[j]) << 61) | end_of(k[j]);
+            run = pk > run ? pk : run;
+        }
+    }
+    uint64_t prev = wave_exclusive_max(run, lane);
+    constexpr uint64_t kLow61 = (1ull << 61) - 1;
+    uint32_t cur = ~0u;
+    uint64_t c_calls = 0, c_busy = 0, c_active = 0;
+#pragma unroll
+    for (int j = 0; j < E; ++j) {
+        if (first + j >= valid)
+            continue;                                  // (sorted: every later j too)
+        const uint32_t m = llm_of(k[j]);
+        const uint64_t s = start_of(k[j]), e = s + (k[j] & 0xFFFFFFFFull);
+        if (m != cur) {
+            if (cur != ~0u) {
+                atomicAdd(&s_sum[3 * cur + 0], (unsigned long long)c_calls);
+                atomicAdd(&s_sum[3 * cur + 1], (unsigned long long)c_busy);
+                atomicAdd(&s_sum[3 * cur + 2], (unsigned long long)c_active);
+            }
+            c_calls = c_busy = c_active = 0;
+            cur = m;
+        }
+        uint64_t from = s;
+        if ((prev >> 61) == m) {
+            const uint64_t reach = prev & kLow61;
+            from = reach > s ? reach : s;
+        }
+        c_calls += 1;
+        c_busy += e - s;
+        c_active += e > from ? e - from : 0;
+        const uint64_t pk = ((uint64_t)m << 61) | e;
+        prev = pk > prev ? pk : prev;
+    }
+    if (cur != ~0u) {
+        atomicAdd(&s_sum[3 * cur + 0], (unsigned long long)c_calls);
+        atomicAdd(&s_sum[3 * cur + 1], (unsigned long long)c_busy);
+        atomicAdd(&s_sum[3 * cur + 2], (unsigned long long)c_active);
+    }
+}
+
+constexpr uint32_t kWaveSortWaves = 4;       // traces per workgroup of the direct sort
+constexpr uint32_t kWaveSortMax = 64 * 32;   // longest trace one wave sorts (32 keys per lane)
+
+// Trace r (calls lo .. lo + n - 1, n <= 64 E) sorted and swept by one wave: lane l loads calls
+// j * 64 + l (j < E; each load instruction reads 64 consecutive calls) into its E keys, the
+// wave sorts the 64 E keys in registers and across lanes (no LDS, no barrier), sweeps them, and
+// adds the per-LLM sums to s_sum (the wave's own) and then to the trace's copy of the totals.
+// Keys hold a call's start relative to base = (first call's start) - 2^28; a trace with a valid
+// call outside [base, base + 2^29) goes to the work list for the block sort, which handles any
+// span.  Malformed calls are reported and left out, as in the block sort.
+template <int E>
+__device__ __forceinline__ void wave_trace(const StatsArgs &a, uint32_t r, uint64_t lo, uint32_t n,
+                                           uint32_t lane, unsigned long long *s_sum)
+{
+    const uint32_t M = a.M;
+    const uint64_t base = a.start[lo] - (1ull << 28);      // modulo 2^64
+    uint64_t k[E];
+    uint32_t bad = 0, valid = 0;
+    bool far = false;
+#pragma unroll
+    for (int j = 0; j < E; ++j) {
+        const uint32_t i = (uint32_t)j * 64 + lane;
+        k[j] = kPad;
+        if (i < n) {
+            const uint32_t m = a.llm[lo + i];
+            const uint64_t s = a.start[lo + i], e = a.end[lo + i];
+            if (m >= M) {
+                bad |= 1u;
+            } else if (e < s) {
+                bad |= 2u;
+            } else if (s >= kStartLimit || e - s >= kDurationLimit) {
+                bad |= 4u;
+            } else {
+                const uint64_t off = s - base;
+                if (off >= (1ull << 29)) {
+                    far = true;
+                } else {
+                    k[j] = ((uint64_t)m << 61) | (off << 32) | (e - s);
+                    ++valid;
+                }
+            }
+        }
+    }
+    if (bad)
+        atomicOr(a.flags, bad);
+    if (__ballot(far)) {
+        if (lane == 0)
+            a.work[atomicAdd(a.work_count, 1u)] = r;
+        return;
+    }
+    const uint32_t nvalid = wave_sum_u32(valid);
+    if (nvalid == 0)
+        return;
+    bitonic_sort_regs<E>(k, nullptr, 64 * E, lane);
+    if (lane < 3 * M)
+        s_sum[lane] = 0;
+    wave_sweep_regs<E>(k, nvalid, base, s_sum, lane);
+    unsigned long long *copy = a.totals + (uint64_t)(r % kStatsCopies) * kStatsCopyStride;
+    if (lane < 3 * M) {
+        const unsigned long long v = s_sum[lane];
+        if (v)
+            atomicAdd(&copy[lane], v);
+    }
+}
+
+// Every short trace sorted directly (the context found most traces out of end order): one wave
+// per trace, kWaveSortWaves traces per workgroup; traces the wave does not take (a span beyond
+// its packed keys) are listed for the block sort that follows.
+__global__ void __launch_bounds__(64 * kWaveSortWaves) __attribute__((amdgpu_waves_per_eu(4)))
+trace_wave_kernel(StatsArgs a)
+{
+    __shared__ unsigned long long s_sum[kWaveSortWaves][3 * ALP_MAX_LLMS];
+    const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const uint32_t r = (uint32_t)__builtin_amdgcn_readfirstlane(
+        (int)(blockIdx.x * kWaveSortWaves + wave));
+    if (r >= a.R)
+        return;                                        // uniform over the wave
+    const uint64_t lo = a.offsets[r], n64 = a.offsets[r + 1] - lo;
+    if (n64 == 0 || n64 > a.lds_cap)
+        return;                                        // empty, or the long pass takes it
+    const uint32_t n = (uint32_t)n64;
+    unsigned long long *sum = s_sum[wave];
+    if (n > kWaveSortMax) {
+        if (lane == 0)
+            a.work[atomicAdd(a.work_count, 1u)] = r;
+    } else if (n <= 64) {
+        wave_trace<1>(a, r, lo, n, lane, sum);
+    } else if (n <= 128) {
+        wave_trace<2>(a, r, lo, n, lane, sum);
+    } else if (n <= 256) {
+        wave_trace<4>(a, r, lo, n, lane, sum);
+    } else if (n <= 512) {
+        wave_trace<8>(a, r, lo, n, lane, sum);
+    } else if (n <= 1024) {
+        wave_trace<16>(a, r, lo, n, lane, sum);
+    } else {
+        wave_trace<32>(a, r, lo, n, lane, sum);
+    }
+}
+
+// Sorts the traces of the work list (written by the sweep, or by the direct sort for the traces
+// it leaves), a grid of blocks taking its entries in turn.
+// Blocks of the sort launch that have work: the first min(listed, grid) blocks, and block 0
+// always (it finishes when nothing is listed).
 __device__ __forceinline__ uint32_t sort_participants(const StatsArgs &a)
 {
-    if (!a.work)
-        return a.sort_grid;
     const uint32_t listed = *a.work_count;
     return listed == 0 ? 1u : (listed < a.sort_grid ? listed : a.sort_grid);
 }
@@ -774,15 +960,11 @@ __global__ void __launch_bounds__(kThreads) trace_sort_kernel(StatsArgs a)
     const uint32_t P = sort_participants(a);
     if (blockIdx.x >= P)
         return;                                        // nothing listed for this block
-    if (!a.work) {
-        one_trace<kSort>(a, blockIdx.x, 0, s_dyn);
-    } else {
-        const uint32_t listed = *a.work_count;
-        for (uint32_t w = blockIdx.x; w < listed; w += gridDim.x) {
-            if (w != blockIdx.x)
-                __syncthreads();                       // the previous trace's sums are read
-            one_trace<kSort>(a, a.work[w], 0, s_dyn);
-        }
+    const uint32_t listed = *a.work_count;
+    for (uint32_t w = blockIdx.x; w < listed; w += gridDim.x) {
+        if (w != blockIdx.x)
+            __syncthreads();                           // the previous trace's sums are read
+        one_trace<kSort>(a, a.work[w], 0, s_dyn);
     }
     finish_block(a, blockIdx.x, P + a.num_long);
 }
@@ -823,7 +1005,7 @@ hipError_t launch_trace_stats(uint32_t M, uint32_t R, const uint64_t *offsets, c
     a.scratch = scratch;
     a.totals = reinterpret_cast<unsigned long long *>(totals);
     a.flags = reinterpret_cast<uint32_t *>(totals + kStatsTotalsWords);
-    a.work = sweep ? work : nullptr;
+    a.work = work;
     a.work_count = reinterpret_cast<uint32_t *>(totals + kStatsTotalsWords + 1);
     a.done = reinterpret_cast<uint32_t *>(totals + kStatsTotalsWords + 1) + 1;
     a.slot_done = reinterpret_cast<uint32_t *>(totals + kStatsTotalsWords + 2);
@@ -838,11 +1020,16 @@ hipError_t launch_trace_stats(uint32_t M, uint32_t R, const uint64_t *offsets, c
             hipLaunchKernelGGL(trace_sweep_kernel<ALP_MAX_LLMS>, grid, block, 0, st, a);
         if ((e = hipGetLastError()) != hipSuccess)
             return e;
+    } else {
+        hipLaunchKernelGGL(trace_wave_kernel, dim3((R + kWaveSortWaves - 1) / kWaveSortWaves),
+                           dim3(64 * kWaveSortWaves), 0, st, a);
+        if ((e = hipGetLastError()) != hipSuccess)
+            return e;
     }
     // The work list's length is known only on the device: a grid of at most kSortBlocks
     // blocks takes its entries in turn (an empty list costs one short launch).
     const size_t lds = (size_t)2 * lds_cap * sizeof(uint64_t);
-    const uint32_t sort_blocks = sweep && R > kSortBlocks ? kSortBlocks : R;
+    const uint32_t sort_blocks = R > kSortBlocks ? kSortBlocks : R;
     a.sort_grid = sort_blocks;
     a.num_long = num_long;
     hipLaunchKernelGGL(trace_sort_kernel, dim3(sort_blocks), dim3(kThreads), lds, st, a);

@@ -232,3 +232,41 @@ def test_work_list_longer_than_the_sort_grid_with_long_traces():
     with alp.StatsContext(0) as c:
         for _ in range(3):                             # sweep + list, then direct sorts
             _same(c, tr["M"], *arrays)
+
+
+def test_direct_sort_of_every_trace_length_and_span():
+    """After a call whose traces are mostly out of end order, the context sorts every trace
+    directly, one wave per trace of at most 2,048 calls.  A wave keys each call by its start
+    relative to the trace's first call and keeps the trace only if every start lies in
+    [first - 2^28, first + 2^28); other traces go to the block sort.  Traces at both edges of
+    that range and just beyond its upper end, spans of 2^29 us or more, narrow traces of every
+    wave size, empty, single-call and long traces must all match the oracle, on two direct
+    calls in a row."""
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2604_15186_amd import alp
+    rng = np.random.default_rng(31)
+    tr = make_traces("beam", 400, 17)
+    off = tr["offsets"].astype(np.int64)
+    perm = np.concatenate([lo + rng.permutation(hi - lo) for lo, hi in zip(off[:-1], off[1:])])
+    shuffled = (tr["offsets"], tr["llm"][perm], tr["start"][perm], tr["end"][perm])
+    traces = [[]]
+    base = 1 << 40
+    for n in (1, 2, 63, 64, 65, 200, 511, 513, 1000, 1024, 1025, 1700, 2048, 2049, 3000):
+        for lo_off, hi_off in ((0, 1 << 20), (-(1 << 28) + 1, (1 << 28) - 1),
+                               (-(1 << 28), 0), (0, 1 << 28), (-(1 << 30), 1 << 30)):
+            s = base + rng.integers(lo_off, hi_off + 1, n)
+            s[0] = base                                  # the wave's reference call
+            if n > 1:
+                s[1] = base + lo_off                     # both ends of the range present
+            if n > 2:
+                s[2] = base + hi_off
+            m = rng.integers(0, 4, n)
+            d = rng.integers(0, 50_000, n)
+            traces.append([(int(a), int(b), int(b + c)) for a, b, c in zip(m, s, d)])
+    arrays = _pack(traces)
+    with alp.StatsContext(0) as c:
+        _same(c, tr["M"], *shuffled)                   # sweeps, finds the order mixed
+        for _ in range(2):
+            _same(c, 4, *arrays)
