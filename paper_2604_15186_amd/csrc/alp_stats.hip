@@ -17,10 +17,13 @@
 //                            of it before the earliest start of the same LLM's later calls.  Other
 //                            traces go to a work list.
 //   trace_wave_kernel        instead of the sweep, when the traces come out of end order: one
-//                            wave per trace of at most 2,048 calls sorts its calls by packed key
+//                            wave per trace of at most 512 calls sorts its calls by packed key
 //                            (llm << 61 | start << 32 | duration, starts within 2^29 us of a
 //                            reference) in registers and across lanes -- no LDS, no barrier --
 //                            and sweeps them as below; other traces go to the work list.
+//   trace_group_kernel<E,NT> the same for traces of 513 to 1,024 calls (two waves each) and of
+//                            1,025 to 2,048 (four), 8 keys per thread, the exchanges between
+//                            waves through LDS.
 //   trace_sort_kernel        the work list: calls sorted by key (llm << 60 | start), packed into
 //                            one 64-bit key when the starts span under 2^29 us, with a bitonic
 //                            network in registers, across lanes and in LDS; the time covered by
@@ -175,7 +178,9 @@ __device__ __forceinline__ void bitonic_sort(uint64_t *key, uint64_t *val, uint3
 // maximum) of the own and the partner's key.
 __device__ __forceinline__ uint64_t keep_one(uint64_t mine, uint64_t other, bool keep_min)
 {
-    const bool take = keep_min ? other < mine : other > mine;
+    // other < mine selects the minimum where keep_min holds; elsewhere it keeps mine unless
+    // other is larger (equal keys: either is the same value).  One compare and a mask test.
+    const bool take = (other < mine) == keep_min;
     return take ? other : mine;
 }
 
@@ -195,36 +200,48 @@ __device__ __forceinline__ void lane_stage(uint64_t (&k)[E], uint32_t size, uint
     if (2 * stride > size)
         return;
     const bool km = keeps_min(t * E, stride, size);   // the same for all E slots
+    // Partners of up to 4 slots fetched before any is used: the cross-lane moves' latency
+    // overlaps.
 #pragma unroll
-    for (int e = 0; e < E; ++e)
-        k[e] = keep_one(k[e], lane_xor64<Q>(k[e]), km);
+    for (int e0 = 0; e0 < E; e0 += 4) {
+        uint64_t o[4];
+#pragma unroll
+        for (int e = e0; e < e0 + 4 && e < E; ++e)
+            o[e - e0] = lane_xor64<Q>(k[e]);
+#pragma unroll
+        for (int e = e0; e < e0 + 4 && e < E; ++e)
+            k[e] = keep_one(k[e], o[e - e0], km);
+    }
 }
 
-// Bitonic sort of P = 256 E keys held E per thread in registers, ascending by position: thread
-// t holds positions t E .. t E + E - 1 (t = threadIdx.x; a sort within one wave takes P = 64 E
-// and t = the lane, so that no exchange reaches another wave).  An exchange whose partner is in the same thread runs
-// in registers, one whose partner is in the same wave by cross-lane moves (lane ^ stride / E),
-// and only those whose partner is in another wave go through LDS, in a layout (slot e of
-// thread t at e * 256 + t) where a wave's 64 accesses are consecutive; two LDS buffers
-// alternate, so each such exchange needs one barrier.  buf holds 2 P keys.
-template <int E>
+// Bitonic sort of P = NT E keys held E per thread of NT in registers, ascending by position:
+// thread t holds positions t E .. t E + E - 1 (a sort within one wave takes NT = 64 and t = the
+// lane, so that no exchange reaches another wave).  An exchange whose partner is in the same
+// thread runs in registers, one whose partner is in the same wave by cross-lane moves (lane ^
+// stride / E), and only those whose partner is in another wave go through LDS, in a layout
+// (slot e of thread t at e * NT + t) where a wave's 64 accesses are consecutive; two LDS
+// buffers alternate, so each such exchange needs one barrier (buf holds 2 P keys), or, with
+// OneBuf, one buffer of P keys is reused behind a second barrier.
+template <int E, int NT = kThreads, bool OneBuf = false>
 __device__ __forceinline__ void bitonic_sort_regs(uint64_t (&k)[E], uint64_t *buf, uint32_t P,
                                                   uint32_t t)
 {
     uint32_t flip = 0;
     for (uint32_t size = 2; size <= P; size <<= 1) {
         for (uint32_t stride = size >> 1; stride >= (uint32_t)E * 64; stride >>= 1) {
-            uint64_t *b = buf + flip * P;
+            uint64_t *b = OneBuf ? buf : buf + flip * P;
             flip ^= 1u;
 #pragma unroll
             for (int e = 0; e < E; ++e)
-                b[e * kThreads + t] = k[e];
+                b[e * NT + t] = k[e];
             __syncthreads();
             const uint32_t pt = t ^ (stride / E);
             const bool km = keeps_min(t * E, stride, size);
 #pragma unroll
             for (int e = 0; e < E; ++e)
-                k[e] = keep_one(k[e], b[e * kThreads + pt], km);
+                k[e] = keep_one(k[e], b[e * NT + pt], km);
+            if (OneBuf)
+                __syncthreads();                       // read before the next stage writes
         }
         lane_stage<E, 32>(k, size, t);
         lane_stage<E, 16>(k, size, t);
@@ -242,7 +259,7 @@ __device__ __forceinline__ void bitonic_sort_regs(uint64_t (&k)[E], uint64_t *bu
                     continue;
                 const uint64_t a = k[e], b = k[e | st];
                 const bool asc = ((t * E + e) & size) == 0;
-                const bool swap = asc ? a > b : a < b;
+                const bool swap = (a > b) == asc;         // equal keys: either way
                 k[e] = swap ? b : a;
                 k[e | st] = swap ? a : b;
             }
@@ -785,17 +802,17 @@ __device__ __forceinline__ uint64_t wave_exclusive_max(uint64_t v, uint32_t lane
     return lane == 0 ? 0 : excl;
 }
 
-// The sweep of sweep_regs for one wave's sorted keys (lane l holds positions l E .. l E + E - 1
-// of the trace's valid calls and padding), the prefix maximum taken over the wave.  Key of a
-// call: (llm << 61 | start - base << 32 | duration), the field start - base below 2^29.  The
-// calls' fields are unpacked again where they are used rather than held, so that the largest E
-// keeps few registers.
-template <int E>
-__device__ __forceinline__ void wave_sweep_regs(const uint64_t (&k)[E], uint32_t valid,
-                                                uint64_t base, unsigned long long *s_sum,
-                                                uint32_t lane)
+// The sweep of sweep_regs for the sorted keys of one group of NT threads (one wave, NT = 64, or
+// a workgroup): thread t holds positions t E .. t E + E - 1 of the trace's valid calls and
+// padding; the prefix maximum is taken over the group.  Key of a call: (llm << 61 | start - base
+// << 32 | duration), the field start - base below 2^29.  The calls' fields are unpacked again
+// where they are used rather than held, so that large E keep few registers.
+template <int E, int NT>
+__device__ __forceinline__ void group_sweep_regs(const uint64_t (&k)[E], uint32_t valid,
+                                                 uint64_t base, unsigned long long *s_sum,
+                                                 uint32_t t)
 {
-    const uint32_t first = lane * E;
+    const uint32_t first = t * E;
     auto llm_of = [](uint64_t kk) { return (uint32_t)(kk >> 61); };
     auto start_of = [&](uint64_t kk) { return base + ((kk >> 32) & ((1ull << 29) - 1)); };
     auto end_of = [&](uint64_t kk) { return start_of(kk) + (kk & 0xFFFFFFFFull); };
@@ -807,7 +824,11 @@ __device__ __forceinline__ void wave_sweep_regs(const uint64_t (&k)[E], uint32_t
             run = pk > run ? pk : run;
         }
     }
-    uint64_t prev = wave_exclusive_max(run, lane);
+    uint64_t prev;
+    if constexpr (NT == 64)
+        prev = wave_exclusive_max(run, t);
+    else
+        prev = block_exclusive_max(run);
     constexpr uint64_t kLow61 = (1ull << 61) - 1;
     uint32_t cur = ~0u;
     uint64_t c_calls = 0, c_busy = 0, c_active = 0;
@@ -844,16 +865,60 @@ __device__ __forceinline__ void wave_sweep_regs(const uint64_t (&k)[E], uint32_t
     }
 }
 
-constexpr uint32_t kWaveSortWaves = 4;       // traces per workgroup of the direct sort
-constexpr uint32_t kWaveSortMax = 64 * 32;   // longest trace one wave sorts (32 keys per lane)
+// Keys of the calls lo .. lo + n - 1 (n <= NT E) for thread t of a group of NT: calls j NT + t
+// (j < E; each load instruction reads consecutive calls), keyed by start relative to base.
+// Malformed calls are reported in bad and left out, as in the block sort; a valid call outside
+// [base, base + 2^29) sets far (the group then hands the trace to the block sort).  Loads go
+// in groups of up to 4 keys, all in flight together and without branches: positions past the
+// trace load its last call again and become padding.  (A branch per call made the compiler
+// wait for each call's loads before the next; all E at once spill.)
+template <int E, int NT>
+__device__ __forceinline__ void load_keys(const StatsArgs &a, uint64_t lo, uint32_t n, uint32_t t,
+                                          uint64_t base, uint64_t (&k)[E], uint32_t &bad,
+                                          uint32_t &valid, bool &far)
+{
+    const uint32_t M = a.M;
+    constexpr int kGroup = E < 4 ? E : 4;
+#pragma unroll
+    for (int j0 = 0; j0 < E; j0 += kGroup) {
+        uint32_t mm[kGroup];
+        uint64_t ss[kGroup], ee[kGroup];
+#pragma unroll
+        for (int g = 0; g < kGroup; ++g) {
+            const uint32_t i = (uint32_t)(j0 + g) * NT + t;
+            const uint64_t at = lo + (i < n ? i : n - 1);
+            mm[g] = a.llm[at];
+            ss[g] = a.start[at];
+            ee[g] = a.end[at];
+        }
+#pragma unroll
+        for (int g = 0; g < kGroup; ++g) {
+            const uint32_t i = (uint32_t)(j0 + g) * NT + t;
+            const uint32_t m = mm[g];
+            const uint64_t st = ss[g], en = ee[g];
+            const uint32_t b = m >= M ? 1u
+                             : en < st ? 2u
+                             : st >= kStartLimit || en - st >= kDurationLimit ? 4u : 0u;
+            const uint64_t off = st - base;
+            const bool ok = i < n && b == 0;
+            bad |= i < n ? b : 0u;
+            far = far || (ok && off >= (1ull << 29));
+            const bool use = ok && off < (1ull << 29);
+            k[j0 + g] = use ? ((uint64_t)m << 61) | (off << 32) | (en - st) : kPad;
+            valid += use ? 1u : 0u;
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
 
-// Trace r (calls lo .. lo + n - 1, n <= 64 E) sorted and swept by one wave: lane l loads calls
-// j * 64 + l (j < E; each load instruction reads 64 consecutive calls) into its E keys, the
-// wave sorts the 64 E keys in registers and across lanes (no LDS, no barrier), sweeps them, and
-// adds the per-LLM sums to s_sum (the wave's own) and then to the trace's copy of the totals.
-// Keys hold a call's start relative to base = (first call's start) - 2^28; a trace with a valid
-// call outside [base, base + 2^29) goes to the work list for the block sort, which handles any
-// span.  Malformed calls are reported and left out, as in the block sort.
+constexpr uint32_t kWaveSortWaves = 4;       // traces per workgroup of the direct sort
+constexpr uint32_t kWaveSortMax = 64 * 8;    // longest trace one wave sorts (8 keys per lane)
+
+// Trace r (calls lo .. lo + n - 1, n <= 64 E) sorted and swept by one wave: the wave sorts the
+// 64 E keys in registers and across lanes (no LDS, no barrier), sweeps them, and adds the
+// per-LLM sums to s_sum (the wave's own) and then to the trace's copy of the totals.  Keys hold
+// a call's start relative to base = (first call's start) - 2^28; a trace with a valid call
+// outside [base, base + 2^29) goes to the work list for the block sort, which handles any span.
 template <int E>
 __device__ __forceinline__ void wave_trace(const StatsArgs &a, uint32_t r, uint64_t lo, uint32_t n,
                                            uint32_t lane, unsigned long long *s_sum)
@@ -863,30 +928,7 @@ __device__ __forceinline__ void wave_trace(const StatsArgs &a, uint32_t r, uint6
     uint64_t k[E];
     uint32_t bad = 0, valid = 0;
     bool far = false;
-#pragma unroll
-    for (int j = 0; j < E; ++j) {
-        const uint32_t i = (uint32_t)j * 64 + lane;
-        k[j] = kPad;
-        if (i < n) {
-            const uint32_t m = a.llm[lo + i];
-            const uint64_t s = a.start[lo + i], e = a.end[lo + i];
-            if (m >= M) {
-                bad |= 1u;
-            } else if (e < s) {
-                bad |= 2u;
-            } else if (s >= kStartLimit || e - s >= kDurationLimit) {
-                bad |= 4u;
-            } else {
-                const uint64_t off = s - base;
-                if (off >= (1ull << 29)) {
-                    far = true;
-                } else {
-                    k[j] = ((uint64_t)m << 61) | (off << 32) | (e - s);
-                    ++valid;
-                }
-            }
-        }
-    }
+    load_keys<E, 64>(a, lo, n, lane, base, k, bad, valid, far);
     if (bad)
         atomicOr(a.flags, bad);
     if (__ballot(far)) {
@@ -897,10 +939,10 @@ __device__ __forceinline__ void wave_trace(const StatsArgs &a, uint32_t r, uint6
     const uint32_t nvalid = wave_sum_u32(valid);
     if (nvalid == 0)
         return;
-    bitonic_sort_regs<E>(k, nullptr, 64 * E, lane);
+    bitonic_sort_regs<E, 64>(k, nullptr, 64 * E, lane);
     if (lane < 3 * M)
         s_sum[lane] = 0;
-    wave_sweep_regs<E>(k, nvalid, base, s_sum, lane);
+    group_sweep_regs<E, 64>(k, nvalid, base, s_sum, lane);
     unsigned long long *copy = a.totals + (uint64_t)(r % kStatsCopies) * kStatsCopyStride;
     if (lane < 3 * M) {
         const unsigned long long v = s_sum[lane];
@@ -909,11 +951,10 @@ __device__ __forceinline__ void wave_trace(const StatsArgs &a, uint32_t r, uint6
     }
 }
 
-// Every short trace sorted directly (the context found most traces out of end order): one wave
-// per trace, kWaveSortWaves traces per workgroup; traces the wave does not take (a span beyond
-// its packed keys) are listed for the block sort that follows.
-__global__ void __launch_bounds__(64 * kWaveSortWaves) __attribute__((amdgpu_waves_per_eu(4)))
-trace_wave_kernel(StatsArgs a)
+// Every trace of at most 512 calls sorted directly (the context found most traces out of end
+// order): one wave per trace, kWaveSortWaves traces per workgroup; traces the wave does not take
+// (a span beyond its packed keys) are listed for the block sort that follows.
+__global__ void __launch_bounds__(64 * kWaveSortWaves) trace_wave_kernel(StatsArgs a)
 {
     __shared__ unsigned long long s_sum[kWaveSortWaves][3 * ALP_MAX_LLMS];
     const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -922,25 +963,85 @@ trace_wave_kernel(StatsArgs a)
     if (r >= a.R)
         return;                                        // uniform over the wave
     const uint64_t lo = a.offsets[r], n64 = a.offsets[r + 1] - lo;
-    if (n64 == 0 || n64 > a.lds_cap)
-        return;                                        // empty, or the long pass takes it
+    if (n64 == 0 || n64 > a.lds_cap || n64 > kWaveSortMax)
+        return;                                        // empty, or another pass takes it
     const uint32_t n = (uint32_t)n64;
     unsigned long long *sum = s_sum[wave];
-    if (n > kWaveSortMax) {
-        if (lane == 0)
-            a.work[atomicAdd(a.work_count, 1u)] = r;
-    } else if (n <= 64) {
+    if (n <= 64)
         wave_trace<1>(a, r, lo, n, lane, sum);
-    } else if (n <= 128) {
+    else if (n <= 128)
         wave_trace<2>(a, r, lo, n, lane, sum);
-    } else if (n <= 256) {
+    else if (n <= 256)
         wave_trace<4>(a, r, lo, n, lane, sum);
-    } else if (n <= 512) {
+    else
         wave_trace<8>(a, r, lo, n, lane, sum);
-    } else if (n <= 1024) {
-        wave_trace<16>(a, r, lo, n, lane, sum);
-    } else {
-        wave_trace<32>(a, r, lo, n, lane, sum);
+}
+
+// Every trace of P / 2 + 1 to P = NT E calls sorted directly (8 keys per thread: 513 to 1,024
+// calls on two waves, 1,025 to 2,048 on four): one workgroup of NT threads per trace, keyed and
+// handed on as in trace_wave_kernel.  Exchanges whose partners lie in different waves (strides
+// of 64 E and more) go through one LDS buffer of P keys, reused behind a second barrier.  8 keys
+// per thread keep about 50 VGPRs; 16 or 32 keys per lane needed 89 and 171 (2 to 5 waves per
+// SIMD instead of 8).
+template <int E, int NT>
+__global__ void __launch_bounds__(NT) trace_group_kernel(StatsArgs a)
+{
+    constexpr uint32_t P = NT * E;
+    __shared__ uint64_t s_buf[P];
+    __shared__ unsigned long long s_sum[3 * ALP_MAX_LLMS];
+    __shared__ uint32_t s_valid, s_far;
+    const uint32_t r = blockIdx.x, t = threadIdx.x;
+    if (r >= a.R)
+        return;                                        // uniform over the block
+    const uint64_t lo = a.offsets[r], n64 = a.offsets[r + 1] - lo;
+    if (n64 <= P / 2 || n64 > a.lds_cap)
+        return;                                        // another pass takes it
+    if (n64 > P) {
+        // P = 1,024: the P = 2,048 launch's.  P = 2,048: to the block sort (the host keeps
+        // lds_cap within 2,048, so this does not occur).
+        if (P == 2048 && t == 0)
+            a.work[atomicAdd(a.work_count, 1u)] = r;
+        return;
+    }
+    const uint32_t n = (uint32_t)n64, M = a.M;
+    if (t == 0) {
+        s_valid = 0;
+        s_far = 0;
+    }
+    if (t < 3 * M)
+        s_sum[t] = 0;
+    __syncthreads();
+    const uint64_t base = a.start[lo] - (1ull << 28);      // modulo 2^64
+    uint64_t k[E];
+    uint32_t bad = 0, valid = 0;
+    bool far = false;
+    load_keys<E, NT>(a, lo, n, t, base, k, bad, valid, far);
+    if (bad)
+        atomicOr(a.flags, bad);
+    const uint32_t wvalid = wave_sum_u32(valid);
+    const bool wfar = __ballot(far) != 0;
+    if ((t & 63) == 0) {
+        atomicAdd(&s_valid, wvalid);
+        if (wfar)
+            atomicOr(&s_far, 1u);
+    }
+    __syncthreads();
+    if (s_far) {                                       // uniform over the block
+        if (t == 0)
+            a.work[atomicAdd(a.work_count, 1u)] = r;
+        return;
+    }
+    const uint32_t nvalid = s_valid;
+    if (nvalid == 0)
+        return;
+    bitonic_sort_regs<E, NT, true>(k, s_buf, P, t);
+    group_sweep_regs<E, NT>(k, nvalid, base, s_sum, t);
+    __syncthreads();
+    unsigned long long *copy = a.totals + (uint64_t)(r % kStatsCopies) * kStatsCopyStride;
+    if (t < 3 * M) {
+        const unsigned long long v = s_sum[t];
+        if (v)
+            atomicAdd(&copy[t], v);
     }
 }
 
@@ -1021,6 +1122,18 @@ hipError_t launch_trace_stats(uint32_t M, uint32_t R, const uint64_t *offsets, c
         if ((e = hipGetLastError()) != hipSuccess)
             return e;
     } else {
+        if (lds_cap > 1024) {
+            hipLaunchKernelGGL(HIP_KERNEL_NAME(trace_group_kernel<8, 256>), dim3(R), dim3(256), 0,
+                               st, a);
+            if ((e = hipGetLastError()) != hipSuccess)
+                return e;
+        }
+        if (lds_cap > kWaveSortMax) {
+            hipLaunchKernelGGL(HIP_KERNEL_NAME(trace_group_kernel<8, 128>), dim3(R), dim3(128), 0,
+                               st, a);
+            if ((e = hipGetLastError()) != hipSuccess)
+                return e;
+        }
         hipLaunchKernelGGL(trace_wave_kernel, dim3((R + kWaveSortWaves - 1) / kWaveSortWaves),
                            dim3(64 * kWaveSortWaves), 0, st, a);
         if ((e = hipGetLastError()) != hipSuccess)
