@@ -105,42 +105,6 @@ __device__ __forceinline__ uint64_t lane_xor64(uint64_t v)
     return (uint64_t)lane_xor<Q>((uint32_t)v) | ((uint64_t)lane_xor<Q>((uint32_t)(v >> 32)) << 32);
 }
 
-// Block-wide minimum and maximum of 64-bit values and sum of 32-bit counts (every thread gets
-// all three): butterflies within each wave, then the four waves' results through LDS.
-__device__ __forceinline__ void block_min_max_sum(uint64_t &lo, uint64_t &hi, uint32_t &cnt)
-{
-    __shared__ uint64_t s_lo[kThreads / 64], s_hi[kThreads / 64];
-    __shared__ uint32_t s_cnt[kThreads / 64];
-    // Wave reductions by DPP row moves; lane 63 ends with the wave's values.
-    uint32_t ll = (uint32_t)lo, lh = (uint32_t)(lo >> 32), hl = (uint32_t)hi, hh = (uint32_t)(hi >> 32);
-    wave_reduce_steps([&](auto c, auto m) {
-        constexpr int C = decltype(c)::value, RM = decltype(m)::value;
-        const uint64_t a = ((uint64_t)dpp_mov<C, RM>(lh, lh) << 32) | dpp_mov<C, RM>(ll, ll);
-        const uint64_t b = ((uint64_t)dpp_mov<C, RM>(hh, hh) << 32) | dpp_mov<C, RM>(hl, hl);
-        const uint64_t l = ((uint64_t)lh << 32) | ll, h = ((uint64_t)hh << 32) | hl;
-        const uint64_t nl = a < l ? a : l, nh = b > h ? b : h;
-        ll = (uint32_t)nl;
-        lh = (uint32_t)(nl >> 32);
-        hl = (uint32_t)nh;
-        hh = (uint32_t)(nh >> 32);
-        cnt += dpp_mov<C, RM>(0u, cnt);
-    });
-    if ((threadIdx.x & 63) == 63) {
-        s_lo[threadIdx.x >> 6] = ((uint64_t)lh << 32) | ll;
-        s_hi[threadIdx.x >> 6] = ((uint64_t)hh << 32) | hl;
-        s_cnt[threadIdx.x >> 6] = cnt;
-    }
-    __syncthreads();
-    lo = ~0ull;
-    hi = 0;
-    cnt = 0;
-    for (uint32_t w = 0; w < kThreads / 64; ++w) {
-        lo = s_lo[w] < lo ? s_lo[w] : lo;
-        hi = s_hi[w] > hi ? s_hi[w] : hi;
-        cnt += s_cnt[w];
-    }
-}
-
 // Bitonic sort of P (a power of two) entries in place, ascending by key then val when val is
 // given (keys only otherwise).
 template <bool WithVal>
@@ -267,61 +231,6 @@ __device__ __forceinline__ void bitonic_sort_regs(uint64_t (&k)[E], uint64_t *bu
     }
 }
 
-// The sweep below for keys held as bitonic_sort_regs leaves them: thread t's chunk is its own
-// E registers.  Packed key: (llm << 61 | start - smin << 32 | duration).
-template <int E>
-__device__ __forceinline__ void sweep_regs(const uint64_t (&k)[E], uint32_t valid, uint64_t smin,
-                                           unsigned long long *s_sum)
-{
-    const uint32_t base = threadIdx.x * E;
-    uint32_t m[E];
-    uint64_t s[E], e[E];
-    uint64_t run = 0;
-#pragma unroll
-    for (int j = 0; j < E; ++j) {
-        m[j] = (uint32_t)(k[j] >> 61);
-        s[j] = smin + ((k[j] >> 32) & ((1ull << 29) - 1));
-        e[j] = s[j] + (k[j] & 0xFFFFFFFFull);
-        if (base + j < valid) {
-            const uint64_t pk = ((uint64_t)m[j] << 61) | e[j];
-            run = pk > run ? pk : run;
-        }
-    }
-    uint64_t prev = block_exclusive_max(run);
-    constexpr uint64_t kLow61 = (1ull << 61) - 1;
-    uint32_t cur = ~0u;
-    uint64_t c_calls = 0, c_busy = 0, c_active = 0;
-#pragma unroll
-    for (int j = 0; j < E; ++j) {
-        if (base + j >= valid)
-            break;
-        if (m[j] != cur) {
-            if (cur != ~0u) {
-                atomicAdd(&s_sum[3 * cur + 0], (unsigned long long)c_calls);
-                atomicAdd(&s_sum[3 * cur + 1], (unsigned long long)c_busy);
-                atomicAdd(&s_sum[3 * cur + 2], (unsigned long long)c_active);
-            }
-            c_calls = c_busy = c_active = 0;
-            cur = m[j];
-        }
-        uint64_t from = s[j];
-        if ((prev >> 61) == m[j]) {
-            const uint64_t reach = prev & kLow61;
-            from = reach > s[j] ? reach : s[j];
-        }
-        c_calls += 1;
-        c_busy += e[j] - s[j];
-        c_active += e[j] > from ? e[j] - from : 0;
-        const uint64_t pk = ((uint64_t)m[j] << 61) | e[j];
-        prev = pk > prev ? pk : prev;
-    }
-    if (cur != ~0u) {
-        atomicAdd(&s_sum[3 * cur + 0], (unsigned long long)c_calls);
-        atomicAdd(&s_sum[3 * cur + 1], (unsigned long long)c_busy);
-        atomicAdd(&s_sum[3 * cur + 2], (unsigned long long)c_active);
-    }
-}
-
 // The sweep over the sorted calls of one trace: each thread takes a contiguous chunk of the
 // first `valid` entries; get(i, m, s, e) yields entry i.  Packed value of a call: (llm << 61 |
 // end); the maximum of the packed values before a call has high bits equal to its LLM iff an
@@ -399,9 +308,6 @@ __device__ __forceinline__ void wave_add_sums(uint32_t q, uint32_t calls, uint64
     }
 }
 
-// Largest trace the LDS path holds in registers while it loads (calls per thread).
-constexpr uint32_t kMaxPerThread = 8;
-
 // The passes that sort (the sweep of end-ordered traces is trace_sweep_kernel below).  kSort:
 // the work list (or every trace of at most lds_cap calls), sorted in registers or LDS.  kLong:
 // traces beyond lds_cap, sorted in a global scratch region.
@@ -425,6 +331,140 @@ struct StatsArgs {
     alp_stats_t *out;                 // M records, then the StatsTail
 };
 
+// Wave-wide sum of 32-bit values (every lane gets it).
+__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v)
+{
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1)
+        v += (uint32_t)__shfl_xor((int)v, off, 64);
+    return v;
+}
+
+// Exclusive maximum over the lanes of one wave (lane 0 gets 0).
+__device__ __forceinline__ uint64_t wave_exclusive_max(uint64_t v, uint32_t lane)
+{
+    uint64_t incl = v;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const uint64_t o = __shfl_up((unsigned long long)incl, off, 64);
+        if (lane >= (uint32_t)off)
+            incl = o > incl ? o : incl;
+    }
+    const uint64_t excl = __shfl_up((unsigned long long)incl, 1, 64);
+    return lane == 0 ? 0 : excl;
+}
+
+// Per-LLM calls, durations and covered time of one trace's sorted keys, held by a group of NT
+// threads (one wave, NT = 64, or a workgroup), added to s_sum: thread t holds positions
+// t E .. t E + E - 1 of the valid calls and padding.  An exclusive prefix maximum of
+// (llm << 61 | end) over the positions before a call tells whether an earlier call of the same
+// LLM exists and the furthest end among them; the call adds its part beyond that end.  Key of a call: (llm << 61 | start - base
+// << 32 | duration), the field start - base below 2^29.  The calls' fields are unpacked again
+// where they are used rather than held, so that large E keep few registers.
+template <int E, int NT>
+__device__ __forceinline__ void group_sweep_regs(const uint64_t (&k)[E], uint32_t valid,
+                                                 uint64_t base, unsigned long long *s_sum,
+                                                 uint32_t t)
+{
+    const uint32_t first = t * E;
+    auto llm_of = [](uint64_t kk) { return (uint32_t)(kk >> 61); };
+    auto start_of = [&](uint64_t kk) { return base + ((kk >> 32) & ((1ull << 29) - 1)); };
+    auto end_of = [&](uint64_t kk) { return start_of(kk) + (kk & 0xFFFFFFFFull); };
+    uint64_t run = 0;
+#pragma unroll
+    for (int j = 0; j < E; ++j) {
+        if (first + j < valid) {
+            const uint64_t pk = ((uint64_t)llm_of(k[j]) << 61) | end_of(k[j]);
+            run = pk > run ? pk : run;
+        }
+    }
+    uint64_t prev;
+    if constexpr (NT == 64)
+        prev = wave_exclusive_max(run, t);
+    else
+        prev = block_exclusive_max(run);
+    constexpr uint64_t kLow61 = (1ull << 61) - 1;
+    uint32_t cur = ~0u;
+    uint64_t c_calls = 0, c_busy = 0, c_active = 0;
+#pragma unroll
+    for (int j = 0; j < E; ++j) {
+        if (first + j >= valid)
+            continue;                                  // (sorted: every later j too)
+        const uint32_t m = llm_of(k[j]);
+        const uint64_t s = start_of(k[j]), e = s + (k[j] & 0xFFFFFFFFull);
+        if (m != cur) {
+            if (cur != ~0u) {
+                atomicAdd(&s_sum[3 * cur + 0], (unsigned long long)c_calls);
+                atomicAdd(&s_sum[3 * cur + 1], (unsigned long long)c_busy);
+                atomicAdd(&s_sum[3 * cur + 2], (unsigned long long)c_active);
+            }
+            c_calls = c_busy = c_active = 0;
+            cur = m;
+        }
+        uint64_t from = s;
+        if ((prev >> 61) == m) {
+            const uint64_t reach = prev & kLow61;
+            from = reach > s ? reach : s;
+        }
+        c_calls += 1;
+        c_busy += e - s;
+        c_active += e > from ? e - from : 0;
+        const uint64_t pk = ((uint64_t)m << 61) | e;
+        prev = pk > prev ? pk : prev;
+    }
+    if (cur != ~0u) {
+        atomicAdd(&s_sum[3 * cur + 0], (unsigned long long)c_calls);
+        atomicAdd(&s_sum[3 * cur + 1], (unsigned long long)c_busy);
+        atomicAdd(&s_sum[3 * cur + 2], (unsigned long long)c_active);
+    }
+}
+
+// Keys of the calls lo .. lo + n - 1 (n <= NT E) for thread t of a group of NT: calls j NT + t
+// (j < E; each load instruction reads consecutive calls), keyed by start relative to base.
+// Malformed calls are reported in bad and left out, as in the block sort; a valid call outside
+// [base, base + 2^29) sets far (the group then hands the trace to the block sort).  Loads go
+// in groups of up to 4 keys, all in flight together and without branches: positions past the
+// trace load its last call again and become padding.  (A branch per call made the compiler
+// wait for each call's loads before the next; all E at once spill.)
+template <int E, int NT>
+__device__ __forceinline__ void load_keys(const StatsArgs &a, uint64_t lo, uint32_t n, uint32_t t,
+                                          uint64_t base, uint64_t (&k)[E], uint32_t &bad,
+                                          uint32_t &valid, bool &far)
+{
+    const uint32_t M = a.M;
+    constexpr int kGroup = E < 4 ? E : 4;
+#pragma unroll
+    for (int j0 = 0; j0 < E; j0 += kGroup) {
+        uint32_t mm[kGroup];
+        uint64_t ss[kGroup], ee[kGroup];
+#pragma unroll
+        for (int g = 0; g < kGroup; ++g) {
+            const uint32_t i = (uint32_t)(j0 + g) * NT + t;
+            const uint64_t at = lo + (i < n ? i : n - 1);
+            mm[g] = a.llm[at];
+            ss[g] = a.start[at];
+            ee[g] = a.end[at];
+        }
+#pragma unroll
+        for (int g = 0; g < kGroup; ++g) {
+            const uint32_t i = (uint32_t)(j0 + g) * NT + t;
+            const uint32_t m = mm[g];
+            const uint64_t st = ss[g], en = ee[g];
+            const uint32_t b = m >= M ? 1u
+                             : en < st ? 2u
+                             : st >= kStartLimit || en - st >= kDurationLimit ? 4u : 0u;
+            const uint64_t off = st - base;
+            const bool ok = i < n && b == 0;
+            bad |= i < n ? b : 0u;
+            far = far || (ok && off >= (1ull << 29));
+            const bool use = ok && off < (1ull << 29);
+            k[j0 + g] = use ? ((uint64_t)m << 61) | (off << 32) | (en - st) : kPad;
+            valid += use ? 1u : 0u;
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
 // Statistics of trace r (slot = the block's trace slot in long_base for kLong) by one block.
 template <int Pass, int MM = ALP_MAX_LLMS>
 __device__ __forceinline__ void one_trace(const StatsArgs &a, uint32_t r, uint32_t slot,
@@ -437,10 +477,10 @@ __device__ __forceinline__ void one_trace(const StatsArgs &a, uint32_t r, uint32
     const uint64_t *__restrict__ end = a.end;
     uint32_t *flags = a.flags;
     __shared__ unsigned long long s_sum[3 * ALP_MAX_LLMS];   // per LLM: calls, busy, active
-    __shared__ uint32_t s_valid;
+    __shared__ uint32_t s_valid, s_far;
     const uint64_t lo = a.offsets[r], n = a.offsets[r + 1] - lo;
-    if (!Global && n > a.lds_cap)
-        return;                                        // long trace: the global pass takes it
+    if (n == 0 || (!Global && n > a.lds_cap))
+        return;                                        // empty, or the global pass takes it
     uint32_t P = kThreads;                              // padded length: a power of two
     while (P < n)
         P <<= 1;
@@ -449,8 +489,10 @@ __device__ __forceinline__ void one_trace(const StatsArgs &a, uint32_t r, uint32
     uint64_t *val = key + P;
     for (uint32_t k = threadIdx.x; k < 3 * ALP_MAX_LLMS; k += kThreads)
         s_sum[k] = 0;
-    if (threadIdx.x == 0)
+    if (threadIdx.x == 0) {
         s_valid = 0;
+        s_far = 0;
+    }
     __syncthreads();                                   // counters zeroed before any adds
     // Calls i = threadIdx.x + k * kThreads; out-of-range or invalid ones become padding.
     uint32_t bad = 0, valid = 0;
@@ -470,74 +512,54 @@ __device__ __forceinline__ void one_trace(const StatsArgs &a, uint32_t r, uint32
             return true;
         return false;
     };
-    if (!Global) {
-        // Held in registers: the trace's first and last start decide whether a call packs
-        // into one 64-bit key, (llm << 61 | start - first << 32 | duration), which halves the
-        // sort's LDS traffic; traces spanning 2^29 us or more keep (key, end) pairs.  Thread t
-        // loads calls k * 256 + t (k < P / 256), so each load instruction reads consecutive
-        // calls; where a call starts out does not matter to the sort.
-        const uint32_t E = P / kThreads;
-        uint32_t rm[kMaxPerThread];
-        uint64_t rs[kMaxPerThread], re[kMaxPerThread];
-        bool ok[kMaxPerThread];
-        uint64_t smin = ~0ull, smax = 0;
-#pragma unroll
-        for (uint32_t k = 0; k < kMaxPerThread; ++k) {
-            ok[k] = k < E && load((uint64_t)k * kThreads + threadIdx.x, rm[k], rs[k], re[k]);
-            if (ok[k]) {
-                valid += 1;
-                smin = rs[k] < smin ? rs[k] : smin;
-                smax = rs[k] > smax ? rs[k] : smax;
-            }
-        }
-        if (bad)
-            atomicOr(flags, bad);
-        uint32_t nvalid = valid;
-        block_min_max_sum(smin, smax, nvalid);
-        if (nvalid == 0)
-            return;
-        if (smax - smin < (1ull << 29)) {
-            // The thread's loaded calls k < P / 256 become its E sort positions (any placement
-            // of the inputs sorts the same); padding sorts last.
-            uint64_t pk[kMaxPerThread];
-#pragma unroll
-            for (uint32_t k = 0; k < kMaxPerThread; ++k)
-                pk[k] = ok[k] ? ((uint64_t)rm[k] << 61) | ((rs[k] - smin) << 32) | (re[k] - rs[k])
-                              : kPad;
-            auto run = [&](auto e_const) {
-                constexpr int E = decltype(e_const)::value;
-                uint64_t kk[E];
-#pragma unroll
-                for (int j = 0; j < E; ++j)
-                    kk[j] = pk[j];
-                bitonic_sort_regs<E>(kk, key, P, threadIdx.x);
-                sweep_regs<E>(kk, nvalid, smin, s_sum);
-            };
-            switch (P) {
-            case kThreads: run(std::integral_constant<int, 1>{}); break;
-            case 2 * kThreads: run(std::integral_constant<int, 2>{}); break;
-            case 4 * kThreads: run(std::integral_constant<int, 4>{}); break;
-            default: run(std::integral_constant<int, 8>{}); break;
-            }
-        } else {
-#pragma unroll
-            for (uint32_t k = 0; k < kMaxPerThread; ++k) {
-                if (k < E) {
-                    const uint32_t i = k * kThreads + threadIdx.x;
-                    key[i] = ok[k] ? ((uint64_t)rm[k] << 60) | rs[k] : kPad;
-                    val[i] = ok[k] ? re[k] : 0;
-                }
+    bool unpacked = Global;
+    if constexpr (!Global) {
+        // Packed keys in registers, as the direct sort's groups hold them: thread t loads calls
+        // j * 256 + t (j < E = P / 256) and keys each by its start relative to the first call's
+        // start - 2^28 (llm << 61 | start - base << 32 | duration), which halves the sort's LDS
+        // traffic.  A trace with a start outside [base, base + 2^29) falls back to (key, end)
+        // pairs in LDS, loaded again.
+        const uint64_t base = start[lo] - (1ull << 28);      // modulo 2^64
+        auto run = [&](auto e_const) {
+            constexpr int E = decltype(e_const)::value;
+            uint64_t k[E];
+            uint32_t kb = 0, kv = 0;
+            bool far = false;
+            load_keys<E, kThreads>(a, lo, n, threadIdx.x, base, k, kb, kv, far);
+            if (kb)
+                atomicOr(flags, kb);
+            const uint32_t wv = wave_sum_u32(kv);
+            const bool wf = __ballot(far) != 0;
+            if ((threadIdx.x & 63) == 0) {
+                atomicAdd(&s_valid, wv);
+                if (wf)
+                    atomicOr(&s_far, 1u);
             }
             __syncthreads();
-            bitonic_sort<true>(key, val, P);
-            sweep(P, nvalid, [&](uint32_t i, uint32_t &m, uint64_t &s, uint64_t &e) {
-                const uint64_t kk = key[i];
-                m = (uint32_t)(kk >> 60);
-                s = kk & (kStartLimit - 1);
-                e = val[i];
-            }, s_sum);
+            if (s_far) {                                // uniform over the block
+                unpacked = true;
+                return;
+            }
+            const uint32_t nvalid = s_valid;
+            if (nvalid == 0)
+                return;
+            bitonic_sort_regs<E>(k, key, P, threadIdx.x);
+            group_sweep_regs<E, kThreads>(k, nvalid, base, s_sum, threadIdx.x);
+        };
+        switch (P) {
+        case kThreads: run(std::integral_constant<int, 1>{}); break;
+        case 2 * kThreads: run(std::integral_constant<int, 2>{}); break;
+        case 4 * kThreads: run(std::integral_constant<int, 4>{}); break;
+        default: run(std::integral_constant<int, 8>{}); break;
         }
-    } else {
+        if (unpacked) {
+            __syncthreads();                           // every thread has read s_valid
+            if (threadIdx.x == 0)
+                s_valid = 0;
+            __syncthreads();
+        }
+    }
+    if (unpacked) {
         for (uint64_t i = threadIdx.x; i < P; i += kThreads) {
             uint32_t m = 0;
             uint64_t s = 0, e = 0;
@@ -776,138 +798,6 @@ __device__ __forceinline__ void finish_block(const StatsArgs &a, uint32_t i, uin
         t.flags = atomicExch(a.flags, 0u) | s_flags;
         t.listed = atomicExch(a.work_count, 0u);
         *reinterpret_cast<StatsTail *>(a.out + ALP_MAX_LLMS) = t;
-    }
-}
-
-// Wave-wide sum of 32-bit values (every lane gets it).
-__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v)
-{
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1)
-        v += (uint32_t)__shfl_xor((int)v, off, 64);
-    return v;
-}
-
-// Exclusive maximum over the lanes of one wave (lane 0 gets 0).
-__device__ __forceinline__ uint64_t wave_exclusive_max(uint64_t v, uint32_t lane)
-{
-    uint64_t incl = v;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const uint64_t o = __shfl_up((unsigned long long)incl, off, 64);
-        if (lane >= (uint32_t)off)
-            incl = o > incl ? o : incl;
-    }
-    const uint64_t excl = __shfl_up((unsigned long long)incl, 1, 64);
-    return lane == 0 ? 0 : excl;
-}
-
-// The sweep of sweep_regs for the sorted keys of one group of NT threads (one wave, NT = 64, or
-// a workgroup): thread t holds positions t E .. t E + E - 1 of the trace's valid calls and
-// padding; the prefix maximum is taken over the group.  Key of a call: (llm << 61 | start - base
-// << 32 | duration), the field start - base below 2^29.  The calls' fields are unpacked again
-// where they are used rather than held, so that large E keep few registers.
-template <int E, int NT>
-__device__ __forceinline__ void group_sweep_regs(const uint64_t (&k)[E], uint32_t valid,
-                                                 uint64_t base, unsigned long long *s_sum,
-                                                 uint32_t t)
-{
-    const uint32_t first = t * E;
-    auto llm_of = [](uint64_t kk) { return (uint32_t)(kk >> 61); };
-    auto start_of = [&](uint64_t kk) { return base + ((kk >> 32) & ((1ull << 29) - 1)); };
-    auto end_of = [&](uint64_t kk) { return start_of(kk) + (kk & 0xFFFFFFFFull); };
-    uint64_t run = 0;
-#pragma unroll
-    for (int j = 0; j < E; ++j) {
-        if (first + j < valid) {
-            const uint64_t pk = ((uint64_t)llm_of(k[j]) << 61) | end_of(k[j]);
-            run = pk > run ? pk : run;
-        }
-    }
-    uint64_t prev;
-    if constexpr (NT == 64)
-        prev = wave_exclusive_max(run, t);
-    else
-        prev = block_exclusive_max(run);
-    constexpr uint64_t kLow61 = (1ull << 61) - 1;
-    uint32_t cur = ~0u;
-    uint64_t c_calls = 0, c_busy = 0, c_active = 0;
-#pragma unroll
-    for (int j = 0; j < E; ++j) {
-        if (first + j >= valid)
-            continue;                                  // (sorted: every later j too)
-        const uint32_t m = llm_of(k[j]);
-        const uint64_t s = start_of(k[j]), e = s + (k[j] & 0xFFFFFFFFull);
-        if (m != cur) {
-            if (cur != ~0u) {
-                atomicAdd(&s_sum[3 * cur + 0], (unsigned long long)c_calls);
-                atomicAdd(&s_sum[3 * cur + 1], (unsigned long long)c_busy);
-                atomicAdd(&s_sum[3 * cur + 2], (unsigned long long)c_active);
-            }
-            c_calls = c_busy = c_active = 0;
-            cur = m;
-        }
-        uint64_t from = s;
-        if ((prev >> 61) == m) {
-            const uint64_t reach = prev & kLow61;
-            from = reach > s ? reach : s;
-        }
-        c_calls += 1;
-        c_busy += e - s;
-        c_active += e > from ? e - from : 0;
-        const uint64_t pk = ((uint64_t)m << 61) | e;
-        prev = pk > prev ? pk : prev;
-    }
-    if (cur != ~0u) {
-        atomicAdd(&s_sum[3 * cur + 0], (unsigned long long)c_calls);
-        atomicAdd(&s_sum[3 * cur + 1], (unsigned long long)c_busy);
-        atomicAdd(&s_sum[3 * cur + 2], (unsigned long long)c_active);
-    }
-}
-
-// Keys of the calls lo .. lo + n - 1 (n <= NT E) for thread t of a group of NT: calls j NT + t
-// (j < E; each load instruction reads consecutive calls), keyed by start relative to base.
-// Malformed calls are reported in bad and left out, as in the block sort; a valid call outside
-// [base, base + 2^29) sets far (the group then hands the trace to the block sort).  Loads go
-// in groups of up to 4 keys, all in flight together and without branches: positions past the
-// trace load its last call again and become padding.  (A branch per call made the compiler
-// wait for each call's loads before the next; all E at once spill.)
-template <int E, int NT>
-__device__ __forceinline__ void load_keys(const StatsArgs &a, uint64_t lo, uint32_t n, uint32_t t,
-                                          uint64_t base, uint64_t (&k)[E], uint32_t &bad,
-                                          uint32_t &valid, bool &far)
-{
-    const uint32_t M = a.M;
-    constexpr int kGroup = E < 4 ? E : 4;
-#pragma unroll
-    for (int j0 = 0; j0 < E; j0 += kGroup) {
-        uint32_t mm[kGroup];
-        uint64_t ss[kGroup], ee[kGroup];
-#pragma unroll
-        for (int g = 0; g < kGroup; ++g) {
-            const uint32_t i = (uint32_t)(j0 + g) * NT + t;
-            const uint64_t at = lo + (i < n ? i : n - 1);
-            mm[g] = a.llm[at];
-            ss[g] = a.start[at];
-            ee[g] = a.end[at];
-        }
-#pragma unroll
-        for (int g = 0; g < kGroup; ++g) {
-            const uint32_t i = (uint32_t)(j0 + g) * NT + t;
-            const uint32_t m = mm[g];
-            const uint64_t st = ss[g], en = ee[g];
-            const uint32_t b = m >= M ? 1u
-                             : en < st ? 2u
-                             : st >= kStartLimit || en - st >= kDurationLimit ? 4u : 0u;
-            const uint64_t off = st - base;
-            const bool ok = i < n && b == 0;
-            bad |= i < n ? b : 0u;
-            far = far || (ok && off >= (1ull << 29));
-            const bool use = ok && off < (1ull << 29);
-            k[j0 + g] = use ? ((uint64_t)m << 61) | (off << 32) | (en - st) : kPad;
-            valid += use ? 1u : 0u;
-        }
-        __builtin_amdgcn_sched_barrier(0);
     }
 }
 
