@@ -354,6 +354,115 @@ __device__ __forceinline__ uint64_t wave_exclusive_max(uint64_t v, uint32_t lane
     return lane == 0 ? 0 : excl;
 }
 
+// The 32-bit value of lane (lane ^ Q) for any Q below 64: DPP for 1, 2, 3 (quad permutations),
+// 7 (half-row mirror) and 15 (row mirror), a swizzle within 32 lanes up to 31, a lane permute
+// from 32.
+template <int Q>
+__device__ __forceinline__ uint32_t lane_xor_any(uint32_t v)
+{
+    if constexpr (Q == 1 || Q == 2)
+        return lane_xor<Q>(v);
+    else if constexpr (Q == 3)
+        return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x1B, 0xF, 0xF, false);
+    else if constexpr (Q == 7)
+        return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, false);
+    else if constexpr (Q == 15)
+        return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x140, 0xF, 0xF, false);
+    else if constexpr (Q < 32)
+        return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, 0x1F | (Q << 10));
+    else
+        return (uint32_t)__builtin_amdgcn_ds_bpermute((int)((threadIdx.x ^ (uint32_t)Q) << 2),
+                                                       (int)v);
+}
+
+template <int Q>
+__device__ __forceinline__ uint64_t lane_xor_any64(uint64_t v)
+{
+    return (uint64_t)lane_xor_any<Q>((uint32_t)v) |
+           ((uint64_t)lane_xor_any<Q>((uint32_t)(v >> 32)) << 32);
+}
+
+constexpr uint32_t pow2_at_least(uint32_t v)
+{
+    uint32_t p = 1;
+    while (p < v)
+        p <<= 1;
+    return p;
+}
+
+// One stage of a bitonic network whose comparators all put the minimum at the lower position:
+// the first stage of a merge of SIZE pairs position i with its mirror i ^ (SIZE - 1) (MIRROR),
+// the later ones with i ^ STRIDE.  Positions t E + e of NT threads, E keys each (E, NT powers of
+// two or NT a multiple of 64); positions past NT E hold +inf without existing, so a pair whose
+// upper position lies there leaves the lower one as it is.  Partners in the same thread are
+// exchanged in registers, in the same wave across lanes, in other waves through buf (NT E keys,
+// two barriers).
+template <int E, int NT, int SIZE, int STRIDE, bool MIRROR>
+__device__ __forceinline__ void mirror_stage(uint64_t (&k)[E], uint64_t *buf, uint32_t t)
+{
+    // partner of (t, e): thread t ^ TQ, register e ^ EQ
+    constexpr uint32_t D = MIRROR ? SIZE - 1 : STRIDE;       // position xor
+    constexpr uint32_t HALF = MIRROR ? SIZE / 2 : STRIDE;    // bit that marks the upper element
+    constexpr uint32_t EQ = D % E, TQ = D / E;
+    if constexpr (TQ == 0) {
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            if (e & HALF)
+                continue;
+            const int f = e ^ (int)EQ;
+            const uint64_t a = k[e], b = k[f];
+            const bool swap = a > b;
+            k[e] = swap ? b : a;
+            k[f] = swap ? a : b;
+        }
+    } else {
+        const bool lower = (t & (HALF / E)) == 0;
+        if constexpr (TQ < 64) {
+            // Every partner value is fetched before any key changes: with EQ != 0 a key's
+            // partner register may come earlier in the loop.
+            uint64_t o[E];
+#pragma unroll
+            for (int e = 0; e < E; ++e)
+                o[e] = lane_xor_any64<TQ>(k[e ^ EQ]);
+#pragma unroll
+            for (int e = 0; e < E; ++e)
+                k[e] = keep_one(k[e], o[e], lower);
+        } else {
+#pragma unroll
+            for (int e = 0; e < E; ++e)
+                buf[e * NT + t] = k[e];
+            __syncthreads();
+            const uint32_t pt = t ^ TQ;
+            if (pt < (uint32_t)NT) {
+#pragma unroll
+                for (int e = 0; e < E; ++e)
+                    k[e] = keep_one(k[e], buf[(e ^ EQ) * NT + pt], lower);
+            }
+            __syncthreads();
+        }
+    }
+}
+
+template <int E, int NT, int SIZE, int STRIDE>
+__device__ __forceinline__ void mirror_strides(uint64_t (&k)[E], uint64_t *buf, uint32_t t)
+{
+    if constexpr (STRIDE >= 1) {
+        mirror_stage<E, NT, SIZE, STRIDE, false>(k, buf, t);
+        mirror_strides<E, NT, SIZE, STRIDE / 2>(k, buf, t);
+    }
+}
+
+// Ascending sort of the NT E keys (E per thread, thread t at positions t E ..), padded virtually
+// to the next power of two: every merge of SIZE = 2, 4, .. is a mirror stage and half-cleaners.
+template <int E, int NT, int SIZE = 2>
+__device__ __forceinline__ void mirror_sort_regs(uint64_t (&k)[E], uint64_t *buf, uint32_t t)
+{
+    mirror_stage<E, NT, SIZE, SIZE / 2, true>(k, buf, t);
+    mirror_strides<E, NT, SIZE, SIZE / 4>(k, buf, t);
+    if constexpr (SIZE < (int)pow2_at_least(NT * E))
+        mirror_sort_regs<E, NT, SIZE * 2>(k, buf, t);
+}
+
 // Per-LLM calls, durations and covered time of one trace's sorted keys, held by a group of NT
 // threads (one wave, NT = 64, or a workgroup), added to s_sum: thread t holds positions
 // t E .. t E + E - 1 of the valid calls and padding.  An exclusive prefix maximum of
@@ -873,7 +982,7 @@ __global__ void __launch_bounds__(64 * kWaveSortWaves) trace_wave_kernel(StatsAr
 // of 64 E and more) go through one LDS buffer of P keys, reused behind a second barrier.  8 keys
 // per thread keep about 50 VGPRs; 16 or 32 keys per lane needed 89 and 171 (2 to 5 waves per
 // SIMD instead of 8).
-template <int E, int NT>
+template <int E, int NT, int LO>
 __global__ void __launch_bounds__(NT) trace_group_kernel(StatsArgs a)
 {
     constexpr uint32_t P = NT * E;
@@ -884,11 +993,11 @@ __global__ void __launch_bounds__(NT) trace_group_kernel(StatsArgs a)
     if (r >= a.R)
         return;                                        // uniform over the block
     const uint64_t lo = a.offsets[r], n64 = a.offsets[r + 1] - lo;
-    if (n64 <= P / 2 || n64 > a.lds_cap)
+    if (n64 <= (uint64_t)LO || n64 > a.lds_cap)
         return;                                        // another pass takes it
     if (n64 > P) {
-        // P = 1,024: the P = 2,048 launch's.  P = 2,048: to the block sort (the host keeps
-        // lds_cap within 2,048, so this does not occur).
+        // Below 2,048 keys: a larger group's.  2,048: to the block sort (the host keeps lds_cap
+        // within 2,048, so this does not occur).
         if (P == 2048 && t == 0)
             a.work[atomicAdd(a.work_count, 1u)] = r;
         return;
@@ -924,7 +1033,7 @@ __global__ void __launch_bounds__(NT) trace_group_kernel(StatsArgs a)
     const uint32_t nvalid = s_valid;
     if (nvalid == 0)
         return;
-    bitonic_sort_regs<E, NT, true>(k, s_buf, P, t);
+    mirror_sort_regs<E, NT>(k, s_buf, t);
     group_sweep_regs<E, NT>(k, nvalid, base, s_sum, t);
     __syncthreads();
     unsigned long long *copy = a.totals + (uint64_t)(r % kStatsCopies) * kStatsCopyStride;
@@ -1012,15 +1121,21 @@ hipError_t launch_trace_stats(uint32_t M, uint32_t R, const uint64_t *offsets, c
         if ((e = hipGetLastError()) != hipSuccess)
             return e;
     } else {
+        if (lds_cap > 1536) {
+            hipLaunchKernelGGL(HIP_KERNEL_NAME(trace_group_kernel<8, 256, 1536>), dim3(R),
+                               dim3(256), 0, st, a);
+            if ((e = hipGetLastError()) != hipSuccess)
+                return e;
+        }
         if (lds_cap > 1024) {
-            hipLaunchKernelGGL(HIP_KERNEL_NAME(trace_group_kernel<8, 256>), dim3(R), dim3(256), 0,
-                               st, a);
+            hipLaunchKernelGGL(HIP_KERNEL_NAME(trace_group_kernel<8, 192, 1024>), dim3(R),
+                               dim3(192), 0, st, a);
             if ((e = hipGetLastError()) != hipSuccess)
                 return e;
         }
         if (lds_cap > kWaveSortMax) {
-            hipLaunchKernelGGL(HIP_KERNEL_NAME(trace_group_kernel<8, 128>), dim3(R), dim3(128), 0,
-                               st, a);
+            hipLaunchKernelGGL(HIP_KERNEL_NAME(trace_group_kernel<8, 128, kWaveSortMax>),
+                               dim3(R), dim3(128), 0, st, a);
             if ((e = hipGetLastError()) != hipSuccess)
                 return e;
         }

@@ -236,11 +236,12 @@ def test_work_list_longer_than_the_sort_grid_with_long_traces():
 
 def test_direct_sort_of_every_trace_length_and_span():
     """After a call whose traces are mostly out of end order, the context sorts every trace
-    directly, one wave per trace of at most 2,048 calls.  A wave keys each call by its start
+    directly, by groups of one to four waves per trace of at most 2,048 calls (the group sizes
+    change at 512, 1,024 and 1,536 calls).  A group keys each call by its start
     relative to the trace's first call and keeps the trace only if every start lies in
     [first - 2^28, first + 2^28); other traces go to the block sort.  Traces at both edges of
     that range and just beyond its upper end, spans of 2^29 us or more, narrow traces of every
-    wave size, empty, single-call and long traces must all match the oracle, on two direct
+    group size, empty, single-call and long traces must all match the oracle, on two direct
     calls in a row."""
     import torch
     if not torch.cuda.is_available():
@@ -253,7 +254,8 @@ def test_direct_sort_of_every_trace_length_and_span():
     shuffled = (tr["offsets"], tr["llm"][perm], tr["start"][perm], tr["end"][perm])
     traces = [[]]
     base = 1 << 40
-    for n in (1, 2, 63, 64, 65, 200, 511, 513, 1000, 1024, 1025, 1700, 2048, 2049, 3000):
+    for n in (1, 2, 63, 64, 65, 200, 511, 512, 513, 1000, 1024, 1025, 1536, 1537, 1700, 2048,
+              2049, 3000):
         for lo_off, hi_off in ((0, 1 << 20), (-(1 << 28) + 1, (1 << 28) - 1),
                                (-(1 << 28), 0), (0, 1 << 28), (-(1 << 30), 1 << 30)):
             s = base + rng.integers(lo_off, hi_off + 1, n)
