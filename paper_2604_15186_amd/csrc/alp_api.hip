@@ -1737,7 +1737,7 @@ int32_t alp_trace_stats(alp_stats_ctx *c, uint32_t num_llms, uint32_t num_traces
     const bool zero_first = !c->counters_clean;
     c->counters_clean = false;                       // until the kernels have run to the end
     if ((e = alp::launch_trace_stats(num_llms, num_traces, offsets, llm, start_us, end_us, lds_cap,
-                                     (uint32_t)longs.size(), (const uint32_t *)c->long_list.ptr,
+                                     (uint32_t)max_short, (uint32_t)longs.size(), (const uint32_t *)c->long_list.ptr,
                                      (const uint64_t *)c->long_base.ptr, (uint64_t *)c->scratch.ptr,
                                      totals, (uint32_t *)c->work.ptr, sweep, zero_first,
                                      c->host_out_dev, c->stream)) != hipSuccess)

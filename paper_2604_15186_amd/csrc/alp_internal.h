@@ -254,8 +254,9 @@ static_assert(sizeof(alp_pruned_t) == 64 && offsetof(alp_pruned_t, fraction_vect
 // of the work list and the count of finished slots (the low and high half of the next), and
 // kStatsSlots 32-bit counters of finished blocks.  They must be zero when the kernels start; the last block leaves them zero,
 // so zero_first is needed only for fresh memory or after a failed launch.  sweep: traces in end order are swept without a sort and the others listed in work
-// (R entries) for the sort pass; otherwise every trace is sorted.  Writes out[0..M) and the
-// StatsTail at out[ALP_MAX_LLMS].
+// (R entries) for the sort pass; otherwise every trace is sorted.  max_short: the most calls of
+// a trace within lds_cap (direct sorts launch only the group sizes it reaches).  Writes
+// out[0..M) and the StatsTail at out[ALP_MAX_LLMS].
 constexpr uint32_t kStatsCopies = 64;
 constexpr uint32_t kStatsCopyStride = 32;                 // >= 3 * ALP_MAX_LLMS, 256 B apart
 constexpr uint32_t kStatsTotalsWords = kStatsCopies * kStatsCopyStride;
@@ -269,7 +270,7 @@ struct StatsTail {
 static_assert(sizeof(StatsTail) == sizeof(alp_stats_t), "the tail takes one record's place");
 hipError_t launch_trace_stats(uint32_t M, uint32_t R, const uint64_t *offsets, const uint32_t *llm,
                               const uint64_t *start, const uint64_t *end, uint32_t lds_cap,
-                              uint32_t num_long, const uint32_t *long_traces,
+                              uint32_t max_short, uint32_t num_long, const uint32_t *long_traces,
                               const uint64_t *long_base, uint64_t *scratch, uint64_t *totals,
                               uint32_t *work, bool sweep, bool zero_first, alp_stats_t *out,
                               hipStream_t st);

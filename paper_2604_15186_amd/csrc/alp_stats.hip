@@ -1080,7 +1080,7 @@ __global__ void __launch_bounds__(kThreads) trace_long_kernel(StatsArgs a)
 
 hipError_t launch_trace_stats(uint32_t M, uint32_t R, const uint64_t *offsets, const uint32_t *llm,
                               const uint64_t *start, const uint64_t *end, uint32_t lds_cap,
-                              uint32_t num_long, const uint32_t *long_traces,
+                              uint32_t max_short, uint32_t num_long, const uint32_t *long_traces,
                               const uint64_t *long_base, uint64_t *scratch, uint64_t *totals,
                               uint32_t *work, bool sweep, bool zero_first, alp_stats_t *out,
                               hipStream_t st)
@@ -1121,19 +1121,19 @@ hipError_t launch_trace_stats(uint32_t M, uint32_t R, const uint64_t *offsets, c
         if ((e = hipGetLastError()) != hipSuccess)
             return e;
     } else {
-        if (lds_cap > 1536) {
+        if (max_short > 1536) {
             hipLaunchKernelGGL(HIP_KERNEL_NAME(trace_group_kernel<8, 256, 1536>), dim3(R),
                                dim3(256), 0, st, a);
             if ((e = hipGetLastError()) != hipSuccess)
                 return e;
         }
-        if (lds_cap > 1024) {
+        if (max_short > 1024) {
             hipLaunchKernelGGL(HIP_KERNEL_NAME(trace_group_kernel<8, 192, 1024>), dim3(R),
                                dim3(192), 0, st, a);
             if ((e = hipGetLastError()) != hipSuccess)
                 return e;
         }
-        if (lds_cap > kWaveSortMax) {
+        if (max_short > kWaveSortMax) {
             hipLaunchKernelGGL(HIP_KERNEL_NAME(trace_group_kernel<8, 128, kWaveSortMax>),
                                dim3(R), dim3(128), 0, st, a);
             if ((e = hipGetLastError()) != hipSuccess)
