@@ -184,16 +184,15 @@ __device__ __forceinline__ void lane_stage(uint64_t (&k)[E], uint32_t size, uint
 // thread runs in registers, one whose partner is in the same wave by cross-lane moves (lane ^
 // stride / E), and only those whose partner is in another wave go through LDS, in a layout
 // (slot e of thread t at e * NT + t) where a wave's 64 accesses are consecutive; two LDS
-// buffers alternate, so each such exchange needs one barrier (buf holds 2 P keys), or, with
-// OneBuf, one buffer of P keys is reused behind a second barrier.
-template <int E, int NT = kThreads, bool OneBuf = false>
+// buffers alternate, so each such exchange needs one barrier.  buf holds 2 P keys.
+template <int E, int NT = kThreads>
 __device__ __forceinline__ void bitonic_sort_regs(uint64_t (&k)[E], uint64_t *buf, uint32_t P,
                                                   uint32_t t)
 {
     uint32_t flip = 0;
     for (uint32_t size = 2; size <= P; size <<= 1) {
         for (uint32_t stride = size >> 1; stride >= (uint32_t)E * 64; stride >>= 1) {
-            uint64_t *b = OneBuf ? buf : buf + flip * P;
+            uint64_t *b = buf + flip * P;
             flip ^= 1u;
 #pragma unroll
             for (int e = 0; e < E; ++e)
@@ -204,8 +203,6 @@ __device__ __forceinline__ void bitonic_sort_regs(uint64_t (&k)[E], uint64_t *bu
 #pragma unroll
             for (int e = 0; e < E; ++e)
                 k[e] = keep_one(k[e], b[e * NT + pt], km);
-            if (OneBuf)
-                __syncthreads();                       // read before the next stage writes
         }
         lane_stage<E, 32>(k, size, t);
         lane_stage<E, 16>(k, size, t);
@@ -976,12 +973,11 @@ __global__ void __launch_bounds__(64 * kWaveSortWaves) trace_wave_kernel(StatsAr
         wave_trace<8>(a, r, lo, n, lane, sum);
 }
 
-// Every trace of P / 2 + 1 to P = NT E calls sorted directly (8 keys per thread: 513 to 1,024
-// calls on two waves, 1,025 to 2,048 on four): one workgroup of NT threads per trace, keyed and
-// handed on as in trace_wave_kernel.  Exchanges whose partners lie in different waves (strides
-// of 64 E and more) go through one LDS buffer of P keys, reused behind a second barrier.  8 keys
-// per thread keep about 50 VGPRs; 16 or 32 keys per lane needed 89 and 171 (2 to 5 waves per
-// SIMD instead of 8).
+// Every trace of LO + 1 to NT E calls sorted directly (8 keys per thread: 513 to 1,024 calls on
+// two waves, 1,025 to 1,536 on three, 1,537 to 2,048 on four): one workgroup of NT threads per
+// trace, keyed and handed on as in trace_wave_kernel, sorted by mirror_sort_regs (exchanges
+// between waves through one LDS buffer of NT E keys).  8 keys per thread keep about 50 VGPRs;
+// 16 or 32 keys per lane needed 89 and 171 (2 to 5 waves per SIMD instead of 8).
 template <int E, int NT, int LO>
 __global__ void __launch_bounds__(NT) trace_group_kernel(StatsArgs a)
 {
