@@ -105,6 +105,9 @@ def test_malformed_input_is_rejected(ctx):
         (alp.ALP_EINVAL, 2, _pack([[(0, 5, 4)]])),                     # ends before it starts
         (alp.ALP_ERANGE, 2, _pack([[(0, 0, 1 << 32)]])),               # duration of 2^32 us
         (alp.ALP_ERANGE, 2, _pack([[(0, 1 << 60, (1 << 60) + 1)]])),   # start beyond 2^60 us
+        # a trace of 2^24 + 1 calls (rejected from the offsets alone; the call arrays are not read)
+        (alp.ALP_ERANGE, 2, (np.asarray([0, (1 << 24) + 1], np.uint64), np.zeros(1, np.uint32),
+                             np.zeros(1, np.uint64), np.ones(1, np.uint64))),
     ]
     for status, M, arrays in cases:
         with pytest.raises(alp.AlpError) as e:
@@ -119,6 +122,24 @@ def test_malformed_input_is_rejected(ctx):
         ctx.compute(9, off, llm, s, e_)
     # the context still works after rejected calls
     _same(ctx, 1, off, llm, s, e_)
+
+
+def test_trace_of_the_maximum_length(ctx):
+    """One trace of 2^24 calls (the most a trace may hold; the long-trace pass sorts it in a
+    global scratch region), in random order, between short traces."""
+    rng = np.random.default_rng(41)
+    n = 1 << 24
+    m = rng.integers(0, 3, n).astype(np.uint32)
+    s = np.uint64(1 << 35) + rng.integers(0, 1 << 30, n).astype(np.uint64)
+    e = s + rng.integers(0, 100_000, n).astype(np.uint64)
+    offsets = np.asarray([0, 3, 3 + n, 3 + n + 5], np.uint64)
+    llm = np.concatenate([np.zeros(3, np.uint32), m, np.ones(5, np.uint32)])
+    start = np.concatenate([np.asarray([1, 2, 3], np.uint64), s,
+                            np.asarray([9, 8, 7, 6, 5], np.uint64)])
+    end = np.concatenate([np.asarray([4, 5, 6], np.uint64), e,
+                          np.asarray([19, 18, 17, 16, 15], np.uint64)])
+    print(f"trace of {n} calls", flush=True)
+    _same(ctx, 3, offsets, llm, start, end)
 
 
 def test_every_sort_size_and_input_order(ctx):
