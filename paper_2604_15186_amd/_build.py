@@ -53,7 +53,8 @@ def build(extra_flags=(), out: str = LIB) -> str:
             for f in [pool.submit(_run, c) for c in cmds]:
                 f.result()
         tmp_lib = out + ".tmp"
-        _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp_lib])
+        _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp_lib,
+              "-L/opt/rocm/lib", "-lrocprofiler-sdk-roctx"])
         os.replace(tmp_lib, out)
     return out
 

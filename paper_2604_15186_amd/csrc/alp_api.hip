@@ -15,8 +15,21 @@
 #include <new>
 #include <vector>
 
+#include <rocprofiler-sdk-roctx/roctx.h>
+
 #include "alp.h"
 #include "alp_internal.h"
+
+namespace {
+// Names the dispatches that follow for a tracer (rocprofv3 --marker-trace shows the range around
+// the kernels it covers); with no tracer attached both calls return at once.
+struct Marked {
+    explicit Marked(const char *what) { roctxRangePushA(what); }
+    ~Marked() { roctxRangePop(); }
+    Marked(const Marked &) = delete;
+    Marked &operator=(const Marked &) = delete;
+};
+}  // namespace
 
 using alp::kCapacityMax;
 
@@ -665,6 +678,7 @@ int32_t launch_search_with(alp_ctx *c, const alp::QueryDev &q, uint32_t count, a
     hipError_t e;
     c->last_terms = !g.fused;
     if (g.fused) {
+        Marked mark("alp search: one-launch scan and finish");
         alp::FinishArgs fa{};
         fa.sp = sp;
         fa.out = out;
@@ -700,6 +714,7 @@ int32_t launch_search_with(alp_ctx *c, const alp::QueryDev &q, uint32_t count, a
     reset.best = s.best;
     reset.winners = s.winners;
     reset.n_winners = nwin;
+    Marked mark("alp search: option terms, scan and finish");
     if ((e = alp::launch_option_terms(sp, c->tdev, q, count, s.rec, s.ext, s.inner, reset,
                                       c->stream, raw, timed ? ev[0] : nullptr,
                                       timed ? ev[1] : nullptr)) != hipSuccess)
@@ -1128,6 +1143,7 @@ int32_t alp_max_throughput(alp_ctx *ctx, uint32_t count, const uint32_t *instanc
     if ((e = ctx->tmax.ensure(bytes)) != hipSuccess || (e = ctx->rec.ensure(items_bytes)) != hipSuccess ||
         (e = ctx->ext.ensure(items_bytes)) != hipSuccess)
         return hip_fail(e, "hipMalloc(max_throughput)");
+    Marked mark("alp max_throughput: option terms and reduction");
     if ((e = alp::launch_option_terms(ctx->sp, ctx->tdev, q, count, (uint2 *)ctx->rec.ptr,
                                       (uint2 *)ctx->ext.ptr, nullptr, alp::ScanReset{}, ctx->stream)) !=
         hipSuccess)
@@ -1200,6 +1216,7 @@ int32_t alp_allocate_workflows(alp_ctx *ctx, uint32_t count, const uint32_t *ins
     uint32_t *dgpus = ctx->host_split_dev + 8;
     if (ctx->timing && (e = hipEventRecord(ctx->ev[2], ctx->stream)) != hipSuccess)
         return hip_fail(e, "hipEventRecord");
+    Marked mark("alp allocate");
     if ((e = alp::launch_allocate(ctx->host_results_dev, count, total_gpus, policy,
                                   (uint64_t *)ctx->split_dp.ptr, dplan, dgpus, ctx->stream)) != hipSuccess)
         return hip_fail(e, "allocate launch");
@@ -1329,6 +1346,7 @@ int32_t alp_search_pruned(alp_ctx *ctx, uint32_t count, const uint32_t *instance
         return hip_fail(e, "hipEventRecord");
     alp::ScanReset reset;
     reset.done = done;                       // the pruned scan publishes every block's winner
+    Marked mark("alp pruned search: option terms, table and scan");
     if ((e = alp::launch_option_terms(sp, ctx->tdev, q, count, rec, ext, (uint2 *)ctx->inner.ptr,
                                       reset, ctx->stream)) != hipSuccess)
         return hip_fail(e, "option_terms launch");
@@ -1422,6 +1440,7 @@ int32_t alp_place(alp_ctx *ctx, uint32_t count, const alp_result_t *allocations,
         return hip_fail(e, "copy allocations");
     if (ctx->timing && (e = hipEventRecord(ctx->ev[1], ctx->stream)) != hipSuccess)
         return hip_fail(e, "hipEventRecord");
+    Marked mark("alp place");
     if ((e = alp::launch_place(sp.units_per_gpu, small, count - small,
                                (const alp::PlaceIn *)ctx->place_in.ptr,
                                (alp_placement_t *)ctx->place_out.ptr, ctx->stream)) != hipSuccess)
@@ -1476,6 +1495,7 @@ int32_t alp_eval_candidates(alp_ctx *ctx, uint32_t instance, uint32_t gpu_budget
     if ((e = hipMemcpyAsync(ctx->idx.ptr, indices, count * sizeof(uint64_t), hipMemcpyHostToDevice,
                             ctx->stream)) != hipSuccess)
         return hip_fail(e, "copy indices");
+    Marked mark("alp evaluate");
     if ((e = alp::launch_option_terms(ctx->sp, ctx->tdev, q, 1, (uint2 *)ctx->rec.ptr,
                                       (uint2 *)ctx->ext.ptr, nullptr, alp::ScanReset{}, ctx->stream)) !=
         hipSuccess)
@@ -1736,6 +1756,7 @@ int32_t alp_trace_stats(alp_stats_ctx *c, uint32_t num_llms, uint32_t num_traces
         return hip_fail(e, "hipEventRecord");
     const bool zero_first = !c->counters_clean;
     c->counters_clean = false;                       // until the kernels have run to the end
+    Marked mark("alp trace statistics");
     if ((e = alp::launch_trace_stats(num_llms, num_traces, offsets, llm, start_us, end_us, lds_cap,
                                      (uint32_t)max_short, (uint32_t)longs.size(), (const uint32_t *)c->long_list.ptr,
                                      (const uint64_t *)c->long_base.ptr, (uint64_t *)c->scratch.ptr,
