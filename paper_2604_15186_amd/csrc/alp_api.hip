@@ -678,7 +678,6 @@ int32_t launch_search_with(alp_ctx *c, const alp::QueryDev &q, uint32_t count, a
     hipError_t e;
     c->last_terms = !g.fused;
     if (g.fused) {
-        Marked mark("alp search: one-launch scan and finish");
         alp::FinishArgs fa{};
         fa.sp = sp;
         fa.out = out;
@@ -714,7 +713,6 @@ int32_t launch_search_with(alp_ctx *c, const alp::QueryDev &q, uint32_t count, a
     reset.best = s.best;
     reset.winners = s.winners;
     reset.n_winners = nwin;
-    Marked mark("alp search: option terms, scan and finish");
     if ((e = alp::launch_option_terms(sp, c->tdev, q, count, s.rec, s.ext, s.inner, reset,
                                       c->stream, raw, timed ? ev[0] : nullptr,
                                       timed ? ev[1] : nullptr)) != hipSuccess)
@@ -745,6 +743,10 @@ int32_t launch_search(alp_ctx *c, const alp::QueryDev &q, uint32_t count, alp_re
     SearchScratch s;
     if ((st = context_scratch(c, count, g, s)) != ALP_OK)
         return st;
+    // The range stays out of launch_search_with itself: the entry point that must not allocate
+    // calls it too, and a tracer may allocate host memory to record a range.
+    Marked mark(g.fused ? "alp search: one-launch scan and finish"
+                        : "alp search: option terms, scan and finish");
     return launch_search_with(c, q, count, out, raw, ev, g, s, signal, seq);
 }
 
