@@ -374,7 +374,7 @@ int32_t alp_eval_candidates(alp_ctx *ctx, uint32_t instance, uint32_t gpu_budget
  * between the two; rows can only be split with the second, so variant 4 ignores inner_chunks),
  * 6 row-minimum scan over the pair table (LLMs M-3 and M-2 folded into one inner LLM of O^2
  * options, 3 or more LLMs; variant 0 uses it for 5 or more LLMs while the batch's pair tables
- * stay within 4 MiB).  Spaces of fewer than 2^32 candidates searched with the row-minimum scan
+ * stay within 4 MiB).  Spaces of at most 2^25 candidates searched with the row-minimum scan
  * without the pair table run in one launch: every block computes its item's option terms itself
  * (unless ALP_LAUNCH_SEPARATE_TERMS is added).  blocks_per_item and threads_per_block (a multiple
  * of 64, at most 1024):

@@ -358,6 +358,9 @@ uint64_t blocks_per_item_for_rounds(uint64_t count, uint64_t resident, uint64_t 
 // fixed-range form counts a wave's rows in 32 bits, so a wave must get fewer than 2^32 rows
 // (the automatic plan adds blocks until it does; a blocks_per_item override that leaves a wave
 // more is rejected), and a launch holds fewer than 2^31 blocks.
+// Largest space (candidates per item) searched in one launch.
+constexpr uint64_t kFusedCandidatesMax = UINT64_C(1) << 25;
+
 int32_t plan_scan(alp_ctx *c, uint32_t count, alp::ScanGeometry &out, bool allow_fused = true)
 {
     alp::ScanGeometry g{};
@@ -490,12 +493,16 @@ int32_t plan_scan(alp_ctx *c, uint32_t count, alp::ScanGeometry &out, bool allow
             return fail(ALP_ERANGE, "batch too large for one launch (%llu blocks)",
                         (unsigned long long)(bpi * std::max<uint64_t>(1, count)));
         g.blocks_per_item = (uint32_t)bpi;
-        // One launch for spaces of fewer than 2^32 candidates (the winner fits one 64-bit word),
-        // unless the option terms are asked to run in their own kernel.
+        // One launch for spaces of at most 2^25 candidates (the winner fits one 64-bit word in
+        // any space below 2^32), unless the option terms are asked to run in their own kernel.
+        // Larger spaces take the two-launch form: every block of the one-launch scan repeats the
+        // item's option terms (a prologue of about 2.7 us), which a long scan pays for more
+        // than it saves the option-term kernel (a 4-LLM search of 2^28 candidates: 29.3 us per
+        // step in two launches, 30.7 in one; a 3-LLM search of 2^21: 11.9 in two, 9.3 in one).
         // The block keeps the item's curves and records in LDS: at most 56 KiB of them, with
         // the kernel's own few KiB within 64 KiB (every space of fewer than 2^32 candidates
         // fits; the test only guards the layout).
-        g.fused = g.variant == 1 && allow_fused && c->N < (UINT64_C(1) << 32) &&
+        g.fused = g.variant == 1 && allow_fused && c->N <= kFusedCandidatesMax &&
                   alp::fused_lds_bytes(sp) <= (UINT64_C(56) << 10) &&
                   !(c->variant & ALP_LAUNCH_SEPARATE_TERMS) ? 1u : 0u;
     } else {

@@ -86,7 +86,7 @@ CASES = load_cases()
 # row-minimum with fixed per-wave rows, row-minimum with rows handed out within each block,
 # row-minimum over the pair table of LLMs M-3 and M-2 (3 or more LLMs; otherwise automatic).
 SEP = 16                       # ALP_LAUNCH_SEPARATE_TERMS: option terms in their own kernel
-# Spaces below 2^32 candidates run the row-minimum scan in one launch; SEP variants keep the
+# Spaces of at most 2^25 candidates run the row-minimum scan in one launch; SEP variants keep the
 # two-launch form of each work distribution.
 VARIANTS = (1, 2, 3, 4, 5, 6, 1 | SEP, 4 | SEP, 5 | SEP)
 
